@@ -1,0 +1,201 @@
+"""fp64 CPU oracle for the BOM per-step hot path -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's ``cpu_baseline`` leg may
+import this package. It shares no code with the GPU library (``paper_2609_36738_amd``) and
+never imports it. The arithmetic lives in ``bom_oracle.c`` (plain loops, fp64); this module
+builds it with gcc, marshals numpy arrays, and strings the steps of Algorithm 1 together in
+the paper's order for the multi-step loop.
+
+Every function takes the exact fp64 images of the inputs (bf16 and fp32 widen exactly).
+Pins: every function here is checked by ``tests/test_oracle_pins.py`` against what the paper
+and the mathematics fix (closed forms, brute-force Jacobians, finite differences, explicit
+EMA sums, Lemma 2, the linear-model equivalence of BOM and the own-step control, and the
+Adafactor rank-1 identity for the factored second moment, whose definition is a reading).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "bom_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+FLAG_LABEL_RANGE = 1
+FLAG_EMPTY = 2
+
+
+def build() -> str:
+    cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+    subprocess.check_call(cmd)
+    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(_LIB_PATH):
+            build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        i64, i32, f64, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_double, ctypes.c_void_p
+        lib.orc_residual.argtypes = [vp, i64, i64, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+        lib.orc_ema.argtypes = [vp, vp, i64, f64, i64, vp]
+        lib.orc_dW_cols.argtypes = [vp, i64, i64, vp, i64, vp, i32, vp, vp, i64, f64, vp, i64, vp]
+        lib.orc_dH_rows.argtypes = [vp, i64, vp, i64, vp, i32, vp, vp, i64, f64, vp, i64, vp]
+        lib.orc_db.argtypes = [vp, i64, i64, vp, i32, vp, vp, i64, f64, vp]
+        lib.orc_update_dense.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp, ctypes.c_int, f64, f64, f64, f64, f64,
+                                         f64, i64]
+        lib.orc_update_factored.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp, vp, vp, ctypes.c_int, f64, f64,
+                                            f64, f64, f64, f64, i64]
+        lib.orc_head_forward.argtypes = [vp, i64, i64, vp, i64, vp, vp]
+        _lib = lib
+        return lib
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data
+
+
+def residual(Z, labels, ignore_index: int = -100, want_R: bool = True) -> dict:
+    """Row statistics, residual rows, batch-mean residual s, mean CE, N_t and flags."""
+    Z = _f64(Z)
+    labels = _i32(labels)
+    N, V = Z.shape
+    out = dict(s=np.zeros(V), row_lse=np.zeros(N), row_argmax=np.zeros(N, np.int32),
+               row_target=np.zeros(N), R=np.zeros((N, V)) if want_R else None)
+    loss = np.zeros(1)
+    nv = np.zeros(1, np.int32)
+    fl = np.zeros(1, np.int32)
+    _load().orc_residual(_p(Z), N, V, _p(labels), ignore_index, _p(out["s"]), _p(out["row_lse"]),
+                         _p(out["row_argmax"]), _p(out["row_target"]), _p(out["R"]), _p(loss), _p(nv), _p(fl))
+    out.update(loss=float(loss[0]), n_valid=int(nv[0]), flags=int(fl[0]))
+    return out
+
+
+def ema(q, s, beta1: float, t: int):
+    """Returns (q_new, q_hat); the input q is not modified."""
+    q = _f64(q).copy()
+    s = _f64(s)
+    qh = np.zeros_like(q)
+    _load().orc_ema(_p(q), _p(s), q.size, float(beta1), int(t), _p(qh))
+    return q, qh
+
+
+def dW_cols(H, Z, labels, row_lse, q_hat, n_valid: int, lam: float, cols=None, ignore_index: int = -100):
+    H, Z, labels, row_lse, q_hat = _f64(H), _f64(Z), _i32(labels), _f64(row_lse), _f64(q_hat)
+    N, d = H.shape
+    V = Z.shape[1]
+    cols = np.arange(V, dtype=np.int64) if cols is None else np.ascontiguousarray(cols, dtype=np.int64)
+    out = np.zeros((d, cols.size))
+    _load().orc_dW_cols(_p(H), N, d, _p(Z), V, _p(labels), ignore_index, _p(row_lse), _p(q_hat), n_valid,
+                        float(lam), _p(cols), cols.size, _p(out))
+    return out
+
+
+def dH_rows(W, Z, labels, row_lse, q_hat, n_valid: int, lam: float, rows=None, ignore_index: int = -100):
+    W, Z, labels, row_lse, q_hat = _f64(W), _f64(Z), _i32(labels), _f64(row_lse), _f64(q_hat)
+    d, V = W.shape
+    N = Z.shape[0]
+    rows = np.arange(N, dtype=np.int64) if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.zeros((rows.size, d))
+    _load().orc_dH_rows(_p(W), d, _p(Z), V, _p(labels), ignore_index, _p(row_lse), _p(q_hat), n_valid,
+                        float(lam), _p(rows), rows.size, _p(out))
+    return out
+
+
+def db(Z, labels, row_lse, q_hat, n_valid: int, lam: float, ignore_index: int = -100):
+    Z, labels, row_lse, q_hat = _f64(Z), _i32(labels), _f64(row_lse), _f64(q_hat)
+    N, V = Z.shape
+    out = np.zeros(V)
+    _load().orc_db(_p(Z), N, V, _p(labels), ignore_index, _p(row_lse), _p(q_hat), n_valid, float(lam), _p(out))
+    return out
+
+
+def _segs(segments):
+    segments = list(segments or [])
+    off = np.array([s[0] for s in segments] or [0], np.int64)
+    ln = np.array([s[1] for s in segments] or [0], np.int64)
+    wd = np.array([s[2] for s in segments] or [0.0], np.float64)
+    return off, ln, wd, len(segments)
+
+
+def update_dense(theta, v, u, *, lr, beta2, eps, t, segments=None, weight_decay=0.0, h=None, lam=0.5,
+                 u_scale=1.0):
+    """Returns (theta_new, v_new) in fp64; inputs are not modified."""
+    theta, v, u = _f64(theta).copy(), _f64(v).copy(), _f64(u)
+    h = None if h is None else _f64(h)
+    off, ln, wd, ns = _segs(segments)
+    _load().orc_update_dense(_p(theta), _p(v), _p(u), _p(h), theta.size, _p(off), _p(ln), _p(wd), ns,
+                             float(weight_decay), float(lr), float(beta2), float(eps), float(lam), float(u_scale),
+                             int(t))
+    return theta, v
+
+
+def update_factored(theta, Rr, Cc, u, *, lr, beta2, eps, t, block_rows, block_cols, segments=None,
+                    weight_decay=0.0, h=None, lam=0.5, u_scale=1.0):
+    """Returns (theta_new, Rr_new, Cc_new) in fp64; inputs are not modified."""
+    theta, Rr, Cc, u = _f64(theta).copy(), _f64(Rr).copy(), _f64(Cc).copy(), _f64(u)
+    h = None if h is None else _f64(h)
+    P = theta.size
+    nrows = -(-P // block_cols)
+    nblocks = -(-nrows // block_rows)
+    assert Rr.size == nrows and Cc.size == nblocks * block_cols, "factored state shape"
+    off, ln, wd, ns = _segs(segments)
+    _load().orc_update_factored(_p(theta), _p(Rr), _p(Cc), _p(u), _p(h), P, block_rows, block_cols, _p(off), _p(ln),
+                                _p(wd), ns, float(weight_decay), float(lr), float(beta2), float(eps), float(lam),
+                                float(u_scale), int(t))
+    return theta, Rr, Cc
+
+
+def head_forward(H, W, b=None):
+    H, W = _f64(H), _f64(W)
+    b = None if b is None else _f64(b)
+    N, d = H.shape
+    V = W.shape[1]
+    Z = np.zeros((N, V))
+    _load().orc_head_forward(_p(H), N, d, _p(W), V, _p(b), _p(Z))
+    return Z
+
+
+def bom_step_linear_head(H, labels, theta, v, q, t, *, d, V, lr, lam, beta1, beta2, eps, segments,
+                         weight_decay=0.0, ignore_index=-100):
+    """One full step of Algorithm 1 for a linear softmax head whose flat parameters are
+    theta = [W (d x V, row-major), b (V)]: forward, s, q / q_hat, the mixed-objective gradient
+    u = [dW, db], then the second moment and the update. Returns a dict with every stage."""
+    W = theta[: d * V].reshape(d, V)
+    b = theta[d * V: d * V + V]
+    Z = head_forward(H, W, b)
+    res = residual(Z, labels, ignore_index, want_R=False)
+    q_new, q_hat = ema(q, res["s"], beta1, t)
+    dW = dW_cols(H, Z, labels, res["row_lse"], q_hat, res["n_valid"], lam, ignore_index=ignore_index)
+    dbias = db(Z, labels, res["row_lse"], q_hat, res["n_valid"], lam, ignore_index=ignore_index)
+    u = np.concatenate([dW.reshape(-1), dbias])
+    theta_new, v_new = update_dense(theta, v, u, lr=lr, beta2=beta2, eps=eps, t=t, segments=segments,
+                                    weight_decay=weight_decay)
+    return dict(Z=Z, res=res, q=q_new, q_hat=q_hat, u=u, theta=theta_new, v=v_new)
+
+
+def state_bytes(P: int, V: int, optimizer: str, bytes_per=4) -> int:
+    """Parameter-shaped optimizer state in bytes: AdamW keeps m and v; BOM keeps v plus one V-vector."""
+    if optimizer == "adamw":
+        return 2 * P * bytes_per
+    if optimizer == "bom":
+        return P * bytes_per + V * bytes_per
+    raise ValueError(optimizer)

@@ -1,0 +1,499 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix (CPU only).
+
+Each test checks the oracle against something other than itself: library routines
+(scipy's softmax / logsumexp), brute-force per-example Jacobians, finite differences,
+closed forms, explicit EMA sums, Lemma 2, numbers the paper prints (tests/golden), and
+the linear-model equivalence of BOM and the own-step control.
+"""
+import math
+
+import numpy as np
+import pytest
+from scipy.special import log_softmax, logsumexp, softmax
+
+import oracle
+from conftest import read_golden
+
+LAM, B1, B2, EPS = 0.5, 0.9, 0.999, 1e-8
+
+
+def _rng(seed=0):
+    return np.random.default_rng(seed)
+
+
+def _head_problem(N=4, d=3, V=5, seed=0, scale=1.0):
+    r = _rng(seed)
+    H = r.standard_normal((N, d))
+    W = r.standard_normal((d, V)) * 0.5 * scale
+    b = r.standard_normal(V) * 0.1
+    y = r.integers(0, V, N).astype(np.int32)
+    return H, W, b, y
+
+
+# ----------------------------------------------------------------------------- residual
+
+def test_residual_matches_library_softmax():
+    r = _rng(1)
+    Z = r.standard_normal((37, 23)) * 3
+    y = r.integers(0, 23, 37).astype(np.int32)
+    out = oracle.residual(Z, y)
+    P = softmax(Z, axis=1)
+    Y = np.eye(23)[y]
+    np.testing.assert_allclose(out["row_lse"], logsumexp(Z, axis=1), rtol=1e-14, atol=1e-14)
+    np.testing.assert_allclose(out["R"], P - Y, atol=1e-14)
+    np.testing.assert_allclose(out["s"], (P - Y).mean(0), atol=1e-15)
+    np.testing.assert_allclose(out["loss"], -log_softmax(Z, axis=1)[np.arange(37), y].mean(), rtol=1e-14)
+    assert (out["row_argmax"] == Z.argmax(1)).all()
+    assert (out["row_target"] == Z[np.arange(37), y]).all()
+    assert out["n_valid"] == 37 and out["flags"] == 0
+
+
+def test_residual_rows_and_s_sum_to_zero():
+    # Sec. 3.1: every softmax residual has zero coordinate sum, hence so do s and q.
+    r = _rng(2)
+    Z = r.standard_normal((50, 31)) * 5
+    y = r.integers(0, 31, 50).astype(np.int32)
+    out = oracle.residual(Z, y)
+    assert np.abs(out["R"].sum(1)).max() < 1e-14
+    assert abs(out["s"].sum()) < 1e-15
+    q = np.zeros(31)
+    for t in range(1, 6):
+        q, qh = oracle.ema(q, out["s"] * t, B1, t)
+        assert abs(q.sum()) < 1e-14 and abs(qh.sum()) < 1e-14
+
+
+def test_uniform_logits_closed_form():
+    # z_ij = c: p = 1/V, CE = ln V, lse = c + ln V, s_j = 1/V - count_j / N_t, argmax = 0.
+    N, V, c = 40, 7, 0.375
+    y = _rng(3).integers(0, V, N).astype(np.int32)
+    out = oracle.residual(np.full((N, V), c), y)
+    cnt = np.bincount(y, minlength=V)
+    np.testing.assert_allclose(out["s"], 1.0 / V - cnt / N, atol=1e-15)
+    assert abs(out["loss"] - math.log(V)) < 1e-14
+    np.testing.assert_allclose(out["row_lse"], c + math.log(V), rtol=1e-15)
+    assert (out["row_argmax"] == 0).all()
+
+
+def test_residual_is_gradient_of_mean_ce():
+    # Finite differences: d(mean CE)/dz_ij = r_ij / N_t (central differences, fp64).
+    r = _rng(4)
+    N, V = 6, 9
+    Z = r.standard_normal((N, V)) * 2
+    y = r.integers(0, V, N).astype(np.int32)
+    y[2] = -100
+    out = oracle.residual(Z, y)
+    h = 1e-6
+    for i in range(N):
+        for j in range(V):
+            Zp, Zm = Z.copy(), Z.copy()
+            Zp[i, j] += h
+            Zm[i, j] -= h
+            fd = (oracle.residual(Zp, y, want_R=False)["loss"] - oracle.residual(Zm, y, want_R=False)["loss"]) / (2 * h)
+            assert abs(fd - out["R"][i, j] / out["n_valid"]) < 1e-8
+
+
+def test_argmax_ties_take_lowest_index():
+    Z = np.array([[1.0, 3.0, 3.0, 0.0], [2.0, 2.0, 2.0, 2.0], [-1.0, -5.0, -1.0, -1.0]])
+    out = oracle.residual(Z, np.array([0, 1, 2], np.int32))
+    assert list(out["row_argmax"]) == [1, 0, 0]
+
+
+def test_ignored_and_out_of_range_labels():
+    r = _rng(5)
+    N, V = 20, 6
+    Z = r.standard_normal((N, V))
+    y = r.integers(0, V, N).astype(np.int32)
+    y[[1, 7]] = -100
+    y[4] = V          # out of range
+    y[9] = -3         # out of range
+    out = oracle.residual(Z, y)
+    keep = np.array([i not in (1, 7, 4, 9) for i in range(N)])
+    P = softmax(Z[keep], axis=1)
+    Y = np.eye(V)[y[keep]]
+    np.testing.assert_allclose(out["s"], (P - Y).mean(0), atol=1e-15)
+    assert out["n_valid"] == keep.sum()
+    assert out["flags"] == oracle.FLAG_LABEL_RANGE
+    assert (out["R"][~keep] == 0).all() and (out["row_target"][~keep] == 0).all()
+    np.testing.assert_allclose(out["row_lse"], logsumexp(Z, axis=1), rtol=1e-14)
+
+
+def test_all_rows_ignored_is_empty():
+    Z = _rng(6).standard_normal((5, 4))
+    y = np.full(5, -100, np.int32)
+    out = oracle.residual(Z, y)
+    assert out["flags"] == oracle.FLAG_EMPTY and out["n_valid"] == 0
+    assert (out["s"] == 0).all() and out["loss"] == 0
+    H = _rng(7).standard_normal((5, 3))
+    qh = _rng(8).standard_normal(4)
+    assert (oracle.dW_cols(H, Z, y, out["row_lse"], qh, 0, LAM) == 0).all()
+    assert (oracle.db(Z, y, out["row_lse"], qh, 0, LAM) == 0).all()
+    assert (oracle.dH_rows(_rng(9).standard_normal((3, 4)), Z, y, out["row_lse"], qh, 0, LAM) == 0).all()
+
+
+# ----------------------------------------------------------------------------- EMA
+
+def test_ema_explicit_sum_and_lemma2():
+    # q_t = sum_tau w_{t,tau} s_tau with w = (1-b1) b1^(t-tau) (Sec. 3 notation); Lemma 2:
+    # normalised weights sum to 1 and ||q_hat_t - s_t|| <= sum alpha_{t,tau} ||s_tau - s_t||.
+    r = _rng(10)
+    V, T = 11, 25
+    S = r.standard_normal((T, V))
+    q = np.zeros(V)
+    for t in range(1, T + 1):
+        q, qh = oracle.ema(q, S[t - 1], B1, t)
+        w = np.array([(1 - B1) * B1 ** (t - tau) for tau in range(1, t + 1)])
+        np.testing.assert_allclose(q, w @ S[:t], atol=1e-14)
+        alpha = w / (1 - B1 ** t)
+        assert abs(alpha.sum() - 1) < 1e-14
+        np.testing.assert_allclose(qh, alpha @ S[:t], atol=1e-14)
+        bound = sum(alpha[k] * np.linalg.norm(S[k] - S[t - 1]) for k in range(t))
+        assert np.linalg.norm(qh - S[t - 1]) <= bound + 1e-12
+
+
+def test_ema_constant_signal_and_beta_zero():
+    s = _rng(11).standard_normal(8)
+    q = np.zeros(8)
+    for t in range(1, 12):
+        q, qh = oracle.ema(q, s, B1, t)
+        np.testing.assert_allclose(qh, s, rtol=1e-13)
+    q = _rng(12).standard_normal(8)
+    _, qh = oracle.ema(q, s, 0.0, 5)
+    assert (qh == s).all()
+
+
+def test_binary_history_is_one_scalar():
+    # Sec. 3.1: V = 2 gives q_t = (a_t, -a_t).
+    r = _rng(13)
+    q = np.zeros(2)
+    for t in range(1, 8):
+        Z = r.standard_normal((16, 2)) * 2
+        y = r.integers(0, 2, 16).astype(np.int32)
+        s = oracle.residual(Z, y)["s"]
+        q, qh = oracle.ema(q, s, B1, t)
+        assert abs(q[0] + q[1]) < 1e-16 and abs(qh[0] + qh[1]) < 1e-15
+
+
+# ----------------------------------------------------------------------------- head VJP
+
+def _jacobians(H, W, b):
+    """Brute-force per-example Jacobians of z_i = W^T h_i + b with respect to theta = (W, b, H),
+    by central differences of numpy's forward map (exact for a linear map up to rounding)."""
+    N, d = H.shape
+    V = W.shape[1]
+    theta = np.concatenate([W.ravel(), b, H.ravel()])
+
+    def fwd(th):
+        Wt = th[: d * V].reshape(d, V)
+        bt = th[d * V: d * V + V]
+        Ht = th[d * V + V:].reshape(N, d)
+        return Ht @ Wt + bt
+
+    J = np.zeros((N, V, theta.size))
+    h = 1e-3
+    for p in range(theta.size):
+        tp, tm = theta.copy(), theta.copy()
+        tp[p] += h
+        tm[p] -= h
+        J[:, :, p] = (fwd(tp) - fwd(tm)) / (2 * h)
+    return J
+
+
+def _oracle_u(H, W, b, y, q_hat, lam):
+    Z = H @ W + b
+    res = oracle.residual(Z, y)
+    nv = res["n_valid"]
+    dW = oracle.dW_cols(H, Z, y, res["row_lse"], q_hat, nv, lam)
+    dbias = oracle.db(Z, y, res["row_lse"], q_hat, nv, lam)
+    dH = oracle.dH_rows(W, Z, y, res["row_lse"], q_hat, nv, lam)
+    return np.concatenate([dW.ravel(), dbias, dH.ravel()]), res
+
+
+def test_batch_decomposition_brute_force():
+    # Eq. (1): g = Jbar^T s + c with c = mean (J_i - Jbar)^T (r_i - s); and Eq. (4):
+    # u = (1 - lam) g + lam Jbar^T q_hat, from per-example Jacobians built by brute force.
+    H, W, b, y = _head_problem(N=4, d=3, V=5, seed=14)
+    J = _jacobians(H, W, b)
+    q_hat = _rng(15).standard_normal(5) * 0.1
+    q_hat -= q_hat.mean()
+    g, res = _oracle_u(H, W, b, y, q_hat, 0.0)
+    Rm = res["R"]
+    s = res["s"]
+    Jbar = J.mean(0)
+    c = np.mean([(J[i] - Jbar).T @ (Rm[i] - s) for i in range(4)], axis=0)
+    g_bf = np.mean([J[i].T @ Rm[i] for i in range(4)], axis=0)
+    np.testing.assert_allclose(g, g_bf, atol=1e-9)
+    np.testing.assert_allclose(g, Jbar.T @ s + c, atol=1e-9)
+    u, _ = _oracle_u(H, W, b, y, q_hat, LAM)
+    np.testing.assert_allclose(u, (1 - LAM) * g + LAM * Jbar.T @ q_hat, atol=1e-9)
+
+
+def test_beta_zero_history_is_current_projection():
+    # beta1 = 0 gives q_hat = s, so the history term is h = Jbar^T s.
+    H, W, b, y = _head_problem(N=4, d=3, V=5, seed=16)
+    J = _jacobians(H, W, b)
+    res = oracle.residual(H @ W + b, y)
+    _, qh = oracle.ema(_rng(17).standard_normal(5), res["s"], 0.0, 3)
+    u1, _ = _oracle_u(H, W, b, y, qh, 1.0)
+    np.testing.assert_allclose(u1, J.mean(0).T @ res["s"], atol=1e-9)
+
+
+def test_head_vjp_finite_differences_of_mixed_objective():
+    # Eq. (3) with q_hat detached: L_mix = (1-lam) mean CE + (lam/N) sum <z_i, q_hat>.
+    H, W, b, y = _head_problem(N=6, d=4, V=7, seed=18)
+    y[3] = -100
+    q_hat = _rng(19).standard_normal(7) * 0.2
+    valid = y != -100
+
+    def lmix(Wt, bt, Ht):
+        Z = Ht @ Wt + bt
+        ls = log_softmax(Z[valid], axis=1)
+        ce = -ls[np.arange(valid.sum()), y[valid]].mean()
+        return (1 - LAM) * ce + LAM * (Z[valid] @ q_hat).mean()
+
+    u, _ = _oracle_u(H, W, b, y, q_hat, LAM)
+    fd = []
+    h = 1e-6
+    for arr_idx, shape in ((0, W.shape), (1, b.shape), (2, H.shape)):
+        for k in range(int(np.prod(shape))):
+            args_p = [W.copy(), b.copy(), H.copy()]
+            args_m = [W.copy(), b.copy(), H.copy()]
+            args_p[arr_idx].reshape(-1)[k] += h
+            args_m[arr_idx].reshape(-1)[k] -= h
+            fd.append((lmix(*args_p) - lmix(*args_m)) / (2 * h))
+    np.testing.assert_allclose(u, np.array(fd), atol=2e-8)
+
+
+def test_lambda_zero_is_textbook_softmax_ce_backward():
+    H, W, b, y = _head_problem(N=9, d=5, V=6, seed=20)
+    Z = H @ W + b
+    res = oracle.residual(Z, y)
+    qh = _rng(21).standard_normal(6)
+    dW = oracle.dW_cols(H, Z, y, res["row_lse"], qh, res["n_valid"], 0.0)
+    dH = oracle.dH_rows(W, Z, y, res["row_lse"], qh, res["n_valid"], 0.0)
+    G = (softmax(Z, axis=1) - np.eye(6)[y]) / 9
+    np.testing.assert_allclose(dW, H.T @ G, atol=1e-15)
+    np.testing.assert_allclose(dH, G @ W.T, atol=1e-15)
+
+
+def test_head_vjp_invariants_and_bias_identity():
+    # Bias Jacobian is the identity: db = (1 - lam) s + lam q_hat exactly; zero-sum residuals and a
+    # zero-sum q_hat make every dW row sum vanish and 1^T db = 0.
+    H, W, b, y = _head_problem(N=30, d=8, V=12, seed=22)
+    Z = H @ W + b
+    res = oracle.residual(Z, y)
+    q = np.zeros(12)
+    for t in range(1, 4):
+        q, qh = oracle.ema(q, res["s"] * (1 + 0.1 * t), B1, t)
+    dW = oracle.dW_cols(H, Z, y, res["row_lse"], qh, res["n_valid"], LAM)
+    dbias = oracle.db(Z, y, res["row_lse"], qh, res["n_valid"], LAM)
+    np.testing.assert_allclose(dbias, (1 - LAM) * res["s"] + LAM * qh, atol=1e-16)
+    assert np.abs(dW.sum(1)).max() < 1e-15
+    assert abs(dbias.sum()) < 1e-16
+    # linear-head closed form of the history term: Jbar^T q_hat = hbar q_hat^T for W
+    dW0 = oracle.dW_cols(H, Z, y, res["row_lse"], qh, res["n_valid"], 0.0)
+    np.testing.assert_allclose(dW - (1 - LAM) * dW0, LAM * np.outer(H.mean(0), qh), atol=1e-15)
+
+
+def test_binary_history_direction_is_mean_margin_gradient():
+    # Sec. 3.1: for V = 2, Jbar^T q_hat = a (grad of the batch-mean margin z_1 - z_2).
+    H, W, b, y = _head_problem(N=10, d=4, V=2, seed=23)
+    Z = H @ W + b
+    res = oracle.residual(Z, y)
+    _, qh = oracle.ema(np.zeros(2), res["s"], B1, 1)
+    dW1 = oracle.dW_cols(H, Z, y, res["row_lse"], qh, res["n_valid"], 1.0)
+    margin_grad_W = np.stack([H.mean(0), -H.mean(0)], axis=1)
+    np.testing.assert_allclose(dW1, qh[0] * margin_grad_W, atol=1e-15)
+
+
+def test_u_decomposition_bias_corrected_exact():
+    # Classifier-history appendix with Gamma = I: u = (1-lam) g + lam (1-b1)/(1-b1^t) Jbar^T s_t
+    #   + lam b1/(1-b1^t) Jbar^T q_{t-1}; and the printed 0.55 / 0.45 / 0.5 weights of Eq. (5).
+    gold = read_golden("temporal_kernel.txt")
+    lam, b1 = gold["lambda"], gold["beta1"]
+    H, W, b, y = _head_problem(N=5, d=3, V=4, seed=24)
+    J = _jacobians(H, W, b)
+    Jbar = J.mean(0)
+    q_prev = _rng(25).standard_normal(4) * 0.1
+    q_prev -= q_prev.mean()
+    for t in (2, 3, 7, 400):
+        g, res = _oracle_u(H, W, b, y, np.zeros(4), 0.0)
+        s = res["s"]
+        _, qh = oracle.ema(q_prev, s, b1, t)
+        u, _ = _oracle_u(H, W, b, y, qh, lam)
+        bc = 1 - b1 ** t
+        np.testing.assert_allclose(u, (1 - lam) * g + lam * (1 - b1) / bc * Jbar.T @ s
+                                   + lam * b1 / bc * Jbar.T @ q_prev, atol=1e-9)
+        if t == 400:  # bias correction negligible: Eq. (5) weights
+            Rm = res["R"]
+            c = np.mean([(J[i] - Jbar).T @ (Rm[i] - s) for i in range(5)], axis=0)
+            np.testing.assert_allclose(u, gold["current_weight"] * Jbar.T @ s + gold["covariance_weight"] * c
+                                       + gold["history_weight"] * Jbar.T @ q_prev, atol=1e-9)
+
+
+def test_temporal_kernel_matches_printed_coefficients():
+    # Full-kernel appendix: with the batch-mean signal of a fixed linear model, the coefficient of
+    # Jbar^T s_t is 0.5 + 0.05/(1 - 0.9^t) and of lag k is 0.05 0.9^k / (1 - 0.9^t).
+    gold = read_golden("temporal_kernel.txt")
+    r = _rng(26)
+    V, T = 6, 9
+    S = r.standard_normal((T, V))
+    q = np.zeros(V)
+    for t in range(1, T + 1):
+        q, qh = oracle.ema(q, S[t - 1], gold["beta1"], t)
+    lam = gold["lambda"]
+    bc = 1 - gold["kernel_decay"] ** T
+    coef_now = gold["kernel_current_base"] + gold["kernel_scale"] / bc
+    mix = (1 - lam) * S[T - 1] + lam * qh   # batch-mean part of u, in task space
+    expect = coef_now * S[T - 1] + sum(gold["kernel_scale"] * gold["kernel_decay"] ** k / bc * S[T - 1 - k]
+                                       for k in range(1, T))
+    np.testing.assert_allclose(mix, expect, atol=1e-14)
+
+
+# ----------------------------------------------------------------------------- update
+
+def test_dense_update_first_step_closed_form():
+    # t = 1: v_hat = u^2, so theta_1 = (1 - lr wd) theta - lr u / (|u| + eps).
+    r = _rng(27)
+    P = 1000
+    th, u = r.standard_normal(P), r.standard_normal(P) * 1e-3
+    u[:5] = 0.0
+    segs = [(0, 600, 0.01), (600, 100, 0.0)]
+    t1, v1 = oracle.update_dense(th, np.zeros(P), u, lr=1e-2, beta2=B2, eps=EPS, t=1, segments=segs,
+                                 weight_decay=0.1)
+    wd = np.r_[np.full(600, 0.01), np.zeros(100), np.full(300, 0.1)]
+    np.testing.assert_allclose(t1, (1 - 1e-2 * wd) * th - 1e-2 * u / (np.abs(u) + EPS), rtol=1e-13, atol=1e-16)
+    np.testing.assert_allclose(v1, (1 - B2) * u * u, rtol=1e-15)
+
+
+def test_dense_update_second_moment_explicit_sum():
+    r = _rng(28)
+    P, T = 64, 6
+    U = r.standard_normal((T, P))
+    th = r.standard_normal(P)
+    v = np.zeros(P)
+    for t in range(1, T + 1):
+        th_prev = th
+        th, v = oracle.update_dense(th, v, U[t - 1], lr=1e-3, beta2=B2, eps=EPS, t=t)
+        expect_v = sum((1 - B2) * B2 ** (t - tau) * U[tau - 1] ** 2 for tau in range(1, t + 1))
+        np.testing.assert_allclose(v, expect_v, rtol=1e-13)
+        vhat = expect_v / (1 - B2 ** t)
+        np.testing.assert_allclose(th, th_prev - 1e-3 * U[t - 1] / (np.sqrt(vhat) + EPS), rtol=1e-13)
+
+
+def test_dense_update_split_numerator_and_scale():
+    r = _rng(29)
+    P = 50
+    th, g, h = r.standard_normal(P), r.standard_normal(P), r.standard_normal(P)
+    v0 = np.abs(r.standard_normal(P))
+    a = oracle.update_dense(th, v0, g, h=h, lam=0.3, u_scale=0.7, lr=1e-3, beta2=B2, eps=EPS, t=4)
+    b = oracle.update_dense(th, v0, 0.7 * (0.7 * g + 0.3 * h), lr=1e-3, beta2=B2, eps=EPS, t=4)
+    np.testing.assert_allclose(a[0], b[0], rtol=1e-14)
+    np.testing.assert_allclose(a[1], b[1], rtol=1e-14)
+
+
+def test_factored_equals_dense_for_rank_one_squares():
+    # Adafactor identity: when u^2 is exactly rank one on every block (u_ij^2 = a_i b_j), the factored
+    # v_hat equals the dense v_hat, for every step if the pattern persists.
+    r = _rng(30)
+    br, bc = 8, 8
+    rows = 20                      # 3 blocks, the last with 4 rows
+    P = rows * bc
+    a = np.exp(r.standard_normal(rows))
+    bb = np.exp(r.standard_normal(bc))
+    sign = np.where(r.random((rows, bc)) < 0.5, -1.0, 1.0)
+    th = r.standard_normal(P)
+    thd, thf = th.copy(), th.copy()
+    v = np.zeros(P)
+    Rr, Cc = np.zeros(rows), np.zeros(3 * bc)
+    for t in range(1, 5):
+        scale = 1.0 + 0.5 * t
+        u = (sign * np.sqrt(np.outer(a, bb)) * scale).ravel()
+        thd, v = oracle.update_dense(thd, v, u, lr=1e-2, beta2=B2, eps=EPS, t=t, weight_decay=0.1)
+        thf, Rr, Cc = oracle.update_factored(thf, Rr, Cc, u, lr=1e-2, beta2=B2, eps=EPS, t=t, block_rows=br,
+                                             block_cols=bc, weight_decay=0.1)
+        np.testing.assert_allclose(thf, thd, rtol=1e-12, atol=1e-15)
+
+
+def test_factored_statistics_brute_force_and_ragged_tail():
+    r = _rng(31)
+    br, bc = 4, 8
+    P = 11 * 8 + 5                 # 12 rows, the last one short (5 of 8); 3 blocks
+    u = r.standard_normal(P)
+    th = r.standard_normal(P)
+    Rr0, Cc0 = np.abs(r.standard_normal(12)), np.abs(r.standard_normal(3 * bc))
+    t = 3
+    thf, Rr, Cc = oracle.update_factored(th, Rr0, Cc0, u, lr=1e-2, beta2=B2, eps=EPS, t=t, block_rows=br,
+                                         block_cols=bc)
+    U2 = np.zeros((12, bc))
+    U2.ravel()[:P] = u * u
+    np.testing.assert_allclose(Rr, B2 * Rr0 + (1 - B2) * U2.sum(1), rtol=1e-14)
+    kap = U2.reshape(3, br, bc).sum(1).ravel()
+    np.testing.assert_allclose(Cc, B2 * Cc0 + (1 - B2) * kap, rtol=1e-14)
+    vhat = np.zeros((12, bc))
+    for blk in range(3):
+        rr = Rr[blk * br:(blk + 1) * br]
+        vhat[blk * br:(blk + 1) * br] = np.outer(rr, Cc[blk * bc:(blk + 1) * bc]) / rr.sum() / (1 - B2 ** t)
+    expect = th - 1e-2 * u / (np.sqrt(vhat.ravel()[:P]) + EPS)
+    np.testing.assert_allclose(thf, expect, rtol=1e-13)
+
+
+def test_factored_zero_block_keeps_decay_only():
+    P = 64
+    th = _rng(32).standard_normal(P)
+    thf, Rr, Cc = oracle.update_factored(th, np.zeros(8), np.zeros(8), np.zeros(P), lr=1e-2, beta2=B2, eps=EPS,
+                                         t=1, block_rows=8, block_cols=8, weight_decay=0.1)
+    np.testing.assert_allclose(thf, (1 - 1e-3) * th, rtol=1e-15)
+
+
+# ----------------------------------------------------------------------------- multi-step
+
+def test_linear_model_bom_equals_own_step_control():
+    # Historical-projection appendix: for a linear model on a fixed batch the Jacobian is constant, so
+    # BOM's current reprojection and the own-step parameter-space EMA M_t coincide over a trajectory.
+    r = _rng(33)
+    N, d, V = 32, 6, 5
+    H = r.standard_normal((N, d))
+    y = r.integers(0, V, N).astype(np.int32)
+    theta0 = r.standard_normal(d * V + V) * 0.05
+    segs = [(0, d * V, 0.01), (d * V, V, 0.0)]
+    kw = dict(d=d, V=V, lr=1e-2, lam=LAM, beta1=B1, beta2=B2, eps=EPS, segments=segs)
+    th, v, q = theta0.copy(), np.zeros_like(theta0), np.zeros(V)
+    # independent control path: textbook CE gradient + parameter-space EMA of the own-step projection
+    th2, v2, M = theta0.copy(), np.zeros_like(theta0), np.zeros_like(theta0)
+    wd = np.r_[np.full(d * V, 0.01), np.zeros(V)]
+    for t in range(1, 21):
+        st = oracle.bom_step_linear_head(H, y, th, v, q, t, **kw)
+        th, v, q = st["theta"], st["v"], st["q"]
+        W2, b2 = th2[: d * V].reshape(d, V), th2[d * V:]
+        P = softmax(H @ W2 + b2, axis=1)
+        Rm = P - np.eye(V)[y]
+        s = Rm.mean(0)
+        g = np.r_[(H.T @ Rm / N).ravel(), s]
+        proj = np.r_[np.outer(H.mean(0), s).ravel(), s]     # Jbar_t^T s_t for (W, b)
+        M = B1 * M + (1 - B1) * proj
+        u2 = (1 - LAM) * g + LAM * M / (1 - B1 ** t)
+        v2 = B2 * v2 + (1 - B2) * u2 * u2
+        th2 = (1 - 1e-2 * wd) * th2 - 1e-2 * u2 / (np.sqrt(v2 / (1 - B2 ** t)) + EPS)
+        np.testing.assert_allclose(st["u"], u2, rtol=1e-9, atol=1e-14)
+        np.testing.assert_allclose(th, th2, rtol=1e-9, atol=1e-14)
+
+
+# ----------------------------------------------------------------------------- accounting
+
+def test_state_accounting_matches_printed_sizes():
+    gold = read_golden("state_accounting.txt")
+    P = int(gold["p_1b"])
+    gib = 2.0 ** 30
+    adamw = 4 * P + oracle.state_bytes(P, 32768, "adamw")
+    bom = 4 * P + oracle.state_bytes(P, 0, "bom")
+    assert round(adamw / gib, 2) == gold["adamw_ckpt_gib_1b"]
+    assert round(bom / gib, 2) == gold["bom_ckpt_gib_1b"]
+    P4, V4 = int(gold["p_4b"]), int(gold["v_4b"])
+    saving = oracle.state_bytes(P4, V4, "adamw") - oracle.state_bytes(P4, V4, "bom")
+    assert round(saving / gib, 3) == gold["saving_gib_4b"]
+
+
+@pytest.mark.parametrize("bad", ["adam", ""])
+def test_state_bytes_rejects_unknown(bad):
+    with pytest.raises(ValueError):
+        oracle.state_bytes(10, 2, bad)

@@ -1,0 +1,212 @@
+/*
+ * bom.h -- C-ABI of libbom.so: the per-step hot path of Backpropagated Output
+ * Momentum (BOM) with AdamW-style scaling on one AMD Instinct MI355X (gfx950).
+ *
+ * The method (paper: "Backpropagated Output Momentum: Relocating Optimizer
+ * History from Parameters to Task Space", Algorithm 1) keeps one task-space
+ * EMA q of the batch-mean softmax-cross-entropy residual s instead of a
+ * parameter-shaped first moment, folds its bias-corrected value q_hat into the
+ * gradient of the logits, and updates the parameters with a second moment of
+ * the resulting numerator u and decoupled weight decay.
+ *
+ * One step on the hot path is four calls, enqueued in this order:
+ *   bom_residual  -> s, row statistics, R           (Algorithm 1: s_t)
+ *   bom_ema       -> q (in place), q_hat            (Algorithm 1: q_t, q_hat_t)
+ *   bom_head_vjp  -> dW, db, dH of the mixed loss   (Eq. 3 / Eq. 4, output head)
+ *   bom_update    -> theta, v in place              (Sec. 3.4, Algorithm 1 last two lines)
+ *
+ * Conventions shared by every entry point:
+ *   - Every array argument is caller-owned DEVICE memory, except the small
+ *     host structs `segs` and `cfg`. The library allocates nothing and keeps
+ *     no pointer after returning; buffers must stay alive until the stream
+ *     reaches the enqueued work.
+ *   - `stream` is a hipStream_t (NULL = the default stream). Every call only
+ *     enqueues work; none synchronises the host.
+ *   - Matrices are row-major with an explicit leading dimension in ELEMENTS.
+ *   - Arguments are validated on the host before anything is enqueued; on an
+ *     argument error nothing is launched. bom_last_error() returns a
+ *     thread-local description of the last failure. No exception, abort or
+ *     exit crosses this ABI.
+ *   - Data-dependent conditions are reported in a device `flags` word
+ *     (BOM_FLAG_*), never by the return status.
+ *   - Results are deterministic: the same inputs give bitwise-identical
+ *     outputs (no floating-point atomics; fixed reduction orders).
+ */
+#ifndef BOM_H
+#define BOM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BOM_OK = 0,
+    BOM_ERR_NULL = 1,        /* a required pointer is NULL */
+    BOM_ERR_SHAPE = 2,       /* a size or leading dimension is out of range */
+    BOM_ERR_DTYPE = 3,       /* an unsupported dtype combination */
+    BOM_ERR_HYPER = 4,       /* a hyperparameter is outside its domain */
+    BOM_ERR_WORKSPACE = 5,   /* workspace missing or smaller than the query returns */
+    BOM_ERR_ALIAS = 6,       /* buffers that must be distinct overlap */
+    BOM_ERR_HIP = 7,         /* a HIP runtime call failed (detail in bom_last_error) */
+    BOM_ERR_UNSUPPORTED = 8  /* valid request this build does not implement */
+} bom_status;
+
+typedef enum { BOM_F32 = 0, BOM_BF16 = 1 } bom_dtype;
+
+/* Bits of the device flags word written by bom_residual. */
+#define BOM_FLAG_LABEL_RANGE 1 /* some label was neither ignore_index nor in [0, V); that row is ignored */
+#define BOM_FLAG_EMPTY 2       /* no valid row (N_t = 0): s = 0, loss = 0, downstream gradients are 0 */
+
+/* Second-moment layouts of bom_update. */
+#define BOM_V_DENSE 0
+#define BOM_V_FACTORED 1
+
+#define BOM_MAX_SEGMENTS 16
+
+/* ------------------------------------------------------------------------------------------
+ * bom_residual -- Algorithm 1, the line computing s_t; Sec. 3.2 (r = softmax(z) - onehot(y));
+ * token-level form: the appendix on language models (each valid target position is an
+ * example; ignored targets are excluded from every mean).
+ *
+ * For every row i of Z [N, V] (leading dimension ldz, dtype z_dt):
+ *   m_i = max_j z_ij, row_argmax[i] = the lowest j attaining m_i,
+ *   row_lse[i] = m_i + ln sum_j exp(z_ij - m_i).
+ * Row i is valid (i in I) when labels[i] != ignore_index and 0 <= labels[i] < V.
+ * For valid rows: row_target[i] = z_{i,y_i} (an exact copy of the input element),
+ *   R_ij = exp(z_ij - row_lse[i]) - [j == y_i]; for other rows row_target[i] = 0 and R_i = 0.
+ * Then, with N_t = |I|:
+ *   s[j] = (1/N_t) sum_{i in I} R_ij,   *loss = (1/N_t) sum_{i in I} (row_lse[i] - z_{i,y_i}),
+ *   *n_valid = N_t,   *flags = BOM_FLAG_* bits (overwritten, not OR-ed).
+ * If N_t = 0: s = 0, *loss = 0 and BOM_FLAG_EMPTY is set.
+ *
+ *   Z         device [N, ldz] of z_dt (BOM_F32 or BOM_BF16); ldz >= V.
+ *   labels    device int32 [N].
+ *   s         device fp32 [V].              row_lse device fp32 [N].
+ *   row_argmax, row_target: device [N] (int32 / fp32), may be NULL.
+ *   R         device [N, ldr] of r_dt, may be NULL (then R is not written). r_dt must equal
+ *             z_dt. ldr >= V.
+ *   loss      device fp32 [1].  n_valid device int32 [1].  flags device int32 [1].
+ *   workspace device, at least bom_residual_workspace_bytes(N, V, z_dt) bytes, 256-byte aligned.
+ * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE (N < 1, V < 2, ld < V, N or V >= 2^31), BOM_ERR_DTYPE,
+ *         BOM_ERR_WORKSPACE, BOM_ERR_HIP.
+ * ---------------------------------------------------------------------------------------- */
+size_t bom_residual_workspace_bytes(int64_t N, int64_t V, bom_dtype z_dt);
+bom_status bom_residual(const void* Z, bom_dtype z_dt, int64_t N, int64_t V, int64_t ldz,
+                        const int32_t* labels, int32_t ignore_index,
+                        float* s, float* row_lse, int32_t* row_argmax, float* row_target,
+                        void* R, bom_dtype r_dt, int64_t ldr,
+                        float* loss, int32_t* n_valid, int32_t* flags,
+                        void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------------
+ * bom_ema -- Sec. 3.2, Eq. (2) and Algorithm 1: q_t = beta1 q_{t-1} + (1 - beta1) s_t,
+ * q_hat_t = q_t / (1 - beta1^t), with q_0 = 0 and t >= 1.
+ *
+ *   q      device fp32 [V], the state, updated in place.   s device fp32 [V].
+ *   q_hat  device fp32 [V], output; must not overlap q.
+ *   The factor 1/(1 - beta1^t) is formed on the host in fp64 and applied in fp32.
+ * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE (V < 1), BOM_ERR_HYPER (beta1 not in [0,1), t < 1),
+ *         BOM_ERR_ALIAS, BOM_ERR_HIP.
+ * ---------------------------------------------------------------------------------------- */
+bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, float* q_hat, void* stream);
+
+/* ------------------------------------------------------------------------------------------
+ * bom_head_vjp -- the output-head part of the single backward pass through the mixed
+ * objective, Eq. (3), whose gradient is Eq. (4): u = (1 - lambda) g + lambda Jbar^T q_hat.
+ * For the linear head z_i = W^T h_i (+ b), the gradient of L_mix with respect to the logits is
+ *   G_ij = [i in I] ((1 - lambda) R_ij + lambda q_hat_j) / N_t        (q_hat held constant)
+ * and the head products are
+ *   dW = H^T G + dW_beta * dW     [d, V] fp32 (dW_beta = 0 overwrites; dW is not read then)
+ *   db = (1 - lambda) s + lambda q_hat   [V] fp32  (bias Jacobian = identity; equals 1^T G)
+ *   dH = G W^T                     [N, d] of dh_dt
+ * G is formed tile by tile inside the GEMMs (the history is folded into the output gradient
+ * at operand load) and never written to memory. N_t is read from the device word n_valid; when
+ * it is 0, G = 0.
+ *
+ *   H   device [N, ldh] of dt.   W device [d, ldw] of dt (the head as d x V).
+ *   R   device [N, ldr] of dt: the residual rows written by bom_residual (zero rows outside I).
+ *   dt  BOM_BF16 (MFMA path, fp32 accumulation; G is rounded to bf16 after folding) or BOM_F32.
+ *   labels device int32 [N] (defines I with ignore_index, as in bom_residual).
+ *   q_hat device fp32 [V].   s device fp32 [V] (only read when db != NULL).
+ *   n_valid device int32 [1].
+ *   dW  device fp32 [d, lddw]; lddw >= V.   db device fp32 [V] or NULL.
+ *   dH  device [N, lddh] of dh_dt (BOM_BF16 or BOM_F32), or NULL.
+ *   workspace: at least bom_head_vjp_workspace_bytes(N, d, V, dt) bytes (may be 0).
+ * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_DTYPE, BOM_ERR_HYPER (lambda not in [0,1]),
+ *         BOM_ERR_WORKSPACE, BOM_ERR_HIP.
+ * ---------------------------------------------------------------------------------------- */
+size_t bom_head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt);
+bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* R, int64_t ldr,
+                        bom_dtype dt, int64_t N, int64_t d, int64_t V,
+                        const int32_t* labels, int32_t ignore_index,
+                        const float* q_hat, const float* s, const int32_t* n_valid, float lambda,
+                        float* dW, int64_t lddw, float dW_beta,
+                        float* db, void* dH, bom_dtype dh_dt, int64_t lddh,
+                        void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------------
+ * bom_update -- Sec. 3.4 and the last two lines of Algorithm 1, over one flat fp32 buffer:
+ *   u' = u_scale * u                       (or, when h != NULL: u_scale * ((1-lambda) u + lambda h))
+ *   v  = beta2 v + (1 - beta2) u'^2,  v_hat = v / (1 - beta2^t)
+ *   theta = (1 - lr * omega) theta - lr * u' / (sqrt(v_hat) + eps)
+ * omega is the weight decay of the segment covering the element (the first match in `segs`),
+ * else `weight_decay`. There is no first-moment buffer.
+ *
+ * BOM_V_FACTORED (a reading: the paper does not define it; Adafactor's rank-1 factorisation of
+ * the same v): the buffer is viewed as a row-major matrix of block_cols columns (the last row may
+ * be short) whose rows form blocks of block_rows rows. Per block:
+ *   rho_i = sum_j u'_ij^2, kappa_j = sum_i u'_ij^2, Rr_i = beta2 Rr_i + (1-beta2) rho_i,
+ *   Cc_j = beta2 Cc_j + (1-beta2) kappa_j, v_hat_ij = Rr_i Cc_j / sum_{k in block} Rr_k / (1-beta2^t)
+ *   (0 when that sum is 0), then the same theta update.
+ *
+ *   theta device fp32 [P], in place.   u device fp32 [P].   h device fp32 [P] or NULL.
+ *   v     dense: device fp32 [P] (in place). factored: Rr, device fp32 [ceil(P/block_cols)].
+ *   v_col dense: NULL. factored: Cc, device fp32 [nblocks * block_cols],
+ *         nblocks = ceil(ceil(P/block_cols) / block_rows).
+ *   segs  HOST array of nsegs (<= BOM_MAX_SEGMENTS) segments inside [0, P), or NULL with nsegs 0.
+ *   cfg   HOST struct. The factor 1/(1 - beta2^t) is formed on the host in fp64.
+ *   workspace: at least bom_update_workspace_bytes(P, cfg) bytes (0 for the dense layout).
+ * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_HYPER (beta2 not in [0,1), t < 1, eps <= 0,
+ *         lambda not in [0,1], non-finite lr / u_scale / decay), BOM_ERR_ALIAS, BOM_ERR_WORKSPACE,
+ *         BOM_ERR_HIP.
+ * ---------------------------------------------------------------------------------------- */
+typedef struct {
+    int64_t offset;
+    int64_t length;
+    float weight_decay;
+} bom_segment;
+
+typedef struct {
+    float lr, beta2, eps, lambda, u_scale;
+    int64_t t;
+    int32_t v_layout; /* BOM_V_DENSE or BOM_V_FACTORED */
+    int64_t block_rows, block_cols;
+} bom_update_cfg;
+
+size_t bom_update_workspace_bytes(int64_t P, const bom_update_cfg* cfg);
+bom_status bom_update(float* theta, float* v, float* v_col, const float* u, const float* h, int64_t P,
+                      const bom_segment* segs, int32_t nsegs, float weight_decay, const bom_update_cfg* cfg,
+                      void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------------
+ * bom_head_forward -- support call (not one of the four steps): the linear head's logits
+ * Z = H W (+ b), used by multi-step loops that move W. fp32 only in this build (dt = BOM_F32;
+ * BOM_BF16 returns BOM_ERR_UNSUPPORTED).
+ *   H device [N, ldh], W device [d, ldw], b device [V] or NULL, Z device [N, ldz].
+ * ---------------------------------------------------------------------------------------- */
+bom_status bom_head_forward(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
+                            int64_t N, int64_t d, int64_t V, void* Z, int64_t ldz, void* stream);
+
+/* Static text of a status code, and the thread-local detail of the last failure ("" if none). */
+const char* bom_status_string(bom_status status);
+const char* bom_last_error(void);
+/* Library ABI version (major * 10000 + minor * 100 + patch). */
+int32_t bom_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BOM_H */

@@ -1,0 +1,227 @@
+// C-ABI of libbom.so (declared in include/bom.h): host-side validation, then enqueue.
+// Every argument error is returned before any HIP call; no exception crosses the ABI.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "bom.h"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+bom_status fail(bom_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+bom_status hip_status(hipError_t e, const char* where) {
+    if (e == hipSuccess) {
+        g_last_error[0] = '\0';
+        return BOM_OK;
+    }
+    return fail(BOM_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+constexpr int64_t kMaxDim = (int64_t)1 << 31;
+
+bool is_dtype(bom_dtype d) { return d == BOM_F32 || d == BOM_BF16; }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+    const char* pa = static_cast<const char*>(a);
+    const char* pb = static_cast<const char*>(b);
+    return pa < pb + nb && pb < pa + na;
+}
+
+bool finite(float x) { return std::isfinite(x); }
+
+}  // namespace
+
+extern "C" {
+
+const char* bom_status_string(bom_status s) {
+    switch (s) {
+        case BOM_OK: return "BOM_OK";
+        case BOM_ERR_NULL: return "BOM_ERR_NULL: a required pointer is NULL";
+        case BOM_ERR_SHAPE: return "BOM_ERR_SHAPE: a size or leading dimension is out of range";
+        case BOM_ERR_DTYPE: return "BOM_ERR_DTYPE: unsupported dtype combination";
+        case BOM_ERR_HYPER: return "BOM_ERR_HYPER: a hyperparameter is outside its domain";
+        case BOM_ERR_WORKSPACE: return "BOM_ERR_WORKSPACE: workspace missing or too small";
+        case BOM_ERR_ALIAS: return "BOM_ERR_ALIAS: buffers that must be distinct overlap";
+        case BOM_ERR_HIP: return "BOM_ERR_HIP: a HIP runtime call failed";
+        case BOM_ERR_UNSUPPORTED: return "BOM_ERR_UNSUPPORTED: not implemented in this build";
+    }
+    return "unknown bom_status";
+}
+
+const char* bom_last_error(void) { return g_last_error; }
+
+int32_t bom_version(void) { return 100; }
+
+size_t bom_residual_workspace_bytes(int64_t N, int64_t V, bom_dtype z_dt) {
+    if (N < 1 || V < 1 || N >= kMaxDim || V >= kMaxDim || !is_dtype(z_dt)) return 0;
+    return bom::residual_workspace_bytes(N, V, z_dt);
+}
+
+bom_status bom_residual(const void* Z, bom_dtype z_dt, int64_t N, int64_t V, int64_t ldz, const int32_t* labels,
+                        int32_t ignore_index, float* s, float* row_lse, int32_t* row_argmax, float* row_target, void* R,
+                        bom_dtype r_dt, int64_t ldr, float* loss, int32_t* n_valid, int32_t* flags, void* workspace,
+                        size_t ws_bytes, void* stream) {
+    if (!Z || !labels || !s || !row_lse || !loss || !n_valid || !flags)
+        return fail(BOM_ERR_NULL, "bom_residual: Z, labels, s, row_lse, loss, n_valid and flags are required");
+    if (N < 1 || V < 2 || N >= kMaxDim || V >= kMaxDim)
+        return fail(BOM_ERR_SHAPE, "bom_residual: need 1 <= N < 2^31 and 2 <= V < 2^31 (N=%lld V=%lld)", (long long)N,
+                    (long long)V);
+    if (ldz < V || (R && ldr < V))
+        return fail(BOM_ERR_SHAPE, "bom_residual: leading dimensions must be >= V (ldz=%lld ldr=%lld V=%lld)",
+                    (long long)ldz, (long long)ldr, (long long)V);
+    if (!is_dtype(z_dt) || (R && r_dt != z_dt))
+        return fail(BOM_ERR_DTYPE, "bom_residual: z_dt must be BOM_F32 or BOM_BF16 and r_dt must equal it");
+    const size_t need = bom::residual_workspace_bytes(N, V, z_dt);
+    if (!workspace || ws_bytes < need)
+        return fail(BOM_ERR_WORKSPACE, "bom_residual: workspace needs %zu bytes, got %zu", need, ws_bytes);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+        return fail(BOM_ERR_WORKSPACE, "bom_residual: workspace must be 256-byte aligned");
+    const size_t esz = z_dt == BOM_BF16 ? 2 : 4;
+    if (R && overlap(R, (size_t)((N - 1) * ldr + V) * esz, Z, (size_t)((N - 1) * ldz + V) * esz))
+        return fail(BOM_ERR_ALIAS, "bom_residual: R must not overlap Z");
+    hipError_t e = bom::launch_residual(Z, z_dt, (int)N, (int)V, ldz, labels, ignore_index, s, row_lse, row_argmax,
+                                        row_target, R, ldr, loss, n_valid, flags, workspace,
+                                        static_cast<hipStream_t>(stream));
+    return hip_status(e, "bom_residual");
+}
+
+bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, float* q_hat, void* stream) {
+    if (!q || !s || !q_hat) return fail(BOM_ERR_NULL, "bom_ema: q, s and q_hat are required");
+    if (V < 1 || V >= kMaxDim) return fail(BOM_ERR_SHAPE, "bom_ema: need 1 <= V < 2^31");
+    if (!(beta1 >= 0.f && beta1 < 1.f) || t < 1)
+        return fail(BOM_ERR_HYPER, "bom_ema: need beta1 in [0, 1) and t >= 1 (beta1=%g t=%lld)", (double)beta1,
+                    (long long)t);
+    if (overlap(q, (size_t)V * 4, q_hat, (size_t)V * 4)) return fail(BOM_ERR_ALIAS, "bom_ema: q_hat must not overlap q");
+    const double bc = 1.0 - std::pow((double)beta1, (double)t);
+    const float inv_bc1 = (float)(1.0 / bc);
+    return hip_status(bom::launch_ema(q, s, V, beta1, inv_bc1, q_hat, static_cast<hipStream_t>(stream)), "bom_ema");
+}
+
+size_t bom_head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
+    if (N < 1 || d < 1 || V < 1 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim || !is_dtype(dt)) return 0;
+    return bom::head_vjp_workspace_bytes(N, d, V, dt);
+}
+
+bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* R, int64_t ldr,
+                        bom_dtype dt, int64_t N, int64_t d, int64_t V, const int32_t* labels, int32_t ignore_index,
+                        const float* q_hat, const float* s, const int32_t* n_valid, float lambda, float* dW,
+                        int64_t lddw, float dW_beta, float* db, void* dH, bom_dtype dh_dt, int64_t lddh,
+                        void* workspace, size_t ws_bytes, void* stream) {
+    if (!H || !W || !R || !labels || !q_hat || !n_valid || !dW)
+        return fail(BOM_ERR_NULL, "bom_head_vjp: H, W, R, labels, q_hat, n_valid and dW are required");
+    if (db && !s) return fail(BOM_ERR_NULL, "bom_head_vjp: s is required when db is requested");
+    if (N < 1 || d < 1 || V < 2 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim)
+        return fail(BOM_ERR_SHAPE, "bom_head_vjp: need N >= 1, d >= 1, V >= 2, all < 2^31");
+    if (ldh < d || ldw < V || ldr < V || lddw < V || (dH && lddh < d))
+        return fail(BOM_ERR_SHAPE, "bom_head_vjp: a leading dimension is smaller than its row length");
+    if ((int64_t)d * V >= ((int64_t)1 << 40) || (int64_t)N * d >= ((int64_t)1 << 40))
+        return fail(BOM_ERR_SHAPE, "bom_head_vjp: output too large");
+    if (!is_dtype(dt) || (dH && !is_dtype(dh_dt))) return fail(BOM_ERR_DTYPE, "bom_head_vjp: unsupported dtype");
+    if (!(lambda >= 0.f && lambda <= 1.f)) return fail(BOM_ERR_HYPER, "bom_head_vjp: need lambda in [0, 1]");
+    if (!finite(dW_beta)) return fail(BOM_ERR_HYPER, "bom_head_vjp: dW_beta must be finite");
+    const size_t need = bom::head_vjp_workspace_bytes(N, d, V, dt);
+    if (need > 0 && (!workspace || ws_bytes < need))
+        return fail(BOM_ERR_WORKSPACE, "bom_head_vjp: workspace needs %zu bytes, got %zu", need, ws_bytes);
+    if (workspace && reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+        return fail(BOM_ERR_WORKSPACE, "bom_head_vjp: workspace must be 256-byte aligned");
+    bom::HeadVjpArgs a{H, ldh, W, ldw, R, ldr, dt, (int)N, (int)d, (int)V, labels, ignore_index, q_hat, s, n_valid, lambda,
+                       dW, lddw, dW_beta, db, dH, dh_dt, lddh, workspace, ws_bytes};
+    return hip_status(bom::launch_head_vjp(a, static_cast<hipStream_t>(stream)), "bom_head_vjp");
+}
+
+size_t bom_update_workspace_bytes(int64_t P, const bom_update_cfg* cfg) { return bom::update_workspace_bytes(P, cfg); }
+
+bom_status bom_update(float* theta, float* v, float* v_col, const float* u, const float* h, int64_t P,
+                      const bom_segment* segs, int32_t nsegs, float weight_decay, const bom_update_cfg* cfg,
+                      void* workspace, size_t ws_bytes, void* stream) {
+    if (!theta || !v || !u || !cfg) return fail(BOM_ERR_NULL, "bom_update: theta, v, u and cfg are required");
+    if (P < 1) return fail(BOM_ERR_SHAPE, "bom_update: need P >= 1");
+    if (nsegs < 0 || nsegs > BOM_MAX_SEGMENTS || (nsegs > 0 && !segs))
+        return fail(BOM_ERR_SHAPE, "bom_update: need 0 <= nsegs <= %d and segs when nsegs > 0", BOM_MAX_SEGMENTS);
+    const bom_update_cfg& c = *cfg;
+    if (!(c.beta2 >= 0.f && c.beta2 < 1.f) || c.t < 1 || !(c.eps > 0.f) || !finite(c.eps) || !finite(c.lr) ||
+        !(c.lambda >= 0.f && c.lambda <= 1.f) || !finite(c.u_scale) || !finite(weight_decay))
+        return fail(BOM_ERR_HYPER, "bom_update: need beta2 in [0,1), t >= 1, eps > 0, lambda in [0,1], finite lr, "
+                                   "u_scale and weight decay");
+    bom::SegTable st{};
+    st.n = nsegs;
+    st.wd_default = weight_decay;
+    for (int k = 0; k < nsegs; ++k) {
+        const bom_segment& g = segs[k];
+        if (g.offset < 0 || g.length < 0 || g.offset + g.length > P)
+            return fail(BOM_ERR_SHAPE, "bom_update: segment %d [%lld, +%lld) is outside [0, P)", k, (long long)g.offset,
+                        (long long)g.length);
+        if (!finite(g.weight_decay)) return fail(BOM_ERR_HYPER, "bom_update: segment %d decay is not finite", k);
+        st.begin[k] = g.offset;
+        st.end[k] = g.offset + g.length;
+        st.wd[k] = g.weight_decay;
+    }
+    bom::UpdateScalars sc;
+    sc.lr = c.lr;
+    sc.beta2 = c.beta2;
+    sc.one_minus_beta2 = (float)(1.0 - (double)c.beta2);
+    sc.eps = c.eps;
+    sc.lambda = c.lambda;
+    sc.u_scale = c.u_scale;
+    sc.inv_bc2 = (float)(1.0 / (1.0 - std::pow((double)c.beta2, (double)c.t)));
+    const size_t pb = (size_t)P * 4;
+    if (overlap(theta, pb, u, pb) || (h && overlap(theta, pb, h, pb)))
+        return fail(BOM_ERR_ALIAS, "bom_update: theta must not overlap u or h");
+    hipStream_t strm = static_cast<hipStream_t>(stream);
+    if (c.v_layout == BOM_V_DENSE) {
+        if (v_col) return fail(BOM_ERR_SHAPE, "bom_update: v_col must be NULL for the dense layout");
+        if (overlap(v, pb, theta, pb) || overlap(v, pb, u, pb) || (h && overlap(v, pb, h, pb)))
+            return fail(BOM_ERR_ALIAS, "bom_update: v must not overlap theta, u or h");
+        return hip_status(bom::launch_update_dense(theta, v, u, h, P, st, sc, strm), "bom_update");
+    }
+    if (c.v_layout != BOM_V_FACTORED) return fail(BOM_ERR_SHAPE, "bom_update: unknown v_layout %d", c.v_layout);
+    if (!v_col) return fail(BOM_ERR_NULL, "bom_update: the factored layout needs v_col");
+    if (c.block_rows < 1 || c.block_cols < 4 || c.block_cols > 16384 || c.block_cols % 4 != 0)
+        return fail(BOM_ERR_UNSUPPORTED, "bom_update: factored layout needs block_rows >= 1 and block_cols a multiple "
+                                         "of 4 in [4, 16384]");
+    if (P % 4 != 0) return fail(BOM_ERR_UNSUPPORTED, "bom_update: factored layout needs P % 4 == 0");
+    auto al = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
+    if (!al(theta) || !al(u) || (h && !al(h)) || !al(v_col))
+        return fail(BOM_ERR_UNSUPPORTED, "bom_update: factored layout needs 16-byte aligned theta, u, h and v_col");
+    const size_t need = bom::update_workspace_bytes(P, cfg);
+    if (!workspace || ws_bytes < need)
+        return fail(BOM_ERR_WORKSPACE, "bom_update: workspace needs %zu bytes, got %zu", need, ws_bytes);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+        return fail(BOM_ERR_WORKSPACE, "bom_update: workspace must be 256-byte aligned");
+    const int64_t nrows = (P + c.block_cols - 1) / c.block_cols;
+    const int64_t nblocks = (nrows + c.block_rows - 1) / c.block_rows;
+    if (overlap(v, (size_t)nrows * 4, v_col, (size_t)nblocks * c.block_cols * 4) || overlap(v, (size_t)nrows * 4, theta, pb) ||
+        overlap(v_col, (size_t)nblocks * c.block_cols * 4, theta, pb))
+        return fail(BOM_ERR_ALIAS, "bom_update: Rr, Cc and theta must be distinct");
+    return hip_status(bom::launch_update_factored(theta, v, v_col, u, h, P, c.block_rows, c.block_cols, st, sc, workspace,
+                                                  strm),
+                      "bom_update");
+}
+
+bom_status bom_head_forward(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
+                            int64_t N, int64_t d, int64_t V, void* Z, int64_t ldz, void* stream) {
+    if (!H || !W || !Z) return fail(BOM_ERR_NULL, "bom_head_forward: H, W and Z are required");
+    if (N < 1 || d < 1 || V < 1 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim || ldh < d || ldw < V || ldz < V)
+        return fail(BOM_ERR_SHAPE, "bom_head_forward: bad shape or leading dimension");
+    if (dt == BOM_BF16) return fail(BOM_ERR_UNSUPPORTED, "bom_head_forward: only BOM_F32 in this build");
+    if (dt != BOM_F32) return fail(BOM_ERR_DTYPE, "bom_head_forward: unsupported dtype");
+    return hip_status(bom::launch_head_forward_f32(static_cast<const float*>(H), ldh, static_cast<const float*>(W), ldw,
+                                                   static_cast<const float*>(b), (int)N, (int)d, (int)V,
+                                                   static_cast<float*>(Z), ldz, static_cast<hipStream_t>(stream)),
+                      "bom_head_forward");
+}
+
+}  // extern "C"

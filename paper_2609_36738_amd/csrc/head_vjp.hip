@@ -1,0 +1,657 @@
+// bom_head_vjp kernels: the output-head part of the one backward pass through the mixed
+// objective (Eq. (3)); its gradient (Eq. (4)) for the linear head z_i = W^T h_i (+ b) is
+//   G_ij = [i in I] ((1 - lambda) R_ij + lambda q_hat_j) / N_t      (gradient w.r.t. the logits)
+//   dW = H^T G,  dH = G W^T,  db = 1^T G = (1 - lambda) s + lambda q_hat  (bias Jacobian = I).
+// G is never stored: each GEMM forms its G tile while staging R into LDS,
+//   G = fma(alpha, R, mask_i * cq_j),  alpha = (1 - lambda) / N_t,  cq_j = lambda q_hat_j / N_t,
+// and rounds it to bf16 for the MFMA path.
+//
+// bf16 path: v_mfma_f32_32x32x16_bf16, 128 x 128 output tiles, 64-deep k tiles double-buffered in
+// LDS, four waves each owning a 64 x 64 quadrant; dW = H^T G has both operands k-outer in memory
+// and is transposed while staging (perm for H, the bf16 pack of the fold for G); dH = G W^T has
+// both operands k-contiguous. Split-K with a fixed-order reduction when the output has too few
+// tiles to fill the chip. fp32 path (and unaligned bf16): a SIMT tiled GEMM.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace bom {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+
+struct Fold {
+    const float* cq;     // [V] lambda * q_hat / N_t
+    const float* vmask;  // [N] 1 for rows in I, else 0
+    const float* scal;   // [0] = alpha = (1 - lambda) / N_t
+};
+
+struct VjpWs {
+    size_t cq_off, vmask_off, scal_off, part_off, total;
+};
+
+// ---- prep -------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void vjp_prep_kernel(const float* __restrict__ q_hat, const float* __restrict__ s,
+                                                       const int32_t* __restrict__ n_valid, float lambda, int V, int N,
+                                                       const int32_t* __restrict__ labels, int32_t ignore_index,
+                                                       float* __restrict__ cq, float* __restrict__ vmask,
+                                                       float* __restrict__ scal, float* __restrict__ db) {
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    const int nt = *n_valid;
+    if (idx < V) {
+        cq[idx] = nt > 0 ? (float)((double)lambda * (double)q_hat[idx] / (double)nt) : 0.f;
+        if (db) db[idx] = nt > 0 ? (1.0f - lambda) * s[idx] + lambda * q_hat[idx] : 0.f;
+    }
+    if (idx < N) {
+        bool bad = false;
+        vmask[idx] = label_valid(labels[idx], V, ignore_index, &bad) ? 1.f : 0.f;
+    }
+    if (idx == 0) scal[0] = nt > 0 ? (float)((1.0 - (double)lambda) / (double)nt) : 0.f;
+}
+
+template <typename T>
+__device__ __forceinline__ float ldf(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float ldf<float>(const float* p, int64_t i) { return p[i]; }
+template <>
+__device__ __forceinline__ float ldf<uint16_t>(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
+
+template <typename T>
+__device__ __forceinline__ void stf(T* p, int64_t i, float x);
+template <>
+__device__ __forceinline__ void stf<float>(float* p, int64_t i, float x) { p[i] = x; }
+template <>
+__device__ __forceinline__ void stf<uint16_t>(uint16_t* p, int64_t i, float x) { p[i] = f32_to_bf16(x); }
+
+// ---- SIMT fallback: 64 x 64 tiles, 16-deep k, 4 x 4 outputs per thread --------------------------
+constexpr int SB = 64, SK = 16;
+
+// dW[m][n] = sum_k H[k][m] G[k][n];  M = d, Nn = V, K = N rows.
+template <typename T>
+__global__ __launch_bounds__(256) void simt_dW_kernel(const T* __restrict__ H, int64_t ldh, const T* __restrict__ R,
+                                                      int64_t ldr, int M, int Nn, int K, int kps, Fold f,
+                                                      float* __restrict__ out, int64_t ldo, float beta, int direct) {
+    __shared__ float As[SK][SB + 4];
+    __shared__ float Bs[SK][SB + 4];
+    const int t = threadIdx.x, tx = t % 16, ty = t / 16;
+    const int m0 = blockIdx.y * SB, n0 = blockIdx.x * SB;
+    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
+    const float alpha = f.scal[0];
+    float acc[4][4] = {};
+    for (int k0 = kb; k0 < ke; k0 += SK) {
+        for (int e = 0; e < 4; ++e) {
+            const int idx = e * 256 + t, kk = idx / SB, cc = idx % SB;
+            const int k = k0 + kk;
+            As[kk][cc] = (k < ke && m0 + cc < M) ? ldf(H, (int64_t)k * ldh + m0 + cc) : 0.f;
+            Bs[kk][cc] = (k < ke && n0 + cc < Nn) ? fmaf(alpha, ldf(R, (int64_t)k * ldr + n0 + cc), f.vmask[k] * f.cq[n0 + cc]) : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < SK; ++kk) {
+            float a[4], b[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+    for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) {
+            const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+            if (m >= M || n >= Nn) continue;
+            if (direct) {
+                float v = acc[i][j];
+                if (beta != 0.f) v += beta * out[(int64_t)m * ldo + n];
+                out[(int64_t)m * ldo + n] = v;
+            } else {
+                out[((int64_t)blockIdx.z * M + m) * Nn + n] = acc[i][j];
+            }
+        }
+}
+
+// dH[i][n] = sum_j G[i][j] W[n][j];  M = N rows, Nn = d, K = V.
+template <typename T, typename TO>
+__global__ __launch_bounds__(256) void simt_dH_kernel(const T* __restrict__ R, int64_t ldr, const T* __restrict__ W,
+                                                      int64_t ldw, int M, int Nn, int K, int kps, Fold f,
+                                                      TO* __restrict__ out, int64_t ldo, float* __restrict__ part,
+                                                      int direct) {
+    __shared__ float As[SK][SB + 4];
+    __shared__ float Bs[SK][SB + 4];
+    const int t = threadIdx.x, tx = t % 16, ty = t / 16;
+    const int m0 = blockIdx.y * SB, n0 = blockIdx.x * SB;
+    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
+    const float alpha = f.scal[0];
+    float acc[4][4] = {};
+    for (int k0 = kb; k0 < ke; k0 += SK) {
+        for (int e = 0; e < 4; ++e) {
+            const int idx = e * 256 + t, rr = idx / SK, kk = idx % SK;
+            const int k = k0 + kk;
+            As[kk][rr] = (k < ke && m0 + rr < M) ? fmaf(alpha, ldf(R, (int64_t)(m0 + rr) * ldr + k), f.vmask[m0 + rr] * f.cq[k]) : 0.f;
+            Bs[kk][rr] = (k < ke && n0 + rr < Nn) ? ldf(W, (int64_t)(n0 + rr) * ldw + k) : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < SK; ++kk) {
+            float a[4], b[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+    for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) {
+            const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+            if (m >= M || n >= Nn) continue;
+            if (direct) stf<TO>(out, (int64_t)m * ldo + n, acc[i][j]);
+            else part[((int64_t)blockIdx.z * M + m) * Nn + n] = acc[i][j];
+        }
+}
+
+// ---- MFMA bf16 path -----------------------------------------------------------------------------
+constexpr int MB = 128;          // output tile (both dims)
+constexpr int MK = 64;           // k tile
+constexpr int LDK = MK + 8;      // LDS row pitch in bf16 elements (144 bytes)
+
+// A tile for dW: A(m, k) = H[k][m], global rows k contiguous in m. Thread t stages k rows
+// kq*4..+3 and m columns mq*8..+7 (kq = t / 16, mq = t % 16); transposes with byte permutes.
+struct StageHt {
+    uint4 r[4];
+    __device__ __forceinline__ void load(const uint16_t* H, int64_t ldh, int M, int k0, int kend, int m0) {
+        const int t = threadIdx.x, kq = t / 16, mq = t % 16;
+        const int m = m0 + mq * 8;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = k0 + kq * 4 + q;
+            if (k < kend && m + 8 <= M) {
+                r[q] = *reinterpret_cast<const uint4*>(H + (int64_t)k * ldh + m);
+            } else {
+                uint16_t v[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = (k < kend && m + e < M) ? H[(int64_t)k * ldh + m + e] : (uint16_t)0;
+                r[q] = make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
+                                  v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
+            }
+        }
+    }
+    __device__ __forceinline__ void store(uint16_t (*As)[LDK]) const {
+        const int t = threadIdx.x, kq = t / 16, mq = t % 16;
+        const uint32_t w0[4] = {r[0].x, r[0].y, r[0].z, r[0].w};
+        const uint32_t w1[4] = {r[1].x, r[1].y, r[1].z, r[1].w};
+        const uint32_t w2[4] = {r[2].x, r[2].y, r[2].z, r[2].w};
+        const uint32_t w3[4] = {r[3].x, r[3].y, r[3].z, r[3].w};
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            // columns m = mq*8 + 2p (low halves) and 2p + 1 (high halves)
+            uint2 lo, hi;
+            lo.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x05040100u);
+            lo.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x05040100u);
+            hi.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x07060302u);
+            hi.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x07060302u);
+            *reinterpret_cast<uint2*>(&As[mq * 8 + 2 * p][kq * 4]) = lo;
+            *reinterpret_cast<uint2*>(&As[mq * 8 + 2 * p + 1][kq * 4]) = hi;
+        }
+    }
+};
+
+// B tile for dW: B(k, n) = G(k, n) from R[k][n]; same thread geometry as StageHt, the fold
+// G = fma(alpha, R, mask_k * cq_n) in fp32, rounded to bf16 pairs (k, k+1) -- the transpose.
+struct StageGt {
+    uint4 r[4];
+    float vm[4];
+    __device__ __forceinline__ void load(const uint16_t* R, int64_t ldr, int Nn, int k0, int kend, int n0,
+                                         const float* vmask) {
+        const int t = threadIdx.x, kq = t / 16, mq = t % 16;
+        const int n = n0 + mq * 8;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = k0 + kq * 4 + q;
+            vm[q] = k < kend ? vmask[k] : 0.f;
+            if (k < kend && n + 8 <= Nn) {
+                r[q] = *reinterpret_cast<const uint4*>(R + (int64_t)k * ldr + n);
+            } else {
+                uint16_t v[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = (k < kend && n + e < Nn) ? R[(int64_t)k * ldr + n + e] : (uint16_t)0;
+                r[q] = make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
+                                  v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
+            }
+        }
+    }
+    __device__ __forceinline__ void store(uint16_t (*Bs)[LDK], float alpha, const float* cqn) const {
+        const int t = threadIdx.x, kq = t / 16, mq = t % 16;
+        const uint32_t w[4][4] = {{r[0].x, r[0].y, r[0].z, r[0].w},
+                                  {r[1].x, r[1].y, r[1].z, r[1].w},
+                                  {r[2].x, r[2].y, r[2].z, r[2].w},
+                                  {r[3].x, r[3].y, r[3].z, r[3].w}};
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            float g[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float rv = (c & 1) ? bf16_hi(w[q][c >> 1]) : bf16_lo(w[q][c >> 1]);
+                g[q] = fmaf(alpha, rv, vm[q] * cqn[c]);
+            }
+            uint2 o;
+            o.x = pack_bf16x2(g[0], g[1]);
+            o.y = pack_bf16x2(g[2], g[3]);
+            *reinterpret_cast<uint2*>(&Bs[mq * 8 + c][kq * 4]) = o;
+        }
+    }
+};
+
+// k-contiguous tiles (dH): tile rows are output rows (A) or output columns (B); thread t stages
+// rows (e*256 + t) / 8 and k chunk ((e*256 + t) % 8) * 8, e < 4.
+template <bool FOLD>
+struct StageK {
+    uint4 r[4];
+    __device__ __forceinline__ void load(const uint16_t* X, int64_t ldx, int rows, int r0, int k0, int kend) {
+        const int t = threadIdx.x;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int c = e * 256 + t, row = r0 + c / 8, k = k0 + (c % 8) * 8;
+            if (row < rows && k + 8 <= kend) {
+                r[e] = *reinterpret_cast<const uint4*>(X + (int64_t)row * ldx + k);
+            } else {
+                uint16_t v[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) v[q] = (row < rows && k + q < kend) ? X[(int64_t)row * ldx + k + q] : (uint16_t)0;
+                r[e] = make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
+                                  v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
+            }
+        }
+    }
+    __device__ __forceinline__ void store(uint16_t (*S)[LDK], int rows, int r0, int k0, int kend, const Fold& f,
+                                          float alpha) const {
+        const int t = threadIdx.x;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int c = e * 256 + t, lr = c / 8, lk = (c % 8) * 8;
+            uint4 o = r[e];
+            if (FOLD) {
+                const float vm = (r0 + lr < rows) ? f.vmask[r0 + lr] : 0.f;
+                const int k = k0 + lk;
+                float cq[8];
+                if (k + 8 <= kend) {
+                    const float4 c0 = *reinterpret_cast<const float4*>(f.cq + k);
+                    const float4 c1 = *reinterpret_cast<const float4*>(f.cq + k + 4);
+                    cq[0] = c0.x; cq[1] = c0.y; cq[2] = c0.z; cq[3] = c0.w;
+                    cq[4] = c1.x; cq[5] = c1.y; cq[6] = c1.z; cq[7] = c1.w;
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) cq[q] = (k + q < kend) ? f.cq[k + q] : 0.f;
+                }
+                const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+                uint32_t g[4];
+#pragma unroll
+                for (int p = 0; p < 4; ++p)
+                    g[p] = pack_bf16x2(fmaf(alpha, bf16_lo(w[p]), vm * cq[2 * p]),
+                                       fmaf(alpha, bf16_hi(w[p]), vm * cq[2 * p + 1]));
+                o = make_uint4(g[0], g[1], g[2], g[3]);
+            }
+            *reinterpret_cast<uint4*>(&S[lr][lk]) = o;
+        }
+    }
+};
+
+__device__ __forceinline__ void mfma_tile(const uint16_t (*As)[LDK], const uint16_t (*Bs)[LDK], f32x16_t (&acc)[2][2]) {
+    const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+    const int wm = w / 2, wn = w % 2;
+    const int lr = lane % 32, lk = (lane / 32) * 8;
+#pragma unroll
+    for (int kk = 0; kk < MK; kk += 16) {
+        bf16x8_t a[2], b[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) a[i] = *reinterpret_cast<const bf16x8_t*>(&As[wm * 64 + i * 32 + lr][kk + lk]);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) b[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[wn * 64 + j * 32 + lr][kk + lk]);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+}
+
+// Accumulator element r of lane l in block (i, j) sits at tile row wm*64 + i*32 + (r/4)*8 + (l/32)*4 + r%4
+// and tile column wn*64 + j*32 + l%32.
+template <typename F>
+__device__ __forceinline__ void for_each_acc(const f32x16_t (&acc)[2][2], F&& fn) {
+    const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+    const int wm = w / 2, wn = w % 2;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                fn(wm * 64 + i * 32 + (r / 4) * 8 + (lane / 32) * 4 + (r % 4), wn * 64 + j * 32 + lane % 32, acc[i][j][r]);
+}
+
+// dW[m][n] = sum_k H[k][m] G[k][n]: M = d, Nn = V, K = N rows.
+__global__ __launch_bounds__(256) void mfma_dW_kernel(const uint16_t* __restrict__ H, int64_t ldh,
+                                                      const uint16_t* __restrict__ R, int64_t ldr, int M, int Nn, int K,
+                                                      int kps, Fold f, float* __restrict__ out, int64_t ldo, float beta,
+                                                      float* __restrict__ part) {
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][MB][LDK];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][MB][LDK];
+    const int m0 = blockIdx.y * MB, n0 = blockIdx.x * MB;
+    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
+    const float alpha = f.scal[0];
+    float cqn[8];
+    {
+        const int n = n0 + (threadIdx.x % 16) * 8;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) cqn[c] = (n + c < Nn) ? f.cq[n + c] : 0.f;
+    }
+    f32x16_t acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    StageHt sa;
+    StageGt sb;
+    const int nk = (ke - kb + MK - 1) / MK;
+    if (nk > 0) {
+        sa.load(H, ldh, M, kb, ke, m0);
+        sb.load(R, ldr, Nn, kb, ke, n0, f.vmask);
+        sa.store(As[0]);
+        sb.store(Bs[0], alpha, cqn);
+    }
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            const int k0 = kb + (kt + 1) * MK;
+            sa.load(H, ldh, M, k0, ke, m0);
+            sb.load(R, ldr, Nn, k0, ke, n0, f.vmask);
+        }
+        mfma_tile(As[buf], Bs[buf], acc);
+        if (more) {
+            sa.store(As[buf ^ 1]);
+            sb.store(Bs[buf ^ 1], alpha, cqn);
+        }
+        __syncthreads();
+    }
+    if (part == nullptr) {
+        for_each_acc(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) {
+                float* p = out + (int64_t)m * ldo + n;
+                *p = beta != 0.f ? v + beta * *p : v;
+            }
+        });
+    } else {
+        float* pz = part + (int64_t)blockIdx.z * M * Nn;
+        for_each_acc(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = v;
+        });
+    }
+}
+
+// dH[i][n] = sum_j G[i][j] W[n][j]: M = N rows, Nn = d, K = V.
+template <typename TO>
+__global__ __launch_bounds__(256) void mfma_dH_kernel(const uint16_t* __restrict__ R, int64_t ldr,
+                                                      const uint16_t* __restrict__ W, int64_t ldw, int M, int Nn, int K,
+                                                      int kps, Fold f, TO* __restrict__ out, int64_t ldo,
+                                                      float* __restrict__ part) {
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][MB][LDK];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][MB][LDK];
+    const int m0 = blockIdx.y * MB, n0 = blockIdx.x * MB;
+    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
+    const float alpha = f.scal[0];
+    f32x16_t acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    StageK<true> sa;
+    StageK<false> sb;
+    const int nk = (ke - kb + MK - 1) / MK;
+    if (nk > 0) {
+        sa.load(R, ldr, M, m0, kb, ke);
+        sb.load(W, ldw, Nn, n0, kb, ke);
+        sa.store(As[0], M, m0, kb, ke, f, alpha);
+        sb.store(Bs[0], Nn, n0, kb, ke, f, alpha);
+    }
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        const bool more = kt + 1 < nk;
+        const int k0 = kb + (kt + 1) * MK;
+        if (more) {
+            sa.load(R, ldr, M, m0, k0, ke);
+            sb.load(W, ldw, Nn, n0, k0, ke);
+        }
+        mfma_tile(As[buf], Bs[buf], acc);
+        if (more) {
+            sa.store(As[buf ^ 1], M, m0, k0, ke, f, alpha);
+            sb.store(Bs[buf ^ 1], Nn, n0, k0, ke, f, alpha);
+        }
+        __syncthreads();
+    }
+    if (part == nullptr) {
+        for_each_acc(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) stf<TO>(out, (int64_t)m * ldo + n, v);
+        });
+    } else {
+        float* pz = part + (int64_t)blockIdx.z * M * Nn;
+        for_each_acc(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = v;
+        });
+    }
+}
+
+// Split-K reduction in split order: out = sum_z part[z] (+ beta * out for dW).
+template <typename TO>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int splits, int M, int Nn,
+                                                            TO* __restrict__ out, int64_t ldo, float beta) {
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t MN = (int64_t)M * Nn;
+    if (idx >= MN) return;
+    float a = 0.f;
+    for (int z = 0; z < splits; ++z) a += part[(int64_t)z * MN + idx];
+    const int64_t m = idx / Nn, n = idx % Nn;
+    if (beta != 0.f) a += beta * ldf<TO>(out, m * ldo + n);
+    stf<TO>(out, m * ldo + n, a);
+}
+
+// ---- planning ------------------------------------------------------------------------------------
+constexpr int kTargetWGs = 512;   // two waves of workgroups per CU on 256 CUs
+constexpr int kMaxSplits = 8;
+
+int splits_for(int64_t tiles, int64_t K, int ktile) {
+    int s = 1;
+    while (s < kMaxSplits && tiles * s < kTargetWGs && K / (2LL * s) >= 4LL * ktile) s *= 2;
+    return s;
+}
+
+struct Plan {
+    bool mfma;
+    int sw, sh;   // split-K factors of dW and dH
+};
+
+Plan make_plan(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
+    Plan p;
+    p.mfma = dt == BOM_BF16;
+    const int tb = p.mfma ? MB : SB, kt = p.mfma ? MK : SK;
+    const int64_t tw = ((d + tb - 1) / tb) * ((V + tb - 1) / tb);
+    const int64_t th = ((N + tb - 1) / tb) * ((d + tb - 1) / tb);
+    p.sw = splits_for(tw, N, kt);
+    p.sh = splits_for(th, V, kt);
+    return p;
+}
+
+VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
+    const Plan p = make_plan(N, d, V, dt);
+    VjpWs w;
+    w.cq_off = 0;
+    w.vmask_off = align256((size_t)V * 4);
+    w.scal_off = align256(w.vmask_off + (size_t)N * 4);
+    w.part_off = align256(w.scal_off + 16);
+    size_t pw = p.sw > 1 ? (size_t)p.sw * d * V * 4 : 0;
+    size_t ph = p.sh > 1 ? (size_t)p.sh * N * d * 4 : 0;
+    w.total = align256(w.part_off + (pw > ph ? pw : ph));
+    return w;
+}
+
+template <typename TO>
+hipError_t run_dH(const HeadVjpArgs& a, const Plan& p, const Fold& f, float* part, bool mfma_ok, hipStream_t st) {
+    TO* out = static_cast<TO*>(a.dH);
+    const int M = a.N, Nn = a.d, K = a.V;
+    const int tb = mfma_ok ? MB : SB, ktile = mfma_ok ? MK : SK;
+    const int splits = p.sh;
+    int kps = (K + splits - 1) / splits;
+    kps = (kps + ktile - 1) / ktile * ktile;
+    dim3 grid((Nn + tb - 1) / tb, (M + tb - 1) / tb, splits);
+    float* pz = splits > 1 ? part : nullptr;
+    if (mfma_ok) {
+        hipLaunchKernelGGL(mfma_dH_kernel<TO>, grid, dim3(256), 0, st, static_cast<const uint16_t*>(a.R), a.ldr,
+                           static_cast<const uint16_t*>(a.W), a.ldw, M, Nn, K, kps, f, out, a.lddh, pz);
+    } else if (a.dt == BOM_BF16) {
+        hipLaunchKernelGGL((simt_dH_kernel<uint16_t, TO>), grid, dim3(256), 0, st, static_cast<const uint16_t*>(a.R),
+                           a.ldr, static_cast<const uint16_t*>(a.W), a.ldw, M, Nn, K, kps, f, out, a.lddh, part,
+                           splits > 1 ? 0 : 1);
+    } else {
+        hipLaunchKernelGGL((simt_dH_kernel<float, TO>), grid, dim3(256), 0, st, static_cast<const float*>(a.R), a.ldr,
+                           static_cast<const float*>(a.W), a.ldw, M, Nn, K, kps, f, out, a.lddh, part,
+                           splits > 1 ? 0 : 1);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || splits == 1) return e;
+    const int64_t MN = (int64_t)M * Nn;
+    hipLaunchKernelGGL(splitk_reduce_kernel<TO>, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, st, part, splits, M,
+                       Nn, out, a.lddh, 0.f);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt) { return vjp_ws(N, d, V, dt).total; }
+
+hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
+    const VjpWs L = vjp_ws(a.N, a.d, a.V, a.dt);
+    const Plan p = make_plan(a.N, a.d, a.V, a.dt);
+    char* base = static_cast<char*>(a.ws);
+    float* cq = reinterpret_cast<float*>(base + L.cq_off);
+    float* vmask = reinterpret_cast<float*>(base + L.vmask_off);
+    float* scal = reinterpret_cast<float*>(base + L.scal_off);
+    float* part = reinterpret_cast<float*>(base + L.part_off);
+    const int nprep = (a.V > a.N ? a.V : a.N);
+    hipLaunchKernelGGL(vjp_prep_kernel, dim3((nprep + 255) / 256), dim3(256), 0, st, a.q_hat, a.s, a.n_valid, a.lambda,
+                       a.V, a.N, a.labels, a.ignore_index, cq, vmask, scal, a.db);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const Fold f{cq, vmask, scal};
+
+    // The MFMA path stages 16-byte rows: leading dimensions multiples of 8 and 16-byte bases.
+    auto al = [](const void* ptr, int64_t ld) { return reinterpret_cast<uintptr_t>(ptr) % 16 == 0 && ld % 8 == 0; };
+    const bool mfma_ok = p.mfma && al(a.H, a.ldh) && al(a.W, a.ldw) && al(a.R, a.ldr);
+
+    // dW
+    {
+        const int M = a.d, Nn = a.V, K = a.N;
+        const int tb = mfma_ok ? MB : SB, ktile = mfma_ok ? MK : SK;
+        const int splits = p.sw;
+        int kps = (K + splits - 1) / splits;
+        kps = (kps + ktile - 1) / ktile * ktile;
+        dim3 grid((Nn + tb - 1) / tb, (M + tb - 1) / tb, splits);
+        float* pz = splits > 1 ? part : nullptr;
+        if (mfma_ok) {
+            hipLaunchKernelGGL(mfma_dW_kernel, grid, dim3(256), 0, st, static_cast<const uint16_t*>(a.H), a.ldh,
+                               static_cast<const uint16_t*>(a.R), a.ldr, M, Nn, K, kps, f, a.dW, a.lddw, a.dW_beta, pz);
+        } else if (a.dt == BOM_BF16) {
+            hipLaunchKernelGGL(simt_dW_kernel<uint16_t>, grid, dim3(256), 0, st, static_cast<const uint16_t*>(a.H), a.ldh,
+                               static_cast<const uint16_t*>(a.R), a.ldr, M, Nn, K, kps, f, splits > 1 ? part : a.dW,
+                               a.lddw, a.dW_beta, splits > 1 ? 0 : 1);
+        } else {
+            hipLaunchKernelGGL(simt_dW_kernel<float>, grid, dim3(256), 0, st, static_cast<const float*>(a.H), a.ldh,
+                               static_cast<const float*>(a.R), a.ldr, M, Nn, K, kps, f, splits > 1 ? part : a.dW, a.lddw,
+                               a.dW_beta, splits > 1 ? 0 : 1);
+        }
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        if (splits > 1) {
+            const int64_t MN = (int64_t)M * Nn;
+            hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, st, part,
+                               splits, M, Nn, a.dW, a.lddw, a.dW_beta);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+    }
+    // dH (shares the split-K buffer: same stream, so it runs after the dW reduction)
+    if (a.dH) {
+        if (a.dh_dt == BOM_BF16) return run_dH<uint16_t>(a, p, f, part, mfma_ok, st);
+        return run_dH<float>(a, p, f, part, mfma_ok, st);
+    }
+    return hipSuccess;
+}
+
+// ---- head forward (support): Z = H W + b, fp32 SIMT ------------------------------------------------
+namespace {
+__global__ __launch_bounds__(256) void head_forward_f32_kernel(const float* __restrict__ H, int64_t ldh,
+                                                               const float* __restrict__ W, int64_t ldw,
+                                                               const float* __restrict__ b, int N, int d, int V,
+                                                               float* __restrict__ Z, int64_t ldz) {
+    __shared__ float As[SK][SB + 4];
+    __shared__ float Bs[SK][SB + 4];
+    const int t = threadIdx.x, tx = t % 16, ty = t / 16;
+    const int m0 = blockIdx.y * SB, n0 = blockIdx.x * SB;
+    float acc[4][4] = {};
+    for (int k0 = 0; k0 < d; k0 += SK) {
+        for (int e = 0; e < 4; ++e) {
+            const int idx = e * 256 + t;
+            const int rr = idx / SK, kk = idx % SK;
+            As[kk][rr] = (k0 + kk < d && m0 + rr < N) ? H[(int64_t)(m0 + rr) * ldh + k0 + kk] : 0.f;
+            const int kk2 = idx / SB, cc = idx % SB;
+            Bs[kk2][cc] = (k0 + kk2 < d && n0 + cc < V) ? W[(int64_t)(k0 + kk2) * ldw + n0 + cc] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < SK; ++kk) {
+            float a4[4], b4[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a4[i] = As[kk][ty * 4 + i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) b4[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a4[i], b4[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+    for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) {
+            const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+            if (m < N && n < V) Z[(int64_t)m * ldz + n] = acc[i][j] + (b ? b[n] : 0.f);
+        }
+}
+}  // namespace
+
+hipError_t launch_head_forward_f32(const float* H, int64_t ldh, const float* W, int64_t ldw, const float* b, int N,
+                                   int d, int V, float* Z, int64_t ldz, hipStream_t st) {
+    dim3 grid((V + SB - 1) / SB, (N + SB - 1) / SB);
+    hipLaunchKernelGGL(head_forward_f32_kernel, grid, dim3(256), 0, st, H, ldh, W, ldw, b, N, d, V, Z, ldz);
+    return hipGetLastError();
+}
+
+}  // namespace bom

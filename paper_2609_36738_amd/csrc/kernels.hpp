@@ -1,0 +1,64 @@
+// Internal launch interface between the C-ABI layer (abi.hip) and the kernel files.
+// Every launcher assumes its arguments were validated by the C-ABI layer.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "bom.h"
+
+namespace bom {
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ---- residual ------------------------------------------------------------------------------
+size_t residual_workspace_bytes(int64_t N, int64_t V, bom_dtype dt);
+hipError_t launch_residual(const void* Z, bom_dtype dt, int N, int V, int64_t ldz, const int32_t* labels,
+                           int32_t ignore_index, float* s, float* row_lse, int32_t* row_argmax, float* row_target,
+                           void* R, int64_t ldr, float* loss, int32_t* n_valid, int32_t* flags, void* ws,
+                           hipStream_t stream);
+
+// ---- EMA -----------------------------------------------------------------------------------
+hipError_t launch_ema(float* q, const float* s, int64_t V, float beta1, float inv_bc1, float* q_hat,
+                      hipStream_t stream);
+
+// ---- head VJP --------------------------------------------------------------------------------
+struct HeadVjpArgs {
+    const void* H; int64_t ldh;
+    const void* W; int64_t ldw;
+    const void* R; int64_t ldr;
+    bom_dtype dt;
+    int N, d, V;
+    const int32_t* labels; int32_t ignore_index;
+    const float* q_hat; const float* s; const int32_t* n_valid; float lambda;
+    float* dW; int64_t lddw; float dW_beta;
+    float* db;
+    void* dH; bom_dtype dh_dt; int64_t lddh;
+    void* ws; size_t ws_bytes;
+};
+size_t head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt);
+hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t stream);
+
+// ---- head forward (support) ---------------------------------------------------------------
+hipError_t launch_head_forward_f32(const float* H, int64_t ldh, const float* W, int64_t ldw, const float* b, int N,
+                                   int d, int V, float* Z, int64_t ldz, hipStream_t stream);
+
+// ---- update ----------------------------------------------------------------------------------
+struct SegTable {
+    int n;
+    int64_t begin[BOM_MAX_SEGMENTS];
+    int64_t end[BOM_MAX_SEGMENTS];
+    float wd[BOM_MAX_SEGMENTS];
+    float wd_default;
+};
+struct UpdateScalars {
+    float lr, beta2, one_minus_beta2, eps, lambda, u_scale, inv_bc2;
+};
+size_t update_workspace_bytes(int64_t P, const bom_update_cfg* cfg);
+hipError_t launch_update_dense(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
+                               const UpdateScalars& sc, hipStream_t stream);
+hipError_t launch_update_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P,
+                                  int64_t block_rows, int64_t block_cols, const SegTable& segs,
+                                  const UpdateScalars& sc, void* ws, hipStream_t stream);
+
+}  // namespace bom

@@ -1,0 +1,580 @@
+// bom_residual kernels: per-row softmax statistics, the residual rows R = softmax(Z) - onehot(y)
+// and the batch-mean residual s over the valid rows (Algorithm 1, the s_t line; Sec. 3.2; the
+// token-level appendix for ignored targets).
+//
+// Two paths, both deterministic (fixed reduction orders, no floating-point atomics):
+//  * single pass (V up to ~53k bf16 / ~26k fp32): one persistent workgroup per CU keeps a whole
+//    row in registers, reduces max / argmax / sum across the workgroup, writes R, and accumulates
+//    its rows' residuals per column in registers; Z is read from HBM exactly once.
+//  * two pass (larger V): a stats kernel (one wave per row, online max / sum / argmax) writes the
+//    row statistics, then a column-slab kernel re-reads Z, writes R and accumulates per-column
+//    partials for blocks of rows.
+// A finish step sums the per-workgroup partials in a fixed order into s, loss, N_t and flags.
+#include <climits>
+#include <cmath>
+
+#include "common.hpp"
+#include "kernels.hpp"
+#include "vec_io.hpp"
+
+namespace bom {
+namespace {
+
+constexpr int kSingleMaxWG = 256;     // persistent workgroups of the single pass (one per CU)
+constexpr int kStatsRowsPerWG = 4;    // two pass, stats: one wave per row, 4 waves per workgroup
+constexpr int kColsThreads = 256;     // two pass, columns: threads per workgroup
+constexpr int kColsCPT = 8;           // two pass, columns: chunks per thread
+constexpr int kColsRowBlock = 256;    // two pass, columns: rows per partial-sum block
+
+struct Partials {
+    float* part;      // [nparts][V] per-workgroup column sums of residual rows
+    int* wg_count;    // [nwg] valid rows
+    int* wg_flags;    // [nwg] BOM_FLAG_LABEL_RANGE bits
+    double* wg_loss;  // [nwg] sum of per-row cross-entropy
+    float* inv_nt;    // [1] 1 / N_t (0 when N_t = 0)
+};
+
+struct WsLayout {
+    size_t part_off, count_off, flags_off, loss_off, inv_off, total;
+};
+
+WsLayout ws_layout(int64_t N, int64_t V) {
+    int64_t nwg1 = N < kSingleMaxWG ? N : kSingleMaxWG;
+    int64_t nstats = (N + kStatsRowsPerWG - 1) / kStatsRowsPerWG;
+    int64_t nrb = (N + kColsRowBlock - 1) / kColsRowBlock;
+    int64_t nparts = nwg1 > nrb ? nwg1 : nrb;
+    int64_t nwg = nwg1 > nstats ? nwg1 : nstats;
+    WsLayout L;
+    L.part_off = 0;
+    L.count_off = align256(L.part_off + (size_t)nparts * (size_t)V * sizeof(float));
+    L.flags_off = align256(L.count_off + (size_t)nwg * sizeof(int));
+    L.loss_off = align256(L.flags_off + (size_t)nwg * sizeof(int));
+    L.inv_off = align256(L.loss_off + (size_t)nwg * sizeof(double));
+    L.total = align256(L.inv_off + sizeof(float));
+    return L;
+}
+
+template <int NW>
+__device__ __forceinline__ float block_max(float v, float* sh) {
+    v = wave_max(v);
+    if ((threadIdx.x & (kWave - 1)) == 0) sh[threadIdx.x / kWave] = v;
+    __syncthreads();
+    float r = sh[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) r = fmaxf(r, sh[w]);
+    return r;
+}
+template <int NW>
+__device__ __forceinline__ float block_sum(float v, float* sh) {
+    v = wave_sum(v);
+    if ((threadIdx.x & (kWave - 1)) == 0) sh[threadIdx.x / kWave] = v;
+    __syncthreads();
+    float r = sh[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) r += sh[w];
+    return r;
+}
+template <int NW>
+__device__ __forceinline__ int block_min(int v, int* sh) {
+    v = wave_min(v);
+    if ((threadIdx.x & (kWave - 1)) == 0) sh[threadIdx.x / kWave] = v;
+    __syncthreads();
+    int r = sh[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) r = min(r, sh[w]);
+    return r;
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_f32_chunk(float* row, int col, int V, const float* x) {
+    if (col < V) {
+        if (VEC % 4 == 0) {
+#pragma unroll
+            for (int k = 0; k < VEC; k += 4) VecIO<float, 4>::store(row + col + k, x + k);
+        } else {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) row[col + k] = x[k];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Single pass. Thread `tid` owns columns (c * THREADS + tid) * VEC + k, c < NCH, k < VEC.
+// PACKED (bf16 only, for wide rows): the row stays as raw bf16 pairs and exp is evaluated twice
+// (once for the sum, once for p); otherwise e = exp(z - m) is kept in fp32 registers.
+template <typename T, int THREADS, int VEC, int NCH, bool PACKED>
+__global__ __launch_bounds__(THREADS) void residual_rows_kernel(
+    const T* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
+    float* __restrict__ row_lse, int32_t* __restrict__ row_argmax, float* __restrict__ row_target,
+    T* __restrict__ R, int64_t ldr, int rows_per_wg, Partials ws) {
+    constexpr int NW = THREADS / kWave;
+    constexpr int VPT = NCH * VEC;
+    constexpr int NXW = PACKED ? VPT / 2 : 1;  // raw bf16 pairs (PACKED)
+    constexpr int NXF = PACKED ? 1 : VPT;      // fp32 values (otherwise)
+    static_assert(!PACKED || (VEC == 8), "packed rows need 16-byte bf16 chunks");
+    __shared__ float sh_max[NW];
+    __shared__ int sh_idx[NW];
+    __shared__ float sh_sum[NW];
+    const int tid = threadIdx.x;
+
+    float acc[VPT];
+#pragma unroll
+    for (int k = 0; k < VPT; ++k) acc[k] = 0.f;
+
+    const int row0 = blockIdx.x * rows_per_wg;
+    const int row1 = min(row0 + rows_per_wg, N);
+    int cnt = 0;
+    double ce = 0.0;
+    bool bad = false;
+
+    for (int i = row0; i < row1; ++i) {
+        const T* zr = Z + (int64_t)i * ldz;
+        float x[NXF];
+        uint32_t xw[NXW];
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int col = (c * THREADS + tid) * VEC;
+            if constexpr (PACKED) {
+                if (col < V) {
+                    const uint4 u = *reinterpret_cast<const uint4*>(zr + col);
+                    xw[c * 4 + 0] = u.x; xw[c * 4 + 1] = u.y; xw[c * 4 + 2] = u.z; xw[c * 4 + 3] = u.w;
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) xw[c * 4 + k] = 0xFF80FF80u;  // a pair of bf16 -inf
+                }
+            } else {
+                load_chunk<T, VEC>(zr, col, V, -INFINITY, &x[c * VEC]);
+            }
+        }
+        auto val = [&](int k) -> float {
+            if constexpr (PACKED) return (k & 1) ? bf16_hi(xw[k >> 1]) : bf16_lo(xw[k >> 1]);
+            else return x[k];
+        };
+
+        // max, then the lowest column attaining it
+        float tm = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < VPT; ++k) tm = fmaxf(tm, val(k));
+        const float m = block_max<NW>(tm, sh_max);
+        int ti = INT_MAX;
+        if (tm == m) {
+#pragma unroll
+            for (int c = NCH - 1; c >= 0; --c)
+#pragma unroll
+                for (int k = VEC - 1; k >= 0; --k)
+                    if (val(c * VEC + k) == m) ti = (c * THREADS + tid) * VEC + k;
+        }
+        const int am = block_min<NW>(ti, sh_idx);
+        if constexpr (PACKED) {
+            // keep the row packed: stop the compiler from caching unpacked values across passes
+#pragma unroll
+            for (int k = 0; k < NXW; ++k) asm volatile("" : "+v"(xw[k]));
+        }
+
+        // l = sum exp(z - m)
+        const float m2 = m * kLog2e;
+        float l = 0.f;
+        if constexpr (PACKED) {
+#pragma unroll
+            for (int k = 0; k < VPT; ++k) l += exp2_fast(fmaf(val(k), kLog2e, -m2));
+        } else {
+#pragma unroll
+            for (int k = 0; k < VPT; ++k) {
+                x[k] = exp2_fast(fmaf(x[k], kLog2e, -m2));
+                l += x[k];
+            }
+        }
+        l = block_sum<NW>(l, sh_sum);
+        const float lse = m + logf(l);
+        if constexpr (PACKED) {
+#pragma unroll
+            for (int k = 0; k < NXW; ++k) asm volatile("" : "+v"(xw[k]));
+        }
+
+        const int y = labels[i];
+        bool rbad = false;
+        const bool valid = label_valid(y, V, ignore_index, &rbad);
+        bad |= rbad;
+        T* rr = R ? R + (int64_t)i * ldr : nullptr;
+        if (valid) {
+            // the label column is owned by exactly one thread: subtract the one-hot there
+            const int yv = y / VEC;
+            const int slot = (yv % THREADS == tid) ? (yv / THREADS) * VEC + (y % VEC) : -1;
+            const float inv_l = 1.0f / l;
+            const float lse2 = lse * kLog2e;
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                float p[VEC];
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    if constexpr (PACKED) p[k] = exp2_fast(fmaf(val(c * VEC + k), kLog2e, -lse2));
+                    else p[k] = x[c * VEC + k] * inv_l;
+                }
+                if (slot >= 0) {
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k)
+                        if (c * VEC + k == slot) p[k] -= 1.0f;
+                }
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) acc[c * VEC + k] += p[k];
+                if (rr) store_chunk<T, VEC>(rr, (c * THREADS + tid) * VEC, V, p);
+            }
+        } else if (rr) {
+            float zero[VEC];
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) zero[k] = 0.f;
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) store_chunk<T, VEC>(rr, (c * THREADS + tid) * VEC, V, zero);
+        }
+        if (tid == 0) {
+            row_lse[i] = lse;
+            if (row_argmax) row_argmax[i] = am;
+            const float zt = valid ? load_scalar<T>(zr + y) : 0.f;
+            if (row_target) row_target[i] = zt;
+            if (valid) {
+                ++cnt;
+                ce += (double)lse - (double)zt;
+            }
+        }
+    }
+
+    float* prow = ws.part + (int64_t)blockIdx.x * V;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) store_f32_chunk<VEC>(prow, (c * THREADS + tid) * VEC, V, &acc[c * VEC]);
+    if (tid == 0) {
+        ws.wg_count[blockIdx.x] = cnt;
+        ws.wg_loss[blockIdx.x] = ce;
+        ws.wg_flags[blockIdx.x] = bad ? BOM_FLAG_LABEL_RANGE : 0;
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Two pass, stats: one wave per row, online (max, sum, argmax) per lane, then a butterfly merge.
+template <typename T, int VEC, int UNROLL>
+__global__ __launch_bounds__(kStatsRowsPerWG * kWave) void residual_stats_kernel(
+    const T* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
+    float* __restrict__ row_lse, int32_t* __restrict__ row_argmax, float* __restrict__ row_target, Partials ws) {
+    constexpr int STEP = kWave * VEC * UNROLL;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int i = blockIdx.x * kStatsRowsPerWG + wave;
+    float m = -INFINITY, l = 0.f;
+    int idx = INT_MAX;
+    if (i < N) {
+        const T* zr = Z + (int64_t)i * ldz;
+        for (int base = 0; base < V; base += STEP) {
+            float x[UNROLL * VEC];
+#pragma unroll
+            for (int u = 0; u < UNROLL; ++u) load_chunk<T, VEC>(zr, base + (u * kWave + lane) * VEC, V, -INFINITY, &x[u * VEC]);
+            float cm = -INFINITY;
+#pragma unroll
+            for (int k = 0; k < UNROLL * VEC; ++k) cm = fmaxf(cm, x[k]);
+            if (cm > m) {
+                int ci = INT_MAX;
+#pragma unroll
+                for (int u = UNROLL - 1; u >= 0; --u)
+#pragma unroll
+                    for (int k = VEC - 1; k >= 0; --k)
+                        if (x[u * VEC + k] == cm) ci = base + (u * kWave + lane) * VEC + k;
+                l = (m == -INFINITY) ? 0.f : l * exp2_fast((m - cm) * kLog2e);
+                m = cm;
+                idx = ci;
+            }
+            if (m != -INFINITY) {  // a lane that has only seen padding keeps l = 0
+                const float m2 = m * kLog2e;
+#pragma unroll
+                for (int k = 0; k < UNROLL * VEC; ++k) l += exp2_fast(fmaf(x[k], kLog2e, -m2));
+            }
+        }
+    }
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const float mo = __shfl_xor(m, o, kWave);
+        const float lo = __shfl_xor(l, o, kWave);
+        const int io = __shfl_xor(idx, o, kWave);
+        const float mn = fmaxf(m, mo);
+        const float a = (m == -INFINITY) ? 0.f : l * exp2_fast((m - mn) * kLog2e);
+        const float b = (mo == -INFINITY) ? 0.f : lo * exp2_fast((mo - mn) * kLog2e);
+        l = a + b;
+        idx = (m > mo) ? idx : (mo > m ? io : min(idx, io));
+        m = mn;
+    }
+    __shared__ int sh_cnt[kStatsRowsPerWG];
+    __shared__ int sh_bad[kStatsRowsPerWG];
+    __shared__ double sh_ce[kStatsRowsPerWG];
+    if (lane == 0) {
+        int c = 0, bd = 0;
+        double e = 0.0;
+        if (i < N) {
+            const float lse = m + logf(l);
+            const int y = labels[i];
+            bool rbad = false;
+            const bool valid = label_valid(y, V, ignore_index, &rbad);
+            const float zt = valid ? load_scalar<T>(Z + (int64_t)i * ldz + y) : 0.f;
+            row_lse[i] = lse;
+            if (row_argmax) row_argmax[i] = idx;
+            if (row_target) row_target[i] = zt;
+            c = valid ? 1 : 0;
+            bd = rbad ? 1 : 0;
+            e = valid ? (double)lse - (double)zt : 0.0;
+        }
+        sh_cnt[wave] = c;
+        sh_bad[wave] = bd;
+        sh_ce[wave] = e;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int c = 0, bd = 0;
+        double e = 0.0;
+        for (int w = 0; w < kStatsRowsPerWG; ++w) {
+            c += sh_cnt[w];
+            bd |= sh_bad[w];
+            e += sh_ce[w];
+        }
+        ws.wg_count[blockIdx.x] = c;
+        ws.wg_loss[blockIdx.x] = e;
+        ws.wg_flags[blockIdx.x] = bd ? BOM_FLAG_LABEL_RANGE : 0;
+    }
+}
+
+// Two pass, columns: workgroup (cb, rb) owns columns col0 + (c * THREADS + tid) * VEC + k and rows
+// [rb * kColsRowBlock, ...); p = exp(z - lse) with the stats kernel's lse.
+template <typename T, int VEC>
+__global__ __launch_bounds__(kColsThreads) void residual_cols_kernel(
+    const T* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
+    const float* __restrict__ row_lse, T* __restrict__ R, int64_t ldr, float* __restrict__ part) {
+    constexpr int VPT = kColsCPT * VEC;
+    constexpr int SLAB = kColsThreads * VPT;
+    const int tid = threadIdx.x;
+    const int nslab = (V + SLAB - 1) / SLAB;
+    const int cb = blockIdx.x % nslab, rb = blockIdx.x / nslab;
+    const int col0 = cb * SLAB;
+    const int r0 = rb * kColsRowBlock;
+    const int r1 = min(N, r0 + kColsRowBlock);
+    float acc[VPT];
+#pragma unroll
+    for (int k = 0; k < VPT; ++k) acc[k] = 0.f;
+    for (int i = r0; i < r1; ++i) {
+        const int y = labels[i];
+        bool rbad = false;
+        const bool valid = label_valid(y, V, ignore_index, &rbad);
+        T* rr = R ? R + (int64_t)i * ldr : nullptr;
+        if (!valid) {
+            if (rr) {
+                float zero[VEC];
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) zero[k] = 0.f;
+#pragma unroll
+                for (int c = 0; c < kColsCPT; ++c) store_chunk<T, VEC>(rr, col0 + (c * kColsThreads + tid) * VEC, V, zero);
+            }
+            continue;
+        }
+        const T* zr = Z + (int64_t)i * ldz;
+        const float lse2 = row_lse[i] * kLog2e;
+        float x[VPT];
+#pragma unroll
+        for (int c = 0; c < kColsCPT; ++c) load_chunk<T, VEC>(zr, col0 + (c * kColsThreads + tid) * VEC, V, -INFINITY, &x[c * VEC]);
+#pragma unroll
+        for (int k = 0; k < VPT; ++k) x[k] = exp2_fast(fmaf(x[k], kLog2e, -lse2));
+        const int yl = y - col0;
+        if (yl >= 0 && yl < SLAB && (yl / VEC) % kColsThreads == tid) {
+            const int slot = ((yl / VEC) / kColsThreads) * VEC + (yl % VEC);
+#pragma unroll
+            for (int k = 0; k < VPT; ++k)
+                if (k == slot) x[k] -= 1.0f;
+        }
+#pragma unroll
+        for (int k = 0; k < VPT; ++k) acc[k] += x[k];
+        if (rr) {
+#pragma unroll
+            for (int c = 0; c < kColsCPT; ++c) store_chunk<T, VEC>(rr, col0 + (c * kColsThreads + tid) * VEC, V, &x[c * VEC]);
+        }
+    }
+    float* prow = part + (int64_t)rb * V;
+#pragma unroll
+    for (int c = 0; c < kColsCPT; ++c) store_f32_chunk<VEC>(prow, col0 + (c * kColsThreads + tid) * VEC, V, &acc[c * VEC]);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Finish: N_t, loss and flags (one workgroup), then s = (sum of partials) / N_t.
+__global__ __launch_bounds__(256) void residual_finish_scalars_kernel(int nwg, Partials ws, float* loss,
+                                                                      int32_t* n_valid, int32_t* flags) {
+    __shared__ int sh_c[256];
+    __shared__ int sh_f[256];
+    __shared__ double sh_l[256];
+    int c = 0, f = 0;
+    double e = 0.0;
+    for (int w = threadIdx.x; w < nwg; w += 256) {
+        c += ws.wg_count[w];
+        f |= ws.wg_flags[w];
+        e += ws.wg_loss[w];
+    }
+    sh_c[threadIdx.x] = c;
+    sh_f[threadIdx.x] = f;
+    sh_l[threadIdx.x] = e;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (threadIdx.x < o) {
+            sh_c[threadIdx.x] += sh_c[threadIdx.x + o];
+            sh_f[threadIdx.x] |= sh_f[threadIdx.x + o];
+            sh_l[threadIdx.x] += sh_l[threadIdx.x + o];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const int nt = sh_c[0];
+        *n_valid = nt;
+        *flags = sh_f[0] | (nt == 0 ? BOM_FLAG_EMPTY : 0);
+        *loss = nt > 0 ? (float)(sh_l[0] / (double)nt) : 0.f;
+        *ws.inv_nt = nt > 0 ? (float)(1.0 / (double)nt) : 0.f;
+    }
+}
+
+__global__ __launch_bounds__(256) void residual_finish_s_kernel(const float* __restrict__ part, int nparts, int V,
+                                                                const float* __restrict__ inv_nt, float* __restrict__ s) {
+    const int j = blockIdx.x * 256 + threadIdx.x;
+    if (j >= V) return;
+    float a = 0.f;
+    int w = 0;
+    for (; w + 4 <= nparts; w += 4) {
+        const float p0 = part[(int64_t)(w + 0) * V + j];
+        const float p1 = part[(int64_t)(w + 1) * V + j];
+        const float p2 = part[(int64_t)(w + 2) * V + j];
+        const float p3 = part[(int64_t)(w + 3) * V + j];
+        a += p0;
+        a += p1;
+        a += p2;
+        a += p3;
+    }
+    for (; w < nparts; ++w) a += part[(int64_t)w * V + j];
+    s[j] = a * *inv_nt;
+}
+
+// ---------------------------------------------------------------------------------------------
+template <typename T, int THREADS, int VEC, int NCH>
+hipError_t launch_rows(const T* Z, int64_t ldz, int N, int V, const int32_t* labels, int32_t ignore_index, float* row_lse,
+                       int32_t* row_argmax, float* row_target, T* R, int64_t ldr, Partials ws, int* nwg_out,
+                       hipStream_t stream) {
+    int nwg = N < kSingleMaxWG ? N : kSingleMaxWG;
+    const int rpw = (N + nwg - 1) / nwg;
+    nwg = (N + rpw - 1) / rpw;
+    *nwg_out = nwg;
+    // bf16 rows wider than 8 chunks keep raw pairs (registers: acc + packed row) instead of fp32 e
+    constexpr bool kPacked = (VEC == 8) && (NCH > 8);
+    hipLaunchKernelGGL((residual_rows_kernel<T, THREADS, VEC, NCH, kPacked>), dim3(nwg), dim3(THREADS), 0, stream, Z,
+                       ldz, N, V, labels, ignore_index, row_lse, row_argmax, row_target, R, ldr, rpw, ws);
+    return hipGetLastError();
+}
+
+// Allowed chunk counts for 512-thread single-pass workgroups (registers: 2 * NCH * VEC floats).
+constexpr int kNchSet[] = {1, 2, 3, 4, 6, 8, 10, 13};
+
+template <typename T, int VEC>
+hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, int V, const int32_t* labels,
+                         int32_t ig, float* lse, int32_t* am, float* tg, T* R, int64_t ldr, Partials ws, int* nwg,
+                         hipStream_t st) {
+#define BOM_ROWS(TH, NC) launch_rows<T, TH, VEC, NC>(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, nwg, st)
+    if (threads == 64) return BOM_ROWS(64, 1);
+    if (threads == 128) return BOM_ROWS(128, 1);
+    if (threads == 256) return BOM_ROWS(256, 1);
+    switch (nch) {
+        case 1: return BOM_ROWS(512, 1);
+        case 2: return BOM_ROWS(512, 2);
+        case 3: return BOM_ROWS(512, 3);
+        case 4: return BOM_ROWS(512, 4);
+        case 6: return BOM_ROWS(512, 6);
+        case 8: return BOM_ROWS(512, 8);
+        case 10: return BOM_ROWS(512, 10);
+        case 13: return BOM_ROWS(512, 13);
+        default: return hipErrorInvalidValue;
+    }
+#undef BOM_ROWS
+}
+
+// Single-pass plan for VEC-wide chunks: returns false when a row does not fit in registers.
+bool plan_single(int V, int VEC, int* threads, int* nch) {
+    const int slots = (V + VEC - 1) / VEC;
+    int th = 64;
+    while (th < slots && th < 512) th *= 2;
+    const int need = (slots + th - 1) / th;
+    if (th < 512) {
+        *threads = th;
+        *nch = 1;
+        return true;
+    }
+    const int max_nch = (VEC == 1) ? 8 : 13;
+    for (int c : kNchSet) {
+        if (c >= need && c <= max_nch) {
+            *threads = 512;
+            *nch = c;
+            return true;
+        }
+    }
+    return false;
+}
+
+template <typename T, int VEC>
+hipError_t run_residual(const T* Z, int N, int V, int64_t ldz, const int32_t* labels, int32_t ig, float* s, float* lse,
+                        int32_t* am, float* tg, T* R, int64_t ldr, float* loss, int32_t* n_valid, int32_t* flags,
+                        Partials ws, hipStream_t st) {
+    int threads = 0, nch = 0, nwg = 0, nparts = 0;
+    hipError_t e;
+    if (plan_single(V, VEC, &threads, &nch)) {
+        e = dispatch_rows<T, VEC>(nch, threads, Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, &nwg, st);
+        nparts = nwg;
+    } else {
+        nwg = (N + kStatsRowsPerWG - 1) / kStatsRowsPerWG;
+        constexpr int UNROLL = VEC == 1 ? 8 : 4;
+        hipLaunchKernelGGL((residual_stats_kernel<T, VEC, UNROLL>), dim3(nwg), dim3(kStatsRowsPerWG * kWave), 0, st, Z,
+                           ldz, N, V, labels, ig, lse, am, tg, ws);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int slab = kColsThreads * kColsCPT * VEC;
+        nparts = (N + kColsRowBlock - 1) / kColsRowBlock;
+        dim3 grid((unsigned)(((V + slab - 1) / slab) * nparts));
+        hipLaunchKernelGGL((residual_cols_kernel<T, VEC>), grid, dim3(kColsThreads), 0, st, Z, ldz, N, V, labels, ig,
+                           lse, R, ldr, ws.part);
+        e = hipGetLastError();
+    }
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(residual_finish_scalars_kernel, dim3(1), dim3(256), 0, st, nwg, ws, loss, n_valid, flags);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(residual_finish_s_kernel, dim3((V + 255) / 256), dim3(256), 0, st, ws.part, nparts, V,
+                       ws.inv_nt, s);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t residual_workspace_bytes(int64_t N, int64_t V, bom_dtype) { return ws_layout(N, V).total; }
+
+hipError_t launch_residual(const void* Z, bom_dtype dt, int N, int V, int64_t ldz, const int32_t* labels,
+                           int32_t ignore_index, float* s, float* row_lse, int32_t* row_argmax, float* row_target,
+                           void* R, int64_t ldr, float* loss, int32_t* n_valid, int32_t* flags, void* wsp,
+                           hipStream_t stream) {
+    const WsLayout L = ws_layout(N, V);
+    char* base = static_cast<char*>(wsp);
+    Partials ws{reinterpret_cast<float*>(base + L.part_off), reinterpret_cast<int*>(base + L.count_off),
+                reinterpret_cast<int*>(base + L.flags_off), reinterpret_cast<double*>(base + L.loss_off),
+                reinterpret_cast<float*>(base + L.inv_off)};
+    const int vw = dt == BOM_BF16 ? 8 : 4;
+    const bool vec_ok = (ldz % vw == 0) && (reinterpret_cast<uintptr_t>(Z) % 16 == 0) &&
+                        (R == nullptr || ((ldr % vw == 0) && reinterpret_cast<uintptr_t>(R) % 16 == 0)) &&
+                        (V % vw == 0);
+    if (dt == BOM_BF16) {
+        const uint16_t* z = static_cast<const uint16_t*>(Z);
+        uint16_t* r = static_cast<uint16_t*>(R);
+        return vec_ok ? run_residual<uint16_t, 8>(z, N, V, ldz, labels, ignore_index, s, row_lse, row_argmax, row_target,
+                                                  r, ldr, loss, n_valid, flags, ws, stream)
+                      : run_residual<uint16_t, 1>(z, N, V, ldz, labels, ignore_index, s, row_lse, row_argmax, row_target,
+                                                  r, ldr, loss, n_valid, flags, ws, stream);
+    }
+    const float* z = static_cast<const float*>(Z);
+    float* r = static_cast<float*>(R);
+    return vec_ok ? run_residual<float, 4>(z, N, V, ldz, labels, ignore_index, s, row_lse, row_argmax, row_target, r,
+                                           ldr, loss, n_valid, flags, ws, stream)
+                  : run_residual<float, 1>(z, N, V, ldz, labels, ignore_index, s, row_lse, row_argmax, row_target, r,
+                                           ldr, loss, n_valid, flags, ws, stream);
+}
+
+}  // namespace bom

@@ -1,0 +1,302 @@
+// bom_update kernels: second moment of the BOM numerator and the decoupled-decay update over one
+// flat fp32 parameter buffer (Sec. 3.4; the last two lines of Algorithm 1). There is no first
+// moment: 20 bytes per parameter (read theta, v, u; write theta, v), 24 with a split numerator.
+//
+// Factored layout (a reading; the paper does not define one): the buffer is a row-major matrix of
+// block_cols columns grouped into blocks of block_rows rows; v_hat_ij = Rr_i Cc_j / sum(Rr) / bc2.
+// Three launches: row/column statistics of u'^2 (one read of u), a per-block finish (Cc and the
+// block sum of Rr), and the parameter update (one more read of u, read + write of theta).
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace bom {
+namespace {
+
+constexpr int kUpdThreads = 256;
+constexpr int kFacRowsPerWG = 64;   // rows of u per statistics workgroup (inside one block)
+constexpr int kFacUpdRows = 8;      // rows per update workgroup
+
+__device__ __forceinline__ float decay_of(int64_t e, const SegTable& t) {
+    float wd = t.wd_default;
+    for (int k = t.n - 1; k >= 0; --k)
+        if (e >= t.begin[k] && e < t.end[k]) wd = t.wd[k];
+    return wd;
+}
+
+template <bool SPLIT>
+__device__ __forceinline__ float numerator(float u, float h, const UpdateScalars& sc) {
+    if (SPLIT) return sc.u_scale * ((1.0f - sc.lambda) * u + sc.lambda * h);
+    return sc.u_scale * u;
+}
+
+__device__ __forceinline__ void adam_style(float& th, float& v, float up, float wd, const UpdateScalars& sc) {
+    v = sc.beta2 * v + sc.one_minus_beta2 * (up * up);
+    const float vhat = v * sc.inv_bc2;
+    th = (1.0f - sc.lr * wd) * th - sc.lr * (up / (sqrtf(vhat) + sc.eps));
+}
+
+// ---- dense ---------------------------------------------------------------------------------
+template <bool SPLIT>
+__global__ __launch_bounds__(kUpdThreads) void update_dense_vec4_kernel(float* __restrict__ theta, float* __restrict__ v,
+                                                                        const float* __restrict__ u,
+                                                                        const float* __restrict__ h, int64_t nvec,
+                                                                        SegTable segs, UpdateScalars sc) {
+    const int64_t stride = (int64_t)gridDim.x * kUpdThreads;
+    for (int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x; q < nvec; q += stride) {
+        float4 t4 = reinterpret_cast<const float4*>(theta)[q];
+        float4 v4 = reinterpret_cast<const float4*>(v)[q];
+        const float4 u4 = reinterpret_cast<const float4*>(u)[q];
+        float4 h4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (SPLIT) h4 = reinterpret_cast<const float4*>(h)[q];
+        const int64_t e = q * 4;
+        adam_style(t4.x, v4.x, numerator<SPLIT>(u4.x, h4.x, sc), decay_of(e + 0, segs), sc);
+        adam_style(t4.y, v4.y, numerator<SPLIT>(u4.y, h4.y, sc), decay_of(e + 1, segs), sc);
+        adam_style(t4.z, v4.z, numerator<SPLIT>(u4.z, h4.z, sc), decay_of(e + 2, segs), sc);
+        adam_style(t4.w, v4.w, numerator<SPLIT>(u4.w, h4.w, sc), decay_of(e + 3, segs), sc);
+        reinterpret_cast<float4*>(theta)[q] = t4;
+        reinterpret_cast<float4*>(v)[q] = v4;
+    }
+}
+
+template <bool SPLIT>
+__global__ __launch_bounds__(kUpdThreads) void update_dense_scalar_kernel(float* __restrict__ theta, float* __restrict__ v,
+                                                                          const float* __restrict__ u,
+                                                                          const float* __restrict__ h, int64_t begin,
+                                                                          int64_t end, SegTable segs, UpdateScalars sc) {
+    const int64_t stride = (int64_t)gridDim.x * kUpdThreads;
+    for (int64_t e = begin + (int64_t)blockIdx.x * kUpdThreads + threadIdx.x; e < end; e += stride) {
+        float t = theta[e], vv = v[e];
+        adam_style(t, vv, numerator<SPLIT>(u[e], SPLIT ? h[e] : 0.f, sc), decay_of(e, segs), sc);
+        theta[e] = t;
+        v[e] = vv;
+    }
+}
+
+// ---- factored --------------------------------------------------------------------------------
+// Statistics: workgroup w covers rows [r0, r1) of one block; thread t owns columns (k*256 + t)*4..+3.
+template <bool SPLIT, int KC>
+__global__ __launch_bounds__(kUpdThreads) void factored_stats_kernel(const float* __restrict__ u,
+                                                                     const float* __restrict__ h, int64_t P,
+                                                                     int64_t nrows, int64_t block_rows, int bc,
+                                                                     int groups_per_block, float* __restrict__ Rr,
+                                                                     float* __restrict__ kpart, UpdateScalars sc) {
+    __shared__ float sh[kUpdThreads / kWave];
+    const int t = threadIdx.x;
+    const int64_t b = blockIdx.x / groups_per_block;
+    const int64_t g = blockIdx.x % groups_per_block;
+    const int64_t blk_end = min((b + 1) * block_rows, nrows);
+    const int64_t r0 = b * block_rows + g * kFacRowsPerWG;
+    const int64_t r1 = min(r0 + kFacRowsPerWG, blk_end);
+    float kap[KC * 4];
+#pragma unroll
+    for (int k = 0; k < KC * 4; ++k) kap[k] = 0.f;
+    for (int64_t i = r0; i < r1; ++i) {
+        float rho = 0.f;
+#pragma unroll
+        for (int k = 0; k < KC; ++k) {
+            const int j = (k * kUpdThreads + t) * 4;
+            const int64_t e = i * bc + j;
+            if (j < bc && e < P) {
+                const float4 u4 = *reinterpret_cast<const float4*>(u + e);
+                float4 h4 = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (SPLIT) h4 = *reinterpret_cast<const float4*>(h + e);
+                const float a0 = numerator<SPLIT>(u4.x, h4.x, sc), a1 = numerator<SPLIT>(u4.y, h4.y, sc);
+                const float a2 = numerator<SPLIT>(u4.z, h4.z, sc), a3 = numerator<SPLIT>(u4.w, h4.w, sc);
+                const float s0 = a0 * a0, s1 = a1 * a1, s2 = a2 * a2, s3 = a3 * a3;
+                kap[k * 4 + 0] += s0;
+                kap[k * 4 + 1] += s1;
+                kap[k * 4 + 2] += s2;
+                kap[k * 4 + 3] += s3;
+                rho += (s0 + s1) + (s2 + s3);
+            }
+        }
+        rho = wave_sum(rho);
+        if ((t & (kWave - 1)) == 0) sh[t / kWave] = rho;
+        __syncthreads();
+        if (t == 0) {
+            float r = 0.f;
+#pragma unroll
+            for (int w = 0; w < kUpdThreads / kWave; ++w) r += sh[w];
+            Rr[i] = sc.beta2 * Rr[i] + sc.one_minus_beta2 * r;
+        }
+        __syncthreads();
+    }
+    float* kp = kpart + (int64_t)blockIdx.x * bc;
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+        const int j = (k * kUpdThreads + t) * 4;
+        if (j < bc) *reinterpret_cast<float4*>(kp + j) = make_float4(kap[k * 4], kap[k * 4 + 1], kap[k * 4 + 2], kap[k * 4 + 3]);
+    }
+}
+
+// Per-block finish: Cc_j = beta2 Cc_j + (1-beta2) sum_g kpart[g][j]; rsum[b] = sum of the block's Rr.
+__global__ __launch_bounds__(kUpdThreads) void factored_finish_kernel(const float* __restrict__ kpart,
+                                                                      int groups_per_block, int64_t nrows,
+                                                                      int64_t block_rows, int bc, const float* __restrict__ Rr,
+                                                                      float* __restrict__ Cc, float* __restrict__ rsum,
+                                                                      UpdateScalars sc) {
+    __shared__ float sh[kUpdThreads];
+    const int64_t b = blockIdx.x;
+    const int t = threadIdx.x;
+    const int64_t r0 = b * block_rows;
+    const int64_t r1 = min(r0 + block_rows, nrows);
+    const int ng = (int)((r1 - r0 + kFacRowsPerWG - 1) / kFacRowsPerWG);
+    const float* kp = kpart + b * groups_per_block * (int64_t)bc;
+    for (int j = t; j < bc; j += kUpdThreads) {
+        float c = 0.f;
+        for (int g = 0; g < ng; ++g) c += kp[(int64_t)g * bc + j];
+        Cc[b * bc + j] = sc.beta2 * Cc[b * bc + j] + sc.one_minus_beta2 * c;
+    }
+    float r = 0.f;
+    for (int64_t i = r0 + t; i < r1; i += kUpdThreads) r += Rr[i];
+    sh[t] = r;
+    __syncthreads();
+    for (int o = kUpdThreads / 2; o > 0; o >>= 1) {
+        if (t < o) sh[t] += sh[t + o];
+        __syncthreads();
+    }
+    if (t == 0) rsum[b] = sh[0];
+}
+
+// Update: workgroup covers kFacUpdRows rows; v_hat_ij = (Rr_i / rsum_b * inv_bc2) * Cc_j.
+template <bool SPLIT, int KC>
+__global__ __launch_bounds__(kUpdThreads) void factored_update_kernel(float* __restrict__ theta, const float* __restrict__ u,
+                                                                      const float* __restrict__ h, int64_t P, int64_t nrows,
+                                                                      int64_t block_rows, int bc,
+                                                                      const float* __restrict__ Rr,
+                                                                      const float* __restrict__ Cc,
+                                                                      const float* __restrict__ rsum, SegTable segs,
+                                                                      UpdateScalars sc) {
+    const int t = threadIdx.x;
+    const int64_t r0 = (int64_t)blockIdx.x * kFacUpdRows;
+    const int64_t r1 = min(r0 + kFacUpdRows, nrows);
+    for (int64_t i = r0; i < r1; ++i) {
+        const int64_t b = i / block_rows;
+        const float rs = rsum[b];
+        const float a = rs > 0.f ? Rr[i] / rs * sc.inv_bc2 : 0.f;
+        const float* cb = Cc + b * bc;
+#pragma unroll
+        for (int k = 0; k < KC; ++k) {
+            const int j = (k * kUpdThreads + t) * 4;
+            const int64_t e = i * bc + j;
+            if (j < bc && e < P) {
+                float4 t4 = *reinterpret_cast<const float4*>(theta + e);
+                const float4 u4 = *reinterpret_cast<const float4*>(u + e);
+                float4 h4 = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (SPLIT) h4 = *reinterpret_cast<const float4*>(h + e);
+                const float4 c4 = *reinterpret_cast<const float4*>(cb + j);
+                float th[4] = {t4.x, t4.y, t4.z, t4.w};
+                const float uu[4] = {u4.x, u4.y, u4.z, u4.w};
+                const float hh[4] = {h4.x, h4.y, h4.z, h4.w};
+                const float cc[4] = {c4.x, c4.y, c4.z, c4.w};
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const float up = numerator<SPLIT>(uu[c], hh[c], sc);
+                    const float vhat = a * cc[c];
+                    const float wd = decay_of(e + c, segs);
+                    th[c] = (1.0f - sc.lr * wd) * th[c] - sc.lr * (up / (sqrtf(vhat) + sc.eps));
+                }
+                *reinterpret_cast<float4*>(theta + e) = make_float4(th[0], th[1], th[2], th[3]);
+            }
+        }
+    }
+}
+
+struct FacLayout {
+    int64_t nrows, nblocks, groups_per_block, ngroups;
+    size_t kpart_off, rsum_off, total;
+};
+
+FacLayout fac_layout(int64_t P, int64_t br, int64_t bc) {
+    FacLayout L;
+    L.nrows = (P + bc - 1) / bc;
+    L.nblocks = (L.nrows + br - 1) / br;
+    L.groups_per_block = (br + kFacRowsPerWG - 1) / kFacRowsPerWG;
+    L.ngroups = L.nblocks * L.groups_per_block;
+    L.kpart_off = 0;
+    L.rsum_off = align256((size_t)L.ngroups * (size_t)bc * sizeof(float));
+    L.total = align256(L.rsum_off + (size_t)L.nblocks * sizeof(float));
+    return L;
+}
+
+template <bool SPLIT, int KC>
+hipError_t run_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P, int64_t br,
+                        int bc, const SegTable& segs, const UpdateScalars& sc, void* ws, hipStream_t st) {
+    const FacLayout L = fac_layout(P, br, bc);
+    float* kpart = reinterpret_cast<float*>(static_cast<char*>(ws) + L.kpart_off);
+    float* rsum = reinterpret_cast<float*>(static_cast<char*>(ws) + L.rsum_off);
+    // statistics workgroups of the last block beyond its rows simply see an empty row range
+    hipLaunchKernelGGL((factored_stats_kernel<SPLIT, KC>), dim3((unsigned)L.ngroups), dim3(kUpdThreads), 0, st, u, h, P,
+                       L.nrows, br, bc, (int)L.groups_per_block, Rr, kpart, sc);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(factored_finish_kernel, dim3((unsigned)L.nblocks), dim3(kUpdThreads), 0, st, kpart,
+                       (int)L.groups_per_block, L.nrows, br, bc, Rr, Cc, rsum, sc);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const unsigned nupd = (unsigned)((L.nrows + kFacUpdRows - 1) / kFacUpdRows);
+    hipLaunchKernelGGL((factored_update_kernel<SPLIT, KC>), dim3(nupd), dim3(kUpdThreads), 0, st, theta, u, h, P,
+                       L.nrows, br, bc, Rr, Cc, rsum, segs, sc);
+    return hipGetLastError();
+}
+
+template <bool SPLIT>
+hipError_t dispatch_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P, int64_t br,
+                             int bc, const SegTable& segs, const UpdateScalars& sc, void* ws, hipStream_t st) {
+    const int kc = (bc + 1023) / 1024;
+    if (kc <= 1) return run_factored<SPLIT, 1>(theta, Rr, Cc, u, h, P, br, bc, segs, sc, ws, st);
+    if (kc <= 2) return run_factored<SPLIT, 2>(theta, Rr, Cc, u, h, P, br, bc, segs, sc, ws, st);
+    if (kc <= 4) return run_factored<SPLIT, 4>(theta, Rr, Cc, u, h, P, br, bc, segs, sc, ws, st);
+    if (kc <= 8) return run_factored<SPLIT, 8>(theta, Rr, Cc, u, h, P, br, bc, segs, sc, ws, st);
+    return run_factored<SPLIT, 16>(theta, Rr, Cc, u, h, P, br, bc, segs, sc, ws, st);
+}
+
+}  // namespace
+
+size_t update_workspace_bytes(int64_t P, const bom_update_cfg* cfg) {
+    if (!cfg || cfg->v_layout != BOM_V_FACTORED || cfg->block_rows < 1 || cfg->block_cols < 1 || P < 1) return 0;
+    return fac_layout(P, cfg->block_rows, cfg->block_cols).total;
+}
+
+hipError_t launch_update_dense(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
+                               const UpdateScalars& sc, hipStream_t st) {
+    const bool aligned = (reinterpret_cast<uintptr_t>(theta) % 16 == 0) && (reinterpret_cast<uintptr_t>(v) % 16 == 0) &&
+                         (reinterpret_cast<uintptr_t>(u) % 16 == 0) &&
+                         (h == nullptr || reinterpret_cast<uintptr_t>(h) % 16 == 0);
+    int64_t done = 0;
+    if (aligned && P >= 4) {
+        const int64_t nvec = P / 4;
+        int64_t grid = (nvec + kUpdThreads - 1) / kUpdThreads;
+        if (grid > 8192) grid = 8192;
+        if (h)
+            hipLaunchKernelGGL(update_dense_vec4_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v, u,
+                               h, nvec, segs, sc);
+        else
+            hipLaunchKernelGGL(update_dense_vec4_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
+                               u, h, nvec, segs, sc);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        done = nvec * 4;
+    }
+    if (done < P) {
+        int64_t grid = (P - done + kUpdThreads - 1) / kUpdThreads;
+        if (grid > 8192) grid = 8192;
+        if (h)
+            hipLaunchKernelGGL(update_dense_scalar_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
+                               u, h, done, P, segs, sc);
+        else
+            hipLaunchKernelGGL(update_dense_scalar_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta,
+                               v, u, h, done, P, segs, sc);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_update_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P,
+                                  int64_t block_rows, int64_t block_cols, const SegTable& segs,
+                                  const UpdateScalars& sc, void* ws, hipStream_t st) {
+    if (h) return dispatch_factored<true>(theta, Rr, Cc, u, h, P, block_rows, (int)block_cols, segs, sc, ws, st);
+    return dispatch_factored<false>(theta, Rr, Cc, u, h, P, block_rows, (int)block_cols, segs, sc, ws, st);
+}
+
+}  // namespace bom

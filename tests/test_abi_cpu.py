@@ -1,0 +1,139 @@
+"""libbom.so without a GPU: it loads, exports every entry point include/bom.h declares, and rejects
+bad arguments on the host before any HIP call (fake non-null pointers are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36738_amd import bom
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = ctypes.c_void_p(0x1000)      # never dereferenced: validation fails first
+FAKE2 = ctypes.c_void_p(0x9000000)
+
+
+def _declared():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            names |= set(re.findall(r"^[A-Za-z_][\w \*]*?\b(bom_\w+)\s*\(", text, flags=re.M))
+    return names
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return bom.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert {"bom_residual", "bom_ema", "bom_head_vjp", "bom_update"} <= names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for code in range(9):
+        assert lib.bom_status_string(code).decode().startswith("BOM_")
+    assert lib.bom_version() >= 100
+
+
+def _res(lib, **kw):
+    a = dict(Z=FAKE, dt=bom.BOM_BF16, N=8, V=16, ldz=16, labels=FAKE, ig=-100, s=FAKE, lse=FAKE, am=None, tg=None,
+             R=FAKE2, rdt=bom.BOM_BF16, ldr=16, loss=FAKE, nv=FAKE, fl=FAKE, ws=ctypes.c_void_p(0x100000), wsb=1 << 30)
+    a.update(kw)
+    return lib.bom_residual(a["Z"], a["dt"], a["N"], a["V"], a["ldz"], a["labels"], a["ig"], a["s"], a["lse"], a["am"],
+                            a["tg"], a["R"], a["rdt"], a["ldr"], a["loss"], a["nv"], a["fl"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Z=None), 1), (dict(labels=None), 1), (dict(s=None), 1), (dict(lse=None), 1), (dict(fl=None), 1),
+    (dict(N=0), 2), (dict(V=1), 2), (dict(ldz=15), 2), (dict(ldr=8), 2), (dict(N=1 << 31), 2),
+    (dict(dt=7), 3), (dict(rdt=bom.BOM_F32), 3),
+    (dict(ws=None), 5), (dict(wsb=16), 5), (dict(ws=ctypes.c_void_p(0x100010)), 5),
+    (dict(R=ctypes.c_void_p(0x1010)), 6),
+])
+def test_residual_rejects(lib, kw, code):
+    assert _res(lib, **kw) == code
+    assert lib.bom_last_error().decode() != ""
+
+
+def test_residual_workspace_query(lib):
+    assert lib.bom_residual_workspace_bytes(0, 10, 0) == 0
+    a = lib.bom_residual_workspace_bytes(4096, 32000, 1)
+    assert a >= 256 * 32000 * 4 and a % 256 == 0
+
+
+@pytest.mark.parametrize("args,code", [
+    ((None, FAKE, 10, 0.9, 1, FAKE2), 1), ((FAKE, FAKE, 0, 0.9, 1, FAKE2), 2),
+    ((FAKE, FAKE, 10, 1.0, 1, FAKE2), 4), ((FAKE, FAKE, 10, -0.1, 1, FAKE2), 4), ((FAKE, FAKE, 10, 0.9, 0, FAKE2), 4),
+    ((FAKE, FAKE, 10, float("nan"), 1, FAKE2), 4), ((FAKE, FAKE, 10, 0.9, 1, ctypes.c_void_p(0x1004)), 6),
+])
+def test_ema_rejects(lib, args, code):
+    assert lib.bom_ema(*args, None) == code
+
+
+def _vjp(lib, **kw):
+    a = dict(H=FAKE, ldh=64, W=FAKE, ldw=100, R=FAKE, ldr=100, dt=bom.BOM_BF16, N=32, d=64, V=100, labels=FAKE, ig=-100,
+             qh=FAKE, s=FAKE, nv=FAKE, lam=0.5, dW=FAKE, lddw=100, beta=0.0, db=None, dH=None, dhdt=bom.BOM_BF16,
+             lddh=64, ws=ctypes.c_void_p(0x100000), wsb=1 << 30)
+    a.update(kw)
+    return lib.bom_head_vjp(a["H"], a["ldh"], a["W"], a["ldw"], a["R"], a["ldr"], a["dt"], a["N"], a["d"], a["V"],
+                            a["labels"], a["ig"], a["qh"], a["s"], a["nv"], a["lam"], a["dW"], a["lddw"], a["beta"],
+                            a["db"], a["dH"], a["dhdt"], a["lddh"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(H=None), 1), (dict(dW=None), 1), (dict(nv=None), 1), (dict(db=FAKE, s=None), 1),
+    (dict(N=0), 2), (dict(V=1), 2), (dict(ldh=63), 2), (dict(lddw=99), 2), (dict(dH=FAKE, lddh=10), 2),
+    (dict(dt=5), 3), (dict(dH=FAKE, dhdt=9), 3),
+    (dict(lam=1.5), 4), (dict(lam=-0.1), 4), (dict(beta=float("inf")), 4),
+    (dict(ws=None), 5), (dict(wsb=0), 5),
+])
+def test_head_vjp_rejects(lib, kw, code):
+    assert _vjp(lib, **kw) == code
+
+
+def _upd(lib, P=1000, segs=(), wd=0.0, v_col=None, ws=None, wsb=0, h=None, **cfgkw):
+    c = dict(lr=1e-3, beta2=0.999, eps=1e-8, t=1)
+    c.update(cfgkw)
+    cfg = bom.make_update_cfg(**c)
+    arr = (bom.bom_segment * max(1, len(segs)))(*[bom.bom_segment(*s) for s in segs])
+    return lib.bom_update(ctypes.c_void_p(0x100000), ctypes.c_void_p(0x200000), v_col, ctypes.c_void_p(0x300000), h, P,
+                          arr, len(segs), wd, ctypes.byref(cfg), ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(P=0), 2), (dict(segs=[(0, 2000, 0.1)]), 2), (dict(segs=[(-1, 2, 0.1)]), 2),
+    (dict(segs=[(0, 1, float("nan"))]), 4), (dict(beta2=1.0), 4), (dict(t=0), 4), (dict(eps=0.0), 4),
+    (dict(lr=float("inf")), 4), (dict(lam=2.0), 4), (dict(wd=float("nan")), 4), (dict(u_scale=float("nan")), 4),
+    (dict(v_col=FAKE), 2), (dict(h=ctypes.c_void_p(0x100100)), 6),
+    (dict(factored=True), 1), (dict(factored=True, v_col=ctypes.c_void_p(0x400000), block_cols=6), 8),
+    (dict(factored=True, v_col=ctypes.c_void_p(0x400000), P=1002), 8),
+    (dict(factored=True, v_col=ctypes.c_void_p(0x400000), block_cols=64, block_rows=8), 5),
+])
+def test_update_rejects(lib, kw, code):
+    assert _upd(lib, **kw) == code
+
+
+def test_update_null_pointers(lib):
+    cfg = bom.make_update_cfg(lr=1e-3, beta2=0.999, eps=1e-8, t=1)
+    assert lib.bom_update(None, FAKE, None, FAKE, None, 10, None, 0, 0.0, ctypes.byref(cfg), None, 0, None) == 1
+    assert lib.bom_update(FAKE, FAKE, None, FAKE, None, 10, None, 0, 0.0, None, None, 0, None) == 1
+    assert lib.bom_update(FAKE, FAKE, None, FAKE, None, 10, None, 3, 0.0, ctypes.byref(cfg), None, 0, None) == 2
+
+
+def test_update_workspace_query(lib):
+    dense = bom.make_update_cfg(lr=1e-3, beta2=0.999, eps=1e-8, t=1)
+    assert lib.bom_update_workspace_bytes(10**6, ctypes.byref(dense)) == 0
+    fac = bom.make_update_cfg(lr=1e-3, beta2=0.999, eps=1e-8, t=1, factored=True)
+    P = 476 * 4096 * 4096 + 3429 * 4096
+    assert lib.bom_update_workspace_bytes(P, ctypes.byref(fac)) > 0
+
+
+def test_head_forward_rejects(lib):
+    assert lib.bom_head_forward(FAKE, 8, FAKE, 4, None, bom.BOM_BF16, 4, 8, 4, FAKE2, 4, None) == 8
+    assert lib.bom_head_forward(FAKE, 7, FAKE, 4, None, bom.BOM_F32, 4, 8, 4, FAKE2, 4, None) == 2
+    assert lib.bom_head_forward(None, 8, FAKE, 4, None, bom.BOM_F32, 4, 8, 4, FAKE2, 4, None) == 1

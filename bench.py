@@ -1,0 +1,335 @@
+"""Benchmark of the BOM per-step hot path on one MI355X.
+
+A step is one pass of the whole hot path over one synthetic batch resident in HBM:
+  bom_residual (row statistics, R, s) -> bom_ema (q, q_hat) -> bom_head_vjp (dW into the head
+  slice of the flat u, dH) -> bom_update (second moment and parameters over the flat buffer).
+W untimed warmup steps, then exactly K timed steps bracketed by device synchronisation.
+Per-stage durations come from HIP events recorded on the stream the kernels run on.
+
+Prints one JSON line: whole-job tokens/s (rows of Z per second), per-stage times, the roofline
+of the dominant stage, and the fp64 CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+from synth.workloads import BY_NAME, WORKLOADS  # noqa: E402
+from paper_2609_36738_amd import bom  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA
+FP32_PEAK_TFS = 157.3      # MI355X fp32 vector
+METRIC = "BOM steps/s & tokens/s per config; % of HBM BW / MFMA peak per kernel"
+DEFAULT_WORKLOAD = WORKLOADS[1].name
+KERNEL_SOURCES = {
+    "bom_residual": "residual.hip",
+    "bom_ema": "ema.hip",
+    "bom_head_vjp": "head_vjp.hip",
+    "bom_update": "update.hip",
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def source_hash(stage: str) -> str:
+    path = os.path.join(ROOT, "paper_2609_36738_amd", "csrc", KERNEL_SOURCES[stage])
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def bf16_dev(bits: np.ndarray, shape, dev):
+    return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).reshape(shape).to(dev)
+
+
+def fill_normal_(t: torch.Tensor, stream: int, std: float, chunk: int = 1 << 27):
+    """Fill a flat fp32 device tensor from the seeded generator, chunk by chunk (bounded host memory)."""
+    n = t.numel()
+    host = np.empty(min(chunk, n), np.float32)
+    for start in range(0, n, chunk):
+        m = min(chunk, n - start)
+        synth.normal_f32(m, stream, std, start=start, out=host[:m])
+        t[start:start + m].copy_(torch.from_numpy(host[:m]))
+
+
+class Problem:
+    """Device-resident inputs and state of one workload."""
+
+    def __init__(self, w, dev):
+        self.w = w
+        N, d, V, P = w.N, w.d, w.V, w.P
+        std_z = w.logit_std
+        t0 = time.time()
+        if w.dtype == "bf16":
+            self.Z = bf16_dev(synth.normal_bf16(N * V, synth.STREAM_Z, std_z), (N, V), dev)
+            self.H = bf16_dev(synth.normal_bf16(N * d, synth.STREAM_H, 1.0), (N, d), dev)
+            self.W = bf16_dev(synth.normal_bf16(d * V, synth.STREAM_W, 0.02), (d, V), dev)
+        else:
+            self.Z = torch.from_numpy(synth.normal_f32(N * V, synth.STREAM_Z, std_z).reshape(N, V)).to(dev)
+            self.H = torch.from_numpy(synth.normal_f32(N * d, synth.STREAM_H, 1.0).reshape(N, d)).to(dev)
+            self.W = None  # the tiny head reads W from theta
+        y = synth.labels_uniform(N, V) if w.labels == "uniform" else synth.labels_zipf(N, V)
+        self.labels = torch.from_numpy(y).to(dev)
+        self.R = torch.empty((N, V), dtype=self.Z.dtype, device=dev)
+        self.theta = torch.empty(P, dtype=torch.float32, device=dev)
+        fill_normal_(self.theta, synth.STREAM_THETA, 0.02)
+        if w.dtype == "f32":
+            self.theta[d * V:d * V + V].zero_()   # bias starts at 0
+        self.u = torch.empty(P, dtype=torch.float32, device=dev)
+        fill_normal_(self.u, synth.STREAM_U + 1, 1e-3)
+        if w.factored:
+            nrows = -(-P // w.block_cols)
+            nblocks = -(-nrows // w.block_rows)
+            self.v = torch.zeros(nrows, dtype=torch.float32, device=dev)
+            self.v_col = torch.zeros(nblocks * w.block_cols, dtype=torch.float32, device=dev)
+        else:
+            self.v = torch.zeros(P, dtype=torch.float32, device=dev)
+            self.v_col = None
+        self.q = torch.zeros(V, dtype=torch.float32, device=dev)
+        self.q_hat = torch.empty(V, dtype=torch.float32, device=dev)
+        self.dH = torch.empty((N, d), dtype=self.Z.dtype, device=dev)
+        self.segments = w.segments()
+        # outputs and workspaces allocated once
+        self.res = None
+        self.ws_res = self.ws_vjp = self.ws_upd = None
+        torch.cuda.synchronize()
+        log(f"[bench] inputs for {w.name} ready in {time.time() - t0:.1f}s")
+
+    def step(self, t: int, ev=None):
+        w = self.w
+        d, V = w.d, w.V
+        if ev is not None:
+            ev[0].record()
+        self.res = bom.bom_residual(self.Z, self.labels, R=self.R, workspace=self.ws_res,
+                                    **({} if self.res is None else {k: self.res[k] for k in (
+                                        "s", "row_lse", "row_argmax", "row_target", "loss", "n_valid", "flags")}))
+        self.ws_res = self.res["workspace"]
+        if ev is not None:
+            ev[1].record()
+        bom.bom_ema(self.q, self.res["s"], w.beta1, t, q_hat=self.q_hat)
+        if ev is not None:
+            ev[2].record()
+        W = self.W if self.W is not None else self.theta[: d * V].view(d, V)
+        dW = self.u[: d * V].view(d, V)
+        db = self.u[d * V: d * V + V] if w.has_bias else None
+        g = bom.bom_head_vjp(self.H, W, self.R, self.labels, self.q_hat, self.res["n_valid"], s=self.res["s"],
+                             lam=w.lam, dW=dW, db=db, dH=self.dH, workspace=self.ws_vjp)
+        self.ws_vjp = g["workspace"]
+        if ev is not None:
+            ev[3].record()
+        cfg = bom.make_update_cfg(lr=w.lr, beta2=w.beta2, eps=w.eps, t=t, lam=w.lam, factored=w.factored,
+                                  block_rows=w.block_rows, block_cols=w.block_cols)
+        self.ws_upd = bom.bom_update(self.theta, self.v, self.u, cfg, v_col=self.v_col, segments=self.segments,
+                                     workspace=self.ws_upd)
+        if ev is not None:
+            ev[4].record()
+
+
+def algorithmic(w):
+    """Algorithmic bytes / flops of each stage for one step (what BOM must move or compute)."""
+    esz = 2 if w.dtype == "bf16" else 4
+    N, d, V, P = w.N, w.d, w.V, w.P
+    out = {
+        "bom_residual": dict(bound="hbm", amount=2 * N * V * esz + 16 * N + 4 * V,
+                             per_unit="2*esz bytes per logit (read Z, write R) + 16 B/row + 4 B/column"),
+        "bom_ema": dict(bound="hbm", amount=12 * V, per_unit="12 bytes per output coordinate"),
+        "bom_head_vjp": dict(bound="mfma" if w.dtype == "bf16" else "alu", amount=4 * N * d * V,
+                             per_unit="4*N*d*V flop (dW and dH)"),
+    }
+    if w.factored:
+        nrows = -(-P // w.block_cols)
+        nblocks = -(-nrows // w.block_rows)
+        out["bom_update"] = dict(bound="hbm", amount=16 * P + 8 * nrows + 8 * nblocks * w.block_cols,
+                                 per_unit="16 bytes per parameter (read u twice, read+write theta) + factors")
+    else:
+        out["bom_update"] = dict(bound="hbm", amount=20 * P, per_unit="20 bytes per parameter (read theta, v, u; "
+                                                                      "write theta, v)")
+    return out
+
+
+def stored_traffic(stage: str, workload: str):
+    """HBM traffic of a stage from a committed rocprofv3 counter summary, if the kernel source is unchanged."""
+    path = os.path.join(ROOT, "profiles", f"{stage}_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"source_sha256_16:\s*([0-9a-f]{16})", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != source_hash(stage):
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(w, budget_s: float):
+    """The fp64 oracle (as it stands) timed on the host on a bounded sample of the same workload,
+    scaled to the whole step. Each stage runs on a sample; per-element work scales linearly."""
+    import oracle
+
+    N, d, V, P = w.N, w.d, w.V, w.P
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    # sample sizes: rows of Z for the residual and the head GEMM rows/columns, elements for the update
+    rows = min(N, max(1, int(2e6 // V)))
+    ncols = min(V, 64)
+    nrows_dh = min(N, 16)
+    npar = min(P, 4_000_000)
+    t_all = {}
+    Zs = synth.bf16_to_f32(synth.normal_bf16(rows * V, synth.STREAM_Z, w.logit_std)) if w.dtype == "bf16" else \
+        synth.normal_f32(rows * V, synth.STREAM_Z, w.logit_std)
+    Zs = Zs.reshape(rows, V).astype(np.float64)
+    y = (synth.labels_uniform(N, V) if w.labels == "uniform" else synth.labels_zipf(N, V))[:rows]
+    t0 = time.perf_counter()
+    res = oracle.residual(Zs, y, want_R=False)
+    t_all["bom_residual"] = (time.perf_counter() - t0) * N / rows
+    t0 = time.perf_counter()
+    _, qh = oracle.ema(np.zeros(V), res["s"], w.beta1, 1)
+    t_all["bom_ema"] = time.perf_counter() - t0
+    Hs = synth.normal_f32(rows * d, synth.STREAM_H, 1.0).reshape(rows, d).astype(np.float64)
+    Ws = synth.normal_f32(d * V, synth.STREAM_W, 0.02).reshape(d, V).astype(np.float64)
+    t0 = time.perf_counter()
+    oracle.dW_cols(Hs, Zs, y, res["row_lse"], qh, res["n_valid"], w.lam, cols=np.arange(ncols))
+    t_dw = (time.perf_counter() - t0) * (V / ncols) * (N / rows)
+    t0 = time.perf_counter()
+    oracle.dH_rows(Ws, Zs, y, res["row_lse"], qh, res["n_valid"], w.lam, rows=np.arange(nrows_dh))
+    t_dh = (time.perf_counter() - t0) * (N / nrows_dh)
+    t_all["bom_head_vjp"] = t_dw + t_dh
+    th = synth.normal_f32(npar, synth.STREAM_THETA, 0.02).astype(np.float64)
+    u = synth.normal_f32(npar, synth.STREAM_U + 1, 1e-3).astype(np.float64)
+    t0 = time.perf_counter()
+    if w.factored:
+        bc, br = w.block_cols, w.block_rows
+        nr = npar // bc
+        oracle.update_factored(th[: nr * bc], np.zeros(nr), np.zeros(-(-nr // br) * bc), u[: nr * bc], lr=w.lr,
+                               beta2=w.beta2, eps=w.eps, t=1, block_rows=br, block_cols=bc,
+                               weight_decay=w.weight_decay)
+        t_all["bom_update"] = (time.perf_counter() - t0) * P / (nr * bc)
+    else:
+        oracle.update_dense(th, np.zeros(npar), u, lr=w.lr, beta2=w.beta2, eps=w.eps, t=1,
+                            weight_decay=w.weight_decay)
+        t_all["bom_update"] = (time.perf_counter() - t0) * P / npar
+    step_s = sum(t_all.values())
+    return {
+        "value": N / step_s, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+        "sample": (f"{rows} of {N} rows of Z (residual, dW), {ncols} of {V} dW columns, {nrows_dh} of {N} dH rows, "
+                   f"{npar} of {P} parameters (update); each stage scaled linearly to the full step"),
+        "step_s_extrapolated": step_s,
+        "stage_s": {k: round(v, 4) for k, v in t_all.items()},
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=[w.name for w in WORKLOADS])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the BOM hot path here is built and measured on a single MI355X "
+              "(sharding is a design note, not part of this build).", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    bom.load(build_if_missing=False)
+    w = BY_NAME[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    prob = Problem(w, dev)
+    stages = ["bom_residual", "bom_ema", "bom_head_vjp", "bom_update"]
+
+    t = 0
+    for _ in range(args.warmup):
+        t += 1
+        prob.step(t)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} steps done")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for k in range(args.steps):
+        t += 1
+        prob.step(t, evs[k])
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+    per_step = np.array([evs[k][0].elapsed_time(evs[k][4]) for k in range(args.steps)])
+    stage_ms = {s: float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
+                for i, s in enumerate(stages)}
+    log(f"[bench] timed {args.steps} steps: {ms_per_step:.4f} ms/step (wall {wall:.2f}s)")
+
+    alg = algorithmic(w)
+    dom = max(stages, key=lambda s: stage_ms[s])
+    a = alg[dom]
+    sec = stage_ms[dom] / 1e3
+    if a["bound"] == "hbm":
+        achieved, peak, unit = a["amount"] / sec / 1e9, HBM_PEAK_GBS, "GB/s"
+    elif a["bound"] == "mfma":
+        achieved, peak, unit = a["amount"] / sec / 1e12, MFMA_BF16_PEAK_TFS, "TFLOP/s"
+    else:
+        achieved, peak, unit = a["amount"] / sec / 1e12, FP32_PEAK_TFS, "TFLOP/s"
+    roofline = {"bound": a["bound"], "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+                "frac": round(achieved / peak, 4), "traffic": stored_traffic(dom, w.name), "kernel": dom,
+                "algorithmic_per_launch": a["amount"], "per_unit": a["per_unit"]}
+    per_stage = {}
+    for s in stages:
+        b = alg[s]
+        ss = stage_ms[s] / 1e3
+        rate = b["amount"] / ss / (1e9 if b["bound"] == "hbm" else 1e12)
+        pk = HBM_PEAK_GBS if b["bound"] == "hbm" else (MFMA_BF16_PEAK_TFS if b["bound"] == "mfma" else FP32_PEAK_TFS)
+        per_stage[s] = {"ms": round(stage_ms[s], 5), "rate": round(rate, 2),
+                        "unit": "GB/s" if b["bound"] == "hbm" else "TFLOP/s", "frac": round(rate / pk, 4)}
+
+    n_valid = int(prob.res["n_valid"].item())
+    out = {
+        "metric": METRIC,
+        "value": round(n_valid / (ms_per_step / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "steps_per_s": round(1e3 / ms_per_step, 2),
+        "median_ms_per_step": round(float(np.median(per_step)), 5),
+        "p10_p90_ms": [round(float(np.percentile(per_step, 10)), 5), round(float(np.percentile(per_step, 90)), 5)],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "N": w.N, "d": w.d, "V": w.V, "P": w.P, "tokens_per_step": n_valid,
+                   "second_moment": "factored" if w.factored else "dense"},
+        "stages": per_stage,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -142,7 +142,9 @@ def _vjp_inputs(N, d, V, dtype, ign, t=3):
     Wh, Wd = gen_matrix(d, V, synth.STREAM_W, 0.02, dtype)
     Zh, Zd = gen_matrix(N, V, synth.STREAM_Z, math.sqrt(0.0004 * d), dtype)
     y = gen_labels(N, V, "zipf" if V > 1000 else "uniform", ign)
+    # a task-space history is an EMA of zero-sum residual means, so it sums to zero too
     q_prev = synth.normal_f32(V, synth.STREAM_U, 0.01)
+    q_prev = (q_prev - q_prev.astype(np.float64).mean()).astype(np.float32)
     return Hh, Hd, Wh, Wd, Zh, Zd, y, q_prev, t
 
 
@@ -336,4 +338,4 @@ def test_vision_head_full_size():
     thg = to_f64(theta)
     _check_theta(thg[d * V:], tho, lr, "vision theta (backbone)")
     step = np.abs(thg[: d * V] - (1 - lr * 0.01) * th_in[: d * V].astype(np.float64))
-    assert (step <= lr * (1 + 1e-5)).all()
+    assert (step <= lr * (1 + 1e-5) + 2.5e-7 * np.abs(th_in[: d * V])).all()   # + one fp32 ulp of theta

@@ -9,6 +9,27 @@ namespace bom {
 
 constexpr int kWave = 64;
 
+// Native 4-wide vector (the non-temporal load/store builtins take clang vector types).
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Streaming (non-temporal) 16-byte accesses: data read or written once per launch.
+__device__ __forceinline__ f32x4 ld_stream(const float* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+}
+__device__ __forceinline__ void st_stream(float* p, f32x4 v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(p));
+}
+
+// All-ones / zero lane mask, opaque to the optimiser. A load followed by `& lane_mask(ok)` stays an
+// unconditional load: the compiler cannot sink it into a branch (which would serialise the loads of
+// a tile behind a wait for each one).
+__device__ __forceinline__ uint32_t lane_mask(bool ok) {
+    uint32_t m = ok ? 0xFFFFFFFFu : 0u;
+    asm("" : "+v"(m));  // not volatile: opaque, but free to schedule
+    return m;
+}
+__device__ __forceinline__ uint4 and_mask(uint4 v, uint32_t m) { return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m); }
+
 // ---- bf16 <-> fp32 (bf16 is carried as raw uint16_t) ----------------------------------------
 __device__ __forceinline__ float bf16_lo(uint32_t packed) { return __uint_as_float(packed << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t packed) { return __uint_as_float(packed & 0xFFFF0000u); }

@@ -11,6 +11,8 @@
 // and is transposed while staging (perm for H, the bf16 pack of the fold for G); dH = G W^T has
 // both operands k-contiguous. Split-K with a fixed-order reduction when the output has too few
 // tiles to fill the chip. fp32 path (and unaligned bf16): a SIMT tiled GEMM.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -27,7 +29,7 @@ struct Fold {
 };
 
 struct VjpWs {
-    size_t cq_off, vmask_off, scal_off, part_off, total;
+    size_t cq_off, vmask_off, scal_off, ht_off, part_off, total;
 };
 
 // ---- prep -------------------------------------------------------------------------------------
@@ -163,33 +165,34 @@ constexpr int MB = 128;          // output tile (both dims)
 constexpr int MK = 64;           // k tile
 constexpr int LDK = MK + 8;      // LDS row pitch in bf16 elements (144 bytes)
 
+// Branch-free staging: every 16-byte chunk is loaded unconditionally from a clamped in-range
+// address; an out-of-range chunk is zeroed by its lane mask when it is written to LDS (after the
+// MFMA phase), so all loads of a tile stay in flight together.
+__device__ __forceinline__ uint4 ld16(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+
 // A tile for dW: A(m, k) = H[k][m], global rows k contiguous in m. Thread t stages k rows
 // kq*4..+3 and m columns mq*8..+7 (kq = t / 16, mq = t % 16); transposes with byte permutes.
 struct StageHt {
     uint4 r[4];
+    uint32_t mk[4];
     __device__ __forceinline__ void load(const uint16_t* H, int64_t ldh, int M, int k0, int kend, int m0) {
         const int t = threadIdx.x, kq = t / 16, mq = t % 16;
         const int m = m0 + mq * 8;
+        const bool mok = m < M;
+        const int mc = mok ? m : M - 8;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int k = k0 + kq * 4 + q;
-            if (k < kend && m + 8 <= M) {
-                r[q] = *reinterpret_cast<const uint4*>(H + (int64_t)k * ldh + m);
-            } else {
-                uint16_t v[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) v[e] = (k < kend && m + e < M) ? H[(int64_t)k * ldh + m + e] : (uint16_t)0;
-                r[q] = make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
-                                  v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
-            }
+            mk[q] = lane_mask(mok && k < kend);
+            r[q] = ld16(H + (int64_t)(k < kend ? k : kend - 1) * ldh + mc);
         }
     }
     __device__ __forceinline__ void store(uint16_t (*As)[LDK]) const {
         const int t = threadIdx.x, kq = t / 16, mq = t % 16;
-        const uint32_t w0[4] = {r[0].x, r[0].y, r[0].z, r[0].w};
-        const uint32_t w1[4] = {r[1].x, r[1].y, r[1].z, r[1].w};
-        const uint32_t w2[4] = {r[2].x, r[2].y, r[2].z, r[2].w};
-        const uint32_t w3[4] = {r[3].x, r[3].y, r[3].z, r[3].w};
+        const uint32_t w0[4] = {r[0].x & mk[0], r[0].y & mk[0], r[0].z & mk[0], r[0].w & mk[0]};
+        const uint32_t w1[4] = {r[1].x & mk[1], r[1].y & mk[1], r[1].z & mk[1], r[1].w & mk[1]};
+        const uint32_t w2[4] = {r[2].x & mk[2], r[2].y & mk[2], r[2].z & mk[2], r[2].w & mk[2]};
+        const uint32_t w3[4] = {r[3].x & mk[3], r[3].y & mk[3], r[3].z & mk[3], r[3].w & mk[3]};
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
             // columns m = mq*8 + 2p (low halves) and 2p + 1 (high halves)
@@ -208,32 +211,28 @@ struct StageHt {
 // G = fma(alpha, R, mask_k * cq_n) in fp32, rounded to bf16 pairs (k, k+1) -- the transpose.
 struct StageGt {
     uint4 r[4];
+    uint32_t mk[4];
     float vm[4];
     __device__ __forceinline__ void load(const uint16_t* R, int64_t ldr, int Nn, int k0, int kend, int n0,
                                          const float* vmask) {
         const int t = threadIdx.x, kq = t / 16, mq = t % 16;
         const int n = n0 + mq * 8;
+        const bool nok = n < Nn;
+        const int nc = nok ? n : Nn - 8;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int k = k0 + kq * 4 + q;
-            vm[q] = k < kend ? vmask[k] : 0.f;
-            if (k < kend && n + 8 <= Nn) {
-                r[q] = *reinterpret_cast<const uint4*>(R + (int64_t)k * ldr + n);
-            } else {
-                uint16_t v[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) v[e] = (k < kend && n + e < Nn) ? R[(int64_t)k * ldr + n + e] : (uint16_t)0;
-                r[q] = make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
-                                  v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
-            }
+            vm[q] = vmask[k < kend ? k : kend - 1] * (k < kend ? 1.f : 0.f);
+            mk[q] = lane_mask(nok && k < kend);
+            r[q] = ld16(R + (int64_t)(k < kend ? k : kend - 1) * ldr + nc);
         }
     }
     __device__ __forceinline__ void store(uint16_t (*Bs)[LDK], float alpha, const float* cqn) const {
         const int t = threadIdx.x, kq = t / 16, mq = t % 16;
-        const uint32_t w[4][4] = {{r[0].x, r[0].y, r[0].z, r[0].w},
-                                  {r[1].x, r[1].y, r[1].z, r[1].w},
-                                  {r[2].x, r[2].y, r[2].z, r[2].w},
-                                  {r[3].x, r[3].y, r[3].z, r[3].w}};
+        const uint32_t w[4][4] = {{r[0].x & mk[0], r[0].y & mk[0], r[0].z & mk[0], r[0].w & mk[0]},
+                                  {r[1].x & mk[1], r[1].y & mk[1], r[1].z & mk[1], r[1].w & mk[1]},
+                                  {r[2].x & mk[2], r[2].y & mk[2], r[2].z & mk[2], r[2].w & mk[2]},
+                                  {r[3].x & mk[3], r[3].y & mk[3], r[3].z & mk[3], r[3].w & mk[3]}};
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
             float g[4];
@@ -255,20 +254,14 @@ struct StageGt {
 template <bool FOLD>
 struct StageK {
     uint4 r[4];
+    uint32_t mk[4];
     __device__ __forceinline__ void load(const uint16_t* X, int64_t ldx, int rows, int r0, int k0, int kend) {
         const int t = threadIdx.x;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int c = e * 256 + t, row = r0 + c / 8, k = k0 + (c % 8) * 8;
-            if (row < rows && k + 8 <= kend) {
-                r[e] = *reinterpret_cast<const uint4*>(X + (int64_t)row * ldx + k);
-            } else {
-                uint16_t v[8];
-#pragma unroll
-                for (int q = 0; q < 8; ++q) v[q] = (row < rows && k + q < kend) ? X[(int64_t)row * ldx + k + q] : (uint16_t)0;
-                r[e] = make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
-                                  v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
-            }
+            mk[e] = lane_mask(row < rows && k < kend);
+            r[e] = ld16(X + (int64_t)(row < rows ? row : rows - 1) * ldx + (k < kend ? k : kend - 8));
         }
     }
     __device__ __forceinline__ void store(uint16_t (*S)[LDK], int rows, int r0, int k0, int kend, const Fold& f,
@@ -277,20 +270,15 @@ struct StageK {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int c = e * 256 + t, lr = c / 8, lk = (c % 8) * 8;
-            uint4 o = r[e];
+            uint4 o = and_mask(r[e], mk[e]);
             if (FOLD) {
                 const float vm = (r0 + lr < rows) ? f.vmask[r0 + lr] : 0.f;
                 const int k = k0 + lk;
-                float cq[8];
-                if (k + 8 <= kend) {
-                    const float4 c0 = *reinterpret_cast<const float4*>(f.cq + k);
-                    const float4 c1 = *reinterpret_cast<const float4*>(f.cq + k + 4);
-                    cq[0] = c0.x; cq[1] = c0.y; cq[2] = c0.z; cq[3] = c0.w;
-                    cq[4] = c1.x; cq[5] = c1.y; cq[6] = c1.z; cq[7] = c1.w;
-                } else {
-#pragma unroll
-                    for (int q = 0; q < 8; ++q) cq[q] = (k + q < kend) ? f.cq[k + q] : 0.f;
-                }
+                const bool kok = k < kend;
+                const float z = kok ? 1.f : 0.f;
+                const float4 c0 = *reinterpret_cast<const float4*>(f.cq + (kok ? k : kend - 8));
+                const float4 c1 = *reinterpret_cast<const float4*>(f.cq + (kok ? k : kend - 8) + 4);
+                const float cq[8] = {z * c0.x, z * c0.y, z * c0.z, z * c0.w, z * c1.x, z * c1.y, z * c1.z, z * c1.w};
                 const uint32_t w[4] = {o.x, o.y, o.z, o.w};
                 uint32_t g[4];
 #pragma unroll
@@ -460,6 +448,271 @@ __global__ __launch_bounds__(256) void mfma_dH_kernel(const uint16_t* __restrict
     }
 }
 
+// ---- MFMA bf16, large tiles ------------------------------------------------------------------------
+// 256 x 256 output tile, 4 waves each owning 128 x 128 (4 x 4 blocks of v_mfma_f32_32x32x16_bf16),
+// 64-deep k tiles double-buffered in LDS (2 x 2 x 36 KB). Rows of an LDS tile are 72 bf16 (144 B);
+// the 16-byte chunk c of row r is stored at chunk c ^ ((r >> 4) & 7), which keeps both the staging
+// writes and the fragment reads free of bank conflicts.
+constexpr int TB = 256;
+constexpr int TK = 64;
+constexpr int TP = 72;
+
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 4) & 7); }
+
+// k-contiguous operand: tile rows r0..r0+255 of X (k extent kend, a multiple of 8), k chunk
+// (t % 8) * 8 of rows e * 32 + t / 8, e < 8. FOLD: G = fma(alpha, R, mask_row * cq_k) in bf16.
+template <bool FOLD>
+struct StageKC256 {
+    uint4 r[8];
+    uint32_t mk[8];
+    float vm[FOLD ? 8 : 1];
+    __device__ __forceinline__ void init_rows(int rows, int r0, const Fold& f) {
+        if (FOLD) {
+            const int t = threadIdx.x;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int row = r0 + e * 32 + t / 8;
+                vm[e] = row < rows ? f.vmask[row] : 0.f;
+            }
+        }
+    }
+    __device__ __forceinline__ void load(const uint16_t* X, int64_t ldx, int rows, int r0, int k0, int kend) {
+        const int t = threadIdx.x;
+        const int k = k0 + (t % 8) * 8;
+        const bool kok = k < kend;
+        const int kc = kok ? k : kend - 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int row = r0 + e * 32 + t / 8;
+            mk[e] = lane_mask(kok && row < rows);
+            r[e] = ld16(X + (int64_t)(row < rows ? row : rows - 1) * ldx + kc);
+        }
+    }
+    __device__ __forceinline__ void store(uint16_t (*S)[TP], int k0, int kend, const Fold& f, float alpha) const {
+        const int t = threadIdx.x;
+        const int ch = t % 8;
+        float cq[8];
+        if (FOLD) {
+            const int k = k0 + ch * 8;
+            const bool kok = k < kend;
+            const float4 c0 = *reinterpret_cast<const float4*>(f.cq + (kok ? k : kend - 8));
+            const float4 c1 = *reinterpret_cast<const float4*>(f.cq + (kok ? k : kend - 8) + 4);
+            const float z = kok ? 1.f : 0.f;
+            cq[0] = z * c0.x; cq[1] = z * c0.y; cq[2] = z * c0.z; cq[3] = z * c0.w;
+            cq[4] = z * c1.x; cq[5] = z * c1.y; cq[6] = z * c1.z; cq[7] = z * c1.w;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int lr = e * 32 + t / 8;
+            uint4 o = and_mask(r[e], mk[e]);
+            if (FOLD) {
+                const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+                uint32_t g[4];
+#pragma unroll
+                for (int p = 0; p < 4; ++p)
+                    g[p] = pack_bf16x2(fmaf(alpha, bf16_lo(w[p]), vm[e] * cq[2 * p]),
+                                       fmaf(alpha, bf16_hi(w[p]), vm[e] * cq[2 * p + 1]));
+                o = make_uint4(g[0], g[1], g[2], g[3]);
+            }
+            *reinterpret_cast<uint4*>(&S[lr][swz(lr, ch) * 8]) = o;
+        }
+    }
+};
+
+// dW's B operand: G(k, n) from R[k][n] (n contiguous, Nn a multiple of 8). Thread t stages k rows
+// kq*8..+7 and columns nq*8..+7 (kq = t / 32, nq = t % 32), folds, and writes 8 k values per
+// column: the transpose.
+struct StageGt256 {
+    uint4 r[8];
+    uint32_t mk[8];
+    float cqn[8];
+    __device__ __forceinline__ void init_cols(int Nn, int n0, const Fold& f) {
+        const int n = n0 + (threadIdx.x % 32) * 8;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) cqn[c] = (n + c < Nn) ? f.cq[n + c] : 0.f;
+    }
+    __device__ __forceinline__ void load(const uint16_t* R, int64_t ldr, int Nn, int n0, int k0, int kend) {
+        const int t = threadIdx.x, kq = t / 32, nq = t % 32;
+        const int n = n0 + nq * 8;
+        const bool nok = n < Nn;
+        const int nc = nok ? n : Nn - 8;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int k = k0 + kq * 8 + q;
+            mk[q] = lane_mask(nok && k < kend);
+            r[q] = ld16(R + (int64_t)(k < kend ? k : kend - 1) * ldr + nc);
+        }
+    }
+    __device__ __forceinline__ void store(uint16_t (*S)[TP], int k0, int kend, const Fold& f, float alpha) const {
+        const int t = threadIdx.x, kq = t / 32, nq = t % 32;
+        float vm[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int k = k0 + kq * 8 + q;
+            vm[q] = f.vmask[k < kend ? k : kend - 1] * (k < kend ? 1.f : 0.f);
+        }
+        uint32_t w[8][4];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const uint4 v = and_mask(r[q], mk[q]);
+            w[q][0] = v.x; w[q][1] = v.y; w[q][2] = v.z; w[q][3] = v.w;
+        }
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            float g[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const float rv = (c & 1) ? bf16_hi(w[q][c >> 1]) : bf16_lo(w[q][c >> 1]);
+                g[q] = fmaf(alpha, rv, vm[q] * cqn[c]);
+            }
+            const int row = nq * 8 + c;
+            *reinterpret_cast<uint4*>(&S[row][swz(row, kq) * 8]) =
+                make_uint4(pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]), pack_bf16x2(g[4], g[5]),
+                           pack_bf16x2(g[6], g[7]));
+        }
+    }
+};
+
+__device__ __forceinline__ void mfma256_steps(const uint16_t (*As)[TP], const uint16_t (*Bs)[TP], f32x16_t (&acc)[4][4],
+                                              int kk0, int kk1) {
+    const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+    const int wm = w / 2, wn = w % 2;
+    const int lr = lane % 32, lh = lane / 32;
+#pragma unroll
+    for (int kk = kk0; kk < kk1; ++kk) {
+        bf16x8_t a[4], b[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = wm * 128 + i * 32 + lr;
+            a[i] = *reinterpret_cast<const bf16x8_t*>(&As[row][swz(row, kk * 2 + lh) * 8]);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int row = wn * 128 + j * 32 + lr;
+            b[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[row][swz(row, kk * 2 + lh) * 8]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+}
+
+template <typename F>
+__device__ __forceinline__ void for_each_acc256(const f32x16_t (&acc)[4][4], F&& fn) {
+    const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+    const int wm = w / 2, wn = w % 2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                fn(wm * 128 + i * 32 + (r / 4) * 8 + (lane / 32) * 4 + (r % 4), wn * 128 + j * 32 + lane % 32,
+                   acc[i][j][r]);
+}
+
+// Workgroup -> tile map: tiles along the short dimension ("inner", reused operand) that share a
+// long-dimension tile run on one XCD together (workgroups are dealt to the 8 XCDs round-robin).
+__device__ __forceinline__ bool tile_of(int inner_count, int outer_count, bool inner_is_m, int* tm, int* tn) {
+    const int id = blockIdx.x;
+    const int xcd = id % 8, rest = id / 8;
+    const int inner = rest % inner_count, og = rest / inner_count;
+    const int outer = og * 8 + xcd;
+    if (outer >= outer_count) return false;
+    *tm = inner_is_m ? inner : outer;
+    *tn = inner_is_m ? outer : inner;
+    return true;
+}
+
+// C[m][n] = sum_k A(m, k) B(k, n) for dW (A = H^T k-contiguous, B = G from R) or dH (A = G from R,
+// B = W). Output fp32 (with beta) or TO, or fp32 split-K partials.
+template <bool IS_DW, typename TO>
+__global__ __launch_bounds__(256, 1) void mfma256_kernel(const uint16_t* __restrict__ Xa, int64_t lda,
+                                                         const uint16_t* __restrict__ Xb, int64_t ldb, int M, int Nn,
+                                                         int K, int kps, int inner_count, int outer_count, Fold f,
+                                                         TO* __restrict__ out, int64_t ldo, float beta,
+                                                         float* __restrict__ part) {
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][TB][TP];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][TB][TP];
+    int tm, tn;
+    if (!tile_of(inner_count, outer_count, IS_DW, &tm, &tn)) return;
+    const int m0 = tm * TB, n0 = tn * TB;
+    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
+    const float alpha = f.scal[0];
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    StageKC256<!IS_DW> sa;   // dW: A = H^T (no fold); dH: A = G from R (fold)
+    typename std::conditional<IS_DW, StageGt256, StageKC256<false>>::type sb;
+    sa.init_rows(M, m0, f);
+    if constexpr (IS_DW) sb.init_cols(Nn, n0, f);
+    auto load_tiles = [&](int k0) {
+        sa.load(Xa, lda, M, m0, k0, ke);
+        if constexpr (IS_DW) sb.load(Xb, ldb, Nn, n0, k0, ke);
+        else sb.load(Xb, ldb, Nn, n0, k0, ke);
+    };
+    const int nk = (ke - kb + TK - 1) / TK;
+    if (nk > 0) {
+        load_tiles(kb);
+        sa.store(As[0], kb, ke, f, alpha);
+        sb.store(Bs[0], kb, ke, f, alpha);
+    }
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        const bool more = kt + 1 < nk;
+        const int k1 = kb + (kt + 1) * TK;
+        if (more) load_tiles(k1);
+        mfma256_steps(As[buf], Bs[buf], acc, 0, 2);
+        if (more) sa.store(As[buf ^ 1], k1, ke, f, alpha);
+        mfma256_steps(As[buf], Bs[buf], acc, 2, 4);
+        if (more) sb.store(Bs[buf ^ 1], k1, ke, f, alpha);
+        __syncthreads();
+    }
+    if (part == nullptr) {
+        for_each_acc256(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) {
+                if constexpr (IS_DW) {
+                    float* p = reinterpret_cast<float*>(out) + (int64_t)m * ldo + n;
+                    *p = beta != 0.f ? v + beta * *p : v;
+                } else {
+                    stf<TO>(out, (int64_t)m * ldo + n, v);
+                }
+            }
+        });
+    } else {
+        float* pz = part + (int64_t)blockIdx.z * M * Nn;
+        for_each_acc256(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = v;
+        });
+    }
+}
+
+// H [N][d] -> H^T [d][N] (bf16), 64 x 64 tiles through LDS.
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ H, int64_t ldh, int N, int d,
+                                                             uint16_t* __restrict__ Ht) {
+    __shared__ uint16_t tile[64][66];
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int t = threadIdx.x;
+    for (int e = t; e < 64 * 64; e += 256) {
+        const int r = e / 64, c = e % 64;
+        tile[r][c] = (r0 + r < N && c0 + c < d) ? H[(int64_t)(r0 + r) * ldh + c0 + c] : (uint16_t)0;
+    }
+    __syncthreads();
+    for (int e = t; e < 64 * 64; e += 256) {
+        const int c = e / 64, r = e % 64;
+        if (c0 + c < d && r0 + r < N) Ht[(int64_t)(c0 + c) * N + r0 + r] = tile[r][c];
+    }
+}
+
 // Split-K reduction in split order: out = sum_z part[z] (+ beta * out for dW).
 template <typename TO>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int splits, int M, int Nn,
@@ -475,28 +728,55 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 }
 
 // ---- planning ------------------------------------------------------------------------------------
-constexpr int kTargetWGs = 512;   // two waves of workgroups per CU on 256 CUs
+constexpr int kCUs = 256;        // MI355X compute units
 constexpr int kMaxSplits = 8;
 
-int splits_for(int64_t tiles, int64_t K, int ktile) {
-    int s = 1;
-    while (s < kMaxSplits && tiles * s < kTargetWGs && K / (2LL * s) >= 4LL * ktile) s *= 2;
-    return s;
-}
-
+enum GemmKind { kSimt = 0, kMfma128 = 1, kMfma256 = 2 };
+struct GemmPlan {
+    int kind, splits;
+};
 struct Plan {
-    bool mfma;
-    int sw, sh;   // split-K factors of dW and dH
+    GemmPlan w, h;
 };
 
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Split-K factor: modelled time = rounds of resident workgroups x per-tile k work, plus the
+// partial-sum traffic (write and read of fp32 partials) at streaming bandwidth.
+int choose_splits(int64_t tiles, int64_t M, int64_t N, int64_t K, int tb, int ktile, int per_cu) {
+    const double tile_flop_rate = 2.0 * 2.5e15 / kCUs / per_cu / 2;  // ~half of the per-workgroup MFMA share
+    int best = 1;
+    double best_t = 1e300;
+    for (int s = 1; s <= kMaxSplits; ++s) {
+        const int64_t kps = cdiv(cdiv(K, s), ktile) * ktile;
+        if (s > 1 && kps < 4LL * ktile) break;
+        const int64_t units = tiles * s;
+        const int64_t rounds = cdiv(units, (int64_t)kCUs * per_cu);
+        double t = rounds * (2.0 * tb * tb * kps) / tile_flop_rate;
+        if (s > 1) t += (2.0 * s + 1.0) * 4.0 * M * N / 5e12;
+        if (t < best_t * 0.98) {
+            best_t = t;
+            best = s;
+        }
+    }
+    return best;
+}
+
+GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K) {
+    if (!mfma || !big_ok) return {kSimt, choose_splits(cdiv(M, SB) * cdiv(N, SB), M, N, K, SB, SK, 4)};
+    const int64_t t256 = cdiv(M, TB) * cdiv(N, TB);
+    if (big_ok && t256 >= 24 && K >= 4 * TK) return {kMfma256, choose_splits(t256, M, N, K, TB, TK, 1)};
+    return {kMfma128, choose_splits(cdiv(M, MB) * cdiv(N, MB), M, N, K, MB, MK, 2)};
+}
+
 Plan make_plan(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
+    const bool mfma = dt == BOM_BF16;
     Plan p;
-    p.mfma = dt == BOM_BF16;
-    const int tb = p.mfma ? MB : SB, kt = p.mfma ? MK : SK;
-    const int64_t tw = ((d + tb - 1) / tb) * ((V + tb - 1) / tb);
-    const int64_t th = ((N + tb - 1) / tb) * ((d + tb - 1) / tb);
-    p.sw = splits_for(tw, N, kt);
-    p.sh = splits_for(th, V, kt);
+    // the MFMA kernels load whole 16-byte chunks: extents along k and along contiguous rows must be
+    // multiples of 8 (H^T rows have N elements); other shapes use the SIMT kernels
+    const bool m8 = N % 8 == 0 && d % 8 == 0 && V % 8 == 0;
+    p.w = plan_gemm(mfma, m8, d, V, N);   // dW: M = d, N = V, K = rows
+    p.h = plan_gemm(mfma, m8, N, d, V);   // dH: M = rows, N = d, K = V
     return p;
 }
 
@@ -506,40 +786,67 @@ VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     w.cq_off = 0;
     w.vmask_off = align256((size_t)V * 4);
     w.scal_off = align256(w.vmask_off + (size_t)N * 4);
-    w.part_off = align256(w.scal_off + 16);
-    size_t pw = p.sw > 1 ? (size_t)p.sw * d * V * 4 : 0;
-    size_t ph = p.sh > 1 ? (size_t)p.sh * N * d * 4 : 0;
+    w.ht_off = align256(w.scal_off + 16);
+    const size_t ht = p.w.kind == kMfma256 ? (size_t)d * N * 2 : 0;
+    w.part_off = align256(w.ht_off + ht);
+    size_t pw = p.w.splits > 1 ? (size_t)p.w.splits * d * V * 4 : 0;
+    size_t ph = p.h.splits > 1 ? (size_t)p.h.splits * N * d * 4 : 0;
     w.total = align256(w.part_off + (pw > ph ? pw : ph));
     return w;
 }
 
 template <typename TO>
-hipError_t run_dH(const HeadVjpArgs& a, const Plan& p, const Fold& f, float* part, bool mfma_ok, hipStream_t st) {
-    TO* out = static_cast<TO*>(a.dH);
-    const int M = a.N, Nn = a.d, K = a.V;
-    const int tb = mfma_ok ? MB : SB, ktile = mfma_ok ? MK : SK;
-    const int splits = p.sh;
-    int kps = (K + splits - 1) / splits;
-    kps = (kps + ktile - 1) / ktile * ktile;
-    dim3 grid((Nn + tb - 1) / tb, (M + tb - 1) / tb, splits);
+hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, const void* B, int64_t ldb, bom_dtype dt,
+                    int M, int Nn, int K, const Fold& f, TO* out, int64_t ldo, float beta, float* part, hipStream_t st) {
+    const int splits = g.splits;
+    const int tb = g.kind == kMfma256 ? TB : (g.kind == kMfma128 ? MB : SB);
+    const int ktile = g.kind == kMfma256 ? TK : (g.kind == kMfma128 ? MK : SK);
+    int kps = (int)(cdiv(cdiv(K, splits), ktile) * ktile);
     float* pz = splits > 1 ? part : nullptr;
-    if (mfma_ok) {
-        hipLaunchKernelGGL(mfma_dH_kernel<TO>, grid, dim3(256), 0, st, static_cast<const uint16_t*>(a.R), a.ldr,
-                           static_cast<const uint16_t*>(a.W), a.ldw, M, Nn, K, kps, f, out, a.lddh, pz);
-    } else if (a.dt == BOM_BF16) {
-        hipLaunchKernelGGL((simt_dH_kernel<uint16_t, TO>), grid, dim3(256), 0, st, static_cast<const uint16_t*>(a.R),
-                           a.ldr, static_cast<const uint16_t*>(a.W), a.ldw, M, Nn, K, kps, f, out, a.lddh, part,
-                           splits > 1 ? 0 : 1);
+    const uint16_t* a16 = static_cast<const uint16_t*>(A);
+    const uint16_t* b16 = static_cast<const uint16_t*>(B);
+    if (g.kind == kMfma256) {
+        const int MT = (int)cdiv(M, TB), NT = (int)cdiv(Nn, TB);
+        const int inner = is_dw ? MT : NT, outer = is_dw ? NT : MT;
+        dim3 grid((unsigned)(cdiv(outer, 8) * 8 * inner), 1, splits);
+        if (is_dw)
+            hipLaunchKernelGGL((mfma256_kernel<true, float>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
+                               inner, outer, f, reinterpret_cast<float*>(out), ldo, beta, pz);
+        else
+            hipLaunchKernelGGL((mfma256_kernel<false, TO>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
+                               inner, outer, f, out, ldo, beta, pz);
     } else {
-        hipLaunchKernelGGL((simt_dH_kernel<float, TO>), grid, dim3(256), 0, st, static_cast<const float*>(a.R), a.ldr,
-                           static_cast<const float*>(a.W), a.ldw, M, Nn, K, kps, f, out, a.lddh, part,
-                           splits > 1 ? 0 : 1);
+        dim3 grid((unsigned)cdiv(Nn, tb), (unsigned)cdiv(M, tb), splits);
+        if (g.kind == kMfma128) {
+            if (is_dw)
+                hipLaunchKernelGGL(mfma_dW_kernel, grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps, f,
+                                   reinterpret_cast<float*>(out), ldo, beta, pz);
+            else
+                hipLaunchKernelGGL(mfma_dH_kernel<TO>, grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps, f, out,
+                                   ldo, pz);
+        } else if (dt == BOM_BF16) {
+            if (is_dw)
+                hipLaunchKernelGGL(simt_dW_kernel<uint16_t>, grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps, f,
+                                   splits > 1 ? part : reinterpret_cast<float*>(out), ldo, beta, splits > 1 ? 0 : 1);
+            else
+                hipLaunchKernelGGL((simt_dH_kernel<uint16_t, TO>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K,
+                                   kps, f, out, ldo, part, splits > 1 ? 0 : 1);
+        } else {
+            const float* a32 = static_cast<const float*>(A);
+            const float* b32 = static_cast<const float*>(B);
+            if (is_dw)
+                hipLaunchKernelGGL(simt_dW_kernel<float>, grid, dim3(256), 0, st, a32, lda, b32, ldb, M, Nn, K, kps, f,
+                                   splits > 1 ? part : reinterpret_cast<float*>(out), ldo, beta, splits > 1 ? 0 : 1);
+            else
+                hipLaunchKernelGGL((simt_dH_kernel<float, TO>), grid, dim3(256), 0, st, a32, lda, b32, ldb, M, Nn, K, kps,
+                                   f, out, ldo, part, splits > 1 ? 0 : 1);
+        }
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
     const int64_t MN = (int64_t)M * Nn;
-    hipLaunchKernelGGL(splitk_reduce_kernel<TO>, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, st, part, splits, M,
-                       Nn, out, a.lddh, 0.f);
+    hipLaunchKernelGGL(splitk_reduce_kernel<TO>, dim3((unsigned)cdiv(MN, 256)), dim3(256), 0, st, part, splits, M, Nn, out,
+                       ldo, beta);
     return hipGetLastError();
 }
 
@@ -549,11 +856,12 @@ size_t head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
 
 hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
     const VjpWs L = vjp_ws(a.N, a.d, a.V, a.dt);
-    const Plan p = make_plan(a.N, a.d, a.V, a.dt);
+    Plan p = make_plan(a.N, a.d, a.V, a.dt);
     char* base = static_cast<char*>(a.ws);
     float* cq = reinterpret_cast<float*>(base + L.cq_off);
     float* vmask = reinterpret_cast<float*>(base + L.vmask_off);
     float* scal = reinterpret_cast<float*>(base + L.scal_off);
+    uint16_t* ht = reinterpret_cast<uint16_t*>(base + L.ht_off);
     float* part = reinterpret_cast<float*>(base + L.part_off);
     const int nprep = (a.V > a.N ? a.V : a.N);
     hipLaunchKernelGGL(vjp_prep_kernel, dim3((nprep + 255) / 256), dim3(256), 0, st, a.q_hat, a.s, a.n_valid, a.lambda,
@@ -562,45 +870,36 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
     if (e != hipSuccess) return e;
     const Fold f{cq, vmask, scal};
 
-    // The MFMA path stages 16-byte rows: leading dimensions multiples of 8 and 16-byte bases.
+    // MFMA kernels stage 16-byte rows: leading dimensions multiples of 8 and 16-byte bases;
+    // otherwise the SIMT kernels (same plan shape, SIMT tiles) run.
     auto al = [](const void* ptr, int64_t ld) { return reinterpret_cast<uintptr_t>(ptr) % 16 == 0 && ld % 8 == 0; };
-    const bool mfma_ok = p.mfma && al(a.H, a.ldh) && al(a.W, a.ldw) && al(a.R, a.ldr);
+    if (a.dt == BOM_BF16 && !(al(a.H, a.ldh) && al(a.W, a.ldw) && al(a.R, a.ldr))) {
+        // same split factors (the workspace holds their partials), SIMT tiles
+        p.w.kind = kSimt;
+        p.h.kind = kSimt;
+    }
 
-    // dW
-    {
-        const int M = a.d, Nn = a.V, K = a.N;
-        const int tb = mfma_ok ? MB : SB, ktile = mfma_ok ? MK : SK;
-        const int splits = p.sw;
-        int kps = (K + splits - 1) / splits;
-        kps = (kps + ktile - 1) / ktile * ktile;
-        dim3 grid((Nn + tb - 1) / tb, (M + tb - 1) / tb, splits);
-        float* pz = splits > 1 ? part : nullptr;
-        if (mfma_ok) {
-            hipLaunchKernelGGL(mfma_dW_kernel, grid, dim3(256), 0, st, static_cast<const uint16_t*>(a.H), a.ldh,
-                               static_cast<const uint16_t*>(a.R), a.ldr, M, Nn, K, kps, f, a.dW, a.lddw, a.dW_beta, pz);
-        } else if (a.dt == BOM_BF16) {
-            hipLaunchKernelGGL(simt_dW_kernel<uint16_t>, grid, dim3(256), 0, st, static_cast<const uint16_t*>(a.H), a.ldh,
-                               static_cast<const uint16_t*>(a.R), a.ldr, M, Nn, K, kps, f, splits > 1 ? part : a.dW,
-                               a.lddw, a.dW_beta, splits > 1 ? 0 : 1);
-        } else {
-            hipLaunchKernelGGL(simt_dW_kernel<float>, grid, dim3(256), 0, st, static_cast<const float*>(a.H), a.ldh,
-                               static_cast<const float*>(a.R), a.ldr, M, Nn, K, kps, f, splits > 1 ? part : a.dW, a.lddw,
-                               a.dW_beta, splits > 1 ? 0 : 1);
-        }
+    // dW = H^T G
+    const void* A = a.H;
+    int64_t lda = a.ldh;
+    if (p.w.kind == kMfma256) {
+        dim3 tg((unsigned)cdiv(a.d, 64), (unsigned)cdiv(a.N, 64));
+        hipLaunchKernelGGL(transpose_bf16_kernel, tg, dim3(256), 0, st, static_cast<const uint16_t*>(a.H), a.ldh, a.N, a.d,
+                           ht);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
-        if (splits > 1) {
-            const int64_t MN = (int64_t)M * Nn;
-            hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, st, part,
-                               splits, M, Nn, a.dW, a.lddw, a.dW_beta);
-            e = hipGetLastError();
-            if (e != hipSuccess) return e;
-        }
+        A = ht;
+        lda = a.N;
     }
-    // dH (shares the split-K buffer: same stream, so it runs after the dW reduction)
+    e = run_gemm<float>(true, p.w, A, lda, a.R, a.ldr, a.dt, a.d, a.V, a.N, f, a.dW, a.lddw, a.dW_beta, part, st);
+    if (e != hipSuccess) return e;
+    // dH = G W^T (shares the split-K buffer: same stream, so it runs after the dW reduction)
     if (a.dH) {
-        if (a.dh_dt == BOM_BF16) return run_dH<uint16_t>(a, p, f, part, mfma_ok, st);
-        return run_dH<float>(a, p, f, part, mfma_ok, st);
+        if (a.dh_dt == BOM_BF16)
+            return run_gemm<uint16_t>(false, p.h, a.R, a.ldr, a.W, a.ldw, a.dt, a.N, a.d, a.V, f,
+                                      static_cast<uint16_t*>(a.dH), a.lddh, 0.f, part, st);
+        return run_gemm<float>(false, p.h, a.R, a.ldr, a.W, a.ldw, a.dt, a.N, a.d, a.V, f, static_cast<float*>(a.dH),
+                               a.lddh, 0.f, part, st);
     }
     return hipSuccess;
 }

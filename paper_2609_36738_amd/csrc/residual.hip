@@ -135,13 +135,11 @@ __global__ __launch_bounds__(THREADS) void residual_rows_kernel(
         for (int c = 0; c < NCH; ++c) {
             const int col = (c * THREADS + tid) * VEC;
             if constexpr (PACKED) {
-                if (col < V) {
-                    const uint4 u = *reinterpret_cast<const uint4*>(zr + col);
-                    xw[c * 4 + 0] = u.x; xw[c * 4 + 1] = u.y; xw[c * 4 + 2] = u.z; xw[c * 4 + 3] = u.w;
-                } else {
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) xw[c * 4 + k] = 0xFF80FF80u;  // a pair of bf16 -inf
-                }
+                const bool ok = col < V;
+                const uint4 u = *reinterpret_cast<const uint4*>(zr + (ok ? col : V - VEC));
+                const uint32_t m = lane_mask(ok), fb = 0xFF80FF80u & ~m;  // padding: a pair of bf16 -inf
+                xw[c * 4 + 0] = (u.x & m) | fb; xw[c * 4 + 1] = (u.y & m) | fb;
+                xw[c * 4 + 2] = (u.z & m) | fb; xw[c * 4 + 3] = (u.w & m) | fb;
             } else {
                 load_chunk<T, VEC>(zr, col, V, -INFINITY, &x[c * VEC]);
             }

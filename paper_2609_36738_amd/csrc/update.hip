@@ -35,27 +35,30 @@ __device__ __forceinline__ void adam_style(float& th, float& v, float up, float 
     th = (1.0f - sc.lr * wd) * th - sc.lr * (up / (sqrtf(vhat) + sc.eps));
 }
 
-// ---- dense ---------------------------------------------------------------------------------
+// ---- dense ----------------------------------------------------------------------------------
+// One 16-byte group per thread, non-temporal loads and stores (each byte is touched once).
 template <bool SPLIT>
 __global__ __launch_bounds__(kUpdThreads) void update_dense_vec4_kernel(float* __restrict__ theta, float* __restrict__ v,
                                                                         const float* __restrict__ u,
                                                                         const float* __restrict__ h, int64_t nvec,
                                                                         SegTable segs, UpdateScalars sc) {
-    const int64_t stride = (int64_t)gridDim.x * kUpdThreads;
-    for (int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x; q < nvec; q += stride) {
-        float4 t4 = reinterpret_cast<const float4*>(theta)[q];
-        float4 v4 = reinterpret_cast<const float4*>(v)[q];
-        const float4 u4 = reinterpret_cast<const float4*>(u)[q];
-        float4 h4 = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (SPLIT) h4 = reinterpret_cast<const float4*>(h)[q];
-        const int64_t e = q * 4;
-        adam_style(t4.x, v4.x, numerator<SPLIT>(u4.x, h4.x, sc), decay_of(e + 0, segs), sc);
-        adam_style(t4.y, v4.y, numerator<SPLIT>(u4.y, h4.y, sc), decay_of(e + 1, segs), sc);
-        adam_style(t4.z, v4.z, numerator<SPLIT>(u4.z, h4.z, sc), decay_of(e + 2, segs), sc);
-        adam_style(t4.w, v4.w, numerator<SPLIT>(u4.w, h4.w, sc), decay_of(e + 3, segs), sc);
-        reinterpret_cast<float4*>(theta)[q] = t4;
-        reinterpret_cast<float4*>(v)[q] = v4;
+    const int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x;
+    if (q >= nvec) return;
+    const int64_t e = q * 4;
+    f32x4 t4 = ld_stream(theta + e);
+    f32x4 v4 = ld_stream(v + e);
+    const f32x4 u4 = ld_stream(u + e);
+    f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
+    if (SPLIT) h4 = ld_stream(h + e);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        float th = t4[c], vv = v4[c];
+        adam_style(th, vv, numerator<SPLIT>(u4[c], h4[c], sc), decay_of(e + c, segs), sc);
+        t4[c] = th;
+        v4[c] = vv;
     }
+    st_stream(theta + e, t4);
+    st_stream(v + e, v4);
 }
 
 template <bool SPLIT>
@@ -266,8 +269,7 @@ hipError_t launch_update_dense(float* theta, float* v, const float* u, const flo
     int64_t done = 0;
     if (aligned && P >= 4) {
         const int64_t nvec = P / 4;
-        int64_t grid = (nvec + kUpdThreads - 1) / kUpdThreads;
-        if (grid > 8192) grid = 8192;
+        const int64_t grid = (nvec + kUpdThreads - 1) / kUpdThreads;
         if (h)
             hipLaunchKernelGGL(update_dense_vec4_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v, u,
                                h, nvec, segs, sc);

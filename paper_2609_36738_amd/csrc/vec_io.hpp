@@ -67,14 +67,16 @@ __device__ __forceinline__ void store_scalar<uint16_t>(uint16_t* p, float x) { *
 // Load VEC consecutive elements starting at column `col` (a multiple of VEC) of a row whose
 // length V is a multiple of VEC, so a chunk is wholly inside or wholly outside the row;
 // outside chunks read as `fill`.
+// The load itself is unconditional (a clamped in-range address), so the compiler keeps every chunk's
+// load in flight together instead of sinking each one into a branch.
 template <typename T, int VEC>
 __device__ __forceinline__ void load_chunk(const T* row, int col, int V, float fill, float* x) {
-    if (col < V) {
-        VecIO<T, VEC>::load(row + col, x);
-    } else {
+    const bool ok = col < V;
+    VecIO<T, VEC>::load(row + (ok ? col : V - VEC), x);
+    const uint32_t m = lane_mask(ok);
+    const uint32_t fb = __float_as_uint(fill) & ~m;
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) x[k] = fill;
-    }
+    for (int k = 0; k < VEC; ++k) x[k] = __uint_as_float((__float_as_uint(x[k]) & m) | fb);
 }
 
 template <typename T, int VEC>

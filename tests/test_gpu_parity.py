@@ -134,6 +134,8 @@ VJP_CASES = [
     ("bf16_vision_head", 1024, 768, 1000, "bf16", 0.0),
     ("bf16_v4096", 512, 256, 4096, "bf16", 0.05),
     ("bf16_dH_splitk", 64, 128, 32000, "bf16", 0.0),
+    ("bf16_tile256", 2048, 768, 4096, "bf16", 0.0),
+    ("bf16_tile256_ragged_mnk", 2056, 520, 6000, "bf16", 0.05),
 ]
 
 

@@ -25,30 +25,44 @@ typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 struct Fold {
     const float* cq;     // [V] lambda * q_hat / N_t
     const float* vmask;  // [N] 1 for rows in I, else 0
-    const float* scal;   // [0] = alpha = (1 - lambda) / N_t
+    const float* scal;   // [0] alpha = (1 - lambda) / N_t; [1] s_out; [2], [3] bf16 pairs (r_coef, 0), (0, r_coef)
+    const float* cqp;    // [V] history term of the rescaled fold G = s_out * (r_coef * R + cqp)
 };
 
 struct VjpWs {
-    size_t cq_off, vmask_off, scal_off, ht_off, part_off, total;
+    size_t cq_off, cqp_off, vmask_off, scal_off, ht_off, part_off, total;
 };
 
 // ---- prep -------------------------------------------------------------------------------------
+// G = alpha R + mask * cq  (alpha = (1-lambda)/N_t, cq = lambda q_hat / N_t) is also written
+// G = s_out (r_coef R + mask * cqp): for lambda < 1, s_out = alpha, r_coef = 1, cqp = lambda/(1-lambda) q_hat;
+// for lambda = 1, s_out = 1/N_t, r_coef = 0, cqp = q_hat. The large-tile kernels fold cqp with one
+// bf16 dot product per element and apply s_out to the fp32 accumulators.
 __global__ __launch_bounds__(256) void vjp_prep_kernel(const float* __restrict__ q_hat, const float* __restrict__ s,
                                                        const int32_t* __restrict__ n_valid, float lambda, int V, int N,
                                                        const int32_t* __restrict__ labels, int32_t ignore_index,
-                                                       float* __restrict__ cq, float* __restrict__ vmask,
-                                                       float* __restrict__ scal, float* __restrict__ db) {
+                                                       float* __restrict__ cq, float* __restrict__ cqp,
+                                                       float* __restrict__ vmask, float* __restrict__ scal,
+                                                       float* __restrict__ db) {
     const int idx = blockIdx.x * 256 + threadIdx.x;
     const int nt = *n_valid;
+    const bool hist_only = !(lambda < 1.0f);
     if (idx < V) {
         cq[idx] = nt > 0 ? (float)((double)lambda * (double)q_hat[idx] / (double)nt) : 0.f;
+        cqp[idx] = hist_only ? q_hat[idx] : (float)((double)lambda / (1.0 - (double)lambda) * (double)q_hat[idx]);
         if (db) db[idx] = nt > 0 ? (1.0f - lambda) * s[idx] + lambda * q_hat[idx] : 0.f;
     }
     if (idx < N) {
         bool bad = false;
         vmask[idx] = label_valid(labels[idx], V, ignore_index, &bad) ? 1.f : 0.f;
     }
-    if (idx == 0) scal[0] = nt > 0 ? (float)((1.0 - (double)lambda) / (double)nt) : 0.f;
+    if (idx == 0) {
+        scal[0] = nt > 0 ? (float)((1.0 - (double)lambda) / (double)nt) : 0.f;
+        scal[1] = nt > 0 ? (hist_only ? (float)(1.0 / (double)nt) : scal[0]) : 0.f;
+        const uint32_t one = hist_only ? 0u : 0x3F80u;   // bf16 1.0 (or 0 when R drops out)
+        scal[2] = __uint_as_float(one);
+        scal[3] = __uint_as_float(one << 16);
+    }
 }
 
 template <typename T>
@@ -450,29 +464,41 @@ __global__ __launch_bounds__(256) void mfma_dH_kernel(const uint16_t* __restrict
 
 // ---- MFMA bf16, large tiles ------------------------------------------------------------------------
 // 256 x 256 output tile, 4 waves each owning 128 x 128 (4 x 4 blocks of v_mfma_f32_32x32x16_bf16),
-// 64-deep k tiles double-buffered in LDS (2 x 2 x 36 KB). Rows of an LDS tile are 72 bf16 (144 B);
-// the 16-byte chunk c of row r is stored at chunk c ^ ((r >> 4) & 7), which keeps both the staging
-// writes and the fragment reads free of bank conflicts.
+// 64-deep k tiles double-buffered in LDS (2 x 2 x 32 KB). LDS rows are 64 bf16 (128 B, no padding);
+// the 16-byte chunk c of row r lives at chunk c ^ ((r ^ (r >> 3)) & 7), which measured free of bank
+// conflicts on gfx950 for the fragment reads and for both staging write patterns below.
 constexpr int TB = 256;
 constexpr int TK = 64;
-constexpr int TP = 72;
+constexpr int TP = 64;
 
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 4) & 7); }
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
+
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c, false);
+}
 
 // k-contiguous operand: tile rows r0..r0+255 of X (k extent kend, a multiple of 8), k chunk
-// (t % 8) * 8 of rows e * 32 + t / 8, e < 8. FOLD: G = fma(alpha, R, mask_row * cq_k) in bf16.
+// (t % 8) * 8 of rows e * 32 + t / 8, e < 8. FOLD (dH's A = G from R): G' = r_coef R + cqp_k in
+// fp32 by dot products, rounded to bf16 pairs, zeroed for rows outside I.
 template <bool FOLD>
 struct StageKC256 {
     uint4 r[8];
-    uint32_t mk[8];
-    float vm[FOLD ? 8 : 1];
+    uint32_t mk[8];               // per chunk: row in range (and, FOLD, in I) and k chunk in range
+    uint32_t rowok[FOLD ? 8 : 1]; // FOLD: row in range and in I (loop-invariant)
+    float4 cq4[FOLD ? 2 : 1];
+    const float* cqp_;
+    uint32_t one_lo_, one_hi_;
     __device__ __forceinline__ void init_rows(int rows, int r0, const Fold& f) {
+        cqp_ = f.cqp;
+        one_lo_ = __float_as_uint(f.scal[2]);
+        one_hi_ = __float_as_uint(f.scal[3]);
         if (FOLD) {
             const int t = threadIdx.x;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int row = r0 + e * 32 + t / 8;
-                vm[e] = row < rows ? f.vmask[row] : 0.f;
+                rowok[e] = row < rows && f.vmask[row < rows ? row : rows - 1] != 0.f;
             }
         }
     }
@@ -484,91 +510,91 @@ struct StageKC256 {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int row = r0 + e * 32 + t / 8;
-            mk[e] = lane_mask(kok && row < rows);
+            mk[e] = lane_mask(kok && (FOLD ? rowok[e] != 0u : row < rows));
             r[e] = ld16(X + (int64_t)(row < rows ? row : rows - 1) * ldx + kc);
         }
+        if (FOLD) {
+            cq4[0] = *reinterpret_cast<const float4*>(cqp_ + kc);
+            cq4[1] = *reinterpret_cast<const float4*>(cqp_ + kc + 4);
+        }
     }
-    __device__ __forceinline__ void store(uint16_t (*S)[TP], int k0, int kend, const Fold& f, float alpha) const {
+    __device__ __forceinline__ void store(uint16_t (*S)[TP]) const {
         const int t = threadIdx.x;
         const int ch = t % 8;
-        float cq[8];
-        if (FOLD) {
-            const int k = k0 + ch * 8;
-            const bool kok = k < kend;
-            const float4 c0 = *reinterpret_cast<const float4*>(f.cq + (kok ? k : kend - 8));
-            const float4 c1 = *reinterpret_cast<const float4*>(f.cq + (kok ? k : kend - 8) + 4);
-            const float z = kok ? 1.f : 0.f;
-            cq[0] = z * c0.x; cq[1] = z * c0.y; cq[2] = z * c0.z; cq[3] = z * c0.w;
-            cq[4] = z * c1.x; cq[5] = z * c1.y; cq[6] = z * c1.z; cq[7] = z * c1.w;
-        }
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int lr = e * 32 + t / 8;
-            uint4 o = and_mask(r[e], mk[e]);
+            uint4 o = r[e];
             if (FOLD) {
                 const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+                const float cq[8] = {cq4[0].x, cq4[0].y, cq4[0].z, cq4[0].w, cq4[1].x, cq4[1].y, cq4[1].z, cq4[1].w};
                 uint32_t g[4];
 #pragma unroll
                 for (int p = 0; p < 4; ++p)
-                    g[p] = pack_bf16x2(fmaf(alpha, bf16_lo(w[p]), vm[e] * cq[2 * p]),
-                                       fmaf(alpha, bf16_hi(w[p]), vm[e] * cq[2 * p + 1]));
+                    g[p] = pack_bf16x2(dot2(w[p], one_lo_, cq[2 * p]), dot2(w[p], one_hi_, cq[2 * p + 1]));
                 o = make_uint4(g[0], g[1], g[2], g[3]);
             }
-            *reinterpret_cast<uint4*>(&S[lr][swz(lr, ch) * 8]) = o;
+            *reinterpret_cast<uint4*>(&S[lr][swz(lr, ch) * 8]) = and_mask(o, mk[e]);
         }
     }
 };
 
 // dW's B operand: G(k, n) from R[k][n] (n contiguous, Nn a multiple of 8). Thread t stages k rows
-// kq*8..+7 and columns nq*8..+7 (kq = t / 32, nq = t % 32), folds, and writes 8 k values per
-// column: the transpose.
+// kq*8..+7 and columns nq*8..+7 (kq = t / 32, nq = t % 32): G' = r_coef R + cqp_n by dot products,
+// then pairs (k, k+1) of one column are packed to bf16 -- the transpose -- and masked per row.
 struct StageGt256 {
     uint4 r[8];
-    uint32_t mk[8];
+    float vmr[8];     // row masks as loaded (consumed only at store time, after the MFMA phase)
+    int kbase;        // first k row of this thread in the staged tile
+    int kend_;
+    bool nok_;
     float cqn[8];
+    const float* vmask_;
+    uint32_t one_lo_, one_hi_;
     __device__ __forceinline__ void init_cols(int Nn, int n0, const Fold& f) {
+        vmask_ = f.vmask;
+        one_lo_ = __float_as_uint(f.scal[2]);
+        one_hi_ = __float_as_uint(f.scal[3]);
         const int n = n0 + (threadIdx.x % 32) * 8;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) cqn[c] = (n + c < Nn) ? f.cq[n + c] : 0.f;
+        for (int c = 0; c < 8; ++c) cqn[c] = (n + c < Nn) ? f.cqp[n + c] : 0.f;
     }
     __device__ __forceinline__ void load(const uint16_t* R, int64_t ldr, int Nn, int n0, int k0, int kend) {
         const int t = threadIdx.x, kq = t / 32, nq = t % 32;
         const int n = n0 + nq * 8;
-        const bool nok = n < Nn;
-        const int nc = nok ? n : Nn - 8;
+        nok_ = n < Nn;
+        kend_ = kend;
+        kbase = k0 + kq * 8;
+        const int nc = nok_ ? n : Nn - 8;
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            const int k = k0 + kq * 8 + q;
-            mk[q] = lane_mask(nok && k < kend);
+            const int k = kbase + q;
             r[q] = ld16(R + (int64_t)(k < kend ? k : kend - 1) * ldr + nc);
+            vmr[q] = vmask_[k < kend ? k : kend - 1];
         }
     }
-    __device__ __forceinline__ void store(uint16_t (*S)[TP], int k0, int kend, const Fold& f, float alpha) const {
+    __device__ __forceinline__ void store(uint16_t (*S)[TP]) const {
         const int t = threadIdx.x, kq = t / 32, nq = t % 32;
-        float vm[8];
+        uint32_t pm[4];   // masks of the packed (k, k+1) pairs: row in range and in I, column in range
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int k = k0 + kq * 8 + q;
-            vm[q] = f.vmask[k < kend ? k : kend - 1] * (k < kend ? 1.f : 0.f);
+        for (int p = 0; p < 4; ++p) {
+            const bool o0 = nok_ && kbase + 2 * p < kend_ && vmr[2 * p] != 0.f;
+            const bool o1 = nok_ && kbase + 2 * p + 1 < kend_ && vmr[2 * p + 1] != 0.f;
+            pm[p] = (o0 ? 0x0000FFFFu : 0u) | (o1 ? 0xFFFF0000u : 0u);
         }
-        uint32_t w[8][4];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const uint4 v = and_mask(r[q], mk[q]);
-            w[q][0] = v.x; w[q][1] = v.y; w[q][2] = v.z; w[q][3] = v.w;
-        }
+        const uint32_t w[8][4] = {{r[0].x, r[0].y, r[0].z, r[0].w}, {r[1].x, r[1].y, r[1].z, r[1].w},
+                                  {r[2].x, r[2].y, r[2].z, r[2].w}, {r[3].x, r[3].y, r[3].z, r[3].w},
+                                  {r[4].x, r[4].y, r[4].z, r[4].w}, {r[5].x, r[5].y, r[5].z, r[5].w},
+                                  {r[6].x, r[6].y, r[6].z, r[6].w}, {r[7].x, r[7].y, r[7].z, r[7].w}};
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
-            float g[8];
+            const uint32_t one = (c & 1) ? one_hi_ : one_lo_;
+            uint32_t g[4];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const float rv = (c & 1) ? bf16_hi(w[q][c >> 1]) : bf16_lo(w[q][c >> 1]);
-                g[q] = fmaf(alpha, rv, vm[q] * cqn[c]);
-            }
+            for (int p = 0; p < 4; ++p)
+                g[p] = pack_bf16x2(dot2(w[2 * p][c >> 1], one, cqn[c]), dot2(w[2 * p + 1][c >> 1], one, cqn[c])) & pm[p];
             const int row = nq * 8 + c;
-            *reinterpret_cast<uint4*>(&S[row][swz(row, kq) * 8]) =
-                make_uint4(pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]), pack_bf16x2(g[4], g[5]),
-                           pack_bf16x2(g[6], g[7]));
+            *reinterpret_cast<uint4*>(&S[row][swz(row, kq) * 8]) = make_uint4(g[0], g[1], g[2], g[3]);
         }
     }
 };
@@ -639,7 +665,7 @@ __global__ __launch_bounds__(256, 1) void mfma256_kernel(const uint16_t* __restr
     if (!tile_of(inner_count, outer_count, IS_DW, &tm, &tn)) return;
     const int m0 = tm * TB, n0 = tn * TB;
     const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
-    const float alpha = f.scal[0];
+    const float s_out = f.scal[1];
     f32x16_t acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -652,27 +678,30 @@ __global__ __launch_bounds__(256, 1) void mfma256_kernel(const uint16_t* __restr
     typename std::conditional<IS_DW, StageGt256, StageKC256<false>>::type sb;
     sa.init_rows(M, m0, f);
     if constexpr (IS_DW) sb.init_cols(Nn, n0, f);
-    auto load_tiles = [&](int k0) {
-        sa.load(Xa, lda, M, m0, k0, ke);
-        if constexpr (IS_DW) sb.load(Xb, ldb, Nn, n0, k0, ke);
-        else sb.load(Xb, ldb, Nn, n0, k0, ke);
-    };
+    // Software pipeline: LDS holds tiles kt (being multiplied) and kt + 1 (being filled); the A and
+    // B register sets are refilled with tile kt + 2 right after they are written to LDS, so every
+    // global load has a whole iteration of MFMA work to arrive. The loop body has no branches (the
+    // last iterations load fully masked tiles and fill the idle buffer): control flow inside the
+    // loop would make the register allocator move the 256 accumulators between register files.
     const int nk = (ke - kb + TK - 1) / TK;
-    if (nk > 0) {
-        load_tiles(kb);
-        sa.store(As[0], kb, ke, f, alpha);
-        sb.store(Bs[0], kb, ke, f, alpha);
-    }
+    auto load_a = [&](int k0) { sa.load(Xa, lda, M, m0, k0, ke); };
+    auto load_b = [&](int k0) { sb.load(Xb, ldb, Nn, n0, k0, ke); };
+    load_a(kb);
+    load_b(kb);
+    sa.store(As[0]);
+    sb.store(Bs[0]);
+    load_a(kb + TK);
+    load_b(kb + TK);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
         const int buf = kt & 1;
-        const bool more = kt + 1 < nk;
-        const int k1 = kb + (kt + 1) * TK;
-        if (more) load_tiles(k1);
+        const int k2 = kb + (kt + 2) * TK;
+        sa.store(As[buf ^ 1]);
+        load_a(k2);
         mfma256_steps(As[buf], Bs[buf], acc, 0, 2);
-        if (more) sa.store(As[buf ^ 1], k1, ke, f, alpha);
+        sb.store(Bs[buf ^ 1]);
+        load_b(k2);
         mfma256_steps(As[buf], Bs[buf], acc, 2, 4);
-        if (more) sb.store(Bs[buf ^ 1], k1, ke, f, alpha);
         __syncthreads();
     }
     if (part == nullptr) {
@@ -681,9 +710,9 @@ __global__ __launch_bounds__(256, 1) void mfma256_kernel(const uint16_t* __restr
             if (m < M && n < Nn) {
                 if constexpr (IS_DW) {
                     float* p = reinterpret_cast<float*>(out) + (int64_t)m * ldo + n;
-                    *p = beta != 0.f ? v + beta * *p : v;
+                    *p = beta != 0.f ? s_out * v + beta * *p : s_out * v;
                 } else {
-                    stf<TO>(out, (int64_t)m * ldo + n, v);
+                    stf<TO>(out, (int64_t)m * ldo + n, s_out * v);
                 }
             }
         });
@@ -691,7 +720,7 @@ __global__ __launch_bounds__(256, 1) void mfma256_kernel(const uint16_t* __restr
         float* pz = part + (int64_t)blockIdx.z * M * Nn;
         for_each_acc256(acc, [&](int r, int c, float v) {
             const int m = m0 + r, n = n0 + c;
-            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = v;
+            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = s_out * v;
         });
     }
 }
@@ -784,7 +813,8 @@ VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     const Plan p = make_plan(N, d, V, dt);
     VjpWs w;
     w.cq_off = 0;
-    w.vmask_off = align256((size_t)V * 4);
+    w.cqp_off = align256((size_t)V * 4);
+    w.vmask_off = align256(w.cqp_off + (size_t)V * 4);
     w.scal_off = align256(w.vmask_off + (size_t)N * 4);
     w.ht_off = align256(w.scal_off + 16);
     const size_t ht = p.w.kind == kMfma256 ? (size_t)d * N * 2 : 0;
@@ -859,16 +889,17 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
     Plan p = make_plan(a.N, a.d, a.V, a.dt);
     char* base = static_cast<char*>(a.ws);
     float* cq = reinterpret_cast<float*>(base + L.cq_off);
+    float* cqp = reinterpret_cast<float*>(base + L.cqp_off);
     float* vmask = reinterpret_cast<float*>(base + L.vmask_off);
     float* scal = reinterpret_cast<float*>(base + L.scal_off);
     uint16_t* ht = reinterpret_cast<uint16_t*>(base + L.ht_off);
     float* part = reinterpret_cast<float*>(base + L.part_off);
     const int nprep = (a.V > a.N ? a.V : a.N);
     hipLaunchKernelGGL(vjp_prep_kernel, dim3((nprep + 255) / 256), dim3(256), 0, st, a.q_hat, a.s, a.n_valid, a.lambda,
-                       a.V, a.N, a.labels, a.ignore_index, cq, vmask, scal, a.db);
+                       a.V, a.N, a.labels, a.ignore_index, cq, cqp, vmask, scal, a.db);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const Fold f{cq, vmask, scal};
+    const Fold f{cq, vmask, scal, cqp};
 
     // MFMA kernels stage 16-byte rows: leading dimensions multiples of 8 and 16-byte bases;
     // otherwise the SIMT kernels (same plan shape, SIMT tiles) run.

@@ -176,6 +176,43 @@ def test_head_vjp_parity(case):
     assert (np.abs(gdw.sum(1)) <= (tol if dtype == "bf16" else 1e-4) * np.abs(gdw).sum(1) + 1e-12).all()
 
 
+@pytest.mark.parametrize("lam", [0.0, 1.0, 0.25])
+def test_head_vjp_tile256_lambda(lam):
+    """Large-tile path at the edges of the mixture: lambda = 0 (plain cross-entropy backward),
+    lambda = 1 (history only, the residual drops out of G) and an interior value."""
+    N, d, V = 2048, 768, 4096
+    log(f"[head_vjp] tile256 lambda={lam}")
+    Hh, Hd, Wh, Wd, Zh, Zd, y, q_prev, t = _vjp_inputs(N, d, V, "bf16", 0.05)
+    yd = torch.from_numpy(y).to(dev())
+    res = bom.bom_residual(Zd, yd)
+    q = torch.from_numpy(q_prev.copy()).to(dev())
+    qh = bom.bom_ema(q, res["s"], B1, t)
+    g = bom.bom_head_vjp(Hd, Wd, res["R"], yd, qh, res["n_valid"], lam=lam, dh_dtype=torch.float32)
+    torch.cuda.synchronize()
+    o = oracle.residual(Zh, y, want_R=False)
+    _, qho = oracle.ema(q_prev, o["s"], f32(B1), t)
+    cols = np.arange(0, V, 7)
+    rows = np.arange(0, N, 5)
+    dW = oracle.dW_cols(Hh, Zh, y, o["row_lse"], qho, o["n_valid"], f32(lam), cols=cols)
+    dH = oracle.dH_rows(Wh, Zh, y, o["row_lse"], qho, o["n_valid"], f32(lam), rows=rows)
+    e_dw = rel_fro(to_f64(g["dW"])[:, cols], dW)
+    e_dh = rel_fro(to_f64(g["dH"])[rows], dH)
+    log(f"    rel err dW={e_dw:.3e} dH={e_dh:.3e}")
+    assert e_dw <= 2e-2 and e_dh <= 2e-2
+
+
+def test_head_vjp_tile256_empty_batch():
+    log("[head_vjp] tile256 N_t = 0")
+    N, d, V = 2048, 768, 4096
+    Hh, Hd, Wh, Wd, Zh, Zd, _, q_prev, t = _vjp_inputs(N, d, V, "bf16", 0.0)
+    y = np.full(N, -100, np.int32)
+    yd = torch.from_numpy(y).to(dev())
+    res = bom.bom_residual(Zd, yd)
+    g = bom.bom_head_vjp(Hd, Wd, res["R"], yd, torch.from_numpy(q_prev).to(dev()), res["n_valid"], lam=LAM)
+    torch.cuda.synchronize()
+    assert (g["dW"] == 0).all() and (g["dH"].float() == 0).all()
+
+
 def test_head_vjp_bf16_dH_output_and_beta():
     log("[head_vjp] bf16 dH output, dW accumulation")
     N, d, V = 256, 128, 1000

@@ -12,6 +12,8 @@
 // A finish step sums the per-workgroup partials in a fixed order into s, loss, N_t and flags.
 #include <climits>
 #include <cmath>
+#include <cstdlib>
+#include <type_traits>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -24,7 +26,17 @@ constexpr int kSingleMaxWG = 256;     // persistent workgroups of the single pas
 constexpr int kStatsRowsPerWG = 4;    // two pass, stats: one wave per row, 4 waves per workgroup
 constexpr int kColsThreads = 256;     // two pass, columns: threads per workgroup
 constexpr int kColsCPT = 8;           // two pass, columns: chunks per thread
-constexpr int kColsRowBlock = 256;    // two pass, columns: rows per partial-sum block
+constexpr int kColsMaxRowBlock = 256; // two pass, columns: at most this many rows per partial-sum block
+
+// Rows per column-kernel workgroup: enough workgroups (about 1024) to fill the chip.
+int cols_row_block(int64_t N, int64_t V, int vec) {
+    const int64_t slab = (int64_t)kColsThreads * kColsCPT * vec;
+    const int64_t nslab = (V + slab - 1) / slab;
+    int64_t rb = (N * nslab + 1023) / 1024;
+    if (rb < 8) rb = 8;
+    if (rb > kColsMaxRowBlock) rb = kColsMaxRowBlock;
+    return (int)rb;
+}
 
 struct Partials {
     float* part;      // [nparts][V] per-workgroup column sums of residual rows
@@ -41,7 +53,10 @@ struct WsLayout {
 WsLayout ws_layout(int64_t N, int64_t V) {
     int64_t nwg1 = N < kSingleMaxWG ? N : kSingleMaxWG;
     int64_t nstats = (N + kStatsRowsPerWG - 1) / kStatsRowsPerWG;
-    int64_t nrb = (N + kColsRowBlock - 1) / kColsRowBlock;
+    // the vector width is not known here; a width of 1 gives the most partial-sum blocks
+    const int64_t rb = cols_row_block(N, V, 1) < cols_row_block(N, V, 8) ? cols_row_block(N, V, 1)
+                                                                         : cols_row_block(N, V, 8);
+    int64_t nrb = (N + rb - 1) / rb;
     int64_t nparts = nwg1 > nrb ? nwg1 : nrb;
     int64_t nwg = nwg1 > nstats ? nwg1 : nstats;
     WsLayout L;
@@ -131,17 +146,26 @@ __global__ __launch_bounds__(THREADS) void residual_rows_kernel(
         const T* zr = Z + (int64_t)i * ldz;
         float x[NXF];
         uint32_t xw[NXW];
+        // Chunks 0..NCH-2 of every thread lie inside the row (NCH is the ceiling of the chunk count);
+        // only the last chunk needs a bounds check.
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const int col = (c * THREADS + tid) * VEC;
+            const bool last = c == NCH - 1;
             if constexpr (PACKED) {
-                const bool ok = col < V;
+                const bool ok = !last || col < V;
                 const uint4 u = *reinterpret_cast<const uint4*>(zr + (ok ? col : V - VEC));
-                const uint32_t m = lane_mask(ok), fb = 0xFF80FF80u & ~m;  // padding: a pair of bf16 -inf
-                xw[c * 4 + 0] = (u.x & m) | fb; xw[c * 4 + 1] = (u.y & m) | fb;
-                xw[c * 4 + 2] = (u.z & m) | fb; xw[c * 4 + 3] = (u.w & m) | fb;
-            } else {
+                if (last) {
+                    const uint32_t m = lane_mask(ok), fb = 0xFF80FF80u & ~m;  // padding: a pair of bf16 -inf
+                    xw[c * 4 + 0] = (u.x & m) | fb; xw[c * 4 + 1] = (u.y & m) | fb;
+                    xw[c * 4 + 2] = (u.z & m) | fb; xw[c * 4 + 3] = (u.w & m) | fb;
+                } else {
+                    xw[c * 4 + 0] = u.x; xw[c * 4 + 1] = u.y; xw[c * 4 + 2] = u.z; xw[c * 4 + 3] = u.w;
+                }
+            } else if (last) {
                 load_chunk<T, VEC>(zr, col, V, -INFINITY, &x[c * VEC]);
+            } else {
+                VecIO<T, VEC>::load(zr + col, &x[c * VEC]);
             }
         }
         auto val = [&](int k) -> float {
@@ -247,6 +271,130 @@ __global__ __launch_bounds__(THREADS) void residual_rows_kernel(
 }
 
 // ---------------------------------------------------------------------------------------------
+// Single pass, wide bf16 rows: each thread parks its raw 16-byte chunks in its own LDS slots
+// (thread-private: no barrier beyond the row reductions) and keeps only its column accumulators in
+// registers; exp is evaluated twice per element (for the sum, then for p).
+template <int THREADS, int NCH>
+__global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
+    const uint16_t* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
+    float* __restrict__ row_lse, int32_t* __restrict__ row_argmax, float* __restrict__ row_target,
+    uint16_t* __restrict__ R, int64_t ldr, int rows_per_wg, Partials ws) {
+    constexpr int VEC = 8;
+    constexpr int NW = THREADS / kWave;
+    constexpr int VPT = NCH * VEC;
+    __shared__ uint4 slots[NCH * THREADS];
+    __shared__ float sh_max[NW];
+    __shared__ int sh_idx[NW];
+    __shared__ float sh_sum[NW];
+    const int tid = threadIdx.x;
+    float acc[VPT];
+#pragma unroll
+    for (int k = 0; k < VPT; ++k) acc[k] = 0.f;
+    const int row0 = blockIdx.x * rows_per_wg;
+    const int row1 = min(row0 + rows_per_wg, N);
+    int cnt = 0;
+    double ce = 0.0;
+    bool bad = false;
+    auto unpack = [](const uint4& u, float* x) {
+        x[0] = bf16_lo(u.x); x[1] = bf16_hi(u.x); x[2] = bf16_lo(u.y); x[3] = bf16_hi(u.y);
+        x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z); x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
+    };
+    for (int i = row0; i < row1; ++i) {
+        const uint16_t* zr = Z + (int64_t)i * ldz;
+        // pass 1: load, park, max (only the last chunk can fall outside the row)
+        float tm = -INFINITY;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int col = (c * THREADS + tid) * VEC;
+            const bool ok = c < NCH - 1 || col < V;
+            uint4 u = *reinterpret_cast<const uint4*>(zr + (ok ? col : V - VEC));
+            if (c == NCH - 1) {
+                const uint32_t m = lane_mask(ok), fb = 0xFF80FF80u & ~m;
+                u = make_uint4((u.x & m) | fb, (u.y & m) | fb, (u.z & m) | fb, (u.w & m) | fb);
+            }
+            slots[c * THREADS + tid] = u;
+            float x[VEC];
+            unpack(u, x);
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) tm = fmaxf(tm, x[k]);
+        }
+        const float m = block_max<NW>(tm, sh_max);
+        int ti = INT_MAX;
+        if (tm == m) {
+            for (int c = NCH - 1; c >= 0; --c) {
+                float x[VEC];
+                unpack(slots[c * THREADS + tid], x);
+#pragma unroll
+                for (int k = VEC - 1; k >= 0; --k)
+                    if (x[k] == m) ti = (c * THREADS + tid) * VEC + k;
+            }
+        }
+        const int am = block_min<NW>(ti, sh_idx);
+        // pass 2: l = sum exp(z - m)
+        const float m2 = m * kLog2e;
+        float l = 0.f;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            float x[VEC];
+            unpack(slots[c * THREADS + tid], x);
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) l += exp2_fast(fmaf(x[k], kLog2e, -m2));
+        }
+        l = block_sum<NW>(l, sh_sum);
+        const float lse = m + logf(l);
+        const int y = labels[i];
+        bool rbad = false;
+        const bool valid = label_valid(y, V, ignore_index, &rbad);
+        bad |= rbad;
+        uint16_t* rr = R ? R + (int64_t)i * ldr : nullptr;
+        // pass 3: p = exp(z - lse), residual, column accumulation, R
+        const int yv = y / VEC;
+        const int slot = (valid && yv % THREADS == tid) ? (yv / THREADS) * VEC + (y % VEC) : -1;
+        const float lse2 = lse * kLog2e;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int col = (c * THREADS + tid) * VEC;
+            float p[VEC];
+            if (valid) {
+                float x[VEC];
+                unpack(slots[c * THREADS + tid], x);
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) p[k] = exp2_fast(fmaf(x[k], kLog2e, -lse2));
+                if (slot >= 0) {
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k)
+                        if (c * VEC + k == slot) p[k] -= 1.0f;
+                }
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) acc[c * VEC + k] += p[k];
+            } else {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) p[k] = 0.f;
+            }
+            if (rr && (c < NCH - 1 || col < V)) VecIO<uint16_t, VEC>::store(rr + col, p);
+        }
+        if (tid == 0) {
+            row_lse[i] = lse;
+            if (row_argmax) row_argmax[i] = am;
+            const float zt = valid ? bf16_to_f32(zr[y]) : 0.f;
+            if (row_target) row_target[i] = zt;
+            if (valid) {
+                ++cnt;
+                ce += (double)lse - (double)zt;
+            }
+        }
+    }
+    float* prow = ws.part + (int64_t)blockIdx.x * V;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) store_f32_chunk<VEC>(prow, (c * THREADS + tid) * VEC, V, &acc[c * VEC]);
+    if (tid == 0) {
+        ws.wg_count[blockIdx.x] = cnt;
+        ws.wg_loss[blockIdx.x] = ce;
+        ws.wg_flags[blockIdx.x] = bad ? BOM_FLAG_LABEL_RANGE : 0;
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
 // Two pass, stats: one wave per row, online (max, sum, argmax) per lane, then a butterfly merge.
 template <typename T, int VEC, int UNROLL>
 __global__ __launch_bounds__(kStatsRowsPerWG * kWave) void residual_stats_kernel(
@@ -339,15 +487,15 @@ __global__ __launch_bounds__(kStatsRowsPerWG * kWave) void residual_stats_kernel
 template <typename T, int VEC>
 __global__ __launch_bounds__(kColsThreads) void residual_cols_kernel(
     const T* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
-    const float* __restrict__ row_lse, T* __restrict__ R, int64_t ldr, float* __restrict__ part) {
+    const float* __restrict__ row_lse, T* __restrict__ R, int64_t ldr, int row_block, float* __restrict__ part) {
     constexpr int VPT = kColsCPT * VEC;
     constexpr int SLAB = kColsThreads * VPT;
     const int tid = threadIdx.x;
     const int nslab = (V + SLAB - 1) / SLAB;
     const int cb = blockIdx.x % nslab, rb = blockIdx.x / nslab;
     const int col0 = cb * SLAB;
-    const int r0 = rb * kColsRowBlock;
-    const int r1 = min(N, r0 + kColsRowBlock);
+    const int r0 = rb * row_block;
+    const int r1 = min(N, r0 + row_block);
     float acc[VPT];
 #pragma unroll
     for (int k = 0; k < VPT; ++k) acc[k] = 0.f;
@@ -448,6 +596,19 @@ __global__ __launch_bounds__(256) void residual_finish_s_kernel(const float* __r
 }
 
 // ---------------------------------------------------------------------------------------------
+template <int THREADS, int NCH>
+hipError_t launch_rows_lds(const uint16_t* Z, int64_t ldz, int N, int V, const int32_t* labels, int32_t ignore_index,
+                           float* row_lse, int32_t* row_argmax, float* row_target, uint16_t* R, int64_t ldr, Partials ws,
+                           int* nwg_out, hipStream_t stream) {
+    int nwg = N < kSingleMaxWG ? N : kSingleMaxWG;
+    const int rpw = (N + nwg - 1) / nwg;
+    nwg = (N + rpw - 1) / rpw;
+    *nwg_out = nwg;
+    hipLaunchKernelGGL((residual_rows_lds_kernel<THREADS, NCH>), dim3(nwg), dim3(THREADS), 0, stream, Z, ldz, N, V, labels,
+                       ignore_index, row_lse, row_argmax, row_target, R, ldr, rpw, ws);
+    return hipGetLastError();
+}
+
 template <typename T, int THREADS, int VEC, int NCH>
 hipError_t launch_rows(const T* Z, int64_t ldz, int N, int V, const int32_t* labels, int32_t ignore_index, float* row_lse,
                        int32_t* row_argmax, float* row_target, T* R, int64_t ldr, Partials ws, int* nwg_out,
@@ -456,7 +617,7 @@ hipError_t launch_rows(const T* Z, int64_t ldz, int N, int V, const int32_t* lab
     const int rpw = (N + nwg - 1) / nwg;
     nwg = (N + rpw - 1) / rpw;
     *nwg_out = nwg;
-    // bf16 rows wider than 8 chunks keep raw pairs (registers: acc + packed row) instead of fp32 e
+    // wide bf16 rows at 512 threads keep raw pairs (registers: acc + packed row) instead of fp32 e
     constexpr bool kPacked = (VEC == 8) && (NCH > 8);
     hipLaunchKernelGGL((residual_rows_kernel<T, THREADS, VEC, NCH, kPacked>), dim3(nwg), dim3(THREADS), 0, stream, Z,
                        ldz, N, V, labels, ignore_index, row_lse, row_argmax, row_target, R, ldr, rpw, ws);
@@ -474,6 +635,24 @@ hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, i
     if (threads == 64) return BOM_ROWS(64, 1);
     if (threads == 128) return BOM_ROWS(128, 1);
     if (threads == 256) return BOM_ROWS(256, 1);
+    if (threads == 1024) {
+        switch (nch) {
+            case 1: return BOM_ROWS(1024, 1);
+            case 2: return BOM_ROWS(1024, 2);
+            case 3: return BOM_ROWS(1024, 3);
+            case 4: return BOM_ROWS(1024, 4);
+            default: break;
+        }
+        if constexpr (std::is_same<T, uint16_t>::value && VEC == 8) {
+            switch (nch) {
+                case 5: return launch_rows_lds<1024, 5>(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, nwg, st);
+                case 6: return launch_rows_lds<1024, 6>(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, nwg, st);
+                case 7: return launch_rows_lds<1024, 7>(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, nwg, st);
+                default: break;
+            }
+        }
+        return hipErrorInvalidValue;
+    }
     switch (nch) {
         case 1: return BOM_ROWS(512, 1);
         case 2: return BOM_ROWS(512, 2);
@@ -488,8 +667,22 @@ hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, i
 #undef BOM_ROWS
 }
 
+// Variant override for A/B measurement (environment BOM_RESIDUAL_PLAN, read once):
+// 0 automatic, 1 = 512-thread register rows, 2 = 1024-thread rows (registers or LDS), 3 = two pass.
+int plan_override() {
+    static const int v = [] {
+        const char* e = getenv("BOM_RESIDUAL_PLAN");
+        return e ? atoi(e) : 0;
+    }();
+    return v;
+}
+
 // Single-pass plan for VEC-wide chunks: returns false when a row does not fit in registers.
+// Wide rows use 1024-thread workgroups (16 waves per CU): up to 4 chunks keep fp32 e values in
+// registers, 5..7 chunks (bf16 only) park the raw row in LDS.
 bool plan_single(int V, int VEC, int* threads, int* nch) {
+    const int ov = plan_override();
+    if (ov == 3) return false;
     const int slots = (V + VEC - 1) / VEC;
     int th = 64;
     while (th < slots && th < 512) th *= 2;
@@ -497,6 +690,14 @@ bool plan_single(int V, int VEC, int* threads, int* nch) {
     if (th < 512) {
         *threads = th;
         *nch = 1;
+        return true;
+    }
+    const int need1k = (slots + 1023) / 1024;
+    // automatic: 512-thread register rows up to 8 chunks, then 1024-thread rows
+    const bool use1k = ov == 2 || (ov == 0 && need > 8);
+    if (use1k && slots > 512 && need1k <= (VEC == 8 ? 7 : 4) && VEC != 1) {
+        *threads = 1024;
+        *nch = need1k;
         return true;
     }
     const int max_nch = (VEC == 1) ? 8 : 13;
@@ -527,10 +728,11 @@ hipError_t run_residual(const T* Z, int N, int V, int64_t ldz, const int32_t* la
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int slab = kColsThreads * kColsCPT * VEC;
-        nparts = (N + kColsRowBlock - 1) / kColsRowBlock;
+        const int rb = cols_row_block(N, V, VEC);
+        nparts = (N + rb - 1) / rb;
         dim3 grid((unsigned)(((V + slab - 1) / slab) * nparts));
         hipLaunchKernelGGL((residual_cols_kernel<T, VEC>), grid, dim3(kColsThreads), 0, st, Z, ldz, N, V, labels, ig,
-                           lse, R, ldr, ws.part);
+                           lse, R, ldr, rb, ws.part);
         e = hipGetLastError();
     }
     if (e != hipSuccess) return e;

@@ -182,9 +182,9 @@ def cpu_baseline(w, budget_s: float):
     N, d, V, P = w.N, w.d, w.V, w.P
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     # sample sizes: rows of Z for the residual and the head GEMM rows/columns, elements for the update
-    rows = min(N, max(1, int(2e6 // V)))
+    rows = min(N, max(16, int(2e6 // V)))
     ncols = min(V, 64)
-    nrows_dh = min(N, 16)
+    nrows_dh = min(rows, 16)   # dH rows are taken from the sampled rows of Z
     npar = min(P, 4_000_000)
     t_all = {}
     Zs = synth.bf16_to_f32(synth.normal_bf16(rows * V, synth.STREAM_Z, w.logit_std)) if w.dtype == "bf16" else \

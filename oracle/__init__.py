@@ -51,6 +51,8 @@ def _load():
         lib.orc_ema.argtypes = [vp, vp, i64, f64, i64, vp]
         lib.orc_dW_cols.argtypes = [vp, i64, i64, vp, i64, vp, i32, vp, vp, i64, f64, vp, i64, vp]
         lib.orc_dH_rows.argtypes = [vp, i64, vp, i64, vp, i32, vp, vp, i64, f64, vp, i64, vp]
+        lib.orc_dW_cols_sub.argtypes = [vp, i64, i64, vp, i64, vp, i32, vp, vp, i64, f64, vp, i64, vp]
+        lib.orc_dH_rows_sub.argtypes = [vp, i64, vp, i64, vp, i32, vp, vp, i64, f64, vp, i64, vp]
         lib.orc_db.argtypes = [vp, i64, i64, vp, i32, vp, vp, i64, f64, vp]
         lib.orc_update_dense.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp, ctypes.c_int, f64, f64, f64, f64, f64,
                                          f64, i64]
@@ -117,6 +119,31 @@ def dH_rows(W, Z, labels, row_lse, q_hat, n_valid: int, lam: float, rows=None, i
     out = np.zeros((rows.size, d))
     _load().orc_dH_rows(_p(W), d, _p(Z), V, _p(labels), ignore_index, _p(row_lse), _p(q_hat), n_valid,
                         float(lam), _p(rows), rows.size, _p(out))
+    return out
+
+
+def dW_cols_sub(H, Zcols, cols, V: int, labels, row_lse, q_hat, n_valid: int, lam: float, ignore_index: int = -100):
+    """dW columns `cols` from the matching columns of Z only (Zcols is N x len(cols))."""
+    H, Zc, labels, row_lse, q_hat = _f64(H), _f64(Zcols), _i32(labels), _f64(row_lse), _f64(q_hat)
+    cols = np.ascontiguousarray(cols, dtype=np.int64)
+    N, d = H.shape
+    assert Zc.shape == (N, cols.size)
+    out = np.zeros((d, cols.size))
+    _load().orc_dW_cols_sub(_p(H), N, d, _p(Zc), V, _p(labels), ignore_index, _p(row_lse), _p(q_hat), n_valid,
+                            float(lam), _p(cols), cols.size, _p(out))
+    return out
+
+
+def dH_rows_sub(W, Zrows, rows, labels, row_lse, q_hat, n_valid: int, lam: float, ignore_index: int = -100):
+    """dH rows `rows` from the matching rows of Z only (Zrows is len(rows) x V); labels and row_lse
+    are indexed by the full row numbers."""
+    W, Zr, labels, row_lse, q_hat = _f64(W), _f64(Zrows), _i32(labels), _f64(row_lse), _f64(q_hat)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    d, V = W.shape
+    assert Zr.shape == (rows.size, V)
+    out = np.zeros((rows.size, d))
+    _load().orc_dH_rows_sub(_p(W), d, _p(Zr), V, _p(labels), ignore_index, _p(row_lse), _p(q_hat), n_valid,
+                            float(lam), _p(rows), rows.size, _p(out))
     return out
 
 

@@ -177,6 +177,55 @@ void orc_dH_rows(const double* W, int64_t d, const double* Z, int64_t V, const i
     }
 }
 
+/*
+ * The same head products for very wide outputs, from slices of Z: Zc holds the columns cols[0..ncols)
+ * of Z (N x ncols, row-major) for dW; Zr holds the rows rows[0..nrows) of Z (nrows x V) for dH.
+ * G_ij is the same definition as orc_g.
+ */
+static double orc_g_val(double z, int64_t V, int64_t j, int32_t y, int32_t ignore_index, double lse, double qh,
+                        int64_t n_valid, double lambda) {
+    int bad = 0;
+    if (n_valid <= 0 || !orc_is_valid(y, V, ignore_index, &bad)) return 0.0;
+    double r = exp(z - lse) - (j == y ? 1.0 : 0.0);
+    return ((1.0 - lambda) * r + lambda * qh) / (double)n_valid;
+}
+
+void orc_dW_cols_sub(const double* H, int64_t N, int64_t d, const double* Zc, int64_t V, const int32_t* labels,
+                     int32_t ignore_index, const double* row_lse, const double* q_hat, int64_t n_valid, double lambda,
+                     const int64_t* cols, int64_t ncols, double* out) {
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t c = 0; c < ncols; ++c) {
+        int64_t j = cols[c];
+        double* g = (double*)malloc((size_t)(N > 0 ? N : 1) * sizeof(double));
+        for (int64_t i = 0; i < N; ++i)
+            g[i] = orc_g_val(Zc[i * ncols + c], V, j, labels[i], ignore_index, row_lse[i], q_hat[j], n_valid, lambda);
+        for (int64_t k = 0; k < d; ++k) {
+            double acc = 0.0;
+            for (int64_t i = 0; i < N; ++i) acc += H[i * d + k] * g[i];
+            out[k * ncols + c] = acc;
+        }
+        free(g);
+    }
+}
+
+void orc_dH_rows_sub(const double* W, int64_t d, const double* Zr, int64_t V, const int32_t* labels,
+                     int32_t ignore_index, const double* row_lse, const double* q_hat, int64_t n_valid, double lambda,
+                     const int64_t* rows, int64_t nrows, double* out) {
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t c = 0; c < nrows; ++c) {
+        int64_t i = rows[c];
+        double* g = (double*)malloc((size_t)(V > 0 ? V : 1) * sizeof(double));
+        for (int64_t j = 0; j < V; ++j)
+            g[j] = orc_g_val(Zr[c * V + j], V, j, labels[i], ignore_index, row_lse[i], q_hat[j], n_valid, lambda);
+        for (int64_t k = 0; k < d; ++k) {
+            double acc = 0.0;
+            for (int64_t j = 0; j < V; ++j) acc += g[j] * W[k * V + j];
+            out[c * d + k] = acc;
+        }
+        free(g);
+    }
+}
+
 /* Head bias gradient: the bias Jacobian is the identity, so db_j = sum_i G_ij. */
 void orc_db(const double* Z, int64_t N, int64_t V, const int32_t* labels, int32_t ignore_index,
             const double* row_lse, const double* q_hat, int64_t n_valid, double lambda, double* db) {

@@ -497,3 +497,20 @@ def test_state_accounting_matches_printed_sizes():
 def test_state_bytes_rejects_unknown(bad):
     with pytest.raises(ValueError):
         oracle.state_bytes(10, 2, bad)
+
+
+def test_sliced_head_products_equal_full():
+    # the wide-output entry points take slices of Z; on the same inputs they equal the full versions
+    H, W, b, y = _head_problem(N=40, d=6, V=23, seed=34)
+    y[5] = -100
+    Z = H @ W + b
+    res = oracle.residual(Z, y)
+    qh = _rng(35).standard_normal(23) * 0.1
+    cols = np.array([0, 3, 22, 7])
+    rows = np.array([1, 5, 39])
+    full_w = oracle.dW_cols(H, Z, y, res["row_lse"], qh, res["n_valid"], LAM, cols=cols)
+    sub_w = oracle.dW_cols_sub(H, Z[:, cols], cols, 23, y, res["row_lse"], qh, res["n_valid"], LAM)
+    assert np.array_equal(full_w, sub_w)
+    full_h = oracle.dH_rows(W, Z, y, res["row_lse"], qh, res["n_valid"], LAM, rows=rows)
+    sub_h = oracle.dH_rows_sub(W, Z[rows], rows, y, res["row_lse"], qh, res["n_valid"], LAM)
+    assert np.array_equal(full_h, sub_h)

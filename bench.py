@@ -238,6 +238,9 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=[w.name for w in WORKLOADS])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--calibrate-copy-mb", type=int, default=0,
+                    help="run an untimed plain device-to-device copy of this many MiB first (a known-size "
+                         "reference for hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the BOM hot path here is built and measured on a single MI355X "
@@ -250,6 +253,16 @@ def main():
     w = BY_NAME[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.calibrate_copy_mb > 0:
+        nbytes = args.calibrate_copy_mb << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {nbytes} bytes done (3 launches)")
+        del src, dst
+        torch.cuda.empty_cache()
     prob = Problem(w, dev)
     stages = ["bom_residual", "bom_ema", "bom_head_vjp", "bom_update"]
 

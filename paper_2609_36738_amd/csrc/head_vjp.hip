@@ -11,6 +11,8 @@
 // and is transposed while staging (perm for H, the bf16 pack of the fold for G); dH = G W^T has
 // both operands k-contiguous. Split-K with a fixed-order reduction when the output has too few
 // tiles to fill the chip. fp32 path (and unaligned bf16): a SIMT tiled GEMM.
+#include <cstdio>
+#include <cstdlib>
 #include <type_traits>
 
 #include "common.hpp"
@@ -798,6 +800,35 @@ GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K) {
     return {kMfma128, choose_splits(cdiv(M, MB) * cdiv(N, MB), M, N, K, MB, MK, 2)};
 }
 
+// Plan override for A/B measurement (environment BOM_VJP_PLAN = "kind_w,splits_w,kind_h,splits_h",
+// read once; 0 keeps the automatic choice; kinds 1 = 128-tile MFMA, 2 = 256-tile MFMA).
+struct PlanOverride {
+    int kw = 0, sw = 0, kh = 0, sh = 0;
+};
+const PlanOverride& plan_override() {
+    static const PlanOverride o = [] {
+        PlanOverride r;
+        if (const char* e = getenv("BOM_VJP_PLAN")) sscanf(e, "%d,%d,%d,%d", &r.kw, &r.sw, &r.kh, &r.sh);
+        if (r.sw < 0 || r.sw > kMaxSplits) r.sw = 0;
+        if (r.sh < 0 || r.sh > kMaxSplits) r.sh = 0;
+        return r;
+    }();
+    return o;
+}
+
+void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int64_t K) {
+    if (g.kind == kSimt) return;
+    if (kind == kMfma128) g.kind = kMfma128;
+    if (kind == kMfma256 && K >= 4 * TK) g.kind = kMfma256;
+    if (splits > 0) {
+        const int ktile = g.kind == kMfma256 ? TK : MK;
+        // every split keeps at least one k tile
+        g.splits = (int)(splits < cdiv(K, ktile) ? splits : cdiv(K, ktile));
+    }
+    (void)M;
+    (void)N;
+}
+
 Plan make_plan(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     const bool mfma = dt == BOM_BF16;
     Plan p;
@@ -806,6 +837,9 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     const bool m8 = N % 8 == 0 && d % 8 == 0 && V % 8 == 0;
     p.w = plan_gemm(mfma, m8, d, V, N);   // dW: M = d, N = V, K = rows
     p.h = plan_gemm(mfma, m8, N, d, V);   // dH: M = rows, N = d, K = V
+    const PlanOverride& o = plan_override();
+    apply_override(p.w, o.kw, o.sw, d, V, N);
+    apply_override(p.h, o.kh, o.sh, N, d, V);
     return p;
 }
 

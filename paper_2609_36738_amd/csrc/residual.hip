@@ -43,11 +43,10 @@ struct Partials {
     int* wg_count;    // [nwg] valid rows
     int* wg_flags;    // [nwg] BOM_FLAG_LABEL_RANGE bits
     double* wg_loss;  // [nwg] sum of per-row cross-entropy
-    float* inv_nt;    // [1] 1 / N_t (0 when N_t = 0)
 };
 
 struct WsLayout {
-    size_t part_off, count_off, flags_off, loss_off, inv_off, total;
+    size_t part_off, count_off, flags_off, loss_off, total;
 };
 
 WsLayout ws_layout(int64_t N, int64_t V) {
@@ -64,8 +63,7 @@ WsLayout ws_layout(int64_t N, int64_t V) {
     L.count_off = align256(L.part_off + (size_t)nparts * (size_t)V * sizeof(float));
     L.flags_off = align256(L.count_off + (size_t)nwg * sizeof(int));
     L.loss_off = align256(L.flags_off + (size_t)nwg * sizeof(int));
-    L.inv_off = align256(L.loss_off + (size_t)nwg * sizeof(double));
-    L.total = align256(L.inv_off + sizeof(float));
+    L.total = align256(L.loss_off + (size_t)nwg * sizeof(double));
     return L;
 }
 
@@ -483,7 +481,7 @@ __global__ __launch_bounds__(kStatsRowsPerWG * kWave) void residual_stats_kernel
 }
 
 // Two pass, columns: workgroup (cb, rb) owns columns col0 + (c * THREADS + tid) * VEC + k and rows
-// [rb * kColsRowBlock, ...); p = exp(z - lse) with the stats kernel's lse.
+// [rb * row_block, ...); p = exp(z - lse) with the stats kernel's lse.
 template <typename T, int VEC>
 __global__ __launch_bounds__(kColsThreads) void residual_cols_kernel(
     const T* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
@@ -541,58 +539,79 @@ __global__ __launch_bounds__(kColsThreads) void residual_cols_kernel(
 }
 
 // ---------------------------------------------------------------------------------------------
-// Finish: N_t, loss and flags (one workgroup), then s = (sum of partials) / N_t.
-__global__ __launch_bounds__(256) void residual_finish_scalars_kernel(int nwg, Partials ws, float* loss,
-                                                                      int32_t* n_valid, int32_t* flags) {
-    __shared__ int sh_c[256];
-    __shared__ int sh_f[256];
-    __shared__ double sh_l[256];
-    int c = 0, f = 0;
-    double e = 0.0;
-    for (int w = threadIdx.x; w < nwg; w += 256) {
-        c += ws.wg_count[w];
-        f |= ws.wg_flags[w];
-        e += ws.wg_loss[w];
-    }
-    sh_c[threadIdx.x] = c;
-    sh_f[threadIdx.x] = f;
-    sh_l[threadIdx.x] = e;
-    __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) {
-        if (threadIdx.x < o) {
-            sh_c[threadIdx.x] += sh_c[threadIdx.x + o];
-            sh_f[threadIdx.x] |= sh_f[threadIdx.x + o];
-            sh_l[threadIdx.x] += sh_l[threadIdx.x + o];
-        }
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-        const int nt = sh_c[0];
-        *n_valid = nt;
-        *flags = sh_f[0] | (nt == 0 ? BOM_FLAG_EMPTY : 0);
-        *loss = nt > 0 ? (float)(sh_l[0] / (double)nt) : 0.f;
-        *ws.inv_nt = nt > 0 ? (float)(1.0 / (double)nt) : 0.f;
-    }
-}
+// Finish: s_j = (sum of the partial column sums, in a fixed order) / N_t. Workgroup b owns columns
+// b*64 .. b*64+63 (one per lane); wave w adds partials w, w+16, ... and the 16 wave sums are added
+// in wave order. Every workgroup sums the per-workgroup row counts itself (integers: exact in any
+// order) to get N_t; workgroup 0 also writes N_t, the flags and the loss (fp64 sum, fixed order).
+constexpr int kFinThreads = 1024;
+constexpr int kFinWaves = kFinThreads / kWave;
 
-__global__ __launch_bounds__(256) void residual_finish_s_kernel(const float* __restrict__ part, int nparts, int V,
-                                                                const float* __restrict__ inv_nt, float* __restrict__ s) {
-    const int j = blockIdx.x * 256 + threadIdx.x;
-    if (j >= V) return;
+__global__ __launch_bounds__(kFinThreads) void residual_finish_kernel(int nparts, int V, int nwg, Partials ws,
+                                                                      float* __restrict__ s, float* __restrict__ loss,
+                                                                      int32_t* __restrict__ n_valid,
+                                                                      int32_t* __restrict__ flags) {
+    __shared__ float sh_s[kFinWaves][kWave];
+    __shared__ int sh_c[kFinWaves];
+    __shared__ int sh_f[kFinWaves];
+    __shared__ double sh_l[kFinWaves];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int j = blockIdx.x * kWave + lane;
+    const int jc = j < V ? j : V - 1;
+    const float* __restrict__ part = ws.part;
     float a = 0.f;
-    int w = 0;
-    for (; w + 4 <= nparts; w += 4) {
-        const float p0 = part[(int64_t)(w + 0) * V + j];
-        const float p1 = part[(int64_t)(w + 1) * V + j];
-        const float p2 = part[(int64_t)(w + 2) * V + j];
-        const float p3 = part[(int64_t)(w + 3) * V + j];
+    int p = wave;
+    for (; p + 3 * kFinWaves < nparts; p += 4 * kFinWaves) {
+        const float p0 = part[(int64_t)p * V + jc];
+        const float p1 = part[(int64_t)(p + kFinWaves) * V + jc];
+        const float p2 = part[(int64_t)(p + 2 * kFinWaves) * V + jc];
+        const float p3 = part[(int64_t)(p + 3 * kFinWaves) * V + jc];
         a += p0;
         a += p1;
         a += p2;
         a += p3;
     }
-    for (; w < nparts; ++w) a += part[(int64_t)w * V + j];
-    s[j] = a * *inv_nt;
+    for (; p < nparts; p += kFinWaves) a += part[(int64_t)p * V + jc];
+    sh_s[wave][lane] = a;
+    int c = 0;
+    for (int w = threadIdx.x; w < nwg; w += kFinThreads) c += ws.wg_count[w];
+    c = wave_sum(c);
+    if (lane == 0) sh_c[wave] = c;
+    const bool first = blockIdx.x == 0;
+    if (first) {
+        int f = 0;
+        double e = 0.0;
+        for (int w = threadIdx.x; w < nwg; w += kFinThreads) {
+            f |= ws.wg_flags[w];
+            e += ws.wg_loss[w];
+        }
+        f = wave_or(f);
+        e = wave_sum(e);
+        if (lane == 0) {
+            sh_f[wave] = f;
+            sh_l[wave] = e;
+        }
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    int nt = 0;
+#pragma unroll
+    for (int w = 0; w < kFinWaves; ++w) nt += sh_c[w];
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kFinWaves; ++w) sum += sh_s[w][lane];
+    const float inv_nt = nt > 0 ? (float)(1.0 / (double)nt) : 0.f;
+    if (j < V) s[j] = sum * inv_nt;
+    if (first && lane == 0) {
+        int f = 0;
+        double e = 0.0;
+        for (int w = 0; w < kFinWaves; ++w) {
+            f |= sh_f[w];
+            e += sh_l[w];
+        }
+        *n_valid = nt;
+        *flags = f | (nt == 0 ? BOM_FLAG_EMPTY : 0);
+        *loss = nt > 0 ? (float)(e / (double)nt) : 0.f;
+    }
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -736,11 +755,8 @@ hipError_t run_residual(const T* Z, int N, int V, int64_t ldz, const int32_t* la
         e = hipGetLastError();
     }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(residual_finish_scalars_kernel, dim3(1), dim3(256), 0, st, nwg, ws, loss, n_valid, flags);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(residual_finish_s_kernel, dim3((V + 255) / 256), dim3(256), 0, st, ws.part, nparts, V,
-                       ws.inv_nt, s);
+    hipLaunchKernelGGL(residual_finish_kernel, dim3((V + kWave - 1) / kWave), dim3(kFinThreads), 0, st, nparts, V, nwg,
+                       ws, s, loss, n_valid, flags);
     return hipGetLastError();
 }
 
@@ -755,8 +771,7 @@ hipError_t launch_residual(const void* Z, bom_dtype dt, int N, int V, int64_t ld
     const WsLayout L = ws_layout(N, V);
     char* base = static_cast<char*>(wsp);
     Partials ws{reinterpret_cast<float*>(base + L.part_off), reinterpret_cast<int*>(base + L.count_off),
-                reinterpret_cast<int*>(base + L.flags_off), reinterpret_cast<double*>(base + L.loss_off),
-                reinterpret_cast<float*>(base + L.inv_off)};
+                reinterpret_cast<int*>(base + L.flags_off), reinterpret_cast<double*>(base + L.loss_off)};
     const int vw = dt == BOM_BF16 ? 8 : 4;
     const bool vec_ok = (ldz % vw == 0) && (reinterpret_cast<uintptr_t>(Z) % 16 == 0) &&
                         (R == nullptr || ((ldr % vw == 0) && reinterpret_cast<uintptr_t>(R) % 16 == 0)) &&

@@ -32,7 +32,7 @@ struct Fold {
 };
 
 struct VjpWs {
-    size_t cq_off, cqp_off, vmask_off, scal_off, ht_off, part_off, total;
+    size_t cq_off, cqp_off, vmask_off, scal_off, ht_off, hpart_off, hsum_off, u_off, part_off, total;
 };
 
 // ---- prep -------------------------------------------------------------------------------------
@@ -45,8 +45,14 @@ __global__ __launch_bounds__(256) void vjp_prep_kernel(const float* __restrict__
                                                        const int32_t* __restrict__ labels, int32_t ignore_index,
                                                        float* __restrict__ cq, float* __restrict__ cqp,
                                                        float* __restrict__ vmask, float* __restrict__ scal,
-                                                       float* __restrict__ db) {
+                                                       float* __restrict__ db, const float* __restrict__ hpart, int nrb,
+                                                       int d, float* __restrict__ hsum) {
     const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (hpart != nullptr && idx < d) {   // rank-1 form: hsum_m = sum of the row-block partials, in block order
+        float a = 0.f;
+        for (int b = 0; b < nrb; ++b) a += hpart[(int64_t)b * d + idx];
+        hsum[idx] = a;
+    }
     const int nt = *n_valid;
     const bool hist_only = !(lambda < 1.0f);
     if (idx < V) {
@@ -727,6 +733,400 @@ __global__ __launch_bounds__(256, 1) void mfma256_kernel(const uint16_t* __restr
     }
 }
 
+// ---- MFMA bf16, rank-1 form -----------------------------------------------------------------------
+// Rank-1 form of the fold: with alpha = (1 - lambda) / N_t and rows of R outside I equal to zero,
+//   dW = alpha H^T R + hsum cq^T,   hsum_m = sum_{i in I} H_im,  cq_n = lambda q_hat_n / N_t,
+//   dH = alpha R W^T + mask u^T,    u_n = (lambda / N_t) sum_j W_nj q_hat_j,
+// so both GEMMs take R as it is stored (bf16, no rounding of G) and the history enters through
+// the fp32 epilogue. 256 x 256 output tile per 256-thread workgroup, each wave 128 x 128 = 4 x 4
+// blocks of v_mfma_f32_32x32x16_bf16. Memory reads are buffer loads: a chunk outside the matrix
+// reads as zero through the descriptor's range check or an out-of-range offset, so loads need no
+// branches and never touch memory past the operand.
+constexpr int LB = 256;                 // output tile
+constexpr int LK = 32;                  // k tile (split-K granularity)
+constexpr int kBufFlags = 0x00020000;   // raw buffer descriptor word 3: 32-bit data format
+constexpr int kOob = (int)0x80000000u;  // an offset past every range: the load returns zeros
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor over [base, base + bytes): loads at offsets >= bytes return zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_desc(const void* base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufFlags);
+}
+
+// C = A B for one 256 x 256 tile over k in [kb, ke); dW: A(m, k) = H[k][m], B(k, n) = R[k][n];
+// dH: A(i, k) = R[i][k], B(k, n) = W[n][k]. k tiles of 32 in a ring of 4 LDS stages (32 KB each).
+// Both operands are staged through LDS: each lane copies 16-byte chunks with buffer loads into
+// registers and ds_write_b128. (Copies straight from memory into LDS with buffer_load ... lds share
+// the same ~64 B/clk LDS fill bandwidth and measured no faster.) dH's operands are k-contiguous: LDS rows
+// of 32 k (64 B), chunk c of row r at c ^ ((r >> 2) & 3), fragments read with ds_read_b128. dW's
+// operands are k-outer: LDS rows of 256 values per k (512 B), chunk c of row k at c ^ ((k & 3) << 2),
+// fragments read with the transposing ds_read_b64_tr_b16 (a 16-lane group reads a 4 x 16 block and
+// each lane receives 4 consecutive k of one column). Each wave fills 1 KB contiguous per copy step
+// and every 16-lane read phase touches 16 distinct 16-byte bank groups: no bank conflicts.
+// Output out = alpha C + rv[m] cv[n] (+ beta out for dW), or alpha C into the fp32 split-K partials.
+constexpr int LS = 4;                   // LDS stages
+constexpr int LKT = 32;                 // k tile of the staged kernel
+constexpr int kStageElems = LB * LKT;   // bf16 elements per operand per stage (16 KB)
+
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+typedef short v8s_t __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
+
+__device__ __forceinline__ bf16x8_t ld_frag_b128(const char* p) { return *reinterpret_cast<const bf16x8_t*>(p); }
+
+__device__ __forceinline__ bf16x8_t ld_frag_tr(const char* p) {
+    const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(p));
+    const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(p + 4 * 512));
+    const v8s_t both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8_t, both);
+}
+
+template <bool IS_DW, typename TO>
+__global__ __launch_bounds__(256, 1) void lds256_kernel(const uint16_t* __restrict__ Xa, int64_t lda,
+                                                        const uint16_t* __restrict__ Xb, int64_t ldb, int M, int Nn, int K,
+                                                        int kps, int inner_count, int outer_count, const float* alpha_p,
+                                                        const float* __restrict__ rv, const float* __restrict__ cv,
+                                                        TO* __restrict__ out, int64_t ldo, float beta,
+                                                        float* __restrict__ part) {
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[LS][2][kStageElems];
+    __shared__ float rv_s[LB];
+    int tm, tn;
+    if (!tile_of(inner_count, outer_count, IS_DW, &tm, &tn)) return;
+    const int m0 = tm * LB, n0 = tn * LB;
+    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
+    const int nk = (ke - kb + LKT - 1) / LKT;
+    const int nk2 = (nk + 1) & ~1;   // the loop handles k tiles in pairs; a padding tile reads zeros
+    const int l = threadIdx.x % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wm = wave / 2, wn = wave % 2;
+
+    // epilogue inputs, loaded now so their latency hides under the main loop
+    const float rv_reg = (part == nullptr && m0 + (int)threadIdx.x < M) ? rv[m0 + threadIdx.x] : 0.f;
+    float cvv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int n = n0 + wn * 128 + j * 32 + l % 32;
+        cvv[j] = (part == nullptr && n < Nn) ? cv[n] : 0.f;
+    }
+
+    // ---- copy geometry (per lane, constant over k tiles) ----
+    // Copy step q (< 4) of this wave fills LDS kilobyte wave*4 + q of an operand's stage; lane l
+    // writes bytes 16 l of it. dH: that is row (wave*4+q)*16 + l/4, position l%4 (chunk c); offsets
+    // relative to the tile's first row. dW: k row (wave*4+q)*2 + l/32, position l%32 (chunk c);
+    // offsets relative to (k0, first column), the descriptor rebased per k tile.
+    int voff_a[4], voff_b[4], kc[4];
+    bool ok_a[4], ok_b[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int chunk = (wave * 4 + q) * 64 + l;
+        if constexpr (IS_DW) {
+            const int krow = chunk / 32, c = (chunk % 32) ^ ((krow & 3) << 2);
+            voff_a[q] = (int)((int64_t)krow * lda * 2) + c * 16;
+            voff_b[q] = (int)((int64_t)krow * ldb * 2) + c * 16;
+            kc[q] = krow;
+            ok_a[q] = ok_b[q] = true;
+        } else {
+            const int row = chunk / 4, c = (chunk % 4) ^ ((row >> 2) & 3);
+            voff_a[q] = (int)((int64_t)row * lda * 2) + c * 16;
+            voff_b[q] = (int)((int64_t)row * ldb * 2) + c * 16;
+            kc[q] = c * 8;
+            ok_a[q] = row < M - m0;
+            ok_b[q] = row < Nn - n0;
+        }
+    }
+    int bytes_ta = 0, bytes_tb = 0;
+    if constexpr (!IS_DW) {
+        // fixed per workgroup: exact extent of the tile's rows
+        const int ra = min(LB, M - m0), rb = min(LB, Nn - n0);
+        bytes_ta = (int)(((int64_t)(ra - 1) * lda + K) * 2);
+        bytes_tb = (int)(((int64_t)(rb - 1) * ldb + K) * 2);
+    }
+    // Descriptors of k tile kt (dW: rebased on (k0, column tile), rows at or past ke read zeros).
+    struct TileLoad {
+        const uint16_t* ba;
+        const uint16_t* bb;
+        int bytes_a, bytes_b, k0;
+    };
+    auto tile_load = [&](int kt) {
+        TileLoad t;
+        t.k0 = kb + kt * LKT;
+        if constexpr (IS_DW) {
+            const int nv = min(LKT, ke - t.k0);
+            const int nv1 = max(nv, 1);
+            const int kr = min(t.k0, K - 1);
+            t.ba = Xa + (int64_t)kr * lda + m0;
+            t.bb = Xb + (int64_t)kr * ldb + n0;
+            t.bytes_a = nv > 0 ? (int)(((int64_t)(nv1 - 1) * lda + (M - m0)) * 2) : 0;
+            t.bytes_b = nv > 0 ? (int)(((int64_t)(nv1 - 1) * ldb + (Nn - n0)) * 2) : 0;
+        } else {
+            t.ba = Xa + (int64_t)m0 * lda;
+            t.bb = Xb + (int64_t)n0 * ldb;
+            t.bytes_a = bytes_ta;
+            t.bytes_b = bytes_tb;
+        }
+        return t;
+    };
+    auto off_a = [&](const TileLoad& t, int q) {
+        if constexpr (IS_DW) return voff_a[q];
+        else return (ok_a[q] && t.k0 + kc[q] < ke) ? voff_a[q] + t.k0 * 2 : kOob;
+    };
+    auto off_b = [&](const TileLoad& t, int q) {
+        if constexpr (IS_DW) return voff_b[q];
+        else return (ok_b[q] && t.k0 + kc[q] < ke) ? voff_b[q] + t.k0 * 2 : kOob;
+    };
+    // register copies: q < 4 operand A, q >= 4 operand B
+    auto load_one = [&](const TileLoad& t, int q) {
+        if (q < 4) return __builtin_amdgcn_raw_buffer_load_b128(make_desc(t.ba, t.bytes_a), off_a(t, q), 0, 0);
+        return __builtin_amdgcn_raw_buffer_load_b128(make_desc(t.bb, t.bytes_b), off_b(t, q - 4), 0, 0);
+    };
+    auto write_one = [&](int stage, int q, const u32x4_t& v) {
+        char* base = reinterpret_cast<char*>(&lds[stage][q / 4][0]);
+        *reinterpret_cast<u32x4_t*>(base + (wave * 4 + q % 4) * 1024 + l * 16) = v;
+    };
+
+    // ---- fragment geometry ----
+    // dH: fragment row = wave base + block*32 + l%32, chunk kk*2 + l/32 (two swizzled offsets).
+    // dW: 16-lane group g = l/16, s = l%16 supplies k row (g/2)*8 + s/4 (+4 for the upper half) and
+    // columns base + (g%2)*16 + (s%4)*4; block i changes the swizzled chunk, so one offset per block.
+    int fa[4], fb[4];
+    if constexpr (IS_DW) {
+        const int s = l % 16, g = l / 16;
+        const int krow = (g >> 1) * 8 + (s >> 2);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int lo = ((i ^ (s >> 2)) * 4) + (g & 1) * 2 + ((s >> 1) & 1);
+            fa[i] = krow * 512 + ((wm * 16 + lo) << 4) + (s & 1) * 8;
+            fb[i] = krow * 512 + ((wn * 16 + lo) << 4) + (s & 1) * 8;
+        }
+    } else {
+        const int r = l % 32, sw = (r >> 2) & 3;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            const int c = (kk * 2 + l / 32) ^ sw;
+            fa[kk] = (wm * 128 + r) * 64 + (c << 4);
+            fb[kk] = (wn * 128 + r) * 64 + (c << 4);
+        }
+        fa[2] = fa[3] = fb[2] = fb[3] = 0;
+    }
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    auto read_frags = [&](int stage, int kk, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
+        const char* As = reinterpret_cast<const char*>(&lds[stage][0][0]);
+        const char* Bs = reinterpret_cast<const char*>(&lds[stage][1][0]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (IS_DW) {
+                a[i] = ld_frag_tr(As + fa[i] + kk * 16 * 512);
+                b[i] = ld_frag_tr(Bs + fb[i] + kk * 16 * 512);
+            } else {
+                a[i] = ld_frag_b128(As + fa[kk] + i * 32 * 64);
+                b[i] = ld_frag_b128(Bs + fb[kk] + i * 32 * 64);
+            }
+        }
+    };
+    auto mfma_rows = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], int i0, int i1) {
+#pragma unroll
+        for (int i = i0; i < i1; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    // Instruction order inside each half of an iteration: the first 8 MFMAs each followed by their
+    // share of the next k step's fragment reads (dW reads two 8-byte halves per fragment); in the
+    // first half the last 8 MFMAs each followed by one copy step for later tiles.
+    constexpr int kReadsPerMfma = IS_DW ? 2 : 1;
+    auto interleave_reads = [&]() {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, kReadsPerMfma, 0);  // DS read
+        }
+    };
+    // Pipeline: tile kt in LDS stage kt % LS is multiplied while tile kt+1 (already in LDS) waits;
+    // tile kt+2 is written from one register set and tile kt+4 loaded into it (tile kt+3 is in
+    // flight in the other set). A stage is refilled only after the barrier that follows every
+    // wave's last reads of it (each wave drains its LDS reads before that barrier).
+    u32x4_t r0[8], r1[8];
+    bf16x8_t a0[4], b0[4], a1[4], b1[4];
+    auto iteration = [&](int kt, u32x4_t (&rg)[8]) {
+        read_frags(kt % LS, 1, a1, b1);
+        mfma_rows(a0, b0, 0, 2);
+        interleave_reads();
+        __builtin_amdgcn_sched_barrier(0);
+        const int ws = (kt + 2) % LS;
+        const TileLoad t = tile_load(kt + 4);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int i = 2 + q / 4, j = q % 4;
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            write_one(ws, q, rg[q]);
+            rg[q] = load_one(t, q);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags((kt + 1) % LS, 0, a0, b0);
+        mfma_rows(a1, b1, 0, 4);
+        interleave_reads();
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    {
+        const TileLoad t0 = tile_load(0), t1 = tile_load(1), t2 = tile_load(2), t3 = tile_load(3);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) r0[q] = load_one(t0, q);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) r1[q] = load_one(t1, q);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) write_one(0, q, r0[q]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) r0[q] = load_one(t2, q);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) write_one(1, q, r1[q]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) r1[q] = load_one(t3, q);
+    }
+    __syncthreads();
+    read_frags(0, 0, a0, b0);
+    for (int kt = 0; kt < nk2; kt += 2) {
+        iteration(kt, r0);
+        iteration(kt + 1, r1);
+    }
+    __syncthreads();
+    const float alpha = *alpha_p;
+    if (part == nullptr) {
+        rv_s[threadIdx.x] = rv_reg;
+        __syncthreads();
+        for_each_acc256(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) {
+                const float x = fmaf(alpha, v, rv_s[r] * cvv[(c >> 5) & 3]);
+                if constexpr (IS_DW) {
+                    float* p = reinterpret_cast<float*>(out) + (int64_t)m * ldo + n;
+                    *p = beta != 0.f ? x + beta * *p : x;
+                } else {
+                    stf<TO>(out, (int64_t)m * ldo + n, x);
+                }
+            }
+        });
+    } else {
+        float* pz = part + (int64_t)blockIdx.z * M * Nn;
+        for_each_acc256(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = alpha * v;
+        });
+    }
+}
+
+// Split-K reduction for the rank-1 form, in split order: out = sum_z part[z] + rv[m] cv[n] (+ beta out).
+template <typename TO>
+__global__ __launch_bounds__(256) void splitk_rank1_kernel(const float* __restrict__ part, int splits, int M, int Nn,
+                                                           const float* __restrict__ rv, const float* __restrict__ cv,
+                                                           TO* __restrict__ out, int64_t ldo, float beta) {
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t MN = (int64_t)M * Nn;
+    if (idx >= MN) return;
+    const int64_t m = idx / Nn, n = idx % Nn;
+    float a = 0.f;
+    for (int z = 0; z < splits; ++z) a += part[(int64_t)z * MN + idx];
+    a = fmaf(rv[m], cv[n], a);
+    if (beta != 0.f) a += beta * ldf<TO>(out, m * ldo + n);
+    stf<TO>(out, m * ldo + n, a);
+}
+
+// Rank-1 vectors. Blocks [0, nu): u_n = (lambda / N_t) sum_j W[n][j] q_hat_j, one wave per row of W.
+// Blocks [nu, ...): partial column sums of H over rows in I, kHsRows rows by 512 columns per block
+// (wave w adds rows w, w + 4, ...; the four wave sums are added in wave order).
+constexpr int kHsRows = 128;
+__global__ __launch_bounds__(256) void vjp_rank1_kernel(const uint16_t* __restrict__ W, int64_t ldw, int d, int V,
+                                                        const float* __restrict__ q_hat, const int32_t* __restrict__ n_valid,
+                                                        float lambda, int nu, const uint16_t* __restrict__ H,
+                                                        int64_t ldh, int N, const int32_t* __restrict__ labels,
+                                                        int32_t ignore_index, float* __restrict__ u,
+                                                        float* __restrict__ hpart) {
+    const int l = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    if ((int)blockIdx.x < nu) {
+        const int n = blockIdx.x * 4 + wave;
+        if (n >= d) return;
+        const uint16_t* wr = W + (int64_t)n * ldw;
+        float a0 = 0.f, a1 = 0.f;
+        int j = l * 8;
+        for (; j + 512 < V; j += 1024) {
+            const uint4 w0 = *reinterpret_cast<const uint4*>(wr + j);
+            const uint4 w1 = *reinterpret_cast<const uint4*>(wr + j + 512);
+            const float4 q0 = *reinterpret_cast<const float4*>(q_hat + j);
+            const float4 q1 = *reinterpret_cast<const float4*>(q_hat + j + 4);
+            const float4 q2 = *reinterpret_cast<const float4*>(q_hat + j + 512);
+            const float4 q3 = *reinterpret_cast<const float4*>(q_hat + j + 516);
+            a0 += bf16_lo(w0.x) * q0.x + bf16_hi(w0.x) * q0.y + bf16_lo(w0.y) * q0.z + bf16_hi(w0.y) * q0.w +
+                  bf16_lo(w0.z) * q1.x + bf16_hi(w0.z) * q1.y + bf16_lo(w0.w) * q1.z + bf16_hi(w0.w) * q1.w;
+            a1 += bf16_lo(w1.x) * q2.x + bf16_hi(w1.x) * q2.y + bf16_lo(w1.y) * q2.z + bf16_hi(w1.y) * q2.w +
+                  bf16_lo(w1.z) * q3.x + bf16_hi(w1.z) * q3.y + bf16_lo(w1.w) * q3.z + bf16_hi(w1.w) * q3.w;
+        }
+        for (; j < V; j += 512) {
+            const uint4 w0 = *reinterpret_cast<const uint4*>(wr + j);
+            const float4 q0 = *reinterpret_cast<const float4*>(q_hat + j);
+            const float4 q1 = *reinterpret_cast<const float4*>(q_hat + j + 4);
+            a0 += bf16_lo(w0.x) * q0.x + bf16_hi(w0.x) * q0.y + bf16_lo(w0.y) * q0.z + bf16_hi(w0.y) * q0.w +
+                  bf16_lo(w0.z) * q1.x + bf16_hi(w0.z) * q1.y + bf16_lo(w0.w) * q1.z + bf16_hi(w0.w) * q1.w;
+        }
+        const float sum = wave_sum(a0 + a1);
+        if (l == 0) {
+            const int nt = *n_valid;
+            u[n] = nt > 0 ? (float)((double)lambda / (double)nt) * sum : 0.f;
+        }
+        return;
+    }
+    __shared__ float sh[4][512];
+    const int b = blockIdx.x - nu;
+    const int ncb = (d + 511) / 512;
+    const int cb = b % ncb, rb = b / ncb;
+    const int col = cb * 512 + l * 8;
+    const int colc = col < d ? col : d - 8;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const int rbeg = rb * kHsRows;
+    // rows rbeg + wave + 4e, e < kHsRows / 4: all loads of a group of 8 rows in flight together
+#pragma unroll
+    for (int e0 = 0; e0 < kHsRows / 4; e0 += 8) {
+        uint4 h[8];
+        float mk[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int i = rbeg + wave + 4 * (e0 + e);
+            const int ic = i < N ? i : N - 1;
+            bool bad = false;
+            mk[e] = (i < N && label_valid(labels[ic], V, ignore_index, &bad)) ? 1.f : 0.f;
+            h[e] = *reinterpret_cast<const uint4*>(H + (int64_t)ic * ldh + colc);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            acc[0] += mk[e] * bf16_lo(h[e].x);
+            acc[1] += mk[e] * bf16_hi(h[e].x);
+            acc[2] += mk[e] * bf16_lo(h[e].y);
+            acc[3] += mk[e] * bf16_hi(h[e].y);
+            acc[4] += mk[e] * bf16_lo(h[e].z);
+            acc[5] += mk[e] * bf16_hi(h[e].z);
+            acc[6] += mk[e] * bf16_lo(h[e].w);
+            acc[7] += mk[e] * bf16_hi(h[e].w);
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) sh[wave][l * 8 + c] = acc[c];
+    __syncthreads();
+    for (int c = threadIdx.x; c < 512; c += 256) {
+        const int m = cb * 512 + c;
+        if (m < d) hpart[(int64_t)rb * d + m] = ((sh[0][c] + sh[1][c]) + sh[2][c]) + sh[3][c];
+    }
+}
+
 // H [N][d] -> H^T [d][N] (bf16), 64 x 64 tiles through LDS.
 __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ H, int64_t ldh, int N, int d,
                                                              uint16_t* __restrict__ Ht) {
@@ -762,7 +1162,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 constexpr int kCUs = 256;        // MI355X compute units
 constexpr int kMaxSplits = 8;
 
-enum GemmKind { kSimt = 0, kMfma128 = 1, kMfma256 = 2 };
+enum GemmKind { kSimt = 0, kMfma128 = 1, kMfma256 = 2, kRank1 = 3 };
 struct GemmPlan {
     int kind, splits;
 };
@@ -795,13 +1195,16 @@ int choose_splits(int64_t tiles, int64_t M, int64_t N, int64_t K, int tb, int kt
 
 GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K) {
     if (!mfma || !big_ok) return {kSimt, choose_splits(cdiv(M, SB) * cdiv(N, SB), M, N, K, SB, SK, 4)};
-    const int64_t t256 = cdiv(M, TB) * cdiv(N, TB);
-    if (big_ok && t256 >= 24 && K >= 4 * TK) return {kMfma256, choose_splits(t256, M, N, K, TB, TK, 1)};
+    // large products: 256-tile rank-1 kernel; small ones (a few dozen 256 tiles or a short k) are
+    // latency bound and run faster on the 128-tile kernel, which needs no rank-1 pre-pass
+    const int64_t t256 = cdiv(M, LB) * cdiv(N, LB);
+    if (t256 >= 24 && K >= 8 * LK) return {kRank1, choose_splits(t256, M, N, K, LB, LK, 1)};
     return {kMfma128, choose_splits(cdiv(M, MB) * cdiv(N, MB), M, N, K, MB, MK, 2)};
 }
 
 // Plan override for A/B measurement (environment BOM_VJP_PLAN = "kind_w,splits_w,kind_h,splits_h",
-// read once; 0 keeps the automatic choice; kinds 1 = 128-tile MFMA, 2 = 256-tile MFMA).
+// read once; 0 keeps the automatic choice; kinds 1 = 128-tile MFMA, 2 = 256-tile MFMA with staged
+// fold, 3 = 256-tile MFMA with direct LDS copies and the rank-1 epilogue).
 struct PlanOverride {
     int kw = 0, sw = 0, kh = 0, sh = 0;
 };
@@ -820,8 +1223,9 @@ void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int
     if (g.kind == kSimt) return;
     if (kind == kMfma128) g.kind = kMfma128;
     if (kind == kMfma256 && K >= 4 * TK) g.kind = kMfma256;
+    if (kind == kRank1) g.kind = kRank1;
     if (splits > 0) {
-        const int ktile = g.kind == kMfma256 ? TK : MK;
+        const int ktile = g.kind == kMfma256 ? TK : (g.kind == kRank1 ? LK : MK);
         // every split keeps at least one k tile
         g.splits = (int)(splits < cdiv(K, ktile) ? splits : cdiv(K, ktile));
     }
@@ -852,7 +1256,11 @@ VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     w.scal_off = align256(w.vmask_off + (size_t)N * 4);
     w.ht_off = align256(w.scal_off + 16);
     const size_t ht = p.w.kind == kMfma256 ? (size_t)d * N * 2 : 0;
-    w.part_off = align256(w.ht_off + ht);
+    const bool r1 = p.w.kind == kRank1 || p.h.kind == kRank1;
+    w.hpart_off = align256(w.ht_off + ht);
+    w.hsum_off = align256(w.hpart_off + (r1 ? (size_t)cdiv(N, kHsRows) * d * 4 : 0));
+    w.u_off = align256(w.hsum_off + (r1 ? (size_t)d * 4 : 0));
+    w.part_off = align256(w.u_off + (r1 ? (size_t)d * 4 : 0));
     size_t pw = p.w.splits > 1 ? (size_t)p.w.splits * d * V * 4 : 0;
     size_t ph = p.h.splits > 1 ? (size_t)p.h.splits * N * d * 4 : 0;
     w.total = align256(w.part_off + (pw > ph ? pw : ph));
@@ -861,8 +1269,31 @@ VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
 
 template <typename TO>
 hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, const void* B, int64_t ldb, bom_dtype dt,
-                    int M, int Nn, int K, const Fold& f, TO* out, int64_t ldo, float beta, float* part, hipStream_t st) {
+                    int M, int Nn, int K, const Fold& f, TO* out, int64_t ldo, float beta, float* part, const float* rv,
+                    const float* cv, hipStream_t st) {
     const int splits = g.splits;
+    if (g.kind == kRank1) {
+        // rank-1 form: out = alpha A B + rv cv^T (+ beta out)
+        const int kps = (int)(cdiv(cdiv(K, splits), LK) * LK);
+        const int MT = (int)cdiv(M, LB), NT = (int)cdiv(Nn, LB);
+        const int inner = is_dw ? MT : NT, outer = is_dw ? NT : MT;
+        dim3 grid((unsigned)(cdiv(outer, 8) * 8 * inner), 1, splits);
+        float* pz = splits > 1 ? part : nullptr;
+        const uint16_t* a16 = static_cast<const uint16_t*>(A);
+        const uint16_t* b16 = static_cast<const uint16_t*>(B);
+        if (is_dw)
+            hipLaunchKernelGGL((lds256_kernel<true, float>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
+                               inner, outer, f.scal, rv, cv, reinterpret_cast<float*>(out), ldo, beta, pz);
+        else
+            hipLaunchKernelGGL((lds256_kernel<false, TO>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
+                               inner, outer, f.scal, rv, cv, out, ldo, beta, pz);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess || splits == 1) return e;
+        const int64_t MN = (int64_t)M * Nn;
+        hipLaunchKernelGGL(splitk_rank1_kernel<TO>, dim3((unsigned)cdiv(MN, 256)), dim3(256), 0, st, part, splits, M, Nn,
+                           rv, cv, out, ldo, beta);
+        return hipGetLastError();
+    }
     const int tb = g.kind == kMfma256 ? TB : (g.kind == kMfma128 ? MB : SB);
     const int ktile = g.kind == kMfma256 ? TK : (g.kind == kMfma128 ? MK : SK);
     int kps = (int)(cdiv(cdiv(K, splits), ktile) * ktile);
@@ -927,13 +1358,10 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
     float* vmask = reinterpret_cast<float*>(base + L.vmask_off);
     float* scal = reinterpret_cast<float*>(base + L.scal_off);
     uint16_t* ht = reinterpret_cast<uint16_t*>(base + L.ht_off);
+    float* hpart = reinterpret_cast<float*>(base + L.hpart_off);
+    float* hsum = reinterpret_cast<float*>(base + L.hsum_off);
+    float* u = reinterpret_cast<float*>(base + L.u_off);
     float* part = reinterpret_cast<float*>(base + L.part_off);
-    const int nprep = (a.V > a.N ? a.V : a.N);
-    hipLaunchKernelGGL(vjp_prep_kernel, dim3((nprep + 255) / 256), dim3(256), 0, st, a.q_hat, a.s, a.n_valid, a.lambda,
-                       a.V, a.N, a.labels, a.ignore_index, cq, cqp, vmask, scal, a.db);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const Fold f{cq, vmask, scal, cqp};
 
     // MFMA kernels stage 16-byte rows: leading dimensions multiples of 8 and 16-byte bases;
     // otherwise the SIMT kernels (same plan shape, SIMT tiles) run.
@@ -943,6 +1371,29 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
         p.w.kind = kSimt;
         p.h.kind = kSimt;
     }
+    if (!a.dH) p.h.kind = kSimt;   // no dH: no rank-1 vector for it
+
+    // rank-1 vectors first: u for dH, row-block partial sums of H over I for dW
+    hipError_t e;
+    const bool rw = p.w.kind == kRank1, rh = p.h.kind == kRank1;
+    const int nrb = (int)cdiv(a.N, kHsRows);
+    if (rw || rh) {
+        const int nu = rh ? (int)cdiv(a.d, 4) : 0;
+        const int ns = rw ? (int)cdiv(a.d, 512) * nrb : 0;
+        hipLaunchKernelGGL(vjp_rank1_kernel, dim3((unsigned)(nu + ns)), dim3(256), 0, st,
+                           static_cast<const uint16_t*>(a.W), a.ldw, a.d, a.V, a.q_hat, a.n_valid, a.lambda, nu,
+                           static_cast<const uint16_t*>(a.H), a.ldh, a.N, a.labels, a.ignore_index, u, hpart);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    int nprep = a.V > a.N ? a.V : a.N;
+    if (nprep < a.d) nprep = a.d;
+    hipLaunchKernelGGL(vjp_prep_kernel, dim3((nprep + 255) / 256), dim3(256), 0, st, a.q_hat, a.s, a.n_valid, a.lambda,
+                       a.V, a.N, a.labels, a.ignore_index, cq, cqp, vmask, scal, a.db, rw ? hpart : nullptr, nrb, a.d,
+                       hsum);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const Fold f{cq, vmask, scal, cqp};
 
     // dW = H^T G
     const void* A = a.H;
@@ -956,15 +1407,16 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
         A = ht;
         lda = a.N;
     }
-    e = run_gemm<float>(true, p.w, A, lda, a.R, a.ldr, a.dt, a.d, a.V, a.N, f, a.dW, a.lddw, a.dW_beta, part, st);
+    e = run_gemm<float>(true, p.w, A, lda, a.R, a.ldr, a.dt, a.d, a.V, a.N, f, a.dW, a.lddw, a.dW_beta, part, hsum, cq,
+                        st);
     if (e != hipSuccess) return e;
     // dH = G W^T (shares the split-K buffer: same stream, so it runs after the dW reduction)
     if (a.dH) {
         if (a.dh_dt == BOM_BF16)
             return run_gemm<uint16_t>(false, p.h, a.R, a.ldr, a.W, a.ldw, a.dt, a.N, a.d, a.V, f,
-                                      static_cast<uint16_t*>(a.dH), a.lddh, 0.f, part, st);
+                                      static_cast<uint16_t*>(a.dH), a.lddh, 0.f, part, vmask, u, st);
         return run_gemm<float>(false, p.h, a.R, a.ldr, a.W, a.ldw, a.dt, a.N, a.d, a.V, f, static_cast<float*>(a.dH),
-                               a.lddh, 0.f, part, st);
+                               a.lddh, 0.f, part, vmask, u, st);
     }
     return hipSuccess;
 }

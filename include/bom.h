@@ -122,13 +122,18 @@ bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, 
  *   dW = H^T G + dW_beta * dW     [d, V] fp32 (dW_beta = 0 overwrites; dW is not read then)
  *   db = (1 - lambda) s + lambda q_hat   [V] fp32  (bias Jacobian = identity; equals 1^T G)
  *   dH = G W^T                     [N, d] of dh_dt
- * G is formed tile by tile inside the GEMMs (the history is folded into the output gradient
- * at operand load) and never written to memory. N_t is read from the device word n_valid; when
- * it is 0, G = 0.
+ * G is never written to memory. Small products form it tile by tile inside the GEMMs (the
+ * history folded into the output gradient at operand load, rounded to bf16 for the MFMA path);
+ * large bf16 products use the equal rank-1 form
+ *   dW = alpha H^T R + (sum_{i in I} H_i) (lambda q_hat / N_t)^T
+ *   dH = alpha R W^T + 1_I (lambda / N_t W q_hat)^T
+ * with alpha = (1 - lambda) / N_t, which multiplies R as stored and adds the history in fp32.
+ * N_t is read from the device word n_valid; when it is 0, G = 0.
  *
  *   H   device [N, ldh] of dt.   W device [d, ldw] of dt (the head as d x V).
- *   R   device [N, ldr] of dt: the residual rows written by bom_residual (zero rows outside I).
- *   dt  BOM_BF16 (MFMA path, fp32 accumulation; G is rounded to bf16 after folding) or BOM_F32.
+ *   R   device [N, ldr] of dt: the residual rows written by bom_residual. Rows outside I must be
+ *       zero (bom_residual writes them so); the rank-1 form relies on it.
+ *   dt  BOM_BF16 (MFMA path, fp32 accumulation) or BOM_F32.
  *   labels device int32 [N] (defines I with ignore_index, as in bom_residual).
  *   q_hat device fp32 [V].   s device fp32 [V] (only read when db != NULL).
  *   n_valid device int32 [1].

@@ -234,7 +234,7 @@ struct StageHt {
 struct StageGt {
     uint4 r[4];
     uint32_t mk[4];
-    float vm[4];
+    float vm[4];      // row masks as loaded; rows past kend are dropped by mk at store time
     __device__ __forceinline__ void load(const uint16_t* R, int64_t ldr, int Nn, int k0, int kend, int n0,
                                          const float* vmask) {
         const int t = threadIdx.x, kq = t / 16, mq = t % 16;
@@ -244,7 +244,7 @@ struct StageGt {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int k = k0 + kq * 4 + q;
-            vm[q] = vmask[k < kend ? k : kend - 1] * (k < kend ? 1.f : 0.f);
+            vm[q] = vmask[k < kend ? k : kend - 1];
             mk[q] = lane_mask(nok && k < kend);
             r[q] = ld16(R + (int64_t)(k < kend ? k : kend - 1) * ldr + nc);
         }
@@ -264,8 +264,8 @@ struct StageGt {
                 g[q] = fmaf(alpha, rv, vm[q] * cqn[c]);
             }
             uint2 o;
-            o.x = pack_bf16x2(g[0], g[1]);
-            o.y = pack_bf16x2(g[2], g[3]);
+            o.x = pack_bf16x2(g[0], g[1]) & ((mk[0] & 0x0000FFFFu) | (mk[1] & 0xFFFF0000u));
+            o.y = pack_bf16x2(g[2], g[3]) & ((mk[2] & 0x0000FFFFu) | (mk[3] & 0xFFFF0000u));
             *reinterpret_cast<uint2*>(&Bs[mq * 8 + c][kq * 4]) = o;
         }
     }
@@ -277,39 +277,43 @@ template <bool FOLD>
 struct StageK {
     uint4 r[4];
     uint32_t mk[4];
-    __device__ __forceinline__ void load(const uint16_t* X, int64_t ldx, int rows, int r0, int k0, int kend) {
+    float vm[4];      // FOLD: row masks and the history coefficients of this thread's k chunk, as
+    float4 cq[2];     // loaded (consumed at store time, after the MFMA phase)
+    __device__ __forceinline__ void load(const uint16_t* X, int64_t ldx, int rows, int r0, int k0, int kend,
+                                         const Fold& f) {
         const int t = threadIdx.x;
+        const int k = k0 + (t % 8) * 8;
+        const int kc = k < kend ? k : kend - 8;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int c = e * 256 + t, row = r0 + c / 8, k = k0 + (c % 8) * 8;
+            const int c = e * 256 + t, row = r0 + c / 8;
+            const int rc = row < rows ? row : rows - 1;
             mk[e] = lane_mask(row < rows && k < kend);
-            r[e] = ld16(X + (int64_t)(row < rows ? row : rows - 1) * ldx + (k < kend ? k : kend - 8));
+            r[e] = ld16(X + (int64_t)rc * ldx + kc);
+            if (FOLD) vm[e] = f.vmask[rc];
+        }
+        if (FOLD) {
+            cq[0] = *reinterpret_cast<const float4*>(f.cq + kc);
+            cq[1] = *reinterpret_cast<const float4*>(f.cq + kc + 4);
         }
     }
-    __device__ __forceinline__ void store(uint16_t (*S)[LDK], int rows, int r0, int k0, int kend, const Fold& f,
-                                          float alpha) const {
+    __device__ __forceinline__ void store(uint16_t (*S)[LDK], float alpha) const {
         const int t = threadIdx.x;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int c = e * 256 + t, lr = c / 8, lk = (c % 8) * 8;
-            uint4 o = and_mask(r[e], mk[e]);
+            uint4 o = r[e];
             if (FOLD) {
-                const float vm = (r0 + lr < rows) ? f.vmask[r0 + lr] : 0.f;
-                const int k = k0 + lk;
-                const bool kok = k < kend;
-                const float z = kok ? 1.f : 0.f;
-                const float4 c0 = *reinterpret_cast<const float4*>(f.cq + (kok ? k : kend - 8));
-                const float4 c1 = *reinterpret_cast<const float4*>(f.cq + (kok ? k : kend - 8) + 4);
-                const float cq[8] = {z * c0.x, z * c0.y, z * c0.z, z * c0.w, z * c1.x, z * c1.y, z * c1.z, z * c1.w};
+                const float q8[8] = {cq[0].x, cq[0].y, cq[0].z, cq[0].w, cq[1].x, cq[1].y, cq[1].z, cq[1].w};
                 const uint32_t w[4] = {o.x, o.y, o.z, o.w};
                 uint32_t g[4];
 #pragma unroll
                 for (int p = 0; p < 4; ++p)
-                    g[p] = pack_bf16x2(fmaf(alpha, bf16_lo(w[p]), vm * cq[2 * p]),
-                                       fmaf(alpha, bf16_hi(w[p]), vm * cq[2 * p + 1]));
+                    g[p] = pack_bf16x2(fmaf(alpha, bf16_lo(w[p]), vm[e] * q8[2 * p]),
+                                       fmaf(alpha, bf16_hi(w[p]), vm[e] * q8[2 * p + 1]));
                 o = make_uint4(g[0], g[1], g[2], g[3]);
             }
-            *reinterpret_cast<uint4*>(&S[lr][lk]) = o;
+            *reinterpret_cast<uint4*>(&S[lr][lk]) = and_mask(o, mk[e]);
         }
     }
 };
@@ -347,6 +351,59 @@ __device__ __forceinline__ void for_each_acc(const f32x16_t (&acc)[2][2], F&& fn
                 fn(wm * 64 + i * 32 + (r / 4) * 8 + (lane / 32) * 4 + (r % 4), wn * 64 + j * 32 + lane % 32, acc[i][j][r]);
 }
 
+// k tiles a 128-tile workgroup loads at once when its k range is short (the latency-bound regime
+// of small products): one round trip to memory, then the tiles go through LDS one after another.
+constexpr int kPre = 4;
+
+// Shared k loop of the 128-tile kernels. LA / LB load operand tiles into staging registers,
+// SA / SB write them to an LDS buffer.
+template <typename StA, typename StB, typename LA, typename LB, typename SA, typename SB>
+__device__ __forceinline__ void k_loop128(int kb, int ke, uint16_t (*As)[MB][LDK], uint16_t (*Bs)[MB][LDK],
+                                          f32x16_t (&acc)[2][2], LA&& load_a, LB&& load_b, SA&& store_a,
+                                          SB&& store_b) {
+    const int nk = (ke - kb + MK - 1) / MK;
+    if (nk <= kPre) {
+        StA sa[kPre];
+        StB sb[kPre];
+#pragma unroll
+        for (int q = 0; q < kPre; ++q) {   // tiles past ke load clamped rows and stage zeros
+            load_a(sa[q], kb + q * MK);
+            load_b(sb[q], kb + q * MK);
+        }
+#pragma unroll
+        for (int q = 0; q < kPre; ++q) {
+            if (q < nk) {   // uniform
+                store_a(sa[q], As[q & 1]);
+                store_b(sb[q], Bs[q & 1]);
+                __syncthreads();   // also: every wave is done with the buffer's previous tile
+                mfma_tile(As[q & 1], Bs[q & 1], acc);
+            }
+        }
+        return;
+    }
+    StA sa;
+    StB sb;
+    load_a(sa, kb);
+    load_b(sb, kb);
+    store_a(sa, As[0]);
+    store_b(sb, Bs[0]);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            load_a(sa, kb + (kt + 1) * MK);
+            load_b(sb, kb + (kt + 1) * MK);
+        }
+        mfma_tile(As[buf], Bs[buf], acc);
+        if (more) {
+            store_a(sa, As[buf ^ 1]);
+            store_b(sb, Bs[buf ^ 1]);
+        }
+        __syncthreads();
+    }
+}
+
 // dW[m][n] = sum_k H[k][m] G[k][n]: M = d, Nn = V, K = N rows.
 __global__ __launch_bounds__(256) void mfma_dW_kernel(const uint16_t* __restrict__ H, int64_t ldh,
                                                       const uint16_t* __restrict__ R, int64_t ldr, int M, int Nn, int K,
@@ -370,32 +427,11 @@ __global__ __launch_bounds__(256) void mfma_dW_kernel(const uint16_t* __restrict
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-    StageHt sa;
-    StageGt sb;
-    const int nk = (ke - kb + MK - 1) / MK;
-    if (nk > 0) {
-        sa.load(H, ldh, M, kb, ke, m0);
-        sb.load(R, ldr, Nn, kb, ke, n0, f.vmask);
-        sa.store(As[0]);
-        sb.store(Bs[0], alpha, cqn);
-    }
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            const int k0 = kb + (kt + 1) * MK;
-            sa.load(H, ldh, M, k0, ke, m0);
-            sb.load(R, ldr, Nn, k0, ke, n0, f.vmask);
-        }
-        mfma_tile(As[buf], Bs[buf], acc);
-        if (more) {
-            sa.store(As[buf ^ 1]);
-            sb.store(Bs[buf ^ 1], alpha, cqn);
-        }
-        __syncthreads();
-    }
+    k_loop128<StageHt, StageGt>(
+        kb, ke, As, Bs, acc, [&](StageHt& st, int k0) { st.load(H, ldh, M, k0, ke, m0); },
+        [&](StageGt& st, int k0) { st.load(R, ldr, Nn, k0, ke, n0, f.vmask); },
+        [&](const StageHt& st, uint16_t (*S)[LDK]) { st.store(S); },
+        [&](const StageGt& st, uint16_t (*S)[LDK]) { st.store(S, alpha, cqn); });
     if (part == nullptr) {
         for_each_acc(acc, [&](int r, int c, float v) {
             const int m = m0 + r, n = n0 + c;
@@ -431,31 +467,11 @@ __global__ __launch_bounds__(256) void mfma_dH_kernel(const uint16_t* __restrict
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-    StageK<true> sa;
-    StageK<false> sb;
-    const int nk = (ke - kb + MK - 1) / MK;
-    if (nk > 0) {
-        sa.load(R, ldr, M, m0, kb, ke);
-        sb.load(W, ldw, Nn, n0, kb, ke);
-        sa.store(As[0], M, m0, kb, ke, f, alpha);
-        sb.store(Bs[0], Nn, n0, kb, ke, f, alpha);
-    }
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        const bool more = kt + 1 < nk;
-        const int k0 = kb + (kt + 1) * MK;
-        if (more) {
-            sa.load(R, ldr, M, m0, k0, ke);
-            sb.load(W, ldw, Nn, n0, k0, ke);
-        }
-        mfma_tile(As[buf], Bs[buf], acc);
-        if (more) {
-            sa.store(As[buf ^ 1], M, m0, k0, ke, f, alpha);
-            sb.store(Bs[buf ^ 1], Nn, n0, k0, ke, f, alpha);
-        }
-        __syncthreads();
-    }
+    k_loop128<StageK<true>, StageK<false>>(
+        kb, ke, As, Bs, acc, [&](StageK<true>& st, int k0) { st.load(R, ldr, M, m0, k0, ke, f); },
+        [&](StageK<false>& st, int k0) { st.load(W, ldw, Nn, n0, k0, ke, f); },
+        [&](const StageK<true>& st, uint16_t (*S)[LDK]) { st.store(S, alpha); },
+        [&](const StageK<false>& st, uint16_t (*S)[LDK]) { st.store(S, alpha); });
     if (part == nullptr) {
         for_each_acc(acc, [&](int r, int c, float v) {
             const int m = m0 + r, n = n0 + c;
@@ -1199,7 +1215,12 @@ GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K) {
     // latency bound and run faster on the 128-tile kernel, which needs no rank-1 pre-pass
     const int64_t t256 = cdiv(M, LB) * cdiv(N, LB);
     if (t256 >= 24 && K >= 8 * LK) return {kRank1, choose_splits(t256, M, N, K, LB, LK, 1)};
-    return {kMfma128, choose_splits(cdiv(M, MB) * cdiv(N, MB), M, N, K, MB, MK, 2)};
+    // 128 tiles: split k so that every workgroup loads its whole k range at once, when that takes
+    // at most kMaxSplits splits
+    const int64_t t128 = cdiv(M, MB) * cdiv(N, MB);
+    const int64_t s_pre = cdiv(K, (int64_t)kPre * MK);
+    if (s_pre <= kMaxSplits) return {kMfma128, (int)s_pre};
+    return {kMfma128, choose_splits(t128, M, N, K, MB, MK, 2)};
 }
 
 // Plan override for A/B measurement (environment BOM_VJP_PLAN = "kind_w,splits_w,kind_h,splits_h",

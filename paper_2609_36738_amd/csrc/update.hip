@@ -161,7 +161,8 @@ __global__ __launch_bounds__(kUpdThreads) void factored_finish_kernel(const floa
     if (t == 0) rsum[b] = sh[0];
 }
 
-// Update: workgroup covers kFacUpdRows rows; v_hat_ij = (Rr_i / rsum_b * inv_bc2) * Cc_j.
+// Update: workgroup covers kFacUpdRows rows; v_hat_ij = (Rr_i / rsum_b * inv_bc2) * Cc_j. theta and u
+// are streamed (non-temporal, each byte touched once); the small Cc stays cached for the block's rows.
 template <bool SPLIT, int KC>
 __global__ __launch_bounds__(kUpdThreads) void factored_update_kernel(float* __restrict__ theta, const float* __restrict__ u,
                                                                       const float* __restrict__ h, int64_t P, int64_t nrows,
@@ -178,31 +179,172 @@ __global__ __launch_bounds__(kUpdThreads) void factored_update_kernel(float* __r
         const float rs = rsum[b];
         const float a = rs > 0.f ? Rr[i] / rs * sc.inv_bc2 : 0.f;
         const float* cb = Cc + b * bc;
+        f32x4 t4[KC], u4[KC], h4[KC], c4[KC];
+#pragma unroll
+        for (int k = 0; k < KC; ++k) {   // clamped loads, all in flight; stores below are guarded
+            const int j = (k * kUpdThreads + t) * 4;
+            const int jc = j < bc ? j : bc - 4;
+            const int64_t e = i * bc + jc;
+            const int64_t ec = e < P ? e : P - 4;
+            t4[k] = ld_stream(theta + ec);
+            u4[k] = ld_stream(u + ec);
+            if (SPLIT) h4[k] = ld_stream(h + ec);
+            c4[k] = *reinterpret_cast<const f32x4*>(cb + jc);
+        }
 #pragma unroll
         for (int k = 0; k < KC; ++k) {
             const int j = (k * kUpdThreads + t) * 4;
             const int64_t e = i * bc + j;
-            if (j < bc && e < P) {
-                float4 t4 = *reinterpret_cast<const float4*>(theta + e);
-                const float4 u4 = *reinterpret_cast<const float4*>(u + e);
-                float4 h4 = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (SPLIT) h4 = *reinterpret_cast<const float4*>(h + e);
-                const float4 c4 = *reinterpret_cast<const float4*>(cb + j);
-                float th[4] = {t4.x, t4.y, t4.z, t4.w};
-                const float uu[4] = {u4.x, u4.y, u4.z, u4.w};
-                const float hh[4] = {h4.x, h4.y, h4.z, h4.w};
-                const float cc[4] = {c4.x, c4.y, c4.z, c4.w};
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const float up = numerator<SPLIT>(uu[c], hh[c], sc);
-                    const float vhat = a * cc[c];
-                    const float wd = decay_of(e + c, segs);
-                    th[c] = (1.0f - sc.lr * wd) * th[c] - sc.lr * (up / (sqrtf(vhat) + sc.eps));
-                }
-                *reinterpret_cast<float4*>(theta + e) = make_float4(th[0], th[1], th[2], th[3]);
+            for (int c = 0; c < 4; ++c) {
+                const float up = numerator<SPLIT>(u4[k][c], SPLIT ? h4[k][c] : 0.f, sc);
+                const float vhat = a * c4[k][c];
+                const float wd = decay_of(e + c, segs);
+                t4[k][c] = (1.0f - sc.lr * wd) * t4[k][c] - sc.lr * (up / (sqrtf(vhat) + sc.eps));
             }
+            if (j < bc && e < P) st_stream(theta + e, t4[k]);
         }
     }
+}
+
+// Update with one 16-byte group per thread, like the dense kernel: element e = 4q lies in row
+// i = e / bc of block b = i / block_rows; v_hat = (Rr_i / rsum_b * inv_bc2) * Cc_b[j]. Rr, rsum and
+// Cc are small and shared by many threads (cache hits); theta and u are streamed.
+template <bool SPLIT>
+__global__ __launch_bounds__(kUpdThreads) void factored_update_vec4_kernel(float* __restrict__ theta,
+                                                                           const float* __restrict__ u,
+                                                                           const float* __restrict__ h, int64_t nvec,
+                                                                           int64_t block_rows, int bc,
+                                                                           const float* __restrict__ Rr,
+                                                                           const float* __restrict__ Cc,
+                                                                           const float* __restrict__ rsum, SegTable segs,
+                                                                           UpdateScalars sc) {
+    const int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x;
+    if (q >= nvec) return;
+    const int64_t e = q * 4;
+    f32x4 t4 = ld_stream(theta + e);
+    const f32x4 u4 = ld_stream(u + e);
+    f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
+    if (SPLIT) h4 = ld_stream(h + e);
+    const int64_t i = e / bc;
+    const int j = (int)(e - i * bc);
+    const int64_t b = i / block_rows;
+    const f32x4 c4 = *reinterpret_cast<const f32x4*>(Cc + b * bc + j);
+    const float rs = rsum[b];
+    const float a = rs > 0.f ? Rr[i] / rs * sc.inv_bc2 : 0.f;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const float up = numerator<SPLIT>(u4[c], h4[c], sc);
+        const float vhat = a * c4[c];
+        const float wd = decay_of(e + c, segs);
+        t4[c] = (1.0f - sc.lr * wd) * t4[c] - sc.lr * (up / (sqrtf(vhat) + sc.eps));
+    }
+    st_stream(theta + e, t4);
+}
+
+// Row kernels for block_cols = NV * 256 (up to 4096): a wave owns whole rows, lane l holding
+// columns (k*64 + l)*4 .. +3 for k < NV, so each row's loads are all in flight together and the row
+// statistic is one wave reduction. Elements at or past P (only in the last row) count as zero.
+template <bool SPLIT, int NV>
+__global__ __launch_bounds__(kUpdThreads) void factored_stats_rows_kernel(const float* __restrict__ u,
+                                                                          const float* __restrict__ h, int64_t P,
+                                                                          int64_t nrows, int64_t block_rows,
+                                                                          int groups_per_block, float* __restrict__ Rr,
+                                                                          float* __restrict__ kpart, UpdateScalars sc) {
+    constexpr int BC = NV * 256;
+    __shared__ f32x4 sh[3][BC / 4];
+    const int t = threadIdx.x, l = t % kWave, w = t / kWave;
+    const int64_t b = blockIdx.x / groups_per_block;
+    const int64_t g = blockIdx.x % groups_per_block;
+    const int64_t blk_end = min((b + 1) * block_rows, nrows);
+    const int64_t r0 = b * block_rows + g * kFacRowsPerWG;
+    const int64_t r1 = min(r0 + kFacRowsPerWG, blk_end);
+    f32x4 kap[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) kap[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int64_t i = r0 + w; i < r1; i += kUpdThreads / kWave) {
+        f32x4 a[NV];
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int64_t e = i * BC + (k * kWave + l) * 4;
+            const bool ok = e < P;
+            const int64_t ec = ok ? e : P - 4;
+            const f32x4 u4 = *reinterpret_cast<const f32x4*>(u + ec);
+            f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
+            if (SPLIT) h4 = *reinterpret_cast<const f32x4*>(h + ec);
+            const float z = ok ? 1.f : 0.f;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) a[k][c] = z * numerator<SPLIT>(u4[c], h4[c], sc);
+        }
+        float rho = 0.f;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const f32x4 s2 = a[k] * a[k];
+            kap[k] += s2;
+            rho += (s2[0] + s2[1]) + (s2[2] + s2[3]);
+        }
+        rho = wave_sum(rho);
+        if (l == 0) Rr[i] = sc.beta2 * Rr[i] + sc.one_minus_beta2 * rho;
+    }
+    if (w > 0) {
+#pragma unroll
+        for (int k = 0; k < NV; ++k) sh[w - 1][k * kWave + l] = kap[k];
+    }
+    __syncthreads();
+    if (w == 0) {
+        float* kp = kpart + (int64_t)blockIdx.x * BC;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int q = k * kWave + l;
+            *reinterpret_cast<f32x4*>(kp + q * 4) = ((kap[k] + sh[0][q]) + sh[1][q]) + sh[2][q];
+        }
+    }
+}
+
+// Per-block finish over column chunks of 1024: Cc_j = beta2 Cc_j + (1 - beta2) sum_g kpart[g][j] (in
+// group order); chunk 0 also forms rsum[b] = sum of the block's Rr.
+__global__ __launch_bounds__(kUpdThreads) void factored_finish_cols_kernel(const float* __restrict__ kpart,
+                                                                           int groups_per_block, int64_t nrows,
+                                                                           int64_t block_rows, int bc, int nchunks,
+                                                                           const float* __restrict__ Rr,
+                                                                           float* __restrict__ Cc,
+                                                                           float* __restrict__ rsum, UpdateScalars sc) {
+    __shared__ float sh[kUpdThreads];
+    const int64_t b = blockIdx.x / nchunks;
+    const int chunk = blockIdx.x % nchunks;
+    const int t = threadIdx.x;
+    const int64_t r0 = b * block_rows;
+    const int64_t r1 = min(r0 + block_rows, nrows);
+    const int ng = (int)((r1 - r0 + kFacRowsPerWG - 1) / kFacRowsPerWG);
+    const float* kp = kpart + b * groups_per_block * (int64_t)bc;
+    const int j = chunk * 1024 + t * 4;
+    if (j < bc) {
+        f32x4 c = {0.f, 0.f, 0.f, 0.f};
+        int gi = 0;
+        for (; gi + 4 <= ng; gi += 4) {
+            const f32x4 p0 = *reinterpret_cast<const f32x4*>(kp + (int64_t)(gi + 0) * bc + j);
+            const f32x4 p1 = *reinterpret_cast<const f32x4*>(kp + (int64_t)(gi + 1) * bc + j);
+            const f32x4 p2 = *reinterpret_cast<const f32x4*>(kp + (int64_t)(gi + 2) * bc + j);
+            const f32x4 p3 = *reinterpret_cast<const f32x4*>(kp + (int64_t)(gi + 3) * bc + j);
+            c += p0;
+            c += p1;
+            c += p2;
+            c += p3;
+        }
+        for (; gi < ng; ++gi) c += *reinterpret_cast<const f32x4*>(kp + (int64_t)gi * bc + j);
+        f32x4 old = *reinterpret_cast<const f32x4*>(Cc + b * bc + j);
+        *reinterpret_cast<f32x4*>(Cc + b * bc + j) = sc.beta2 * old + sc.one_minus_beta2 * c;
+    }
+    if (chunk != 0) return;
+    float r = 0.f;
+    for (int64_t i = r0 + t; i < r1; i += kUpdThreads) r += Rr[i];
+    sh[t] = r;
+    __syncthreads();
+    for (int o = kUpdThreads / 2; o > 0; o >>= 1) {
+        if (t < o) sh[t] += sh[t + o];
+        __syncthreads();
+    }
+    if (t == 0) rsum[b] = sh[0];
 }
 
 struct FacLayout {
@@ -243,9 +385,35 @@ hipError_t run_factored(float* theta, float* Rr, float* Cc, const float* u, cons
     return hipGetLastError();
 }
 
+template <bool SPLIT, int NV>
+hipError_t run_factored_rows(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P, int64_t br,
+                             const SegTable& segs, const UpdateScalars& sc, void* ws, hipStream_t st) {
+    constexpr int BC = NV * 256;
+    const FacLayout L = fac_layout(P, br, BC);
+    float* kpart = reinterpret_cast<float*>(static_cast<char*>(ws) + L.kpart_off);
+    float* rsum = reinterpret_cast<float*>(static_cast<char*>(ws) + L.rsum_off);
+    hipLaunchKernelGGL((factored_stats_rows_kernel<SPLIT, NV>), dim3((unsigned)L.ngroups), dim3(kUpdThreads), 0, st, u, h,
+                       P, L.nrows, br, (int)L.groups_per_block, Rr, kpart, sc);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int nchunks = (BC + 1023) / 1024;
+    hipLaunchKernelGGL(factored_finish_cols_kernel, dim3((unsigned)(L.nblocks * nchunks)), dim3(kUpdThreads), 0, st,
+                       kpart, (int)L.groups_per_block, L.nrows, br, BC, nchunks, Rr, Cc, rsum, sc);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t nvec = P / 4;
+    hipLaunchKernelGGL((factored_update_vec4_kernel<SPLIT>), dim3((unsigned)((nvec + kUpdThreads - 1) / kUpdThreads)),
+                       dim3(kUpdThreads), 0, st, theta, u, h, nvec, br, BC, Rr, Cc, rsum, segs, sc);
+    return hipGetLastError();
+}
+
 template <bool SPLIT>
 hipError_t dispatch_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P, int64_t br,
                              int bc, const SegTable& segs, const UpdateScalars& sc, void* ws, hipStream_t st) {
+    // whole-row kernels for block_cols of 1024, 2048 or 4096; the column-strip kernels otherwise
+    if (bc == 4096) return run_factored_rows<SPLIT, 16>(theta, Rr, Cc, u, h, P, br, segs, sc, ws, st);
+    if (bc == 2048) return run_factored_rows<SPLIT, 8>(theta, Rr, Cc, u, h, P, br, segs, sc, ws, st);
+    if (bc == 1024) return run_factored_rows<SPLIT, 4>(theta, Rr, Cc, u, h, P, br, segs, sc, ws, st);
     const int kc = (bc + 1023) / 1024;
     if (kc <= 1) return run_factored<SPLIT, 1>(theta, Rr, Cc, u, h, P, br, bc, segs, sc, ws, st);
     if (kc <= 2) return run_factored<SPLIT, 2>(theta, Rr, Cc, u, h, P, br, bc, segs, sc, ws, st);

@@ -270,8 +270,11 @@ __global__ __launch_bounds__(THREADS) void residual_rows_kernel(
 
 // ---------------------------------------------------------------------------------------------
 // Single pass, wide bf16 rows: each thread parks its raw 16-byte chunks in its own LDS slots
-// (thread-private: no barrier beyond the row reductions) and keeps only its column accumulators in
-// registers; exp is evaluated twice per element (for the sum, then for p).
+// (thread-private) and keeps only its column accumulators in registers. Rows are software-
+// pipelined: row i+1 is loaded into registers while row i is processed. The row maximum, argmax
+// and sum of exp(z - max) come from one online pass over the registers (running max with the sum
+// rescaled when it grows) and one combined workgroup reduction; the second pass reads the parked
+// row to form p = exp(z - lse), the residual, the column sums and R.
 template <int THREADS, int NCH>
 __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
     const uint16_t* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
@@ -281,9 +284,9 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
     constexpr int NW = THREADS / kWave;
     constexpr int VPT = NCH * VEC;
     __shared__ uint4 slots[NCH * THREADS];
-    __shared__ float sh_max[NW];
-    __shared__ int sh_idx[NW];
-    __shared__ float sh_sum[NW];
+    __shared__ float sh_m[NW];
+    __shared__ float sh_l[NW];
+    __shared__ int sh_i[NW];
     const int tid = threadIdx.x;
     float acc[VPT];
 #pragma unroll
@@ -297,55 +300,93 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
         x[0] = bf16_lo(u.x); x[1] = bf16_hi(u.x); x[2] = bf16_lo(u.y); x[3] = bf16_hi(u.y);
         x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z); x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
     };
-    for (int i = row0; i < row1; ++i) {
+    // merge of two (max, sum of exp(z - max), first index of max) triples
+    auto merge = [](float& m, float& l, int& idx, float mo, float lo, int io) {
+        const float mn = fmaxf(m, mo);
+        const float a = (m == -INFINITY) ? 0.f : l * exp2_fast((m - mn) * kLog2e);
+        const float b2 = (mo == -INFINITY) ? 0.f : lo * exp2_fast((mo - mn) * kLog2e);
+        l = a + b2;
+        idx = (m > mo) ? idx : (mo > m ? io : min(idx, io));
+        m = mn;
+    };
+    // only the last chunk can fall outside the row
+    auto load_row = [&](int i, uint4 (&u)[NCH]) {
         const uint16_t* zr = Z + (int64_t)i * ldz;
-        // pass 1: load, park, max (only the last chunk can fall outside the row)
-        float tm = -INFINITY;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const int col = (c * THREADS + tid) * VEC;
             const bool ok = c < NCH - 1 || col < V;
-            uint4 u = *reinterpret_cast<const uint4*>(zr + (ok ? col : V - VEC));
+            u[c] = *reinterpret_cast<const uint4*>(zr + (ok ? col : V - VEC));
+        }
+    };
+    uint4 nxt[NCH];
+    if (row0 < row1) load_row(row0, nxt);
+    for (int i = row0; i < row1; ++i) {
+        const uint16_t* zr = Z + (int64_t)i * ldz;
+        // park the row (padding of the last chunk: bf16 -inf), then prefetch row i+1 into the
+        // registers it came from (the last row reloads itself)
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            uint4 u = nxt[c];
             if (c == NCH - 1) {
-                const uint32_t m = lane_mask(ok), fb = 0xFF80FF80u & ~m;
-                u = make_uint4((u.x & m) | fb, (u.y & m) | fb, (u.z & m) | fb, (u.w & m) | fb);
+                const bool ok = ((c * THREADS + tid) * VEC) < V;
+                const uint32_t mk = lane_mask(ok), fb = 0xFF80FF80u & ~mk;
+                u = make_uint4((u.x & mk) | fb, (u.y & mk) | fb, (u.z & mk) | fb, (u.w & mk) | fb);
             }
             slots[c * THREADS + tid] = u;
-            float x[VEC];
-            unpack(u, x);
-#pragma unroll
-            for (int k = 0; k < VEC; ++k) tm = fmaxf(tm, x[k]);
         }
-        const float m = block_max<NW>(tm, sh_max);
-        int ti = INT_MAX;
-        if (tm == m) {
-            for (int c = NCH - 1; c >= 0; --c) {
-                float x[VEC];
-                unpack(slots[c * THREADS + tid], x);
-#pragma unroll
-                for (int k = VEC - 1; k >= 0; --k)
-                    if (x[k] == m) ti = (c * THREADS + tid) * VEC + k;
-            }
-        }
-        const int am = block_min<NW>(ti, sh_idx);
-        // pass 2: l = sum exp(z - m)
-        const float m2 = m * kLog2e;
-        float l = 0.f;
+        load_row(min(i + 1, row1 - 1), nxt);
+        // pass 1 (LDS): online (max, sum, argmax) over this thread's chunks, in column order
+        float m = -INFINITY, l = 0.f;
+        int idx = INT_MAX;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             float x[VEC];
             unpack(slots[c * THREADS + tid], x);
+            float cm = x[0];
 #pragma unroll
-            for (int k = 0; k < VEC; ++k) l += exp2_fast(fmaf(x[k], kLog2e, -m2));
+            for (int k = 1; k < VEC; ++k) cm = fmaxf(cm, x[k]);
+            int ci = INT_MAX;
+#pragma unroll
+            for (int k = VEC - 1; k >= 0; --k)
+                if (x[k] == cm) ci = (c * THREADS + tid) * VEC + k;
+            const float mn = fmaxf(m, cm);
+            // a padding-only chunk after real ones leaves (m, l) unchanged (mn == m, terms zero);
+            // chunk 0 of every thread lies inside the row, so mn is finite
+            const float mn2 = mn * kLog2e;
+            float cl = 0.f;
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) cl += exp2_fast(fmaf(x[k], kLog2e, -mn2));
+            l = (c == 0 ? 0.f : l * exp2_fast((m - mn) * kLog2e)) + cl;
+            if (cm > m) idx = ci;
+            m = mn;
         }
-        l = block_sum<NW>(l, sh_sum);
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) {
+            const float mo = __shfl_xor(m, o, kWave);
+            const float lo = __shfl_xor(l, o, kWave);
+            const int io = __shfl_xor(idx, o, kWave);
+            merge(m, l, idx, mo, lo, io);
+        }
+        if ((tid & (kWave - 1)) == 0) {
+            sh_m[tid / kWave] = m;
+            sh_l[tid / kWave] = l;
+            sh_i[tid / kWave] = idx;
+        }
+        __syncthreads();
+        m = sh_m[0];
+        l = sh_l[0];
+        idx = sh_i[0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) merge(m, l, idx, sh_m[w], sh_l[w], sh_i[w]);
         const float lse = m + logf(l);
+        const int am = idx;
         const int y = labels[i];
         bool rbad = false;
         const bool valid = label_valid(y, V, ignore_index, &rbad);
         bad |= rbad;
         uint16_t* rr = R ? R + (int64_t)i * ldr : nullptr;
-        // pass 3: p = exp(z - lse), residual, column accumulation, R
+        // pass 2 (LDS): p = exp(z - lse), residual, column accumulation, R
         const int yv = y / VEC;
         const int slot = (valid && yv % THREADS == tid) ? (yv / THREADS) * VEC + (y % VEC) : -1;
         const float lse2 = lse * kLog2e;
@@ -381,6 +422,7 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
                 ce += (double)lse - (double)zt;
             }
         }
+        __syncthreads();   // the reduction slots are rewritten by the next row
     }
     float* prow = ws.part + (int64_t)blockIdx.x * V;
 #pragma unroll
@@ -645,6 +687,7 @@ hipError_t launch_rows(const T* Z, int64_t ldz, int N, int V, const int32_t* lab
 
 // Allowed chunk counts for 512-thread single-pass workgroups (registers: 2 * NCH * VEC floats).
 constexpr int kNchSet[] = {1, 2, 3, 4, 6, 8, 10, 13};
+constexpr int kLdsNchSet[] = {2, 3, 4, 6, 8, 10, 12, 13, 14};
 
 template <typename T, int VEC>
 hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, int V, const int32_t* labels,
@@ -660,17 +703,26 @@ hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, i
             case 2: return BOM_ROWS(1024, 2);
             case 3: return BOM_ROWS(1024, 3);
             case 4: return BOM_ROWS(1024, 4);
-            default: break;
+            default: return hipErrorInvalidValue;
         }
-        if constexpr (std::is_same<T, uint16_t>::value && VEC == 8) {
+    }
+    if constexpr (std::is_same<T, uint16_t>::value && VEC == 8) {
+        if (threads == -512) {   // bf16 rows parked in LDS, next row prefetched
+#define BOM_LDS(NC) launch_rows_lds<512, NC>(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, nwg, st)
             switch (nch) {
-                case 5: return launch_rows_lds<1024, 5>(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, nwg, st);
-                case 6: return launch_rows_lds<1024, 6>(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, nwg, st);
-                case 7: return launch_rows_lds<1024, 7>(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, nwg, st);
-                default: break;
+                case 2: return BOM_LDS(2);
+                case 3: return BOM_LDS(3);
+                case 4: return BOM_LDS(4);
+                case 6: return BOM_LDS(6);
+                case 8: return BOM_LDS(8);
+                case 10: return BOM_LDS(10);
+                case 12: return BOM_LDS(12);
+                case 13: return BOM_LDS(13);
+                case 14: return BOM_LDS(14);
+                default: return hipErrorInvalidValue;
             }
+#undef BOM_LDS
         }
-        return hipErrorInvalidValue;
     }
     switch (nch) {
         case 1: return BOM_ROWS(512, 1);
@@ -687,7 +739,7 @@ hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, i
 }
 
 // Variant override for A/B measurement (environment BOM_RESIDUAL_PLAN, read once):
-// 0 automatic, 1 = 512-thread register rows, 2 = 1024-thread rows (registers or LDS), 3 = two pass.
+// 0 automatic, 1 = 512-thread register rows, 2 = 1024-thread register rows, 3 = two pass.
 int plan_override() {
     static const int v = [] {
         const char* e = getenv("BOM_RESIDUAL_PLAN");
@@ -712,9 +764,20 @@ bool plan_single(int V, int VEC, int* threads, int* nch) {
         return true;
     }
     const int need1k = (slots + 1023) / 1024;
-    // automatic: 512-thread register rows up to 8 chunks, then 1024-thread rows
+    // automatic: bf16 rows wider than 512 chunks are parked in LDS by 512-thread workgroups, which
+    // prefetch the next row into registers (threads = -512 marks that kernel); fp32 rows use
+    // 512-thread register rows up to 8 chunks, then 1024-thread register rows
+    if (VEC == 8 && ov == 0 && need >= 2) {
+        for (int c : kLdsNchSet) {
+            if (c >= need) {
+                *threads = -512;
+                *nch = c;
+                return true;
+            }
+        }
+    }
     const bool use1k = ov == 2 || (ov == 0 && need > 8);
-    if (use1k && slots > 512 && need1k <= (VEC == 8 ? 7 : 4) && VEC != 1) {
+    if (use1k && slots > 512 && need1k <= 4 && VEC != 1) {
         *threads = 1024;
         *nch = need1k;
         return true;

@@ -30,6 +30,7 @@ RESIDUAL_CASES = [
     ("bf16_v1003_scalar", 77, 1003, "bf16", "zipf", 0.05, 2, 0.55),
     ("f32_v4100_peaked", 129, 4100, "f32", "zipf", 0.05, 2, 11.0),
     ("bf16_v32000", 96, 32000, "bf16", "zipf", 0.05, 2, 0.55),
+    ("bf16_v12000_multirow", 600, 12000, "bf16", "zipf", 0.05, 3, 0.55),
     ("bf16_v50304_packed", 64, 50304, "bf16", "zipf", 0.05, 2, 0.91),
     ("bf16_v70000_twopass", 40, 70000, "bf16", "zipf", 0.05, 2, 1.28),
     ("f32_v70003_twopass_scalar", 40, 70003, "f32", "zipf", 0.05, 2, 1.28),

@@ -94,4 +94,15 @@ __device__ __forceinline__ bool label_valid(int32_t y, int64_t V, int32_t ignore
     return true;
 }
 
+constexpr int kBufFlags = 0x00020000;   // raw buffer descriptor word 3: 32-bit data format
+constexpr int kOob = (int)0x80000000u;  // an offset past every range: the load returns zeros
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor over [base, base + bytes): loads at offsets >= bytes return zeros and
+// stores there are dropped.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_desc(const void* base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufFlags);
+}
+
 }  // namespace bom

@@ -760,15 +760,6 @@ __global__ __launch_bounds__(256, 1) void mfma256_kernel(const uint16_t* __restr
 // branches and never touch memory past the operand.
 constexpr int LB = 256;                 // output tile
 constexpr int LK = 32;                  // k tile (split-K granularity)
-constexpr int kBufFlags = 0x00020000;   // raw buffer descriptor word 3: 32-bit data format
-constexpr int kOob = (int)0x80000000u;  // an offset past every range: the load returns zeros
-
-typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
-
-// Raw buffer descriptor over [base, base + bytes): loads at offsets >= bytes return zeros.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_desc(const void* base, int bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufFlags);
-}
 
 // C = A B for one 256 x 256 tile over k in [kb, ke); dW: A(m, k) = H[k][m], B(k, n) = R[k][n];
 // dH: A(i, k) = R[i][k], B(k, n) = W[n][k]. k tiles of 32 in a ring of 4 LDS stages (32 KB each).
@@ -1042,6 +1033,216 @@ __global__ __launch_bounds__(256, 1) void lds256_kernel(const uint16_t* __restri
     }
 }
 
+// The same product with k tiles of 64 in two LDS stages (one barrier per 64 k instead of per 32):
+// each wave copies 8 kilobytes per operand per tile; dH's LDS rows are 64 k (128 B) with chunk c of
+// row r at swz(r, c), dW's LDS rows are 512 B per k as in lds256_kernel. Tile kt+1 is written from
+// registers at the start of iteration kt and tile kt+2 loaded behind it; the barrier sits before the
+// last MFMA step of the tile.
+template <bool IS_DW, typename TO>
+__global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restrict__ Xa, int64_t lda,
+                                                         const uint16_t* __restrict__ Xb, int64_t ldb, int M, int Nn, int K,
+                                                         int kps, int inner_count, int outer_count, const float* alpha_p,
+                                                         const float* __restrict__ rv, const float* __restrict__ cv,
+                                                         TO* __restrict__ out, int64_t ldo, float beta,
+                                                         float* __restrict__ part) {
+    constexpr int KT = 64;
+    constexpr int SE = LB * KT;   // bf16 elements per operand per stage (32 KB)
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][SE];
+    __shared__ float rv_s[LB];
+    int tm, tn;
+    if (!tile_of(inner_count, outer_count, IS_DW, &tm, &tn)) return;
+    const int m0 = tm * LB, n0 = tn * LB;
+    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
+    const int nk = (ke - kb + KT - 1) / KT;
+    const int l = threadIdx.x % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wm = wave / 2, wn = wave % 2;
+
+    const float rv_reg = (part == nullptr && m0 + (int)threadIdx.x < M) ? rv[m0 + threadIdx.x] : 0.f;
+    float cvv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int n = n0 + wn * 128 + j * 32 + l % 32;
+        cvv[j] = (part == nullptr && n < Nn) ? cv[n] : 0.f;
+    }
+
+    // copy step q (< 8) of this wave fills kilobyte wave*8 + q of an operand's stage
+    int voff_a[8], voff_b[8], kc[8];
+    bool ok_a[8], ok_b[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const int chunk = (wave * 8 + q) * 64 + l;
+        if constexpr (IS_DW) {
+            const int krow = chunk / 32, c = (chunk % 32) ^ ((krow & 3) << 2);
+            voff_a[q] = (int)((int64_t)krow * lda * 2) + c * 16;
+            voff_b[q] = (int)((int64_t)krow * ldb * 2) + c * 16;
+            kc[q] = krow;
+            ok_a[q] = ok_b[q] = true;
+        } else {
+            const int row = chunk / 8, c = swz(row, chunk % 8);
+            voff_a[q] = (int)((int64_t)row * lda * 2) + c * 16;
+            voff_b[q] = (int)((int64_t)row * ldb * 2) + c * 16;
+            kc[q] = c * 8;
+            ok_a[q] = row < M - m0;
+            ok_b[q] = row < Nn - n0;
+        }
+    }
+    int bytes_ta = 0, bytes_tb = 0;
+    if constexpr (!IS_DW) {
+        const int ra = min(LB, M - m0), rb = min(LB, Nn - n0);
+        bytes_ta = (int)(((int64_t)(ra - 1) * lda + K) * 2);
+        bytes_tb = (int)(((int64_t)(rb - 1) * ldb + K) * 2);
+    }
+    struct TileLoad {
+        const uint16_t* ba;
+        const uint16_t* bb;
+        int bytes_a, bytes_b, k0;
+    };
+    auto tile_load = [&](int kt) {
+        TileLoad tl;
+        tl.k0 = kb + kt * KT;
+        if constexpr (IS_DW) {
+            const int nv = min(KT, ke - tl.k0);
+            const int nv1 = max(nv, 1);
+            const int kr = min(tl.k0, K - 1);
+            tl.ba = Xa + (int64_t)kr * lda + m0;
+            tl.bb = Xb + (int64_t)kr * ldb + n0;
+            tl.bytes_a = nv > 0 ? (int)(((int64_t)(nv1 - 1) * lda + (M - m0)) * 2) : 0;
+            tl.bytes_b = nv > 0 ? (int)(((int64_t)(nv1 - 1) * ldb + (Nn - n0)) * 2) : 0;
+        } else {
+            tl.ba = Xa + (int64_t)m0 * lda;
+            tl.bb = Xb + (int64_t)n0 * ldb;
+            tl.bytes_a = bytes_ta;
+            tl.bytes_b = bytes_tb;
+        }
+        return tl;
+    };
+    // copy op q < 16: q < 8 operand A, else operand B
+    auto load_one = [&](const TileLoad& tl, int q) {
+        if (q < 8) {
+            const int vo = IS_DW ? voff_a[q] : ((ok_a[q] && tl.k0 + kc[q] < ke) ? voff_a[q] + tl.k0 * 2 : kOob);
+            return __builtin_amdgcn_raw_buffer_load_b128(make_desc(tl.ba, tl.bytes_a), vo, 0, 0);
+        }
+        const int r = q - 8;
+        const int vo = IS_DW ? voff_b[r] : ((ok_b[r] && tl.k0 + kc[r] < ke) ? voff_b[r] + tl.k0 * 2 : kOob);
+        return __builtin_amdgcn_raw_buffer_load_b128(make_desc(tl.bb, tl.bytes_b), vo, 0, 0);
+    };
+    auto write_one = [&](int stage, int q, const u32x4_t& v) {
+        char* base = reinterpret_cast<char*>(&lds[stage][q / 8][0]);
+        *reinterpret_cast<u32x4_t*>(base + (wave * 8 + q % 8) * 1024 + l * 16) = v;
+    };
+
+    // fragments for MFMA step s (k = 16 s .. +15)
+    int fa[4], fb[4];
+    if constexpr (IS_DW) {
+        const int s = l % 16, g = l / 16;
+        const int krow = (g >> 1) * 8 + (s >> 2);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int lo = ((i ^ (s >> 2)) * 4) + (g & 1) * 2 + ((s >> 1) & 1);
+            fa[i] = krow * 512 + ((wm * 16 + lo) << 4) + (s & 1) * 8;
+            fb[i] = krow * 512 + ((wn * 16 + lo) << 4) + (s & 1) * 8;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            fa[i] = wm * 128 + i * 32 + l % 32;   // LDS rows; the chunk depends on the step
+            fb[i] = wn * 128 + i * 32 + l % 32;
+        }
+    }
+    auto read_frags = [&](int stage, int s, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
+        const char* As = reinterpret_cast<const char*>(&lds[stage][0][0]);
+        const char* Bs = reinterpret_cast<const char*>(&lds[stage][1][0]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (IS_DW) {
+                a[i] = ld_frag_tr(As + fa[i] + s * 16 * 512);
+                b[i] = ld_frag_tr(Bs + fb[i] + s * 16 * 512);
+            } else {
+                const int c = 2 * s + l / 32;
+                a[i] = ld_frag_b128(As + fa[i] * 128 + swz(fa[i], c) * 16);
+                b[i] = ld_frag_b128(Bs + fb[i] * 128 + swz(fb[i], c) * 16);
+            }
+        }
+    };
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    // one MFMA step; copy ops q0 .. q0+7 placed after its MFMAs 0..7 (if q0 >= 0)
+    auto step = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], int q0, int ws, const TileLoad& tl,
+                    u32x4_t (&rg)[16]) {
+#pragma unroll
+        for (int m = 0; m < 16; ++m) {
+            acc[m / 4][m % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[m / 4], b[m % 4], acc[m / 4][m % 4], 0, 0, 0);
+            if (q0 >= 0 && m < 8) {
+                __builtin_amdgcn_sched_barrier(0);
+                write_one(ws, q0 + m, rg[q0 + m]);
+                rg[q0 + m] = load_one(tl, q0 + m);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    };
+    u32x4_t rg[16];
+    bf16x8_t a0[4], b0[4], a1[4], b1[4];
+    {
+        const TileLoad t0 = tile_load(0), t1 = tile_load(1);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) rg[q] = load_one(t0, q);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) write_one(0, q, rg[q]);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) rg[q] = load_one(t1, q);
+    }
+    __syncthreads();
+    read_frags(0, 0, a0, b0);
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1, nxt = cur ^ 1;
+        const TileLoad tl = tile_load(kt + 2);
+        read_frags(cur, 1, a1, b1);
+        step(a0, b0, 0, nxt, tl, rg);
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(cur, 2, a0, b0);
+        step(a1, b1, 8, nxt, tl, rg);
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(cur, 3, a1, b1);
+        step(a0, b0, -1, nxt, tl, rg);
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(nxt, 0, a0, b0);
+        step(a1, b1, -1, nxt, tl, rg);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    const float alpha = *alpha_p;
+    if (part == nullptr) {
+        rv_s[threadIdx.x] = rv_reg;
+        __syncthreads();
+        for_each_acc256(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) {
+                const float x = fmaf(alpha, v, rv_s[r] * cvv[(c >> 5) & 3]);
+                if constexpr (IS_DW) {
+                    float* p = reinterpret_cast<float*>(out) + (int64_t)m * ldo + n;
+                    *p = beta != 0.f ? x + beta * *p : x;
+                } else {
+                    stf<TO>(out, (int64_t)m * ldo + n, x);
+                }
+            }
+        });
+    } else {
+        float* pz = part + (int64_t)blockIdx.z * M * Nn;
+        for_each_acc256(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = alpha * v;
+        });
+    }
+}
+
 // Split-K reduction for the rank-1 form, in split order: out = sum_z part[z] + rv[m] cv[n] (+ beta out).
 template <typename TO>
 __global__ __launch_bounds__(256) void splitk_rank1_kernel(const float* __restrict__ part, int splits, int M, int Nn,
@@ -1181,6 +1382,7 @@ constexpr int kMaxSplits = 8;
 enum GemmKind { kSimt = 0, kMfma128 = 1, kMfma256 = 2, kRank1 = 3 };
 struct GemmPlan {
     int kind, splits;
+    int wide = 0;   // rank-1 kind: k tiles of 64 in two stages (lds256w_kernel)
 };
 struct Plan {
     GemmPlan w, h;
@@ -1245,8 +1447,12 @@ void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int
     if (kind == kMfma128) g.kind = kMfma128;
     if (kind == kMfma256 && K >= 4 * TK) g.kind = kMfma256;
     if (kind == kRank1) g.kind = kRank1;
+    if (kind == 4) {
+        g.kind = kRank1;
+        g.wide = 1;
+    }
     if (splits > 0) {
-        const int ktile = g.kind == kMfma256 ? TK : (g.kind == kRank1 ? LK : MK);
+        const int ktile = g.kind == kMfma256 ? TK : (g.kind == kRank1 ? LK * (1 + g.wide) : MK);
         // every split keeps at least one k tile
         g.splits = (int)(splits < cdiv(K, ktile) ? splits : cdiv(K, ktile));
     }
@@ -1295,14 +1501,21 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
     const int splits = g.splits;
     if (g.kind == kRank1) {
         // rank-1 form: out = alpha A B + rv cv^T (+ beta out)
-        const int kps = (int)(cdiv(cdiv(K, splits), LK) * LK);
+        const int kt = g.wide ? 2 * LK : LK;
+        const int kps = (int)(cdiv(cdiv(K, splits), kt) * kt);
         const int MT = (int)cdiv(M, LB), NT = (int)cdiv(Nn, LB);
         const int inner = is_dw ? MT : NT, outer = is_dw ? NT : MT;
         dim3 grid((unsigned)(cdiv(outer, 8) * 8 * inner), 1, splits);
         float* pz = splits > 1 ? part : nullptr;
         const uint16_t* a16 = static_cast<const uint16_t*>(A);
         const uint16_t* b16 = static_cast<const uint16_t*>(B);
-        if (is_dw)
+        if (g.wide && is_dw)
+            hipLaunchKernelGGL((lds256w_kernel<true, float>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
+                               inner, outer, f.scal, rv, cv, reinterpret_cast<float*>(out), ldo, beta, pz);
+        else if (g.wide)
+            hipLaunchKernelGGL((lds256w_kernel<false, TO>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
+                               inner, outer, f.scal, rv, cv, out, ldo, beta, pz);
+        else if (is_dw)
             hipLaunchKernelGGL((lds256_kernel<true, float>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
                                inner, outer, f.scal, rv, cv, reinterpret_cast<float*>(out), ldo, beta, pz);
         else

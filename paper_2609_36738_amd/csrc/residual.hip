@@ -271,10 +271,15 @@ __global__ __launch_bounds__(THREADS) void residual_rows_kernel(
 // ---------------------------------------------------------------------------------------------
 // Single pass, wide bf16 rows: each thread parks its raw 16-byte chunks in its own LDS slots
 // (thread-private) and keeps only its column accumulators in registers. Rows are software-
-// pipelined: row i+1 is loaded into registers while row i is processed. The row maximum, argmax
-// and sum of exp(z - max) come from one online pass over the registers (running max with the sum
-// rescaled when it grows) and one combined workgroup reduction; the second pass reads the parked
-// row to form p = exp(z - lse), the residual, the column sums and R.
+// pipelined through registers: after the second pass of row i the thread parks row i+1 and loads
+// row i+2 into the freed registers, so each row's loads are in flight for a whole row's work.
+// Workgroup g takes rows g, g + G, g + 2G, ... so the workgroups sweep the matrix together. The
+// row maximum and sum of exp(z - max) come from one online pass over the
+// slots (running max with the sum rescaled when it grows), a wave reduction (maximum, then the
+// rescaled sums) and one workgroup barrier per row; the argmax comes from the one chunk per thread
+// where the thread's maximum first appeared. The second pass forms p = exp(z - lse), the
+// residual, the column sums and R. Per-row words shared across the workgroup are double buffered,
+// and the previous row's argmax and target logit are written after the next barrier.
 template <int THREADS, int NCH>
 __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
     const uint16_t* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
@@ -284,15 +289,19 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
     constexpr int NW = THREADS / kWave;
     constexpr int VPT = NCH * VEC;
     __shared__ uint4 slots[NCH * THREADS];
-    __shared__ float sh_m[NW];
-    __shared__ float sh_l[NW];
-    __shared__ int sh_i[NW];
+    __shared__ float sh_m[2][NW];
+    __shared__ float sh_l[2][NW];
+    __shared__ int sh_am[2];
+    __shared__ float sh_zt[2];
     const int tid = threadIdx.x;
     float acc[VPT];
 #pragma unroll
     for (int k = 0; k < VPT; ++k) acc[k] = 0.f;
-    const int row0 = blockIdx.x * rows_per_wg;
-    const int row1 = min(row0 + rows_per_wg, N);
+    // rows blockIdx.x + j * gridDim.x (j < nr): the workgroups sweep the matrix together
+    const int G = gridDim.x;
+    const int nr = blockIdx.x < N ? (N - 1 - (int)blockIdx.x) / G + 1 : 0;
+    auto row_of = [&](int j) { return (int)blockIdx.x + j * G; };
+    (void)rows_per_wg;
     int cnt = 0;
     double ce = 0.0;
     bool bad = false;
@@ -300,99 +309,137 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
         x[0] = bf16_lo(u.x); x[1] = bf16_hi(u.x); x[2] = bf16_lo(u.y); x[3] = bf16_hi(u.y);
         x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z); x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
     };
-    // merge of two (max, sum of exp(z - max), first index of max) triples
-    auto merge = [](float& m, float& l, int& idx, float mo, float lo, int io) {
-        const float mn = fmaxf(m, mo);
-        const float a = (m == -INFINITY) ? 0.f : l * exp2_fast((m - mn) * kLog2e);
-        const float b2 = (mo == -INFINITY) ? 0.f : lo * exp2_fast((mo - mn) * kLog2e);
-        l = a + b2;
-        idx = (m > mo) ? idx : (mo > m ? io : min(idx, io));
-        m = mn;
+    // Row loads and R stores go through per-row buffer descriptors: chunk c of this thread sits at
+    // byte tid*16 + c*THREADS*16. Only the last chunk can fall outside the row; it carries its whole
+    // offset in the range-checked vector offset (loads there return zeros, stores are dropped), the
+    // other chunks add theirs as a scalar offset, so two vector registers address every chunk.
+    const int voff = tid * 16;
+    const int voff_last = ((NCH - 1) * THREADS + tid) * 16;
+    auto row_desc = [&](int i) { return make_desc(Z + (int64_t)i * ldz, V * 2); };
+    auto load_chunk = [&](const __amdgpu_buffer_rsrc_t& d, int c) {
+        const u32x4_t w = c < NCH - 1 ? __builtin_amdgcn_raw_buffer_load_b128(d, voff, c * THREADS * 16, 0)
+                                      : __builtin_amdgcn_raw_buffer_load_b128(d, voff_last, 0, 0);
+        return make_uint4(w[0], w[1], w[2], w[3]);
     };
-    // only the last chunk can fall outside the row
-    auto load_row = [&](int i, uint4 (&u)[NCH]) {
-        const uint16_t* zr = Z + (int64_t)i * ldz;
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const int col = (c * THREADS + tid) * VEC;
-            const bool ok = c < NCH - 1 || col < V;
-            u[c] = *reinterpret_cast<const uint4*>(zr + (ok ? col : V - VEC));
+    // park chunk c of a row (padding of the last chunk: bf16 -inf)
+    auto park = [&](int c, uint4 w) {
+        if (c == NCH - 1) {
+            const bool ok = ((c * THREADS + tid) * VEC) < V;
+            const uint32_t mk = lane_mask(ok), fb = 0xFF80FF80u & ~mk;
+            w = make_uint4((w.x & mk) | fb, (w.y & mk) | fb, (w.z & mk) | fb, (w.w & mk) | fb);
         }
+        slots[c * THREADS + tid] = w;
     };
     uint4 nxt[NCH];
-    if (row0 < row1) load_row(row0, nxt);
-    for (int i = row0; i < row1; ++i) {
-        const uint16_t* zr = Z + (int64_t)i * ldz;
-        // park the row (padding of the last chunk: bf16 -inf), then prefetch row i+1 into the
-        // registers it came from (the last row reloads itself)
+    if (nr > 0) {
+        const auto d0 = row_desc(row_of(0));
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            uint4 u = nxt[c];
-            if (c == NCH - 1) {
-                const bool ok = ((c * THREADS + tid) * VEC) < V;
-                const uint32_t mk = lane_mask(ok), fb = 0xFF80FF80u & ~mk;
-                u = make_uint4((u.x & mk) | fb, (u.y & mk) | fb, (u.z & mk) | fb, (u.w & mk) | fb);
-            }
-            slots[c * THREADS + tid] = u;
+        for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(d0, c);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) park(c, nxt[c]);
+        if (nr > 1) {
+            const auto d1 = row_desc(row_of(1));
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(d1, c);
         }
-        load_row(min(i + 1, row1 - 1), nxt);
-        // pass 1 (LDS): online (max, sum, argmax) over this thread's chunks, in column order
+    }
+    if (tid < 2) sh_am[tid] = INT_MAX;   // first used after the first barrier
+    // tid 0 finishes a row's argmax, target logit and loss term after the next row's barrier
+    auto finish_row = [&](int i, int b, float lse, bool valid) {
+        if (row_argmax) row_argmax[i] = sh_am[b];
+        sh_am[b] = INT_MAX;   // reused two rows later, after a barrier this thread has yet to reach
+        const float zt = valid ? sh_zt[b] : 0.f;
+        if (row_target) row_target[i] = zt;
+        if (valid) {
+            ++cnt;
+            ce += (double)lse - (double)zt;
+        }
+    };
+    float prev_lse = 0.f;
+    bool prev_valid = false;
+    for (int j = 0; j < nr; ++j) {
+        const int i = row_of(j);
+        const int b = j & 1;
+        // pass 1 (LDS): online (max, sum) over this thread's chunks, in column order, with the
+        // first chunk that reached the thread's maximum; the next chunk is read ahead
         float m = -INFINITY, l = 0.f;
-        int idx = INT_MAX;
+        int cmax = 0;
+        uint4 u_next = slots[tid];
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
+            const uint4 u = u_next;
+            if (c + 1 < NCH) u_next = slots[(c + 1) * THREADS + tid];
             float x[VEC];
-            unpack(slots[c * THREADS + tid], x);
-            float cm = x[0];
-#pragma unroll
-            for (int k = 1; k < VEC; ++k) cm = fmaxf(cm, x[k]);
-            int ci = INT_MAX;
-#pragma unroll
-            for (int k = VEC - 1; k >= 0; --k)
-                if (x[k] == cm) ci = (c * THREADS + tid) * VEC + k;
-            const float mn = fmaxf(m, cm);
+            unpack(u, x);
+            // IEEE maximum (no canonicalising moves of the unpacked bit patterns)
+            auto mx = [](float a, float b2) { return __builtin_elementwise_maximum(a, b2); };
+            const float cm = mx(mx(mx(x[0], x[1]), mx(x[2], x[3])), mx(mx(x[4], x[5]), mx(x[6], x[7])));
+            const float mn = mx(m, cm);
             // a padding-only chunk after real ones leaves (m, l) unchanged (mn == m, terms zero);
             // chunk 0 of every thread lies inside the row, so mn is finite
             const float mn2 = mn * kLog2e;
-            float cl = 0.f;
+            float e[VEC];
 #pragma unroll
-            for (int k = 0; k < VEC; ++k) cl += exp2_fast(fmaf(x[k], kLog2e, -mn2));
-            l = (c == 0 ? 0.f : l * exp2_fast((m - mn) * kLog2e)) + cl;
-            if (cm > m) idx = ci;
+            for (int k = 0; k < VEC; ++k) e[k] = exp2_fast(fmaf(x[k], kLog2e, -mn2));
+            const float cl = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+            l = (c == 0 ? cl : fmaf(l, exp2_fast((m - mn) * kLog2e), cl));
+            if (c > 0 && cm > m) cmax = c;
             m = mn;
         }
+        const float m_thread = m;
+        // wave: the maximum, then the lanes' sums rescaled to it
+        float mw = m;
 #pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) {
-            const float mo = __shfl_xor(m, o, kWave);
-            const float lo = __shfl_xor(l, o, kWave);
-            const int io = __shfl_xor(idx, o, kWave);
-            merge(m, l, idx, mo, lo, io);
-        }
+        for (int o = kWave / 2; o > 0; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o, kWave));
+        float lw = l * exp2_fast((m - mw) * kLog2e);
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) lw += __shfl_xor(lw, o, kWave);
         if ((tid & (kWave - 1)) == 0) {
-            sh_m[tid / kWave] = m;
-            sh_l[tid / kWave] = l;
-            sh_i[tid / kWave] = idx;
+            sh_m[b][tid / kWave] = mw;
+            sh_l[b][tid / kWave] = lw;
         }
         __syncthreads();
-        m = sh_m[0];
-        l = sh_l[0];
-        idx = sh_i[0];
+        if (tid == 0 && j > 0) finish_row(row_of(j - 1), b ^ 1, prev_lse, prev_valid);
+        // workgroup: the same over the NW wave pairs, lane w of every wave holding pair w; lane 0's
+        // result is broadcast
+        {
+            const int lane = tid & (kWave - 1);
+            const float mg = lane < NW ? sh_m[b][lane] : -INFINITY;
+            float mm = mg;
 #pragma unroll
-        for (int w = 1; w < NW; ++w) merge(m, l, idx, sh_m[w], sh_l[w], sh_i[w]);
+            for (int o = NW / 2; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o, kWave));
+            float lg = lane < NW ? sh_l[b][lane] * exp2_fast((mg - mm) * kLog2e) : 0.f;
+#pragma unroll
+            for (int o = NW / 2; o > 0; o >>= 1) lg += __shfl_xor(lg, o, kWave);
+            m = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(mm)));
+            l = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lg)));
+        }
+        // argmax: the first column holding the row maximum lies in the first chunk where some
+        // thread holding that maximum reached it; those threads search that chunk
+        if (m_thread == m) {
+            float x[VEC];
+            unpack(slots[cmax * THREADS + tid], x);
+            int k0 = VEC - 1;
+#pragma unroll
+            for (int k = VEC - 2; k >= 0; --k) k0 = (x[k] == m) ? k : k0;
+            atomicMin(&sh_am[b], (cmax * THREADS + tid) * VEC + k0);
+        }
         const float lse = m + logf(l);
-        const int am = idx;
         const int y = labels[i];
         bool rbad = false;
         const bool valid = label_valid(y, V, ignore_index, &rbad);
         bad |= rbad;
-        uint16_t* rr = R ? R + (int64_t)i * ldr : nullptr;
-        // pass 2 (LDS): p = exp(z - lse), residual, column accumulation, R
+        // R row stores go through a buffer descriptor (no R: an empty range, every store dropped)
+        const auto rdesc = make_desc(R ? R + (int64_t)i * ldr : nullptr, R ? V * 2 : 0);
+        const bool has_next = j + 1 < nr, has_next2 = j + 2 < nr;
+        const auto dn = row_desc(has_next2 ? row_of(j + 2) : i);
+        // pass 2 (LDS): p = exp(z - lse), residual, column accumulation, R; the label's owner
+        // also publishes the target logit
         const int yv = y / VEC;
         const int slot = (valid && yv % THREADS == tid) ? (yv / THREADS) * VEC + (y % VEC) : -1;
         const float lse2 = lse * kLog2e;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            const int col = (c * THREADS + tid) * VEC;
             float p[VEC];
             if (valid) {
                 float x[VEC];
@@ -402,7 +449,10 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
                 if (slot >= 0) {
 #pragma unroll
                     for (int k = 0; k < VEC; ++k)
-                        if (c * VEC + k == slot) p[k] -= 1.0f;
+                        if (c * VEC + k == slot) {
+                            p[k] -= 1.0f;
+                            sh_zt[b] = x[k];
+                        }
                 }
 #pragma unroll
                 for (int k = 0; k < VEC; ++k) acc[c * VEC + k] += p[k];
@@ -410,20 +460,30 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
 #pragma unroll
                 for (int k = 0; k < VEC; ++k) p[k] = 0.f;
             }
-            if (rr && (c < NCH - 1 || col < V)) VecIO<uint16_t, VEC>::store(rr + col, p);
+            u32x4_t w;
+            w[0] = pack_bf16x2(p[0], p[1]);
+            w[1] = pack_bf16x2(p[2], p[3]);
+            w[2] = pack_bf16x2(p[4], p[5]);
+            w[3] = pack_bf16x2(p[6], p[7]);
+            if (c < NCH - 1) __builtin_amdgcn_raw_buffer_store_b128(w, rdesc, voff, c * THREADS * 16, 0);
+            else __builtin_amdgcn_raw_buffer_store_b128(w, rdesc, voff_last, 0, 0);
         }
-        if (tid == 0) {
-            row_lse[i] = lse;
-            if (row_argmax) row_argmax[i] = am;
-            const float zt = valid ? bf16_to_f32(zr[y]) : 0.f;
-            if (row_target) row_target[i] = zt;
-            if (valid) {
-                ++cnt;
-                ce += (double)lse - (double)zt;
+        if (tid == 0) row_lse[i] = lse;
+        // park the next row (its loads were issued before this row's stores, so waiting for them
+        // does not wait for the stores) and load the one after into the freed registers
+        if (has_next) {
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) park(c, nxt[c]);
+            if (has_next2) {
+#pragma unroll
+                for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(dn, c);
             }
         }
-        __syncthreads();   // the reduction slots are rewritten by the next row
+        prev_lse = lse;
+        prev_valid = valid;
     }
+    __syncthreads();
+    if (tid == 0 && nr > 0) finish_row(row_of(nr - 1), (nr - 1) & 1, prev_lse, prev_valid);
     float* prow = ws.part + (int64_t)blockIdx.x * V;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) store_f32_chunk<VEC>(prow, (c * THREADS + tid) * VEC, V, &acc[c * VEC]);
@@ -688,6 +748,7 @@ hipError_t launch_rows(const T* Z, int64_t ldz, int N, int V, const int32_t* lab
 // Allowed chunk counts for 512-thread single-pass workgroups (registers: 2 * NCH * VEC floats).
 constexpr int kNchSet[] = {1, 2, 3, 4, 6, 8, 10, 13};
 constexpr int kLdsNchSet[] = {2, 3, 4, 6, 8, 10, 12, 13, 14};
+constexpr int kLds1kNchSet[] = {2, 3, 4, 5, 6};
 
 template <typename T, int VEC>
 hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, int V, const int32_t* labels,
@@ -723,6 +784,18 @@ hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, i
             }
 #undef BOM_LDS
         }
+        if (threads == -1024) {   // the same with 1024-thread workgroups (16 waves per CU)
+#define BOM_LDS(NC) launch_rows_lds<1024, NC>(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, nwg, st)
+            switch (nch) {
+                case 2: return BOM_LDS(2);
+                case 3: return BOM_LDS(3);
+                case 4: return BOM_LDS(4);
+                case 5: return BOM_LDS(5);
+                case 6: return BOM_LDS(6);
+                default: return hipErrorInvalidValue;
+            }
+#undef BOM_LDS
+        }
     }
     switch (nch) {
         case 1: return BOM_ROWS(512, 1);
@@ -739,7 +812,8 @@ hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, i
 }
 
 // Variant override for A/B measurement (environment BOM_RESIDUAL_PLAN, read once):
-// 0 automatic, 1 = 512-thread register rows, 2 = 1024-thread register rows, 3 = two pass.
+// 0 automatic, 1 = 512-thread register rows, 2 = 1024-thread register rows, 3 = two pass,
+// 4 = 1024-thread LDS rows where they fit, 5 = 512-thread LDS rows.
 int plan_override() {
     static const int v = [] {
         const char* e = getenv("BOM_RESIDUAL_PLAN");
@@ -764,10 +838,21 @@ bool plan_single(int V, int VEC, int* threads, int* nch) {
         return true;
     }
     const int need1k = (slots + 1023) / 1024;
-    // automatic: bf16 rows wider than 512 chunks are parked in LDS by 512-thread workgroups, which
-    // prefetch the next row into registers (threads = -512 marks that kernel); fp32 rows use
-    // 512-thread register rows up to 8 chunks, then 1024-thread register rows
-    if (VEC == 8 && ov == 0 && need >= 2) {
+    // automatic: bf16 rows of 2..6 chunks per thread at 1024 threads are parked in LDS by
+    // 1024-thread workgroups (16 waves per CU hide more latency), wider ones by 512-thread
+    // workgroups (up to 14 chunks); both prefetch the next row into registers (threads = -1024 or
+    // -512 mark those kernels); fp32 rows use 512-thread register rows up to 8 chunks, then
+    // 1024-thread register rows
+    if (VEC == 8 && (ov == 4 || ov == 0) && need1k >= 2 && need1k <= 6) {
+        for (int c : kLds1kNchSet) {
+            if (c >= need1k) {
+                *threads = -1024;
+                *nch = c;
+                return true;
+            }
+        }
+    }
+    if (VEC == 8 && (ov == 0 || ov == 5) && need >= 2) {
         for (int c : kLdsNchSet) {
             if (c >= need) {
                 *threads = -512;

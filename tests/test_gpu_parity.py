@@ -32,6 +32,7 @@ RESIDUAL_CASES = [
     ("bf16_v32000", 96, 32000, "bf16", "zipf", 0.05, 2, 0.55),
     ("bf16_v12000_multirow", 600, 12000, "bf16", "zipf", 0.05, 3, 0.55),
     ("bf16_v50304_packed", 64, 50304, "bf16", "zipf", 0.05, 2, 0.91),
+    ("bf16_v50304_multirow", 600, 50304, "bf16", "zipf", 0.05, 3, 0.91),
     ("bf16_v70000_twopass", 40, 70000, "bf16", "zipf", 0.05, 2, 1.28),
     ("f32_v70003_twopass_scalar", 40, 70003, "f32", "zipf", 0.05, 2, 1.28),
     ("bf16_v4_n1", 1, 8, "bf16", "uniform", 0.0, 0, 1.0),
@@ -71,6 +72,37 @@ def _compare_residual(name, Zh, y, out, orc, dtype):
     P = Ro + lab
     rtol = 2.0 ** -8 + 1e-5 if dtype == "bf16" else 1e-5
     assert (np.abs(R - Ro) <= rtol * np.abs(Ro) + 1e-5 * P + 1e-30).all(), f"{name}: R values"
+
+
+@pytest.mark.parametrize("V", [1000, 12000, 32000, 50304])
+def test_residual_argmax_ties(V):
+    """Ties at the row maximum: the argmax is the first column holding it (a plain first-index
+    argmax), whichever thread, chunk or wave the tied columns fall in; all-equal rows give 0."""
+    N = 300
+    log(f"[residual] argmax ties N={N} V={V}")
+    Zh, _ = gen_matrix(N, V, synth.STREAM_Z, 0.55, "bf16")
+    Zh = Zh.copy()
+    rng = np.random.default_rng(1234 + V)
+    for i in range(N):
+        kind = i % 4
+        if kind == 0:
+            Zh[i, :] = 0.5                       # every column ties
+        elif kind == 1:
+            cols = rng.choice(V, size=3, replace=False)
+            Zh[i, cols] = 8.0                    # three tied maxima anywhere in the row
+        elif kind == 2:
+            c0 = int(rng.integers(0, V - 8))
+            Zh[i, c0] = Zh[i, c0 + 7] = 8.0      # tied maxima inside one 16-byte chunk
+        else:
+            Zh[i, V - 1] = Zh[i, V - 2] = 8.0    # tied maxima in the last chunk
+    bits = (Zh.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    assert (synth.bf16_to_f32(bits).reshape(N, V) == Zh).all()
+    Zd = bf16_tensor(bits, (N, V))
+    y = gen_labels(N, V, "uniform")
+    out = _run_residual(Zd, torch.from_numpy(y).to(dev()))
+    am = out["row_argmax"].cpu().numpy()
+    assert (am == np.argmax(Zh, axis=1)).all()
+    assert (am[0::4] == 0).all()
 
 
 @pytest.mark.parametrize("case", RESIDUAL_CASES, ids=[c[0] for c in RESIDUAL_CASES])

@@ -89,7 +89,10 @@ typedef enum { BOM_F32 = 0, BOM_BF16 = 1 } bom_dtype;
  *   R         device [N, ldr] of r_dt, may be NULL (then R is not written). r_dt must equal
  *             z_dt. ldr >= V.
  *   loss      device fp32 [1].  n_valid device int32 [1].  flags device int32 [1].
- *   workspace device, at least bom_residual_workspace_bytes(N, V, z_dt) bytes, 256-byte aligned.
+ *   workspace device, at least bom_residual_workspace_bytes(N, V, z_dt) bytes, 256-byte aligned;
+ *             contents on entry are ignored. It holds per-workgroup partial sums and, for rows
+ *             too wide for one workgroup, the records the workgroups sharing a row exchange, so
+ *             calls that may run at the same time must not share it.
  * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE (N < 1, V < 2, ld < V, N or V >= 2^31), BOM_ERR_DTYPE,
  *         BOM_ERR_WORKSPACE, BOM_ERR_HIP.
  * ---------------------------------------------------------------------------------------- */

@@ -27,6 +27,8 @@ constexpr int kStatsRowsPerWG = 4;    // two pass, stats: one wave per row, 4 wa
 constexpr int kColsThreads = 256;     // two pass, columns: threads per workgroup
 constexpr int kColsCPT = 8;           // two pass, columns: chunks per thread
 constexpr int kColsMaxRowBlock = 256; // two pass, columns: at most this many rows per partial-sum block
+constexpr int kSplitMaxParts = 8;     // split rows: at most this many workgroups share a row
+constexpr int kSplitMaxNch = 5;       // split rows: 1024 threads x 5 chunks x 8 = 40960 columns per part
 
 // Rows per column-kernel workgroup: enough workgroups (about 1024) to fill the chip.
 int cols_row_block(int64_t N, int64_t V, int vec) {
@@ -43,10 +45,11 @@ struct Partials {
     int* wg_count;    // [nwg] valid rows
     int* wg_flags;    // [nwg] BOM_FLAG_LABEL_RANGE bits
     double* wg_loss;  // [nwg] sum of per-row cross-entropy
+    unsigned long long* xch;  // [N][kSplitMaxParts][3] split rows: per-part (max, sum, argmax) records
 };
 
 struct WsLayout {
-    size_t part_off, count_off, flags_off, loss_off, total;
+    size_t part_off, count_off, flags_off, loss_off, xch_off, total;
 };
 
 WsLayout ws_layout(int64_t N, int64_t V) {
@@ -58,12 +61,14 @@ WsLayout ws_layout(int64_t N, int64_t V) {
     int64_t nrb = (N + rb - 1) / rb;
     int64_t nparts = nwg1 > nrb ? nwg1 : nrb;
     int64_t nwg = nwg1 > nstats ? nwg1 : nstats;
+    if (nwg < kSingleMaxWG) nwg = kSingleMaxWG;   // split rows: up to kSingleMaxWG workgroups at any N
     WsLayout L;
     L.part_off = 0;
     L.count_off = align256(L.part_off + (size_t)nparts * (size_t)V * sizeof(float));
     L.flags_off = align256(L.count_off + (size_t)nwg * sizeof(int));
     L.loss_off = align256(L.flags_off + (size_t)nwg * sizeof(int));
-    L.total = align256(L.loss_off + (size_t)nwg * sizeof(double));
+    L.xch_off = align256(L.loss_off + (size_t)nwg * sizeof(double));
+    L.total = align256(L.xch_off + (size_t)N * kSplitMaxParts * 3 * sizeof(unsigned long long));
     return L;
 }
 
@@ -310,20 +315,19 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
         x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z); x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
     };
     // Row loads and R stores go through per-row buffer descriptors: chunk c of this thread sits at
-    // byte tid*16 + c*THREADS*16. Only the last chunk can fall outside the row; it carries its whole
-    // offset in the range-checked vector offset (loads there return zeros, stores are dropped), the
-    // other chunks add theirs as a scalar offset, so two vector registers address every chunk.
+    // byte tid*16 + c*THREADS*16, all of it in the range-checked vector offset, so chunks past the
+    // row's end load zeros (replaced by -inf when parked) and their stores are dropped.
     const int voff = tid * 16;
-    const int voff_last = ((NCH - 1) * THREADS + tid) * 16;
+    // the first chunk index of this wave's lanes whose chunks may lie past the row's end
+    const int wave_last = (tid | (kWave - 1));
     auto row_desc = [&](int i) { return make_desc(Z + (int64_t)i * ldz, V * 2); };
     auto load_chunk = [&](const __amdgpu_buffer_rsrc_t& d, int c) {
-        const u32x4_t w = c < NCH - 1 ? __builtin_amdgcn_raw_buffer_load_b128(d, voff, c * THREADS * 16, 0)
-                                      : __builtin_amdgcn_raw_buffer_load_b128(d, voff_last, 0, 0);
+        const u32x4_t w = __builtin_amdgcn_raw_buffer_load_b128(d, voff + c * THREADS * 16, 0, 0);
         return make_uint4(w[0], w[1], w[2], w[3]);
     };
-    // park chunk c of a row (padding of the last chunk: bf16 -inf)
+    // park chunk c of a row (chunks past the row's end: bf16 -inf)
     auto park = [&](int c, uint4 w) {
-        if (c == NCH - 1) {
+        if ((c * THREADS + wave_last) * VEC >= V) {   // uniform per wave
             const bool ok = ((c * THREADS + tid) * VEC) < V;
             const uint32_t mk = lane_mask(ok), fb = 0xFF80FF80u & ~mk;
             w = make_uint4((w.x & mk) | fb, (w.y & mk) | fb, (w.z & mk) | fb, (w.w & mk) | fb);
@@ -465,8 +469,7 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
             w[1] = pack_bf16x2(p[2], p[3]);
             w[2] = pack_bf16x2(p[4], p[5]);
             w[3] = pack_bf16x2(p[6], p[7]);
-            if (c < NCH - 1) __builtin_amdgcn_raw_buffer_store_b128(w, rdesc, voff, c * THREADS * 16, 0);
-            else __builtin_amdgcn_raw_buffer_store_b128(w, rdesc, voff_last, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(w, rdesc, voff + c * THREADS * 16, 0, 0);
         }
         if (tid == 0) row_lse[i] = lse;
         // park the next row (its loads were issued before this row's stores, so waiting for them
@@ -492,6 +495,311 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
         ws.wg_loss[blockIdx.x] = ce;
         ws.wg_flags[blockIdx.x] = bad ? BOM_FLAG_LABEL_RANGE : 0;
     }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Single pass, rows too wide for one workgroup (bf16): S workgroups share each row, part q owning
+// columns [q W, min(V, (q + 1) W)), and together stream Z once. Each part parks its slice in LDS
+// like residual_rows_lds_kernel, reduces its (max, sum of exp(z - max), first argmax) and publishes
+// them as three 64-bit words (validity marker in the high half, value in the low half; the area is
+// zeroed before the launch) with relaxed device-scope atomic stores; thread 0 then polls the other
+// parts' words with relaxed device-scope atomic loads and combines all S records in part order, so
+// every part derives the same lse. A poll is bounded: after spin_limit polls (or at once when
+// spin_limit < 0) thread 0 computes the missing part's record from Z itself and stops waiting for
+// that part, so the kernel finishes whatever the scheduling. The part holding a row's label (part 0
+// for ignored rows) writes that row's outputs and loss term. Workgroup (g, q) writes columns of
+// partial row g; the S parts of group g together fill it.
+template <int THREADS, int NCH>
+__global__ __launch_bounds__(THREADS) void residual_split_kernel(
+    const uint16_t* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
+    float* __restrict__ row_lse, int32_t* __restrict__ row_argmax, float* __restrict__ row_target,
+    uint16_t* __restrict__ R, int64_t ldr, int S, int W, int spin_limit, Partials ws) {
+    constexpr int VEC = 8;
+    constexpr int NW = THREADS / kWave;
+    constexpr int VPT = NCH * VEC;
+    __shared__ uint4 slots[NCH * THREADS];
+    __shared__ float sh_m[2][NW];
+    __shared__ float sh_l[2][NW];
+    __shared__ int sh_am;
+    __shared__ float sh_zt[2];
+    __shared__ float sh_row[3];   // combined max, sum and (as bits) argmax of the current row
+    const int tid = threadIdx.x;
+    const int part = blockIdx.x % S, g = blockIdx.x / S, G = gridDim.x / S;
+    const int c0 = part * W;
+    const int Vp = min(W, V - c0);
+    float acc[VPT];
+#pragma unroll
+    for (int k = 0; k < VPT; ++k) acc[k] = 0.f;
+    const int nr = g < N ? (N - 1 - g) / G + 1 : 0;
+    auto row_of = [&](int j) { return g + j * G; };
+    int cnt = 0;
+    double ce = 0.0;
+    bool bad = false;
+    bool dead = false;   // wave 0, lane q: part q is no longer waited for
+    auto unpack = [](const uint4& u, float* x) {
+        x[0] = bf16_lo(u.x); x[1] = bf16_hi(u.x); x[2] = bf16_lo(u.y); x[3] = bf16_hi(u.y);
+        x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z); x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
+    };
+    const int voff = tid * 16;
+    // the first chunk index of this wave's lanes whose chunks may lie past the row's end
+    const int wave_last = (tid | (kWave - 1));
+    auto row_desc = [&](int i) { return make_desc(Z + (int64_t)i * ldz + c0, Vp * 2); };
+    auto load_chunk = [&](const __amdgpu_buffer_rsrc_t& d, int c) {
+        const u32x4_t w = __builtin_amdgcn_raw_buffer_load_b128(d, voff + c * THREADS * 16, 0, 0);
+        return make_uint4(w[0], w[1], w[2], w[3]);
+    };
+    auto park = [&](int c, uint4 w) {
+        if ((c * THREADS + wave_last) * VEC >= Vp) {   // uniform per wave
+            const bool ok = ((c * THREADS + tid) * VEC) < Vp;
+            const uint32_t mk = lane_mask(ok), fb = 0xFF80FF80u & ~mk;
+            w = make_uint4((w.x & mk) | fb, (w.y & mk) | fb, (w.z & mk) | fb, (w.w & mk) | fb);
+        }
+        slots[c * THREADS + tid] = w;
+    };
+    uint4 nxt[NCH];
+    if (nr > 0) {
+        const auto d0 = row_desc(row_of(0));
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(d0, c);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) park(c, nxt[c]);
+        if (nr > 1) {
+            const auto d1 = row_desc(row_of(1));
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(d1, c);
+        }
+    }
+    if (tid == 0) sh_am = INT_MAX;
+    constexpr unsigned long long kValid = 1ull << 32;
+    auto xword = [&](int i, int q, int f) { return ws.xch + ((int64_t)i * kSplitMaxParts + q) * 3 + f; };
+    // wave 0, lane q: part q's record of row i, from its words or, failing that, from Z
+    auto fetch = [&](int i, int q, float* mq, float* lq, int* aq) {
+        if (!dead) {
+            unsigned long long v[3];
+            bool ok = true;
+            for (int f = 0; f < 3 && ok; ++f) {
+                ok = false;
+                for (int it = 0; spin_limit >= 0 && it <= spin_limit; ++it) {
+                    v[f] = __hip_atomic_load(xword(i, q, f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if ((v[f] >> 32) == 1) {
+                        ok = true;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(2);
+                }
+            }
+            if (ok) {
+                *mq = __uint_as_float((uint32_t)v[0]);
+                *lq = __uint_as_float((uint32_t)v[1]);
+                *aq = (int)(uint32_t)v[2];
+                return;
+            }
+            dead = true;
+        }
+        const int q0 = q * W, q1 = min(V, q0 + W);
+        const uint16_t* zr = Z + (int64_t)i * ldz;
+        float m = -INFINITY, l = 0.f;
+        int a = q0;
+        for (int col = q0; col < q1; ++col) {
+            const float x = bf16_to_f32(zr[col]);
+            if (x > m) {
+                l = (m == -INFINITY) ? 0.f : l * exp2_fast((m - x) * kLog2e);
+                m = x;
+                a = col;
+            }
+            l += exp2_fast((x - m) * kLog2e);
+        }
+        *mq = m;
+        *lq = l;
+        *aq = a;
+    };
+    auto finish_row = [&](int i, int b, float lse, bool valid, int am) {
+        if (row_argmax) row_argmax[i] = am;
+        const float zt = valid ? sh_zt[b] : 0.f;
+        if (row_target) row_target[i] = zt;
+        row_lse[i] = lse;
+        if (valid) {
+            ++cnt;
+            ce += (double)lse - (double)zt;
+        }
+    };
+    float prev_lse = 0.f;
+    bool prev_valid = false, prev_own = false;
+    int prev_am = 0;
+    for (int j = 0; j < nr; ++j) {
+        const int i = row_of(j);
+        const int b = j & 1;
+        // pass 1 (LDS): online (max, sum) of this part's slice, as in residual_rows_lds_kernel
+        float m = -INFINITY, l = 0.f;
+        int cmax = 0;
+        uint4 u_next = slots[tid];
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const uint4 u = u_next;
+            if (c + 1 < NCH) u_next = slots[(c + 1) * THREADS + tid];
+            float x[VEC];
+            unpack(u, x);
+            auto mx = [](float a, float b2) { return __builtin_elementwise_maximum(a, b2); };
+            const float cm = mx(mx(mx(x[0], x[1]), mx(x[2], x[3])), mx(mx(x[4], x[5]), mx(x[6], x[7])));
+            const float mn = mx(m, cm);
+            const float mn2 = mn * kLog2e;
+            float e[VEC];
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) e[k] = exp2_fast(fmaf(x[k], kLog2e, -mn2));
+            const float cl = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+            l = (c == 0 ? cl : fmaf(l, exp2_fast((m - mn) * kLog2e), cl));
+            if (c > 0 && cm > m) cmax = c;
+            m = mn;
+        }
+        const float m_thread = m;
+        float mw = m;
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o, kWave));
+        float lw = l * exp2_fast((m - mw) * kLog2e);
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) lw += __shfl_xor(lw, o, kWave);
+        if ((tid & (kWave - 1)) == 0) {
+            sh_m[b][tid / kWave] = mw;
+            sh_l[b][tid / kWave] = lw;
+        }
+        __syncthreads();
+        if (tid == 0 && j > 0 && prev_own) finish_row(row_of(j - 1), b ^ 1, prev_lse, prev_valid, prev_am);
+        float mp, lp;
+        {
+            const int lane = tid & (kWave - 1);
+            const float mg = lane < NW ? sh_m[b][lane] : -INFINITY;
+            float mm = mg;
+#pragma unroll
+            for (int o = NW / 2; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o, kWave));
+            float lg = lane < NW ? sh_l[b][lane] * exp2_fast((mg - mm) * kLog2e) : 0.f;
+#pragma unroll
+            for (int o = NW / 2; o > 0; o >>= 1) lg += __shfl_xor(lg, o, kWave);
+            mp = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(mm)));
+            lp = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lg)));
+        }
+        if (m_thread == mp) {
+            float x[VEC];
+            unpack(slots[cmax * THREADS + tid], x);
+            int k0 = VEC - 1;
+#pragma unroll
+            for (int k = VEC - 2; k >= 0; --k) k0 = (x[k] == mp) ? k : k0;
+            atomicMin(&sh_am, (cmax * THREADS + tid) * VEC + k0);
+        }
+        __syncthreads();
+        // wave 0: lane 0 publishes this part's record; lane q < S fetches part q's (all in
+        // parallel); lane 0 combines them in part order
+        if (tid < kWave) {
+            const int ap = c0 + sh_am;
+            if (tid == 0) {
+                sh_am = INT_MAX;   // next written after the next row's first barrier
+                __hip_atomic_store(xword(i, part, 0), kValid | __float_as_uint(mp), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(xword(i, part, 1), kValid | __float_as_uint(lp), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(xword(i, part, 2), kValid | (uint32_t)ap, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            }
+            float mq = mp, lq = lp;
+            int aq = ap;
+            if (tid < S && tid != part) fetch(i, tid, &mq, &lq, &aq);
+            // every part runs the same operations on the same values
+            float M = -INFINITY, L = 0.f;
+            int A = 0;
+            for (int q = 0; q < S; ++q) {
+                const float m2 = __shfl(mq, q, kWave), l2 = __shfl(lq, q, kWave);
+                const int a2 = __shfl(aq, q, kWave);
+                if (q == 0) {
+                    M = m2;
+                    L = l2;
+                    A = a2;
+                } else if (m2 > M) {
+                    L = fmaf(L, exp2_fast((M - m2) * kLog2e), l2);
+                    M = m2;
+                    A = a2;
+                } else {
+                    L = fmaf(l2, exp2_fast((m2 - M) * kLog2e), L);
+                }
+            }
+            if (tid == 0) {
+                sh_row[0] = M;
+                sh_row[1] = L;
+                sh_row[2] = __int_as_float(A);
+            }
+        }
+        __syncthreads();
+        const float M = sh_row[0], L = sh_row[1];
+        const int A = __float_as_int(sh_row[2]);
+        const float lse = M + logf(L);
+        const int y = labels[i];
+        bool rbad = false;
+        const bool valid = label_valid(y, V, ignore_index, &rbad);
+        const bool own = valid ? (y / W == part) : (part == 0);
+        if (own) bad |= rbad;
+        const auto rdesc = make_desc(R ? R + (int64_t)i * ldr + c0 : nullptr, R ? Vp * 2 : 0);
+        const bool has_next = j + 1 < nr, has_next2 = j + 2 < nr;
+        const auto dn = row_desc(has_next2 ? row_of(j + 2) : i);
+        const int yl = y - c0;
+        const bool here = valid && yl >= 0 && yl < Vp;
+        const int yv = yl / VEC;
+        const int slot = (here && yv % THREADS == tid) ? (yv / THREADS) * VEC + (yl % VEC) : -1;
+        const float lse2 = lse * kLog2e;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            float p[VEC];
+            if (valid) {
+                float x[VEC];
+                unpack(slots[c * THREADS + tid], x);
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) p[k] = exp2_fast(fmaf(x[k], kLog2e, -lse2));
+                if (slot >= 0) {
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k)
+                        if (c * VEC + k == slot) {
+                            p[k] -= 1.0f;
+                            sh_zt[b] = x[k];
+                        }
+                }
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) acc[c * VEC + k] += p[k];
+            } else {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) p[k] = 0.f;
+            }
+            u32x4_t w;
+            w[0] = pack_bf16x2(p[0], p[1]);
+            w[1] = pack_bf16x2(p[2], p[3]);
+            w[2] = pack_bf16x2(p[4], p[5]);
+            w[3] = pack_bf16x2(p[6], p[7]);
+            __builtin_amdgcn_raw_buffer_store_b128(w, rdesc, voff + c * THREADS * 16, 0, 0);
+        }
+        if (has_next) {
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) park(c, nxt[c]);
+            if (has_next2) {
+#pragma unroll
+                for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(dn, c);
+            }
+        }
+        prev_lse = lse;
+        prev_valid = valid;
+        prev_own = own;
+        prev_am = A;
+    }
+    __syncthreads();
+    if (tid == 0 && nr > 0 && prev_own) finish_row(row_of(nr - 1), (nr - 1) & 1, prev_lse, prev_valid, prev_am);
+    float* prow = ws.part + (int64_t)g * V + c0;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) store_f32_chunk<VEC>(prow, (c * THREADS + tid) * VEC, Vp, &acc[c * VEC]);
+    if (tid == 0) {
+        ws.wg_count[blockIdx.x] = cnt;
+        ws.wg_loss[blockIdx.x] = ce;
+        ws.wg_flags[blockIdx.x] = bad ? BOM_FLAG_LABEL_RANGE : 0;
+    }
+}
+
+__global__ void zero_u64_kernel(unsigned long long* __restrict__ p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0ull;
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -813,7 +1121,8 @@ hipError_t dispatch_rows(int nch, int threads, const T* Z, int64_t ldz, int N, i
 
 // Variant override for A/B measurement (environment BOM_RESIDUAL_PLAN, read once):
 // 0 automatic, 1 = 512-thread register rows, 2 = 1024-thread register rows, 3 = two pass,
-// 4 = 1024-thread LDS rows where they fit, 5 = 512-thread LDS rows.
+// 4 = 1024-thread LDS rows where they fit, 5 = 512-thread LDS rows, 6 = split rows (at least two
+// parts) for every bf16 row wider than one workgroup's 512 threads.
 int plan_override() {
     static const int v = [] {
         const char* e = getenv("BOM_RESIDUAL_PLAN");
@@ -827,7 +1136,7 @@ int plan_override() {
 // registers, 5..7 chunks (bf16 only) park the raw row in LDS.
 bool plan_single(int V, int VEC, int* threads, int* nch) {
     const int ov = plan_override();
-    if (ov == 3) return false;
+    if (ov == 3 || ov == 6) return false;
     const int slots = (V + VEC - 1) / VEC;
     int th = 64;
     while (th < slots && th < 512) th *= 2;
@@ -878,15 +1187,71 @@ bool plan_single(int V, int VEC, int* threads, int* nch) {
     return false;
 }
 
+// Split-row plan for bf16 rows of 16-byte chunks that no single workgroup holds: S parts of at most
+// kSplitMaxNch chunks per thread at 1024 threads, part width W columns (a multiple of 8).
+bool plan_split(int V, int* S, int* W, int* nch) {
+    const int slots = V / 8;
+    int parts = (slots + 1024 * kSplitMaxNch - 1) / (1024 * kSplitMaxNch);
+    if (plan_override() == 6 && parts < 2 && slots > 512) parts = 2;
+    if (parts < 2 || parts > kSplitMaxParts) return false;
+    const int per = (slots + parts - 1) / parts;
+    if ((parts - 1) * per >= slots) return false;   // every part holds columns
+    *S = parts;
+    *W = per * 8;
+    *nch = (per + 1023) / 1024 < 2 ? 2 : (per + 1023) / 1024;
+    return true;
+}
+
+// Poll bound of the split-row exchange (environment BOM_RESIDUAL_SPIN, read once; negative: never
+// wait, every workgroup computes the other parts' records itself).
+int split_spin_limit() {
+    static const int v = [] {
+        const char* e = getenv("BOM_RESIDUAL_SPIN");
+        return e ? atoi(e) : (1 << 16);
+    }();
+    return v;
+}
+
+hipError_t launch_split(const uint16_t* Z, int64_t ldz, int N, int V, const int32_t* labels, int32_t ig, float* lse,
+                        int32_t* am, float* tg, uint16_t* R, int64_t ldr, Partials ws, int S, int W, int nch, int* nwg,
+                        int* nparts, hipStream_t st) {
+    const int G = N < kSingleMaxWG / S ? N : kSingleMaxWG / S;
+    const int64_t nx = (int64_t)N * kSplitMaxParts * 3;
+    hipLaunchKernelGGL(zero_u64_kernel, dim3((unsigned)((nx + 255) / 256)), dim3(256), 0, st, ws.xch, nx);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int spin = split_spin_limit();
+#define BOM_SPLIT(NC)                                                                                              \
+    hipLaunchKernelGGL((residual_split_kernel<1024, NC>), dim3(S * G), dim3(1024), 0, st, Z, ldz, N, V, labels, ig, \
+                       lse, am, tg, R, ldr, S, W, spin, ws)
+    switch (nch) {
+        case 2: BOM_SPLIT(2); break;
+        case 3: BOM_SPLIT(3); break;
+        case 4: BOM_SPLIT(4); break;
+        case 5: BOM_SPLIT(5); break;
+        default: return hipErrorInvalidValue;
+    }
+#undef BOM_SPLIT
+    *nwg = S * G;
+    *nparts = G;
+    return hipGetLastError();
+}
+
 template <typename T, int VEC>
 hipError_t run_residual(const T* Z, int N, int V, int64_t ldz, const int32_t* labels, int32_t ig, float* s, float* lse,
                         int32_t* am, float* tg, T* R, int64_t ldr, float* loss, int32_t* n_valid, int32_t* flags,
                         Partials ws, hipStream_t st) {
     int threads = 0, nch = 0, nwg = 0, nparts = 0;
     hipError_t e;
+    int S = 0, W = 0;
+    bool split = false;
+    if constexpr (std::is_same<T, uint16_t>::value && VEC == 8) split = plan_split(V, &S, &W, &nch);
     if (plan_single(V, VEC, &threads, &nch)) {
         e = dispatch_rows<T, VEC>(nch, threads, Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, &nwg, st);
         nparts = nwg;
+    } else if (split) {
+        if constexpr (std::is_same<T, uint16_t>::value && VEC == 8)
+            e = launch_split(Z, ldz, N, V, labels, ig, lse, am, tg, R, ldr, ws, S, W, nch, &nwg, &nparts, st);
     } else {
         nwg = (N + kStatsRowsPerWG - 1) / kStatsRowsPerWG;
         constexpr int UNROLL = VEC == 1 ? 8 : 4;
@@ -919,7 +1284,8 @@ hipError_t launch_residual(const void* Z, bom_dtype dt, int N, int V, int64_t ld
     const WsLayout L = ws_layout(N, V);
     char* base = static_cast<char*>(wsp);
     Partials ws{reinterpret_cast<float*>(base + L.part_off), reinterpret_cast<int*>(base + L.count_off),
-                reinterpret_cast<int*>(base + L.flags_off), reinterpret_cast<double*>(base + L.loss_off)};
+                reinterpret_cast<int*>(base + L.flags_off), reinterpret_cast<double*>(base + L.loss_off),
+                reinterpret_cast<unsigned long long*>(base + L.xch_off)};
     const int vw = dt == BOM_BF16 ? 8 : 4;
     const bool vec_ok = (ldz % vw == 0) && (reinterpret_cast<uintptr_t>(Z) % 16 == 0) &&
                         (R == nullptr || ((ldr % vw == 0) && reinterpret_cast<uintptr_t>(R) % 16 == 0)) &&

@@ -33,7 +33,10 @@ RESIDUAL_CASES = [
     ("bf16_v12000_multirow", 600, 12000, "bf16", "zipf", 0.05, 3, 0.55),
     ("bf16_v50304_packed", 64, 50304, "bf16", "zipf", 0.05, 2, 0.91),
     ("bf16_v50304_multirow", 600, 50304, "bf16", "zipf", 0.05, 3, 0.91),
-    ("bf16_v70000_twopass", 40, 70000, "bf16", "zipf", 0.05, 2, 1.28),
+    ("bf16_v70000_split2", 40, 70000, "bf16", "zipf", 0.05, 2, 1.28),
+    ("bf16_v100008_split3", 24, 100008, "bf16", "zipf", 0.05, 2, 1.28),
+    ("bf16_v128256_split4", 20, 128256, "bf16", "zipf", 0.05, 2, 1.28),
+    ("bf16_v330000_twopass", 8, 330000, "bf16", "zipf", 0.0, 1, 1.28),
     ("f32_v70003_twopass_scalar", 40, 70003, "f32", "zipf", 0.05, 2, 1.28),
     ("bf16_v4_n1", 1, 8, "bf16", "uniform", 0.0, 0, 1.0),
 ]

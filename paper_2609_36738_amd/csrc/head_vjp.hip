@@ -1416,7 +1416,11 @@ GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K) {
     // large products: 256-tile rank-1 kernel; small ones (a few dozen 256 tiles or a short k) are
     // latency bound and run faster on the 128-tile kernel, which needs no rank-1 pre-pass
     const int64_t t256 = cdiv(M, LB) * cdiv(N, LB);
-    if (t256 >= 24 && K >= 8 * LK) return {kRank1, choose_splits(t256, M, N, K, LB, LK, 1)};
+    if (t256 >= 24 && K >= 8 * LK) {
+        GemmPlan g{kRank1, choose_splits(t256, M, N, K, LB, 2 * LK, 1)};
+        g.wide = 1;   // 64-deep k tiles: half the barriers of the 32-deep ring, measured 1-3% faster
+        return g;
+    }
     // 128 tiles: split k so that every workgroup loads its whole k range at once, when that takes
     // at most kMaxSplits splits
     const int64_t t128 = cdiv(M, MB) * cdiv(N, MB);
@@ -1427,7 +1431,8 @@ GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K) {
 
 // Plan override for A/B measurement (environment BOM_VJP_PLAN = "kind_w,splits_w,kind_h,splits_h",
 // read once; 0 keeps the automatic choice; kinds 1 = 128-tile MFMA, 2 = 256-tile MFMA with staged
-// fold, 3 = 256-tile MFMA with direct LDS copies and the rank-1 epilogue).
+// fold, 3 = 256-tile rank-1 kernel with 32-deep k tiles in four stages, 4 = the same with 64-deep k
+// tiles in two stages).
 struct PlanOverride {
     int kw = 0, sw = 0, kh = 0, sh = 0;
 };
@@ -1446,11 +1451,15 @@ void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int
     if (g.kind == kSimt) return;
     if (kind == kMfma128) g.kind = kMfma128;
     if (kind == kMfma256 && K >= 4 * TK) g.kind = kMfma256;
-    if (kind == kRank1) g.kind = kRank1;
+    if (kind == kRank1) {
+        g.kind = kRank1;
+        g.wide = 0;
+    }
     if (kind == 4) {
         g.kind = kRank1;
         g.wide = 1;
     }
+
     if (splits > 0) {
         const int ktile = g.kind == kMfma256 ? TK : (g.kind == kRank1 ? LK * (1 + g.wide) : MK);
         // every split keeps at least one k tile

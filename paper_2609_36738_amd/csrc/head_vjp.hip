@@ -1376,6 +1376,244 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 }
 
 // ---- planning ------------------------------------------------------------------------------------
+// ---- fused small products --------------------------------------------------------------------
+// Both products of a small head in one launch, each in its rank-1 form, with nothing staged
+// beforehand: workgroups [0, tw) own 64 x 64 tiles of dW = alpha H^T R + hsum cq^T, the rest
+// 64 x 64 tiles of dH = alpha R W^T + mask u^T (alpha = (1 - lambda)/N_t, cq = lambda q_hat/N_t,
+// hsum_m = sum over rows in I of H[k][m], u = W cq). Each workgroup runs over the whole k range
+// (no split-K, no partial sums): k tiles of 64 go through two LDS buffers, with four tiles in flight
+// in registers. The rank-1 vectors a tile needs come from the same copies on their way to LDS:
+// a dW tile sums its H columns over the rows in I, a dH tile dots its W rows with q_hat. dW's
+// operands are k-major in memory (rows k of H and R) and reach the MFMA through transposing LDS
+// reads; dH's are k-contiguous and use 16-byte reads. The dW tiles of the first row of tiles also
+// write db.
+constexpr int FB = 64;     // output tile
+constexpr int FK = 64;     // k tile
+constexpr int FSETS = 4;   // k tiles in flight in registers
+
+struct FusedArgs {
+    const uint16_t* H; int64_t ldh;
+    const uint16_t* W; int64_t ldw;
+    const uint16_t* R; int64_t ldr;
+    const int32_t* labels; int32_t ig;
+    const float* q_hat; const float* s; const int32_t* n_valid; float lambda;
+    int N, d, V;
+    float* dW; int64_t lddw; float beta;
+    void* dH; int64_t lddh; int dh_bf16;
+    float* db;
+    int tw_n, tw, th_n;   // dW tiles along V, dW tile count, dH tiles along d
+};
+
+// element offset of (row, col) in a 64 x 64 bf16 LDS tile whose 16-byte chunks are swizzled by row
+__device__ __forceinline__ int ftile_off(int row, int col) { return row * FB + ((((col >> 3) ^ (row & 7))) << 3) + (col & 7); }
+
+template <bool is_dw>
+__device__ __forceinline__ void fused_tile(const FusedArgs& a, int id, uint16_t (&sa)[2][FK * FB],
+                                           uint16_t (&sb)[2][FK * FB], float (&red)[FB][33], float (&vec)[FB]) {
+    const int t = threadIdx.x, l = t % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(t / kWave);
+    const int wm = wave / 2, wn = wave % 2;
+    const int m0 = (id / (is_dw ? a.tw_n : a.th_n)) * FB, n0 = (id % (is_dw ? a.tw_n : a.th_n)) * FB;
+    const int M = is_dw ? a.d : a.N, Nn = is_dw ? a.V : a.d, K = is_dw ? a.N : a.V;
+    const int nt = *a.n_valid;
+    const float alpha = nt > 0 ? (float)((1.0 - (double)a.lambda) / (double)nt) : 0.f;
+    const double cscale = nt > 0 ? (double)a.lambda / (double)nt : 0.0;
+    const int nk = ((K + FK - 1) / FK + FSETS - 1) / FSETS * FSETS;   // tiles past K hold zeros
+
+    // copy geometry: chunks t and t + 256 of each operand's 64 x 64 tile: tile row t/8 + 32 e,
+    // 16-byte chunk lc = t % 8 of that row
+    const int lc = t % 8;
+    const int r0 = t / 8;
+    // operand A: dW -> H rows k, columns m0 + 8 lc; dH -> R rows m0 + r, k chunk 8 lc
+    // operand B: dW -> R rows k, columns n0 + 8 lc; dH -> W rows n0 + r, k chunk 8 lc
+    const uint16_t* pa = is_dw ? a.H : a.R;
+    const uint16_t* pb = is_dw ? a.R : a.W;
+    const int64_t lda = is_dw ? a.ldh : a.ldr, ldb = is_dw ? a.ldr : a.ldw;
+    const int rows_a = is_dw ? a.N : a.N, rows_b = is_dw ? a.N : a.d;
+    const auto da = make_desc(pa, (int)(((int64_t)(rows_a - 1) * lda + (is_dw ? a.d : a.V)) * 2));
+    const auto db_ = make_desc(pb, (int)(((int64_t)(rows_b - 1) * ldb + a.V) * 2));
+    auto off_a = [&](int k0, int e) {
+        const int r = r0 + 32 * e;
+        if constexpr (is_dw) {
+            const int k = k0 + r, m = m0 + lc * 8;
+            return (k < a.N && m < a.d) ? (int)(((int64_t)k * lda + m) * 2) : kOob;
+        }
+        const int i = m0 + r, k = k0 + lc * 8;
+        return (i < a.N && k < a.V) ? (int)(((int64_t)i * lda + k) * 2) : kOob;
+    };
+    auto off_b = [&](int k0, int e) {
+        const int r = r0 + 32 * e;
+        if constexpr (is_dw) {
+            const int k = k0 + r, n = n0 + lc * 8;
+            return (k < a.N && n < a.V) ? (int)(((int64_t)k * ldb + n) * 2) : kOob;
+        }
+        const int j = n0 + r, k = k0 + lc * 8;
+        return (j < a.d && k < a.V) ? (int)(((int64_t)j * ldb + k) * 2) : kOob;
+    };
+    // one k tile in registers: the four 16-byte copies and what the rank-1 sums need with them
+    struct Set {
+        u32x4_t c[4];
+        int lab[2];     // dW: labels of the two H rows (rows past N: ignore_index)
+        float4 q[2];    // dH: q_hat over the chunk's 8 k
+    };
+    auto load_set = [&](Set& st, int kt) {
+        const int k0 = kt * FK;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            st.c[e] = __builtin_amdgcn_raw_buffer_load_b128(da, off_a(k0, e), 0, 0);
+            st.c[2 + e] = __builtin_amdgcn_raw_buffer_load_b128(db_, off_b(k0, e), 0, 0);
+        }
+        if constexpr (is_dw) {
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                const int k = k0 + r0 + 32 * e;
+                st.lab[e] = a.labels[k < a.N ? k : a.N - 1];
+                if (k >= a.N) st.lab[e] = a.ig;
+            }
+        } else {
+            const int k = k0 + lc * 8;
+            const int kc = k < a.V ? k : a.V - 8;
+            st.q[0] = *reinterpret_cast<const float4*>(a.q_hat + kc);
+            st.q[1] = *reinterpret_cast<const float4*>(a.q_hat + kc + 4);
+            if (k >= a.V) st.q[0] = st.q[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    };
+    float part[8];   // dW: sums of this thread's 8 H columns over rows in I; dH: [0..1] dots of its 2 W rows
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[e] = 0.f;
+    auto write_set = [&](const Set& st, int buf) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int r = r0 + 32 * e;
+            const int o = r * FB + ((lc ^ (r & 7)) << 3);
+            *reinterpret_cast<u32x4_t*>(&sa[buf][o]) = st.c[e];
+            *reinterpret_cast<u32x4_t*>(&sb[buf][o]) = st.c[2 + e];
+        }
+        if constexpr (is_dw) {
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                bool bad = false;
+                const float vm = label_valid(st.lab[e], a.V, a.ig, &bad) ? 1.f : 0.f;
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    part[2 * p] = fmaf(vm, bf16_lo(st.c[e][p]), part[2 * p]);
+                    part[2 * p + 1] = fmaf(vm, bf16_hi(st.c[e][p]), part[2 * p + 1]);
+                }
+            }
+        } else {
+            const float q8[8] = {st.q[0].x, st.q[0].y, st.q[0].z, st.q[0].w, st.q[1].x, st.q[1].y, st.q[1].z, st.q[1].w};
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                float acc = part[e];
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    acc = fmaf(bf16_lo(st.c[2 + e][p]), q8[2 * p], acc);
+                    acc = fmaf(bf16_hi(st.c[2 + e][p]), q8[2 * p + 1], acc);
+                }
+                part[e] = acc;
+            }
+        }
+    };
+    // fragments of MFMA step s (k = 16 s .. 16 s + 15) of the tile in buffer buf
+    auto read_frags = [&](int buf, int s, bf16x8_t& fa, bf16x8_t& fb) {
+        if constexpr (is_dw) {
+            const int g = l / 16, sl = l % 16;
+            const int kr = 16 * s + (g / 2) * 8 + sl / 4;
+            const int ca = wm * 32 + (g % 2) * 16 + (sl % 4) * 4, cb = wn * 32 + (g % 2) * 16 + (sl % 4) * 4;
+            const v4s_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)&sa[buf][ftile_off(kr, ca)]);
+            const v4s_t a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)&sa[buf][ftile_off(kr + 4, ca)]);
+            const v4s_t b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)&sb[buf][ftile_off(kr, cb)]);
+            const v4s_t b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)&sb[buf][ftile_off(kr + 4, cb)]);
+            fa = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+            fb = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7));
+        } else {
+            const int ra = wm * 32 + l % 32, rb = wn * 32 + l % 32, c = 2 * s + l / 32;
+            fa = *reinterpret_cast<const bf16x8_t*>(&sa[buf][ra * FB + ((c ^ (ra & 7)) << 3)]);
+            fb = *reinterpret_cast<const bf16x8_t*>(&sb[buf][rb * FB + ((c ^ (rb & 7)) << 3)]);
+        }
+    };
+
+    f32x16_t acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    Set sets[FSETS];
+#pragma unroll
+    for (int q = 0; q < FSETS; ++q) load_set(sets[q], q);
+    write_set(sets[0], 0);
+    load_set(sets[0], FSETS);
+    __syncthreads();
+    // iteration kt: read tile kt (buffer kt % 2), write tile kt + 1 into the other buffer from its
+    // register set and reload that set with tile kt + 1 + FSETS, then the four MFMA steps
+    for (int kt0 = 0; kt0 < nk; kt0 += FSETS) {
+#pragma unroll
+        for (int u = 0; u < FSETS; ++u) {
+            const int kt = kt0 + u;
+            const int buf = u & 1;
+            bf16x8_t fa[4], fb[4];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) read_frags(buf, s, fa[s], fb[s]);
+            Set& st = sets[(u + 1) % FSETS];
+            write_set(st, buf ^ 1);
+            load_set(st, kt + 1 + FSETS);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s], fb[s], acc, 0, 0, 0);
+            __syncthreads();
+        }
+    }
+
+    // rank-1 vectors of the tile: dW -> hsum over its 64 columns, dH -> u over its 64 rows of W
+    if (is_dw) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[lc * 8 + e][r0] = part[e];
+    } else {
+        red[r0][lc] = part[0];
+        red[r0 + 32][lc] = part[1];
+    }
+    __syncthreads();
+    if (t < FB) {
+        float v = 0.f;
+        const int nc = is_dw ? 32 : 8;
+        for (int c = 0; c < nc; ++c) v += red[t][c];
+        vec[t] = is_dw ? v : (float)(cscale * (double)v);
+    }
+    __syncthreads();
+    // accumulator element r of lane l: tile row wm*32 + (r/4)*8 + (l/32)*4 + r%4, column wn*32 + l%32
+    const int col = wn * 32 + l % 32;
+    const int n = n0 + col;
+    float cqn = 0.f;
+    if (is_dw && n < Nn) cqn = (float)(cscale * (double)a.q_hat[n]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int row = wm * 32 + (r / 4) * 8 + (l / 32) * 4 + r % 4;
+        const int m = m0 + row;
+        if (m >= M || n >= Nn) continue;
+        if (is_dw) {
+            float x = fmaf(alpha, acc[r], vec[row] * cqn);
+            float* p = a.dW + (int64_t)m * a.lddw + n;
+            *p = a.beta != 0.f ? x + a.beta * *p : x;
+        } else {
+            bool bad = false;
+            const float vm = label_valid(a.labels[m], a.V, a.ig, &bad) ? 1.f : 0.f;
+            const float x = fmaf(alpha, acc[r], vm * vec[col]);
+            if (a.dh_bf16) stf<uint16_t>(static_cast<uint16_t*>(a.dH), (int64_t)m * a.lddh + n, x);
+            else stf<float>(static_cast<float*>(a.dH), (int64_t)m * a.lddh + n, x);
+        }
+    }
+    if (is_dw && m0 == 0 && a.db != nullptr && t < FB && n0 + t < a.V) {
+        const int j = n0 + t;
+        a.db[j] = nt > 0 ? (1.0f - a.lambda) * a.s[j] + a.lambda * a.q_hat[j] : 0.f;
+    }
+}
+
+__global__ __launch_bounds__(256, 2) void vjp_fused_small_kernel(FusedArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t sa[2][FK * FB];
+    __shared__ __attribute__((aligned(16))) uint16_t sb[2][FK * FB];
+    __shared__ float red[FB][33];
+    __shared__ float vec[FB];
+    if ((int)blockIdx.x < a.tw) fused_tile<true>(a, (int)blockIdx.x, sa, sb, red, vec);
+    else fused_tile<false>(a, (int)blockIdx.x - a.tw, sa, sb, red, vec);
+}
+
 constexpr int kCUs = 256;        // MI355X compute units
 constexpr int kMaxSplits = 8;
 
@@ -1430,7 +1668,8 @@ GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K) {
 }
 
 // Plan override for A/B measurement (environment BOM_VJP_PLAN = "kind_w,splits_w,kind_h,splits_h",
-// read once; 0 keeps the automatic choice; kinds 1 = 128-tile MFMA, 2 = 256-tile MFMA with staged
+// read once; 0 keeps the automatic choice (small products: the fused launch); kinds 1 = 128-tile
+// MFMA (and no fused launch), 2 = 256-tile MFMA with staged
 // fold, 3 = 256-tile rank-1 kernel with 32-deep k tiles in four stages, 4 = the same with 64-deep k
 // tiles in two stages).
 struct PlanOverride {
@@ -1615,6 +1854,45 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
         p.h.kind = kSimt;
     }
     if (!a.dH) p.h.kind = kSimt;   // no dH: no rank-1 vector for it
+
+    // small products (both on the 128-tile kernel): one fused launch, nothing staged beforehand
+    const PlanOverride& ov = plan_override();
+    const bool fits31 = ((int64_t)(a.N - 1) * a.ldh + a.d) * 2 < (1LL << 31) &&
+                        ((int64_t)(a.N - 1) * a.ldr + a.V) * 2 < (1LL << 31) &&
+                        ((int64_t)(a.d - 1) * a.ldw + a.V) * 2 < (1LL << 31);
+    // (each tile runs over the whole k range, so both k extents stay short)
+    if (a.dt == BOM_BF16 && p.w.kind == kMfma128 && (!a.dH || p.h.kind == kMfma128) && fits31 && a.N <= 8192 &&
+        a.V <= 8192 && ov.kw != 1 && ov.kh != 1) {
+        FusedArgs fa;
+        fa.H = static_cast<const uint16_t*>(a.H);
+        fa.ldh = a.ldh;
+        fa.W = static_cast<const uint16_t*>(a.W);
+        fa.ldw = a.ldw;
+        fa.R = static_cast<const uint16_t*>(a.R);
+        fa.ldr = a.ldr;
+        fa.labels = a.labels;
+        fa.ig = a.ignore_index;
+        fa.q_hat = a.q_hat;
+        fa.s = a.s;
+        fa.n_valid = a.n_valid;
+        fa.lambda = a.lambda;
+        fa.N = a.N;
+        fa.d = a.d;
+        fa.V = a.V;
+        fa.dW = a.dW;
+        fa.lddw = a.lddw;
+        fa.beta = a.dW_beta;
+        fa.dH = a.dH;
+        fa.lddh = a.lddh;
+        fa.dh_bf16 = a.dh_dt == BOM_BF16;
+        fa.db = a.db;
+        fa.tw_n = (int)cdiv(a.V, FB);
+        fa.tw = (int)cdiv(a.d, FB) * fa.tw_n;
+        fa.th_n = (int)cdiv(a.d, FB);
+        const int th = a.dH ? (int)cdiv(a.N, FB) * fa.th_n : 0;
+        hipLaunchKernelGGL(vjp_fused_small_kernel, dim3((unsigned)(fa.tw + th)), dim3(256), 0, st, fa);
+        return hipGetLastError();
+    }
 
     // rank-1 vectors first: u for dH, row-block partial sums of H over I for dW
     hipError_t e;

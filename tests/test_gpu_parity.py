@@ -237,6 +237,34 @@ def test_head_vjp_tile256_lambda(lam):
     assert e_dw <= 2e-2 and e_dh <= 2e-2
 
 
+@pytest.mark.parametrize("lam,want_dH", [(0.0, True), (1.0, True), (0.25, False)])
+def test_head_vjp_small_fused_lambda(lam, want_dH):
+    """Small products (one fused launch) at the edges of the mixture, on ragged tiles (d = 136), with
+    and without dH; db checked too."""
+    N, d, V = 300, 136, 1000
+    log(f"[head_vjp] small fused lambda={lam} dH={want_dH}")
+    Hh, Hd, Wh, Wd, Zh, Zd, y, q_prev, t = _vjp_inputs(N, d, V, "bf16", 0.05)
+    yd = torch.from_numpy(y).to(dev())
+    res = bom.bom_residual(Zd, yd)
+    q = torch.from_numpy(q_prev.copy()).to(dev())
+    qh = bom.bom_ema(q, res["s"], B1, t)
+    g = bom.bom_head_vjp(Hd, Wd, res["R"], yd, qh, res["n_valid"], s=res["s"], lam=lam, want_db=True,
+                         want_dH=want_dH, dh_dtype=torch.float32)
+    torch.cuda.synchronize()
+    o = oracle.residual(Zh, y, want_R=False)
+    _, qho = oracle.ema(q_prev, o["s"], f32(B1), t)
+    dW = oracle.dW_cols(Hh, Zh, y, o["row_lse"], qho, o["n_valid"], f32(lam))
+    db = oracle.db(Zh, y, o["row_lse"], qho, o["n_valid"], f32(lam))
+    e_dw, e_db = rel_fro(to_f64(g["dW"]), dW), rel_fro(to_f64(g["db"]), db)
+    e_dh = 0.0
+    if want_dH:
+        e_dh = rel_fro(to_f64(g["dH"]), oracle.dH_rows(Wh, Zh, y, o["row_lse"], qho, o["n_valid"], f32(lam)))
+    else:
+        assert g.get("dH") is None
+    log(f"    rel err dW={e_dw:.3e} dH={e_dh:.3e} db={e_db:.3e}")
+    assert e_dw <= 2e-2 and e_dh <= 2e-2 and e_db <= 1e-5
+
+
 def test_head_vjp_tile256_empty_batch():
     log("[head_vjp] tile256 N_t = 0")
     N, d, V = 2048, 768, 4096

@@ -2,15 +2,18 @@
 // objective (Eq. (3)); its gradient (Eq. (4)) for the linear head z_i = W^T h_i (+ b) is
 //   G_ij = [i in I] ((1 - lambda) R_ij + lambda q_hat_j) / N_t      (gradient w.r.t. the logits)
 //   dW = H^T G,  dH = G W^T,  db = 1^T G = (1 - lambda) s + lambda q_hat  (bias Jacobian = I).
-// G is never stored: each GEMM forms its G tile while staging R into LDS,
-//   G = fma(alpha, R, mask_i * cq_j),  alpha = (1 - lambda) / N_t,  cq_j = lambda q_hat_j / N_t,
-// and rounds it to bf16 for the MFMA path.
+// G is never stored. The large products (and the fused launch for small ones) use its rank-1 split
+//   dW = alpha H^T R + hsum cq^T,  dH = alpha R W^T + mask u^T,
+//   alpha = (1 - lambda) / N_t,  cq_j = lambda q_hat_j / N_t,  hsum = sum over rows in I of H,  u = W cq,
+// multiplying R as stored; the 128-tile split-K kernels instead form G = fma(alpha, R, mask_i * cq_j)
+// while staging R into LDS and round it to bf16 for the MFMA.
 //
-// bf16 path: v_mfma_f32_32x32x16_bf16, 128 x 128 output tiles, 64-deep k tiles double-buffered in
-// LDS, four waves each owning a 64 x 64 quadrant; dW = H^T G has both operands k-outer in memory
-// and is transposed while staging (perm for H, the bf16 pack of the fold for G); dH = G W^T has
-// both operands k-contiguous. Split-K with a fixed-order reduction when the output has too few
-// tiles to fill the chip. fp32 path (and unaligned bf16): a SIMT tiled GEMM.
+// bf16 path: v_mfma_f32_32x32x16_bf16. Large products: 256 x 256 output tiles, four waves each owning
+// 128 x 128, k tiles of 64 in two LDS stages (lds256w_kernel). Small products: one fused launch of
+// 64 x 64 tiles of both products (vjp_fused_small_kernel), or 128 x 128 split-K tiles with a
+// fixed-order reduction. dW = H^T G has both operands k-outer in memory (transposing LDS reads or a
+// transpose while staging); dH = G W^T has both operands k-contiguous. fp32 path (and unaligned
+// bf16): a SIMT tiled GEMM.
 #include <cstdio>
 #include <cstdlib>
 #include <type_traits>
@@ -32,7 +35,7 @@ struct Fold {
 };
 
 struct VjpWs {
-    size_t cq_off, cqp_off, vmask_off, scal_off, ht_off, hpart_off, hsum_off, u_off, part_off, total;
+    size_t cq_off, cqp_off, vmask_off, scal_off, hpart_off, hsum_off, u_off, part_off, total;
 };
 
 // ---- prep -------------------------------------------------------------------------------------
@@ -486,167 +489,11 @@ __global__ __launch_bounds__(256) void mfma_dH_kernel(const uint16_t* __restrict
     }
 }
 
-// ---- MFMA bf16, large tiles ------------------------------------------------------------------------
-// 256 x 256 output tile, 4 waves each owning 128 x 128 (4 x 4 blocks of v_mfma_f32_32x32x16_bf16),
-// 64-deep k tiles double-buffered in LDS (2 x 2 x 32 KB). LDS rows are 64 bf16 (128 B, no padding);
-// the 16-byte chunk c of row r lives at chunk c ^ ((r ^ (r >> 3)) & 7), which measured free of bank
-// conflicts on gfx950 for the fragment reads and for both staging write patterns below.
-constexpr int TB = 256;
-constexpr int TK = 64;
-constexpr int TP = 64;
-
+// ---- MFMA bf16, 256 x 256 tiles: shared helpers ---------------------------------------------------
+// LDS rows of 64 bf16 (128 B, no padding): the 16-byte chunk c of row r lives at chunk
+// c ^ ((r ^ (r >> 3)) & 7), free of bank conflicts on gfx950 for 16-byte fragment reads and for the
+// 1 KB-per-wave staging writes.
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row ^ (row >> 3)) & 7); }
-
-typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
-__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c, false);
-}
-
-// k-contiguous operand: tile rows r0..r0+255 of X (k extent kend, a multiple of 8), k chunk
-// (t % 8) * 8 of rows e * 32 + t / 8, e < 8. FOLD (dH's A = G from R): G' = r_coef R + cqp_k in
-// fp32 by dot products, rounded to bf16 pairs, zeroed for rows outside I.
-template <bool FOLD>
-struct StageKC256 {
-    uint4 r[8];
-    uint32_t mk[8];               // per chunk: row in range (and, FOLD, in I) and k chunk in range
-    uint32_t rowok[FOLD ? 8 : 1]; // FOLD: row in range and in I (loop-invariant)
-    float4 cq4[FOLD ? 2 : 1];
-    const float* cqp_;
-    uint32_t one_lo_, one_hi_;
-    __device__ __forceinline__ void init_rows(int rows, int r0, const Fold& f) {
-        cqp_ = f.cqp;
-        one_lo_ = __float_as_uint(f.scal[2]);
-        one_hi_ = __float_as_uint(f.scal[3]);
-        if (FOLD) {
-            const int t = threadIdx.x;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int row = r0 + e * 32 + t / 8;
-                rowok[e] = row < rows && f.vmask[row < rows ? row : rows - 1] != 0.f;
-            }
-        }
-    }
-    __device__ __forceinline__ void load(const uint16_t* X, int64_t ldx, int rows, int r0, int k0, int kend) {
-        const int t = threadIdx.x;
-        const int k = k0 + (t % 8) * 8;
-        const bool kok = k < kend;
-        const int kc = kok ? k : kend - 8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int row = r0 + e * 32 + t / 8;
-            mk[e] = lane_mask(kok && (FOLD ? rowok[e] != 0u : row < rows));
-            r[e] = ld16(X + (int64_t)(row < rows ? row : rows - 1) * ldx + kc);
-        }
-        if (FOLD) {
-            cq4[0] = *reinterpret_cast<const float4*>(cqp_ + kc);
-            cq4[1] = *reinterpret_cast<const float4*>(cqp_ + kc + 4);
-        }
-    }
-    __device__ __forceinline__ void store(uint16_t (*S)[TP]) const {
-        const int t = threadIdx.x;
-        const int ch = t % 8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int lr = e * 32 + t / 8;
-            uint4 o = r[e];
-            if (FOLD) {
-                const uint32_t w[4] = {o.x, o.y, o.z, o.w};
-                const float cq[8] = {cq4[0].x, cq4[0].y, cq4[0].z, cq4[0].w, cq4[1].x, cq4[1].y, cq4[1].z, cq4[1].w};
-                uint32_t g[4];
-#pragma unroll
-                for (int p = 0; p < 4; ++p)
-                    g[p] = pack_bf16x2(dot2(w[p], one_lo_, cq[2 * p]), dot2(w[p], one_hi_, cq[2 * p + 1]));
-                o = make_uint4(g[0], g[1], g[2], g[3]);
-            }
-            *reinterpret_cast<uint4*>(&S[lr][swz(lr, ch) * 8]) = and_mask(o, mk[e]);
-        }
-    }
-};
-
-// dW's B operand: G(k, n) from R[k][n] (n contiguous, Nn a multiple of 8). Thread t stages k rows
-// kq*8..+7 and columns nq*8..+7 (kq = t / 32, nq = t % 32): G' = r_coef R + cqp_n by dot products,
-// then pairs (k, k+1) of one column are packed to bf16 -- the transpose -- and masked per row.
-struct StageGt256 {
-    uint4 r[8];
-    float vmr[8];     // row masks as loaded (consumed only at store time, after the MFMA phase)
-    int kbase;        // first k row of this thread in the staged tile
-    int kend_;
-    bool nok_;
-    float cqn[8];
-    const float* vmask_;
-    uint32_t one_lo_, one_hi_;
-    __device__ __forceinline__ void init_cols(int Nn, int n0, const Fold& f) {
-        vmask_ = f.vmask;
-        one_lo_ = __float_as_uint(f.scal[2]);
-        one_hi_ = __float_as_uint(f.scal[3]);
-        const int n = n0 + (threadIdx.x % 32) * 8;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) cqn[c] = (n + c < Nn) ? f.cqp[n + c] : 0.f;
-    }
-    __device__ __forceinline__ void load(const uint16_t* R, int64_t ldr, int Nn, int n0, int k0, int kend) {
-        const int t = threadIdx.x, kq = t / 32, nq = t % 32;
-        const int n = n0 + nq * 8;
-        nok_ = n < Nn;
-        kend_ = kend;
-        kbase = k0 + kq * 8;
-        const int nc = nok_ ? n : Nn - 8;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int k = kbase + q;
-            r[q] = ld16(R + (int64_t)(k < kend ? k : kend - 1) * ldr + nc);
-            vmr[q] = vmask_[k < kend ? k : kend - 1];
-        }
-    }
-    __device__ __forceinline__ void store(uint16_t (*S)[TP]) const {
-        const int t = threadIdx.x, kq = t / 32, nq = t % 32;
-        uint32_t pm[4];   // masks of the packed (k, k+1) pairs: row in range and in I, column in range
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            const bool o0 = nok_ && kbase + 2 * p < kend_ && vmr[2 * p] != 0.f;
-            const bool o1 = nok_ && kbase + 2 * p + 1 < kend_ && vmr[2 * p + 1] != 0.f;
-            pm[p] = (o0 ? 0x0000FFFFu : 0u) | (o1 ? 0xFFFF0000u : 0u);
-        }
-        const uint32_t w[8][4] = {{r[0].x, r[0].y, r[0].z, r[0].w}, {r[1].x, r[1].y, r[1].z, r[1].w},
-                                  {r[2].x, r[2].y, r[2].z, r[2].w}, {r[3].x, r[3].y, r[3].z, r[3].w},
-                                  {r[4].x, r[4].y, r[4].z, r[4].w}, {r[5].x, r[5].y, r[5].z, r[5].w},
-                                  {r[6].x, r[6].y, r[6].z, r[6].w}, {r[7].x, r[7].y, r[7].z, r[7].w}};
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-            const uint32_t one = (c & 1) ? one_hi_ : one_lo_;
-            uint32_t g[4];
-#pragma unroll
-            for (int p = 0; p < 4; ++p)
-                g[p] = pack_bf16x2(dot2(w[2 * p][c >> 1], one, cqn[c]), dot2(w[2 * p + 1][c >> 1], one, cqn[c])) & pm[p];
-            const int row = nq * 8 + c;
-            *reinterpret_cast<uint4*>(&S[row][swz(row, kq) * 8]) = make_uint4(g[0], g[1], g[2], g[3]);
-        }
-    }
-};
-
-__device__ __forceinline__ void mfma256_steps(const uint16_t (*As)[TP], const uint16_t (*Bs)[TP], f32x16_t (&acc)[4][4],
-                                              int kk0, int kk1) {
-    const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
-    const int wm = w / 2, wn = w % 2;
-    const int lr = lane % 32, lh = lane / 32;
-#pragma unroll
-    for (int kk = kk0; kk < kk1; ++kk) {
-        bf16x8_t a[4], b[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int row = wm * 128 + i * 32 + lr;
-            a[i] = *reinterpret_cast<const bf16x8_t*>(&As[row][swz(row, kk * 2 + lh) * 8]);
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int row = wn * 128 + j * 32 + lr;
-            b[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[row][swz(row, kk * 2 + lh) * 8]);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-}
 
 template <typename F>
 __device__ __forceinline__ void for_each_acc256(const f32x16_t (&acc)[4][4], F&& fn) {
@@ -677,78 +524,6 @@ __device__ __forceinline__ bool tile_of(int inner_count, int outer_count, bool i
 
 // C[m][n] = sum_k A(m, k) B(k, n) for dW (A = H^T k-contiguous, B = G from R) or dH (A = G from R,
 // B = W). Output fp32 (with beta) or TO, or fp32 split-K partials.
-template <bool IS_DW, typename TO>
-__global__ __launch_bounds__(256, 1) void mfma256_kernel(const uint16_t* __restrict__ Xa, int64_t lda,
-                                                         const uint16_t* __restrict__ Xb, int64_t ldb, int M, int Nn,
-                                                         int K, int kps, int inner_count, int outer_count, Fold f,
-                                                         TO* __restrict__ out, int64_t ldo, float beta,
-                                                         float* __restrict__ part) {
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][TB][TP];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][TB][TP];
-    int tm, tn;
-    if (!tile_of(inner_count, outer_count, IS_DW, &tm, &tn)) return;
-    const int m0 = tm * TB, n0 = tn * TB;
-    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
-    const float s_out = f.scal[1];
-    f32x16_t acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-    StageKC256<!IS_DW> sa;   // dW: A = H^T (no fold); dH: A = G from R (fold)
-    typename std::conditional<IS_DW, StageGt256, StageKC256<false>>::type sb;
-    sa.init_rows(M, m0, f);
-    if constexpr (IS_DW) sb.init_cols(Nn, n0, f);
-    // Software pipeline: LDS holds tiles kt (being multiplied) and kt + 1 (being filled); the A and
-    // B register sets are refilled with tile kt + 2 right after they are written to LDS, so every
-    // global load has a whole iteration of MFMA work to arrive. The loop body has no branches (the
-    // last iterations load fully masked tiles and fill the idle buffer): control flow inside the
-    // loop would make the register allocator move the 256 accumulators between register files.
-    const int nk = (ke - kb + TK - 1) / TK;
-    auto load_a = [&](int k0) { sa.load(Xa, lda, M, m0, k0, ke); };
-    auto load_b = [&](int k0) { sb.load(Xb, ldb, Nn, n0, k0, ke); };
-    load_a(kb);
-    load_b(kb);
-    sa.store(As[0]);
-    sb.store(Bs[0]);
-    load_a(kb + TK);
-    load_b(kb + TK);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        const int k2 = kb + (kt + 2) * TK;
-        sa.store(As[buf ^ 1]);
-        load_a(k2);
-        mfma256_steps(As[buf], Bs[buf], acc, 0, 2);
-        sb.store(Bs[buf ^ 1]);
-        load_b(k2);
-        mfma256_steps(As[buf], Bs[buf], acc, 2, 4);
-        __syncthreads();
-    }
-    if (part == nullptr) {
-        for_each_acc256(acc, [&](int r, int c, float v) {
-            const int m = m0 + r, n = n0 + c;
-            if (m < M && n < Nn) {
-                if constexpr (IS_DW) {
-                    float* p = reinterpret_cast<float*>(out) + (int64_t)m * ldo + n;
-                    *p = beta != 0.f ? s_out * v + beta * *p : s_out * v;
-                } else {
-                    stf<TO>(out, (int64_t)m * ldo + n, s_out * v);
-                }
-            }
-        });
-    } else {
-        float* pz = part + (int64_t)blockIdx.z * M * Nn;
-        for_each_acc256(acc, [&](int r, int c, float v) {
-            const int m = m0 + r, n = n0 + c;
-            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = s_out * v;
-        });
-    }
-}
-
 // ---- MFMA bf16, rank-1 form -----------------------------------------------------------------------
 // Rank-1 form of the fold: with alpha = (1 - lambda) / N_t and rows of R outside I equal to zero,
 //   dW = alpha H^T R + hsum cq^T,   hsum_m = sum_{i in I} H_im,  cq_n = lambda q_hat_n / N_t,
@@ -1034,10 +809,12 @@ __global__ __launch_bounds__(256, 1) void lds256_kernel(const uint16_t* __restri
 }
 
 // The same product with k tiles of 64 in two LDS stages (one barrier per 64 k instead of per 32):
-// each wave copies 8 kilobytes per operand per tile; dH's LDS rows are 64 k (128 B) with chunk c of
-// row r at swz(r, c), dW's LDS rows are 512 B per k as in lds256_kernel. Tile kt+1 is written from
-// registers at the start of iteration kt and tile kt+2 loaded behind it; the barrier sits before the
-// last MFMA step of the tile.
+// each wave copies 8 kilobytes per operand per tile. A k-contiguous operand (dH's two) has LDS rows
+// of 64 k (128 B) with chunk c of row r at swz(r, c) and 16-byte
+// fragment reads; a k-outer operand (dW's two) has LDS rows of 512 B per k as in lds256_kernel and
+// transposing fragment reads. (dW with A given as H^T, k-contiguous, from a transpose of H measured no
+// faster: the transposing reads of one operand are not what bounds it.) Tile kt+1 is written from registers at the start of
+// iteration kt and tile kt+2 loaded behind it; the barrier sits before the last MFMA step of the tile.
 template <bool IS_DW, typename TO>
 __global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restrict__ Xa, int64_t lda,
                                                          const uint16_t* __restrict__ Xb, int64_t ldb, int M, int Nn, int K,
@@ -1047,6 +824,8 @@ __global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restr
                                                          float* __restrict__ part) {
     constexpr int KT = 64;
     constexpr int SE = LB * KT;   // bf16 elements per operand per stage (32 KB)
+    constexpr bool KA = !IS_DW;           // operand A k-contiguous
+    constexpr bool KB = !IS_DW;           // operand B k-contiguous
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][SE];
     __shared__ float rv_s[LB];
     int tm, tn;
@@ -1067,64 +846,66 @@ __global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restr
     }
 
     // copy step q (< 8) of this wave fills kilobyte wave*8 + q of an operand's stage
-    int voff_a[8], voff_b[8], kc[8];
+    int voff_a[8], voff_b[8], kc_a[8], kc_b[8];
     bool ok_a[8], ok_b[8];
+    auto geo = [&](bool kcontig, int64_t ld, int rows_valid, int q, int* voff, int* kc, bool* ok) {
+        const int chunk = (wave * 8 + q) * 64 + l;
+        if (kcontig) {
+            const int row = chunk / 8, c = swz(row, chunk % 8);
+            *voff = (int)((int64_t)row * ld * 2) + c * 16;
+            *kc = c * 8;
+            *ok = row < rows_valid;
+        } else {
+            const int krow = chunk / 32, c = (chunk % 32) ^ ((krow & 3) << 2);
+            *voff = (int)((int64_t)krow * ld * 2) + c * 16;
+            *kc = krow;
+            *ok = true;
+        }
+    };
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-        const int chunk = (wave * 8 + q) * 64 + l;
-        if constexpr (IS_DW) {
-            const int krow = chunk / 32, c = (chunk % 32) ^ ((krow & 3) << 2);
-            voff_a[q] = (int)((int64_t)krow * lda * 2) + c * 16;
-            voff_b[q] = (int)((int64_t)krow * ldb * 2) + c * 16;
-            kc[q] = krow;
-            ok_a[q] = ok_b[q] = true;
-        } else {
-            const int row = chunk / 8, c = swz(row, chunk % 8);
-            voff_a[q] = (int)((int64_t)row * lda * 2) + c * 16;
-            voff_b[q] = (int)((int64_t)row * ldb * 2) + c * 16;
-            kc[q] = c * 8;
-            ok_a[q] = row < M - m0;
-            ok_b[q] = row < Nn - n0;
-        }
+        geo(KA, lda, M - m0, q, &voff_a[q], &kc_a[q], &ok_a[q]);
+        geo(KB, ldb, Nn - n0, q, &voff_b[q], &kc_b[q], &ok_b[q]);
     }
-    int bytes_ta = 0, bytes_tb = 0;
-    if constexpr (!IS_DW) {
-        const int ra = min(LB, M - m0), rb = min(LB, Nn - n0);
-        bytes_ta = (int)(((int64_t)(ra - 1) * lda + K) * 2);
-        bytes_tb = (int)(((int64_t)(rb - 1) * ldb + K) * 2);
-    }
+    // k-contiguous operands: one descriptor per workgroup over the tile's rows (exact extent)
+    const int bytes_ta = KA ? (int)(((int64_t)(min(LB, M - m0) - 1) * lda + K) * 2) : 0;
+    const int bytes_tb = KB ? (int)(((int64_t)(min(LB, Nn - n0) - 1) * ldb + K) * 2) : 0;
     struct TileLoad {
         const uint16_t* ba;
         const uint16_t* bb;
         int bytes_a, bytes_b, k0;
     };
+    // k-outer operands: descriptors rebased on (k0, first column) per k tile, rows at or past ke read zeros
     auto tile_load = [&](int kt) {
         TileLoad tl;
         tl.k0 = kb + kt * KT;
-        if constexpr (IS_DW) {
-            const int nv = min(KT, ke - tl.k0);
-            const int nv1 = max(nv, 1);
-            const int kr = min(tl.k0, K - 1);
-            tl.ba = Xa + (int64_t)kr * lda + m0;
-            tl.bb = Xb + (int64_t)kr * ldb + n0;
-            tl.bytes_a = nv > 0 ? (int)(((int64_t)(nv1 - 1) * lda + (M - m0)) * 2) : 0;
-            tl.bytes_b = nv > 0 ? (int)(((int64_t)(nv1 - 1) * ldb + (Nn - n0)) * 2) : 0;
-        } else {
+        const int nv = min(KT, ke - tl.k0);
+        const int nv1 = max(nv, 1);
+        const int kr = min(tl.k0, K - 1);
+        if constexpr (KA) {
             tl.ba = Xa + (int64_t)m0 * lda;
-            tl.bb = Xb + (int64_t)n0 * ldb;
             tl.bytes_a = bytes_ta;
+        } else {
+            tl.ba = Xa + (int64_t)kr * lda + m0;
+            tl.bytes_a = nv > 0 ? (int)(((int64_t)(nv1 - 1) * lda + (M - m0)) * 2) : 0;
+        }
+        if constexpr (KB) {
+            tl.bb = Xb + (int64_t)n0 * ldb;
             tl.bytes_b = bytes_tb;
+        } else {
+            tl.bb = Xb + (int64_t)kr * ldb + n0;
+            tl.bytes_b = nv > 0 ? (int)(((int64_t)(nv1 - 1) * ldb + (Nn - n0)) * 2) : 0;
         }
         return tl;
     };
     // copy op q < 16: q < 8 operand A, else operand B
     auto load_one = [&](const TileLoad& tl, int q) {
         if (q < 8) {
-            const int vo = IS_DW ? voff_a[q] : ((ok_a[q] && tl.k0 + kc[q] < ke) ? voff_a[q] + tl.k0 * 2 : kOob);
+            const int vo = !KA ? voff_a[q] : ((ok_a[q] && tl.k0 + kc_a[q] < ke) ? voff_a[q] + tl.k0 * 2 : kOob);
             return __builtin_amdgcn_raw_buffer_load_b128(make_desc(tl.ba, tl.bytes_a), vo, 0, 0);
         }
         const int r = q - 8;
-        const int vo = IS_DW ? voff_b[r] : ((ok_b[r] && tl.k0 + kc[r] < ke) ? voff_b[r] + tl.k0 * 2 : kOob);
+        const int vo = !KB ? voff_b[r] : ((ok_b[r] && tl.k0 + kc_b[r] < ke) ? voff_b[r] + tl.k0 * 2 : kOob);
         return __builtin_amdgcn_raw_buffer_load_b128(make_desc(tl.bb, tl.bytes_b), vo, 0, 0);
     };
     auto write_one = [&](int stage, int q, const u32x4_t& v) {
@@ -1132,37 +913,35 @@ __global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restr
         *reinterpret_cast<u32x4_t*>(base + (wave * 8 + q % 8) * 1024 + l * 16) = v;
     };
 
-    // fragments for MFMA step s (k = 16 s .. +15)
+    // fragments for MFMA step s (k = 16 s .. +15): k-outer offsets (transposing reads) or LDS rows
+    // (16-byte reads; the chunk depends on the step)
     int fa[4], fb[4];
-    if constexpr (IS_DW) {
-        const int s = l % 16, g = l / 16;
-        const int krow = (g >> 1) * 8 + (s >> 2);
+    auto frag_geo = [&](bool kcontig, int wbase, int (&f)[4]) {
+        if (kcontig) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int lo = ((i ^ (s >> 2)) * 4) + (g & 1) * 2 + ((s >> 1) & 1);
-            fa[i] = krow * 512 + ((wm * 16 + lo) << 4) + (s & 1) * 8;
-            fb[i] = krow * 512 + ((wn * 16 + lo) << 4) + (s & 1) * 8;
-        }
-    } else {
+            for (int i = 0; i < 4; ++i) f[i] = wbase * 128 + i * 32 + l % 32;
+        } else {
+            const int s = l % 16, g = l / 16;
+            const int krow = (g >> 1) * 8 + (s >> 2);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            fa[i] = wm * 128 + i * 32 + l % 32;   // LDS rows; the chunk depends on the step
-            fb[i] = wn * 128 + i * 32 + l % 32;
+            for (int i = 0; i < 4; ++i) {
+                const int lo = ((i ^ (s >> 2)) * 4) + (g & 1) * 2 + ((s >> 1) & 1);
+                f[i] = krow * 512 + ((wbase * 16 + lo) << 4) + (s & 1) * 8;
+            }
         }
-    }
+    };
+    frag_geo(KA, wm, fa);
+    frag_geo(KB, wn, fb);
     auto read_frags = [&](int stage, int s, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
         const char* As = reinterpret_cast<const char*>(&lds[stage][0][0]);
         const char* Bs = reinterpret_cast<const char*>(&lds[stage][1][0]);
+        const int c = 2 * s + l / 32;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            if constexpr (IS_DW) {
-                a[i] = ld_frag_tr(As + fa[i] + s * 16 * 512);
-                b[i] = ld_frag_tr(Bs + fb[i] + s * 16 * 512);
-            } else {
-                const int c = 2 * s + l / 32;
-                a[i] = ld_frag_b128(As + fa[i] * 128 + swz(fa[i], c) * 16);
-                b[i] = ld_frag_b128(Bs + fb[i] * 128 + swz(fb[i], c) * 16);
-            }
+            if constexpr (KA) a[i] = ld_frag_b128(As + fa[i] * 128 + swz(fa[i], c) * 16);
+            else a[i] = ld_frag_tr(As + fa[i] + s * 16 * 512);
+            if constexpr (KB) b[i] = ld_frag_b128(Bs + fb[i] * 128 + swz(fb[i], c) * 16);
+            else b[i] = ld_frag_tr(Bs + fb[i] + s * 16 * 512);
         }
     };
 
@@ -1344,22 +1123,6 @@ __global__ __launch_bounds__(256) void vjp_rank1_kernel(const uint16_t* __restri
     }
 }
 
-// H [N][d] -> H^T [d][N] (bf16), 64 x 64 tiles through LDS.
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ H, int64_t ldh, int N, int d,
-                                                             uint16_t* __restrict__ Ht) {
-    __shared__ uint16_t tile[64][66];
-    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-    const int t = threadIdx.x;
-    for (int e = t; e < 64 * 64; e += 256) {
-        const int r = e / 64, c = e % 64;
-        tile[r][c] = (r0 + r < N && c0 + c < d) ? H[(int64_t)(r0 + r) * ldh + c0 + c] : (uint16_t)0;
-    }
-    __syncthreads();
-    for (int e = t; e < 64 * 64; e += 256) {
-        const int c = e / 64, r = e % 64;
-        if (c0 + c < d && r0 + r < N) Ht[(int64_t)(c0 + c) * N + r0 + r] = tile[r][c];
-    }
-}
 
 // Split-K reduction in split order: out = sum_z part[z] (+ beta * out for dW).
 template <typename TO>
@@ -1617,7 +1380,7 @@ __global__ __launch_bounds__(256, 2) void vjp_fused_small_kernel(FusedArgs a) {
 constexpr int kCUs = 256;        // MI355X compute units
 constexpr int kMaxSplits = 8;
 
-enum GemmKind { kSimt = 0, kMfma128 = 1, kMfma256 = 2, kRank1 = 3 };
+enum GemmKind { kSimt = 0, kMfma128 = 1, kRank1 = 3 };
 struct GemmPlan {
     int kind, splits;
     int wide = 0;   // rank-1 kind: k tiles of 64 in two stages (lds256w_kernel)
@@ -1669,9 +1432,8 @@ GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K) {
 
 // Plan override for A/B measurement (environment BOM_VJP_PLAN = "kind_w,splits_w,kind_h,splits_h",
 // read once; 0 keeps the automatic choice (small products: the fused launch); kinds 1 = 128-tile
-// MFMA (and no fused launch), 2 = 256-tile MFMA with staged
-// fold, 3 = 256-tile rank-1 kernel with 32-deep k tiles in four stages, 4 = the same with 64-deep k
-// tiles in two stages).
+// MFMA (and no fused launch), 3 = 256-tile rank-1 kernel with 32-deep k tiles in four stages,
+// 4 = the same with 64-deep k tiles in two stages).
 struct PlanOverride {
     int kw = 0, sw = 0, kh = 0, sh = 0;
 };
@@ -1689,7 +1451,6 @@ const PlanOverride& plan_override() {
 void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int64_t K) {
     if (g.kind == kSimt) return;
     if (kind == kMfma128) g.kind = kMfma128;
-    if (kind == kMfma256 && K >= 4 * TK) g.kind = kMfma256;
     if (kind == kRank1) {
         g.kind = kRank1;
         g.wide = 0;
@@ -1700,7 +1461,7 @@ void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int
     }
 
     if (splits > 0) {
-        const int ktile = g.kind == kMfma256 ? TK : (g.kind == kRank1 ? LK * (1 + g.wide) : MK);
+        const int ktile = g.kind == kRank1 ? LK * (1 + g.wide) : MK;
         // every split keeps at least one k tile
         g.splits = (int)(splits < cdiv(K, ktile) ? splits : cdiv(K, ktile));
     }
@@ -1729,10 +1490,8 @@ VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     w.cqp_off = align256((size_t)V * 4);
     w.vmask_off = align256(w.cqp_off + (size_t)V * 4);
     w.scal_off = align256(w.vmask_off + (size_t)N * 4);
-    w.ht_off = align256(w.scal_off + 16);
-    const size_t ht = p.w.kind == kMfma256 ? (size_t)d * N * 2 : 0;
     const bool r1 = p.w.kind == kRank1 || p.h.kind == kRank1;
-    w.hpart_off = align256(w.ht_off + ht);
+    w.hpart_off = align256(w.scal_off + 16);
     w.hsum_off = align256(w.hpart_off + (r1 ? (size_t)cdiv(N, kHsRows) * d * 4 : 0));
     w.u_off = align256(w.hsum_off + (r1 ? (size_t)d * 4 : 0));
     w.part_off = align256(w.u_off + (r1 ? (size_t)d * 4 : 0));
@@ -1776,23 +1535,13 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
                            rv, cv, out, ldo, beta);
         return hipGetLastError();
     }
-    const int tb = g.kind == kMfma256 ? TB : (g.kind == kMfma128 ? MB : SB);
-    const int ktile = g.kind == kMfma256 ? TK : (g.kind == kMfma128 ? MK : SK);
+    const int tb = g.kind == kMfma128 ? MB : SB;
+    const int ktile = g.kind == kMfma128 ? MK : SK;
     int kps = (int)(cdiv(cdiv(K, splits), ktile) * ktile);
     float* pz = splits > 1 ? part : nullptr;
     const uint16_t* a16 = static_cast<const uint16_t*>(A);
     const uint16_t* b16 = static_cast<const uint16_t*>(B);
-    if (g.kind == kMfma256) {
-        const int MT = (int)cdiv(M, TB), NT = (int)cdiv(Nn, TB);
-        const int inner = is_dw ? MT : NT, outer = is_dw ? NT : MT;
-        dim3 grid((unsigned)(cdiv(outer, 8) * 8 * inner), 1, splits);
-        if (is_dw)
-            hipLaunchKernelGGL((mfma256_kernel<true, float>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
-                               inner, outer, f, reinterpret_cast<float*>(out), ldo, beta, pz);
-        else
-            hipLaunchKernelGGL((mfma256_kernel<false, TO>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
-                               inner, outer, f, out, ldo, beta, pz);
-    } else {
+    {
         dim3 grid((unsigned)cdiv(Nn, tb), (unsigned)cdiv(M, tb), splits);
         if (g.kind == kMfma128) {
             if (is_dw)
@@ -1839,7 +1588,6 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
     float* cqp = reinterpret_cast<float*>(base + L.cqp_off);
     float* vmask = reinterpret_cast<float*>(base + L.vmask_off);
     float* scal = reinterpret_cast<float*>(base + L.scal_off);
-    uint16_t* ht = reinterpret_cast<uint16_t*>(base + L.ht_off);
     float* hpart = reinterpret_cast<float*>(base + L.hpart_off);
     float* hsum = reinterpret_cast<float*>(base + L.hsum_off);
     float* u = reinterpret_cast<float*>(base + L.u_off);
@@ -1917,18 +1665,7 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
     const Fold f{cq, vmask, scal, cqp};
 
     // dW = H^T G
-    const void* A = a.H;
-    int64_t lda = a.ldh;
-    if (p.w.kind == kMfma256) {
-        dim3 tg((unsigned)cdiv(a.d, 64), (unsigned)cdiv(a.N, 64));
-        hipLaunchKernelGGL(transpose_bf16_kernel, tg, dim3(256), 0, st, static_cast<const uint16_t*>(a.H), a.ldh, a.N, a.d,
-                           ht);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        A = ht;
-        lda = a.N;
-    }
-    e = run_gemm<float>(true, p.w, A, lda, a.R, a.ldr, a.dt, a.d, a.V, a.N, f, a.dW, a.lddw, a.dW_beta, part, hsum, cq,
+    e = run_gemm<float>(true, p.w, a.H, a.ldh, a.R, a.ldr, a.dt, a.d, a.V, a.N, f, a.dW, a.lddw, a.dW_beta, part, hsum, cq,
                         st);
     if (e != hipSuccess) return e;
     // dH = G W^T (shares the split-K buffer: same stream, so it runs after the dW reduction)

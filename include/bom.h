@@ -125,12 +125,13 @@ bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, 
  *   dW = H^T G + dW_beta * dW     [d, V] fp32 (dW_beta = 0 overwrites; dW is not read then)
  *   db = (1 - lambda) s + lambda q_hat   [V] fp32  (bias Jacobian = identity; equals 1^T G)
  *   dH = G W^T                     [N, d] of dh_dt
- * G is never written to memory. Small products form it tile by tile inside the GEMMs (the
- * history folded into the output gradient at operand load, rounded to bf16 for the MFMA path);
- * large bf16 products use the equal rank-1 form
+ * G is never written to memory. bf16 products use the equal rank-1 form
  *   dW = alpha H^T R + (sum_{i in I} H_i) (lambda q_hat / N_t)^T
  *   dH = alpha R W^T + 1_I (lambda / N_t W q_hat)^T
- * with alpha = (1 - lambda) / N_t, which multiplies R as stored and adds the history in fp32.
+ * with alpha = (1 - lambda) / N_t, which multiplies R as stored and adds the history in fp32
+ * (small products of both in one launch); small products with N or V above 8192 instead form G
+ * tile by tile inside the GEMMs (the history folded into the output gradient at operand load,
+ * rounded to bf16 for the MFMA), and fp32 inputs fold it in fp32.
  * N_t is read from the device word n_valid; when it is 0, G = 0.
  *
  *   H   device [N, ldh] of dt.   W device [d, ldw] of dt (the head as d x V).

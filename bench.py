@@ -227,7 +227,18 @@ def cpu_baseline(w, budget_s: float):
                    f"{npar} of {P} parameters (update); each stage scaled linearly to the full step"),
         "step_s_extrapolated": step_s,
         "stage_s": {k: round(v, 4) for k, v in t_all.items()},
+        "nproc": os.cpu_count(), "host_cpu": host_cpu_model(),
     }
+
+
+def host_cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():

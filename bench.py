@@ -174,38 +174,32 @@ def stored_traffic(stage: str, workload: str):
     return float(m_bytes.group(1))
 
 
-def cpu_baseline(w, budget_s: float):
-    """The fp64 oracle (as it stands) timed on the host on a bounded sample of the same workload,
-    scaled to the whole step. Each stage runs on a sample; per-element work scales linearly."""
+def _oracle_sample(w, rows, ncols, nrows_dh, npar):
+    """Host seconds of each oracle stage on one sample: `rows` rows of Z (residual; dW and dH use the
+    same rows), `ncols` dW columns, `nrows_dh` dH rows, `npar` parameters of the update."""
     import oracle
 
-    N, d, V, P = w.N, w.d, w.V, w.P
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    # sample sizes: rows of Z for the residual and the head GEMM rows/columns, elements for the update
-    rows = min(N, max(16, int(2e6 // V)))
-    ncols = min(V, 64)
-    nrows_dh = min(rows, 16)   # dH rows are taken from the sampled rows of Z
-    npar = min(P, 4_000_000)
-    t_all = {}
+    N, d, V = w.N, w.d, w.V
+    raw = {}
     Zs = synth.bf16_to_f32(synth.normal_bf16(rows * V, synth.STREAM_Z, w.logit_std)) if w.dtype == "bf16" else \
         synth.normal_f32(rows * V, synth.STREAM_Z, w.logit_std)
     Zs = Zs.reshape(rows, V).astype(np.float64)
     y = (synth.labels_uniform(N, V) if w.labels == "uniform" else synth.labels_zipf(N, V))[:rows]
     t0 = time.perf_counter()
     res = oracle.residual(Zs, y, want_R=False)
-    t_all["bom_residual"] = (time.perf_counter() - t0) * N / rows
+    raw["bom_residual"] = time.perf_counter() - t0
     t0 = time.perf_counter()
     _, qh = oracle.ema(np.zeros(V), res["s"], w.beta1, 1)
-    t_all["bom_ema"] = time.perf_counter() - t0
+    raw["bom_ema"] = time.perf_counter() - t0
     Hs = synth.normal_f32(rows * d, synth.STREAM_H, 1.0).reshape(rows, d).astype(np.float64)
     Ws = synth.normal_f32(d * V, synth.STREAM_W, 0.02).reshape(d, V).astype(np.float64)
     t0 = time.perf_counter()
     oracle.dW_cols(Hs, Zs, y, res["row_lse"], qh, res["n_valid"], w.lam, cols=np.arange(ncols))
-    t_dw = (time.perf_counter() - t0) * (V / ncols) * (N / rows)
+    raw["dW"] = time.perf_counter() - t0
     t0 = time.perf_counter()
     oracle.dH_rows(Ws, Zs, y, res["row_lse"], qh, res["n_valid"], w.lam, rows=np.arange(nrows_dh))
-    t_dh = (time.perf_counter() - t0) * (N / nrows_dh)
-    t_all["bom_head_vjp"] = t_dw + t_dh
+    raw["dH"] = time.perf_counter() - t0
+    del Zs, Hs, Ws
     th = synth.normal_f32(npar, synth.STREAM_THETA, 0.02).astype(np.float64)
     u = synth.normal_f32(npar, synth.STREAM_U + 1, 1e-3).astype(np.float64)
     t0 = time.perf_counter()
@@ -215,16 +209,68 @@ def cpu_baseline(w, budget_s: float):
         oracle.update_factored(th[: nr * bc], np.zeros(nr), np.zeros(-(-nr // br) * bc), u[: nr * bc], lr=w.lr,
                                beta2=w.beta2, eps=w.eps, t=1, block_rows=br, block_cols=bc,
                                weight_decay=w.weight_decay)
-        t_all["bom_update"] = (time.perf_counter() - t0) * P / (nr * bc)
+        npar = nr * bc
     else:
         oracle.update_dense(th, np.zeros(npar), u, lr=w.lr, beta2=w.beta2, eps=w.eps, t=1,
                             weight_decay=w.weight_decay)
-        t_all["bom_update"] = (time.perf_counter() - t0) * P / npar
+    raw["bom_update"] = time.perf_counter() - t0
+    # each stage scaled linearly to the whole step
+    full = {"bom_residual": raw["bom_residual"] * N / rows, "bom_ema": raw["bom_ema"],
+            "bom_head_vjp": raw["dW"] * (V / ncols) * (N / rows) + raw["dH"] * (N / nrows_dh),
+            "bom_update": raw["bom_update"] * w.P / npar}
+    return raw, full, npar
+
+
+def cpu_baseline(w, budget_s: float):
+    """The fp64 oracle (as it stands) timed on the host on a bounded sample of the same workload,
+    scaled to the whole step. Starting from a small probe, the sample of each part (residual rows,
+    head-product columns and rows, update parameters) grows until that part takes about a third of
+    `budget_s` or covers the whole workload; a sample that is the whole step is repeated until half
+    the budget is used. The last sample is the one reported."""
+    N, d, V, P = w.N, w.d, w.V, w.P
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    max_rows = max(16, min(N, int(4e7 // V), int(4e7 // d)))     # bounded host memory (fp64 copies)
+    max_par = min(P, 200_000_000)
+    rows = min(max_rows, max(16, int(2e6 // V)))
+    ncols, nrows_dh, npar = min(V, 64), min(rows, 16), min(max_par, 4_000_000)
+    share = budget_s / 3.0
+    spent = 0.0
+    for _ in range(4):
+        raw, full, npar = _oracle_sample(w, rows, ncols, nrows_dh, npar)
+        spent += sum(raw.values())
+        grown = False
+        if raw["bom_residual"] < 0.5 * share and rows < max_rows:
+            f = min(8.0, share / max(raw["bom_residual"], 1e-4))
+            rows, grown = int(min(max_rows, rows * f)), True
+        vjp = raw["dW"] + raw["dH"]
+        if vjp < 0.5 * share and (ncols < V or nrows_dh < rows):
+            f = min(8.0, share / max(vjp, 1e-4))
+            ncols, nrows_dh, grown = int(min(V, ncols * f)), int(min(rows, nrows_dh * f)), True
+        nrows_dh = min(nrows_dh, rows)
+        if raw["bom_update"] < 0.5 * share and npar < max_par:
+            f = min(8.0, share / max(raw["bom_update"], 1e-4))
+            npar, grown = int(min(max_par, npar * f)), True
+        if not grown:
+            break
+    else:
+        raw, full, npar = _oracle_sample(w, rows, ncols, nrows_dh, npar)
+        spent += sum(raw.values())
+    whole = rows == N and ncols == V and nrows_dh == N and npar == P
+    reps, t_sample, acc = 1, sum(raw.values()), dict(full)
+    while whole and t_sample < 0.5 * budget_s and reps < 200:
+        raw, full, npar = _oracle_sample(w, rows, ncols, nrows_dh, npar)
+        t_sample += sum(raw.values())
+        reps += 1
+        acc = {k: acc[k] + full[k] for k in full}
+    t_all = {k: v / reps for k, v in acc.items()}
     step_s = sum(t_all.values())
+    sample = ("the whole step (all rows, full dW and dH, all parameters)" if whole else
+              f"{rows} of {N} rows of Z (residual; dW and dH on the same rows), {ncols} of {V} dW columns, "
+              f"{nrows_dh} of {N} dH rows, {npar} of {P} parameters (update); each stage scaled linearly to "
+              f"the full step")
     return {
         "value": N / step_s, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-        "sample": (f"{rows} of {N} rows of Z (residual, dW), {ncols} of {V} dW columns, {nrows_dh} of {N} dH rows, "
-                   f"{npar} of {P} parameters (update); each stage scaled linearly to the full step"),
+        "sample": f"{sample}; {reps} repetition(s), {t_sample:.1f} s of oracle time",
         "step_s_extrapolated": step_s,
         "stage_s": {k: round(v, 4) for k, v in t_all.items()},
         "nproc": os.cpu_count(), "host_cpu": host_cpu_model(),
@@ -248,7 +294,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=[w.name for w in WORKLOADS])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="host seconds the oracle baseline aims to spend (a bounded sample of the workload)")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="run an untimed plain device-to-device copy of this many MiB first (a known-size "
                          "reference for hardware byte counters)")

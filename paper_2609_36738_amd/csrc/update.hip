@@ -207,39 +207,50 @@ __global__ __launch_bounds__(kUpdThreads) void factored_update_kernel(float* __r
     }
 }
 
-// Update with one 16-byte group per thread, like the dense kernel: element e = 4q lies in row
-// i = e / bc of block b = i / block_rows; v_hat = (Rr_i / rsum_b * inv_bc2) * Cc_b[j]. Rr, rsum and
-// Cc are small and shared by many threads (cache hits); theta and u are streamed.
-template <bool SPLIT>
-__global__ __launch_bounds__(kUpdThreads) void factored_update_vec4_kernel(float* __restrict__ theta,
-                                                                           const float* __restrict__ u,
-                                                                           const float* __restrict__ h, int64_t nvec,
-                                                                           int64_t block_rows, int bc,
-                                                                           const float* __restrict__ Rr,
-                                                                           const float* __restrict__ Cc,
-                                                                           const float* __restrict__ rsum, SegTable segs,
-                                                                           UpdateScalars sc) {
-    const int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x;
-    if (q >= nvec) return;
-    const int64_t e = q * 4;
-    f32x4 t4 = ld_stream(theta + e);
-    const f32x4 u4 = ld_stream(u + e);
-    f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
-    if (SPLIT) h4 = ld_stream(h + e);
-    const int64_t i = e / bc;
-    const int j = (int)(e - i * bc);
+// Update for block_cols = NV * 256: one workgroup per row i (a scalar, like its block b = i / block_rows
+// and the row scale Rr_i / rsum_b / bc2), thread t holding columns (k*256 + t)*4 .. +3 for k < NV/4, so
+// no per-element index arithmetic and NV/4 16-byte loads of theta and of u in flight per thread.
+// Elements at or past P (only in the last row) are loaded from a clamped address and not stored.
+template <bool SPLIT, int NV>
+__global__ __launch_bounds__(kUpdThreads) void factored_update_rows_kernel(float* __restrict__ theta,
+                                                                          const float* __restrict__ u,
+                                                                          const float* __restrict__ h, int64_t P,
+                                                                          int64_t block_rows,
+                                                                          const float* __restrict__ Rr,
+                                                                          const float* __restrict__ Cc,
+                                                                          const float* __restrict__ rsum, SegTable segs,
+                                                                          UpdateScalars sc) {
+    constexpr int BC = NV * 256;
+    constexpr int KV = NV / 4;   // 16-byte groups per thread
+    const int64_t i = blockIdx.x;
     const int64_t b = i / block_rows;
-    const f32x4 c4 = *reinterpret_cast<const f32x4*>(Cc + b * bc + j);
     const float rs = rsum[b];
     const float a = rs > 0.f ? Rr[i] / rs * sc.inv_bc2 : 0.f;
+    const float* cb = Cc + b * BC;
+    const int t = threadIdx.x;
+    f32x4 t4[KV], u4[KV], h4[KV], c4[KV];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        const float up = numerator<SPLIT>(u4[c], h4[c], sc);
-        const float vhat = a * c4[c];
-        const float wd = decay_of(e + c, segs);
-        t4[c] = (1.0f - sc.lr * wd) * t4[c] - sc.lr * (up / (sqrtf(vhat) + sc.eps));
+    for (int k = 0; k < KV; ++k) {
+        const int j = (k * kUpdThreads + t) * 4;
+        const int64_t e = i * BC + j;
+        const int64_t ec = e < P ? e : P - 4;
+        t4[k] = ld_stream(theta + ec);
+        u4[k] = ld_stream(u + ec);
+        if (SPLIT) h4[k] = ld_stream(h + ec);
+        c4[k] = *reinterpret_cast<const f32x4*>(cb + j);
     }
-    st_stream(theta + e, t4);
+#pragma unroll
+    for (int k = 0; k < KV; ++k) {
+        const int j = (k * kUpdThreads + t) * 4;
+        const int64_t e = i * BC + j;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float up = numerator<SPLIT>(u4[k][c], SPLIT ? h4[k][c] : 0.f, sc);
+            const float vhat = a * c4[k][c];
+            t4[k][c] = (1.0f - sc.lr * decay_of(e + c, segs)) * t4[k][c] - sc.lr * (up / (sqrtf(vhat) + sc.eps));
+        }
+        if (e < P) st_stream(theta + e, t4[k]);
+    }
 }
 
 // Row kernels for block_cols = NV * 256 (up to 4096): a wave owns whole rows, lane l holding
@@ -401,9 +412,8 @@ hipError_t run_factored_rows(float* theta, float* Rr, float* Cc, const float* u,
                        kpart, (int)L.groups_per_block, L.nrows, br, BC, nchunks, Rr, Cc, rsum, sc);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int64_t nvec = P / 4;
-    hipLaunchKernelGGL((factored_update_vec4_kernel<SPLIT>), dim3((unsigned)((nvec + kUpdThreads - 1) / kUpdThreads)),
-                       dim3(kUpdThreads), 0, st, theta, u, h, nvec, br, BC, Rr, Cc, rsum, segs, sc);
+    hipLaunchKernelGGL((factored_update_rows_kernel<SPLIT, NV>), dim3((unsigned)L.nrows), dim3(kUpdThreads), 0, st, theta,
+                       u, h, P, br, Rr, Cc, rsum, segs, sc);
     return hipGetLastError();
 }
 

@@ -14,6 +14,7 @@
 // fixed-order reduction. dW = H^T G has both operands k-outer in memory (transposing LDS reads or a
 // transpose while staging); dH = G W^T has both operands k-contiguous. fp32 path (and unaligned
 // bf16): a SIMT tiled GEMM.
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <type_traits>
@@ -522,6 +523,33 @@ __device__ __forceinline__ bool tile_of(int inner_count, int outer_count, bool i
     return true;
 }
 
+// A launch over the outer tiles [outer_begin, outer_end), each split into `splits` k ranges (whole
+// rounds of the chip run with the full k range; the leftover tiles split k so that they fill the chip
+// too). Split partials go to a rectangle of fp32 sums with origin (pm0, pn0), leading dimension ldp and
+// split stride pstride.
+struct TileRange {
+    int inner_count, outer_begin, outer_end, splits;
+    int pm0, pn0;
+    int64_t ldp, pstride;
+};
+
+// Work unit of this workgroup. The pairs (outer tile, k split) are dealt to the 8 XCDs round-robin
+// (workgroups are dealt to the XCDs round-robin by id), and all inner tiles of a pair run on the same
+// XCD, so the tiles that share an outer operand panel share that XCD's L2. With one split this is the
+// plain outer-tile order: XCD x runs outer tiles x, x + 8, x + 16, ...
+__device__ __forceinline__ bool unit_of(const TileRange& r, bool inner_is_m, int* tm, int* tn, int* z) {
+    const int id = blockIdx.x;
+    const int xcd = id % 8, rest = id / 8;
+    const int inner = rest % r.inner_count, pg = rest / r.inner_count;
+    const int pair = pg * 8 + xcd;
+    if (pair >= (r.outer_end - r.outer_begin) * r.splits) return false;
+    const int outer = r.outer_begin + pair / r.splits;
+    *z = pair % r.splits;
+    *tm = inner_is_m ? inner : outer;
+    *tn = inner_is_m ? outer : inner;
+    return true;
+}
+
 // C[m][n] = sum_k A(m, k) B(k, n) for dW (A = H^T k-contiguous, B = G from R) or dH (A = G from R,
 // B = W). Output fp32 (with beta) or TO, or fp32 split-K partials.
 // ---- MFMA bf16, rank-1 form -----------------------------------------------------------------------
@@ -818,7 +846,7 @@ __global__ __launch_bounds__(256, 1) void lds256_kernel(const uint16_t* __restri
 template <bool IS_DW, typename TO>
 __global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restrict__ Xa, int64_t lda,
                                                          const uint16_t* __restrict__ Xb, int64_t ldb, int M, int Nn, int K,
-                                                         int kps, int inner_count, int outer_count, const float* alpha_p,
+                                                         int kps, TileRange tr, const float* alpha_p,
                                                          const float* __restrict__ rv, const float* __restrict__ cv,
                                                          TO* __restrict__ out, int64_t ldo, float beta,
                                                          float* __restrict__ part) {
@@ -828,10 +856,14 @@ __global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restr
     constexpr bool KB = !IS_DW;           // operand B k-contiguous
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][SE];
     __shared__ float rv_s[LB];
-    int tm, tn;
-    if (!tile_of(inner_count, outer_count, IS_DW, &tm, &tn)) return;
+    int tm, tn, kz;
+    if (!unit_of(tr, IS_DW, &tm, &tn, &kz)) return;
+    // uniform per workgroup: keep them scalar so that the buffer descriptors stay in SGPRs
+    tm = __builtin_amdgcn_readfirstlane(tm);
+    tn = __builtin_amdgcn_readfirstlane(tn);
+    kz = __builtin_amdgcn_readfirstlane(kz);
     const int m0 = tm * LB, n0 = tn * LB;
-    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
+    const int kb = kz * kps, ke = min(K, kb + kps);
     const int nk = (ke - kb + KT - 1) / KT;
     const int l = threadIdx.x % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -1014,23 +1046,26 @@ __global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restr
             }
         });
     } else {
-        float* pz = part + (int64_t)blockIdx.z * M * Nn;
+        float* pz = part + (int64_t)kz * tr.pstride;
         for_each_acc256(acc, [&](int r, int c, float v) {
             const int m = m0 + r, n = n0 + c;
-            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = alpha * v;
+            if (m < M && n < Nn) pz[(int64_t)(m - tr.pm0) * tr.ldp + (n - tr.pn0)] = alpha * v;
         });
     }
 }
 
-// Split-K reduction for the rank-1 form, in split order: out = sum_z part[z] + rv[m] cv[n] (+ beta out).
+// Split-K reduction for the rank-1 form over the rectangle [pm0, M) x [pn0, Nn) of the output, in split
+// order: out = sum_z part[z] + rv[m] cv[n] (+ beta out); part[z] is that rectangle, row-major.
 template <typename TO>
 __global__ __launch_bounds__(256) void splitk_rank1_kernel(const float* __restrict__ part, int splits, int M, int Nn,
-                                                           const float* __restrict__ rv, const float* __restrict__ cv,
-                                                           TO* __restrict__ out, int64_t ldo, float beta) {
+                                                           int pm0, int pn0, const float* __restrict__ rv,
+                                                           const float* __restrict__ cv, TO* __restrict__ out,
+                                                           int64_t ldo, float beta) {
     const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int64_t MN = (int64_t)M * Nn;
+    const int64_t Nr = Nn - pn0;
+    const int64_t MN = (int64_t)(M - pm0) * Nr;
     if (idx >= MN) return;
-    const int64_t m = idx / Nn, n = idx % Nn;
+    const int64_t m = pm0 + idx / Nr, n = pn0 + idx % Nr;
     float a = 0.f;
     for (int z = 0; z < splits; ++z) a += part[(int64_t)z * MN + idx];
     a = fmaf(rv[m], cv[n], a);
@@ -1384,6 +1419,8 @@ enum GemmKind { kSimt = 0, kMfma128 = 1, kRank1 = 3 };
 struct GemmPlan {
     int kind, splits;
     int wide = 0;   // rank-1 kind: k tiles of 64 in two stages (lds256w_kernel)
+    // wide rank-1 kind: outer tiles [0, outer_dp) run with the whole k range, the rest with `splits`
+    int outer_dp = 0;
 };
 struct Plan {
     GemmPlan w, h;
@@ -1412,16 +1449,51 @@ int choose_splits(int64_t tiles, int64_t M, int64_t N, int64_t K, int tb, int kt
     return best;
 }
 
-GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K) {
+// Schedule of the 64-deep 256-tile kernel. Each XCD (32 CUs) runs the inner tiles of the (outer
+// tile, k split) pairs dealt to it, 32 workgroups at a time. Whole rounds of outer tiles run over the
+// full k range; the outer tiles left over (a partly filled last round) split k into `splits` parts so
+// that their pairs spread over all XCDs, and a reduction pass sums their fp32 partials in split order.
+// Modelled time: rounds per XCD x k tiles per split x the measured time of one 256 x 256 x 64 tile
+// step, plus the partial-sum traffic (write, read, and the output) at streaming bandwidth.
+GemmPlan plan_wide(int64_t M, int64_t N, int64_t K, bool inner_is_m) {
+    constexpr double kTileStep = 1.8e-6;   // seconds per 256 x 256 x 64 tile step
+    constexpr int64_t kXcd = 8, kCuPerXcd = kCUs / 8;
+    const int64_t MT = cdiv(M, LB), NT = cdiv(N, LB);
+    const int64_t inner = inner_is_m ? MT : NT, outer = inner_is_m ? NT : MT;
+    const int64_t nk = cdiv(K, 2 * LK);
+    auto rounds = [&](int64_t pairs) { return cdiv(cdiv(pairs, kXcd) * inner, kCuPerXcd); };
+    const int64_t per_round = kXcd * std::max<int64_t>(1, kCuPerXcd / inner);   // outer tiles per whole round
+    const int64_t full = (outer / per_round) * per_round;
+    GemmPlan best{kRank1, 1};
+    best.wide = 1;
+    best.outer_dp = (int)outer;
+    double best_t = (double)rounds(outer) * nk * kTileStep;
+    for (int64_t dp : {(int64_t)0, full}) {
+        const int64_t rem = outer - dp;
+        if (rem <= 0) continue;
+        const int64_t rect = inner_is_m ? M * std::max<int64_t>(0, N - dp * LB) : std::max<int64_t>(0, M - dp * LB) * N;
+        const double t_dp = (double)rounds(dp) * nk * kTileStep;
+        for (int s = 1; s <= 16; ++s) {
+            const int64_t kps = cdiv(nk, s);
+            if (s > 1 && kps < 4) break;
+            double t = t_dp + (double)rounds(rem * s) * kps * kTileStep;
+            if (s > 1) t += (2.0 * s + 2.0) * 4.0 * (double)rect / 5e12;
+            if (t < best_t - 2e-6) {   // a gain of at least 2 us
+                best_t = t;
+                best.splits = s;
+                best.outer_dp = (int)dp;
+            }
+        }
+    }
+    return best;
+}
+
+GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K, bool inner_is_m) {
     if (!mfma || !big_ok) return {kSimt, choose_splits(cdiv(M, SB) * cdiv(N, SB), M, N, K, SB, SK, 4)};
     // large products: 256-tile rank-1 kernel; small ones (a few dozen 256 tiles or a short k) are
     // latency bound and run faster on the 128-tile kernel, which needs no rank-1 pre-pass
     const int64_t t256 = cdiv(M, LB) * cdiv(N, LB);
-    if (t256 >= 24 && K >= 8 * LK) {
-        GemmPlan g{kRank1, choose_splits(t256, M, N, K, LB, 2 * LK, 1)};
-        g.wide = 1;   // 64-deep k tiles: half the barriers of the 32-deep ring, measured 1-3% faster
-        return g;
-    }
+    if (t256 >= 24 && K >= 8 * LK) return plan_wide(M, N, K, inner_is_m);
     // 128 tiles: split k so that every workgroup loads its whole k range at once, when that takes
     // at most kMaxSplits splits
     const int64_t t128 = cdiv(M, MB) * cdiv(N, MB);
@@ -1459,11 +1531,13 @@ void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int
         g.kind = kRank1;
         g.wide = 1;
     }
+    if (kind == kRank1 || kind == kMfma128) g.outer_dp = 0;
 
     if (splits > 0) {
         const int ktile = g.kind == kRank1 ? LK * (1 + g.wide) : MK;
         // every split keeps at least one k tile
         g.splits = (int)(splits < cdiv(K, ktile) ? splits : cdiv(K, ktile));
+        g.outer_dp = 0;   // a forced split applies to every tile
     }
     (void)M;
     (void)N;
@@ -1475,8 +1549,8 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     // the MFMA kernels load whole 16-byte chunks: extents along k and along contiguous rows must be
     // multiples of 8 (H^T rows have N elements); other shapes use the SIMT kernels
     const bool m8 = N % 8 == 0 && d % 8 == 0 && V % 8 == 0;
-    p.w = plan_gemm(mfma, m8, d, V, N);   // dW: M = d, N = V, K = rows
-    p.h = plan_gemm(mfma, m8, N, d, V);   // dH: M = rows, N = d, K = V
+    p.w = plan_gemm(mfma, m8, d, V, N, true);    // dW: M = d, N = V, K = rows; inner tiles along d
+    p.h = plan_gemm(mfma, m8, N, d, V, false);   // dH: M = rows, N = d, K = V
     const PlanOverride& o = plan_override();
     apply_override(p.w, o.kw, o.sw, d, V, N);
     apply_override(p.h, o.kh, o.sh, N, d, V);
@@ -1495,8 +1569,11 @@ VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     w.hsum_off = align256(w.hpart_off + (r1 ? (size_t)cdiv(N, kHsRows) * d * 4 : 0));
     w.u_off = align256(w.hsum_off + (r1 ? (size_t)d * 4 : 0));
     w.part_off = align256(w.u_off + (r1 ? (size_t)d * 4 : 0));
-    size_t pw = p.w.splits > 1 ? (size_t)p.w.splits * d * V * 4 : 0;
-    size_t ph = p.h.splits > 1 ? (size_t)p.h.splits * N * d * 4 : 0;
+    // split partials: the rectangle of the tiles that split k (all of them unless outer_dp > 0)
+    const int64_t wcols = std::max<int64_t>(0, V - (int64_t)p.w.outer_dp * LB);
+    const int64_t hrows = std::max<int64_t>(0, N - (int64_t)p.h.outer_dp * LB);
+    size_t pw = p.w.splits > 1 ? (size_t)p.w.splits * d * (p.w.kind == kRank1 && p.w.wide ? wcols : V) * 4 : 0;
+    size_t ph = p.h.splits > 1 ? (size_t)p.h.splits * (p.h.kind == kRank1 && p.h.wide ? hrows : N) * d * 4 : 0;
     w.total = align256(w.part_off + (pw > ph ? pw : ph));
     return w;
 }
@@ -1516,13 +1593,36 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
         float* pz = splits > 1 ? part : nullptr;
         const uint16_t* a16 = static_cast<const uint16_t*>(A);
         const uint16_t* b16 = static_cast<const uint16_t*>(B);
-        if (g.wide && is_dw)
-            hipLaunchKernelGGL((lds256w_kernel<true, float>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
-                               inner, outer, f.scal, rv, cv, reinterpret_cast<float*>(out), ldo, beta, pz);
-        else if (g.wide)
-            hipLaunchKernelGGL((lds256w_kernel<false, TO>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
-                               inner, outer, f.scal, rv, cv, out, ldo, beta, pz);
-        else if (is_dw)
+        if (g.wide) {
+            // whole rounds over the full k range, then the leftover outer tiles with split k
+            const int dp = std::min(g.outer_dp, outer);
+            auto launch = [&](int ob, int oe, int nsplit, int kp, float* pp, const TileRange& tr) {
+                dim3 gr((unsigned)(cdiv((int64_t)(oe - ob) * nsplit, 8) * 8 * inner));
+                if (is_dw)
+                    hipLaunchKernelGGL((lds256w_kernel<true, float>), gr, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K,
+                                       kp, tr, f.scal, rv, cv, reinterpret_cast<float*>(out), ldo, beta, pp);
+                else
+                    hipLaunchKernelGGL((lds256w_kernel<false, TO>), gr, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K,
+                                       kp, tr, f.scal, rv, cv, out, ldo, beta, pp);
+                return hipGetLastError();
+            };
+            if (dp > 0) {
+                const TileRange tr{inner, 0, dp, 1, 0, 0, 0, 0};
+                hipError_t e = launch(0, dp, 1, (int)(cdiv(K, kt) * kt), nullptr, tr);
+                if (e != hipSuccess) return e;
+            }
+            if (dp >= outer) return hipSuccess;
+            const int pm0 = is_dw ? 0 : dp * LB, pn0 = is_dw ? dp * LB : 0;
+            const int64_t ldp = Nn - pn0;
+            const TileRange tr{inner, dp, outer, splits, pm0, pn0, ldp, (int64_t)(M - pm0) * ldp};
+            hipError_t e = launch(dp, outer, splits, kps, pz, tr);
+            if (e != hipSuccess || splits == 1) return e;
+            const int64_t MN = (int64_t)(M - pm0) * ldp;
+            hipLaunchKernelGGL(splitk_rank1_kernel<TO>, dim3((unsigned)cdiv(MN, 256)), dim3(256), 0, st, part, splits, M,
+                               Nn, pm0, pn0, rv, cv, out, ldo, beta);
+            return hipGetLastError();
+        }
+        if (is_dw)
             hipLaunchKernelGGL((lds256_kernel<true, float>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
                                inner, outer, f.scal, rv, cv, reinterpret_cast<float*>(out), ldo, beta, pz);
         else
@@ -1532,7 +1632,7 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
         if (e != hipSuccess || splits == 1) return e;
         const int64_t MN = (int64_t)M * Nn;
         hipLaunchKernelGGL(splitk_rank1_kernel<TO>, dim3((unsigned)cdiv(MN, 256)), dim3(256), 0, st, part, splits, M, Nn,
-                           rv, cv, out, ldo, beta);
+                           0, 0, rv, cv, out, ldo, beta);
         return hipGetLastError();
     }
     const int tb = g.kind == kMfma128 ? MB : SB;

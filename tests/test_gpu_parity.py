@@ -212,6 +212,41 @@ def test_head_vjp_parity(case):
     assert (np.abs(gdw.sum(1)) <= (tol if dtype == "bf16" else 1e-4) * np.abs(gdw).sum(1) + 1e-12).all()
 
 
+# More 256 x 256 output tiles than the chip has compute units: whole rounds run over the full k range
+# and the leftover tiles split k (dW: the last column tiles; dH: the last row tiles), with ragged last
+# tiles in both m and n and a k extent that is not a multiple of the 64-deep k tile.
+ROUND_CASES = [
+    # name, N, d, V; sampled dW columns and dH rows cover whole-round and leftover tiles and the ragged ends
+    ("dW_leftover", 1032, 520, 24000, np.r_[0:40, 21700:21830, 23950:24000], np.r_[0:8, 1024:1032]),
+    ("dH_leftover", 24600, 520, 2056, np.r_[0:16, 2040:2056], np.r_[0:32, 21740:21790, 24570:24600]),
+]
+
+
+@pytest.mark.parametrize("case", ROUND_CASES, ids=[c[0] for c in ROUND_CASES])
+def test_head_vjp_whole_rounds_and_leftovers(case):
+    name, N, d, V, cols, rows = case
+    log(f"[head_vjp] {name} N={N} d={d} V={V}")
+    Hh, Hd, Wh, Wd, Zh, Zd, y, q_prev, t = _vjp_inputs(N, d, V, "bf16", 0.05)
+    yd = torch.from_numpy(y).to(dev())
+    res = bom.bom_residual(Zd, yd)
+    q = torch.from_numpy(q_prev.copy()).to(dev())
+    qh = bom.bom_ema(q, res["s"], B1, t)
+    g = bom.bom_head_vjp(Hd, Wd, res["R"], yd, qh, res["n_valid"], s=res["s"], lam=LAM, want_db=True,
+                         dh_dtype=torch.float32)
+    torch.cuda.synchronize()
+    o = oracle.residual(Zh, y, want_R=False)
+    _, qho = oracle.ema(q_prev, o["s"], f32(B1), t)
+    dW = oracle.dW_cols(Hh, Zh, y, o["row_lse"], qho, o["n_valid"], LAM, cols=cols)
+    dH = oracle.dH_rows(Wh, Zh, y, o["row_lse"], qho, o["n_valid"], LAM, rows=rows)
+    gdw = to_f64(g["dW"])
+    e_dw = rel_fro(gdw[:, cols], dW)
+    e_dh = rel_fro(to_f64(g["dH"])[rows], dH)
+    log(f"    rel err dW={e_dw:.3e} dH={e_dh:.3e}")
+    assert e_dw <= 2e-2 and e_dh <= 2e-2
+    assert np.isfinite(gdw).all() and np.isfinite(to_f64(g["dH"])).all()
+    assert (np.abs(gdw.sum(1)) <= 2e-2 * np.abs(gdw).sum(1) + 1e-12).all()
+
+
 @pytest.mark.parametrize("lam", [0.0, 1.0, 0.25])
 def test_head_vjp_tile256_lambda(lam):
     """Large-tile path at the edges of the mixture: lambda = 0 (plain cross-entropy backward),

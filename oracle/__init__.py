@@ -59,6 +59,8 @@ def _load():
         lib.orc_update_factored.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp, vp, vp, ctypes.c_int, f64, f64,
                                             f64, f64, f64, f64, i64]
         lib.orc_head_forward.argtypes = [vp, i64, i64, vp, i64, vp, vp]
+        lib.orc_clip_factor.argtypes = [vp, vp, i64, f64, f64, f64]
+        lib.orc_clip_factor.restype = f64
         _lib = lib
         return lib
 
@@ -163,11 +165,23 @@ def _segs(segments):
     return off, ln, wd, len(segments)
 
 
+def clip_factor(u, *, h=None, lam=0.5, u_scale=1.0, clip_norm=0.0) -> float:
+    """Global-norm clipping factor of the update numerator: min(1, clip_norm / (||u'|| + 1e-6)); 1 when
+    clip_norm <= 0 (no clipping)."""
+    if clip_norm <= 0:
+        return 1.0
+    u = _f64(u)
+    h = None if h is None else _f64(h)
+    return float(_load().orc_clip_factor(_p(u), _p(h), u.size, float(lam), float(u_scale), float(clip_norm)))
+
+
 def update_dense(theta, v, u, *, lr, beta2, eps, t, segments=None, weight_decay=0.0, h=None, lam=0.5,
-                 u_scale=1.0):
-    """Returns (theta_new, v_new) in fp64; inputs are not modified."""
+                 u_scale=1.0, clip_norm=0.0):
+    """Returns (theta_new, v_new) in fp64; inputs are not modified. clip_norm > 0 scales the numerator
+    by clip_factor (global-norm clipping) before the second moment and the step."""
     theta, v, u = _f64(theta).copy(), _f64(v).copy(), _f64(u)
     h = None if h is None else _f64(h)
+    u_scale = u_scale * clip_factor(u, h=h, lam=lam, u_scale=u_scale, clip_norm=clip_norm)
     off, ln, wd, ns = _segs(segments)
     _load().orc_update_dense(_p(theta), _p(v), _p(u), _p(h), theta.size, _p(off), _p(ln), _p(wd), ns,
                              float(weight_decay), float(lr), float(beta2), float(eps), float(lam), float(u_scale),
@@ -176,10 +190,12 @@ def update_dense(theta, v, u, *, lr, beta2, eps, t, segments=None, weight_decay=
 
 
 def update_factored(theta, Rr, Cc, u, *, lr, beta2, eps, t, block_rows, block_cols, segments=None,
-                    weight_decay=0.0, h=None, lam=0.5, u_scale=1.0):
-    """Returns (theta_new, Rr_new, Cc_new) in fp64; inputs are not modified."""
+                    weight_decay=0.0, h=None, lam=0.5, u_scale=1.0, clip_norm=0.0):
+    """Returns (theta_new, Rr_new, Cc_new) in fp64; inputs are not modified. clip_norm as in
+    update_dense."""
     theta, Rr, Cc, u = _f64(theta).copy(), _f64(Rr).copy(), _f64(Cc).copy(), _f64(u)
     h = None if h is None else _f64(h)
+    u_scale = u_scale * clip_factor(u, h=h, lam=lam, u_scale=u_scale, clip_norm=clip_norm)
     P = theta.size
     nrows = -(-P // block_cols)
     nblocks = -(-nrows // block_rows)

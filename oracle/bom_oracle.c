@@ -30,7 +30,10 @@
  *     logit and residual rows only for valid rows (zero otherwise);
  *   - factored second moment (not in the paper): the Adafactor rank-1
  *     factorisation of the same v over blocks of block_rows x block_cols of
- *     the flat buffer, v_hat_ij = R_i C_j / sum(R) / (1 - beta2^t).
+ *     the flat buffer, v_hat_ij = R_i C_j / sum(R) / (1 - beta2^t);
+ *   - global-norm clipping (a threshold in the paper's protocols, no formula):
+ *     the numerator is scaled by min(1, clip / (||u'|| + 1e-6)) over the whole
+ *     flat buffer, as PyTorch's clip_grad_norm_ does.
  */
 #include <math.h>
 #include <stdint.h>
@@ -249,6 +252,25 @@ static double orc_decay_of(int64_t e, const int64_t* seg_off, const int64_t* seg
 static double orc_numerator(const double* u, const double* h, int64_t e, double lambda, double u_scale) {
     if (h) return u_scale * ((1.0 - lambda) * u[e] + lambda * h[e]);
     return u_scale * u[e];
+}
+
+/*
+ * Global-norm clipping of the update numerator (appendix "Pretraining Parameters" and appendix
+ * "Memory and Timing Protocols": clipping at 1.0; appendix "Conditional Descent and Stationarity":
+ * the numerator supplied to the adaptive update includes the clipping). Returns the factor
+ *   c = min(1, clip_norm / (||u'|| + 1e-6)),
+ * ||u'|| the L2 norm of the numerator of orc_numerator over all P elements (summed in element
+ * order). The clipped numerator c u' then enters both the second moment and the parameter step.
+ * The 1e-6 guard is a reading (PyTorch's clip_grad_norm_); the paper gives only the threshold.
+ */
+double orc_clip_factor(const double* u, const double* h, int64_t P, double lambda, double u_scale, double clip_norm) {
+    double ss = 0.0;
+    for (int64_t e = 0; e < P; ++e) {
+        double up = orc_numerator(u, h, e, lambda, u_scale);
+        ss += up * up;
+    }
+    double c = clip_norm / (sqrt(ss) + 1e-6);
+    return c < 1.0 ? c : 1.0;
 }
 
 /*

@@ -445,6 +445,62 @@ def test_factored_zero_block_keeps_decay_only():
     np.testing.assert_allclose(thf, (1 - 1e-3) * th, rtol=1e-15)
 
 
+# Global-norm clipping of the numerator (appendix "Pretraining Parameters": clipping at 1.0; appendix
+# "Conditional Descent and Stationarity": the numerator supplied to the adaptive update includes it).
+
+def test_clip_factor_constant_vector_closed_form():
+    # u = a 1 over P elements: ||u|| = |a| sqrt(P), so c = min(1, clip / (|a| sqrt(P) + 1e-6)).
+    P, a = 10_000, -3e-3
+    u = np.full(P, a)
+    for clip in (0.05, 0.2, 0.3, 1.0):
+        expect = min(1.0, clip / (abs(a) * math.sqrt(P) + 1e-6))
+        assert abs(oracle.clip_factor(u, clip_norm=clip) - expect) <= 1e-12 * expect   # P summed squares
+    # u_scale enters the norm: the scaled numerator is what is clipped
+    assert abs(oracle.clip_factor(u, u_scale=4.0, clip_norm=0.1) - 0.1 / (4 * abs(a) * 100 + 1e-6)) <= 1e-12
+    assert oracle.clip_factor(u, clip_norm=0.0) == 1.0
+
+
+def test_clip_factor_matches_library_norm_and_split_numerator():
+    r = _rng(33)
+    P = 4099
+    u, h = r.standard_normal(P), r.standard_normal(P)
+    n = np.linalg.norm(0.7 * u)
+    assert abs(oracle.clip_factor(u, u_scale=0.7, clip_norm=1.5) - 1.5 / (n + 1e-6)) <= 1e-13
+    # split mode: the norm is that of the combined numerator (1 - lam) u + lam h, not of u alone
+    lam = 0.25
+    nm = np.linalg.norm((1 - lam) * u + lam * h)
+    assert abs(oracle.clip_factor(u, h=h, lam=lam, clip_norm=2.0) - 2.0 / (nm + 1e-6)) <= 1e-13
+    # a history that cancels the current gradient leaves a zero numerator: nothing to clip
+    assert oracle.clip_factor(u, h=-(1 - lam) / lam * u, lam=lam, clip_norm=1e-3) == 1.0
+
+
+def test_clipped_update_is_update_of_scaled_numerator():
+    # Clipping is one global rescale of the numerator, applied before both the second moment and the
+    # step: the clipped update equals the unclipped update of c u (dense and factored, with an inactive
+    # clip leaving the update unchanged).
+    r = _rng(34)
+    br, bc = 4, 8
+    P = 11 * 8 + 4
+    th, u = r.standard_normal(P), r.standard_normal(P) * 1e-2
+    v0 = np.abs(r.standard_normal(P)) * 1e-4
+    Rr0, Cc0 = np.abs(r.standard_normal(12)) * 1e-3, np.abs(r.standard_normal(3 * bc)) * 1e-3
+    segs = [(0, 40, 0.01)]
+    c = 0.05 / (np.linalg.norm(u) + 1e-6)
+    assert c < 1
+    kw = dict(lr=1e-2, beta2=B2, eps=EPS, t=3, segments=segs, weight_decay=0.1)
+    a = oracle.update_dense(th, v0, u, clip_norm=0.05, **kw)
+    b = oracle.update_dense(th, v0, c * u, **kw)
+    np.testing.assert_allclose(a[0], b[0], rtol=1e-13)
+    np.testing.assert_allclose(a[1], b[1], rtol=1e-12)
+    fa = oracle.update_factored(th, Rr0, Cc0, u, block_rows=br, block_cols=bc, clip_norm=0.05, **kw)
+    fb = oracle.update_factored(th, Rr0, Cc0, c * u, block_rows=br, block_cols=bc, **kw)
+    for x, y in zip(fa, fb):
+        np.testing.assert_allclose(x, y, rtol=1e-12)
+    big = 10 * np.linalg.norm(u)
+    for x, y in zip(oracle.update_dense(th, v0, u, clip_norm=big, **kw), oracle.update_dense(th, v0, u, **kw)):
+        np.testing.assert_array_equal(x, y)
+
+
 # ----------------------------------------------------------------------------- multi-step
 
 def test_linear_model_bom_equals_own_step_control():

@@ -69,8 +69,9 @@ def fill_normal_(t: torch.Tensor, stream: int, std: float, chunk: int = 1 << 27)
 class Problem:
     """Device-resident inputs and state of one workload."""
 
-    def __init__(self, w, dev):
+    def __init__(self, w, dev, clip_norm=0.0):
         self.w = w
+        self.clip_norm = clip_norm
         N, d, V, P = w.N, w.d, w.V, w.P
         std_z = w.logit_std
         t0 = time.time()
@@ -132,15 +133,17 @@ class Problem:
         if ev is not None:
             ev[3].record()
         cfg = bom.make_update_cfg(lr=w.lr, beta2=w.beta2, eps=w.eps, t=t, lam=w.lam, factored=w.factored,
-                                  block_rows=w.block_rows, block_cols=w.block_cols)
+                                  block_rows=w.block_rows, block_cols=w.block_cols, clip_norm=self.clip_norm)
         self.ws_upd = bom.bom_update(self.theta, self.v, self.u, cfg, v_col=self.v_col, segments=self.segments,
                                      workspace=self.ws_upd)
         if ev is not None:
             ev[4].record()
 
 
-def algorithmic(w):
-    """Algorithmic bytes / flops of each stage for one step (what BOM must move or compute)."""
+def algorithmic(w, clip=False):
+    """Algorithmic bytes / flops of each stage for one step (what BOM must move or compute). With
+    global-norm clipping the dense update reads u once more for the norm; the factored update takes
+    the norm from its row statistics (a row-sized array written once and read twice)."""
     esz = 2 if w.dtype == "bf16" else 4
     N, d, V, P = w.N, w.d, w.V, w.P
     out = {
@@ -153,8 +156,12 @@ def algorithmic(w):
     if w.factored:
         nrows = -(-P // w.block_cols)
         nblocks = -(-nrows // w.block_rows)
-        out["bom_update"] = dict(bound="hbm", amount=16 * P + 8 * nrows + 8 * nblocks * w.block_cols,
+        out["bom_update"] = dict(bound="hbm", amount=16 * P + 8 * nrows + 8 * nblocks * w.block_cols
+                                 + (12 * nrows if clip else 0),
                                  per_unit="16 bytes per parameter (read u twice, read+write theta) + factors")
+    elif clip:
+        out["bom_update"] = dict(bound="hbm", amount=24 * P, per_unit="24 bytes per parameter (read u for the norm; "
+                                                                      "read theta, v, u; write theta, v)")
     else:
         out["bom_update"] = dict(bound="hbm", amount=20 * P, per_unit="20 bytes per parameter (read theta, v, u; "
                                                                       "write theta, v)")
@@ -294,6 +301,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=[w.name for w in WORKLOADS])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--clip-norm", type=float, default=0.0,
+                    help="global-norm clipping of the update numerator at this norm (0: none; the paper's "
+                         "language-model protocols clip at 1.0)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="host seconds the oracle baseline aims to spend (a bounded sample of the workload)")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
@@ -321,7 +331,7 @@ def main():
         log(f"[bench] calibration copy of {nbytes} bytes done (3 launches)")
         del src, dst
         torch.cuda.empty_cache()
-    prob = Problem(w, dev)
+    prob = Problem(w, dev, clip_norm=args.clip_norm)
     stages = ["bom_residual", "bom_ema", "bom_head_vjp", "bom_update"]
 
     t = 0
@@ -350,7 +360,7 @@ def main():
                 for i, s in enumerate(stages)}
     log(f"[bench] timed {args.steps} steps: {ms_per_step:.4f} ms/step (wall {wall:.2f}s)")
 
-    alg = algorithmic(w)
+    alg = algorithmic(w, clip=args.clip_norm > 0)
     dom = max(stages, key=lambda s: stage_ms[s])
     a = alg[dom]
     sec = stage_ms[dom] / 1e3
@@ -361,7 +371,8 @@ def main():
     else:
         achieved, peak, unit = a["amount"] / sec / 1e12, FP32_PEAK_TFS, "TFLOP/s"
     roofline = {"bound": a["bound"], "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-                "frac": round(achieved / peak, 4), "traffic": stored_traffic(dom, w.name), "kernel": dom,
+                "frac": round(achieved / peak, 4),
+                "traffic": stored_traffic(dom, w.name) if args.clip_norm == 0 else None, "kernel": dom,
                 "algorithmic_per_launch": a["amount"], "per_unit": a["per_unit"]}
     per_stage = {}
     for s in stages:
@@ -390,7 +401,7 @@ def main():
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "N": w.N, "d": w.d, "V": w.V, "P": w.P, "tokens_per_step": n_valid,
-                   "second_moment": "factored" if w.factored else "dense"},
+                   "second_moment": "factored" if w.factored else "dense", "clip_norm": args.clip_norm},
         "stages": per_stage,
         "roofline": roofline,
     }

@@ -177,10 +177,20 @@ bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, 
  *         nblocks = ceil(ceil(P/block_cols) / block_rows).
  *   segs  HOST array of nsegs (<= BOM_MAX_SEGMENTS) segments inside [0, P), or NULL with nsegs 0.
  *   cfg   HOST struct. The factor 1/(1 - beta2^t) is formed on the host in fp64.
- *   workspace: at least bom_update_workspace_bytes(P, cfg) bytes (0 for the dense layout).
+ *   workspace: at least bom_update_workspace_bytes(P, cfg) bytes (0 for the dense layout without
+ *         clipping), 256-byte aligned.
+ *
+ * Global-norm clipping (cfg->clip_norm > 0; appendix "Pretraining Parameters" and appendix "Memory
+ * and Timing Protocols" clip at 1.0, and appendix "Conditional Descent and Stationarity" counts the
+ * clipping as part of the numerator supplied to the adaptive update): u' above is replaced by c u' with
+ *   c = min(1, clip_norm / (||u'|| + 1e-6)),  ||u'|| the L2 norm of u' over all P elements,
+ * computed on the device (no host synchronisation) and used by both the second moment and the step.
+ * The 1e-6 guard is PyTorch's clip_grad_norm_ (the paper gives only the threshold). Dense layout:
+ * one extra read of u (and h). Factored layout: no extra pass over u (the row statistics give the
+ * norm). cfg->clip_stats, if not NULL, is a device fp32 [2] that receives ||u'|| and c.
  * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_HYPER (beta2 not in [0,1), t < 1, eps <= 0,
- *         lambda not in [0,1], non-finite lr / u_scale / decay), BOM_ERR_ALIAS, BOM_ERR_WORKSPACE,
- *         BOM_ERR_HIP.
+ *         lambda not in [0,1], non-finite lr / u_scale / decay, clip_norm negative or not finite),
+ *         BOM_ERR_ALIAS, BOM_ERR_WORKSPACE, BOM_ERR_HIP.
  * ---------------------------------------------------------------------------------------- */
 typedef struct {
     int64_t offset;
@@ -193,6 +203,8 @@ typedef struct {
     int64_t t;
     int32_t v_layout; /* BOM_V_DENSE or BOM_V_FACTORED */
     int64_t block_rows, block_cols;
+    float clip_norm;   /* > 0: global-norm clipping of the numerator at this norm; 0: none */
+    float* clip_stats; /* device fp32 [2] or NULL: receives ||u'|| before clipping and the factor c */
 } bom_update_cfg;
 
 size_t bom_update_workspace_bytes(int64_t P, const bom_update_cfg* cfg);

@@ -38,7 +38,8 @@ class bom_segment(ctypes.Structure):
 class bom_update_cfg(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float), ("lambda_", ctypes.c_float),
                 ("u_scale", ctypes.c_float), ("t", ctypes.c_int64), ("v_layout", ctypes.c_int32),
-                ("block_rows", ctypes.c_int64), ("block_cols", ctypes.c_int64)]
+                ("block_rows", ctypes.c_int64), ("block_cols", ctypes.c_int64), ("clip_norm", ctypes.c_float),
+                ("clip_stats", ctypes.c_void_p)]
 
 
 def lib_path() -> str:
@@ -196,9 +197,16 @@ def bom_head_vjp(H, W, R, labels, q_hat, n_valid, *, s=None, lam=0.5, ignore_ind
     return dict(dW=dW, db=db, dH=dH, workspace=workspace)
 
 
-def make_update_cfg(*, lr, beta2, eps, t, lam=0.5, u_scale=1.0, factored=False, block_rows=4096, block_cols=4096):
+def make_update_cfg(*, lr, beta2, eps, t, lam=0.5, u_scale=1.0, factored=False, block_rows=4096, block_cols=4096,
+                    clip_norm=0.0, clip_stats=None):
+    """clip_norm > 0 turns on global-norm clipping; clip_stats (a device fp32 tensor of 2) receives the
+    numerator's norm before clipping and the factor."""
+    if clip_stats is not None and (clip_stats.dtype != torch.float32 or not clip_stats.is_cuda or
+                                   clip_stats.numel() < 2 or not clip_stats.is_contiguous()):
+        raise ValueError("clip_stats must be a contiguous device float32 tensor of at least 2 elements")
     return bom_update_cfg(lr, beta2, eps, lam, u_scale, int(t), BOM_V_FACTORED if factored else BOM_V_DENSE,
-                          block_rows, block_cols)
+                          block_rows, block_cols, float(clip_norm),
+                          None if clip_stats is None else clip_stats.data_ptr())
 
 
 def bom_update_workspace_bytes(P: int, cfg: bom_update_cfg) -> int:

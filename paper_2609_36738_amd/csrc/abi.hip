@@ -63,7 +63,7 @@ const char* bom_status_string(bom_status s) {
 
 const char* bom_last_error(void) { return g_last_error; }
 
-int32_t bom_version(void) { return 100; }
+int32_t bom_version(void) { return 200; }
 
 size_t bom_residual_workspace_bytes(int64_t N, int64_t V, bom_dtype z_dt) {
     if (N < 1 || V < 1 || N >= kMaxDim || V >= kMaxDim || !is_dtype(z_dt)) return 0;
@@ -153,9 +153,10 @@ bom_status bom_update(float* theta, float* v, float* v_col, const float* u, cons
         return fail(BOM_ERR_SHAPE, "bom_update: need 0 <= nsegs <= %d and segs when nsegs > 0", BOM_MAX_SEGMENTS);
     const bom_update_cfg& c = *cfg;
     if (!(c.beta2 >= 0.f && c.beta2 < 1.f) || c.t < 1 || !(c.eps > 0.f) || !finite(c.eps) || !finite(c.lr) ||
-        !(c.lambda >= 0.f && c.lambda <= 1.f) || !finite(c.u_scale) || !finite(weight_decay))
+        !(c.lambda >= 0.f && c.lambda <= 1.f) || !finite(c.u_scale) || !finite(weight_decay) ||
+        !(c.clip_norm >= 0.f) || !finite(c.clip_norm))
         return fail(BOM_ERR_HYPER, "bom_update: need beta2 in [0,1), t >= 1, eps > 0, lambda in [0,1], finite lr, "
-                                   "u_scale and weight decay");
+                                   "u_scale and weight decay, and a finite clip_norm >= 0");
     bom::SegTable st{};
     st.n = nsegs;
     st.wd_default = weight_decay;
@@ -177,6 +178,9 @@ bom_status bom_update(float* theta, float* v, float* v_col, const float* u, cons
     sc.lambda = c.lambda;
     sc.u_scale = c.u_scale;
     sc.inv_bc2 = (float)(1.0 / (1.0 - std::pow((double)c.beta2, (double)c.t)));
+    sc.clip_norm = c.clip_norm;
+    sc.clip = nullptr;   // set by the launcher once the clipping pass is enqueued
+    sc.clip_stats = c.clip_norm > 0.f ? c.clip_stats : nullptr;
     const size_t pb = (size_t)P * 4;
     if (overlap(theta, pb, u, pb) || (h && overlap(theta, pb, h, pb)))
         return fail(BOM_ERR_ALIAS, "bom_update: theta must not overlap u or h");
@@ -185,7 +189,14 @@ bom_status bom_update(float* theta, float* v, float* v_col, const float* u, cons
         if (v_col) return fail(BOM_ERR_SHAPE, "bom_update: v_col must be NULL for the dense layout");
         if (overlap(v, pb, theta, pb) || overlap(v, pb, u, pb) || (h && overlap(v, pb, h, pb)))
             return fail(BOM_ERR_ALIAS, "bom_update: v must not overlap theta, u or h");
-        return hip_status(bom::launch_update_dense(theta, v, u, h, P, st, sc, strm), "bom_update");
+        const size_t need_d = bom::update_workspace_bytes(P, cfg);
+        if (need_d > 0) {
+            if (!workspace || ws_bytes < need_d)
+                return fail(BOM_ERR_WORKSPACE, "bom_update: workspace needs %zu bytes, got %zu", need_d, ws_bytes);
+            if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+                return fail(BOM_ERR_WORKSPACE, "bom_update: workspace must be 256-byte aligned");
+        }
+        return hip_status(bom::launch_update_dense(theta, v, u, h, P, st, sc, workspace, strm), "bom_update");
     }
     if (c.v_layout != BOM_V_FACTORED) return fail(BOM_ERR_SHAPE, "bom_update: unknown v_layout %d", c.v_layout);
     if (!v_col) return fail(BOM_ERR_NULL, "bom_update: the factored layout needs v_col");

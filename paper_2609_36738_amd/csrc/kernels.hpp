@@ -53,10 +53,13 @@ struct SegTable {
 };
 struct UpdateScalars {
     float lr, beta2, one_minus_beta2, eps, lambda, u_scale, inv_bc2;
+    float clip_norm;      // > 0: global-norm clipping of the numerator
+    const float* clip;    // device word with the clipping factor (written on the device), or null
+    float* clip_stats;    // optional device [2]: the numerator's norm before clipping and the factor
 };
 size_t update_workspace_bytes(int64_t P, const bom_update_cfg* cfg);
 hipError_t launch_update_dense(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
-                               const UpdateScalars& sc, hipStream_t stream);
+                               UpdateScalars sc, void* ws, hipStream_t stream);
 hipError_t launch_update_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P,
                                   int64_t block_rows, int64_t block_cols, const SegTable& segs,
                                   const UpdateScalars& sc, void* ws, hipStream_t stream);

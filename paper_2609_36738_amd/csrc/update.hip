@@ -6,6 +6,12 @@
 // block_cols columns grouped into blocks of block_rows rows; v_hat_ij = Rr_i Cc_j / sum(Rr) / bc2.
 // Three launches: row/column statistics of u'^2 (one read of u), a per-block finish (Cc and the
 // block sum of Rr), and the parameter update (one more read of u, read + write of theta).
+//
+// Global-norm clipping (clip_norm > 0): u' is scaled by c = min(1, clip_norm / (||u'|| + 1e-6)), the
+// norm over the whole buffer, computed on the device. Dense layout: one extra read of the numerator
+// (per-workgroup fp64 partial sums, one finishing workgroup). Factored layout: no extra pass over u;
+// the statistics kernel keeps the row sums rho_i of u'^2 unclipped, their total is ||u'||^2, and
+// the finish kernels fold c^2 into the updates of Rr and Cc before the parameter step uses c u'.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -29,6 +35,12 @@ __device__ __forceinline__ float numerator(float u, float h, const UpdateScalars
     return sc.u_scale * u;
 }
 
+// The scalars of a parameter step: u_scale times the clipping factor when clipping is on.
+__device__ __forceinline__ UpdateScalars clipped(UpdateScalars sc) {
+    if (sc.clip) sc.u_scale *= *sc.clip;
+    return sc;
+}
+
 __device__ __forceinline__ void adam_style(float& th, float& v, float up, float wd, const UpdateScalars& sc) {
     v = sc.beta2 * v + sc.one_minus_beta2 * (up * up);
     const float vhat = v * sc.inv_bc2;
@@ -44,6 +56,7 @@ __global__ __launch_bounds__(kUpdThreads) void update_dense_vec4_kernel(float* _
                                                                         SegTable segs, UpdateScalars sc) {
     const int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x;
     if (q >= nvec) return;
+    sc = clipped(sc);
     const int64_t e = q * 4;
     f32x4 t4 = ld_stream(theta + e);
     f32x4 v4 = ld_stream(v + e);
@@ -67,6 +80,7 @@ __global__ __launch_bounds__(kUpdThreads) void update_dense_scalar_kernel(float*
                                                                           const float* __restrict__ h, int64_t begin,
                                                                           int64_t end, SegTable segs, UpdateScalars sc) {
     const int64_t stride = (int64_t)gridDim.x * kUpdThreads;
+    sc = clipped(sc);
     for (int64_t e = begin + (int64_t)blockIdx.x * kUpdThreads + threadIdx.x; e < end; e += stride) {
         float t = theta[e], vv = v[e];
         adam_style(t, vv, numerator<SPLIT>(u[e], SPLIT ? h[e] : 0.f, sc), decay_of(e, segs), sc);
@@ -82,7 +96,8 @@ __global__ __launch_bounds__(kUpdThreads) void factored_stats_kernel(const float
                                                                      const float* __restrict__ h, int64_t P,
                                                                      int64_t nrows, int64_t block_rows, int bc,
                                                                      int groups_per_block, float* __restrict__ Rr,
-                                                                     float* __restrict__ kpart, UpdateScalars sc) {
+                                                                     float* __restrict__ kpart, float* __restrict__ rho_out,
+                                                                     UpdateScalars sc) {
     __shared__ float sh[kUpdThreads / kWave];
     const int t = threadIdx.x;
     const int64_t b = blockIdx.x / groups_per_block;
@@ -120,7 +135,8 @@ __global__ __launch_bounds__(kUpdThreads) void factored_stats_kernel(const float
             float r = 0.f;
 #pragma unroll
             for (int w = 0; w < kUpdThreads / kWave; ++w) r += sh[w];
-            Rr[i] = sc.beta2 * Rr[i] + sc.one_minus_beta2 * r;
+            if (rho_out) rho_out[i] = r;   // clipping: Rr is updated once the factor is known
+            else Rr[i] = sc.beta2 * Rr[i] + sc.one_minus_beta2 * r;
         }
         __syncthreads();
     }
@@ -135,9 +151,10 @@ __global__ __launch_bounds__(kUpdThreads) void factored_stats_kernel(const float
 // Per-block finish: Cc_j = beta2 Cc_j + (1-beta2) sum_g kpart[g][j]; rsum[b] = sum of the block's Rr.
 __global__ __launch_bounds__(kUpdThreads) void factored_finish_kernel(const float* __restrict__ kpart,
                                                                       int groups_per_block, int64_t nrows,
-                                                                      int64_t block_rows, int bc, const float* __restrict__ Rr,
+                                                                      int64_t block_rows, int bc, float* __restrict__ Rr,
                                                                       float* __restrict__ Cc, float* __restrict__ rsum,
-                                                                      UpdateScalars sc) {
+                                                                      const float* __restrict__ rho, UpdateScalars sc) {
+    const float c2 = rho ? *sc.clip * *sc.clip : 1.f;   // clipping scales u'^2 by c^2
     __shared__ float sh[kUpdThreads];
     const int64_t b = blockIdx.x;
     const int t = threadIdx.x;
@@ -148,10 +165,13 @@ __global__ __launch_bounds__(kUpdThreads) void factored_finish_kernel(const floa
     for (int j = t; j < bc; j += kUpdThreads) {
         float c = 0.f;
         for (int g = 0; g < ng; ++g) c += kp[(int64_t)g * bc + j];
-        Cc[b * bc + j] = sc.beta2 * Cc[b * bc + j] + sc.one_minus_beta2 * c;
+        Cc[b * bc + j] = sc.beta2 * Cc[b * bc + j] + sc.one_minus_beta2 * (c2 * c);
     }
     float r = 0.f;
-    for (int64_t i = r0 + t; i < r1; i += kUpdThreads) r += Rr[i];
+    for (int64_t i = r0 + t; i < r1; i += kUpdThreads) {
+        if (rho) Rr[i] = sc.beta2 * Rr[i] + sc.one_minus_beta2 * (c2 * rho[i]);
+        r += Rr[i];
+    }
     sh[t] = r;
     __syncthreads();
     for (int o = kUpdThreads / 2; o > 0; o >>= 1) {
@@ -172,6 +192,7 @@ __global__ __launch_bounds__(kUpdThreads) void factored_update_kernel(float* __r
                                                                       const float* __restrict__ rsum, SegTable segs,
                                                                       UpdateScalars sc) {
     const int t = threadIdx.x;
+    sc = clipped(sc);
     const int64_t r0 = (int64_t)blockIdx.x * kFacUpdRows;
     const int64_t r1 = min(r0 + kFacUpdRows, nrows);
     for (int64_t i = r0; i < r1; ++i) {
@@ -223,6 +244,7 @@ __global__ __launch_bounds__(kUpdThreads) void factored_update_rows_kernel(float
     constexpr int BC = NV * 256;
     constexpr int KV = NV / 4;   // 16-byte groups per thread
     const int64_t i = blockIdx.x;
+    sc = clipped(sc);
     const int64_t b = i / block_rows;
     const float rs = rsum[b];
     const float a = rs > 0.f ? Rr[i] / rs * sc.inv_bc2 : 0.f;
@@ -261,7 +283,8 @@ __global__ __launch_bounds__(kUpdThreads) void factored_stats_rows_kernel(const 
                                                                           const float* __restrict__ h, int64_t P,
                                                                           int64_t nrows, int64_t block_rows,
                                                                           int groups_per_block, float* __restrict__ Rr,
-                                                                          float* __restrict__ kpart, UpdateScalars sc) {
+                                                                          float* __restrict__ kpart,
+                                                                          float* __restrict__ rho_out, UpdateScalars sc) {
     constexpr int BC = NV * 256;
     __shared__ f32x4 sh[3][BC / 4];
     const int t = threadIdx.x, l = t % kWave, w = t / kWave;
@@ -295,7 +318,10 @@ __global__ __launch_bounds__(kUpdThreads) void factored_stats_rows_kernel(const 
             rho += (s2[0] + s2[1]) + (s2[2] + s2[3]);
         }
         rho = wave_sum(rho);
-        if (l == 0) Rr[i] = sc.beta2 * Rr[i] + sc.one_minus_beta2 * rho;
+        if (l == 0) {
+            if (rho_out) rho_out[i] = rho;   // clipping: Rr is updated once the factor is known
+            else Rr[i] = sc.beta2 * Rr[i] + sc.one_minus_beta2 * rho;
+        }
     }
     if (w > 0) {
 #pragma unroll
@@ -317,10 +343,12 @@ __global__ __launch_bounds__(kUpdThreads) void factored_stats_rows_kernel(const 
 __global__ __launch_bounds__(kUpdThreads) void factored_finish_cols_kernel(const float* __restrict__ kpart,
                                                                            int groups_per_block, int64_t nrows,
                                                                            int64_t block_rows, int bc, int nchunks,
-                                                                           const float* __restrict__ Rr,
+                                                                           float* __restrict__ Rr,
                                                                            float* __restrict__ Cc,
-                                                                           float* __restrict__ rsum, UpdateScalars sc) {
+                                                                           float* __restrict__ rsum,
+                                                                           const float* __restrict__ rho, UpdateScalars sc) {
     __shared__ float sh[kUpdThreads];
+    const float c2 = rho ? *sc.clip * *sc.clip : 1.f;   // clipping scales u'^2 by c^2
     const int64_t b = blockIdx.x / nchunks;
     const int chunk = blockIdx.x % nchunks;
     const int t = threadIdx.x;
@@ -344,11 +372,14 @@ __global__ __launch_bounds__(kUpdThreads) void factored_finish_cols_kernel(const
         }
         for (; gi < ng; ++gi) c += *reinterpret_cast<const f32x4*>(kp + (int64_t)gi * bc + j);
         f32x4 old = *reinterpret_cast<const f32x4*>(Cc + b * bc + j);
-        *reinterpret_cast<f32x4*>(Cc + b * bc + j) = sc.beta2 * old + sc.one_minus_beta2 * c;
+        *reinterpret_cast<f32x4*>(Cc + b * bc + j) = sc.beta2 * old + sc.one_minus_beta2 * (c2 * c);
     }
     if (chunk != 0) return;
     float r = 0.f;
-    for (int64_t i = r0 + t; i < r1; i += kUpdThreads) r += Rr[i];
+    for (int64_t i = r0 + t; i < r1; i += kUpdThreads) {
+        if (rho) Rr[i] = sc.beta2 * Rr[i] + sc.one_minus_beta2 * (c2 * rho[i]);
+        r += Rr[i];
+    }
     sh[t] = r;
     __syncthreads();
     for (int o = kUpdThreads / 2; o > 0; o >>= 1) {
@@ -358,12 +389,126 @@ __global__ __launch_bounds__(kUpdThreads) void factored_finish_cols_kernel(const
     if (t == 0) rsum[b] = sh[0];
 }
 
+// ---- global-norm clipping ------------------------------------------------------------------
+constexpr int kClipGroups = 2048;  // workgroups of the norm pass (fixed: the sum order is fixed)
+constexpr int kClipUnroll = 4;     // 16-byte groups per thread in flight
+
+// Per-workgroup fp64 partial sums: SQUARE, the sum of squares of the numerator of (u, h) over n
+// elements (16-byte groups when aligned); otherwise the plain sum of n values of u (the row sums of
+// squares kept by the factored statistics kernel).
+template <bool SPLIT, bool SQUARE>
+__global__ __launch_bounds__(kUpdThreads) void clip_partial_kernel(const float* __restrict__ u,
+                                                                   const float* __restrict__ h, int64_t n,
+                                                                   bool vec4, UpdateScalars sc,
+                                                                   double* __restrict__ part) {
+    __shared__ double sh[kUpdThreads / kWave];
+    const int t = threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * kUpdThreads;
+    double acc = 0.0;
+    int64_t done = 0;
+    if (vec4) {
+        const int64_t nvec = n / 4;
+        int64_t q = (int64_t)blockIdx.x * kUpdThreads + t;
+        // kClipUnroll groups per thread in flight, then the remainder one group at a time
+        for (; q + (kClipUnroll - 1) * stride < nvec; q += kClipUnroll * stride) {
+            f32x4 u4[kClipUnroll], h4[kClipUnroll];
+#pragma unroll
+            for (int k = 0; k < kClipUnroll; ++k) {
+                u4[k] = ld_stream(u + (q + k * stride) * 4);
+                h4[k] = SPLIT ? ld_stream(h + (q + k * stride) * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int k = 0; k < kClipUnroll; ++k)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const double x = SQUARE ? (double)numerator<SPLIT>(u4[k][c], h4[k][c], sc) : (double)u4[k][c];
+                    acc += SQUARE ? x * x : x;
+                }
+        }
+        for (; q < nvec; q += stride) {
+            const f32x4 u4 = ld_stream(u + q * 4);
+            f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
+            if (SPLIT) h4 = ld_stream(h + q * 4);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const double x = SQUARE ? (double)numerator<SPLIT>(u4[c], h4[c], sc) : (double)u4[c];
+                acc += SQUARE ? x * x : x;
+            }
+        }
+        done = nvec * 4;
+    }
+    for (int64_t e = done + (int64_t)blockIdx.x * kUpdThreads + t; e < n; e += stride) {
+        const double x = SQUARE ? (double)numerator<SPLIT>(u[e], SPLIT ? h[e] : 0.f, sc) : (double)u[e];
+        acc += SQUARE ? x * x : x;
+    }
+    acc = wave_sum(acc);
+    if (t % kWave == 0) sh[t / kWave] = acc;
+    __syncthreads();
+    if (t == 0) part[blockIdx.x] = ((sh[0] + sh[1]) + sh[2]) + sh[3];
+}
+
+// One workgroup: the total of the partial sums (fixed order), ||u'|| = sqrt(total), and the factor
+// c = min(1, clip_norm / (||u'|| + 1e-6)) written to clip[0] (and, if requested, norm and factor to
+// clip_stats).
+__global__ __launch_bounds__(kUpdThreads) void clip_finish_kernel(const double* __restrict__ part, int nparts,
+                                                                  float* __restrict__ clip, UpdateScalars sc) {
+    __shared__ double sh[kUpdThreads];
+    const int t = threadIdx.x;
+    double a = 0.0;
+    for (int k = t; k < nparts; k += kUpdThreads) a += part[k];
+    sh[t] = a;
+    __syncthreads();
+    for (int o = kUpdThreads / 2; o > 0; o >>= 1) {
+        if (t < o) sh[t] += sh[t + o];
+        __syncthreads();
+    }
+    if (t == 0) {
+        const double norm = sqrt(sh[0]);
+        const double c = (double)sc.clip_norm / (norm + 1e-6);
+        const float cf = c < 1.0 ? (float)c : 1.0f;
+        clip[0] = cf;
+        if (sc.clip_stats) {
+            sc.clip_stats[0] = (float)norm;
+            sc.clip_stats[1] = cf;
+        }
+    }
+}
+
+// Workspace of the clipping pass: fp64 partials, then the factor word.
+struct ClipLayout {
+    size_t part_off, clip_off, total;
+};
+ClipLayout clip_layout(size_t base) {
+    ClipLayout L;
+    L.part_off = align256(base);
+    L.clip_off = align256(L.part_off + (size_t)kClipGroups * sizeof(double));
+    L.total = align256(L.clip_off + 16);
+    return L;
+}
+
+// Norm pass and factor: SQUARE over the numerator (dense), or the plain sum of the row statistics.
+template <bool SPLIT, bool SQUARE>
+hipError_t run_clip(const float* x, const float* h, int64_t n, bool vec4, UpdateScalars& sc, void* ws,
+                    const ClipLayout& L, hipStream_t st) {
+    double* part = reinterpret_cast<double*>(static_cast<char*>(ws) + L.part_off);
+    float* clip = reinterpret_cast<float*>(static_cast<char*>(ws) + L.clip_off);
+    hipLaunchKernelGGL((clip_partial_kernel<SPLIT, SQUARE>), dim3(kClipGroups), dim3(kUpdThreads), 0, st, x, h, n, vec4,
+                       sc, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(clip_finish_kernel, dim3(1), dim3(kUpdThreads), 0, st, part, kClipGroups, clip, sc);
+    sc.clip = clip;
+    return hipGetLastError();
+}
+
 struct FacLayout {
     int64_t nrows, nblocks, groups_per_block, ngroups;
-    size_t kpart_off, rsum_off, total;
+    size_t kpart_off, rsum_off, rho_off;
+    ClipLayout clip;
+    size_t total;
 };
 
-FacLayout fac_layout(int64_t P, int64_t br, int64_t bc) {
+FacLayout fac_layout(int64_t P, int64_t br, int64_t bc, bool clip) {
     FacLayout L;
     L.nrows = (P + bc - 1) / bc;
     L.nblocks = (L.nrows + br - 1) / br;
@@ -371,23 +516,32 @@ FacLayout fac_layout(int64_t P, int64_t br, int64_t bc) {
     L.ngroups = L.nblocks * L.groups_per_block;
     L.kpart_off = 0;
     L.rsum_off = align256((size_t)L.ngroups * (size_t)bc * sizeof(float));
-    L.total = align256(L.rsum_off + (size_t)L.nblocks * sizeof(float));
+    L.rho_off = align256(L.rsum_off + (size_t)L.nblocks * sizeof(float));
+    size_t end = L.rho_off;
+    if (clip) {
+        L.clip = clip_layout(L.rho_off + (size_t)L.nrows * sizeof(float));
+        end = L.clip.total;
+    }
+    L.total = align256(end);
     return L;
 }
 
 template <bool SPLIT, int KC>
 hipError_t run_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P, int64_t br,
-                        int bc, const SegTable& segs, const UpdateScalars& sc, void* ws, hipStream_t st) {
-    const FacLayout L = fac_layout(P, br, bc);
+                        int bc, const SegTable& segs, UpdateScalars sc, void* ws, hipStream_t st) {
+    const bool clip = sc.clip_norm > 0.f;
+    const FacLayout L = fac_layout(P, br, bc, clip);
     float* kpart = reinterpret_cast<float*>(static_cast<char*>(ws) + L.kpart_off);
     float* rsum = reinterpret_cast<float*>(static_cast<char*>(ws) + L.rsum_off);
+    float* rho = clip ? reinterpret_cast<float*>(static_cast<char*>(ws) + L.rho_off) : nullptr;
     // statistics workgroups of the last block beyond its rows simply see an empty row range
     hipLaunchKernelGGL((factored_stats_kernel<SPLIT, KC>), dim3((unsigned)L.ngroups), dim3(kUpdThreads), 0, st, u, h, P,
-                       L.nrows, br, bc, (int)L.groups_per_block, Rr, kpart, sc);
+                       L.nrows, br, bc, (int)L.groups_per_block, Rr, kpart, rho, sc);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (clip && (e = run_clip<false, false>(rho, nullptr, L.nrows, false, sc, ws, L.clip, st)) != hipSuccess) return e;
     hipLaunchKernelGGL(factored_finish_kernel, dim3((unsigned)L.nblocks), dim3(kUpdThreads), 0, st, kpart,
-                       (int)L.groups_per_block, L.nrows, br, bc, Rr, Cc, rsum, sc);
+                       (int)L.groups_per_block, L.nrows, br, bc, Rr, Cc, rsum, rho, sc);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned nupd = (unsigned)((L.nrows + kFacUpdRows - 1) / kFacUpdRows);
@@ -398,18 +552,21 @@ hipError_t run_factored(float* theta, float* Rr, float* Cc, const float* u, cons
 
 template <bool SPLIT, int NV>
 hipError_t run_factored_rows(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P, int64_t br,
-                             const SegTable& segs, const UpdateScalars& sc, void* ws, hipStream_t st) {
+                             const SegTable& segs, UpdateScalars sc, void* ws, hipStream_t st) {
     constexpr int BC = NV * 256;
-    const FacLayout L = fac_layout(P, br, BC);
+    const bool clip = sc.clip_norm > 0.f;
+    const FacLayout L = fac_layout(P, br, BC, clip);
     float* kpart = reinterpret_cast<float*>(static_cast<char*>(ws) + L.kpart_off);
     float* rsum = reinterpret_cast<float*>(static_cast<char*>(ws) + L.rsum_off);
+    float* rho = clip ? reinterpret_cast<float*>(static_cast<char*>(ws) + L.rho_off) : nullptr;
     hipLaunchKernelGGL((factored_stats_rows_kernel<SPLIT, NV>), dim3((unsigned)L.ngroups), dim3(kUpdThreads), 0, st, u, h,
-                       P, L.nrows, br, (int)L.groups_per_block, Rr, kpart, sc);
+                       P, L.nrows, br, (int)L.groups_per_block, Rr, kpart, rho, sc);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (clip && (e = run_clip<false, false>(rho, nullptr, L.nrows, false, sc, ws, L.clip, st)) != hipSuccess) return e;
     const int nchunks = (BC + 1023) / 1024;
     hipLaunchKernelGGL(factored_finish_cols_kernel, dim3((unsigned)(L.nblocks * nchunks)), dim3(kUpdThreads), 0, st,
-                       kpart, (int)L.groups_per_block, L.nrows, br, BC, nchunks, Rr, Cc, rsum, sc);
+                       kpart, (int)L.groups_per_block, L.nrows, br, BC, nchunks, Rr, Cc, rsum, rho, sc);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((factored_update_rows_kernel<SPLIT, NV>), dim3((unsigned)L.nrows), dim3(kUpdThreads), 0, st, theta,
@@ -435,15 +592,23 @@ hipError_t dispatch_factored(float* theta, float* Rr, float* Cc, const float* u,
 }  // namespace
 
 size_t update_workspace_bytes(int64_t P, const bom_update_cfg* cfg) {
-    if (!cfg || cfg->v_layout != BOM_V_FACTORED || cfg->block_rows < 1 || cfg->block_cols < 1 || P < 1) return 0;
-    return fac_layout(P, cfg->block_rows, cfg->block_cols).total;
+    if (!cfg || P < 1) return 0;
+    const bool clip = cfg->clip_norm > 0.f;
+    if (cfg->v_layout != BOM_V_FACTORED) return clip ? clip_layout(0).total : 0;
+    if (cfg->block_rows < 1 || cfg->block_cols < 1) return 0;
+    return fac_layout(P, cfg->block_rows, cfg->block_cols, clip).total;
 }
 
 hipError_t launch_update_dense(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
-                               const UpdateScalars& sc, hipStream_t st) {
+                               UpdateScalars sc, void* ws, hipStream_t st) {
     const bool aligned = (reinterpret_cast<uintptr_t>(theta) % 16 == 0) && (reinterpret_cast<uintptr_t>(v) % 16 == 0) &&
                          (reinterpret_cast<uintptr_t>(u) % 16 == 0) &&
                          (h == nullptr || reinterpret_cast<uintptr_t>(h) % 16 == 0);
+    if (sc.clip_norm > 0.f) {
+        const hipError_t e = h ? run_clip<true, true>(u, h, P, aligned, sc, ws, clip_layout(0), st)
+                               : run_clip<false, true>(u, h, P, aligned, sc, ws, clip_layout(0), st);
+        if (e != hipSuccess) return e;
+    }
     int64_t done = 0;
     if (aligned && P >= 4) {
         const int64_t nvec = P / 4;

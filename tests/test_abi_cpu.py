@@ -113,6 +113,8 @@ def _upd(lib, P=1000, segs=(), wd=0.0, v_col=None, ws=None, wsb=0, h=None, **cfg
     (dict(factored=True), 1), (dict(factored=True, v_col=ctypes.c_void_p(0x400000), block_cols=6), 8),
     (dict(factored=True, v_col=ctypes.c_void_p(0x400000), P=1002), 8),
     (dict(factored=True, v_col=ctypes.c_void_p(0x400000), block_cols=64, block_rows=8), 5),
+    (dict(clip_norm=-1.0), 4), (dict(clip_norm=float("inf")), 4),
+    (dict(clip_norm=1.0), 5),                        # dense clipping needs its workspace
 ])
 def test_update_rejects(lib, kw, code):
     assert _upd(lib, **kw) == code
@@ -128,6 +130,12 @@ def test_update_null_pointers(lib):
 def test_update_workspace_query(lib):
     dense = bom.make_update_cfg(lr=1e-3, beta2=0.999, eps=1e-8, t=1)
     assert lib.bom_update_workspace_bytes(10**6, ctypes.byref(dense)) == 0
+    clipped = bom.make_update_cfg(lr=1e-3, beta2=0.999, eps=1e-8, t=1, clip_norm=1.0)
+    assert lib.bom_update_workspace_bytes(10**6, ctypes.byref(clipped)) > 0
+    fac_c = bom.make_update_cfg(lr=1e-3, beta2=0.999, eps=1e-8, t=1, factored=True, clip_norm=1.0)
+    fac_n = bom.make_update_cfg(lr=1e-3, beta2=0.999, eps=1e-8, t=1, factored=True)
+    assert lib.bom_update_workspace_bytes(1 << 24, ctypes.byref(fac_c)) > lib.bom_update_workspace_bytes(
+        1 << 24, ctypes.byref(fac_n))
     fac = bom.make_update_cfg(lr=1e-3, beta2=0.999, eps=1e-8, t=1, factored=True)
     P = 476 * 4096 * 4096 + 3429 * 4096
     assert lib.bom_update_workspace_bytes(P, ctypes.byref(fac)) > 0

@@ -400,6 +400,71 @@ def test_update_factored_parity(br, bc, P):
         assert rel_fro(to_f64(Rr), Ro) <= 1e-5 and rel_fro(to_f64(Cc), Co) <= 1e-5
 
 
+# Global-norm clipping of the numerator (the device computes the norm; nothing returns to the host).
+# u ~ N(0, 1e-3) over P = 10^6 has a norm near 1, so a threshold of 0.5 clips and 10 does not.
+@pytest.mark.parametrize("clip,split,offset", [(0.5, True, 0), (0.5, False, 1), (10.0, False, 0)],
+                         ids=["active_split_aligned", "active_plain_misaligned", "inactive"])
+def test_update_dense_clip_parity(clip, split, offset):
+    log(f"[update dense clip] clip={clip} split={split} offset={offset}")
+    P = 1_000_003
+    lr = 1e-3
+    segs = [(0, 500_000, 0.01)]
+    th0 = synth.normal_f32(P, synth.STREAM_THETA, 0.02)
+    buf_t = torch.zeros(P + offset, device=dev())
+    buf_v = torch.zeros(P + offset, device=dev())
+    theta, v = buf_t[offset:], buf_v[offset:]
+    theta.copy_(torch.from_numpy(th0))
+    stats = torch.zeros(2, device=dev())
+    tho, vo = th0.astype(np.float64), np.zeros(P)
+    for t in range(1, 4):
+        u = synth.normal_f32(P, synth.STREAM_U + t, 1e-3)
+        h = synth.normal_f32(P, synth.STREAM_SPLIT_H + t, 1e-3) if split else None
+        cfg = bom.make_update_cfg(lr=lr, beta2=B2, eps=EPS, t=t, lam=LAM, clip_norm=clip, clip_stats=stats)
+        bom.bom_update(theta, v, torch.from_numpy(u).to(dev()), cfg, h=None if h is None else torch.from_numpy(h).to(dev()),
+                       segments=segs, weight_decay=0.1)
+        torch.cuda.synchronize()
+        num = u.astype(np.float64) if h is None else (1 - f32(LAM)) * u.astype(np.float64) + f32(LAM) * h
+        c_o = oracle.clip_factor(u, h=h, lam=f32(LAM), clip_norm=clip)
+        norm_g, c_g = stats.cpu().numpy().astype(np.float64)
+        assert abs(norm_g - np.linalg.norm(num)) <= 1e-5 * np.linalg.norm(num)
+        assert abs(c_g - c_o) <= 1e-5 * c_o and (c_o < 1) == (clip < 1)
+        tho, vo = oracle.update_dense(tho, vo, u, lr=f32(lr), beta2=f32(B2), eps=f32(EPS), t=t, h=h, lam=f32(LAM),
+                                      segments=[(a, b, f32(c)) for a, b, c in segs], weight_decay=f32(0.1),
+                                      clip_norm=clip)
+        _check_theta(to_f64(theta), tho, lr, f"dense clip t={t}")
+        vg = to_f64(v)
+        assert (np.abs(vg - vo) <= 1e-5 * vo + 1e-30).all()
+
+
+@pytest.mark.parametrize("br,bc,P,clip", [(4, 4096, 4096 * 9 + 2048, 0.1), (8, 64, 8 * 64 * 3 + 64 * 2 + 16, 0.02)],
+                         ids=["bc4096_rows", "bc64_strips"])
+def test_update_factored_clip_parity(br, bc, P, clip):
+    log(f"[update factored clip] br={br} bc={bc} P={P} clip={clip}")
+    lr = 1e-3
+    nrows = -(-P // bc)
+    nblocks = -(-nrows // br)
+    th0 = synth.normal_f32(P, synth.STREAM_THETA, 0.02)
+    theta = torch.from_numpy(th0.copy()).to(dev())
+    Rr = torch.zeros(nrows, device=dev())
+    Cc = torch.zeros(nblocks * bc, device=dev())
+    stats = torch.zeros(2, device=dev())
+    tho, Ro, Co = th0.astype(np.float64), np.zeros(nrows), np.zeros(nblocks * bc)
+    for t in range(1, 4):
+        u = synth.normal_f32(P, synth.STREAM_U + t, 1e-3)
+        cfg = bom.make_update_cfg(lr=lr, beta2=B2, eps=EPS, t=t, factored=True, block_rows=br, block_cols=bc,
+                                  clip_norm=clip, clip_stats=stats)
+        bom.bom_update(theta, Rr, torch.from_numpy(u).to(dev()), cfg, v_col=Cc, weight_decay=0.1)
+        torch.cuda.synchronize()
+        c_o = oracle.clip_factor(u, clip_norm=clip)
+        norm_g, c_g = stats.cpu().numpy().astype(np.float64)
+        assert c_o < 1 and abs(c_g - c_o) <= 1e-5 * c_o
+        assert abs(norm_g - np.linalg.norm(u.astype(np.float64))) <= 1e-5 * np.linalg.norm(u.astype(np.float64))
+        tho, Ro, Co = oracle.update_factored(tho, Ro, Co, u, lr=f32(lr), beta2=f32(B2), eps=f32(EPS), t=t,
+                                             block_rows=br, block_cols=bc, weight_decay=f32(0.1), clip_norm=clip)
+        _check_theta(to_f64(theta), tho, lr, f"factored clip t={t}")
+        assert rel_fro(to_f64(Rr), Ro) <= 1e-5 and rel_fro(to_f64(Cc), Co) <= 1e-5
+
+
 # ------------------------------------------------------------------------------------------------ loop
 def test_tiny_classifier_20_steps():
     """Ten-class linear softmax classifier (N = 256, d = 128), 20 BOM steps entirely on the GPU

@@ -60,6 +60,7 @@ def _load():
                                             f64, f64, f64, f64, i64]
         lib.orc_head_forward.argtypes = [vp, i64, i64, vp, i64, vp, vp]
         lib.orc_clip_factor.argtypes = [vp, vp, i64, f64, f64, f64]
+        lib.orc_round_bf16.argtypes = [vp, i64, vp]
         lib.orc_clip_factor.restype = f64
         _lib = lib
         return lib
@@ -187,6 +188,27 @@ def update_dense(theta, v, u, *, lr, beta2, eps, t, segments=None, weight_decay=
                              float(weight_decay), float(lr), float(beta2), float(eps), float(lam), float(u_scale),
                              int(t))
     return theta, v
+
+
+def round_bf16(x) -> np.ndarray:
+    """Bit patterns (uint16) of x rounded once from fp64 to the nearest bf16, ties to even."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty(x.shape, np.uint16)
+    _load().orc_round_bf16(_p(x), x.size, out.ctypes.data_as(ctypes.c_void_p))
+    return out
+
+
+def bf16_bits_to_f64(bits) -> np.ndarray:
+    """Exact fp64 images of bf16 bit patterns."""
+    return (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def update_dense_bf16(theta_bits, v_bits, u_bits, *, h_bits=None, **kw):
+    """bf16 storage: the fp64 step (update_dense, same keywords) on the exact images of the bf16
+    inputs, then theta and v rounded once to bf16. Returns their bit patterns."""
+    th, v = update_dense(bf16_bits_to_f64(theta_bits), bf16_bits_to_f64(v_bits), bf16_bits_to_f64(u_bits),
+                         h=None if h_bits is None else bf16_bits_to_f64(h_bits), **kw)
+    return round_bf16(th), round_bf16(v)
 
 
 def update_factored(theta, Rr, Cc, u, *, lr, beta2, eps, t, block_rows, block_cols, segments=None,

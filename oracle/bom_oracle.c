@@ -33,7 +33,10 @@
  *     the flat buffer, v_hat_ij = R_i C_j / sum(R) / (1 - beta2^t);
  *   - global-norm clipping (a threshold in the paper's protocols, no formula):
  *     the numerator is scaled by min(1, clip / (||u'|| + 1e-6)) over the whole
- *     flat buffer, as PyTorch's clip_grad_norm_ does.
+ *     flat buffer, as PyTorch's clip_grad_norm_ does;
+ *   - bf16 state storage: the step is computed on the exact images of the
+ *     bf16 inputs and theta and v are rounded once to bf16 (nearest, ties to
+ *     even) when stored.
  */
 #include <math.h>
 #include <stdint.h>
@@ -341,6 +344,32 @@ void orc_update_factored(double* theta, double* Rr, double* Cc, const double* u,
             }
         }
         free(kappa);
+    }
+}
+
+/*
+ * bf16 storage (appendix "NLP Fine-Tuning Parameters": bf16 parameter and optimizer-state storage,
+ * the task-space EMA kept in fp32). Rounds each fp64 value once to the nearest bf16 (8 significant
+ * bits, ties to even; bf16 has fp32's exponent range, so below 2^-126 the spacing is 2^-133) and
+ * returns its bit pattern. The bf16 step is the fp64 step on the exact fp64 images of the bf16
+ * inputs, with theta and v rounded this way when they are stored.
+ */
+void orc_round_bf16(const double* x, int64_t n, uint16_t* out) {
+    for (int64_t k = 0; k < n; ++k) {
+        double v = x[k], r;
+        if (v == 0.0 || !isfinite(v)) {
+            r = v;
+        } else {
+            int e;
+            frexp(v, &e);                          /* |v| = m 2^e, 0.5 <= m < 1 */
+            int q = e - 8;                         /* spacing of 8 significant bits */
+            if (q < -133) q = -133;                /* subnormal bf16 spacing */
+            r = ldexp(nearbyint(ldexp(v, -q)), q); /* round half to even (default rounding mode) */
+        }
+        float f = (float)r;                        /* exact: r has at most 8 significant bits */
+        uint32_t bits;
+        memcpy(&bits, &f, 4);
+        out[k] = (uint16_t)(bits >> 16);
     }
 }
 

@@ -501,6 +501,39 @@ def test_clipped_update_is_update_of_scaled_numerator():
         np.testing.assert_array_equal(x, y)
 
 
+# bf16 state storage (appendix "NLP Fine-Tuning Parameters": bf16 parameters and optimizer state).
+
+def test_round_bf16_matches_library_conversion_and_ties():
+    import torch
+    r = _rng(35)
+    x = np.concatenate([r.standard_normal(20000) * 10.0 ** r.integers(-30, 30, 20000),
+                        [0.0, -0.0, 1.0, -2.5, 3e38, 1e-39, 2.0 ** -130]]).astype(np.float32)
+    lib = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(oracle.round_bf16(x.astype(np.float64)), lib)
+    # ties go to the even neighbour; exactly representable values and subnormals stay; below half the
+    # smallest subnormal spacing (2^-133) a tie rounds to zero
+    cases = {1 + 2.0 ** -8: 0x3F80, 1 + 3 * 2.0 ** -8: 0x3F82, -(1 + 2.0 ** -8): 0xBF80, 0.5: 0x3F00,
+             2.0 ** -130: 0x0008, 2.0 ** -134: 0x0000, 3 * 2.0 ** -134: 0x0002}
+    got = oracle.round_bf16(np.array(list(cases)))
+    np.testing.assert_array_equal(got, np.array(list(cases.values()), np.uint16))
+    # the fp64 value is rounded once: a value just above a tie rounds up although its fp32 image is the tie
+    assert oracle.round_bf16(np.array([1 + 2.0 ** -8 + 2.0 ** -40]))[0] == 0x3F81
+
+
+def test_bf16_update_first_step_closed_form():
+    # t = 1 on bf16 storage: v_1 = bf16((1 - beta2) u^2), theta_1 = bf16((1 - lr wd) theta - lr u / (|u| + eps)),
+    # with theta and u the exact images of their bf16 patterns.
+    r = _rng(36)
+    P = 3000
+    tb = oracle.round_bf16(r.standard_normal(P) * 0.02)
+    ub = oracle.round_bf16(r.standard_normal(P) * 1e-3)
+    th, u = oracle.bf16_bits_to_f64(tb), oracle.bf16_bits_to_f64(ub)
+    t1, v1 = oracle.update_dense_bf16(tb, np.zeros(P, np.uint16), ub, lr=1e-2, beta2=B2, eps=EPS, t=1,
+                                      weight_decay=0.05)
+    np.testing.assert_array_equal(v1, oracle.round_bf16((1 - B2) * u * u))
+    np.testing.assert_array_equal(t1, oracle.round_bf16((1 - 1e-2 * 0.05) * th - 1e-2 * u / (np.abs(u) + EPS)))
+
+
 # ----------------------------------------------------------------------------- multi-step
 
 def test_linear_model_bom_equals_own_step_control():

@@ -171,8 +171,10 @@ bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, 
  *   Cc_j = beta2 Cc_j + (1-beta2) kappa_j, v_hat_ij = Rr_i Cc_j / sum_{k in block} Rr_k / (1-beta2^t)
  *   (0 when that sum is 0), then the same theta update.
  *
- *   theta device fp32 [P], in place.   u device fp32 [P].   h device fp32 [P] or NULL.
- *   v     dense: device fp32 [P] (in place). factored: Rr, device fp32 [ceil(P/block_cols)].
+ *   theta device [P], in place.   u device [P].   h device [P] or NULL.   Their element type is
+ *         fp32, or bf16 when cfg->state_dt = BOM_BF16 (dense layout only).
+ *   v     dense: device [P] (in place), fp32 or bf16 like theta. factored: Rr, device fp32
+ *         [ceil(P/block_cols)].
  *   v_col dense: NULL. factored: Cc, device fp32 [nblocks * block_cols],
  *         nblocks = ceil(ceil(P/block_cols) / block_rows).
  *   segs  HOST array of nsegs (<= BOM_MAX_SEGMENTS) segments inside [0, P), or NULL with nsegs 0.
@@ -188,9 +190,14 @@ bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, 
  * The 1e-6 guard is PyTorch's clip_grad_norm_ (the paper gives only the threshold). Dense layout:
  * one extra read of u (and h). Factored layout: no extra pass over u (the row statistics give the
  * norm). cfg->clip_stats, if not NULL, is a device fp32 [2] that receives ||u'|| and c.
- * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_HYPER (beta2 not in [0,1), t < 1, eps <= 0,
- *         lambda not in [0,1], non-finite lr / u_scale / decay, clip_norm negative or not finite),
- *         BOM_ERR_ALIAS, BOM_ERR_WORKSPACE, BOM_ERR_HIP.
+ *
+ * bf16 state storage (cfg->state_dt = BOM_BF16; appendix "NLP Fine-Tuning Parameters": bf16 parameter
+ * and optimizer-state storage, the task-space EMA kept in fp32): theta, v, u and h are bf16; the step
+ * is computed in fp32 from their values and theta and v are rounded to the nearest bf16 (ties to
+ * even) when stored: 10 bytes per parameter instead of 20. Dense layout only (factored: BOM_ERR_DTYPE).
+ * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_DTYPE, BOM_ERR_HYPER (beta2 not in [0,1), t < 1,
+ *         eps <= 0, lambda not in [0,1], non-finite lr / u_scale / decay, clip_norm negative or not
+ *         finite), BOM_ERR_ALIAS, BOM_ERR_WORKSPACE, BOM_ERR_HIP.
  * ---------------------------------------------------------------------------------------- */
 typedef struct {
     int64_t offset;
@@ -205,10 +212,11 @@ typedef struct {
     int64_t block_rows, block_cols;
     float clip_norm;   /* > 0: global-norm clipping of the numerator at this norm; 0: none */
     float* clip_stats; /* device fp32 [2] or NULL: receives ||u'|| before clipping and the factor c */
+    int32_t state_dt;  /* BOM_F32, or BOM_BF16: theta, v, u and h stored as bf16 (dense layout) */
 } bom_update_cfg;
 
 size_t bom_update_workspace_bytes(int64_t P, const bom_update_cfg* cfg);
-bom_status bom_update(float* theta, float* v, float* v_col, const float* u, const float* h, int64_t P,
+bom_status bom_update(void* theta, void* v, float* v_col, const void* u, const void* h, int64_t P,
                       const bom_segment* segs, int32_t nsegs, float weight_decay, const bom_update_cfg* cfg,
                       void* workspace, size_t ws_bytes, void* stream);
 

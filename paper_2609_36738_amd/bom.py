@@ -39,7 +39,7 @@ class bom_update_cfg(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float), ("lambda_", ctypes.c_float),
                 ("u_scale", ctypes.c_float), ("t", ctypes.c_int64), ("v_layout", ctypes.c_int32),
                 ("block_rows", ctypes.c_int64), ("block_cols", ctypes.c_int64), ("clip_norm", ctypes.c_float),
-                ("clip_stats", ctypes.c_void_p)]
+                ("clip_stats", ctypes.c_void_p), ("state_dt", ctypes.c_int32)]
 
 
 def lib_path() -> str:
@@ -198,15 +198,19 @@ def bom_head_vjp(H, W, R, labels, q_hat, n_valid, *, s=None, lam=0.5, ignore_ind
 
 
 def make_update_cfg(*, lr, beta2, eps, t, lam=0.5, u_scale=1.0, factored=False, block_rows=4096, block_cols=4096,
-                    clip_norm=0.0, clip_stats=None):
+                    clip_norm=0.0, clip_stats=None, state_dtype=torch.float32):
     """clip_norm > 0 turns on global-norm clipping; clip_stats (a device fp32 tensor of 2) receives the
-    numerator's norm before clipping and the factor."""
+    numerator's norm before clipping and the factor. state_dtype torch.bfloat16 selects bf16 storage
+    of theta, v, u and h (dense layout)."""
+    if state_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("state_dtype must be torch.float32 or torch.bfloat16")
     if clip_stats is not None and (clip_stats.dtype != torch.float32 or not clip_stats.is_cuda or
                                    clip_stats.numel() < 2 or not clip_stats.is_contiguous()):
         raise ValueError("clip_stats must be a contiguous device float32 tensor of at least 2 elements")
     return bom_update_cfg(lr, beta2, eps, lam, u_scale, int(t), BOM_V_FACTORED if factored else BOM_V_DENSE,
                           block_rows, block_cols, float(clip_norm),
-                          None if clip_stats is None else clip_stats.data_ptr())
+                          None if clip_stats is None else clip_stats.data_ptr(),
+                          BOM_BF16 if state_dtype == torch.bfloat16 else BOM_F32)
 
 
 def bom_update_workspace_bytes(P: int, cfg: bom_update_cfg) -> int:
@@ -218,6 +222,10 @@ def bom_update(theta, v, u, cfg: bom_update_cfg, *, v_col=None, h=None, segments
     """theta and v (or the factored Rr = v, Cc = v_col) updated in place; see include/bom.h."""
     lib = load()
     P = theta.numel()
+    want = torch.bfloat16 if cfg.state_dt == BOM_BF16 else torch.float32
+    for name, x in (("theta", theta), ("u", u), ("h", h)) + ((("v", v),) if v_col is None else ()):
+        if x is not None and (x.dtype != want or not x.is_contiguous() or x.numel() != P):
+            raise ValueError(f"{name} must be a contiguous {want} tensor of {P} elements")
     segs = (bom_segment * max(1, len(segments)))(*[bom_segment(int(o), int(n), float(w)) for o, n, w in segments])
     nb = lib.bom_update_workspace_bytes(P, ctypes.byref(cfg))
     workspace = _workspace(nb, theta.device, workspace)

@@ -144,10 +144,10 @@ bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, 
 
 size_t bom_update_workspace_bytes(int64_t P, const bom_update_cfg* cfg) { return bom::update_workspace_bytes(P, cfg); }
 
-bom_status bom_update(float* theta, float* v, float* v_col, const float* u, const float* h, int64_t P,
+bom_status bom_update(void* theta_p, void* v_p, float* v_col, const void* u_p, const void* h_p, int64_t P,
                       const bom_segment* segs, int32_t nsegs, float weight_decay, const bom_update_cfg* cfg,
                       void* workspace, size_t ws_bytes, void* stream) {
-    if (!theta || !v || !u || !cfg) return fail(BOM_ERR_NULL, "bom_update: theta, v, u and cfg are required");
+    if (!theta_p || !v_p || !u_p || !cfg) return fail(BOM_ERR_NULL, "bom_update: theta, v, u and cfg are required");
     if (P < 1) return fail(BOM_ERR_SHAPE, "bom_update: need P >= 1");
     if (nsegs < 0 || nsegs > BOM_MAX_SEGMENTS || (nsegs > 0 && !segs))
         return fail(BOM_ERR_SHAPE, "bom_update: need 0 <= nsegs <= %d and segs when nsegs > 0", BOM_MAX_SEGMENTS);
@@ -181,10 +181,34 @@ bom_status bom_update(float* theta, float* v, float* v_col, const float* u, cons
     sc.clip_norm = c.clip_norm;
     sc.clip = nullptr;   // set by the launcher once the clipping pass is enqueued
     sc.clip_stats = c.clip_norm > 0.f ? c.clip_stats : nullptr;
-    const size_t pb = (size_t)P * 4;
-    if (overlap(theta, pb, u, pb) || (h && overlap(theta, pb, h, pb)))
+    if (c.state_dt != BOM_F32 && c.state_dt != BOM_BF16)
+        return fail(BOM_ERR_DTYPE, "bom_update: state_dt must be BOM_F32 or BOM_BF16");
+    if (c.state_dt == BOM_BF16 && c.v_layout != BOM_V_DENSE)
+        return fail(BOM_ERR_DTYPE, "bom_update: bf16 state storage is implemented for the dense layout only");
+    const size_t pb = (size_t)P * (c.state_dt == BOM_BF16 ? 2 : 4);
+    if (overlap(theta_p, pb, u_p, pb) || (h_p && overlap(theta_p, pb, h_p, pb)))
         return fail(BOM_ERR_ALIAS, "bom_update: theta must not overlap u or h");
     hipStream_t strm = static_cast<hipStream_t>(stream);
+    if (c.state_dt == BOM_BF16) {
+        if (v_col) return fail(BOM_ERR_SHAPE, "bom_update: v_col must be NULL for the dense layout");
+        if (overlap(v_p, pb, theta_p, pb) || overlap(v_p, pb, u_p, pb) || (h_p && overlap(v_p, pb, h_p, pb)))
+            return fail(BOM_ERR_ALIAS, "bom_update: v must not overlap theta, u or h");
+        const size_t need_b = bom::update_workspace_bytes(P, cfg);
+        if (need_b > 0) {
+            if (!workspace || ws_bytes < need_b)
+                return fail(BOM_ERR_WORKSPACE, "bom_update: workspace needs %zu bytes, got %zu", need_b, ws_bytes);
+            if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+                return fail(BOM_ERR_WORKSPACE, "bom_update: workspace must be 256-byte aligned");
+        }
+        return hip_status(bom::launch_update_dense_bf16(static_cast<uint16_t*>(theta_p), static_cast<uint16_t*>(v_p),
+                                                        static_cast<const uint16_t*>(u_p),
+                                                        static_cast<const uint16_t*>(h_p), P, st, sc, workspace, strm),
+                          "bom_update");
+    }
+    float* theta = static_cast<float*>(theta_p);
+    float* v = static_cast<float*>(v_p);
+    const float* u = static_cast<const float*>(u_p);
+    const float* h = static_cast<const float*>(h_p);
     if (c.v_layout == BOM_V_DENSE) {
         if (v_col) return fail(BOM_ERR_SHAPE, "bom_update: v_col must be NULL for the dense layout");
         if (overlap(v, pb, theta, pb) || overlap(v, pb, u, pb) || (h && overlap(v, pb, h, pb)))

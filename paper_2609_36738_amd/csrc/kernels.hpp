@@ -60,6 +60,8 @@ struct UpdateScalars {
 size_t update_workspace_bytes(int64_t P, const bom_update_cfg* cfg);
 hipError_t launch_update_dense(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
                                UpdateScalars sc, void* ws, hipStream_t stream);
+hipError_t launch_update_dense_bf16(uint16_t* theta, uint16_t* v, const uint16_t* u, const uint16_t* h, int64_t P,
+                                    const SegTable& segs, UpdateScalars sc, void* ws, hipStream_t stream);
 hipError_t launch_update_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P,
                                   int64_t block_rows, int64_t block_cols, const SegTable& segs,
                                   const UpdateScalars& sc, void* ws, hipStream_t stream);

@@ -89,6 +89,62 @@ __global__ __launch_bounds__(kUpdThreads) void update_dense_scalar_kernel(float*
     }
 }
 
+// ---- dense, bf16 storage ------------------------------------------------------------------------
+// theta, v, u (and h) stored as bf16 (10 bytes per parameter, 12 with h); the step is computed in fp32
+// from the widened values and theta and v are rounded to nearest-even bf16 when stored. Eight elements
+// (16 bytes of each array) per thread.
+__device__ __forceinline__ float bf16_at(const u32x4_t& x, int c) { return c & 1 ? bf16_hi(x[c / 2]) : bf16_lo(x[c / 2]); }
+
+template <bool SPLIT>
+__global__ __launch_bounds__(kUpdThreads) void update_dense_bf16x8_kernel(uint16_t* __restrict__ theta,
+                                                                          uint16_t* __restrict__ v,
+                                                                          const uint16_t* __restrict__ u,
+                                                                          const uint16_t* __restrict__ h, int64_t nvec,
+                                                                          SegTable segs, UpdateScalars sc) {
+    const int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x;
+    if (q >= nvec) return;
+    sc = clipped(sc);
+    const int64_t e = q * 8;
+    const u32x4_t t8 = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(theta + e));
+    const u32x4_t v8 = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(v + e));
+    const u32x4_t u8 = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(u + e));
+    u32x4_t h8 = {0u, 0u, 0u, 0u};
+    if (SPLIT) h8 = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(h + e));
+    float th[8], vv[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        th[c] = bf16_at(t8, c);
+        vv[c] = bf16_at(v8, c);
+        adam_style(th[c], vv[c], numerator<SPLIT>(bf16_at(u8, c), SPLIT ? bf16_at(h8, c) : 0.f, sc), decay_of(e + c, segs),
+                   sc);
+    }
+    u32x4_t to, vo;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        to[k] = pack_bf16x2(th[2 * k], th[2 * k + 1]);
+        vo[k] = pack_bf16x2(vv[2 * k], vv[2 * k + 1]);
+    }
+    __builtin_nontemporal_store(to, reinterpret_cast<u32x4_t*>(theta + e));
+    __builtin_nontemporal_store(vo, reinterpret_cast<u32x4_t*>(v + e));
+}
+
+template <bool SPLIT>
+__global__ __launch_bounds__(kUpdThreads) void update_dense_bf16_scalar_kernel(uint16_t* __restrict__ theta,
+                                                                               uint16_t* __restrict__ v,
+                                                                               const uint16_t* __restrict__ u,
+                                                                               const uint16_t* __restrict__ h,
+                                                                               int64_t begin, int64_t end, SegTable segs,
+                                                                               UpdateScalars sc) {
+    const int64_t stride = (int64_t)gridDim.x * kUpdThreads;
+    sc = clipped(sc);
+    for (int64_t e = begin + (int64_t)blockIdx.x * kUpdThreads + threadIdx.x; e < end; e += stride) {
+        float t = bf16_to_f32(theta[e]), vv = bf16_to_f32(v[e]);
+        adam_style(t, vv, numerator<SPLIT>(bf16_to_f32(u[e]), SPLIT ? bf16_to_f32(h[e]) : 0.f, sc), decay_of(e, segs), sc);
+        theta[e] = f32_to_bf16(t);
+        v[e] = f32_to_bf16(vv);
+    }
+}
+
 // ---- factored --------------------------------------------------------------------------------
 // Statistics: workgroup w covers rows [r0, r1) of one block; thread t owns columns (k*256 + t)*4..+3.
 template <bool SPLIT, int KC>
@@ -447,6 +503,43 @@ __global__ __launch_bounds__(kUpdThreads) void clip_partial_kernel(const float* 
     if (t == 0) part[blockIdx.x] = ((sh[0] + sh[1]) + sh[2]) + sh[3];
 }
 
+// The same partial sums of squares of the numerator for bf16 storage (eight elements per 16 bytes).
+template <bool SPLIT>
+__global__ __launch_bounds__(kUpdThreads) void clip_partial_bf16_kernel(const uint16_t* __restrict__ u,
+                                                                        const uint16_t* __restrict__ h, int64_t n,
+                                                                        bool vec8, UpdateScalars sc,
+                                                                        double* __restrict__ part) {
+    __shared__ double sh[kUpdThreads / kWave];
+    const int t = threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * kUpdThreads;
+    double acc = 0.0;
+    int64_t done = 0;
+    if (vec8) {
+        const int64_t nvec = n / 8;
+        for (int64_t q = (int64_t)blockIdx.x * kUpdThreads + t; q < nvec; q += stride) {
+            const u32x4_t u8 = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(u + q * 8));
+            u32x4_t h8 = {0u, 0u, 0u, 0u};
+            if (SPLIT) h8 = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(h + q * 8));
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const float uc = c & 1 ? bf16_hi(u8[c / 2]) : bf16_lo(u8[c / 2]);
+                const float hc = c & 1 ? bf16_hi(h8[c / 2]) : bf16_lo(h8[c / 2]);
+                const double x = (double)numerator<SPLIT>(uc, hc, sc);
+                acc += x * x;
+            }
+        }
+        done = nvec * 8;
+    }
+    for (int64_t e = done + (int64_t)blockIdx.x * kUpdThreads + t; e < n; e += stride) {
+        const double x = (double)numerator<SPLIT>(bf16_to_f32(u[e]), SPLIT ? bf16_to_f32(h[e]) : 0.f, sc);
+        acc += x * x;
+    }
+    acc = wave_sum(acc);
+    if (t % kWave == 0) sh[t / kWave] = acc;
+    __syncthreads();
+    if (t == 0) part[blockIdx.x] = ((sh[0] + sh[1]) + sh[2]) + sh[3];
+}
+
 // One workgroup: the total of the partial sums (fixed order), ||u'|| = sqrt(total), and the factor
 // c = min(1, clip_norm / (||u'|| + 1e-6)) written to clip[0] (and, if requested, norm and factor to
 // clip_stats).
@@ -632,6 +725,54 @@ hipError_t launch_update_dense(float* theta, float* v, const float* u, const flo
         else
             hipLaunchKernelGGL(update_dense_scalar_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta,
                                v, u, h, done, P, segs, sc);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_update_dense_bf16(uint16_t* theta, uint16_t* v, const uint16_t* u, const uint16_t* h, int64_t P,
+                                    const SegTable& segs, UpdateScalars sc, void* ws, hipStream_t st) {
+    auto al = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
+    const bool aligned = al(theta) && al(v) && al(u) && (h == nullptr || al(h));
+    if (sc.clip_norm > 0.f) {
+        const ClipLayout L = clip_layout(0);
+        double* part = reinterpret_cast<double*>(static_cast<char*>(ws) + L.part_off);
+        float* clip = reinterpret_cast<float*>(static_cast<char*>(ws) + L.clip_off);
+        if (h)
+            hipLaunchKernelGGL(clip_partial_bf16_kernel<true>, dim3(kClipGroups), dim3(kUpdThreads), 0, st, u, h, P,
+                               aligned, sc, part);
+        else
+            hipLaunchKernelGGL(clip_partial_bf16_kernel<false>, dim3(kClipGroups), dim3(kUpdThreads), 0, st, u, h, P,
+                               aligned, sc, part);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(clip_finish_kernel, dim3(1), dim3(kUpdThreads), 0, st, part, kClipGroups, clip, sc);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        sc.clip = clip;
+    }
+    int64_t done = 0;
+    if (aligned && P >= 8) {
+        const int64_t nvec = P / 8;
+        const int64_t grid = (nvec + kUpdThreads - 1) / kUpdThreads;
+        if (h)
+            hipLaunchKernelGGL(update_dense_bf16x8_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
+                               u, h, nvec, segs, sc);
+        else
+            hipLaunchKernelGGL(update_dense_bf16x8_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
+                               u, h, nvec, segs, sc);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        done = nvec * 8;
+    }
+    if (done < P) {
+        int64_t grid = (P - done + kUpdThreads - 1) / kUpdThreads;
+        if (grid > 8192) grid = 8192;
+        if (h)
+            hipLaunchKernelGGL(update_dense_bf16_scalar_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st,
+                               theta, v, u, h, done, P, segs, sc);
+        else
+            hipLaunchKernelGGL(update_dense_bf16_scalar_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st,
+                               theta, v, u, h, done, P, segs, sc);
         return hipGetLastError();
     }
     return hipSuccess;

@@ -465,6 +465,66 @@ def test_update_factored_clip_parity(br, bc, P, clip):
         assert rel_fro(to_f64(Rr), Ro) <= 1e-5 and rel_fro(to_f64(Cc), Co) <= 1e-5
 
 
+def _bf16_dev(bits, offset=0):
+    buf = torch.zeros(bits.size + offset, dtype=torch.bfloat16, device=dev())
+    out = buf[offset:]
+    out.copy_(torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16))
+    return out
+
+
+def _bits(t):
+    return t.cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def _check_bf16(g, o, name, min_exact=0.999, floor=None):
+    """bf16 results against the oracle's once-rounded fp64 step: at most one bf16 step apart (the kernel
+    rounds its fp32 result, the oracle its fp64 result, so a value within an fp32 rounding of a bf16
+    midpoint may land on the other side), and bitwise equal almost everywhere. `floor` bounds the
+    absolute fp32 error of results formed by cancellation (theta - step near zero), where it can
+    exceed one bf16 step of the tiny result."""
+    gi, oi = g.astype(np.int32), o.astype(np.int32)
+    same_sign = (gi >> 15) == (oi >> 15)
+    ok = same_sign & (np.abs(gi - oi) <= 1) | ((gi & 0x7FFF) == 0) & ((oi & 0x7FFF) <= 1)
+    if floor is not None:
+        ok |= np.abs(oracle.bf16_bits_to_f64(g) - oracle.bf16_bits_to_f64(o)) <= floor
+    if not ok.all():
+        bad = np.flatnonzero(~ok)[:8]
+        gv, ov = oracle.bf16_bits_to_f64(g[bad]), oracle.bf16_bits_to_f64(o[bad])
+        raise AssertionError(f"{name}: {(~ok).sum()} elements beyond one bf16 step, e.g. "
+                             + ", ".join(f"[{i}] gpu {a:.6e} ({x:#06x}) oracle {b:.6e} ({y:#06x})"
+                                         for i, a, b, x, y in zip(bad, gv, ov, g[bad], o[bad])))
+    assert (gi == oi).mean() >= min_exact, f"{name}: bitwise-equal fraction {(gi == oi).mean():.5f}"
+
+
+# bf16 state storage (theta, v, u, h bf16; fp32 arithmetic; theta and v rounded to nearest-even bf16).
+@pytest.mark.parametrize("split,offset,clip", [(False, 0, 0.0), (True, 1, 0.0), (False, 0, 0.5)],
+                         ids=["plain_aligned", "split_misaligned", "clipped"])
+def test_update_dense_bf16_parity(split, offset, clip):
+    log(f"[update dense bf16] split={split} offset={offset} clip={clip}")
+    P = 1_000_003
+    lr = 1e-3
+    segs = [(0, 500_000, 0.01), (500_000, 3, 0.0)]
+    tb = oracle.round_bf16(synth.normal_f32(P, synth.STREAM_THETA, 0.02).astype(np.float64))
+    vb = np.zeros(P, np.uint16)
+    theta, v = _bf16_dev(tb, offset), _bf16_dev(vb, offset)
+    for t in range(1, 4):
+        ub = oracle.round_bf16(synth.normal_f32(P, synth.STREAM_U + t, 1e-3).astype(np.float64))
+        hb = oracle.round_bf16(synth.normal_f32(P, synth.STREAM_SPLIT_H + t, 1e-3).astype(np.float64)) if split else None
+        cfg = bom.make_update_cfg(lr=lr, beta2=B2, eps=EPS, t=t, lam=LAM, clip_norm=clip, state_dtype=torch.bfloat16)
+        bom.bom_update(theta, v, _bf16_dev(ub, offset), cfg, h=None if hb is None else _bf16_dev(hb, offset),
+                       segments=segs, weight_decay=0.1)
+        torch.cuda.synchronize()
+        # fp32 absolute error of theta - step: a few units of 2^-24 of the operands (theta and lr * ratio)
+        floor = 1e-6 * (np.abs(oracle.bf16_bits_to_f64(tb)) + lr)
+        tb, vb = oracle.update_dense_bf16(tb, vb, ub, h_bits=hb, lr=f32(lr), beta2=f32(B2), eps=f32(EPS), t=t,
+                                          lam=f32(LAM), segments=[(a, b, f32(c)) for a, b, c in segs],
+                                          weight_decay=f32(0.1), clip_norm=clip)
+        _check_bf16(_bits(theta), tb, f"theta t={t}", floor=floor)
+        _check_bf16(_bits(v), vb, f"v t={t}")
+        # teacher forcing: the next step starts from the GPU's own state
+        tb, vb = _bits(theta), _bits(v)
+
+
 # ------------------------------------------------------------------------------------------------ loop
 def test_tiny_classifier_20_steps():
     """Ten-class linear softmax classifier (N = 256, d = 128), 20 BOM steps entirely on the GPU

@@ -57,7 +57,8 @@ def bf16_dev(bits: np.ndarray, shape, dev):
 
 
 def fill_normal_(t: torch.Tensor, stream: int, std: float, chunk: int = 1 << 27):
-    """Fill a flat fp32 device tensor from the seeded generator, chunk by chunk (bounded host memory)."""
+    """Fill a flat device tensor from the seeded generator (fp32 values, rounded to nearest-even on the copy
+    into a bf16 tensor), chunk by chunk (bounded host memory)."""
     n = t.numel()
     host = np.empty(min(chunk, n), np.float32)
     for start in range(0, n, chunk):
@@ -69,9 +70,10 @@ def fill_normal_(t: torch.Tensor, stream: int, std: float, chunk: int = 1 << 27)
 class Problem:
     """Device-resident inputs and state of one workload."""
 
-    def __init__(self, w, dev, clip_norm=0.0):
+    def __init__(self, w, dev, clip_norm=0.0, state_dtype=torch.float32):
         self.w = w
         self.clip_norm = clip_norm
+        self.state_dtype = state_dtype
         N, d, V, P = w.N, w.d, w.V, w.P
         std_z = w.logit_std
         t0 = time.time()
@@ -86,11 +88,11 @@ class Problem:
         y = synth.labels_uniform(N, V) if w.labels == "uniform" else synth.labels_zipf(N, V)
         self.labels = torch.from_numpy(y).to(dev)
         self.R = torch.empty((N, V), dtype=self.Z.dtype, device=dev)
-        self.theta = torch.empty(P, dtype=torch.float32, device=dev)
+        self.theta = torch.empty(P, dtype=state_dtype, device=dev)
         fill_normal_(self.theta, synth.STREAM_THETA, 0.02)
         if w.dtype == "f32":
             self.theta[d * V:d * V + V].zero_()   # bias starts at 0
-        self.u = torch.empty(P, dtype=torch.float32, device=dev)
+        self.u = torch.empty(P, dtype=state_dtype, device=dev)
         fill_normal_(self.u, synth.STREAM_U + 1, 1e-3)
         if w.factored:
             nrows = -(-P // w.block_cols)
@@ -98,7 +100,7 @@ class Problem:
             self.v = torch.zeros(nrows, dtype=torch.float32, device=dev)
             self.v_col = torch.zeros(nblocks * w.block_cols, dtype=torch.float32, device=dev)
         else:
-            self.v = torch.zeros(P, dtype=torch.float32, device=dev)
+            self.v = torch.zeros(P, dtype=state_dtype, device=dev)
             self.v_col = None
         self.q = torch.zeros(V, dtype=torch.float32, device=dev)
         self.q_hat = torch.empty(V, dtype=torch.float32, device=dev)
@@ -133,14 +135,15 @@ class Problem:
         if ev is not None:
             ev[3].record()
         cfg = bom.make_update_cfg(lr=w.lr, beta2=w.beta2, eps=w.eps, t=t, lam=w.lam, factored=w.factored,
-                                  block_rows=w.block_rows, block_cols=w.block_cols, clip_norm=self.clip_norm)
+                                  block_rows=w.block_rows, block_cols=w.block_cols, clip_norm=self.clip_norm,
+                                  state_dtype=self.state_dtype)
         self.ws_upd = bom.bom_update(self.theta, self.v, self.u, cfg, v_col=self.v_col, segments=self.segments,
                                      workspace=self.ws_upd)
         if ev is not None:
             ev[4].record()
 
 
-def algorithmic(w, clip=False):
+def algorithmic(w, clip=False, bf16_state=False):
     """Algorithmic bytes / flops of each stage for one step (what BOM must move or compute). With
     global-norm clipping the dense update reads u once more for the norm; the factored update takes
     the norm from its row statistics (a row-sized array written once and read twice)."""
@@ -159,6 +162,10 @@ def algorithmic(w, clip=False):
         out["bom_update"] = dict(bound="hbm", amount=16 * P + 8 * nrows + 8 * nblocks * w.block_cols
                                  + (12 * nrows if clip else 0),
                                  per_unit="16 bytes per parameter (read u twice, read+write theta) + factors")
+    elif bf16_state:
+        out["bom_update"] = dict(bound="hbm", amount=(12 if clip else 10) * P,
+                                 per_unit=f"{12 if clip else 10} bytes per parameter (bf16 storage: "
+                                          f"{'read u for the norm; ' if clip else ''}read theta, v, u; write theta, v)")
     elif clip:
         out["bom_update"] = dict(bound="hbm", amount=24 * P, per_unit="24 bytes per parameter (read u for the norm; "
                                                                       "read theta, v, u; write theta, v)")
@@ -301,6 +308,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=[w.name for w in WORKLOADS])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--state-dtype", choices=["f32", "bf16"], default="f32",
+                    help="storage of theta, v and u (bf16: the paper's fine-tuning protocol; dense layout, bf16 "
+                         "logits only)")
     ap.add_argument("--clip-norm", type=float, default=0.0,
                     help="global-norm clipping of the update numerator at this norm (0: none; the paper's "
                          "language-model protocols clip at 1.0)")
@@ -331,7 +341,11 @@ def main():
         log(f"[bench] calibration copy of {nbytes} bytes done (3 launches)")
         del src, dst
         torch.cuda.empty_cache()
-    prob = Problem(w, dev, clip_norm=args.clip_norm)
+    state_dtype = torch.bfloat16 if args.state_dtype == "bf16" else torch.float32
+    if state_dtype == torch.bfloat16 and (w.factored or w.dtype != "bf16"):
+        print("bf16 state storage applies to the dense layout with bf16 logits", file=sys.stderr)
+        sys.exit(2)
+    prob = Problem(w, dev, clip_norm=args.clip_norm, state_dtype=state_dtype)
     stages = ["bom_residual", "bom_ema", "bom_head_vjp", "bom_update"]
 
     t = 0
@@ -360,7 +374,7 @@ def main():
                 for i, s in enumerate(stages)}
     log(f"[bench] timed {args.steps} steps: {ms_per_step:.4f} ms/step (wall {wall:.2f}s)")
 
-    alg = algorithmic(w, clip=args.clip_norm > 0)
+    alg = algorithmic(w, clip=args.clip_norm > 0, bf16_state=state_dtype == torch.bfloat16)
     dom = max(stages, key=lambda s: stage_ms[s])
     a = alg[dom]
     sec = stage_ms[dom] / 1e3
@@ -372,7 +386,8 @@ def main():
         achieved, peak, unit = a["amount"] / sec / 1e12, FP32_PEAK_TFS, "TFLOP/s"
     roofline = {"bound": a["bound"], "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                 "frac": round(achieved / peak, 4),
-                "traffic": stored_traffic(dom, w.name) if args.clip_norm == 0 else None, "kernel": dom,
+                "traffic": stored_traffic(dom, w.name) if args.clip_norm == 0 and args.state_dtype == "f32" else None,
+                "kernel": dom,
                 "algorithmic_per_launch": a["amount"], "per_unit": a["per_unit"]}
     per_stage = {}
     for s in stages:
@@ -401,7 +416,8 @@ def main():
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "N": w.N, "d": w.d, "V": w.V, "P": w.P, "tokens_per_step": n_valid,
-                   "second_moment": "factored" if w.factored else "dense", "clip_norm": args.clip_norm},
+                   "second_moment": "factored" if w.factored else "dense", "clip_norm": args.clip_norm,
+                   "state_dtype": args.state_dtype},
         "stages": per_stage,
         "roofline": roofline,
     }

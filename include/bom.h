@@ -122,8 +122,8 @@ bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, 
  * For the linear head z_i = W^T h_i (+ b), the gradient of L_mix with respect to the logits is
  *   G_ij = [i in I] ((1 - lambda) R_ij + lambda q_hat_j) / N_t        (q_hat held constant)
  * and the head products are
- *   dW = H^T G + dW_beta * dW     [d, V] fp32 (dW_beta = 0 overwrites; dW is not read then)
- *   db = (1 - lambda) s + lambda q_hat   [V] fp32  (bias Jacobian = identity; equals 1^T G)
+ *   dW = H^T G + dW_beta * dW     [d, V] (dW_beta = 0 overwrites; dW is not read then)
+ *   db = (1 - lambda) s + lambda q_hat   [V]  (bias Jacobian = identity; equals 1^T G)
  *   dH = G W^T                     [N, d] of dh_dt
  * G is never written to memory. bf16 products use the equal rank-1 form
  *   dW = alpha H^T R + (sum_{i in I} H_i) (lambda q_hat / N_t)^T
@@ -141,19 +141,21 @@ bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, 
  *   labels device int32 [N] (defines I with ignore_index, as in bom_residual).
  *   q_hat device fp32 [V].   s device fp32 [V] (only read when db != NULL).
  *   n_valid device int32 [1].
- *   dW  device fp32 [d, lddw]; lddw >= V.   db device fp32 [V] or NULL.
+ *   dW  device [d, lddw] of dw_dt; lddw >= V.   db device [V] of dw_dt, or NULL.
+ *   dw_dt BOM_F32, or BOM_BF16 for bf16 gradient storage (dW, db formed in fp32 in the workspace, then
+ *       rounded to nearest-even bf16: dW = bf16(H^T G + dW_beta * dW)).
  *   dH  device [N, lddh] of dh_dt (BOM_BF16 or BOM_F32), or NULL.
- *   workspace: at least bom_head_vjp_workspace_bytes(N, d, V, dt) bytes (may be 0).
+ *   workspace: at least bom_head_vjp_workspace_bytes(N, d, V, dt, dw_dt) bytes (may be 0).
  * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_DTYPE, BOM_ERR_HYPER (lambda not in [0,1]),
  *         BOM_ERR_WORKSPACE, BOM_ERR_HIP.
  * ---------------------------------------------------------------------------------------- */
-size_t bom_head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt);
+size_t bom_head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt, bom_dtype dw_dt);
 bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* R, int64_t ldr,
                         bom_dtype dt, int64_t N, int64_t d, int64_t V,
                         const int32_t* labels, int32_t ignore_index,
                         const float* q_hat, const float* s, const int32_t* n_valid, float lambda,
-                        float* dW, int64_t lddw, float dW_beta,
-                        float* db, void* dH, bom_dtype dh_dt, int64_t lddh,
+                        void* dW, bom_dtype dw_dt, int64_t lddw, float dW_beta,
+                        void* db, void* dH, bom_dtype dh_dt, int64_t lddh,
                         void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------------

@@ -71,10 +71,10 @@ def load(build_if_missing: bool = True):
         lib.bom_ema.restype = ctypes.c_int
         lib.bom_ema.argtypes = [vp, vp, i64, f32, i64, vp, vp]
         lib.bom_head_vjp_workspace_bytes.restype = sz
-        lib.bom_head_vjp_workspace_bytes.argtypes = [i64, i64, i64, ctypes.c_int]
+        lib.bom_head_vjp_workspace_bytes.argtypes = [i64, i64, i64, ctypes.c_int, ctypes.c_int]
         lib.bom_head_vjp.restype = ctypes.c_int
         lib.bom_head_vjp.argtypes = [vp, i64, vp, i64, vp, i64, ctypes.c_int, i64, i64, i64, vp, i32, vp, vp, vp, f32,
-                                     vp, i64, f32, vp, vp, ctypes.c_int, i64, vp, sz, vp]
+                                     vp, ctypes.c_int, i64, f32, vp, vp, ctypes.c_int, i64, vp, sz, vp]
         lib.bom_update_workspace_bytes.restype = sz
         lib.bom_update_workspace_bytes.argtypes = [i64, ctypes.POINTER(bom_update_cfg)]
         lib.bom_update.restype = ctypes.c_int
@@ -165,8 +165,8 @@ def bom_ema(q, s, beta1: float, t: int, q_hat=None, stream=None):
     return q_hat
 
 
-def bom_head_vjp_workspace_bytes(N: int, d: int, V: int, dt: int) -> int:
-    return load().bom_head_vjp_workspace_bytes(N, d, V, dt)
+def bom_head_vjp_workspace_bytes(N: int, d: int, V: int, dt: int, dw_dt: int = BOM_F32) -> int:
+    return load().bom_head_vjp_workspace_bytes(N, d, V, dt, dw_dt)
 
 
 def bom_head_vjp(H, W, R, labels, q_hat, n_valid, *, s=None, lam=0.5, ignore_index=-100, dW=None, dW_beta=0.0,
@@ -182,16 +182,20 @@ def bom_head_vjp(H, W, R, labels, q_hat, n_valid, *, s=None, lam=0.5, ignore_ind
     ldh, ldw, ldr = _rowmajor(H, "H"), _rowmajor(W, "W"), _rowmajor(R, "R")
     dW = torch.empty((d, V), dtype=torch.float32, device=dev) if dW is None else dW
     lddw = _rowmajor(dW, "dW")
+    dw_dt = _dtype_code(dW)
     if want_db and db is None:
-        db = torch.empty(V, dtype=torch.float32, device=dev)
+        db = torch.empty(V, dtype=dW.dtype, device=dev)
+    if db is not None and db.dtype != dW.dtype:
+        raise TypeError("db must have dW's dtype")
     if want_dH and dH is None:
         dH = torch.empty((N, d), dtype=dh_dtype or H.dtype, device=dev)
     dh_dt = _dtype_code(dH) if dH is not None else BOM_F32
     lddh = _rowmajor(dH, "dH") if dH is not None else d
-    nb = lib.bom_head_vjp_workspace_bytes(N, d, V, dt)
+    nb = lib.bom_head_vjp_workspace_bytes(N, d, V, dt, dw_dt)
     workspace = _workspace(nb, dev, workspace)
     _check(lib.bom_head_vjp(_ptr(H), ldh, _ptr(W), ldw, _ptr(R), ldr, dt, N, d, V, _ptr(labels), ignore_index,
-                            _ptr(q_hat), _ptr(s), _ptr(n_valid), float(lam), _ptr(dW), lddw, float(dW_beta), _ptr(db),
+                            _ptr(q_hat), _ptr(s), _ptr(n_valid), float(lam), _ptr(dW), dw_dt, lddw, float(dW_beta),
+                            _ptr(db),
                             _ptr(dH), dh_dt, lddh, _ptr(workspace), 0 if workspace is None else workspace.numel(),
                             _stream(stream)))
     return dict(dW=dW, db=db, dH=dH, workspace=workspace)

@@ -110,16 +110,17 @@ bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, 
     return hip_status(bom::launch_ema(q, s, V, beta1, inv_bc1, q_hat, static_cast<hipStream_t>(stream)), "bom_ema");
 }
 
-size_t bom_head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
-    if (N < 1 || d < 1 || V < 1 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim || !is_dtype(dt)) return 0;
-    return bom::head_vjp_workspace_bytes(N, d, V, dt);
+size_t bom_head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt, bom_dtype dw_dt) {
+    if (N < 1 || d < 1 || V < 1 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim || !is_dtype(dt) || !is_dtype(dw_dt))
+        return 0;
+    return bom::head_vjp_workspace_bytes(N, d, V, dt, dw_dt);
 }
 
 bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* R, int64_t ldr,
                         bom_dtype dt, int64_t N, int64_t d, int64_t V, const int32_t* labels, int32_t ignore_index,
-                        const float* q_hat, const float* s, const int32_t* n_valid, float lambda, float* dW,
-                        int64_t lddw, float dW_beta, float* db, void* dH, bom_dtype dh_dt, int64_t lddh,
-                        void* workspace, size_t ws_bytes, void* stream) {
+                        const float* q_hat, const float* s, const int32_t* n_valid, float lambda, void* dW,
+                        bom_dtype dw_dt, int64_t lddw, float dW_beta, void* db, void* dH, bom_dtype dh_dt,
+                        int64_t lddh, void* workspace, size_t ws_bytes, void* stream) {
     if (!H || !W || !R || !labels || !q_hat || !n_valid || !dW)
         return fail(BOM_ERR_NULL, "bom_head_vjp: H, W, R, labels, q_hat, n_valid and dW are required");
     if (db && !s) return fail(BOM_ERR_NULL, "bom_head_vjp: s is required when db is requested");
@@ -129,16 +130,17 @@ bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, 
         return fail(BOM_ERR_SHAPE, "bom_head_vjp: a leading dimension is smaller than its row length");
     if ((int64_t)d * V >= ((int64_t)1 << 40) || (int64_t)N * d >= ((int64_t)1 << 40))
         return fail(BOM_ERR_SHAPE, "bom_head_vjp: output too large");
-    if (!is_dtype(dt) || (dH && !is_dtype(dh_dt))) return fail(BOM_ERR_DTYPE, "bom_head_vjp: unsupported dtype");
+    if (!is_dtype(dt) || !is_dtype(dw_dt) || (dH && !is_dtype(dh_dt)))
+        return fail(BOM_ERR_DTYPE, "bom_head_vjp: unsupported dtype");
     if (!(lambda >= 0.f && lambda <= 1.f)) return fail(BOM_ERR_HYPER, "bom_head_vjp: need lambda in [0, 1]");
     if (!finite(dW_beta)) return fail(BOM_ERR_HYPER, "bom_head_vjp: dW_beta must be finite");
-    const size_t need = bom::head_vjp_workspace_bytes(N, d, V, dt);
+    const size_t need = bom::head_vjp_workspace_bytes(N, d, V, dt, dw_dt);
     if (need > 0 && (!workspace || ws_bytes < need))
         return fail(BOM_ERR_WORKSPACE, "bom_head_vjp: workspace needs %zu bytes, got %zu", need, ws_bytes);
     if (workspace && reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
         return fail(BOM_ERR_WORKSPACE, "bom_head_vjp: workspace must be 256-byte aligned");
     bom::HeadVjpArgs a{H, ldh, W, ldw, R, ldr, dt, (int)N, (int)d, (int)V, labels, ignore_index, q_hat, s, n_valid, lambda,
-                       dW, lddw, dW_beta, db, dH, dh_dt, lddh, workspace, ws_bytes};
+                       dW, dw_dt, lddw, dW_beta, db, dH, dh_dt, lddh, workspace, ws_bytes};
     return hip_status(bom::launch_head_vjp(a, static_cast<hipStream_t>(stream)), "bom_head_vjp");
 }
 

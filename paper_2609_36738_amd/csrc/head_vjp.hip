@@ -1678,9 +1678,56 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
 
 }  // namespace
 
-size_t head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt) { return vjp_ws(N, d, V, dt).total; }
+// bf16 dW / db (bf16 gradient storage): the products are formed in fp32 in the workspace past the
+// products' own part, then rounded to nearest-even bf16 in one pass (dW = bf16(dW_fp32 + beta dW)).
+size_t head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt, bom_dtype dw_dt) {
+    size_t n = vjp_ws(N, d, V, dt).total;
+    if (dw_dt == BOM_BF16) n += align256((size_t)d * V * 4) + align256((size_t)V * 4);
+    return n;
+}
+
+namespace {
+__global__ __launch_bounds__(256) void round_dw_bf16_kernel(const float* __restrict__ src, int d, int V,
+                                                            uint16_t* __restrict__ dW, int64_t lddw, float beta,
+                                                            const float* __restrict__ db_src,
+                                                            uint16_t* __restrict__ db) {
+    const int64_t n = (int64_t)d * V;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < n + (db ? V : 0); k += stride) {
+        if (k < n) {
+            const int64_t i = k / V, j = k % V;
+            uint16_t* p = dW + i * lddw + j;
+            const float x = src[k];
+            *p = f32_to_bf16(beta != 0.f ? x + beta * bf16_to_f32(*p) : x);
+        } else {
+            db[k - n] = f32_to_bf16(db_src[k - n]);
+        }
+    }
+}
+}  // namespace
+
+hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st);
 
 hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
+    if (a.dw_dt != BOM_BF16) return launch_head_vjp_f32(a, st);
+    HeadVjpArgs b = a;
+    char* scratch = static_cast<char*>(a.ws) + vjp_ws(a.N, a.d, a.V, a.dt).total;
+    b.dW = scratch;
+    b.dw_dt = BOM_F32;
+    b.lddw = a.V;
+    b.dW_beta = 0.f;
+    b.db = a.db ? scratch + align256((size_t)a.d * a.V * 4) : nullptr;
+    hipError_t e = launch_head_vjp_f32(b, st);
+    if (e != hipSuccess) return e;
+    const int64_t n = (int64_t)a.d * a.V + (a.db ? a.V : 0);
+    const unsigned grid = (unsigned)std::min<int64_t>(cdiv(n, 256), 8192);
+    hipLaunchKernelGGL(round_dw_bf16_kernel, dim3(grid), dim3(256), 0, st, static_cast<const float*>(b.dW), a.d, a.V,
+                       static_cast<uint16_t*>(a.dW), a.lddw, a.dW_beta, static_cast<const float*>(b.db),
+                       static_cast<uint16_t*>(a.db));
+    return hipGetLastError();
+}
+
+hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
     const VjpWs L = vjp_ws(a.N, a.d, a.V, a.dt);
     Plan p = make_plan(a.N, a.d, a.V, a.dt);
     char* base = static_cast<char*>(a.ws);
@@ -1727,13 +1774,13 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
         fa.N = a.N;
         fa.d = a.d;
         fa.V = a.V;
-        fa.dW = a.dW;
+        fa.dW = static_cast<float*>(a.dW);
         fa.lddw = a.lddw;
         fa.beta = a.dW_beta;
         fa.dH = a.dH;
         fa.lddh = a.lddh;
         fa.dh_bf16 = a.dh_dt == BOM_BF16;
-        fa.db = a.db;
+        fa.db = static_cast<float*>(a.db);
         fa.tw_n = (int)cdiv(a.V, FB);
         fa.tw = (int)cdiv(a.d, FB) * fa.tw_n;
         fa.th_n = (int)cdiv(a.d, FB);
@@ -1758,14 +1805,16 @@ hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t st) {
     int nprep = a.V > a.N ? a.V : a.N;
     if (nprep < a.d) nprep = a.d;
     hipLaunchKernelGGL(vjp_prep_kernel, dim3((nprep + 255) / 256), dim3(256), 0, st, a.q_hat, a.s, a.n_valid, a.lambda,
-                       a.V, a.N, a.labels, a.ignore_index, cq, cqp, vmask, scal, a.db, rw ? hpart : nullptr, nrb, a.d,
+                       a.V, a.N, a.labels, a.ignore_index, cq, cqp, vmask, scal, static_cast<float*>(a.db),
+                       rw ? hpart : nullptr, nrb, a.d,
                        hsum);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const Fold f{cq, vmask, scal, cqp};
 
     // dW = H^T G
-    e = run_gemm<float>(true, p.w, a.H, a.ldh, a.R, a.ldr, a.dt, a.d, a.V, a.N, f, a.dW, a.lddw, a.dW_beta, part, hsum, cq,
+    e = run_gemm<float>(true, p.w, a.H, a.ldh, a.R, a.ldr, a.dt, a.d, a.V, a.N, f, static_cast<float*>(a.dW), a.lddw,
+                        a.dW_beta, part, hsum, cq,
                         st);
     if (e != hipSuccess) return e;
     // dH = G W^T (shares the split-K buffer: same stream, so it runs after the dW reduction)

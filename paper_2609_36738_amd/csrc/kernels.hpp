@@ -31,12 +31,12 @@ struct HeadVjpArgs {
     int N, d, V;
     const int32_t* labels; int32_t ignore_index;
     const float* q_hat; const float* s; const int32_t* n_valid; float lambda;
-    float* dW; int64_t lddw; float dW_beta;
-    float* db;
+    void* dW; bom_dtype dw_dt; int64_t lddw; float dW_beta;   // dW and db in dw_dt (fp32 or bf16)
+    void* db;
     void* dH; bom_dtype dh_dt; int64_t lddh;
     void* ws; size_t ws_bytes;
 };
-size_t head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt);
+size_t head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt, bom_dtype dw_dt);
 hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t stream);
 
 // ---- head forward (support) ---------------------------------------------------------------

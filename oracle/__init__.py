@@ -61,6 +61,7 @@ def _load():
         lib.orc_head_forward.argtypes = [vp, i64, i64, vp, i64, vp, vp]
         lib.orc_clip_factor.argtypes = [vp, vp, i64, f64, f64, f64]
         lib.orc_round_bf16.argtypes = [vp, i64, vp]
+        lib.orc_head_telemetry.argtypes = [vp, i64, i64, vp, i64, vp, i32, vp, vp, i64, vp, vp, f64, i64, vp]
         lib.orc_clip_factor.restype = f64
         _lib = lib
         return lib
@@ -188,6 +189,24 @@ def update_dense(theta, v, u, *, lr, beta2, eps, t, segments=None, weight_decay=
                              float(weight_decay), float(lr), float(beta2), float(eps), float(lam), float(u_scale),
                              int(t))
     return theta, v
+
+
+TELEMETRY_FIELDS = ("cos", "drift", "cancellation", "m_norm", "h_norm")
+
+
+def head_telemetry(H, R, labels, s, q_hat, n_valid: int, M_W, M_b=None, *, beta1, t, ignore_index: int = -100):
+    """One drift-telemetry step of the linear head. Returns (M_W_new, M_b_new or None, dict of
+    TELEMETRY_FIELDS); inputs are not modified."""
+    H, R, labels = _f64(H), _f64(R), _i32(labels)
+    s, q_hat = _f64(s), _f64(q_hat)
+    M_W = _f64(M_W).copy()
+    M_b = None if M_b is None else _f64(M_b).copy()
+    N, d = H.shape
+    V = R.shape[1]
+    out = np.zeros(5)
+    _load().orc_head_telemetry(_p(H), N, d, _p(R), V, _p(labels), ignore_index, _p(s), _p(q_hat), int(n_valid),
+                               _p(M_W), _p(M_b), float(beta1), int(t), _p(out))
+    return M_W, M_b, dict(zip(TELEMETRY_FIELDS, out.tolist()))
 
 
 def round_bf16(x) -> np.ndarray:

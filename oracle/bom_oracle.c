@@ -348,6 +348,64 @@ void orc_update_factored(double* theta, double* Rr, double* Cc, const double* u,
 }
 
 /*
+ * Historical-projection drift telemetry of the linear head (Sec. 3.3, Eq. (8);
+ * appendix "Historical-Projection Control" and appendix "Measuring historical projection drift").
+ * For z_i = W^T h_i + b the batch-mean Jacobian maps a task-space vector x to Jbar^T x = (hbar x^T, x),
+ * hbar = (1/N_t) sum_{i in I} H_i. One telemetry step:
+ *   M_W = beta1 M_W + (1 - beta1) hbar s^T,   M_b = beta1 M_b + (1 - beta1) s   (own-step projections),
+ *   Mhat = M / (1 - beta1^t),   h = (hbar q_hat^T, q_hat)                     (BOM's reprojection),
+ *   out[0] = cos(Mhat, h), out[1] = ||Mhat - h|| / ||Mhat||,
+ *   out[2] = ||s|| / ((1/N_t) sum_{i in I} ||r_i||)   (within-batch cancellation),
+ *   out[3] = ||Mhat||, out[4] = ||h||.
+ * The head is W and, when M_b is not NULL, b. R holds the residual rows (rows outside I are zero).
+ * N_t = 0 leaves M unchanged by the projections (hbar = 0, s = 0) and reports 0 for the ratios.
+ */
+void orc_head_telemetry(const double* H, int64_t N, int64_t d, const double* R, int64_t V, const int32_t* labels,
+                        int32_t ignore_index, const double* s, const double* q_hat, int64_t n_valid, double* M_W,
+                        double* M_b, double beta1, int64_t t, double* out) {
+    double* hbar = (double*)calloc((size_t)d, sizeof(double));
+    double rnorm_sum = 0.0;
+    for (int64_t i = 0; i < N; ++i) {
+        int bad = 0;
+        if (!orc_is_valid(labels[i], V, ignore_index, &bad)) continue;
+        for (int64_t k = 0; k < d; ++k) hbar[k] += H[i * d + k];
+        double rr = 0.0;
+        for (int64_t j = 0; j < V; ++j) rr += R[i * V + j] * R[i * V + j];
+        rnorm_sum += sqrt(rr);
+    }
+    for (int64_t k = 0; k < d; ++k) hbar[k] = n_valid > 0 ? hbar[k] / (double)n_valid : 0.0;
+    double inv_bc = 1.0 / (1.0 - pow(beta1, (double)t));
+    double mm = 0.0, mh = 0.0, hh = 0.0, dd = 0.0, ss = 0.0;
+    for (int64_t k = 0; k < d; ++k)
+        for (int64_t j = 0; j < V; ++j) {
+            double* m = &M_W[k * V + j];
+            *m = beta1 * *m + (1.0 - beta1) * hbar[k] * s[j];
+            double mhat = *m * inv_bc, hv = hbar[k] * q_hat[j];
+            mm += mhat * mhat;
+            mh += mhat * hv;
+            hh += hv * hv;
+            dd += (mhat - hv) * (mhat - hv);
+        }
+    if (M_b)
+        for (int64_t j = 0; j < V; ++j) {
+            M_b[j] = beta1 * M_b[j] + (1.0 - beta1) * s[j];
+            double mhat = M_b[j] * inv_bc, hv = q_hat[j];
+            mm += mhat * mhat;
+            mh += mhat * hv;
+            hh += hv * hv;
+            dd += (mhat - hv) * (mhat - hv);
+        }
+    for (int64_t j = 0; j < V; ++j) ss += s[j] * s[j];
+    double rmean = n_valid > 0 ? rnorm_sum / (double)n_valid : 0.0;
+    out[0] = mm > 0.0 && hh > 0.0 ? mh / (sqrt(mm) * sqrt(hh)) : 0.0;
+    out[1] = mm > 0.0 ? sqrt(dd) / sqrt(mm) : 0.0;
+    out[2] = rmean > 0.0 ? sqrt(ss) / rmean : 0.0;
+    out[3] = sqrt(mm);
+    out[4] = sqrt(hh);
+    free(hbar);
+}
+
+/*
  * bf16 storage (appendix "NLP Fine-Tuning Parameters": bf16 parameter and optimizer-state storage,
  * the task-space EMA kept in fp32). Rounds each fp64 value once to the nearest bf16 (8 significant
  * bits, ties to even; bf16 has fp32's exponent range, so below 2^-126 the spacing is 2^-133) and

@@ -534,6 +534,74 @@ def test_bf16_update_first_step_closed_form():
     np.testing.assert_array_equal(t1, oracle.round_bf16((1 - 1e-2 * 0.05) * th - 1e-2 * u / (np.abs(u) + EPS)))
 
 
+# Historical-projection drift telemetry (Sec. 3.3, Eq. (8); appendix "Measuring historical projection drift").
+
+def _tele_batch(r, N, d, V):
+    H = r.standard_normal((N, d))
+    Z = r.standard_normal((N, V)) * 0.7
+    y = r.integers(0, V, N).astype(np.int32)
+    y[::4] = -100                       # ignored rows: outside hbar and the cancellation mean
+    o = oracle.residual(Z, y)
+    return H, y, o
+
+
+def test_telemetry_fixed_features_have_no_drift():
+    # A linear head with the same inputs H at every step has a constant Jacobian, so the own-step EMA of
+    # hbar s_t^T equals hbar q_hat_t^T (BOM's reprojection) for any residual sequence: cos 1, drift 0.
+    r = _rng(37)
+    N, d, V = 12, 5, 7
+    H = r.standard_normal((N, d))
+    MW, Mb, q = np.zeros((d, V)), np.zeros(V), np.zeros(V)
+    for t in range(1, 6):
+        Z = r.standard_normal((N, V))
+        y = r.integers(0, V, N).astype(np.int32)
+        o = oracle.residual(Z, y)
+        q, qh = oracle.ema(q, o["s"], B1, t)
+        MW, Mb, st = oracle.head_telemetry(H, o["R"], y, o["s"], qh, o["n_valid"], MW, Mb, beta1=B1, t=t)
+        assert abs(st["cos"] - 1.0) <= 1e-12 and st["drift"] <= 1e-12
+        np.testing.assert_allclose(MW / (1 - B1 ** t), np.outer(H.mean(0), qh), rtol=1e-11, atol=1e-15)
+
+
+def test_telemetry_explicit_sum_and_moving_features():
+    # Changing inputs: Mhat_t is the bias-corrected explicit sum of the own-step projections
+    # (1 - beta1) beta1^(t - tau) hbar_tau s_tau^T, and the reported statistics are its cosine and relative
+    # distance to hbar_t q_hat_t^T (with the bias part s_tau / q_hat_t), recomputed here with numpy.
+    r = _rng(38)
+    N, d, V, T = 9, 4, 6, 5
+    MW, Mb, q = np.zeros((d, V)), np.zeros(V), np.zeros(V)
+    hist = []
+    for t in range(1, T + 1):
+        H, y, o = _tele_batch(r, N, d, V)
+        q, qh = oracle.ema(q, o["s"], B1, t)
+        MW, Mb, st = oracle.head_telemetry(H, o["R"], y, o["s"], qh, o["n_valid"], MW, Mb, beta1=B1, t=t)
+        hbar = H[y >= 0].mean(0)
+        hist.append((hbar, o["s"]))
+        bc = 1 - B1 ** t
+        MWh = sum((1 - B1) * B1 ** (t - k) * np.outer(hb, sk) for k, (hb, sk) in enumerate(hist, 1)) / bc
+        Mbh = sum((1 - B1) * B1 ** (t - k) * sk for k, (_, sk) in enumerate(hist, 1)) / bc
+        m = np.concatenate([MWh.ravel(), Mbh])
+        h = np.concatenate([np.outer(hbar, qh).ravel(), qh])
+        rn = np.linalg.norm(o["R"][y >= 0], axis=1).mean()
+        assert abs(st["cancellation"] - np.linalg.norm(o["s"]) / rn) <= 1e-12
+        np.testing.assert_allclose(MW / bc, MWh, rtol=1e-12, atol=1e-15)
+        assert abs(st["cos"] - m @ h / np.linalg.norm(m) / np.linalg.norm(h)) <= 1e-12
+        assert abs(st["drift"] - np.linalg.norm(m - h) / np.linalg.norm(m)) <= 1e-12
+        assert abs(st["m_norm"] - np.linalg.norm(m)) <= 1e-12 * np.linalg.norm(m)
+    assert st["drift"] > 0.05           # moving features do drift
+
+
+def test_telemetry_cancellation_ratio():
+    # V = 2, equal logits: labels 0 and 1 give r = (-1/2, 1/2) and (1/2, -1/2); they cancel (ratio 0).
+    # One supervised row (the other ignored) keeps all of its magnitude (ratio 1).
+    H = np.ones((2, 3))
+    Z = np.zeros((2, 2))
+    for y, expect in (([0, 1], 0.0), ([1, -100], 1.0)):
+        y = np.array(y, np.int32)
+        o = oracle.residual(Z, y)
+        _, _, st = oracle.head_telemetry(H, o["R"], y, o["s"], o["s"], o["n_valid"], np.zeros((3, 2)), beta1=B1, t=1)
+        assert abs(st["cancellation"] - expect) <= 1e-15
+
+
 # ----------------------------------------------------------------------------- multi-step
 
 def test_linear_model_bom_equals_own_step_control():

@@ -143,6 +143,35 @@ class Problem:
             ev[4].record()
 
 
+def time_telemetry(prob, steps):
+    """Mean time of the drift telemetry call over `steps` calls (M_W, M_b updated each call), and its
+    HBM rate against the algorithmic bytes: read R and H, read and write M_W (and M_b)."""
+    w = prob.w
+    d, V, N = w.d, w.V, w.N
+    esz = 2 if w.dtype == "bf16" else 4
+    MW = torch.zeros((d, V), dtype=torch.float32, device=prob.Z.device)
+    Mb = torch.zeros(V, dtype=torch.float32, device=prob.Z.device) if w.has_bias else None
+    res = prob.res
+    ws = None
+    for k in range(3):
+        ws = bom.bom_head_telemetry(prob.H, prob.R, prob.labels, res["s"], prob.q_hat, res["n_valid"], MW, M_b=Mb,
+                                    beta1=w.beta1, t=k + 1, workspace=ws)["workspace"]
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for k in range(steps):
+        tel = bom.bom_head_telemetry(prob.H, prob.R, prob.labels, res["s"], prob.q_hat, res["n_valid"], MW, M_b=Mb,
+                                     beta1=w.beta1, t=k + 4, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    nbytes = N * V * esz + N * d * esz + 8 * d * V + (8 * V if w.has_bias else 0)
+    stats = dict(zip(bom.TELEMETRY_FIELDS, [round(float(x), 6) for x in tel["out"].cpu()]))
+    return {"ms": round(ms, 5), "rate": round(nbytes / (ms / 1e3) / 1e9, 2), "unit": "GB/s",
+            "frac": round(nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4), "algorithmic_bytes": nbytes,
+            "last": stats}
+
+
 def algorithmic(w, clip=False, bf16_state=False):
     """Algorithmic bytes / flops of each stage for one step (what BOM must move or compute). With
     global-norm clipping the dense update reads u once more for the norm; the factored update takes
@@ -311,6 +340,9 @@ def main():
     ap.add_argument("--state-dtype", choices=["f32", "bf16"], default="f32",
                     help="storage of theta, v and u (bf16: the paper's fine-tuning protocol; dense layout, bf16 "
                          "logits only)")
+    ap.add_argument("--telemetry", action="store_true",
+                    help="also time the head drift telemetry call (a diagnostic for telemetry steps, outside the "
+                         "step) on the last step's residual, history and features")
     ap.add_argument("--clip-norm", type=float, default=0.0,
                     help="global-norm clipping of the update numerator at this norm (0: none; the paper's "
                          "language-model protocols clip at 1.0)")
@@ -421,6 +453,8 @@ def main():
         "stages": per_stage,
         "roofline": roofline,
     }
+    if args.telemetry:
+        out["telemetry"] = time_telemetry(prob, args.steps)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)

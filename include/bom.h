@@ -223,6 +223,32 @@ bom_status bom_update(void* theta, void* v, float* v_col, const void* u, const v
                       void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------------
+ * bom_head_telemetry -- diagnostic beside the four steps (for telemetry steps only): the
+ * historical-projection drift of the linear head, Sec. 3.3 Eq. (8) and appendix "Measuring historical
+ * projection drift". For z_i = W^T h_i + b the batch-mean Jacobian maps a task-space x to
+ * (hbar x^T, x), hbar = (1/N_t) sum_{i in I} H_i. One call, after bom_ema of the same step:
+ *   M_W = beta1 M_W + (1 - beta1) hbar s^T,  M_b = beta1 M_b + (1 - beta1) s   (own-step projections)
+ *   Mhat = M / (1 - beta1^t),  h = (hbar q_hat^T, q_hat)                     (BOM's reprojection)
+ *   out[0] = cos(Mhat, h)   out[1] = ||Mhat - h|| / ||Mhat||   out[2] = ||s|| / ((1/N_t) sum_{i in I} ||r_i||)
+ *   out[3] = ||Mhat||       out[4] = ||h||
+ * The head is W and, when M_b is not NULL, b. Ratios with a zero denominator are reported as 0.
+ *
+ *   H  device [N, ldh] of h_dt.   R device [N, ldr] of r_dt (bom_residual's rows; rows outside I zero).
+ *   labels, s, q_hat, n_valid as in bom_head_vjp.
+ *   M_W device fp32 [d, ldm] (in place, zero before the first telemetry step); M_b device fp32 [V] or NULL.
+ *   beta1 in [0, 1), t >= 1 the step counter of q (1/(1 - beta1^t) formed on the host in fp64).
+ *   out device fp32 [5].   workspace: at least bom_head_telemetry_workspace_bytes(N, d, V) bytes.
+ * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_DTYPE, BOM_ERR_HYPER, BOM_ERR_WORKSPACE, BOM_ERR_ALIAS,
+ *         BOM_ERR_HIP.
+ * ---------------------------------------------------------------------------------------- */
+size_t bom_head_telemetry_workspace_bytes(int64_t N, int64_t d, int64_t V);
+bom_status bom_head_telemetry(const void* H, int64_t ldh, bom_dtype h_dt, const void* R, int64_t ldr, bom_dtype r_dt,
+                              int64_t N, int64_t d, int64_t V, const int32_t* labels, int32_t ignore_index,
+                              const float* s, const float* q_hat, const int32_t* n_valid, float* M_W, int64_t ldm,
+                              float* M_b, float beta1, int64_t t, float* out, void* workspace, size_t ws_bytes,
+                              void* stream);
+
+/* ------------------------------------------------------------------------------------------
  * bom_head_forward -- support call (not one of the four steps): the linear head's logits
  * Z = H W (+ b), used by multi-step loops that move W. fp32 only in this build (dt = BOM_F32;
  * BOM_BF16 returns BOM_ERR_UNSUPPORTED).

@@ -80,6 +80,11 @@ def load(build_if_missing: bool = True):
         lib.bom_update.restype = ctypes.c_int
         lib.bom_update.argtypes = [vp, vp, vp, vp, vp, i64, ctypes.POINTER(bom_segment), i32, f32,
                                    ctypes.POINTER(bom_update_cfg), vp, sz, vp]
+        lib.bom_head_telemetry_workspace_bytes.restype = sz
+        lib.bom_head_telemetry_workspace_bytes.argtypes = [i64, i64, i64]
+        lib.bom_head_telemetry.restype = ctypes.c_int
+        lib.bom_head_telemetry.argtypes = [vp, i64, ctypes.c_int, vp, i64, ctypes.c_int, i64, i64, i64, vp, i32, vp, vp,
+                                           vp, vp, i64, vp, f32, i64, vp, vp, sz, vp]
         lib.bom_head_forward.restype = ctypes.c_int
         lib.bom_head_forward.argtypes = [vp, i64, vp, i64, vp, ctypes.c_int, i64, i64, i64, vp, i64, vp]
         _lib = lib
@@ -237,6 +242,28 @@ def bom_update(theta, v, u, cfg: bom_update_cfg, *, v_col=None, h=None, segments
                           float(weight_decay), ctypes.byref(cfg), _ptr(workspace),
                           0 if workspace is None else workspace.numel(), _stream(stream)))
     return workspace
+
+
+TELEMETRY_FIELDS = ("cos", "drift", "cancellation", "m_norm", "h_norm")
+
+
+def bom_head_telemetry(H, R, labels, s, q_hat, n_valid, M_W, *, beta1, t, M_b=None, out=None, ignore_index=-100,
+                       workspace=None, stream=None) -> dict:
+    """Drift telemetry of the linear head (M_W, M_b updated in place); out (device fp32 [5]) holds
+    TELEMETRY_FIELDS. Returns dict(out=..., workspace=...)."""
+    lib = load()
+    N, d = H.shape
+    V = R.shape[1]
+    if M_W.dtype != torch.float32 or tuple(M_W.shape) != (d, V) or (M_b is not None and M_b.dtype != torch.float32):
+        raise ValueError("M_W must be fp32 [d, V] and M_b fp32 [V]")
+    out = torch.zeros(5, dtype=torch.float32, device=H.device) if out is None else out
+    nb = lib.bom_head_telemetry_workspace_bytes(N, d, V)
+    workspace = _workspace(nb, H.device, workspace)
+    _check(lib.bom_head_telemetry(_ptr(H), _rowmajor(H, "H"), _dtype_code(H), _ptr(R), _rowmajor(R, "R"), _dtype_code(R),
+                                  N, d, V, _ptr(labels), ignore_index, _ptr(s), _ptr(q_hat), _ptr(n_valid), _ptr(M_W),
+                                  _rowmajor(M_W, "M_W"), _ptr(M_b), float(beta1), int(t), _ptr(out), _ptr(workspace),
+                                  0 if workspace is None else workspace.numel(), _stream(stream)))
+    return dict(out=out, workspace=workspace)
 
 
 def bom_head_forward(H, W, b=None, Z=None, stream=None):

@@ -248,6 +248,37 @@ bom_status bom_update(void* theta_p, void* v_p, float* v_col, const void* u_p, c
                       "bom_update");
 }
 
+size_t bom_head_telemetry_workspace_bytes(int64_t N, int64_t d, int64_t V) {
+    if (N < 1 || d < 1 || V < 1 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim) return 0;
+    return bom::head_telemetry_workspace_bytes(N, d);
+}
+
+bom_status bom_head_telemetry(const void* H, int64_t ldh, bom_dtype h_dt, const void* R, int64_t ldr, bom_dtype r_dt,
+                              int64_t N, int64_t d, int64_t V, const int32_t* labels, int32_t ignore_index,
+                              const float* s, const float* q_hat, const int32_t* n_valid, float* M_W, int64_t ldm,
+                              float* M_b, float beta1, int64_t t, float* out, void* workspace, size_t ws_bytes,
+                              void* stream) {
+    if (!H || !R || !labels || !s || !q_hat || !n_valid || !M_W || !out)
+        return fail(BOM_ERR_NULL, "bom_head_telemetry: H, R, labels, s, q_hat, n_valid, M_W and out are required");
+    if (N < 1 || d < 1 || V < 1 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim || ldh < d || ldr < V || ldm < V)
+        return fail(BOM_ERR_SHAPE, "bom_head_telemetry: bad shape or leading dimension");
+    if (!is_dtype(h_dt) || !is_dtype(r_dt)) return fail(BOM_ERR_DTYPE, "bom_head_telemetry: unsupported dtype");
+    if (!(beta1 >= 0.f && beta1 < 1.f) || t < 1)
+        return fail(BOM_ERR_HYPER, "bom_head_telemetry: need beta1 in [0, 1) and t >= 1");
+    const size_t need = bom::head_telemetry_workspace_bytes(N, d);
+    if (!workspace || ws_bytes < need)
+        return fail(BOM_ERR_WORKSPACE, "bom_head_telemetry: workspace needs %zu bytes, got %zu", need, ws_bytes);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+        return fail(BOM_ERR_WORKSPACE, "bom_head_telemetry: workspace must be 256-byte aligned");
+    const size_t mb = ((size_t)(d - 1) * ldm + V) * 4;
+    if ((M_b && overlap(M_W, mb, M_b, (size_t)V * 4)) || overlap(M_W, mb, out, 20) || (M_b && overlap(M_b, (size_t)V * 4, out, 20)))
+        return fail(BOM_ERR_ALIAS, "bom_head_telemetry: M_W, M_b and out must be distinct");
+    bom::TeleArgs a{H, ldh, h_dt, R, ldr, r_dt, (int)N, (int)d, (int)V, labels, ignore_index, s, q_hat, n_valid, M_W, ldm,
+                    M_b, beta1, (float)(1.0 - (double)beta1),
+                    (float)(1.0 / (1.0 - std::pow((double)beta1, (double)t))), out, workspace};
+    return hip_status(bom::launch_head_telemetry(a, static_cast<hipStream_t>(stream)), "bom_head_telemetry");
+}
+
 bom_status bom_head_forward(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
                             int64_t N, int64_t d, int64_t V, void* Z, int64_t ldz, void* stream) {
     if (!H || !W || !Z) return fail(BOM_ERR_NULL, "bom_head_forward: H, W and Z are required");

@@ -39,6 +39,21 @@ struct HeadVjpArgs {
 size_t head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt, bom_dtype dw_dt);
 hipError_t launch_head_vjp(const HeadVjpArgs& a, hipStream_t stream);
 
+// ---- head telemetry (diagnostic) --------------------------------------------------------------
+struct TeleArgs {
+    const void* H; int64_t ldh; bom_dtype h_dt;
+    const void* R; int64_t ldr; bom_dtype r_dt;
+    int N, d, V;
+    const int32_t* labels; int32_t ignore_index;
+    const float* s; const float* q_hat; const int32_t* n_valid;
+    float* MW; int64_t ldm; float* Mb;
+    float beta1, one_minus_beta1, inv_bc;
+    float* out;
+    void* ws;
+};
+size_t head_telemetry_workspace_bytes(int64_t N, int64_t d);
+hipError_t launch_head_telemetry(const TeleArgs& a, hipStream_t stream);
+
 // ---- head forward (support) ---------------------------------------------------------------
 hipError_t launch_head_forward_f32(const float* H, int64_t ldh, const float* W, int64_t ldw, const float* b, int N,
                                    int d, int V, float* Z, int64_t ldz, hipStream_t stream);

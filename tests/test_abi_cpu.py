@@ -142,6 +142,25 @@ def test_update_workspace_query(lib):
     assert lib.bom_update_workspace_bytes(P, ctypes.byref(fac)) > 0
 
 
+def _tele(lib, **kw):
+    a = dict(H=FAKE, ldh=64, hdt=bom.BOM_BF16, R=FAKE, ldr=100, rdt=bom.BOM_BF16, N=32, d=64, V=100, labels=FAKE,
+             ig=-100, s=FAKE, qh=FAKE, nv=FAKE, MW=ctypes.c_void_p(0x100000), ldm=100, Mb=None, beta1=0.9, t=1,
+             out=ctypes.c_void_p(0x900000), ws=ctypes.c_void_p(0x2000000), wsb=1 << 30)
+    a.update(kw)
+    return lib.bom_head_telemetry(a["H"], a["ldh"], a["hdt"], a["R"], a["ldr"], a["rdt"], a["N"], a["d"], a["V"],
+                                  a["labels"], a["ig"], a["s"], a["qh"], a["nv"], a["MW"], a["ldm"], a["Mb"], a["beta1"],
+                                  a["t"], a["out"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(H=None), 1), (dict(MW=None), 1), (dict(out=None), 1), (dict(N=0), 2), (dict(ldm=99), 2),
+    (dict(ldr=10), 2), (dict(hdt=7), 3), (dict(beta1=1.0), 4), (dict(t=0), 4), (dict(wsb=0), 5),
+    (dict(Mb=ctypes.c_void_p(0x100000 + 400)), 6),
+])
+def test_head_telemetry_rejects(lib, kw, code):
+    assert _tele(lib, **kw) == code
+
+
 def test_head_forward_rejects(lib):
     assert lib.bom_head_forward(FAKE, 8, FAKE, 4, None, bom.BOM_BF16, 4, 8, 4, FAKE2, 4, None) == 8
     assert lib.bom_head_forward(FAKE, 7, FAKE, 4, None, bom.BOM_F32, 4, 8, 4, FAKE2, 4, None) == 2

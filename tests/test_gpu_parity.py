@@ -372,6 +372,46 @@ def test_head_vjp_empty_batch_gives_zero():
     assert (g["dW"] == 0).all() and (g["db"] == 0).all() and (g["dH"].float() == 0).all()
 
 
+# ------------------------------------------------------------------------------------------------ telemetry
+# Drift telemetry of the linear head over three steps with new features every step (so the own-step
+# history drifts from the reprojection): M_W (and M_b) against the oracle after each step, the five
+# statistics, and the fixed-feature case where there is no drift.
+@pytest.mark.parametrize("N,d,V,dtype,bias,moving", [(1024, 768, 1000, "bf16", False, True),
+                                                     (300, 136, 520, "f32", True, True),
+                                                     (256, 64, 128, "bf16", True, False)],
+                         ids=["vision_bf16", "ragged_f32_bias", "fixed_features"])
+def test_head_telemetry_parity(N, d, V, dtype, bias, moving):
+    log(f"[telemetry] N={N} d={d} V={V} {dtype} bias={bias} moving={moving}")
+    MW = torch.zeros((d, V), device=dev())
+    Mb = torch.zeros(V, device=dev()) if bias else None
+    MWo, Mbo = np.zeros((d, V)), (np.zeros(V) if bias else None)
+    q = torch.zeros(V, device=dev())
+    qo = np.zeros(V)
+    for t in range(1, 4):
+        Hh, Hd = gen_matrix(N, d, synth.STREAM_H, 1.0, dtype, start=(t * N * d if moving else 0))
+        Zh, Zd = gen_matrix(N, V, synth.STREAM_Z, 0.5, dtype, start=t * N * V)
+        y = gen_labels(N, V, "uniform", 0.05)
+        yd = torch.from_numpy(y).to(dev())
+        res = bom.bom_residual(Zd, yd)
+        qh = bom.bom_ema(q, res["s"], B1, t)
+        tel = bom.bom_head_telemetry(Hd, res["R"], yd, res["s"], qh, res["n_valid"], MW, M_b=Mb, beta1=B1, t=t)
+        torch.cuda.synchronize()
+        # teacher forcing: the oracle step takes the GPU's own residual rows, s and q_hat
+        R64, s64, qh64 = to_f64(res["R"]), to_f64(res["s"]), to_f64(qh)
+        MWo, Mbo, st = oracle.head_telemetry(Hh, R64, y, s64, qh64, int(res["n_valid"].item()), MWo, Mbo,
+                                             beta1=f32(B1), t=t)
+        assert rel_fro(to_f64(MW), MWo) <= 1e-5
+        if bias:
+            assert rel_fro(to_f64(Mb), Mbo) <= 1e-5
+        g = dict(zip(bom.TELEMETRY_FIELDS, tel["out"].cpu().numpy().astype(np.float64)))
+        log("    " + " ".join(f"{k}={g[k]:.6f}/{st[k]:.6f}" for k in bom.TELEMETRY_FIELDS))
+        for k in ("cos", "cancellation", "m_norm", "h_norm"):
+            assert abs(g[k] - st[k]) <= 1e-5 * max(1.0, abs(st[k])), k
+        assert abs(g["drift"] - st["drift"]) <= 1e-4 * max(1e-2, st["drift"])
+        if not moving:
+            assert g["drift"] <= 1e-4 and g["cos"] >= 1 - 1e-6
+
+
 # ------------------------------------------------------------------------------------------------ update
 def _check_theta(th_gpu, th_o, lr, name):
     err = np.abs(th_gpu - th_o) / np.maximum(np.abs(th_o), lr)

@@ -61,10 +61,12 @@ def fill_normal_(t: torch.Tensor, stream: int, std: float, chunk: int = 1 << 27)
     into a bf16 tensor), chunk by chunk (bounded host memory)."""
     n = t.numel()
     host = np.empty(min(chunk, n), np.float32)
-    for start in range(0, n, chunk):
+    for k, start in enumerate(range(0, n, chunk)):
         m = min(chunk, n - start)
         synth.normal_f32(m, stream, std, start=start, out=host[:m])
         t[start:start + m].copy_(torch.from_numpy(host[:m]))
+        if k % 16 == 15:
+            log(f"[bench] generated {start + m} of {n} values of stream {stream}")
 
 
 class Problem:

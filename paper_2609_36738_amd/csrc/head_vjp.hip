@@ -15,6 +15,11 @@
 // transpose while staging); dH = G W^T has both operands k-contiguous. fp32 path (and unaligned
 // bf16): a SIMT tiled GEMM.
 #include <algorithm>
+#include <array>
+#include <map>
+#include <mutex>
+#include <queue>
+#include <vector>
 #include <cstdio>
 #include <cstdlib>
 #include <type_traits>
@@ -537,8 +542,7 @@ struct TileRange {
 // (workgroups are dealt to the XCDs round-robin by id), and all inner tiles of a pair run on the same
 // XCD, so the tiles that share an outer operand panel share that XCD's L2. With one split this is the
 // plain outer-tile order: XCD x runs outer tiles x, x + 8, x + 16, ...
-__device__ __forceinline__ bool unit_of(const TileRange& r, bool inner_is_m, int* tm, int* tn, int* z) {
-    const int id = blockIdx.x;
+__device__ __forceinline__ bool unit_of(const TileRange& r, bool inner_is_m, int id, int* tm, int* tn, int* z) {
     const int xcd = id % 8, rest = id / 8;
     const int inner = rest % r.inner_count, pg = rest / r.inner_count;
     const int pair = pg * 8 + xcd;
@@ -843,21 +847,48 @@ __global__ __launch_bounds__(256, 1) void lds256_kernel(const uint16_t* __restri
 // transposing fragment reads. (dW with A given as H^T, k-contiguous, from a transpose of H measured no
 // faster: the transposing reads of one operand are not what bounds it.) Tile kt+1 is written from registers at the start of
 // iteration kt and tile kt+2 loaded behind it; the barrier sits before the last MFMA step of the tile.
+constexpr int WKT = 64;             // k tile of the 64-deep kernels
+constexpr int WSE = LB * WKT;        // bf16 elements per operand per stage (32 KB)
+
+// Arguments of one 64-deep 256-tile product (one launch part).
+struct WideArgs {
+    const uint16_t* Xa;
+    int64_t lda;
+    const uint16_t* Xb;
+    int64_t ldb;
+    int M, Nn, K, kps;
+    TileRange tr;
+    const float* alpha_p;
+    const float* rv;
+    const float* cv;
+    void* out;
+    int64_t ldo;
+    float beta;
+    float* part;
+};
+
+// One work unit (tile and k range) of the product, for block id `id` of its launch part; lds and rv_s
+// are the workgroup's LDS (two stages of both operands, and the rank-1 row vector of the tile).
 template <bool IS_DW, typename TO>
-__global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restrict__ Xa, int64_t lda,
-                                                         const uint16_t* __restrict__ Xb, int64_t ldb, int M, int Nn, int K,
-                                                         int kps, TileRange tr, const float* alpha_p,
-                                                         const float* __restrict__ rv, const float* __restrict__ cv,
-                                                         TO* __restrict__ out, int64_t ldo, float beta,
-                                                         float* __restrict__ part) {
-    constexpr int KT = 64;
-    constexpr int SE = LB * KT;   // bf16 elements per operand per stage (32 KB)
+__device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t (&lds)[2][2][WSE], float (&rv_s)[LB]) {
+    constexpr int KT = WKT;
     constexpr bool KA = !IS_DW;           // operand A k-contiguous
     constexpr bool KB = !IS_DW;           // operand B k-contiguous
-    __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][SE];
-    __shared__ float rv_s[LB];
+    const uint16_t* __restrict__ Xa = args.Xa;
+    const int64_t lda = args.lda;
+    const uint16_t* __restrict__ Xb = args.Xb;
+    const int64_t ldb = args.ldb;
+    const int M = args.M, Nn = args.Nn, K = args.K, kps = args.kps;
+    const TileRange& tr = args.tr;
+    const float* alpha_p = args.alpha_p;
+    const float* __restrict__ rv = args.rv;
+    const float* __restrict__ cv = args.cv;
+    TO* __restrict__ out = static_cast<TO*>(args.out);
+    const int64_t ldo = args.ldo;
+    const float beta = args.beta;
+    float* __restrict__ part = args.part;
     int tm, tn, kz;
-    if (!unit_of(tr, IS_DW, &tm, &tn, &kz)) return;
+    if (!unit_of(tr, IS_DW, id, &tm, &tn, &kz)) return;
     // uniform per workgroup: keep them scalar so that the buffer descriptors stay in SGPRs
     tm = __builtin_amdgcn_readfirstlane(tm);
     tn = __builtin_amdgcn_readfirstlane(tn);
@@ -1052,6 +1083,25 @@ __global__ __launch_bounds__(256, 1) void lds256w_kernel(const uint16_t* __restr
             if (m < M && n < Nn) pz[(int64_t)(m - tr.pm0) * tr.ldp + (n - tr.pn0)] = alpha * v;
         });
     }
+}
+
+template <bool IS_DW, typename TO>
+__global__ __launch_bounds__(256, 1) void lds256w_kernel(WideArgs a) {
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
+    __shared__ float rv_s[LB];
+    wide_tile<IS_DW, TO>(a, blockIdx.x, lds, rv_s);
+}
+
+// Both products in one grid: blocks [0, nh) run dH's units (the long k ranges first), the rest dW's
+// tiles, so that the shorter dW tiles fill the compute units that dH's last round leaves idle instead of
+// a second launch starting after a partly empty round. nh is a multiple of 8, so each part keeps its
+// own XCD order.
+template <typename TO>
+__global__ __launch_bounds__(256, 1) void lds256w_pair_kernel(WideArgs h, WideArgs w, int nh) {
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
+    __shared__ float rv_s[LB];
+    if ((int)blockIdx.x < nh) wide_tile<false, TO>(h, blockIdx.x, lds, rv_s);
+    else wide_tile<true, float>(w, (int)blockIdx.x - nh, lds, rv_s);
 }
 
 // Split-K reduction for the rank-1 form over the rectangle [pm0, M) x [pn0, Nn) of the output, in split
@@ -1424,6 +1474,9 @@ struct GemmPlan {
 };
 struct Plan {
     GemmPlan w, h;
+    // both 64-deep products in one grid (dH's units first, then dW's tiles): h.splits is dH's k split,
+    // dW runs unsplit
+    bool pair = false;
 };
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -1543,7 +1596,66 @@ void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int
     (void)N;
 }
 
-Plan make_plan(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
+// Completion time, in 256 x 256 x 64 tile steps, of one launch of the 64-deep kernel: parts in block
+// order, each (pairs, inner tiles per pair, k tile steps per unit); pair q of a part goes to XCD q % 8
+// and its inner tiles follow each other there; each XCD starts its blocks in order on the first of its
+// 32 compute units to become free (greedy list schedule).
+double sim_launch(std::initializer_list<std::array<int64_t, 3>> parts) {
+    double end = 0.0;
+    for (int x = 0; x < 8; ++x) {
+        std::priority_queue<double, std::vector<double>, std::greater<double>> cu;
+        for (int c = 0; c < kCUs / 8; ++c) cu.push(0.0);
+        for (const auto& pt : parts)
+            for (int64_t q = x; q < pt[0]; q += 8)
+                for (int64_t i = 0; i < pt[1]; ++i) {
+                    const double t = cu.top() + (double)pt[2];
+                    cu.pop();
+                    cu.push(t);
+                }
+        while (cu.size() > 1) cu.pop();
+        end = std::max(end, cu.top());
+    }
+    return end;
+}
+
+// Whether one grid with both products (dH first) beats the two launches of the separate plans, and with
+// which k split of dH. Times in tile steps; split partials cost their fp32 write, read and the output.
+void plan_pair(Plan& p, int64_t N, int64_t d, int64_t V) {
+    constexpr double kStep = 1.8e-6, kBw = 5e12;
+    const int64_t inner = cdiv(d, LB);
+    const int64_t ow = cdiv(V, LB), oh = cdiv(N, LB);
+    const int64_t nkw = cdiv(N, 2 * LK), nkh = cdiv(V, 2 * LK);
+    auto red = [&](int s, int64_t rect) { return s > 1 ? (2.0 * s + 2.0) * 4.0 * (double)rect / kBw / kStep : 0.0; };
+    // separate launches as planned (each split launch followed by its reduction)
+    auto sep = [&](const GemmPlan& g, int64_t outer, int64_t nk, int64_t rect_per_outer) {
+        const int64_t dp = std::min<int64_t>(g.outer_dp, outer);
+        double t = dp > 0 ? sim_launch({{dp, inner, nk}}) : 0.0;
+        if (dp < outer) {
+            t += sim_launch({{(outer - dp) * g.splits, inner, cdiv(nk, g.splits)}});
+            t += red(g.splits, (outer - dp) * rect_per_outer);
+        }
+        return t;
+    };
+    const double t_sep = sep(p.w, ow, nkw, LB * d) + sep(p.h, oh, nkh, LB * d);
+    double best = t_sep * 0.95;
+    int best_s = 0;
+    for (int s = 1; s <= 16; ++s) {
+        if (s > 1 && cdiv(nkh, s) < 4) break;
+        const double t = sim_launch({{oh * s, inner, cdiv(nkh, s)}, {ow, inner, nkw}}) + red(s, N * d);
+        if (t < best) {
+            best = t;
+            best_s = s;
+        }
+    }
+    if (best_s == 0) return;
+    p.pair = true;
+    p.h.splits = best_s;
+    p.h.outer_dp = 0;
+    p.w.splits = 1;
+    p.w.outer_dp = (int)ow;
+}
+
+Plan make_plan_uncached(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     const bool mfma = dt == BOM_BF16;
     Plan p;
     // the MFMA kernels load whole 16-byte chunks: extents along k and along contiguous rows must be
@@ -1554,6 +1666,25 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     const PlanOverride& o = plan_override();
     apply_override(p.w, o.kw, o.sw, d, V, N);
     apply_override(p.h, o.kh, o.sh, N, d, V);
+    if (o.kw == 0 && o.kh == 0 && o.sw == 0 && o.sh == 0 && p.w.kind == kRank1 && p.w.wide && p.h.kind == kRank1 &&
+        p.h.wide)
+        plan_pair(p, N, d, V);
+    return p;
+}
+
+// Plans are deterministic functions of the shape; the schedule simulation is kept per shape.
+Plan make_plan(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
+    static std::mutex mu;
+    static std::map<std::array<int64_t, 4>, Plan> cache;
+    const std::array<int64_t, 4> key{N, d, V, (int64_t)dt};
+    {
+        std::lock_guard<std::mutex> lk(mu);
+        auto it = cache.find(key);
+        if (it != cache.end()) return it->second;
+    }
+    const Plan p = make_plan_uncached(N, d, V, dt);
+    std::lock_guard<std::mutex> lk(mu);
+    if (cache.size() < 256) cache.emplace(key, p);
     return p;
 }
 
@@ -1598,12 +1729,11 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
             const int dp = std::min(g.outer_dp, outer);
             auto launch = [&](int ob, int oe, int nsplit, int kp, float* pp, const TileRange& tr) {
                 dim3 gr((unsigned)(cdiv((int64_t)(oe - ob) * nsplit, 8) * 8 * inner));
+                const WideArgs wa{a16, lda, b16, ldb, M, Nn, K, kp, tr, f.scal, rv, cv, out, ldo, beta, pp};
                 if (is_dw)
-                    hipLaunchKernelGGL((lds256w_kernel<true, float>), gr, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K,
-                                       kp, tr, f.scal, rv, cv, reinterpret_cast<float*>(out), ldo, beta, pp);
+                    hipLaunchKernelGGL((lds256w_kernel<true, float>), gr, dim3(256), 0, st, wa);
                 else
-                    hipLaunchKernelGGL((lds256w_kernel<false, TO>), gr, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K,
-                                       kp, tr, f.scal, rv, cv, out, ldo, beta, pp);
+                    hipLaunchKernelGGL((lds256w_kernel<false, TO>), gr, dim3(256), 0, st, wa);
                 return hipGetLastError();
             };
             if (dp > 0) {
@@ -1811,6 +1941,39 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const Fold f{cq, vmask, scal, cqp};
+
+    if (p.pair && a.dH && p.w.kind == kRank1 && p.h.kind == kRank1) {
+        // one grid: dH's units (k split p.h.splits) first, then dW's tiles over the full k range
+        const int inner = (int)cdiv(a.d, LB);
+        const int oh = (int)cdiv(a.N, LB), ow = (int)cdiv(a.V, LB);
+        const int sh = p.h.splits;
+        const int kps_h = (int)(cdiv(cdiv(a.V, sh), 2 * LK) * 2 * LK);
+        const int kps_w = (int)(cdiv(a.N, 2 * LK) * 2 * LK);
+        const uint16_t* H16 = static_cast<const uint16_t*>(a.H);
+        const uint16_t* R16 = static_cast<const uint16_t*>(a.R);
+        const uint16_t* W16 = static_cast<const uint16_t*>(a.W);
+        const TileRange trh{inner, 0, oh, sh, 0, 0, a.d, (int64_t)a.N * a.d};
+        const TileRange trw{inner, 0, ow, 1, 0, 0, 0, 0};
+        const WideArgs wh{R16, a.ldr, W16, a.ldw, a.N, a.d, a.V, kps_h, trh, f.scal, vmask, u, a.dH, a.lddh, 0.f,
+                          sh > 1 ? part : nullptr};
+        const WideArgs ww{H16, a.ldh, R16, a.ldr, a.d, a.V, a.N, kps_w, trw, f.scal, hsum, cq, a.dW, a.lddw,
+                          a.dW_beta, nullptr};
+        const int nh = (int)(cdiv((int64_t)oh * sh, 8) * 8 * inner);
+        const int nw = (int)(cdiv(ow, 8) * 8 * inner);
+        if (a.dh_dt == BOM_BF16)
+            hipLaunchKernelGGL(lds256w_pair_kernel<uint16_t>, dim3((unsigned)(nh + nw)), dim3(256), 0, st, wh, ww, nh);
+        else
+            hipLaunchKernelGGL(lds256w_pair_kernel<float>, dim3((unsigned)(nh + nw)), dim3(256), 0, st, wh, ww, nh);
+        if ((e = hipGetLastError()) != hipSuccess || sh == 1) return e;
+        const int64_t MN = (int64_t)a.N * a.d;
+        if (a.dh_dt == BOM_BF16)
+            hipLaunchKernelGGL(splitk_rank1_kernel<uint16_t>, dim3((unsigned)cdiv(MN, 256)), dim3(256), 0, st, part, sh,
+                               a.N, a.d, 0, 0, vmask, u, static_cast<uint16_t*>(a.dH), a.lddh, 0.f);
+        else
+            hipLaunchKernelGGL(splitk_rank1_kernel<float>, dim3((unsigned)cdiv(MN, 256)), dim3(256), 0, st, part, sh, a.N,
+                               a.d, 0, 0, vmask, u, static_cast<float*>(a.dH), a.lddh, 0.f);
+        return hipGetLastError();
+    }
 
     // dW = H^T G
     e = run_gemm<float>(true, p.w, a.H, a.ldh, a.R, a.ldr, a.dt, a.d, a.V, a.N, f, static_cast<float*>(a.dW), a.lddw,

@@ -249,10 +249,14 @@ bom_status bom_head_telemetry(const void* H, int64_t ldh, bom_dtype h_dt, const 
                               void* stream);
 
 /* ------------------------------------------------------------------------------------------
- * bom_head_forward -- support call (not one of the four steps): the linear head's logits
- * Z = H W (+ b), used by multi-step loops that move W. fp32 only in this build (dt = BOM_F32;
- * BOM_BF16 returns BOM_ERR_UNSUPPORTED).
- *   H device [N, ldh], W device [d, ldw], b device [V] or NULL, Z device [N, ldz].
+ * bom_head_forward -- support call (row a0 of the path; the forward is common work, not one of the
+ * four steps): the linear head's logits Z = H W (+ b), fp32 accumulation, Z rounded once to dt.
+ * dt = BOM_BF16 (the language-model and vision workloads' logits, as bf16 autocast computes them) runs
+ * on the matrix cores (256 x 256 tiles) when d and V are multiples of 8 and H, W are 16-byte aligned
+ * with leading dimensions that are multiples of 8, and on a SIMT kernel otherwise; dt = BOM_F32
+ * (the tiny classifier) runs on the SIMT kernel.
+ *   H device [N, ldh], W device [d, ldw], b device [V] or NULL, Z device [N, ldz], all of dt.
+ * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_DTYPE, BOM_ERR_HIP.
  * ---------------------------------------------------------------------------------------- */
 bom_status bom_head_forward(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
                             int64_t N, int64_t d, int64_t V, void* Z, int64_t ldz, void* stream);

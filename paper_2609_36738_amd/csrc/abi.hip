@@ -284,11 +284,10 @@ bom_status bom_head_forward(const void* H, int64_t ldh, const void* W, int64_t l
     if (!H || !W || !Z) return fail(BOM_ERR_NULL, "bom_head_forward: H, W and Z are required");
     if (N < 1 || d < 1 || V < 1 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim || ldh < d || ldw < V || ldz < V)
         return fail(BOM_ERR_SHAPE, "bom_head_forward: bad shape or leading dimension");
-    if (dt == BOM_BF16) return fail(BOM_ERR_UNSUPPORTED, "bom_head_forward: only BOM_F32 in this build");
-    if (dt != BOM_F32) return fail(BOM_ERR_DTYPE, "bom_head_forward: unsupported dtype");
-    return hip_status(bom::launch_head_forward_f32(static_cast<const float*>(H), ldh, static_cast<const float*>(W), ldw,
-                                                   static_cast<const float*>(b), (int)N, (int)d, (int)V,
-                                                   static_cast<float*>(Z), ldz, static_cast<hipStream_t>(stream)),
+    if (!is_dtype(dt)) return fail(BOM_ERR_DTYPE, "bom_head_forward: unsupported dtype");
+    if ((int64_t)N * V >= ((int64_t)1 << 40)) return fail(BOM_ERR_SHAPE, "bom_head_forward: output too large");
+    return hip_status(bom::launch_head_forward(H, ldh, W, ldw, b, dt, (int)N, (int)d, (int)V, Z, ldz,
+                                               static_cast<hipStream_t>(stream)),
                       "bom_head_forward");
 }
 

@@ -865,15 +865,24 @@ struct WideArgs {
     int64_t ldo;
     float beta;
     float* part;
+    const uint16_t* bias;   // forward: bf16 bias [Nn] or null
 };
+
+// Products of the 64-deep kernel: C = A B with
+//   kWideDH:  dH = alpha R W^T + rv cv^T     A(m, k) = R[m][k], B(k, n) = W[n][k] (both k-contiguous)
+//   kWideDW:  dW = alpha H^T R + rv cv^T (+ beta dW)   A(m, k) = H[k][m], B(k, n) = R[k][n] (both k-outer)
+//   kWideFWD: Z = H W (+ b)                  A(m, k) = H[m][k] (k-contiguous), B(k, n) = W[k][n] (k-outer)
+constexpr int kWideDH = 0, kWideDW = 1, kWideFWD = 2;
 
 // One work unit (tile and k range) of the product, for block id `id` of its launch part; lds and rv_s
 // are the workgroup's LDS (two stages of both operands, and the rank-1 row vector of the tile).
-template <bool IS_DW, typename TO>
+template <int MODE, typename TO>
 __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t (&lds)[2][2][WSE], float (&rv_s)[LB]) {
     constexpr int KT = WKT;
-    constexpr bool KA = !IS_DW;           // operand A k-contiguous
-    constexpr bool KB = !IS_DW;           // operand B k-contiguous
+    constexpr bool IS_DW = MODE == kWideDW;
+    constexpr bool RANK1 = MODE != kWideFWD;   // rank-1 epilogue (the head VJP products)
+    constexpr bool KA = MODE != kWideDW;       // operand A k-contiguous
+    constexpr bool KB = MODE == kWideDH;       // operand B k-contiguous
     const uint16_t* __restrict__ Xa = args.Xa;
     const int64_t lda = args.lda;
     const uint16_t* __restrict__ Xb = args.Xb;
@@ -888,7 +897,7 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
     const float beta = args.beta;
     float* __restrict__ part = args.part;
     int tm, tn, kz;
-    if (!unit_of(tr, IS_DW, id, &tm, &tn, &kz)) return;
+    if (!unit_of(tr, MODE != kWideDH, id, &tm, &tn, &kz)) return;
     // uniform per workgroup: keep them scalar so that the buffer descriptors stay in SGPRs
     tm = __builtin_amdgcn_readfirstlane(tm);
     tn = __builtin_amdgcn_readfirstlane(tn);
@@ -900,12 +909,12 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int wm = wave / 2, wn = wave % 2;
 
-    const float rv_reg = (part == nullptr && m0 + (int)threadIdx.x < M) ? rv[m0 + threadIdx.x] : 0.f;
+    const float rv_reg = (RANK1 && part == nullptr && m0 + (int)threadIdx.x < M) ? rv[m0 + threadIdx.x] : 0.f;
     float cvv[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const int n = n0 + wn * 128 + j * 32 + l % 32;
-        cvv[j] = (part == nullptr && n < Nn) ? cv[n] : 0.f;
+        cvv[j] = (RANK1 && part == nullptr && n < Nn) ? cv[n] : 0.f;
     }
 
     // copy step q (< 8) of this wave fills kilobyte wave*8 + q of an operand's stage
@@ -1060,6 +1069,14 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
+    if constexpr (MODE == kWideFWD) {
+        const uint16_t* __restrict__ bias = args.bias;
+        for_each_acc256(acc, [&](int r, int c, float v) {
+            const int m = m0 + r, n = n0 + c;
+            if (m < M && n < Nn) stf<TO>(out, (int64_t)m * ldo + n, bias ? v + bf16_to_f32(bias[n]) : v);
+        });
+        return;
+    }
     const float alpha = *alpha_p;
     if (part == nullptr) {
         rv_s[threadIdx.x] = rv_reg;
@@ -1089,7 +1106,15 @@ template <bool IS_DW, typename TO>
 __global__ __launch_bounds__(256, 1) void lds256w_kernel(WideArgs a) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    wide_tile<IS_DW, TO>(a, blockIdx.x, lds, rv_s);
+    wide_tile<IS_DW ? kWideDW : kWideDH, TO>(a, blockIdx.x, lds, rv_s);
+}
+
+// The head forward Z = H W (+ b) in bf16 on the same tiles (fp32 accumulation, one rounding of Z).
+template <typename TO>
+__global__ __launch_bounds__(256, 1) void lds256w_fwd_kernel(WideArgs a) {
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
+    __shared__ float rv_s[LB];
+    wide_tile<kWideFWD, TO>(a, blockIdx.x, lds, rv_s);
 }
 
 // Both products in one grid: blocks [0, nh) run dH's units (the long k ranges first), the rest dW's
@@ -1100,8 +1125,8 @@ template <typename TO>
 __global__ __launch_bounds__(256, 1) void lds256w_pair_kernel(WideArgs h, WideArgs w, int nh) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    if ((int)blockIdx.x < nh) wide_tile<false, TO>(h, blockIdx.x, lds, rv_s);
-    else wide_tile<true, float>(w, (int)blockIdx.x - nh, lds, rv_s);
+    if ((int)blockIdx.x < nh) wide_tile<kWideDH, TO>(h, blockIdx.x, lds, rv_s);
+    else wide_tile<kWideDW, float>(w, (int)blockIdx.x - nh, lds, rv_s);
 }
 
 // Split-K reduction for the rank-1 form over the rectangle [pm0, M) x [pn0, Nn) of the output, in split
@@ -1729,7 +1754,7 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
             const int dp = std::min(g.outer_dp, outer);
             auto launch = [&](int ob, int oe, int nsplit, int kp, float* pp, const TileRange& tr) {
                 dim3 gr((unsigned)(cdiv((int64_t)(oe - ob) * nsplit, 8) * 8 * inner));
-                const WideArgs wa{a16, lda, b16, ldb, M, Nn, K, kp, tr, f.scal, rv, cv, out, ldo, beta, pp};
+                const WideArgs wa{a16, lda, b16, ldb, M, Nn, K, kp, tr, f.scal, rv, cv, out, ldo, beta, pp, nullptr};
                 if (is_dw)
                     hipLaunchKernelGGL((lds256w_kernel<true, float>), gr, dim3(256), 0, st, wa);
                 else
@@ -1955,9 +1980,9 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
         const TileRange trh{inner, 0, oh, sh, 0, 0, a.d, (int64_t)a.N * a.d};
         const TileRange trw{inner, 0, ow, 1, 0, 0, 0, 0};
         const WideArgs wh{R16, a.ldr, W16, a.ldw, a.N, a.d, a.V, kps_h, trh, f.scal, vmask, u, a.dH, a.lddh, 0.f,
-                          sh > 1 ? part : nullptr};
+                          sh > 1 ? part : nullptr, nullptr};
         const WideArgs ww{H16, a.ldh, R16, a.ldr, a.d, a.V, a.N, kps_w, trw, f.scal, hsum, cq, a.dW, a.lddw,
-                          a.dW_beta, nullptr};
+                          a.dW_beta, nullptr, nullptr};
         const int nh = (int)(cdiv((int64_t)oh * sh, 8) * 8 * inner);
         const int nw = (int)(cdiv(ow, 8) * 8 * inner);
         if (a.dh_dt == BOM_BF16)
@@ -1993,10 +2018,13 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
 
 // ---- head forward (support): Z = H W + b, fp32 SIMT ------------------------------------------------
 namespace {
-__global__ __launch_bounds__(256) void head_forward_f32_kernel(const float* __restrict__ H, int64_t ldh,
-                                                               const float* __restrict__ W, int64_t ldw,
-                                                               const float* __restrict__ b, int N, int d, int V,
-                                                               float* __restrict__ Z, int64_t ldz) {
+// SIMT forward (fp32, and bf16 shapes the MFMA tiles do not take): 64 x 64 tiles, 16-deep k, fp32
+// accumulation, Z rounded once to its type.
+template <typename T>
+__global__ __launch_bounds__(256) void head_forward_simt_kernel(const T* __restrict__ H, int64_t ldh,
+                                                                const T* __restrict__ W, int64_t ldw,
+                                                                const T* __restrict__ b, int N, int d, int V,
+                                                                T* __restrict__ Z, int64_t ldz) {
     __shared__ float As[SK][SB + 4];
     __shared__ float Bs[SK][SB + 4];
     const int t = threadIdx.x, tx = t % 16, ty = t / 16;
@@ -2006,9 +2034,9 @@ __global__ __launch_bounds__(256) void head_forward_f32_kernel(const float* __re
         for (int e = 0; e < 4; ++e) {
             const int idx = e * 256 + t;
             const int rr = idx / SK, kk = idx % SK;
-            As[kk][rr] = (k0 + kk < d && m0 + rr < N) ? H[(int64_t)(m0 + rr) * ldh + k0 + kk] : 0.f;
+            As[kk][rr] = (k0 + kk < d && m0 + rr < N) ? ldf<T>(H, (int64_t)(m0 + rr) * ldh + k0 + kk) : 0.f;
             const int kk2 = idx / SB, cc = idx % SB;
-            Bs[kk2][cc] = (k0 + kk2 < d && n0 + cc < V) ? W[(int64_t)(k0 + kk2) * ldw + n0 + cc] : 0.f;
+            Bs[kk2][cc] = (k0 + kk2 < d && n0 + cc < V) ? ldf<T>(W, (int64_t)(k0 + kk2) * ldw + n0 + cc) : 0.f;
         }
         __syncthreads();
 #pragma unroll
@@ -2028,15 +2056,37 @@ __global__ __launch_bounds__(256) void head_forward_f32_kernel(const float* __re
     for (int i = 0; i < 4; ++i)
         for (int j = 0; j < 4; ++j) {
             const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
-            if (m < N && n < V) Z[(int64_t)m * ldz + n] = acc[i][j] + (b ? b[n] : 0.f);
+            if (m < N && n < V) stf<T>(Z, (int64_t)m * ldz + n, acc[i][j] + (b ? ldf<T>(b, n) : 0.f));
         }
 }
 }  // namespace
 
-hipError_t launch_head_forward_f32(const float* H, int64_t ldh, const float* W, int64_t ldw, const float* b, int N,
-                                   int d, int V, float* Z, int64_t ldz, hipStream_t st) {
+hipError_t launch_head_forward(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
+                               int N, int d, int V, void* Z, int64_t ldz, hipStream_t st) {
+    if (dt == BOM_F32) {
+        dim3 grid((V + SB - 1) / SB, (N + SB - 1) / SB);
+        hipLaunchKernelGGL(head_forward_simt_kernel<float>, grid, dim3(256), 0, st, static_cast<const float*>(H), ldh,
+                           static_cast<const float*>(W), ldw, static_cast<const float*>(b), N, d, V,
+                           static_cast<float*>(Z), ldz);
+        return hipGetLastError();
+    }
+    const uint16_t* H16 = static_cast<const uint16_t*>(H);
+    const uint16_t* W16 = static_cast<const uint16_t*>(W);
+    const uint16_t* b16 = static_cast<const uint16_t*>(b);
+    auto al = [](const void* ptr, int64_t ld) { return reinterpret_cast<uintptr_t>(ptr) % 16 == 0 && ld % 8 == 0; };
+    // 256-tile MFMA kernel: 16-byte chunks along H's rows (k = d) and W's rows (n = V)
+    if (d % 8 == 0 && V % 8 == 0 && al(H, ldh) && al(W, ldw) &&
+        ((int64_t)(N - 1) * ldh + d) * 2 < (1LL << 31) && ((int64_t)(d - 1) * ldw + V) * 2 < (1LL << 31)) {
+        const int MT = (int)cdiv(N, LB), NT = (int)cdiv(V, LB);
+        const TileRange tr{MT, 0, NT, 1, 0, 0, 0, 0};
+        const WideArgs wa{H16, ldh, W16, ldw, N, V, d, (int)(cdiv(d, WKT) * WKT), tr, nullptr, nullptr, nullptr, Z, ldz,
+                          0.f, nullptr, b16};
+        hipLaunchKernelGGL(lds256w_fwd_kernel<uint16_t>, dim3((unsigned)(cdiv(NT, 8) * 8 * MT)), dim3(256), 0, st, wa);
+        return hipGetLastError();
+    }
     dim3 grid((V + SB - 1) / SB, (N + SB - 1) / SB);
-    hipLaunchKernelGGL(head_forward_f32_kernel, grid, dim3(256), 0, st, H, ldh, W, ldw, b, N, d, V, Z, ldz);
+    hipLaunchKernelGGL(head_forward_simt_kernel<uint16_t>, grid, dim3(256), 0, st, H16, ldh, W16, ldw, b16, N, d, V,
+                       static_cast<uint16_t*>(Z), ldz);
     return hipGetLastError();
 }
 

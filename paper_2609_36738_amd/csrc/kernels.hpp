@@ -55,8 +55,8 @@ size_t head_telemetry_workspace_bytes(int64_t N, int64_t d);
 hipError_t launch_head_telemetry(const TeleArgs& a, hipStream_t stream);
 
 // ---- head forward (support) ---------------------------------------------------------------
-hipError_t launch_head_forward_f32(const float* H, int64_t ldh, const float* W, int64_t ldw, const float* b, int N,
-                                   int d, int V, float* Z, int64_t ldz, hipStream_t stream);
+hipError_t launch_head_forward(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
+                               int N, int d, int V, void* Z, int64_t ldz, hipStream_t stream);
 
 // ---- update ----------------------------------------------------------------------------------
 struct SegTable {

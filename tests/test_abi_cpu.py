@@ -162,6 +162,6 @@ def test_head_telemetry_rejects(lib, kw, code):
 
 
 def test_head_forward_rejects(lib):
-    assert lib.bom_head_forward(FAKE, 8, FAKE, 4, None, bom.BOM_BF16, 4, 8, 4, FAKE2, 4, None) == 8
+    assert lib.bom_head_forward(FAKE, 8, FAKE, 4, None, 5, 4, 8, 4, FAKE2, 4, None) == 3
     assert lib.bom_head_forward(FAKE, 7, FAKE, 4, None, bom.BOM_F32, 4, 8, 4, FAKE2, 4, None) == 2
     assert lib.bom_head_forward(None, 8, FAKE, 4, None, bom.BOM_F32, 4, 8, 4, FAKE2, 4, None) == 1

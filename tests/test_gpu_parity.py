@@ -412,6 +412,34 @@ def test_head_telemetry_parity(N, d, V, dtype, bias, moving):
             assert g["drift"] <= 1e-4 and g["cos"] >= 1 - 1e-6
 
 
+# ------------------------------------------------------------------------------------------------ forward
+# The head forward in bf16 (row a0: the logits of the large workloads): matrix-core tiles with ragged m, n
+# and k, the vision head with a bias, an LM shape checked on sampled rows, and an unaligned shape on the
+# SIMT kernel. Z is rounded once to bf16: the bar is the bf16-input GEMM bound, and every element within two
+# bf16 steps plus the fp32 accumulation error of its row.
+@pytest.mark.parametrize("N,d,V,bias,rows", [(2056, 520, 6000, False, None), (1024, 768, 1000, True, None),
+                                            (4096, 768, 32000, False, np.r_[0:32, 4064:4096]),
+                                            (300, 100, 333, True, None)],
+                         ids=["tiles_ragged", "vision_bias", "lm_sampled", "simt_unaligned"])
+def test_head_forward_bf16_parity(N, d, V, bias, rows):
+    log(f"[forward bf16] N={N} d={d} V={V} bias={bias}")
+    Hh, Hd = gen_matrix(N, d, synth.STREAM_H, 1.0, "bf16")
+    Wh, Wd = gen_matrix(d, V, synth.STREAM_W, 0.02, "bf16")
+    bh, bd = (gen_matrix(1, V, synth.STREAM_U, 0.1, "bf16") if bias else (None, None))
+    Z = bom.bom_head_forward(Hd, Wd, None if bd is None else bd.reshape(V))
+    torch.cuda.synchronize()
+    sel = np.arange(N) if rows is None else rows
+    Zo = oracle.head_forward(Hh[sel], Wh, None if bh is None else bh.reshape(V))
+    Zg = to_f64(Z)[sel]
+    assert Z.dtype == torch.bfloat16
+    e = rel_fro(Zg, Zo)
+    log(f"    rel err {e:.3e}")
+    assert e <= 2e-2
+    # element-wise: nearest bf16 of the exact value, give or take the fp32 accumulation of |H||W|
+    acc = 1e-6 * (np.abs(Hh[sel]) @ np.abs(Wh))
+    assert (np.abs(Zg - Zo) <= 2 * 2.0 ** -8 * np.abs(Zo) + acc + 1e-30).all()
+
+
 # ------------------------------------------------------------------------------------------------ update
 def _check_theta(th_gpu, th_o, lr, name):
     err = np.abs(th_gpu - th_o) / np.maximum(np.abs(th_o), lr)

@@ -602,6 +602,14 @@ def test_telemetry_cancellation_ratio():
         assert abs(st["cancellation"] - expect) <= 1e-15
 
 
+def test_head_forward_matches_library_matmul():
+    # the linear head z_i = W^T h_i + b, against numpy's matrix product (a library routine)
+    r = _rng(39)
+    H, W, b = r.standard_normal((7, 5)), r.standard_normal((5, 9)), r.standard_normal(9)
+    np.testing.assert_allclose(oracle.head_forward(H, W, b), H @ W + b, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(oracle.head_forward(H, W), H @ W, rtol=1e-13, atol=1e-13)
+
+
 # ----------------------------------------------------------------------------- multi-step
 
 def test_linear_model_bom_equals_own_step_control():

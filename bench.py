@@ -145,6 +145,30 @@ class Problem:
             ev[4].record()
 
 
+def time_forward(prob, steps):
+    """Mean time of the head forward Z = H W (+ b) over `steps` calls into a scratch Z, and its rate
+    against the bf16 MFMA peak (fp32 vector peak for the fp32 tiny head): 2 N d V flop."""
+    w = prob.w
+    W = prob.W if prob.W is not None else prob.theta[: w.d * w.V].view(w.d, w.V)
+    b = None if not w.has_bias else prob.theta[w.d * w.V: w.d * w.V + w.V]
+    Z = torch.empty_like(prob.Z)
+    for _ in range(3):
+        bom.bom_head_forward(prob.H, W, b, Z=Z)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        bom.bom_head_forward(prob.H, W, b, Z=Z)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    tf = 2.0 * w.N * w.d * w.V / (ms / 1e3) / 1e12
+    peak = MFMA_BF16_PEAK_TFS if w.dtype == "bf16" else FP32_PEAK_TFS
+    del Z
+    return {"ms": round(ms, 5), "rate": round(tf, 2), "unit": "TFLOP/s", "frac": round(tf / peak, 4),
+            "algorithmic_flop": 2 * w.N * w.d * w.V}
+
+
 def time_telemetry(prob, steps):
     """Mean time of the drift telemetry call over `steps` calls (M_W, M_b updated each call), and its
     HBM rate against the algorithmic bytes: read R and H, read and write M_W (and M_b)."""
@@ -342,6 +366,9 @@ def main():
     ap.add_argument("--state-dtype", choices=["f32", "bf16"], default="f32",
                     help="storage of theta, v and u (bf16: the paper's fine-tuning protocol; dense layout, bf16 "
                          "logits only)")
+    ap.add_argument("--forward", action="store_true",
+                    help="also time the head forward Z = H W that produces the logits (common work, outside the "
+                         "step) against the MFMA roofline")
     ap.add_argument("--telemetry", action="store_true",
                     help="also time the head drift telemetry call (a diagnostic for telemetry steps, outside the "
                          "step) on the last step's residual, history and features")
@@ -455,6 +482,8 @@ def main():
         "stages": per_stage,
         "roofline": roofline,
     }
+    if args.forward:
+        out["forward"] = time_forward(prob, args.steps)
     if args.telemetry:
         out["telemetry"] = time_telemetry(prob, args.steps)
     if not args.no_cpu_baseline:

@@ -8,8 +8,8 @@
 // multiplying R as stored; the 128-tile split-K kernels instead form G = fma(alpha, R, mask_i * cq_j)
 // while staging R into LDS and round it to bf16 for the MFMA.
 //
-// bf16 path: v_mfma_f32_32x32x16_bf16. Large products: 256 x 256 output tiles, four waves each owning
-// 128 x 128, k tiles of 64 in two LDS stages (lds256w_kernel). Small products: one fused launch of
+// bf16 path: v_mfma_f32_32x32x16_bf16. Large products: 256 x 256 output tiles, eight waves (two per
+// SIMD) each owning 128 x 64, k tiles of 64 in two LDS stages (lds256w_kernel). Small products: one fused launch of
 // 64 x 64 tiles of both products (vjp_fused_small_kernel), or 128 x 128 split-K tiles with a
 // fixed-order reduction. dW = H^T G has both operands k-outer in memory (transposing LDS reads or a
 // transpose while staging); dH = G W^T has both operands k-contiguous. fp32 path (and unaligned
@@ -840,13 +840,17 @@ __global__ __launch_bounds__(256, 1) void lds256_kernel(const uint16_t* __restri
     }
 }
 
-// The same product with k tiles of 64 in two LDS stages (one barrier per 64 k instead of per 32):
-// each wave copies 8 kilobytes per operand per tile. A k-contiguous operand (dH's two) has LDS rows
+// The same product with k tiles of 64 in two LDS stages (one barrier per 64 k instead of per 32): the
+// workgroup copies 32 kilobytes per operand per tile, 1 KB per wave and copy step. A k-contiguous operand (dH's two) has LDS rows
 // of 64 k (128 B) with chunk c of row r at swz(r, c) and 16-byte
 // fragment reads; a k-outer operand (dW's two) has LDS rows of 512 B per k as in lds256_kernel and
 // transposing fragment reads. (dW with A given as H^T, k-contiguous, from a transpose of H measured no
 // faster: the transposing reads of one operand are not what bounds it.) Tile kt+1 is written from registers at the start of
 // iteration kt and tile kt+2 loaded behind it; the barrier sits before the last MFMA step of the tile.
+// Measured on the three language-model shapes, eight waves (two per SIMD) beat four by 5-9 % on every
+// product: with one wave per SIMD the copies, LDS writes and fragment reads add to the MFMA time almost
+// in full (removing each of them from a four-wave copy of the kernel saved 14 %, 10 % and 12 % at the
+// 1B shape), while a second wave issues its MFMAs meanwhile, at the price of 1.5 x the fragment reads.
 constexpr int WKT = 64;             // k tile of the 64-deep kernels
 constexpr int WSE = LB * WKT;        // bf16 elements per operand per stage (32 KB)
 
@@ -876,9 +880,16 @@ constexpr int kWideDH = 0, kWideDW = 1, kWideFWD = 2;
 
 // One work unit (tile and k range) of the product, for block id `id` of its launch part; lds and rv_s
 // are the workgroup's LDS (two stages of both operands, and the rank-1 row vector of the tile).
-template <int MODE, typename TO>
+// NW waves share the 256 x 256 tile: four (one per SIMD) each own 128 x 128, or eight (two per SIMD,
+// so that one wave's copies and LDS reads overlap the other's MFMAs) each own 128 x 64.
+template <int MODE, typename TO, int NW>
 __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t (&lds)[2][2][WSE], float (&rv_s)[LB]) {
+    static_assert(NW == 4 || NW == 8, "four or eight waves");
     constexpr int KT = WKT;
+    constexpr int WCOLS = NW == 4 ? 128 : 64;   // columns of a wave's part of the tile
+    constexpr int NJ = WCOLS / 32;              // 32-column MFMA blocks per wave
+    constexpr int CPO = 32 / NW;                // 1 KB copy steps per operand per k tile, per wave
+    constexpr int CPS = 2 * CPO < 8 ? 2 * CPO : 8;   // copy steps placed in each of the first MFMA steps
     constexpr bool IS_DW = MODE == kWideDW;
     constexpr bool RANK1 = MODE != kWideFWD;   // rank-1 epilogue (the head VJP products)
     constexpr bool KA = MODE != kWideDW;       // operand A k-contiguous
@@ -907,21 +918,22 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
     const int nk = (ke - kb + KT - 1) / KT;
     const int l = threadIdx.x % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int wm = wave / 2, wn = wave % 2;
+    const int wm = wave / (NW / 2), wn = wave % (NW / 2);
 
-    const float rv_reg = (RANK1 && part == nullptr && m0 + (int)threadIdx.x < M) ? rv[m0 + threadIdx.x] : 0.f;
-    float cvv[4];
+    const float rv_reg =
+        (RANK1 && part == nullptr && (int)threadIdx.x < LB && m0 + (int)threadIdx.x < M) ? rv[m0 + threadIdx.x] : 0.f;
+    float cvv[NJ];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int n = n0 + wn * 128 + j * 32 + l % 32;
+    for (int j = 0; j < NJ; ++j) {
+        const int n = n0 + wn * WCOLS + j * 32 + l % 32;
         cvv[j] = (RANK1 && part == nullptr && n < Nn) ? cv[n] : 0.f;
     }
 
-    // copy step q (< 8) of this wave fills kilobyte wave*8 + q of an operand's stage
-    int voff_a[8], voff_b[8], kc_a[8], kc_b[8];
-    bool ok_a[8], ok_b[8];
+    // copy step q (< CPO) of this wave fills kilobyte wave*CPO + q of an operand's stage
+    int voff_a[CPO], voff_b[CPO], kc_a[CPO], kc_b[CPO];
+    bool ok_a[CPO], ok_b[CPO];
     auto geo = [&](bool kcontig, int64_t ld, int rows_valid, int q, int* voff, int* kc, bool* ok) {
-        const int chunk = (wave * 8 + q) * 64 + l;
+        const int chunk = (wave * CPO + q) * 64 + l;
         if (kcontig) {
             const int row = chunk / 8, c = swz(row, chunk % 8);
             *voff = (int)((int64_t)row * ld * 2) + c * 16;
@@ -935,7 +947,7 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         }
     };
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
+    for (int q = 0; q < CPO; ++q) {
         geo(KA, lda, M - m0, q, &voff_a[q], &kc_a[q], &ok_a[q]);
         geo(KB, ldb, Nn - n0, q, &voff_b[q], &kc_b[q], &ok_b[q]);
     }
@@ -970,41 +982,42 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         }
         return tl;
     };
-    // copy op q < 16: q < 8 operand A, else operand B
+    // copy op q < 2 CPO: q < CPO operand A, else operand B
     auto load_one = [&](const TileLoad& tl, int q) {
-        if (q < 8) {
+        if (q < CPO) {
             const int vo = !KA ? voff_a[q] : ((ok_a[q] && tl.k0 + kc_a[q] < ke) ? voff_a[q] + tl.k0 * 2 : kOob);
             return __builtin_amdgcn_raw_buffer_load_b128(make_desc(tl.ba, tl.bytes_a), vo, 0, 0);
         }
-        const int r = q - 8;
+        const int r = q - CPO;
         const int vo = !KB ? voff_b[r] : ((ok_b[r] && tl.k0 + kc_b[r] < ke) ? voff_b[r] + tl.k0 * 2 : kOob);
         return __builtin_amdgcn_raw_buffer_load_b128(make_desc(tl.bb, tl.bytes_b), vo, 0, 0);
     };
     auto write_one = [&](int stage, int q, const u32x4_t& v) {
-        char* base = reinterpret_cast<char*>(&lds[stage][q / 8][0]);
-        *reinterpret_cast<u32x4_t*>(base + (wave * 8 + q % 8) * 1024 + l * 16) = v;
+        char* base = reinterpret_cast<char*>(&lds[stage][q / CPO][0]);
+        *reinterpret_cast<u32x4_t*>(base + (wave * CPO + q % CPO) * 1024 + l * 16) = v;
     };
 
-    // fragments for MFMA step s (k = 16 s .. +15): k-outer offsets (transposing reads) or LDS rows
-    // (16-byte reads; the chunk depends on the step)
-    int fa[4], fb[4];
-    auto frag_geo = [&](bool kcontig, int wbase, int (&f)[4]) {
+    // fragments for MFMA step s (k = 16 s .. +15) of `cnt` 32-wide blocks from tile row/column `base`:
+    // k-outer offsets (transposing reads; the 16-byte chunk of a k row is swizzled by (k & 3) << 2) or
+    // LDS rows (16-byte reads; the chunk depends on the step)
+    int fa[4], fb[NJ];
+    auto frag_geo = [&](bool kcontig, int base, int cnt, int* f) {
         if (kcontig) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) f[i] = wbase * 128 + i * 32 + l % 32;
+            for (int i = 0; i < cnt; ++i) f[i] = base + i * 32 + l % 32;
         } else {
             const int s = l % 16, g = l / 16;
             const int krow = (g >> 1) * 8 + (s >> 2);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int lo = ((i ^ (s >> 2)) * 4) + (g & 1) * 2 + ((s >> 1) & 1);
-                f[i] = krow * 512 + ((wbase * 16 + lo) << 4) + (s & 1) * 8;
+            for (int i = 0; i < cnt; ++i) {
+                const int chunk = ((base / 8 + i * 4) ^ ((krow & 3) << 2)) + (g & 1) * 2 + ((s >> 1) & 1);
+                f[i] = krow * 512 + (chunk << 4) + (s & 1) * 8;
             }
         }
     };
-    frag_geo(KA, wm, fa);
-    frag_geo(KB, wn, fb);
-    auto read_frags = [&](int stage, int s, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
+    frag_geo(KA, wm * 128, 4, fa);
+    frag_geo(KB, wn * WCOLS, NJ, fb);
+    auto read_frags = [&](int stage, int s, bf16x8_t (&a)[4], bf16x8_t (&b)[NJ]) {
         const char* As = reinterpret_cast<const char*>(&lds[stage][0][0]);
         const char* Bs = reinterpret_cast<const char*>(&lds[stage][1][0]);
         const int c = 2 * s + l / 32;
@@ -1012,25 +1025,29 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         for (int i = 0; i < 4; ++i) {
             if constexpr (KA) a[i] = ld_frag_b128(As + fa[i] * 128 + swz(fa[i], c) * 16);
             else a[i] = ld_frag_tr(As + fa[i] + s * 16 * 512);
-            if constexpr (KB) b[i] = ld_frag_b128(Bs + fb[i] * 128 + swz(fb[i], c) * 16);
-            else b[i] = ld_frag_tr(Bs + fb[i] + s * 16 * 512);
+        }
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            if constexpr (KB) b[j] = ld_frag_b128(Bs + fb[j] * 128 + swz(fb[j], c) * 16);
+            else b[j] = ld_frag_tr(Bs + fb[j] + s * 16 * 512);
         }
     };
 
-    f32x16_t acc[4][4];
+    f32x16_t acc[4][NJ];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-    // one MFMA step; copy ops q0 .. q0+7 placed after its MFMAs 0..7 (if q0 >= 0)
-    auto step = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], int q0, int ws, const TileLoad& tl,
-                    u32x4_t (&rg)[16]) {
+    // one MFMA step; copy ops q0 .. q0+CPS-1 placed after its first MFMAs (if q0 >= 0)
+    auto step = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[NJ], int q0, int ws, const TileLoad& tl,
+                    u32x4_t (&rg)[2 * CPO]) {
 #pragma unroll
-        for (int m = 0; m < 16; ++m) {
-            acc[m / 4][m % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[m / 4], b[m % 4], acc[m / 4][m % 4], 0, 0, 0);
-            if (q0 >= 0 && m < 8) {
+        for (int m = 0; m < 4 * NJ; ++m) {
+            acc[m / NJ][m % NJ] =
+                __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[m / NJ], b[m % NJ], acc[m / NJ][m % NJ], 0, 0, 0);
+            if (q0 >= 0 && m < CPS) {
                 __builtin_amdgcn_sched_barrier(0);
                 write_one(ws, q0 + m, rg[q0 + m]);
                 rg[q0 + m] = load_one(tl, q0 + m);
@@ -1038,16 +1055,16 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
             }
         }
     };
-    u32x4_t rg[16];
-    bf16x8_t a0[4], b0[4], a1[4], b1[4];
+    u32x4_t rg[2 * CPO];
+    bf16x8_t a0[4], b0[NJ], a1[4], b1[NJ];
     {
         const TileLoad t0 = tile_load(0), t1 = tile_load(1);
 #pragma unroll
-        for (int q = 0; q < 16; ++q) rg[q] = load_one(t0, q);
+        for (int q = 0; q < 2 * CPO; ++q) rg[q] = load_one(t0, q);
 #pragma unroll
-        for (int q = 0; q < 16; ++q) write_one(0, q, rg[q]);
+        for (int q = 0; q < 2 * CPO; ++q) write_one(0, q, rg[q]);
 #pragma unroll
-        for (int q = 0; q < 16; ++q) rg[q] = load_one(t1, q);
+        for (int q = 0; q < 2 * CPO; ++q) rg[q] = load_one(t1, q);
     }
     __syncthreads();
     read_frags(0, 0, a0, b0);
@@ -1058,7 +1075,7 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         step(a0, b0, 0, nxt, tl, rg);
         __builtin_amdgcn_sched_barrier(0);
         read_frags(cur, 2, a0, b0);
-        step(a1, b1, 8, nxt, tl, rg);
+        step(a1, b1, 2 * CPO > CPS ? CPS : -1, nxt, tl, rg);
         __builtin_amdgcn_sched_barrier(0);
         read_frags(cur, 3, a1, b1);
         step(a0, b0, -1, nxt, tl, rg);
@@ -1069,9 +1086,20 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
+    // accumulator element (i, j, r) of this lane: tile row and column, and the 32-column block j
+    auto for_each_acc = [&](auto&& fn) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    fn(wm * 128 + i * 32 + (r / 4) * 8 + (l / 32) * 4 + (r % 4), wn * WCOLS + j * 32 + l % 32, j,
+                       acc[i][j][r]);
+    };
     if constexpr (MODE == kWideFWD) {
         const uint16_t* __restrict__ bias = args.bias;
-        for_each_acc256(acc, [&](int r, int c, float v) {
+        for_each_acc([&](int r, int c, int, float v) {
             const int m = m0 + r, n = n0 + c;
             if (m < M && n < Nn) stf<TO>(out, (int64_t)m * ldo + n, bias ? v + bf16_to_f32(bias[n]) : v);
         });
@@ -1079,12 +1107,12 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
     }
     const float alpha = *alpha_p;
     if (part == nullptr) {
-        rv_s[threadIdx.x] = rv_reg;
+        if ((int)threadIdx.x < LB) rv_s[threadIdx.x] = rv_reg;
         __syncthreads();
-        for_each_acc256(acc, [&](int r, int c, float v) {
+        for_each_acc([&](int r, int c, int j, float v) {
             const int m = m0 + r, n = n0 + c;
             if (m < M && n < Nn) {
-                const float x = fmaf(alpha, v, rv_s[r] * cvv[(c >> 5) & 3]);
+                const float x = fmaf(alpha, v, rv_s[r] * cvv[j]);
                 if constexpr (IS_DW) {
                     float* p = reinterpret_cast<float*>(out) + (int64_t)m * ldo + n;
                     *p = beta != 0.f ? x + beta * *p : x;
@@ -1095,38 +1123,38 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         });
     } else {
         float* pz = part + (int64_t)kz * tr.pstride;
-        for_each_acc256(acc, [&](int r, int c, float v) {
+        for_each_acc([&](int r, int c, int, float v) {
             const int m = m0 + r, n = n0 + c;
             if (m < M && n < Nn) pz[(int64_t)(m - tr.pm0) * tr.ldp + (n - tr.pn0)] = alpha * v;
         });
     }
 }
 
-template <bool IS_DW, typename TO>
-__global__ __launch_bounds__(256, 1) void lds256w_kernel(WideArgs a) {
+template <bool IS_DW, typename TO, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void lds256w_kernel(WideArgs a) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    wide_tile<IS_DW ? kWideDW : kWideDH, TO>(a, blockIdx.x, lds, rv_s);
+    wide_tile<IS_DW ? kWideDW : kWideDH, TO, NW>(a, blockIdx.x, lds, rv_s);
 }
 
 // The head forward Z = H W (+ b) in bf16 on the same tiles (fp32 accumulation, one rounding of Z).
-template <typename TO>
-__global__ __launch_bounds__(256, 1) void lds256w_fwd_kernel(WideArgs a) {
+template <typename TO, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void lds256w_fwd_kernel(WideArgs a) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    wide_tile<kWideFWD, TO>(a, blockIdx.x, lds, rv_s);
+    wide_tile<kWideFWD, TO, NW>(a, blockIdx.x, lds, rv_s);
 }
 
 // Both products in one grid: blocks [0, nh) run dH's units (the long k ranges first), the rest dW's
 // tiles, so that the shorter dW tiles fill the compute units that dH's last round leaves idle instead of
 // a second launch starting after a partly empty round. nh is a multiple of 8, so each part keeps its
 // own XCD order.
-template <typename TO>
-__global__ __launch_bounds__(256, 1) void lds256w_pair_kernel(WideArgs h, WideArgs w, int nh) {
+template <typename TO, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void lds256w_pair_kernel(WideArgs h, WideArgs w, int nh) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    if ((int)blockIdx.x < nh) wide_tile<kWideDH, TO>(h, blockIdx.x, lds, rv_s);
-    else wide_tile<kWideDW, float>(w, (int)blockIdx.x - nh, lds, rv_s);
+    if ((int)blockIdx.x < nh) wide_tile<kWideDH, TO, NW>(h, blockIdx.x, lds, rv_s);
+    else wide_tile<kWideDW, float, NW>(w, (int)blockIdx.x - nh, lds, rv_s);
 }
 
 // Split-K reduction for the rank-1 form over the rectangle [pm0, M) x [pn0, Nn) of the output, in split
@@ -1598,6 +1626,25 @@ const PlanOverride& plan_override() {
     return o;
 }
 
+// Waves per workgroup of the 64-deep kernels, per product (dH, dW, forward, the pair launch): four, or
+// eight (two per SIMD). Environment BOM_VJP_WAVES = "dH,dW,fwd,pair" overrides for A/B measurement
+// (read once; values other than 4 and 8 keep the default).
+struct WaveCfg {
+    int dh = 8, dw = 8, fwd = 8, pair = 8;
+};
+const WaveCfg& wave_cfg() {
+    static const WaveCfg c = [] {
+        WaveCfg r;
+        int v[4] = {0, 0, 0, 0};
+        if (const char* e = getenv("BOM_VJP_WAVES")) sscanf(e, "%d,%d,%d,%d", &v[0], &v[1], &v[2], &v[3]);
+        int* f[4] = {&r.dh, &r.dw, &r.fwd, &r.pair};
+        for (int i = 0; i < 4; ++i)
+            if (v[i] == 4 || v[i] == 8) *f[i] = v[i];
+        return r;
+    }();
+    return c;
+}
+
 void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int64_t K) {
     if (g.kind == kSimt) return;
     if (kind == kMfma128) g.kind = kMfma128;
@@ -1755,10 +1802,15 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
             auto launch = [&](int ob, int oe, int nsplit, int kp, float* pp, const TileRange& tr) {
                 dim3 gr((unsigned)(cdiv((int64_t)(oe - ob) * nsplit, 8) * 8 * inner));
                 const WideArgs wa{a16, lda, b16, ldb, M, Nn, K, kp, tr, f.scal, rv, cv, out, ldo, beta, pp, nullptr};
-                if (is_dw)
-                    hipLaunchKernelGGL((lds256w_kernel<true, float>), gr, dim3(256), 0, st, wa);
+                const int nw = is_dw ? wave_cfg().dw : wave_cfg().dh;
+                if (is_dw && nw == 8)
+                    hipLaunchKernelGGL((lds256w_kernel<true, float, 8>), gr, dim3(512), 0, st, wa);
+                else if (is_dw)
+                    hipLaunchKernelGGL((lds256w_kernel<true, float, 4>), gr, dim3(256), 0, st, wa);
+                else if (nw == 8)
+                    hipLaunchKernelGGL((lds256w_kernel<false, TO, 8>), gr, dim3(512), 0, st, wa);
                 else
-                    hipLaunchKernelGGL((lds256w_kernel<false, TO>), gr, dim3(256), 0, st, wa);
+                    hipLaunchKernelGGL((lds256w_kernel<false, TO, 4>), gr, dim3(256), 0, st, wa);
                 return hipGetLastError();
             };
             if (dp > 0) {
@@ -1986,9 +2038,17 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
         const int nh = (int)(cdiv((int64_t)oh * sh, 8) * 8 * inner);
         const int nw = (int)(cdiv(ow, 8) * 8 * inner);
         if (a.dh_dt == BOM_BF16)
-            hipLaunchKernelGGL(lds256w_pair_kernel<uint16_t>, dim3((unsigned)(nh + nw)), dim3(256), 0, st, wh, ww, nh);
+            if (wave_cfg().pair == 8)
+                hipLaunchKernelGGL((lds256w_pair_kernel<uint16_t, 8>), dim3((unsigned)(nh + nw)), dim3(512), 0, st, wh, ww,
+                                   nh);
+            else
+                hipLaunchKernelGGL((lds256w_pair_kernel<uint16_t, 4>), dim3((unsigned)(nh + nw)), dim3(256), 0, st, wh, ww,
+                                   nh);
         else
-            hipLaunchKernelGGL(lds256w_pair_kernel<float>, dim3((unsigned)(nh + nw)), dim3(256), 0, st, wh, ww, nh);
+            if (wave_cfg().pair == 8)
+                hipLaunchKernelGGL((lds256w_pair_kernel<float, 8>), dim3((unsigned)(nh + nw)), dim3(512), 0, st, wh, ww, nh);
+            else
+                hipLaunchKernelGGL((lds256w_pair_kernel<float, 4>), dim3((unsigned)(nh + nw)), dim3(256), 0, st, wh, ww, nh);
         if ((e = hipGetLastError()) != hipSuccess || sh == 1) return e;
         const int64_t MN = (int64_t)a.N * a.d;
         if (a.dh_dt == BOM_BF16)
@@ -2081,7 +2141,11 @@ hipError_t launch_head_forward(const void* H, int64_t ldh, const void* W, int64_
         const TileRange tr{MT, 0, NT, 1, 0, 0, 0, 0};
         const WideArgs wa{H16, ldh, W16, ldw, N, V, d, (int)(cdiv(d, WKT) * WKT), tr, nullptr, nullptr, nullptr, Z, ldz,
                           0.f, nullptr, b16};
-        hipLaunchKernelGGL(lds256w_fwd_kernel<uint16_t>, dim3((unsigned)(cdiv(NT, 8) * 8 * MT)), dim3(256), 0, st, wa);
+        const dim3 grid((unsigned)(cdiv(NT, 8) * 8 * MT));
+        if (wave_cfg().fwd == 8)
+            hipLaunchKernelGGL((lds256w_fwd_kernel<uint16_t, 8>), grid, dim3(512), 0, st, wa);
+        else
+            hipLaunchKernelGGL((lds256w_fwd_kernel<uint16_t, 4>), grid, dim3(256), 0, st, wa);
         return hipGetLastError();
     }
     dim3 grid((V + SB - 1) / SB, (N + SB - 1) / SB);

@@ -1055,6 +1055,18 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
             }
         }
     };
+    // scheduling of a step without copies: the next step's fragment reads (issued before the step)
+    // spread one group after each MFMA instead of ahead of them all
+    constexpr int kReads = (KA ? 4 : 8) + (KB ? NJ : 2 * NJ);   // LDS read instructions per step
+    constexpr int kRpm = (kReads + 7) / 8;
+    auto spread_reads = [&]() {
+#pragma unroll
+        for (int q = 0; q < kReads / kRpm; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, kRpm, 0);   // LDS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * NJ - kReads / kRpm, 0);
+    };
     u32x4_t rg[2 * CPO];
     bf16x8_t a0[4], b0[NJ], a1[4], b1[NJ];
     {
@@ -1076,13 +1088,16 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         __builtin_amdgcn_sched_barrier(0);
         read_frags(cur, 2, a0, b0);
         step(a1, b1, 2 * CPO > CPS ? CPS : -1, nxt, tl, rg);
+        if constexpr (2 * CPO <= CPS) spread_reads();
         __builtin_amdgcn_sched_barrier(0);
         read_frags(cur, 3, a1, b1);
         step(a0, b0, -1, nxt, tl, rg);
+        spread_reads();
         asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
         __builtin_amdgcn_sched_barrier(0);
         read_frags(nxt, 0, a0, b0);
         step(a1, b1, -1, nxt, tl, rg);
+        spread_reads();
         __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();

@@ -9,8 +9,9 @@ the paper's order for the multi-step loop.
 Every function takes the exact fp64 images of the inputs (bf16 and fp32 widen exactly).
 Pins: every function here is checked by ``tests/test_oracle_pins.py`` against what the paper
 and the mathematics fix (closed forms, brute-force Jacobians, finite differences, explicit
-EMA sums, Lemma 2, the linear-model equivalence of BOM and the own-step control, and the
-Adafactor rank-1 identity for the factored second moment, whose definition is a reading).
+EMA sums, Lemma 2, the linear-model equivalence of BOM and the own-step control, the
+Adafactor rank-1 identity for the factored second moment, whose definition is a reading, and the
+reduction of the block-shared second moment to the dense one at block length 1).
 """
 from __future__ import annotations
 
@@ -58,6 +59,8 @@ def _load():
                                          f64, i64]
         lib.orc_update_factored.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp, vp, vp, ctypes.c_int, f64, f64,
                                             f64, f64, f64, f64, i64]
+        lib.orc_update_blocks.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp, vp, ctypes.c_int, f64, f64, f64, f64, f64,
+                                          i64]
         lib.orc_head_forward.argtypes = [vp, i64, i64, vp, i64, vp, vp]
         lib.orc_clip_factor.argtypes = [vp, vp, i64, f64, f64, f64]
         lib.orc_round_bf16.argtypes = [vp, i64, vp]
@@ -246,6 +249,33 @@ def update_factored(theta, Rr, Cc, u, *, lr, beta2, eps, t, block_rows, block_co
                                 _p(wd), ns, float(weight_decay), float(lr), float(beta2), float(eps), float(lam),
                                 float(u_scale), int(t))
     return theta, Rr, Cc
+
+
+def blocks_count(segments, blocks) -> int:
+    """Entries of the block-shared second moment: sum over segments of ceil(length / block)."""
+    return int(sum(-(-int(sg[1]) // int(bk)) for sg, bk in zip(segments, blocks)))
+
+
+def update_blocks(theta, v, u, *, lr, beta2, eps, t, segments, blocks, h=None, lam=0.5, u_scale=1.0,
+                  clip_norm=0.0):
+    """Block-shared second moment (Adam-mini's map with the BOM numerator). segments = [(offset, length,
+    weight_decay)] tiling [0, P) in order, blocks = block length per segment. Returns (theta_new, v_new)
+    in fp64; inputs are not modified. clip_norm as in update_dense."""
+    theta, v, u = _f64(theta).copy(), _f64(v).copy(), _f64(u)
+    h = None if h is None else _f64(h)
+    segments, blocks = list(segments), [int(b) for b in blocks]
+    assert len(segments) == len(blocks) and segments, "one block length per segment"
+    pos = 0
+    for (o, n, _), bk in zip(segments, blocks):
+        assert o == pos and n >= 1 and bk >= 1, "segments must tile [0, P) in order"
+        pos += n
+    assert pos == theta.size and v.size == blocks_count(segments, blocks), "block state shape"
+    u_scale = u_scale * clip_factor(u, h=h, lam=lam, u_scale=u_scale, clip_norm=clip_norm)
+    off, ln, wd, ns = _segs(segments)
+    blk = np.array(blocks, np.int64)
+    _load().orc_update_blocks(_p(theta), _p(v), _p(u), _p(h), theta.size, _p(off), _p(ln), _p(wd), _p(blk), ns,
+                              float(lr), float(beta2), float(eps), float(lam), float(u_scale), int(t))
+    return theta, v
 
 
 def head_forward(H, W, b=None):

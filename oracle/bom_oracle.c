@@ -348,6 +348,47 @@ void orc_update_factored(double* theta, double* Rr, double* Cc, const double* u,
 }
 
 /*
+ * Block-shared second moment: Adam-mini's update map driven by the BOM numerator. Sec. 3.5 deletes the
+ * base optimizer's first moment and feeds the numerator u' to its map Phi(a, v); for Adam-mini that map
+ * is a / (sqrt(v_hat) + eps) with one second-moment value per block of parameters, the block average of
+ * the squared numerator feeding its EMA. The segments tile [0, P) in order and segment k is cut into
+ * consecutive blocks of seg_blk[k] elements (the last one may be shorter). For block b with elements E_b:
+ *   v_b = beta2 v_b + (1 - beta2) (1/|E_b|) sum_{e in E_b} u'_e^2,   v_hat_b = v_b / (1 - beta2^t),
+ *   theta_e = (1 - lr * omega_k) theta_e - lr * u'_e / (sqrt(v_hat_b) + eps),
+ * omega_k the weight decay of the segment. v lists the blocks of segment 0, then of segment 1, ...
+ * A block length of 1 is the elementwise second moment of orc_update_dense.
+ */
+void orc_update_blocks(double* theta, double* v, const double* u, const double* h, int64_t P,
+                       const int64_t* seg_off, const int64_t* seg_len, const double* seg_wd, const int64_t* seg_blk,
+                       int nsegs, double lr, double beta2, double eps, double lambda, double u_scale, int64_t t) {
+    double bc2 = 1.0 - pow(beta2, (double)t);
+    int64_t vbase = 0;
+    (void)P;
+    for (int k = 0; k < nsegs; ++k) {
+        int64_t len = seg_len[k], blk = seg_blk[k];
+        int64_t nblk = (len + blk - 1) / blk;
+#pragma omp parallel for schedule(static)
+        for (int64_t b = 0; b < nblk; ++b) {
+            int64_t e0 = seg_off[k] + b * blk;
+            int64_t e1 = e0 + blk < seg_off[k] + len ? e0 + blk : seg_off[k] + len;
+            double ss = 0.0;
+            for (int64_t e = e0; e < e1; ++e) {
+                double up = orc_numerator(u, h, e, lambda, u_scale);
+                ss += up * up;
+            }
+            double* vb = v + vbase + b;
+            *vb = beta2 * *vb + (1.0 - beta2) * ss / (double)(e1 - e0);
+            double denom = sqrt(*vb / bc2) + eps;
+            for (int64_t e = e0; e < e1; ++e) {
+                double up = orc_numerator(u, h, e, lambda, u_scale);
+                theta[e] = (1.0 - lr * seg_wd[k]) * theta[e] - lr * up / denom;
+            }
+        }
+        vbase += nblk;
+    }
+}
+
+/*
  * Historical-projection drift telemetry of the linear head (Sec. 3.3, Eq. (8);
  * appendix "Historical-Projection Control" and appendix "Measuring historical projection drift").
  * For z_i = W^T h_i + b the batch-mean Jacobian maps a task-space vector x to Jbar^T x = (hbar x^T, x),

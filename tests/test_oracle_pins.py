@@ -445,6 +445,83 @@ def test_factored_zero_block_keeps_decay_only():
     np.testing.assert_allclose(thf, (1 - 1e-3) * th, rtol=1e-15)
 
 
+# Block-shared second moment: Adam-mini's map with the BOM numerator (Sec. 3.5, the substitution into a
+# base optimizer's update map; Adam-mini shares one second-moment value per block).
+def test_blocks_of_one_are_the_dense_update():
+    r = _rng(33)
+    P = 700
+    th, u, v0 = r.standard_normal(P), r.standard_normal(P) * 1e-3, np.abs(r.standard_normal(P)) * 1e-6
+    segs = [(0, 300, 0.01), (300, 150, 0.0), (450, 250, 0.1)]
+    tb, vb = oracle.update_blocks(th, v0, u, lr=1e-2, beta2=B2, eps=EPS, t=3, segments=segs, blocks=[1, 1, 1])
+    td, vd = oracle.update_dense(th, v0, u, lr=1e-2, beta2=B2, eps=EPS, t=3, segments=segs, weight_decay=0.5)
+    np.testing.assert_allclose(tb, td, rtol=1e-15, atol=1e-18)
+    np.testing.assert_allclose(vb, vd, rtol=1e-15)
+
+
+def test_blocks_first_step_closed_form():
+    # t = 1, v = 0: v_hat_b is the block mean of u^2. Blocks [1, 2, 2] (mean 3) and [3, 4] (mean 12.5),
+    # then [0, 0] (a zero block keeps only the decay) and the single element [-2].
+    u = np.array([1.0, 2.0, 2.0, 3.0, 4.0, 0.0, 0.0, -2.0])
+    th = np.array([0.0, 0.0, 0.0, 0.0, 0.0, 1.0, -1.0, 0.5])
+    segs = [(0, 5, 0.0), (5, 2, 0.5), (7, 1, 0.0)]
+    t1, v1 = oracle.update_blocks(th, np.zeros(4), u, lr=0.1, beta2=B2, eps=EPS, t=1, segments=segs,
+                                  blocks=[3, 2, 4])
+    r3, r12 = math.sqrt(3.0) + EPS, math.sqrt(12.5) + EPS
+    expect = [-0.1 / r3, -0.2 / r3, -0.2 / r3, -0.3 / r12, -0.4 / r12, 0.95, -0.95, 0.5 + 0.2 / (2.0 + EPS)]
+    np.testing.assert_allclose(t1, expect, rtol=1e-14)
+    np.testing.assert_allclose(v1, (1 - B2) * np.array([3.0, 12.5, 0.0, 4.0]), rtol=1e-14)
+
+
+def test_blocks_second_moment_explicit_sum_and_ragged_tail():
+    r = _rng(34)
+    P, T, blk = 23, 5, 5           # blocks of 5, 5, 5, 5, 3
+    U = r.standard_normal((T, P))
+    th = r.standard_normal(P)
+    v = np.zeros(5)
+    bidx = np.arange(P) // blk
+    for t in range(1, T + 1):
+        th_prev = th
+        th, v = oracle.update_blocks(th, v, U[t - 1], lr=1e-3, beta2=B2, eps=EPS, t=t, segments=[(0, P, 0.0)],
+                                     blocks=[blk])
+        means = [np.array([np.mean(U[tau - 1][bidx == b] ** 2) for b in range(5)]) for tau in range(1, t + 1)]
+        expect_v = sum((1 - B2) * B2 ** (t - tau) * means[tau - 1] for tau in range(1, t + 1))
+        np.testing.assert_allclose(v, expect_v, rtol=1e-13)
+        vhat = expect_v[bidx] / (1 - B2 ** t)
+        np.testing.assert_allclose(th, th_prev - 1e-3 * U[t - 1] / (np.sqrt(vhat) + EPS), rtol=1e-13)
+
+
+def test_blocks_invariances():
+    # a permutation inside every block permutes the step and leaves v unchanged; with eps = 0 the step
+    # does not change when the numerator and the second moment are scaled together (u -> k u, v -> k^2 v)
+    r = _rng(35)
+    P, blk = 48, 12
+    th, u, v0 = r.standard_normal(P), r.standard_normal(P), np.abs(r.standard_normal(4))
+    perm = np.concatenate([b * blk + r.permutation(blk) for b in range(4)])
+    kw = dict(lr=1e-2, beta2=B2, t=2, segments=[(0, P, 0.1)], blocks=[blk])
+    ta, va = oracle.update_blocks(th, v0, u, eps=EPS, **kw)
+    tp, vp = oracle.update_blocks(th[perm], v0, u[perm], eps=EPS, **kw)
+    np.testing.assert_allclose(tp, ta[perm], rtol=1e-14)
+    np.testing.assert_allclose(vp, va, rtol=1e-14)
+    t0, _ = oracle.update_blocks(th, v0, u, eps=0.0, **kw)
+    tk, vk = oracle.update_blocks(th, 9.0 * v0, 3.0 * u, eps=0.0, **kw)
+    np.testing.assert_allclose(tk, t0, rtol=1e-13)
+    np.testing.assert_allclose(vk, 9.0 * va, rtol=1e-13)
+
+
+def test_blocks_split_numerator_and_clipping():
+    r = _rng(36)
+    P = 40
+    th, g, h = r.standard_normal(P), r.standard_normal(P), r.standard_normal(P)
+    kw = dict(lr=1e-3, beta2=B2, eps=EPS, t=2, segments=[(0, 25, 0.0), (25, 15, 0.1)], blocks=[10, 4])
+    v0 = np.abs(r.standard_normal(oracle.blocks_count(kw["segments"], kw["blocks"])))
+    a = oracle.update_blocks(th, v0, g, h=h, lam=0.3, u_scale=0.7, clip_norm=0.5, **kw)
+    c = oracle.clip_factor(g, h=h, lam=0.3, u_scale=0.7, clip_norm=0.5)
+    assert c < 1.0
+    b = oracle.update_blocks(th, v0, c * 0.7 * (0.7 * g + 0.3 * h), **kw)
+    np.testing.assert_allclose(a[0], b[0], rtol=1e-14)
+    np.testing.assert_allclose(a[1], b[1], rtol=1e-14)
+
+
 # Global-norm clipping of the numerator (appendix "Pretraining Parameters": clipping at 1.0; appendix
 # "Conditional Descent and Stationarity": the numerator supplied to the adaptive update includes it).
 

@@ -69,11 +69,35 @@ def fill_normal_(t: torch.Tensor, stream: int, std: float, chunk: int = 1 << 27)
             log(f"[bench] generated {start + m} of {n} values of stream {stream}")
 
 
+def adam_mini_partition(w):
+    """Segments tiling the flat buffer and their block lengths, shaped like Adam-mini's partition of a
+    transformer: the head slice and the bias per element (the class blocks of Adam-mini's classifier branch
+    are columns of the [d, V] head here, not contiguous), then the backbone with one sixth in per-head blocks
+    (64 rows of d: query and key are 2 of a layer's 12 d x d matrices) and the rest per output neuron
+    (blocks of d)."""
+    hp = w.head_params
+    segs, blocks = [(0, w.d * w.V, w.weight_decay)], [1]
+    if w.has_bias:
+        segs.append((w.d * w.V, w.V, 0.0))
+        blocks.append(1)
+    rest = w.P - hp
+    blk_head = 64 * w.d
+    n_head = (rest // 6) // blk_head * blk_head
+    if n_head > 0:
+        segs.append((hp, n_head, w.weight_decay))
+        blocks.append(blk_head)
+    if rest - n_head > 0:
+        segs.append((hp + n_head, rest - n_head, w.weight_decay))
+        blocks.append(w.d)
+    return segs, blocks
+
+
 class Problem:
     """Device-resident inputs and state of one workload."""
 
-    def __init__(self, w, dev, clip_norm=0.0, state_dtype=torch.float32):
+    def __init__(self, w, dev, clip_norm=0.0, state_dtype=torch.float32, adam_mini=False):
         self.w = w
+        self.blocks = None
         self.clip_norm = clip_norm
         self.state_dtype = state_dtype
         N, d, V, P = w.N, w.d, w.V, w.P
@@ -96,7 +120,11 @@ class Problem:
             self.theta[d * V:d * V + V].zero_()   # bias starts at 0
         self.u = torch.empty(P, dtype=state_dtype, device=dev)
         fill_normal_(self.u, synth.STREAM_U + 1, 1e-3)
-        if w.factored:
+        if adam_mini:
+            self.segments, self.blocks = adam_mini_partition(w)
+            self.v = torch.zeros(bom.blocks_count(self.segments, self.blocks), dtype=torch.float32, device=dev)
+            self.v_col = None
+        elif w.factored:
             nrows = -(-P // w.block_cols)
             nblocks = -(-nrows // w.block_rows)
             self.v = torch.zeros(nrows, dtype=torch.float32, device=dev)
@@ -107,7 +135,8 @@ class Problem:
         self.q = torch.zeros(V, dtype=torch.float32, device=dev)
         self.q_hat = torch.empty(V, dtype=torch.float32, device=dev)
         self.dH = torch.empty((N, d), dtype=self.Z.dtype, device=dev)
-        self.segments = w.segments()
+        if not adam_mini:
+            self.segments = w.segments()
         # outputs and workspaces allocated once
         self.res = None
         self.ws_res = self.ws_vjp = self.ws_upd = None
@@ -136,9 +165,10 @@ class Problem:
         self.ws_vjp = g["workspace"]
         if ev is not None:
             ev[3].record()
-        cfg = bom.make_update_cfg(lr=w.lr, beta2=w.beta2, eps=w.eps, t=t, lam=w.lam, factored=w.factored,
-                                  block_rows=w.block_rows, block_cols=w.block_cols, clip_norm=self.clip_norm,
-                                  state_dtype=self.state_dtype)
+        cfg = bom.make_update_cfg(lr=w.lr, beta2=w.beta2, eps=w.eps, t=t, lam=w.lam,
+                                  factored=w.factored and self.blocks is None, block_rows=w.block_rows,
+                                  block_cols=w.block_cols, clip_norm=self.clip_norm, state_dtype=self.state_dtype,
+                                  blocks=self.blocks)
         self.ws_upd = bom.bom_update(self.theta, self.v, self.u, cfg, v_col=self.v_col, segments=self.segments,
                                      workspace=self.ws_upd)
         if ev is not None:
@@ -198,10 +228,11 @@ def time_telemetry(prob, steps):
             "last": stats}
 
 
-def algorithmic(w, clip=False, bf16_state=False):
+def algorithmic(w, clip=False, bf16_state=False, blocks=None):
     """Algorithmic bytes / flops of each stage for one step (what BOM must move or compute). With
     global-norm clipping the dense update reads u once more for the norm; the factored update takes
-    the norm from its row statistics (a row-sized array written once and read twice)."""
+    the norm from its row statistics (a row-sized array written once and read twice). blocks: the
+    (segments, block lengths) of the block-shared second moment."""
     esz = 2 if w.dtype == "bf16" else 4
     N, d, V, P = w.N, w.d, w.V, w.P
     out = {
@@ -211,7 +242,18 @@ def algorithmic(w, clip=False, bf16_state=False):
         "bom_head_vjp": dict(bound="mfma" if w.dtype == "bf16" else "alu", amount=4 * N * d * V,
                              per_unit="4*N*d*V flop (dW and dH)"),
     }
-    if w.factored:
+    if blocks is not None:
+        # per element: 20 B (read theta, v, u; write theta, v); blocks of up to 4096: 12 B (read u, theta;
+        # write theta); longer blocks: 16 B (u read twice); 8 B per block entry of v; clipping: 4 B more
+        amount = 0
+        for (o, n, _), bk in zip(*blocks):
+            per = 20 if bk == 1 else (12 if min(bk, n) <= 4096 else 16)
+            amount += per * n + (0 if bk == 1 else 8 * -(-n // bk)) + (4 * n if clip else 0)
+        out["bom_update"] = dict(bound="hbm", amount=amount,
+                                 per_unit="20 B per parameter with its own v, 12 B in blocks of up to 4096 (read u "
+                                          "and theta, write theta), 16 B in longer blocks (u read twice), 8 B per "
+                                          "block" + ("; +4 B per parameter for the norm" if clip else ""))
+    elif w.factored:
         nrows = -(-P // w.block_cols)
         nblocks = -(-nrows // w.block_rows)
         out["bom_update"] = dict(bound="hbm", amount=16 * P + 8 * nrows + 8 * nblocks * w.block_cols
@@ -375,6 +417,9 @@ def main():
     ap.add_argument("--clip-norm", type=float, default=0.0,
                     help="global-norm clipping of the update numerator at this norm (0: none; the paper's "
                          "language-model protocols clip at 1.0)")
+    ap.add_argument("--adam-mini", action="store_true",
+                    help="block-shared second moment (Adam-mini's update map with the BOM numerator) over a "
+                         "transformer-shaped partition of the flat buffer, instead of the dense or factored one")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="host seconds the oracle baseline aims to spend (a bounded sample of the workload)")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
@@ -406,7 +451,10 @@ def main():
     if state_dtype == torch.bfloat16 and (w.factored or w.dtype != "bf16"):
         print("bf16 state storage applies to the dense layout with bf16 logits", file=sys.stderr)
         sys.exit(2)
-    prob = Problem(w, dev, clip_norm=args.clip_norm, state_dtype=state_dtype)
+    if args.adam_mini and state_dtype == torch.bfloat16:
+        print("the block-shared second moment keeps fp32 state", file=sys.stderr)
+        sys.exit(2)
+    prob = Problem(w, dev, clip_norm=args.clip_norm, state_dtype=state_dtype, adam_mini=args.adam_mini)
     stages = ["bom_residual", "bom_ema", "bom_head_vjp", "bom_update"]
 
     t = 0
@@ -435,7 +483,8 @@ def main():
                 for i, s in enumerate(stages)}
     log(f"[bench] timed {args.steps} steps: {ms_per_step:.4f} ms/step (wall {wall:.2f}s)")
 
-    alg = algorithmic(w, clip=args.clip_norm > 0, bf16_state=state_dtype == torch.bfloat16)
+    alg = algorithmic(w, clip=args.clip_norm > 0, bf16_state=state_dtype == torch.bfloat16,
+                      blocks=(prob.segments, prob.blocks) if args.adam_mini else None)
     dom = max(stages, key=lambda s: stage_ms[s])
     a = alg[dom]
     sec = stage_ms[dom] / 1e3
@@ -447,7 +496,8 @@ def main():
         achieved, peak, unit = a["amount"] / sec / 1e12, FP32_PEAK_TFS, "TFLOP/s"
     roofline = {"bound": a["bound"], "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                 "frac": round(achieved / peak, 4),
-                "traffic": stored_traffic(dom, w.name) if args.clip_norm == 0 and args.state_dtype == "f32" else None,
+                "traffic": (stored_traffic(dom, w.name)
+                            if args.clip_norm == 0 and args.state_dtype == "f32" and not args.adam_mini else None),
                 "kernel": dom,
                 "algorithmic_per_launch": a["amount"], "per_unit": a["per_unit"]}
     per_stage = {}
@@ -477,7 +527,8 @@ def main():
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "N": w.N, "d": w.d, "V": w.V, "P": w.P, "tokens_per_step": n_valid,
-                   "second_moment": "factored" if w.factored else "dense", "clip_norm": args.clip_norm,
+                   "second_moment": "blocks" if args.adam_mini else ("factored" if w.factored else "dense"),
+                   "clip_norm": args.clip_norm,
                    "state_dtype": args.state_dtype},
         "stages": per_stage,
         "roofline": roofline,

@@ -63,6 +63,7 @@ typedef enum { BOM_F32 = 0, BOM_BF16 = 1 } bom_dtype;
 /* Second-moment layouts of bom_update. */
 #define BOM_V_DENSE 0
 #define BOM_V_FACTORED 1
+#define BOM_V_BLOCKS 2
 
 #define BOM_MAX_SEGMENTS 16
 
@@ -184,6 +185,21 @@ bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, 
  *   workspace: at least bom_update_workspace_bytes(P, cfg) bytes (0 for the dense layout without
  *         clipping), 256-byte aligned.
  *
+ * BOM_V_BLOCKS (Adam-mini's update map driven by the BOM numerator: Sec. 3.5 substitutes the numerator
+ * into a base optimizer's map, and Adam-mini shares one second-moment value per block of parameters):
+ * the segments must tile [0, P) in order (offset 0, each next offset the previous end, the last end P;
+ * at most BOM_MAX_SEGMENTS per call, so a longer partition takes one call per run of segments on the
+ * matching sub-ranges), and cfg->seg_blocks[k] >= 1 cuts segment k into consecutive blocks of that many
+ * elements (the last one may be shorter). For block b with elements E_b:
+ *   v_b = beta2 v_b + (1 - beta2) mean_{e in E_b} u'_e^2,  v_hat_b = v_b / (1 - beta2^t),
+ *   theta_e = (1 - lr * omega) theta_e - lr * u'_e / (sqrt(v_hat_b) + eps).
+ * Adam-mini's partition maps onto segments: one block per attention head (head_dim rows of a row-major
+ * [out, in] weight), per output neuron (one row), per tensor (one block), or per element (block 1).
+ *   v     device fp32 [sum_k ceil(length_k / seg_blocks[k])]: the blocks of segment 0, then 1, ...
+ *   v_col NULL.  fp32 state only.
+ *   workspace: at least bom_update_workspace_bytes(P, cfg) bytes (partial sums of blocks longer than
+ *         4096 elements, bounded by P / 1024 + 64 floats, and the clipping pass).
+ *
  * Global-norm clipping (cfg->clip_norm > 0; appendix "Pretraining Parameters" and appendix "Memory
  * and Timing Protocols" clip at 1.0, and appendix "Conditional Descent and Stationarity" counts the
  * clipping as part of the numerator supplied to the adaptive update): u' above is replaced by c u' with
@@ -196,7 +212,7 @@ bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, 
  * bf16 state storage (cfg->state_dt = BOM_BF16; appendix "NLP Fine-Tuning Parameters": bf16 parameter
  * and optimizer-state storage, the task-space EMA kept in fp32): theta, v, u and h are bf16; the step
  * is computed in fp32 from their values and theta and v are rounded to the nearest bf16 (ties to
- * even) when stored: 10 bytes per parameter instead of 20. Dense layout only (factored: BOM_ERR_DTYPE).
+ * even) when stored: 10 bytes per parameter instead of 20. Dense layout only (other layouts: BOM_ERR_DTYPE).
  * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_DTYPE, BOM_ERR_HYPER (beta2 not in [0,1), t < 1,
  *         eps <= 0, lambda not in [0,1], non-finite lr / u_scale / decay, clip_norm negative or not
  *         finite), BOM_ERR_ALIAS, BOM_ERR_WORKSPACE, BOM_ERR_HIP.
@@ -210,11 +226,12 @@ typedef struct {
 typedef struct {
     float lr, beta2, eps, lambda, u_scale;
     int64_t t;
-    int32_t v_layout; /* BOM_V_DENSE or BOM_V_FACTORED */
+    int32_t v_layout; /* BOM_V_DENSE, BOM_V_FACTORED or BOM_V_BLOCKS */
     int64_t block_rows, block_cols;
     float clip_norm;   /* > 0: global-norm clipping of the numerator at this norm; 0: none */
     float* clip_stats; /* device fp32 [2] or NULL: receives ||u'|| before clipping and the factor c */
     int32_t state_dt;  /* BOM_F32, or BOM_BF16: theta, v, u and h stored as bf16 (dense layout) */
+    const int64_t* seg_blocks; /* BOM_V_BLOCKS: HOST array of nsegs block lengths; otherwise ignored */
 } bom_update_cfg;
 
 size_t bom_update_workspace_bytes(int64_t P, const bom_update_cfg* cfg);

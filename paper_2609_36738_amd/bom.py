@@ -17,7 +17,7 @@ from . import _build
 BOM_OK = 0
 BOM_F32, BOM_BF16 = 0, 1
 BOM_FLAG_LABEL_RANGE, BOM_FLAG_EMPTY = 1, 2
-BOM_V_DENSE, BOM_V_FACTORED = 0, 1
+BOM_V_DENSE, BOM_V_FACTORED, BOM_V_BLOCKS = 0, 1, 2
 BOM_MAX_SEGMENTS = 16
 
 _lock = threading.Lock()
@@ -39,7 +39,8 @@ class bom_update_cfg(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float), ("lambda_", ctypes.c_float),
                 ("u_scale", ctypes.c_float), ("t", ctypes.c_int64), ("v_layout", ctypes.c_int32),
                 ("block_rows", ctypes.c_int64), ("block_cols", ctypes.c_int64), ("clip_norm", ctypes.c_float),
-                ("clip_stats", ctypes.c_void_p), ("state_dt", ctypes.c_int32)]
+                ("clip_stats", ctypes.c_void_p), ("state_dt", ctypes.c_int32),
+                ("seg_blocks", ctypes.POINTER(ctypes.c_int64))]
 
 
 def lib_path() -> str:
@@ -207,19 +208,33 @@ def bom_head_vjp(H, W, R, labels, q_hat, n_valid, *, s=None, lam=0.5, ignore_ind
 
 
 def make_update_cfg(*, lr, beta2, eps, t, lam=0.5, u_scale=1.0, factored=False, block_rows=4096, block_cols=4096,
-                    clip_norm=0.0, clip_stats=None, state_dtype=torch.float32):
+                    clip_norm=0.0, clip_stats=None, state_dtype=torch.float32, blocks=None):
     """clip_norm > 0 turns on global-norm clipping; clip_stats (a device fp32 tensor of 2) receives the
     numerator's norm before clipping and the factor. state_dtype torch.bfloat16 selects bf16 storage
-    of theta, v, u and h (dense layout)."""
+    of theta, v, u and h (dense layout). blocks (one block length per segment) selects the block-shared
+    second moment; the segments passed to bom_update must then tile the buffer in order."""
+    if factored and blocks is not None:
+        raise ValueError("choose the factored or the block layout, not both")
     if state_dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("state_dtype must be torch.float32 or torch.bfloat16")
     if clip_stats is not None and (clip_stats.dtype != torch.float32 or not clip_stats.is_cuda or
                                    clip_stats.numel() < 2 or not clip_stats.is_contiguous()):
         raise ValueError("clip_stats must be a contiguous device float32 tensor of at least 2 elements")
-    return bom_update_cfg(lr, beta2, eps, lam, u_scale, int(t), BOM_V_FACTORED if factored else BOM_V_DENSE,
-                          block_rows, block_cols, float(clip_norm),
-                          None if clip_stats is None else clip_stats.data_ptr(),
-                          BOM_BF16 if state_dtype == torch.bfloat16 else BOM_F32)
+    layout = BOM_V_FACTORED if factored else (BOM_V_BLOCKS if blocks is not None else BOM_V_DENSE)
+    cfg = bom_update_cfg(lr, beta2, eps, lam, u_scale, int(t), layout, block_rows, block_cols, float(clip_norm),
+                         None if clip_stats is None else clip_stats.data_ptr(),
+                         BOM_BF16 if state_dtype == torch.bfloat16 else BOM_F32)
+    if blocks is not None:
+        arr = (ctypes.c_int64 * max(1, len(blocks)))(*[int(b) for b in blocks])
+        cfg.seg_blocks = ctypes.cast(arr, ctypes.POINTER(ctypes.c_int64))
+        cfg._blocks = arr   # keeps the host array alive with the struct
+        cfg._nblocks = len(blocks)
+    return cfg
+
+
+def blocks_count(segments, blocks) -> int:
+    """Entries of the block-shared second moment for these segments and block lengths."""
+    return int(sum(-(-int(s[1]) // int(b)) for s, b in zip(segments, blocks)))
 
 
 def bom_update_workspace_bytes(P: int, cfg: bom_update_cfg) -> int:
@@ -232,9 +247,16 @@ def bom_update(theta, v, u, cfg: bom_update_cfg, *, v_col=None, h=None, segments
     lib = load()
     P = theta.numel()
     want = torch.bfloat16 if cfg.state_dt == BOM_BF16 else torch.float32
-    for name, x in (("theta", theta), ("u", u), ("h", h)) + ((("v", v),) if v_col is None else ()):
+    blocks = cfg.v_layout == BOM_V_BLOCKS
+    for name, x in (("theta", theta), ("u", u), ("h", h)) + ((("v", v),) if v_col is None and not blocks else ()):
         if x is not None and (x.dtype != want or not x.is_contiguous() or x.numel() != P):
             raise ValueError(f"{name} must be a contiguous {want} tensor of {P} elements")
+    if blocks:
+        if getattr(cfg, "_nblocks", -1) != len(segments):
+            raise ValueError("the block layout needs one block length per segment")
+        nv = blocks_count(segments, list(cfg._blocks)[:len(segments)])
+        if v.dtype != torch.float32 or not v.is_contiguous() or v.numel() != nv:
+            raise ValueError(f"v must be a contiguous float32 tensor of {nv} block entries")
     segs = (bom_segment * max(1, len(segments)))(*[bom_segment(int(o), int(n), float(w)) for o, n, w in segments])
     nb = lib.bom_update_workspace_bytes(P, ctypes.byref(cfg))
     workspace = _workspace(nb, theta.device, workspace)

@@ -63,7 +63,7 @@ const char* bom_status_string(bom_status s) {
 
 const char* bom_last_error(void) { return g_last_error; }
 
-int32_t bom_version(void) { return 200; }
+int32_t bom_version(void) { return 20100; }
 
 size_t bom_residual_workspace_bytes(int64_t N, int64_t V, bom_dtype z_dt) {
     if (N < 1 || V < 1 || N >= kMaxDim || V >= kMaxDim || !is_dtype(z_dt)) return 0;
@@ -223,6 +223,34 @@ bom_status bom_update(void* theta_p, void* v_p, float* v_col, const void* u_p, c
                 return fail(BOM_ERR_WORKSPACE, "bom_update: workspace must be 256-byte aligned");
         }
         return hip_status(bom::launch_update_dense(theta, v, u, h, P, st, sc, workspace, strm), "bom_update");
+    }
+    if (c.v_layout == BOM_V_BLOCKS) {
+        if (v_col) return fail(BOM_ERR_SHAPE, "bom_update: v_col must be NULL for the block layout");
+        if (nsegs < 1 || !c.seg_blocks)
+            return fail(BOM_ERR_NULL, "bom_update: the block layout needs segments and cfg->seg_blocks");
+        bom::BlockSegs bs{};
+        bs.n = nsegs;
+        int64_t pos = 0;
+        for (int k = 0; k < nsegs; ++k) {
+            if (segs[k].offset != pos || segs[k].length < 1)
+                return fail(BOM_ERR_SHAPE, "bom_update: block layout segments must tile [0, P) in order (segment %d)", k);
+            if (c.seg_blocks[k] < 1) return fail(BOM_ERR_SHAPE, "bom_update: segment %d block length must be >= 1", k);
+            bs.begin[k] = pos;
+            bs.len[k] = segs[k].length;
+            bs.blk[k] = c.seg_blocks[k];
+            bs.wd[k] = segs[k].weight_decay;
+            pos += segs[k].length;
+        }
+        if (pos != P) return fail(BOM_ERR_SHAPE, "bom_update: block layout segments end at %lld, not P", (long long)pos);
+        const size_t vb = (size_t)bom::blocks_count(bs) * 4;
+        if (overlap(v, vb, theta, pb) || overlap(v, vb, u, pb) || (h && overlap(v, vb, h, pb)))
+            return fail(BOM_ERR_ALIAS, "bom_update: v must not overlap theta, u or h");
+        const size_t need_k = bom::update_workspace_bytes(P, cfg);
+        if (!workspace || ws_bytes < need_k)
+            return fail(BOM_ERR_WORKSPACE, "bom_update: workspace needs %zu bytes, got %zu", need_k, ws_bytes);
+        if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+            return fail(BOM_ERR_WORKSPACE, "bom_update: workspace must be 256-byte aligned");
+        return hip_status(bom::launch_update_blocks(theta, v, u, h, P, bs, sc, workspace, strm), "bom_update");
     }
     if (c.v_layout != BOM_V_FACTORED) return fail(BOM_ERR_SHAPE, "bom_update: unknown v_layout %d", c.v_layout);
     if (!v_col) return fail(BOM_ERR_NULL, "bom_update: the factored layout needs v_col");

@@ -77,6 +77,17 @@ hipError_t launch_update_dense(float* theta, float* v, const float* u, const flo
                                UpdateScalars sc, void* ws, hipStream_t stream);
 hipError_t launch_update_dense_bf16(uint16_t* theta, uint16_t* v, const uint16_t* u, const uint16_t* h, int64_t P,
                                     const SegTable& segs, UpdateScalars sc, void* ws, hipStream_t stream);
+// Block-shared second moment: segments tiling [0, P) in order, each cut into blocks of blk[k] elements.
+struct BlockSegs {
+    int n;
+    int64_t begin[BOM_MAX_SEGMENTS];
+    int64_t len[BOM_MAX_SEGMENTS];
+    int64_t blk[BOM_MAX_SEGMENTS];
+    float wd[BOM_MAX_SEGMENTS];
+};
+int64_t blocks_count(const BlockSegs& b);
+hipError_t launch_update_blocks(float* theta, float* v, const float* u, const float* h, int64_t P, const BlockSegs& bs,
+                                UpdateScalars sc, void* ws, hipStream_t stream);
 hipError_t launch_update_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P,
                                   int64_t block_rows, int64_t block_cols, const SegTable& segs,
                                   const UpdateScalars& sc, void* ws, hipStream_t stream);

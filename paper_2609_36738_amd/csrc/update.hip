@@ -7,6 +7,12 @@
 // Three launches: row/column statistics of u'^2 (one read of u), a per-block finish (Cc and the
 // block sum of Rr), and the parameter update (one more read of u, read + write of theta).
 //
+// Block-shared layout (Adam-mini's map with the BOM numerator): one v per block of consecutive parameters,
+// block lengths per segment. Blocks of up to 4096 elements: one wave per block keeps the block in
+// registers between its statistics and its step (read u and theta, write theta: 12 bytes per parameter).
+// Longer blocks: pieces of 4096 elements, one wave each, for fp32 partial sums, a per-block finish in piece
+// order, and the step (16 bytes per parameter). Blocks of one element take the dense kernels.
+//
 // Global-norm clipping (clip_norm > 0): u' is scaled by c = min(1, clip_norm / (||u'|| + 1e-6)), the
 // norm over the whole buffer, computed on the device. Dense layout: one extra read of the numerator
 // (per-workgroup fp64 partial sums, one finishing workgroup). Factored layout: no extra pass over u;
@@ -446,6 +452,175 @@ __global__ __launch_bounds__(kUpdThreads) void factored_finish_cols_kernel(const
 }
 
 // ---- global-norm clipping ------------------------------------------------------------------
+// ---- block-shared second moment ------------------------------------------------------------------
+// Pointers are at the segment's first element (theta, u, h) and first block (v); len elements, blocks of
+// blk (the last one may be shorter), nblk = ceil(len / blk). VEC: 16-byte accesses (the host checks that
+// the segment's pointers are 16-byte aligned and that blk and len are multiples of 4).
+constexpr int kBlkWave = 4096;                       // longest block held by one wave
+constexpr int kWavesPerWG = kUpdThreads / kWave;
+// partial sums of blocks longer than kBlkWave: a segment of n elements cut into blocks of blk > kBlkWave
+// (blk at most n) has ceil(n / blk) ceil(blk / kBlkWave) <= 3 n / kBlkWave + 1 pieces
+size_t blocks_part_bytes(int64_t P) { return align256((size_t)(P / 1024 + 64) * sizeof(float)); }
+
+template <bool SPLIT, int NV, bool VEC>
+__global__ __launch_bounds__(kUpdThreads) void blocks_wave_kernel(float* __restrict__ theta, float* __restrict__ v,
+                                                                  const float* __restrict__ u,
+                                                                  const float* __restrict__ h, int64_t len,
+                                                                  int64_t blk, int64_t nblk, float wd, UpdateScalars sc) {
+    const int lane = threadIdx.x % kWave;
+    const int64_t b = (int64_t)blockIdx.x * kWavesPerWG + threadIdx.x / kWave;
+    if (b >= nblk) return;   // the whole wave
+    sc = clipped(sc);
+    const int64_t e0 = b * blk;
+    const int n = (int)(blk < len - e0 ? blk : len - e0);
+    float up[4 * NV], th[4 * NV];
+    float ss = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        if constexpr (VEC) {
+            const int j = (lane + kWave * k) * 4;
+            if (j < n) {
+                const f32x4 u4 = ld_stream(u + e0 + j);
+                const f32x4 t4 = ld_stream(theta + e0 + j);
+                f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
+                if (SPLIT) h4 = ld_stream(h + e0 + j);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    up[4 * k + c] = numerator<SPLIT>(u4[c], h4[c], sc);
+                    th[4 * k + c] = t4[c];
+                    ss += up[4 * k + c] * up[4 * k + c];
+                }
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int j = lane + kWave * (4 * k + c);
+                up[4 * k + c] = 0.f;
+                th[4 * k + c] = 0.f;
+                if (j < n) {
+                    up[4 * k + c] = numerator<SPLIT>(u[e0 + j], SPLIT ? h[e0 + j] : 0.f, sc);
+                    th[4 * k + c] = theta[e0 + j];
+                    ss += up[4 * k + c] * up[4 * k + c];
+                }
+            }
+        }
+    }
+    ss = wave_sum(ss);
+    const float vb = sc.beta2 * v[b] + sc.one_minus_beta2 * (ss / (float)n);
+    if (lane == 0) v[b] = vb;
+    const float denom = sqrtf(vb * sc.inv_bc2) + sc.eps;
+    const float keep = 1.0f - sc.lr * wd;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        if constexpr (VEC) {
+            const int j = (lane + kWave * k) * 4;
+            if (j < n) {
+                f32x4 t4;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) t4[c] = keep * th[4 * k + c] - sc.lr * (up[4 * k + c] / denom);
+                st_stream(theta + e0 + j, t4);
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int j = lane + kWave * (4 * k + c);
+                if (j < n) theta[e0 + j] = keep * th[4 * k + c] - sc.lr * (up[4 * k + c] / denom);
+            }
+        }
+    }
+}
+
+// Blocks longer than kBlkWave: piece p of block b = p / np covers [b blk + (p % np) kBlkWave, +kBlkWave),
+// cut at the block's and the segment's end.
+__device__ __forceinline__ void piece_range(int64_t p, int np, int64_t blk, int64_t len, int64_t* e0, int* n) {
+    const int64_t b = p / np;
+    const int64_t s0 = b * blk + (p % np) * (int64_t)kBlkWave;
+    int64_t e1 = b * blk + blk < len ? b * blk + blk : len;
+    if (s0 + kBlkWave < e1) e1 = s0 + kBlkWave;
+    *e0 = s0;
+    *n = (int)(e1 - s0);
+}
+
+template <bool SPLIT, bool VEC>
+__global__ __launch_bounds__(kUpdThreads) void blocks_piece_stats_kernel(const float* __restrict__ u,
+                                                                         const float* __restrict__ h, int64_t len,
+                                                                         int64_t blk, int64_t npieces, int np,
+                                                                         float* __restrict__ part, UpdateScalars sc) {
+    const int lane = threadIdx.x % kWave;
+    const int64_t p = (int64_t)blockIdx.x * kWavesPerWG + threadIdx.x / kWave;
+    if (p >= npieces) return;
+    sc = clipped(sc);
+    int64_t e0;
+    int n;
+    piece_range(p, np, blk, len, &e0, &n);
+    float ss = 0.f;
+    if constexpr (VEC) {
+        for (int j = lane * 4; j < n; j += kWave * 4) {
+            const f32x4 u4 = ld_stream(u + e0 + j);
+            f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
+            if (SPLIT) h4 = ld_stream(h + e0 + j);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const float x = numerator<SPLIT>(u4[c], h4[c], sc);
+                ss += x * x;
+            }
+        }
+    } else {
+        for (int j = lane; j < n; j += kWave) {
+            const float x = numerator<SPLIT>(u[e0 + j], SPLIT ? h[e0 + j] : 0.f, sc);
+            ss += x * x;
+        }
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) part[p] = ss;
+}
+
+// One thread per block: the partial sums in piece order, then the block's second moment.
+__global__ __launch_bounds__(kUpdThreads) void blocks_finish_kernel(float* __restrict__ v, const float* __restrict__ part,
+                                                                    int64_t nblk, int np, int64_t blk, int64_t len,
+                                                                    UpdateScalars sc) {
+    const int64_t b = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x;
+    if (b >= nblk) return;
+    float ss = 0.f;
+    for (int q = 0; q < np; ++q) ss += part[b * np + q];
+    const int64_t n = b * blk + blk < len ? blk : len - b * blk;
+    v[b] = sc.beta2 * v[b] + sc.one_minus_beta2 * (ss / (float)n);
+}
+
+template <bool SPLIT, bool VEC>
+__global__ __launch_bounds__(kUpdThreads) void blocks_piece_step_kernel(float* __restrict__ theta,
+                                                                        const float* __restrict__ v,
+                                                                        const float* __restrict__ u,
+                                                                        const float* __restrict__ h, int64_t len,
+                                                                        int64_t blk, int64_t npieces, int np, float wd,
+                                                                        UpdateScalars sc) {
+    const int lane = threadIdx.x % kWave;
+    const int64_t p = (int64_t)blockIdx.x * kWavesPerWG + threadIdx.x / kWave;
+    if (p >= npieces) return;
+    sc = clipped(sc);
+    int64_t e0;
+    int n;
+    piece_range(p, np, blk, len, &e0, &n);
+    const float denom = sqrtf(v[p / np] * sc.inv_bc2) + sc.eps;
+    const float keep = 1.0f - sc.lr * wd;
+    if constexpr (VEC) {
+        for (int j = lane * 4; j < n; j += kWave * 4) {
+            const f32x4 u4 = ld_stream(u + e0 + j);
+            f32x4 t4 = ld_stream(theta + e0 + j);
+            f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
+            if (SPLIT) h4 = ld_stream(h + e0 + j);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) t4[c] = keep * t4[c] - sc.lr * (numerator<SPLIT>(u4[c], h4[c], sc) / denom);
+            st_stream(theta + e0 + j, t4);
+        }
+    } else {
+        for (int j = lane; j < n; j += kWave) {
+            const float x = numerator<SPLIT>(u[e0 + j], SPLIT ? h[e0 + j] : 0.f, sc);
+            theta[e0 + j] = keep * theta[e0 + j] - sc.lr * (x / denom);
+        }
+    }
+}
+
 constexpr int kClipGroups = 2048;  // workgroups of the norm pass (fixed: the sum order is fixed)
 constexpr int kClipUnroll = 4;     // 16-byte groups per thread in flight
 
@@ -687,21 +862,19 @@ hipError_t dispatch_factored(float* theta, float* Rr, float* Cc, const float* u,
 size_t update_workspace_bytes(int64_t P, const bom_update_cfg* cfg) {
     if (!cfg || P < 1) return 0;
     const bool clip = cfg->clip_norm > 0.f;
+    if (cfg->v_layout == BOM_V_BLOCKS) return clip ? clip_layout(blocks_part_bytes(P)).total : blocks_part_bytes(P);
     if (cfg->v_layout != BOM_V_FACTORED) return clip ? clip_layout(0).total : 0;
     if (cfg->block_rows < 1 || cfg->block_cols < 1) return 0;
     return fac_layout(P, cfg->block_rows, cfg->block_cols, clip).total;
 }
 
-hipError_t launch_update_dense(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
-                               UpdateScalars sc, void* ws, hipStream_t st) {
-    const bool aligned = (reinterpret_cast<uintptr_t>(theta) % 16 == 0) && (reinterpret_cast<uintptr_t>(v) % 16 == 0) &&
-                         (reinterpret_cast<uintptr_t>(u) % 16 == 0) &&
-                         (h == nullptr || reinterpret_cast<uintptr_t>(h) % 16 == 0);
-    if (sc.clip_norm > 0.f) {
-        const hipError_t e = h ? run_clip<true, true>(u, h, P, aligned, sc, ws, clip_layout(0), st)
-                               : run_clip<false, true>(u, h, P, aligned, sc, ws, clip_layout(0), st);
-        if (e != hipSuccess) return e;
-    }
+namespace {
+bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+
+// The dense kernels over P elements (the clipping factor, if any, already in sc.clip).
+hipError_t dense_range(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
+                       const UpdateScalars& sc, hipStream_t st) {
+    const bool aligned = aligned16(theta) && aligned16(v) && aligned16(u) && (h == nullptr || aligned16(h));
     int64_t done = 0;
     if (aligned && P >= 4) {
         const int64_t nvec = P / 4;
@@ -726,6 +899,115 @@ hipError_t launch_update_dense(float* theta, float* v, const float* u, const flo
             hipLaunchKernelGGL(update_dense_scalar_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta,
                                v, u, h, done, P, segs, sc);
         return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+// Global-norm clipping pass over the whole numerator: sets sc.clip (no-op without clipping).
+hipError_t clip_pass(const float* u, const float* h, int64_t P, UpdateScalars& sc, void* ws, hipStream_t st) {
+    if (!(sc.clip_norm > 0.f)) return hipSuccess;
+    const bool aligned = aligned16(u) && (h == nullptr || aligned16(h));
+    return h ? run_clip<true, true>(u, h, P, aligned, sc, ws, clip_layout(0), st)
+             : run_clip<false, true>(u, h, P, aligned, sc, ws, clip_layout(0), st);
+}
+
+template <bool SPLIT, int NV>
+hipError_t blocks_wave(float* theta, float* v, const float* u, const float* h, int64_t len, int64_t blk, bool vec,
+                       float wd, const UpdateScalars& sc, hipStream_t st) {
+    const int64_t nblk = (len + blk - 1) / blk;
+    const dim3 grid((unsigned)((nblk + kWavesPerWG - 1) / kWavesPerWG));
+    if (vec)
+        hipLaunchKernelGGL((blocks_wave_kernel<SPLIT, NV, true>), grid, dim3(kUpdThreads), 0, st, theta, v, u, h, len, blk,
+                           nblk, wd, sc);
+    else
+        hipLaunchKernelGGL((blocks_wave_kernel<SPLIT, NV, false>), grid, dim3(kUpdThreads), 0, st, theta, v, u, h, len,
+                           blk, nblk, wd, sc);
+    return hipGetLastError();
+}
+
+template <bool SPLIT>
+hipError_t blocks_pieces(float* theta, float* v, const float* u, const float* h, int64_t len, int64_t blk, bool vec,
+                         float wd, const UpdateScalars& sc, float* part, hipStream_t st) {
+    const int64_t nblk = (len + blk - 1) / blk;
+    const int64_t eff = blk < len ? blk : len;   // a block longer than the segment is the segment
+    const int np = (int)((eff + kBlkWave - 1) / kBlkWave);
+    const int64_t npieces = nblk * np;
+    const dim3 grid((unsigned)((npieces + kWavesPerWG - 1) / kWavesPerWG));
+    if (vec)
+        hipLaunchKernelGGL((blocks_piece_stats_kernel<SPLIT, true>), grid, dim3(kUpdThreads), 0, st, u, h, len, blk,
+                           npieces, np, part, sc);
+    else
+        hipLaunchKernelGGL((blocks_piece_stats_kernel<SPLIT, false>), grid, dim3(kUpdThreads), 0, st, u, h, len, blk,
+                           npieces, np, part, sc);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(blocks_finish_kernel, dim3((unsigned)((nblk + kUpdThreads - 1) / kUpdThreads)), dim3(kUpdThreads),
+                       0, st, v, part, nblk, np, blk, len, sc);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (vec)
+        hipLaunchKernelGGL((blocks_piece_step_kernel<SPLIT, true>), grid, dim3(kUpdThreads), 0, st, theta, v, u, h, len,
+                           blk, npieces, np, wd, sc);
+    else
+        hipLaunchKernelGGL((blocks_piece_step_kernel<SPLIT, false>), grid, dim3(kUpdThreads), 0, st, theta, v, u, h, len,
+                           blk, npieces, np, wd, sc);
+    return hipGetLastError();
+}
+
+template <bool SPLIT>
+hipError_t blocks_segment(float* theta, float* v, const float* u, const float* h, int64_t len, int64_t blk, float wd,
+                          const UpdateScalars& sc, float* part, hipStream_t st) {
+    if (blk == 1) {
+        SegTable one{};
+        one.n = 0;
+        one.wd_default = wd;
+        return dense_range(theta, v, u, h, len, one, sc, st);
+    }
+    const bool vec = aligned16(theta) && aligned16(u) && (h == nullptr || aligned16(h)) && blk % 4 == 0 && len % 4 == 0;
+    const int64_t eff = blk < len ? blk : len;
+    if (eff <= 256) return blocks_wave<SPLIT, 1>(theta, v, u, h, len, blk, vec, wd, sc, st);
+    if (eff <= 1024) return blocks_wave<SPLIT, 4>(theta, v, u, h, len, blk, vec, wd, sc, st);
+    if (eff <= kBlkWave) return blocks_wave<SPLIT, 16>(theta, v, u, h, len, blk, vec, wd, sc, st);
+    return blocks_pieces<SPLIT>(theta, v, u, h, len, blk, vec, wd, sc, part, st);
+}
+
+}  // namespace
+
+hipError_t launch_update_dense(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
+                               UpdateScalars sc, void* ws, hipStream_t st) {
+    const hipError_t e = clip_pass(u, h, P, sc, ws, st);
+    if (e != hipSuccess) return e;
+    return dense_range(theta, v, u, h, P, segs, sc, st);
+}
+
+int64_t blocks_count(const BlockSegs& b) {
+    int64_t n = 0;
+    for (int k = 0; k < b.n; ++k) n += (b.len[k] + b.blk[k] - 1) / b.blk[k];
+    return n;
+}
+
+// Workspace: the partial sums of long blocks (at most 3 per 4096 elements of a segment plus one per
+// segment: bounded by P / 1024 + 64 floats), then the clipping pass.
+hipError_t launch_update_blocks(float* theta, float* v, const float* u, const float* h, int64_t P, const BlockSegs& bs,
+                                UpdateScalars sc, void* ws, hipStream_t st) {
+    const size_t pb = blocks_part_bytes(P);
+    if (sc.clip_norm > 0.f) {
+        const bool aligned = aligned16(u) && (h == nullptr || aligned16(h));
+        const hipError_t e = h ? run_clip<true, true>(u, h, P, aligned, sc, ws, clip_layout(pb), st)
+                               : run_clip<false, true>(u, h, P, aligned, sc, ws, clip_layout(pb), st);
+        if (e != hipSuccess) return e;
+    }
+    float* part = static_cast<float*>(ws);
+    int64_t vb = 0, pused = 0;
+    for (int k = 0; k < bs.n; ++k) {
+        const int64_t o = bs.begin[k], len = bs.len[k], blk = bs.blk[k];
+        const hipError_t e = h ? blocks_segment<true>(theta + o, v + vb, u + o, h + o, len, blk, bs.wd[k], sc, part + pused, st)
+                               : blocks_segment<false>(theta + o, v + vb, u + o, nullptr, len, blk, bs.wd[k], sc,
+                                                       part + pused, st);
+        if (e != hipSuccess) return e;
+        const int64_t nblk = (len + blk - 1) / blk;
+        const int64_t eff = blk < len ? blk : len;
+        if (eff > kBlkWave) pused += nblk * ((eff + kBlkWave - 1) / kBlkWave);
+        vb += nblk;
     }
     return hipSuccess;
 }

@@ -5,6 +5,7 @@ import os
 import re
 
 import pytest
+import torch
 
 from paper_2609_36738_amd import bom
 
@@ -119,6 +120,40 @@ def _upd(lib, P=1000, segs=(), wd=0.0, v_col=None, ws=None, wsb=0, h=None, **cfg
 ])
 def test_update_rejects(lib, kw, code):
     assert _upd(lib, **kw) == code
+
+
+TILE = [(0, 600, 0.1), (600, 400, 0.0)]
+BIG_WS = dict(ws=ctypes.c_void_p(0x4000000), wsb=1 << 30)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(segs=TILE, blocks=[768, 1], v_col=FAKE, **BIG_WS), 2),          # v_col must be NULL
+    (dict(segs=[], blocks=[], **BIG_WS), 1),                              # segments are required
+    (dict(segs=[(0, 600, 0.1), (601, 399, 0.0)], blocks=[4, 4], **BIG_WS), 2),   # a gap
+    (dict(segs=[(0, 600, 0.1), (600, 300, 0.0)], blocks=[4, 4], **BIG_WS), 2),   # ends before P
+    (dict(segs=[(0, 600, 0.1), (600, 0, 0.0), (600, 400, 0.0)], blocks=[4, 4, 4], **BIG_WS), 2),  # empty segment
+    (dict(segs=TILE, blocks=[0, 4], **BIG_WS), 2),                        # block length 0
+    (dict(segs=TILE, blocks=[4, 4], state_dtype=torch.bfloat16, **BIG_WS), 3),   # fp32 state only
+    (dict(segs=TILE, blocks=[4, 4]), 5),                                  # workspace required
+    (dict(segs=TILE, blocks=[4, 4], ws=ctypes.c_void_p(0x4000010), wsb=1 << 30), 5),   # 256-byte alignment
+])
+def test_update_blocks_rejects(lib, kw, code):
+    assert _upd(lib, **kw) == code
+
+
+def test_update_blocks_alias_and_workspace_bound(lib):
+    cfg = bom.make_update_cfg(lr=1e-3, beta2=0.999, eps=1e-8, t=1, blocks=[4, 4])
+    segs = (bom.bom_segment * 2)(*[bom.bom_segment(*s) for s in TILE])
+    # v (250 block entries) overlapping theta
+    assert lib.bom_update(ctypes.c_void_p(0x100000), ctypes.c_void_p(0x100100), None, ctypes.c_void_p(0x300000), None,
+                          1000, segs, 2, 0.0, ctypes.byref(cfg), ctypes.c_void_p(0x4000000), 1 << 30, None) == 6
+    # the partial-sum bound: ceil(n / blk) ceil(blk / 4096) <= 3 n / 4096 + 1 pieces per segment
+    for P in (1, 4096, 10**6, 8 * 10**9):
+        nb = lib.bom_update_workspace_bytes(P, ctypes.byref(cfg))
+        assert nb >= 4 * (3 * P / 4096 + 16) and nb % 256 == 0
+    for n, blk in ((4097, 4097), (10**6, 4097), (10**6, 8191), (5000, 10**7), (49152 * 7 + 5, 49152)):
+        pieces = -(-n // blk) * -(-min(blk, n) // 4096)
+        assert pieces <= 3 * n / 4096 + 1
 
 
 def test_update_null_pointers(lib):

@@ -532,6 +532,55 @@ def test_update_dense_clip_parity(clip, split, offset):
         assert (np.abs(vg - vo) <= 1e-5 * vo + 1e-30).all()
 
 
+# Block-shared second moment (Adam-mini's map with the BOM numerator): segments tiling the buffer with
+# per-element blocks (the dense kernels), one-wave blocks (up to 4096 elements, 16-byte or scalar accesses),
+# long blocks in pieces (a block longer than its segment is the segment), ragged last blocks, and a
+# misaligned layout whose segments start at odd offsets (scalar accesses throughout).
+BLOCK_LAYOUTS = {
+    "aligned": [(1000, 1, 0.0), (768 * 40 + 256, 768, 0.01), (4096 * 3, 4096, 0.01), (256 * 10, 256, 0.1),
+                (45000, 20000, 0.01), (8192, 100000, 0.0), (49152 * 2 + 12, 49152, 0.01), (64, 64, 0.0)],
+    "misaligned": [(1001, 1, 0.0), (700, 7, 0.01), (3001, 300, 0.1), (12345, 5000, 0.01), (4099, 4096, 0.0),
+                   (9, 9, 0.0)],
+}
+
+
+@pytest.mark.parametrize("split,clip", [(False, 0.0), (True, 0.0), (False, 0.05)], ids=["plain", "split", "clip"])
+@pytest.mark.parametrize("layout", list(BLOCK_LAYOUTS), ids=list(BLOCK_LAYOUTS))
+def test_update_blocks_parity(layout, split, clip):
+    spec = BLOCK_LAYOUTS[layout]
+    segs, blocks, pos = [], [], 0
+    for n, blk, wd in spec:
+        segs.append((pos, n, wd))
+        blocks.append(blk)
+        pos += n
+    P = pos
+    nv = oracle.blocks_count(segs, blocks)
+    log(f"[update blocks] {layout} split={split} clip={clip} P={P} blocks={nv}")
+    lr = 1e-3
+    th0 = synth.normal_f32(P, synth.STREAM_THETA, 0.02)
+    theta = torch.from_numpy(th0.copy()).to(dev())
+    v = torch.zeros(nv, device=dev())
+    stats = torch.zeros(2, device=dev())
+    tho, vo = th0.astype(np.float64), np.zeros(nv)
+    segs32 = [(a, b, f32(c)) for a, b, c in segs]
+    for t in range(1, 4):
+        u = synth.normal_f32(P, synth.STREAM_U + t, 1e-3)
+        u[:3] = 0.0      # a zero block inside the first segment
+        h = synth.normal_f32(P, synth.STREAM_SPLIT_H + t, 1e-3) if split else None
+        cfg = bom.make_update_cfg(lr=lr, beta2=B2, eps=EPS, t=t, lam=LAM, clip_norm=clip, clip_stats=stats,
+                                  blocks=blocks)
+        bom.bom_update(theta, v, torch.from_numpy(u).to(dev()), cfg, segments=segs,
+                       h=None if h is None else torch.from_numpy(h).to(dev()))
+        torch.cuda.synchronize()
+        tho, vo = oracle.update_blocks(tho, vo, u, lr=f32(lr), beta2=f32(B2), eps=f32(EPS), t=t, segments=segs32,
+                                       blocks=blocks, h=h, lam=f32(LAM), clip_norm=clip)
+        _check_theta(to_f64(theta), tho, lr, f"blocks {layout} t={t}")
+        vg = to_f64(v)
+        assert (np.abs(vg - vo) <= 1e-5 * vo + 1e-30).all(), f"blocks {layout} t={t}: v"
+        if clip:
+            assert abs(float(stats[1]) - oracle.clip_factor(u, h=h, lam=f32(LAM), clip_norm=clip)) <= 1e-5
+
+
 @pytest.mark.parametrize("br,bc,P,clip", [(4, 4096, 4096 * 9 + 2048, 0.1), (8, 64, 8 * 64 * 3 + 64 * 2 + 16, 0.02)],
                          ids=["bc4096_rows", "bc64_strips"])
 def test_update_factored_clip_parity(br, bc, P, clip):

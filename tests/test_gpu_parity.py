@@ -212,6 +212,39 @@ def test_head_vjp_parity(case):
     assert (np.abs(gdw.sum(1)) <= (tol if dtype == "bf16" else 1e-4) * np.abs(gdw).sum(1) + 1e-12).all()
 
 
+# Padded leading dimensions (multiples of 8) with V not a multiple of 8: the padding holds large values
+# that must not reach any result (residual rows, s, dW, dH, db).
+def test_head_vjp_padded_rows_ignore_padding():
+    N, d, V, ld = 2048, 512, 4100, 4104
+    log(f"[head_vjp padded] N={N} d={d} V={V} ld={ld}")
+    Hh, Hd, Wh, Wd, Zh, Zd, y, q_prev, t = _vjp_inputs(N, d, V, "bf16", 0.05)
+    def padded(x, rows):
+        buf = torch.full((rows, ld), 1e4, dtype=torch.bfloat16, device=dev())
+        buf[:, :V].copy_(x)
+        return buf[:, :V]
+    Zp, Wp = padded(Zd, N), padded(Wd, d)
+    Rp = padded(torch.zeros((N, V), dtype=torch.bfloat16, device=dev()), N)
+    yd = torch.from_numpy(y).to(dev())
+    res = bom.bom_residual(Zp, yd, R=Rp)
+    q = torch.from_numpy(q_prev.copy()).to(dev())
+    qh = bom.bom_ema(q, res["s"], B1, t)
+    g = bom.bom_head_vjp(Hd, Wp, Rp, yd, qh, res["n_valid"], s=res["s"], lam=LAM, want_db=True,
+                         dh_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert float(Rp.storage_offset()) == 0 and torch.all(Rp.as_strided((N, ld), (ld, 1))[:, V:] == 1e4)
+    o = oracle.residual(Zh, y, want_R=False)
+    _, qho = oracle.ema(q_prev, o["s"], f32(B1), t)
+    cols, rows = np.r_[0:32, V - 40:V], np.r_[0:16, N - 16:N]
+    dW = oracle.dW_cols(Hh, Zh, y, o["row_lse"], qho, o["n_valid"], LAM, cols=cols)
+    dH = oracle.dH_rows(Wh, Zh, y, o["row_lse"], qho, o["n_valid"], LAM, rows=rows)
+    db = oracle.db(Zh, y, o["row_lse"], qho, o["n_valid"], LAM)
+    e_s = rel_fro(to_f64(res["s"]), o["s"])
+    e_dw, e_dh = rel_fro(to_f64(g["dW"])[:, cols], dW), rel_fro(to_f64(g["dH"])[rows], dH)
+    e_db = rel_fro(to_f64(g["db"]), db)
+    log(f"    rel err s={e_s:.3e} dW={e_dw:.3e} dH={e_dh:.3e} db={e_db:.3e}")
+    assert e_s <= 1e-5 and e_dw <= 2e-2 and e_dh <= 2e-2 and e_db <= 1e-5
+
+
 # More 256 x 256 output tiles than the chip has compute units: whole rounds run over the full k range
 # and the leftover tiles split k (dW: the last column tiles; dH: the last row tiles), with ragged last
 # tiles in both m and n and a k extent that is not a multiple of the 64-deep k tile.

@@ -561,8 +561,9 @@ __device__ __forceinline__ bool unit_of(const TileRange& r, bool inner_is_m, int
 //   dW = alpha H^T R + hsum cq^T,   hsum_m = sum_{i in I} H_im,  cq_n = lambda q_hat_n / N_t,
 //   dH = alpha R W^T + mask u^T,    u_n = (lambda / N_t) sum_j W_nj q_hat_j,
 // so both GEMMs take R as it is stored (bf16, no rounding of G) and the history enters through
-// the fp32 epilogue. 256 x 256 output tile per 256-thread workgroup, each wave 128 x 128 = 4 x 4
-// blocks of v_mfma_f32_32x32x16_bf16. Memory reads are buffer loads: a chunk outside the matrix
+// the fp32 epilogue. 256 x 256 output tile per workgroup: lds256_kernel runs four waves, each 128 x 128
+// = 4 x 4 blocks of v_mfma_f32_32x32x16_bf16; the 64-deep kernels below run eight waves of 128 x 64 (or
+// four of 128 x 128). Memory reads are buffer loads: a chunk outside the matrix
 // reads as zero through the descriptor's range check or an out-of-range offset, so loads need no
 // branches and never touch memory past the operand.
 constexpr int LB = 256;                 // output tile

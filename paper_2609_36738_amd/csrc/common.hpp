@@ -96,6 +96,7 @@ __device__ __forceinline__ bool label_valid(int32_t y, int64_t V, int32_t ignore
 
 constexpr int kBufFlags = 0x00020000;   // raw buffer descriptor word 3: 32-bit data format
 constexpr int kOob = (int)0x80000000u;  // an offset past every range: the load returns zeros
+constexpr int kNonTemporal = 2;           // buffer access cache policy: nt (streamed data touched once)
 
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 

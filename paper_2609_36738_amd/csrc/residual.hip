@@ -508,7 +508,9 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
 // spin_limit < 0) thread 0 computes the missing part's record from Z itself and stops waiting for
 // that part, so the kernel finishes whatever the scheduling. The part holding a row's label (part 0
 // for ignored rows) writes that row's outputs and loss term. Workgroup (g, q) writes columns of
-// partial row g; the S parts of group g together fill it.
+// partial row g; the S parts of group g together fill it. Its logit loads and residual stores carry the
+// non-temporal hint (128 K vocabulary: 1.80 -> 1.73 ms; the row-parked kernel of narrower rows ran 5 %
+// slower with it and keeps the default policy).
 template <int THREADS, int NCH>
 __global__ __launch_bounds__(THREADS) void residual_split_kernel(
     const uint16_t* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
@@ -545,7 +547,7 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
     const int wave_last = (tid | (kWave - 1));
     auto row_desc = [&](int i) { return make_desc(Z + (int64_t)i * ldz + c0, Vp * 2); };
     auto load_chunk = [&](const __amdgpu_buffer_rsrc_t& d, int c) {
-        const u32x4_t w = __builtin_amdgcn_raw_buffer_load_b128(d, voff + c * THREADS * 16, 0, 0);
+        const u32x4_t w = __builtin_amdgcn_raw_buffer_load_b128(d, voff + c * THREADS * 16, 0, kNonTemporal);
         return make_uint4(w[0], w[1], w[2], w[3]);
     };
     auto park = [&](int c, uint4 w) {
@@ -770,7 +772,7 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
             w[1] = pack_bf16x2(p[2], p[3]);
             w[2] = pack_bf16x2(p[4], p[5]);
             w[3] = pack_bf16x2(p[6], p[7]);
-            __builtin_amdgcn_raw_buffer_store_b128(w, rdesc, voff + c * THREADS * 16, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(w, rdesc, voff + c * THREADS * 16, 0, kNonTemporal);
         }
         if (has_next) {
 #pragma unroll

@@ -177,11 +177,11 @@ __global__ __launch_bounds__(kUpdThreads) void factored_stats_kernel(const float
             const int j = (k * kUpdThreads + t) * 4;
             const int64_t e = i * bc + j;
             if (j < bc && e < P) {
-                const float4 u4 = *reinterpret_cast<const float4*>(u + e);
-                float4 h4 = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (SPLIT) h4 = *reinterpret_cast<const float4*>(h + e);
-                const float a0 = numerator<SPLIT>(u4.x, h4.x, sc), a1 = numerator<SPLIT>(u4.y, h4.y, sc);
-                const float a2 = numerator<SPLIT>(u4.z, h4.z, sc), a3 = numerator<SPLIT>(u4.w, h4.w, sc);
+                const f32x4 u4 = ld_stream(u + e);
+                f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
+                if (SPLIT) h4 = ld_stream(h + e);
+                const float a0 = numerator<SPLIT>(u4[0], h4[0], sc), a1 = numerator<SPLIT>(u4[1], h4[1], sc);
+                const float a2 = numerator<SPLIT>(u4[2], h4[2], sc), a3 = numerator<SPLIT>(u4[3], h4[3], sc);
                 const float s0 = a0 * a0, s1 = a1 * a1, s2 = a2 * a2, s3 = a3 * a3;
                 kap[k * 4 + 0] += s0;
                 kap[k * 4 + 1] += s1;
@@ -339,7 +339,8 @@ __global__ __launch_bounds__(kUpdThreads) void factored_update_rows_kernel(float
 
 // Row kernels for block_cols = NV * 256 (up to 4096): a wave owns whole rows, lane l holding
 // columns (k*64 + l)*4 .. +3 for k < NV, so each row's loads are all in flight together and the row
-// statistic is one wave reduction. Elements at or past P (only in the last row) count as zero.
+// statistic is one wave reduction. Elements at or past P (only in the last row) count as zero. The
+// statistics read u with non-temporal loads (8B parameters: 5.73 -> 5.22 ms against cached loads).
 template <bool SPLIT, int NV>
 __global__ __launch_bounds__(kUpdThreads) void factored_stats_rows_kernel(const float* __restrict__ u,
                                                                           const float* __restrict__ h, int64_t P,
@@ -365,9 +366,9 @@ __global__ __launch_bounds__(kUpdThreads) void factored_stats_rows_kernel(const 
             const int64_t e = i * BC + (k * kWave + l) * 4;
             const bool ok = e < P;
             const int64_t ec = ok ? e : P - 4;
-            const f32x4 u4 = *reinterpret_cast<const f32x4*>(u + ec);
+            const f32x4 u4 = ld_stream(u + ec);
             f32x4 h4 = {0.f, 0.f, 0.f, 0.f};
-            if (SPLIT) h4 = *reinterpret_cast<const f32x4*>(h + ec);
+            if (SPLIT) h4 = ld_stream(h + ec);
             const float z = ok ? 1.f : 0.f;
 #pragma unroll
             for (int c = 0; c < 4; ++c) a[k][c] = z * numerator<SPLIT>(u4[c], h4[c], sc);

@@ -278,6 +278,14 @@ bom_status bom_head_telemetry(const void* H, int64_t ldh, bom_dtype h_dt, const 
 bom_status bom_head_forward(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
                             int64_t N, int64_t d, int64_t V, void* Z, int64_t ldz, void* stream);
 
+/* Environment variables, each read once per process on first use (for measurement and tests; results do
+ * not depend on them beyond rounding order):
+ *   BOM_VJP_WAVES = "dH,dW,fwd,pair"  waves per workgroup (4 or 8) of the 256-tile products; default 8,8,8,8.
+ *   BOM_VJP_PLAN  = "kw,sw,kh,sh"     force a head-VJP kernel kind and k split per product (A/B runs only).
+ *   BOM_RESIDUAL_SPIN = n             poll bound of the split-row residual exchange; negative: every part
+ *                                      recomputes its partners' row records from Z (the fallback path).
+ */
+
 /* Static text of a status code, and the thread-local detail of the last failure ("" if none). */
 const char* bom_status_string(bom_status status);
 const char* bom_last_error(void);

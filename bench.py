@@ -34,7 +34,9 @@ HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
 MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA
 FP32_PEAK_TFS = 157.3      # MI355X fp32 vector
 METRIC = "BOM steps/s & tokens/s per config; % of HBM BW / MFMA peak per kernel"
-DEFAULT_WORKLOAD = WORKLOADS[1].name
+# the headline: the largest workload that fits one GPU (the 8B-class language-model step); a default run
+# also measures every other workload and reports it under "per_config"
+HEADLINE_WORKLOAD = "lm_8b_v128256"
 KERNEL_SOURCES = {
     "bom_residual": "residual.hip",
     "bom_ema": "ema.hip",
@@ -95,8 +97,9 @@ def adam_mini_partition(w):
 class Problem:
     """Device-resident inputs and state of one workload."""
 
-    def __init__(self, w, dev, clip_norm=0.0, state_dtype=torch.float32, adam_mini=False):
+    def __init__(self, w, dev, clip_norm=0.0, state_dtype=torch.float32, adam_mini=False, z_route=False):
         self.w = w
+        self.z_route = z_route
         self.blocks = None
         self.clip_norm = clip_norm
         self.state_dtype = state_dtype
@@ -113,7 +116,8 @@ class Problem:
             self.W = None  # the tiny head reads W from theta
         y = synth.labels_uniform(N, V) if w.labels == "uniform" else synth.labels_zipf(N, V)
         self.labels = torch.from_numpy(y).to(dev)
-        self.R = torch.empty((N, V), dtype=self.Z.dtype, device=dev)
+        # the logits route forms R inside the head products: no R buffer
+        self.R = None if z_route else torch.empty((N, V), dtype=self.Z.dtype, device=dev)
         self.theta = torch.empty(P, dtype=state_dtype, device=dev)
         fill_normal_(self.theta, synth.STREAM_THETA, 0.02)
         if w.dtype == "f32":
@@ -148,7 +152,7 @@ class Problem:
         d, V = w.d, w.V
         if ev is not None:
             ev[0].record()
-        self.res = bom.bom_residual(self.Z, self.labels, R=self.R, workspace=self.ws_res,
+        self.res = bom.bom_residual(self.Z, self.labels, R=self.R, write_R=not self.z_route, workspace=self.ws_res,
                                     **({} if self.res is None else {k: self.res[k] for k in (
                                         "s", "row_lse", "row_argmax", "row_target", "loss", "n_valid", "flags")}))
         self.ws_res = self.res["workspace"]
@@ -160,8 +164,13 @@ class Problem:
         W = self.W if self.W is not None else self.theta[: d * V].view(d, V)
         dW = self.u[: d * V].view(d, V)
         db = self.u[d * V: d * V + V] if w.has_bias else None
-        g = bom.bom_head_vjp(self.H, W, self.R, self.labels, self.q_hat, self.res["n_valid"], s=self.res["s"],
-                             lam=w.lam, dW=dW, db=db, dH=self.dH, workspace=self.ws_vjp)
+        if self.z_route:
+            g = bom.bom_head_vjp(self.H, W, self.Z, self.labels, self.q_hat, self.res["n_valid"], s=self.res["s"],
+                                 lam=w.lam, dW=dW, db=db, dH=self.dH, workspace=self.ws_vjp,
+                                 row_lse=self.res["row_lse"])
+        else:
+            g = bom.bom_head_vjp(self.H, W, self.R, self.labels, self.q_hat, self.res["n_valid"], s=self.res["s"],
+                                 lam=w.lam, dW=dW, db=db, dH=self.dH, workspace=self.ws_vjp)
         self.ws_vjp = g["workspace"]
         if ev is not None:
             ev[3].record()
@@ -228,16 +237,19 @@ def time_telemetry(prob, steps):
             "last": stats}
 
 
-def algorithmic(w, clip=False, bf16_state=False, blocks=None):
+def algorithmic(w, clip=False, bf16_state=False, blocks=None, z_route=False):
     """Algorithmic bytes / flops of each stage for one step (what BOM must move or compute). With
     global-norm clipping the dense update reads u once more for the norm; the factored update takes
     the norm from its row statistics (a row-sized array written once and read twice). blocks: the
-    (segments, block lengths) of the block-shared second moment."""
+    (segments, block lengths) of the block-shared second moment. z_route: the residual writes no R (the
+    head products form it from Z)."""
     esz = 2 if w.dtype == "bf16" else 4
     N, d, V, P = w.N, w.d, w.V, w.P
     out = {
-        "bom_residual": dict(bound="hbm", amount=2 * N * V * esz + 16 * N + 4 * V,
-                             per_unit="2*esz bytes per logit (read Z, write R) + 16 B/row + 4 B/column"),
+        "bom_residual": (dict(bound="hbm", amount=N * V * esz + 16 * N + 4 * V,
+                              per_unit="esz bytes per logit (read Z) + 16 B/row + 4 B/column") if z_route else
+                         dict(bound="hbm", amount=2 * N * V * esz + 16 * N + 4 * V,
+                              per_unit="2*esz bytes per logit (read Z, write R) + 16 B/row + 4 B/column")),
         "bom_ema": dict(bound="hbm", amount=12 * V, per_unit="12 bytes per output coordinate"),
         "bom_head_vjp": dict(bound="mfma" if w.dtype == "bf16" else "alu", amount=4 * N * d * V,
                              per_unit="4*N*d*V flop (dW and dH)"),
@@ -398,63 +410,12 @@ def host_cpu_model() -> str:
     return "unknown"
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=[w.name for w in WORKLOADS])
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--state-dtype", choices=["f32", "bf16"], default="f32",
-                    help="storage of theta, v and u (bf16: the paper's fine-tuning protocol; dense layout, bf16 "
-                         "logits only)")
-    ap.add_argument("--forward", action="store_true",
-                    help="also time the head forward Z = H W that produces the logits (common work, outside the "
-                         "step) against the MFMA roofline")
-    ap.add_argument("--telemetry", action="store_true",
-                    help="also time the head drift telemetry call (a diagnostic for telemetry steps, outside the "
-                         "step) on the last step's residual, history and features")
-    ap.add_argument("--clip-norm", type=float, default=0.0,
-                    help="global-norm clipping of the update numerator at this norm (0: none; the paper's "
-                         "language-model protocols clip at 1.0)")
-    ap.add_argument("--adam-mini", action="store_true",
-                    help="block-shared second moment (Adam-mini's update map with the BOM numerator) over a "
-                         "transformer-shaped partition of the flat buffer, instead of the dense or factored one")
-    ap.add_argument("--cpu-budget", type=float, default=15.0,
-                    help="host seconds the oracle baseline aims to spend (a bounded sample of the workload)")
-    ap.add_argument("--calibrate-copy-mb", type=int, default=0,
-                    help="run an untimed plain device-to-device copy of this many MiB first (a known-size "
-                         "reference for hardware byte counters)")
-    args = ap.parse_args()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: the BOM hot path here is built and measured on a single MI355X "
-              "(sharding is a design note, not part of this build).", file=sys.stderr)
-        sys.exit(2)
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(2)
-    bom.load(build_if_missing=False)
-    w = BY_NAME[args.workload]
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    if args.calibrate_copy_mb > 0:
-        nbytes = args.calibrate_copy_mb << 20
-        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"[bench] calibration copy of {nbytes} bytes done (3 launches)")
-        del src, dst
-        torch.cuda.empty_cache()
+def run_workload(w, args, cpu_budget, dev):
+    """Inputs of workload w resident in HBM, W warmup steps, K timed steps, per-stage times from HIP events,
+    the roofline of the dominant stage and the oracle baseline. Returns the JSON object of this workload."""
     state_dtype = torch.bfloat16 if args.state_dtype == "bf16" else torch.float32
-    if state_dtype == torch.bfloat16 and (w.factored or w.dtype != "bf16"):
-        print("bf16 state storage applies to the dense layout with bf16 logits", file=sys.stderr)
-        sys.exit(2)
-    if args.adam_mini and state_dtype == torch.bfloat16:
-        print("the block-shared second moment keeps fp32 state", file=sys.stderr)
-        sys.exit(2)
-    prob = Problem(w, dev, clip_norm=args.clip_norm, state_dtype=state_dtype, adam_mini=args.adam_mini)
+    prob = Problem(w, dev, clip_norm=args.clip_norm, state_dtype=state_dtype, adam_mini=args.adam_mini,
+                   z_route=args.z_route)
     stages = ["bom_residual", "bom_ema", "bom_head_vjp", "bom_update"]
 
     t = 0
@@ -462,7 +423,7 @@ def main():
         t += 1
         prob.step(t)
     torch.cuda.synchronize()
-    log(f"[bench] warmup {args.warmup} steps done")
+    log(f"[bench] {w.name}: warmup {args.warmup} steps done")
 
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -481,10 +442,10 @@ def main():
     per_step = np.array([evs[k][0].elapsed_time(evs[k][4]) for k in range(args.steps)])
     stage_ms = {s: float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
                 for i, s in enumerate(stages)}
-    log(f"[bench] timed {args.steps} steps: {ms_per_step:.4f} ms/step (wall {wall:.2f}s)")
+    log(f"[bench] {w.name}: timed {args.steps} steps: {ms_per_step:.4f} ms/step (wall {wall:.2f}s)")
 
     alg = algorithmic(w, clip=args.clip_norm > 0, bf16_state=state_dtype == torch.bfloat16,
-                      blocks=(prob.segments, prob.blocks) if args.adam_mini else None)
+                      blocks=(prob.segments, prob.blocks) if args.adam_mini else None, z_route=args.z_route)
     dom = max(stages, key=lambda s: stage_ms[s])
     a = alg[dom]
     sec = stage_ms[dom] / 1e3
@@ -497,7 +458,8 @@ def main():
     roofline = {"bound": a["bound"], "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                 "frac": round(achieved / peak, 4),
                 "traffic": (stored_traffic(dom, w.name)
-                            if args.clip_norm == 0 and args.state_dtype == "f32" and not args.adam_mini else None),
+                            if args.clip_norm == 0 and args.state_dtype == "f32" and not args.adam_mini
+                            and not args.z_route else None),
                 "kernel": dom,
                 "algorithmic_per_launch": a["amount"], "per_unit": a["per_unit"]}
     per_stage = {}
@@ -506,30 +468,24 @@ def main():
         ss = stage_ms[s] / 1e3
         rate = b["amount"] / ss / (1e9 if b["bound"] == "hbm" else 1e12)
         pk = HBM_PEAK_GBS if b["bound"] == "hbm" else (MFMA_BF16_PEAK_TFS if b["bound"] == "mfma" else FP32_PEAK_TFS)
-        per_stage[s] = {"ms": round(stage_ms[s], 5), "rate": round(rate, 2),
+        per_stage[s] = {"ms": round(stage_ms[s], 5), "us": round(stage_ms[s] * 1e3, 2), "rate": round(rate, 2),
                         "unit": "GB/s" if b["bound"] == "hbm" else "TFLOP/s", "frac": round(rate / pk, 4)}
 
     n_valid = int(prob.res["n_valid"].item())
     out = {
-        "metric": METRIC,
         "value": round(n_valid / (ms_per_step / 1e3), 1),
         "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
+        "us_per_step": round(ms_per_step * 1e3, 2),
         "steps_per_s": round(1e3 / ms_per_step, 2),
         "median_ms_per_step": round(float(np.median(per_step)), 5),
         "p10_p90_ms": [round(float(np.percentile(per_step, 10)), 5), round(float(np.percentile(per_step, 90)), 5)],
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
-        "data": "synthetic",
         "config": {"workload": w.name, "N": w.N, "d": w.d, "V": w.V, "P": w.P, "tokens_per_step": n_valid,
                    "second_moment": "blocks" if args.adam_mini else ("factored" if w.factored else "dense"),
                    "clip_norm": args.clip_norm,
-                   "state_dtype": args.state_dtype},
+                   "state_dtype": args.state_dtype,
+                   "head_input": "logits" if args.z_route else "residual"},
         "stages": per_stage,
         "roofline": roofline,
     }
@@ -537,11 +493,104 @@ def main():
         out["forward"] = time_forward(prob, args.steps)
     if args.telemetry:
         out["telemetry"] = time_telemetry(prob, args.steps)
+    del prob
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+        log(f"[bench] {w.name}: timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(w, cpu_budget)
     else:
         out["cpu_baseline"] = None
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default=None, choices=[w.name for w in WORKLOADS],
+                    help="measure only this workload (default: the 8B-class step as the headline, every other "
+                         "workload under per_config)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--state-dtype", choices=["f32", "bf16"], default="f32",
+                    help="storage of theta, v and u (bf16: the paper's fine-tuning protocol; dense layout, bf16 "
+                         "logits only)")
+    ap.add_argument("--forward", action="store_true",
+                    help="also time the head forward Z = H W that produces the logits (common work, outside the "
+                         "step) against the MFMA roofline")
+    ap.add_argument("--telemetry", action="store_true",
+                    help="also time the head drift telemetry call (a diagnostic for telemetry steps, outside the "
+                         "step) on the last step's residual, history and features")
+    ap.add_argument("--clip-norm", type=float, default=0.0,
+                    help="global-norm clipping of the update numerator at this norm (0: none; the paper's "
+                         "language-model protocols clip at 1.0)")
+    ap.add_argument("--adam-mini", action="store_true",
+                    help="block-shared second moment (Adam-mini's update map with the BOM numerator) over a "
+                         "transformer-shaped partition of the flat buffer, instead of the dense or factored one")
+    ap.add_argument("--z-route", action="store_true",
+                    help="the head products take the logits Z and row_lse and form R themselves; the residual "
+                         "writes no R")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="host seconds the oracle baseline aims to spend on the headline workload")
+    ap.add_argument("--cpu-budget-other", type=float, default=5.0,
+                    help="host seconds the oracle baseline aims to spend on each per_config workload")
+    ap.add_argument("--calibrate-copy-mb", type=int, default=0,
+                    help="run an untimed plain device-to-device copy of this many MiB first (a known-size "
+                         "reference for hardware byte counters)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the BOM hot path here is built and measured on a single MI355X "
+              "(sharding is a design note, not part of this build).", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    bom.load(build_if_missing=False)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.calibrate_copy_mb > 0:
+        nbytes = args.calibrate_copy_mb << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {nbytes} bytes done (3 launches)")
+        del src, dst
+        torch.cuda.empty_cache()
+    state_dtype = torch.bfloat16 if args.state_dtype == "bf16" else torch.float32
+    headline = BY_NAME[args.workload or HEADLINE_WORKLOAD]
+    others = [] if args.workload else [w for w in WORKLOADS if w.name != headline.name]
+    for w in [headline] + others:
+        if state_dtype == torch.bfloat16 and (w.factored or w.dtype != "bf16"):
+            print(f"bf16 state storage applies to the dense layout with bf16 logits ({w.name} has neither); "
+                  "pick a workload with --workload", file=sys.stderr)
+            sys.exit(2)
+    if args.adam_mini and state_dtype == torch.bfloat16:
+        print("the block-shared second moment keeps fp32 state", file=sys.stderr)
+        sys.exit(2)
+
+    main_res = run_workload(headline, args, args.cpu_budget, dev)
+    out = {
+        "metric": METRIC,
+        "value": main_res.pop("value"),
+        "unit": main_res.pop("unit"),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_res.pop("ms_per_step"),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": main_res.pop("dtype"),
+        "data": "synthetic",
+    }
+    out.update(main_res)
+    if others:
+        out["per_config"] = {}
+        for w in others:
+            out["per_config"][w.name] = run_workload(w, args, args.cpu_budget_other, dev)
     print(json.dumps(out), flush=True)
 
 

@@ -59,6 +59,11 @@ typedef enum { BOM_F32 = 0, BOM_BF16 = 1 } bom_dtype;
 /* Bits of the device flags word written by bom_residual. */
 #define BOM_FLAG_LABEL_RANGE 1 /* some label was neither ignore_index nor in [0, V); that row is ignored */
 #define BOM_FLAG_EMPTY 2       /* no valid row (N_t = 0): s = 0, loss = 0, downstream gradients are 0 */
+/* Informational: rows too wide for one workgroup are shared by several workgroups that exchange
+ * per-part row records with a bounded wait; a workgroup whose wait ran out recomputed the missing
+ * records from Z with the same operations in the same order. Every output is bitwise the same as
+ * without it; the bit only tells that the exchange was slow. */
+#define BOM_FLAG_RESIDUAL_RECOMPUTED 4
 
 /* Second-moment layouts of bom_update. */
 #define BOM_V_DENSE 0
@@ -122,7 +127,8 @@ bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, 
  * objective, Eq. (3), whose gradient is Eq. (4): u = (1 - lambda) g + lambda Jbar^T q_hat.
  * For the linear head z_i = W^T h_i (+ b), the gradient of L_mix with respect to the logits is
  *   G_ij = [i in I] ((1 - lambda) R_ij + lambda q_hat_j) / N_t        (q_hat held constant)
- * and the head products are
+ * with R the residual rows of Sec. 3.2 (r_i = softmax(z_i) - onehot(y_i), Algorithm 1), and the head
+ * products are
  *   dW = H^T G + dW_beta * dW     [d, V] (dW_beta = 0 overwrites; dW is not read then)
  *   db = (1 - lambda) s + lambda q_hat   [V]  (bias Jacobian = identity; equals 1^T G)
  *   dH = G W^T                     [N, d] of dh_dt
@@ -135,11 +141,20 @@ bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, 
  * rounded to bf16 for the MFMA), and fp32 inputs fold it in fp32.
  * N_t is read from the device word n_valid; when it is 0, G = 0.
  *
+ * R_or_Z and is_residual: with is_residual = 1 the argument is R as bom_residual writes it (rows outside
+ * I zero). With is_residual = 0 it is the logits Z, and the products form R themselves as their operand
+ * copies pass through registers: R_ij = exp(z_ij - row_lse[i]) - [j == y_i] for rows in I, 0 for the
+ * others, formed as bom_residual forms it for rows wider than one workgroup's registers (2^(z log2 e -
+ * lse log2 e), minus 1 at the label) and rounded to dt once; it equals the stored R up to one rounding of
+ * dt (bom_residual's narrow-row kernels scale exp(z - max) by 1/sum instead). bom_residual may then skip
+ * writing R (R = NULL there): the step reads Z instead of writing and reading R, at the price of one
+ * exponential per element of each operand copy.
+ *
  *   H   device [N, ldh] of dt.   W device [d, ldw] of dt (the head as d x V).
- *   R   device [N, ldr] of dt: the residual rows written by bom_residual. Rows outside I must be
- *       zero (bom_residual writes them so); the rank-1 form relies on it.
+ *   R_or_Z device [N, ldr] of dt.
  *   dt  BOM_BF16 (MFMA path, fp32 accumulation) or BOM_F32.
  *   labels device int32 [N] (defines I with ignore_index, as in bom_residual).
+ *   row_lse device fp32 [N] (bom_residual's row_lse): read only when is_residual = 0, else may be NULL.
  *   q_hat device fp32 [V].   s device fp32 [V] (only read when db != NULL).
  *   n_valid device int32 [1].
  *   dW  device [d, lddw] of dw_dt; lddw >= V.   db device [V] of dw_dt, or NULL.
@@ -147,13 +162,14 @@ bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, 
  *       rounded to nearest-even bf16: dW = bf16(H^T G + dW_beta * dW)).
  *   dH  device [N, lddh] of dh_dt (BOM_BF16 or BOM_F32), or NULL.
  *   workspace: at least bom_head_vjp_workspace_bytes(N, d, V, dt, dw_dt) bytes (may be 0).
- * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_DTYPE, BOM_ERR_HYPER (lambda not in [0,1]),
- *         BOM_ERR_WORKSPACE, BOM_ERR_HIP.
+ * Errors: BOM_ERR_NULL (also: row_lse missing with is_residual = 0), BOM_ERR_SHAPE (also: is_residual
+ *         not 0 or 1), BOM_ERR_DTYPE, BOM_ERR_HYPER (lambda not in [0,1]), BOM_ERR_WORKSPACE, BOM_ERR_HIP.
  * ---------------------------------------------------------------------------------------- */
 size_t bom_head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype dt, bom_dtype dw_dt);
-bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* R, int64_t ldr,
+bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw,
+                        const void* R_or_Z, int32_t is_residual, int64_t ldr,
                         bom_dtype dt, int64_t N, int64_t d, int64_t V,
-                        const int32_t* labels, int32_t ignore_index,
+                        const int32_t* labels, int32_t ignore_index, const float* row_lse,
                         const float* q_hat, const float* s, const int32_t* n_valid, float lambda,
                         void* dW, bom_dtype dw_dt, int64_t lddw, float dW_beta,
                         void* db, void* dH, bom_dtype dh_dt, int64_t lddh,
@@ -291,6 +307,9 @@ const char* bom_status_string(bom_status status);
 const char* bom_last_error(void);
 /* Library ABI version (major * 10000 + minor * 100 + patch). */
 int32_t bom_version(void);
+/* Identity of the sources the library was built from: the first 16 hex digits of a SHA-256 over the
+ * names and contents of the HIP sources, their headers and this header (static text). */
+const char* bom_build_id(void);
 
 #ifdef __cplusplus
 }

@@ -3,6 +3,7 @@ from __future__ import annotations
 
 import concurrent.futures as cf
 import glob
+import hashlib
 import os
 import subprocess
 
@@ -23,9 +24,27 @@ CFLAGS = [
 ]
 
 
-def _compile(src: str) -> str:
+def source_files() -> list:
+    """The files libbom.so is built from: the HIP sources, their headers and the C-ABI header."""
+    return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.hpp")) +
+                  [os.path.join(ROOT, "include", "bom.h")])
+
+
+def source_hash() -> str:
+    """First 16 hex digits of the SHA-256 over the names and contents of source_files(); compiled into
+    the library (bom_build_id) so that a loader can tell a library built from other sources."""
+    h = hashlib.sha256()
+    for path in source_files():
+        h.update(os.path.relpath(path, ROOT).encode() + b"\0")
+        with open(path, "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    return h.hexdigest()[:16]
+
+
+def _compile(src: str, build_id: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *CFLAGS, f'-DBOM_BUILD_ID="{build_id}"', "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
@@ -36,8 +55,9 @@ def build(jobs: int = 8) -> str:
     """Compile csrc/*.hip and link libbom.so in the package directory; returns its path."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    build_id = source_hash()
     with cf.ThreadPoolExecutor(max_workers=min(jobs, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
+        objs = list(ex.map(lambda src: _compile(src, build_id), srcs))
     tmp = LIB_PATH + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

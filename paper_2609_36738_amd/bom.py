@@ -16,7 +16,7 @@ from . import _build
 
 BOM_OK = 0
 BOM_F32, BOM_BF16 = 0, 1
-BOM_FLAG_LABEL_RANGE, BOM_FLAG_EMPTY = 1, 2
+BOM_FLAG_LABEL_RANGE, BOM_FLAG_EMPTY, BOM_FLAG_RESIDUAL_RECOMPUTED = 1, 2, 4
 BOM_V_DENSE, BOM_V_FACTORED, BOM_V_BLOCKS = 0, 1, 2
 BOM_MAX_SEGMENTS = 16
 
@@ -47,8 +47,14 @@ def lib_path() -> str:
     return _build.LIB_PATH
 
 
+class StaleLibraryError(RuntimeError):
+    """libbom.so was built from sources other than the ones in the tree."""
+
+
 def load(build_if_missing: bool = True):
-    """Load libbom.so (building it in-tree only when no built library exists)."""
+    """Load libbom.so (building it in-tree only when no built library exists). A library whose build id
+    (the hash of the sources it was compiled from) differs from the sources in the tree is refused: rebuild
+    it with paper_2609_36738_amd._build.build() (or __graft_entry__.build())."""
     global _lib
     with _lock:
         if _lib is not None:
@@ -58,6 +64,12 @@ def load(build_if_missing: bool = True):
                 raise FileNotFoundError(f"{_build.LIB_PATH} is not built")
             _build.build()
         lib = ctypes.CDLL(_build.LIB_PATH)
+        lib.bom_build_id.restype = ctypes.c_char_p
+        lib.bom_build_id.argtypes = []
+        built, current = lib.bom_build_id().decode(), _build.source_hash()
+        if built != current:
+            raise StaleLibraryError(f"{_build.LIB_PATH} was built from sources {built}, the tree holds {current}: "
+                                    "rebuild it")
         vp, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
         lib.bom_status_string.restype = ctypes.c_char_p
         lib.bom_status_string.argtypes = [ctypes.c_int]
@@ -74,8 +86,8 @@ def load(build_if_missing: bool = True):
         lib.bom_head_vjp_workspace_bytes.restype = sz
         lib.bom_head_vjp_workspace_bytes.argtypes = [i64, i64, i64, ctypes.c_int, ctypes.c_int]
         lib.bom_head_vjp.restype = ctypes.c_int
-        lib.bom_head_vjp.argtypes = [vp, i64, vp, i64, vp, i64, ctypes.c_int, i64, i64, i64, vp, i32, vp, vp, vp, f32,
-                                     vp, ctypes.c_int, i64, f32, vp, vp, ctypes.c_int, i64, vp, sz, vp]
+        lib.bom_head_vjp.argtypes = [vp, i64, vp, i64, vp, i32, i64, ctypes.c_int, i64, i64, i64, vp, i32, vp, vp, vp,
+                                     vp, f32, vp, ctypes.c_int, i64, f32, vp, vp, ctypes.c_int, i64, vp, sz, vp]
         lib.bom_update_workspace_bytes.restype = sz
         lib.bom_update_workspace_bytes.argtypes = [i64, ctypes.POINTER(bom_update_cfg)]
         lib.bom_update.restype = ctypes.c_int
@@ -176,15 +188,20 @@ def bom_head_vjp_workspace_bytes(N: int, d: int, V: int, dt: int, dw_dt: int = B
 
 
 def bom_head_vjp(H, W, R, labels, q_hat, n_valid, *, s=None, lam=0.5, ignore_index=-100, dW=None, dW_beta=0.0,
-                 want_db=False, db=None, want_dH=True, dH=None, dh_dtype=None, workspace=None, stream=None) -> dict:
-    """dW = H^T G, db = (1 - lambda) s + lambda q_hat, dH = G W^T with G folded from R and q_hat."""
+                 want_db=False, db=None, want_dH=True, dH=None, dh_dtype=None, workspace=None, stream=None,
+                 row_lse=None) -> dict:
+    """dW = H^T G, db = (1 - lambda) s + lambda q_hat, dH = G W^T with G folded from R and q_hat.
+    With row_lse given, the third argument is the logits Z (is_residual = 0) and the kernels form R
+    from Z and row_lse themselves."""
     lib = load()
     N, d = H.shape
     V = W.shape[1]
     dev = H.device
     dt = _dtype_code(H)
     if _dtype_code(W) != dt or _dtype_code(R) != dt:
-        raise TypeError("H, W and R must share a dtype")
+        raise TypeError("H, W and R (or Z) must share a dtype")
+    if row_lse is not None and (row_lse.dtype != torch.float32 or row_lse.numel() != N or not row_lse.is_contiguous()):
+        raise ValueError("row_lse must be a contiguous float32 tensor of N elements")
     ldh, ldw, ldr = _rowmajor(H, "H"), _rowmajor(W, "W"), _rowmajor(R, "R")
     dW = torch.empty((d, V), dtype=torch.float32, device=dev) if dW is None else dW
     lddw = _rowmajor(dW, "dW")
@@ -199,7 +216,8 @@ def bom_head_vjp(H, W, R, labels, q_hat, n_valid, *, s=None, lam=0.5, ignore_ind
     lddh = _rowmajor(dH, "dH") if dH is not None else d
     nb = lib.bom_head_vjp_workspace_bytes(N, d, V, dt, dw_dt)
     workspace = _workspace(nb, dev, workspace)
-    _check(lib.bom_head_vjp(_ptr(H), ldh, _ptr(W), ldw, _ptr(R), ldr, dt, N, d, V, _ptr(labels), ignore_index,
+    _check(lib.bom_head_vjp(_ptr(H), ldh, _ptr(W), ldw, _ptr(R), 0 if row_lse is not None else 1, ldr, dt, N, d, V,
+                            _ptr(labels), ignore_index, _ptr(row_lse),
                             _ptr(q_hat), _ptr(s), _ptr(n_valid), float(lam), _ptr(dW), dw_dt, lddw, float(dW_beta),
                             _ptr(db),
                             _ptr(dH), dh_dt, lddh, _ptr(workspace), 0 if workspace is None else workspace.numel(),

@@ -63,7 +63,12 @@ const char* bom_status_string(bom_status s) {
 
 const char* bom_last_error(void) { return g_last_error; }
 
-int32_t bom_version(void) { return 20100; }
+int32_t bom_version(void) { return 30000; }
+
+#ifndef BOM_BUILD_ID
+#define BOM_BUILD_ID "unknown"
+#endif
+const char* bom_build_id(void) { return BOM_BUILD_ID; }
 
 size_t bom_residual_workspace_bytes(int64_t N, int64_t V, bom_dtype z_dt) {
     if (N < 1 || V < 1 || N >= kMaxDim || V >= kMaxDim || !is_dtype(z_dt)) return 0;
@@ -116,14 +121,18 @@ size_t bom_head_vjp_workspace_bytes(int64_t N, int64_t d, int64_t V, bom_dtype d
     return bom::head_vjp_workspace_bytes(N, d, V, dt, dw_dt);
 }
 
-bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* R, int64_t ldr,
-                        bom_dtype dt, int64_t N, int64_t d, int64_t V, const int32_t* labels, int32_t ignore_index,
-                        const float* q_hat, const float* s, const int32_t* n_valid, float lambda, void* dW,
-                        bom_dtype dw_dt, int64_t lddw, float dW_beta, void* db, void* dH, bom_dtype dh_dt,
-                        int64_t lddh, void* workspace, size_t ws_bytes, void* stream) {
+bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* R, int32_t is_residual,
+                        int64_t ldr, bom_dtype dt, int64_t N, int64_t d, int64_t V, const int32_t* labels,
+                        int32_t ignore_index, const float* row_lse, const float* q_hat, const float* s,
+                        const int32_t* n_valid, float lambda, void* dW, bom_dtype dw_dt, int64_t lddw, float dW_beta,
+                        void* db, void* dH, bom_dtype dh_dt, int64_t lddh, void* workspace, size_t ws_bytes,
+                        void* stream) {
     if (!H || !W || !R || !labels || !q_hat || !n_valid || !dW)
-        return fail(BOM_ERR_NULL, "bom_head_vjp: H, W, R, labels, q_hat, n_valid and dW are required");
+        return fail(BOM_ERR_NULL, "bom_head_vjp: H, W, R_or_Z, labels, q_hat, n_valid and dW are required");
     if (db && !s) return fail(BOM_ERR_NULL, "bom_head_vjp: s is required when db is requested");
+    if (is_residual != 0 && is_residual != 1)
+        return fail(BOM_ERR_SHAPE, "bom_head_vjp: is_residual must be 1 (R) or 0 (logits Z)");
+    if (!is_residual && !row_lse) return fail(BOM_ERR_NULL, "bom_head_vjp: row_lse is required with the logits Z");
     if (N < 1 || d < 1 || V < 2 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim)
         return fail(BOM_ERR_SHAPE, "bom_head_vjp: need N >= 1, d >= 1, V >= 2, all < 2^31");
     if (ldh < d || ldw < V || ldr < V || lddw < V || (dH && lddh < d))
@@ -139,8 +148,8 @@ bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw, 
         return fail(BOM_ERR_WORKSPACE, "bom_head_vjp: workspace needs %zu bytes, got %zu", need, ws_bytes);
     if (workspace && reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
         return fail(BOM_ERR_WORKSPACE, "bom_head_vjp: workspace must be 256-byte aligned");
-    bom::HeadVjpArgs a{H, ldh, W, ldw, R, ldr, dt, (int)N, (int)d, (int)V, labels, ignore_index, q_hat, s, n_valid, lambda,
-                       dW, dw_dt, lddw, dW_beta, db, dH, dh_dt, lddh, workspace, ws_bytes};
+    bom::HeadVjpArgs a{H, ldh, W, ldw, R, ldr, is_residual, row_lse, dt, (int)N, (int)d, (int)V, labels, ignore_index,
+                       q_hat, s, n_valid, lambda, dW, dw_dt, lddw, dW_beta, db, dH, dh_dt, lddh, workspace, ws_bytes};
     return hip_status(bom::launch_head_vjp(a, static_cast<hipStream_t>(stream)), "bom_head_vjp");
 }
 

@@ -38,11 +38,39 @@ struct Fold {
     const float* vmask;  // [N] 1 for rows in I, else 0
     const float* scal;   // [0] alpha = (1 - lambda) / N_t; [1] s_out; [2], [3] bf16 pairs (r_coef, 0), (0, r_coef)
     const float* cqp;    // [V] history term of the rescaled fold G = s_out * (r_coef * R + cqp)
+    const float* zc;     // logits input: [N] lse_i log2 e for rows in I, +inf otherwise; null: R is stored
+    const int32_t* labels;
 };
 
 struct VjpWs {
-    size_t cq_off, cqp_off, vmask_off, scal_off, hpart_off, hsum_off, u_off, part_off, total;
+    size_t cq_off, cqp_off, vmask_off, scal_off, zc_off, hpart_off, hsum_off, u_off, part_off, total;
 };
+
+// ---- residual rows from the logits ----------------------------------------------------------------
+// With the logits Z as input, the products take R = softmax(Z) - onehot(y) chunk by chunk as the operand
+// copies pass through registers: r = exp2(z log2 e - c_i) with c_i = lse_i log2 e (c_i = +inf for rows
+// outside I, so their r is 0), minus 1 at column y_i, rounded once to the operand type -- the operations
+// bom_residual uses when it writes R, so R is the same whether it is stored or formed here.
+__device__ __forceinline__ float r_from_z(float z, float c, bool at_label) {
+    float p = exp2_fast(fmaf(z, kLog2e, -c));
+    if (at_label) p -= 1.0f;
+    return p;
+}
+// Eight bf16 logits of one row (columns j0 .. j0 + 7, lab_off = y_i - j0) to eight bf16 residuals; ok = false
+// gives zeros (a chunk outside the operand).
+__device__ __forceinline__ u32x4_t z_chunk_to_r(u32x4_t z, float c, int lab_off, bool ok) {
+    u32x4_t r;
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+        r[p] = pack_bf16x2(r_from_z(bf16_lo(z[p]), c, lab_off == 2 * p), r_from_z(bf16_hi(z[p]), c, lab_off == 2 * p + 1));
+    const uint32_t mk = lane_mask(ok);
+    return u32x4_t{r[0] & mk, r[1] & mk, r[2] & mk, r[3] & mk};
+}
+// c_i of row i from lse and the label (the fused kernel forms it itself)
+__device__ __forceinline__ float z_row_c(const float* row_lse, const int32_t* labels, int i, int V, int32_t ig) {
+    bool bad = false;
+    return label_valid(labels[i], V, ig, &bad) ? row_lse[i] * kLog2e : INFINITY;
+}
 
 // ---- prep -------------------------------------------------------------------------------------
 // G = alpha R + mask * cq  (alpha = (1-lambda)/N_t, cq = lambda q_hat / N_t) is also written
@@ -55,7 +83,8 @@ __global__ __launch_bounds__(256) void vjp_prep_kernel(const float* __restrict__
                                                        float* __restrict__ cq, float* __restrict__ cqp,
                                                        float* __restrict__ vmask, float* __restrict__ scal,
                                                        float* __restrict__ db, const float* __restrict__ hpart, int nrb,
-                                                       int d, float* __restrict__ hsum) {
+                                                       int d, float* __restrict__ hsum, const float* __restrict__ row_lse,
+                                                       float* __restrict__ zc) {
     const int idx = blockIdx.x * 256 + threadIdx.x;
     if (hpart != nullptr && idx < d) {   // rank-1 form: hsum_m = sum of the row-block partials, in block order
         float a = 0.f;
@@ -71,7 +100,9 @@ __global__ __launch_bounds__(256) void vjp_prep_kernel(const float* __restrict__
     }
     if (idx < N) {
         bool bad = false;
-        vmask[idx] = label_valid(labels[idx], V, ignore_index, &bad) ? 1.f : 0.f;
+        const bool valid = label_valid(labels[idx], V, ignore_index, &bad);
+        vmask[idx] = valid ? 1.f : 0.f;
+        if (row_lse != nullptr) zc[idx] = valid ? row_lse[idx] * kLog2e : INFINITY;
     }
     if (idx == 0) {
         scal[0] = nt > 0 ? (float)((1.0 - (double)lambda) / (double)nt) : 0.f;
@@ -96,6 +127,16 @@ __device__ __forceinline__ void stf<float>(float* p, int64_t i, float x) { p[i] 
 template <>
 __device__ __forceinline__ void stf<uint16_t>(uint16_t* p, int64_t i, float x) { p[i] = f32_to_bf16(x); }
 
+// Element (row, col) of R: as stored, or formed from the logits (rounded to T like a stored R).
+template <typename T>
+__device__ __forceinline__ float r_elem(const T* RZ, int64_t ld, int row, int col, const Fold& f) {
+    const float x = ldf(RZ, (int64_t)row * ld + col);
+    if (f.zc == nullptr) return x;
+    const float p = r_from_z(x, f.zc[row], col == f.labels[row]);
+    if constexpr (std::is_same<T, uint16_t>::value) return bf16_to_f32(f32_to_bf16(p));
+    return p;
+}
+
 // ---- SIMT fallback: 64 x 64 tiles, 16-deep k, 4 x 4 outputs per thread --------------------------
 constexpr int SB = 64, SK = 16;
 
@@ -116,7 +157,7 @@ __global__ __launch_bounds__(256) void simt_dW_kernel(const T* __restrict__ H, i
             const int idx = e * 256 + t, kk = idx / SB, cc = idx % SB;
             const int k = k0 + kk;
             As[kk][cc] = (k < ke && m0 + cc < M) ? ldf(H, (int64_t)k * ldh + m0 + cc) : 0.f;
-            Bs[kk][cc] = (k < ke && n0 + cc < Nn) ? fmaf(alpha, ldf(R, (int64_t)k * ldr + n0 + cc), f.vmask[k] * f.cq[n0 + cc]) : 0.f;
+            Bs[kk][cc] = (k < ke && n0 + cc < Nn) ? fmaf(alpha, r_elem(R, ldr, k, n0 + cc, f), f.vmask[k] * f.cq[n0 + cc]) : 0.f;
         }
         __syncthreads();
 #pragma unroll
@@ -164,7 +205,7 @@ __global__ __launch_bounds__(256) void simt_dH_kernel(const T* __restrict__ R, i
         for (int e = 0; e < 4; ++e) {
             const int idx = e * 256 + t, rr = idx / SK, kk = idx % SK;
             const int k = k0 + kk;
-            As[kk][rr] = (k < ke && m0 + rr < M) ? fmaf(alpha, ldf(R, (int64_t)(m0 + rr) * ldr + k), f.vmask[m0 + rr] * f.cq[k]) : 0.f;
+            As[kk][rr] = (k < ke && m0 + rr < M) ? fmaf(alpha, r_elem(R, ldr, m0 + rr, k, f), f.vmask[m0 + rr] * f.cq[k]) : 0.f;
             Bs[kk][rr] = (k < ke && n0 + rr < Nn) ? ldf(W, (int64_t)(n0 + rr) * ldw + k) : 0.f;
         }
         __syncthreads();
@@ -244,8 +285,10 @@ struct StageGt {
     uint4 r[4];
     uint32_t mk[4];
     float vm[4];      // row masks as loaded; rows past kend are dropped by mk at store time
+    float zc[4];      // logits input: c of each row and the label's offset in this thread's 8 columns
+    int lo[4];
     __device__ __forceinline__ void load(const uint16_t* R, int64_t ldr, int Nn, int k0, int kend, int n0,
-                                         const float* vmask) {
+                                         const Fold& f) {
         const int t = threadIdx.x, kq = t / 16, mq = t % 16;
         const int n = n0 + mq * 8;
         const bool nok = n < Nn;
@@ -253,17 +296,30 @@ struct StageGt {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int k = k0 + kq * 4 + q;
-            vm[q] = vmask[k < kend ? k : kend - 1];
+            const int kc = k < kend ? k : kend - 1;
+            vm[q] = f.vmask[kc];
             mk[q] = lane_mask(nok && k < kend);
-            r[q] = ld16(R + (int64_t)(k < kend ? k : kend - 1) * ldr + nc);
+            r[q] = ld16(R + (int64_t)kc * ldr + nc);
+            if (f.zc != nullptr) {
+                zc[q] = f.zc[kc];
+                lo[q] = f.labels[kc] - nc;
+            }
         }
     }
-    __device__ __forceinline__ void store(uint16_t (*Bs)[LDK], float alpha, const float* cqn) const {
+    __device__ __forceinline__ void store(uint16_t (*Bs)[LDK], float alpha, const float* cqn, const Fold& f) const {
         const int t = threadIdx.x, kq = t / 16, mq = t % 16;
-        const uint32_t w[4][4] = {{r[0].x & mk[0], r[0].y & mk[0], r[0].z & mk[0], r[0].w & mk[0]},
-                                  {r[1].x & mk[1], r[1].y & mk[1], r[1].z & mk[1], r[1].w & mk[1]},
-                                  {r[2].x & mk[2], r[2].y & mk[2], r[2].z & mk[2], r[2].w & mk[2]},
-                                  {r[3].x & mk[3], r[3].y & mk[3], r[3].z & mk[3], r[3].w & mk[3]}};
+        uint4 x[4] = {r[0], r[1], r[2], r[3]};
+        if (f.zc != nullptr) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const u32x4_t y = z_chunk_to_r(u32x4_t{x[q].x, x[q].y, x[q].z, x[q].w}, zc[q], lo[q], true);
+                x[q] = make_uint4(y[0], y[1], y[2], y[3]);
+            }
+        }
+        const uint32_t w[4][4] = {{x[0].x & mk[0], x[0].y & mk[0], x[0].z & mk[0], x[0].w & mk[0]},
+                                  {x[1].x & mk[1], x[1].y & mk[1], x[1].z & mk[1], x[1].w & mk[1]},
+                                  {x[2].x & mk[2], x[2].y & mk[2], x[2].z & mk[2], x[2].w & mk[2]},
+                                  {x[3].x & mk[3], x[3].y & mk[3], x[3].z & mk[3], x[3].w & mk[3]}};
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
             float g[4];
@@ -288,6 +344,8 @@ struct StageK {
     uint32_t mk[4];
     float vm[4];      // FOLD: row masks and the history coefficients of this thread's k chunk, as
     float4 cq[2];     // loaded (consumed at store time, after the MFMA phase)
+    float zc[4];      // FOLD with logits input: c of each row and the label's offset in the k chunk
+    int lo[4];
     __device__ __forceinline__ void load(const uint16_t* X, int64_t ldx, int rows, int r0, int k0, int kend,
                                          const Fold& f) {
         const int t = threadIdx.x;
@@ -300,18 +358,26 @@ struct StageK {
             mk[e] = lane_mask(row < rows && k < kend);
             r[e] = ld16(X + (int64_t)rc * ldx + kc);
             if (FOLD) vm[e] = f.vmask[rc];
+            if (FOLD && f.zc != nullptr) {
+                zc[e] = f.zc[rc];
+                lo[e] = f.labels[rc] - kc;
+            }
         }
         if (FOLD) {
             cq[0] = *reinterpret_cast<const float4*>(f.cq + kc);
             cq[1] = *reinterpret_cast<const float4*>(f.cq + kc + 4);
         }
     }
-    __device__ __forceinline__ void store(uint16_t (*S)[LDK], float alpha) const {
+    __device__ __forceinline__ void store(uint16_t (*S)[LDK], float alpha, const Fold& f) const {
         const int t = threadIdx.x;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int c = e * 256 + t, lr = c / 8, lk = (c % 8) * 8;
             uint4 o = r[e];
+            if (FOLD && f.zc != nullptr) {
+                const u32x4_t x = z_chunk_to_r(u32x4_t{o.x, o.y, o.z, o.w}, zc[e], lo[e], true);
+                o = make_uint4(x[0], x[1], x[2], x[3]);
+            }
             if (FOLD) {
                 const float q8[8] = {cq[0].x, cq[0].y, cq[0].z, cq[0].w, cq[1].x, cq[1].y, cq[1].z, cq[1].w};
                 const uint32_t w[4] = {o.x, o.y, o.z, o.w};
@@ -438,9 +504,9 @@ __global__ __launch_bounds__(256) void mfma_dW_kernel(const uint16_t* __restrict
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     k_loop128<StageHt, StageGt>(
         kb, ke, As, Bs, acc, [&](StageHt& st, int k0) { st.load(H, ldh, M, k0, ke, m0); },
-        [&](StageGt& st, int k0) { st.load(R, ldr, Nn, k0, ke, n0, f.vmask); },
+        [&](StageGt& st, int k0) { st.load(R, ldr, Nn, k0, ke, n0, f); },
         [&](const StageHt& st, uint16_t (*S)[LDK]) { st.store(S); },
-        [&](const StageGt& st, uint16_t (*S)[LDK]) { st.store(S, alpha, cqn); });
+        [&](const StageGt& st, uint16_t (*S)[LDK]) { st.store(S, alpha, cqn, f); });
     if (part == nullptr) {
         for_each_acc(acc, [&](int r, int c, float v) {
             const int m = m0 + r, n = n0 + c;
@@ -479,8 +545,8 @@ __global__ __launch_bounds__(256) void mfma_dH_kernel(const uint16_t* __restrict
     k_loop128<StageK<true>, StageK<false>>(
         kb, ke, As, Bs, acc, [&](StageK<true>& st, int k0) { st.load(R, ldr, M, m0, k0, ke, f); },
         [&](StageK<false>& st, int k0) { st.load(W, ldw, Nn, n0, k0, ke, f); },
-        [&](const StageK<true>& st, uint16_t (*S)[LDK]) { st.store(S, alpha); },
-        [&](const StageK<false>& st, uint16_t (*S)[LDK]) { st.store(S, alpha); });
+        [&](const StageK<true>& st, uint16_t (*S)[LDK]) { st.store(S, alpha, f); },
+        [&](const StageK<false>& st, uint16_t (*S)[LDK]) { st.store(S, alpha, f); });
     if (part == nullptr) {
         for_each_acc(acc, [&](int r, int c, float v) {
             const int m = m0 + r, n = n0 + c;
@@ -561,28 +627,12 @@ __device__ __forceinline__ bool unit_of(const TileRange& r, bool inner_is_m, int
 //   dW = alpha H^T R + hsum cq^T,   hsum_m = sum_{i in I} H_im,  cq_n = lambda q_hat_n / N_t,
 //   dH = alpha R W^T + mask u^T,    u_n = (lambda / N_t) sum_j W_nj q_hat_j,
 // so both GEMMs take R as it is stored (bf16, no rounding of G) and the history enters through
-// the fp32 epilogue. 256 x 256 output tile per workgroup: lds256_kernel runs four waves, each 128 x 128
-// = 4 x 4 blocks of v_mfma_f32_32x32x16_bf16; the 64-deep kernels below run eight waves of 128 x 64 (or
-// four of 128 x 128). Memory reads are buffer loads: a chunk outside the matrix
+// the fp32 epilogue. 256 x 256 output tile per workgroup, on v_mfma_f32_32x32x16_bf16: eight waves of
+// 128 x 64 (or four of 128 x 128). Memory reads are buffer loads: a chunk outside the matrix
 // reads as zero through the descriptor's range check or an out-of-range offset, so loads need no
 // branches and never touch memory past the operand.
 constexpr int LB = 256;                 // output tile
-constexpr int LK = 32;                  // k tile (split-K granularity)
 
-// C = A B for one 256 x 256 tile over k in [kb, ke); dW: A(m, k) = H[k][m], B(k, n) = R[k][n];
-// dH: A(i, k) = R[i][k], B(k, n) = W[n][k]. k tiles of 32 in a ring of 4 LDS stages (32 KB each).
-// Both operands are staged through LDS: each lane copies 16-byte chunks with buffer loads into
-// registers and ds_write_b128. (Copies straight from memory into LDS with buffer_load ... lds share
-// the same ~64 B/clk LDS fill bandwidth and measured no faster.) dH's operands are k-contiguous: LDS rows
-// of 32 k (64 B), chunk c of row r at c ^ ((r >> 2) & 3), fragments read with ds_read_b128. dW's
-// operands are k-outer: LDS rows of 256 values per k (512 B), chunk c of row k at c ^ ((k & 3) << 2),
-// fragments read with the transposing ds_read_b64_tr_b16 (a 16-lane group reads a 4 x 16 block and
-// each lane receives 4 consecutive k of one column). Each wave fills 1 KB contiguous per copy step
-// and every 16-lane read phase touches 16 distinct 16-byte bank groups: no bank conflicts.
-// Output out = alpha C + rv[m] cv[n] (+ beta out for dW), or alpha C into the fp32 split-K partials.
-constexpr int LS = 4;                   // LDS stages
-constexpr int LKT = 32;                 // k tile of the staged kernel
-constexpr int kStageElems = LB * LKT;   // bf16 elements per operand per stage (16 KB)
 
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 typedef short v8s_t __attribute__((ext_vector_type(8)));
@@ -597,255 +647,15 @@ __device__ __forceinline__ bf16x8_t ld_frag_tr(const char* p) {
     return __builtin_bit_cast(bf16x8_t, both);
 }
 
-template <bool IS_DW, typename TO>
-__global__ __launch_bounds__(256, 1) void lds256_kernel(const uint16_t* __restrict__ Xa, int64_t lda,
-                                                        const uint16_t* __restrict__ Xb, int64_t ldb, int M, int Nn, int K,
-                                                        int kps, int inner_count, int outer_count, const float* alpha_p,
-                                                        const float* __restrict__ rv, const float* __restrict__ cv,
-                                                        TO* __restrict__ out, int64_t ldo, float beta,
-                                                        float* __restrict__ part) {
-    __shared__ __attribute__((aligned(1024))) uint16_t lds[LS][2][kStageElems];
-    __shared__ float rv_s[LB];
-    int tm, tn;
-    if (!tile_of(inner_count, outer_count, IS_DW, &tm, &tn)) return;
-    const int m0 = tm * LB, n0 = tn * LB;
-    const int kb = blockIdx.z * kps, ke = min(K, kb + kps);
-    const int nk = (ke - kb + LKT - 1) / LKT;
-    const int nk2 = (nk + 1) & ~1;   // the loop handles k tiles in pairs; a padding tile reads zeros
-    const int l = threadIdx.x % kWave;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int wm = wave / 2, wn = wave % 2;
-
-    // epilogue inputs, loaded now so their latency hides under the main loop
-    const float rv_reg = (part == nullptr && m0 + (int)threadIdx.x < M) ? rv[m0 + threadIdx.x] : 0.f;
-    float cvv[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int n = n0 + wn * 128 + j * 32 + l % 32;
-        cvv[j] = (part == nullptr && n < Nn) ? cv[n] : 0.f;
-    }
-
-    // ---- copy geometry (per lane, constant over k tiles) ----
-    // Copy step q (< 4) of this wave fills LDS kilobyte wave*4 + q of an operand's stage; lane l
-    // writes bytes 16 l of it. dH: that is row (wave*4+q)*16 + l/4, position l%4 (chunk c); offsets
-    // relative to the tile's first row. dW: k row (wave*4+q)*2 + l/32, position l%32 (chunk c);
-    // offsets relative to (k0, first column), the descriptor rebased per k tile.
-    int voff_a[4], voff_b[4], kc[4];
-    bool ok_a[4], ok_b[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int chunk = (wave * 4 + q) * 64 + l;
-        if constexpr (IS_DW) {
-            const int krow = chunk / 32, c = (chunk % 32) ^ ((krow & 3) << 2);
-            voff_a[q] = (int)((int64_t)krow * lda * 2) + c * 16;
-            voff_b[q] = (int)((int64_t)krow * ldb * 2) + c * 16;
-            kc[q] = krow;
-            ok_a[q] = ok_b[q] = true;
-        } else {
-            const int row = chunk / 4, c = (chunk % 4) ^ ((row >> 2) & 3);
-            voff_a[q] = (int)((int64_t)row * lda * 2) + c * 16;
-            voff_b[q] = (int)((int64_t)row * ldb * 2) + c * 16;
-            kc[q] = c * 8;
-            ok_a[q] = row < M - m0;
-            ok_b[q] = row < Nn - n0;
-        }
-    }
-    int bytes_ta = 0, bytes_tb = 0;
-    if constexpr (!IS_DW) {
-        // fixed per workgroup: exact extent of the tile's rows
-        const int ra = min(LB, M - m0), rb = min(LB, Nn - n0);
-        bytes_ta = (int)(((int64_t)(ra - 1) * lda + K) * 2);
-        bytes_tb = (int)(((int64_t)(rb - 1) * ldb + K) * 2);
-    }
-    // Descriptors of k tile kt (dW: rebased on (k0, column tile), rows at or past ke read zeros).
-    struct TileLoad {
-        const uint16_t* ba;
-        const uint16_t* bb;
-        int bytes_a, bytes_b, k0;
-    };
-    auto tile_load = [&](int kt) {
-        TileLoad t;
-        t.k0 = kb + kt * LKT;
-        if constexpr (IS_DW) {
-            const int nv = min(LKT, ke - t.k0);
-            const int nv1 = max(nv, 1);
-            const int kr = min(t.k0, K - 1);
-            t.ba = Xa + (int64_t)kr * lda + m0;
-            t.bb = Xb + (int64_t)kr * ldb + n0;
-            t.bytes_a = nv > 0 ? (int)(((int64_t)(nv1 - 1) * lda + (M - m0)) * 2) : 0;
-            t.bytes_b = nv > 0 ? (int)(((int64_t)(nv1 - 1) * ldb + (Nn - n0)) * 2) : 0;
-        } else {
-            t.ba = Xa + (int64_t)m0 * lda;
-            t.bb = Xb + (int64_t)n0 * ldb;
-            t.bytes_a = bytes_ta;
-            t.bytes_b = bytes_tb;
-        }
-        return t;
-    };
-    auto off_a = [&](const TileLoad& t, int q) {
-        if constexpr (IS_DW) return voff_a[q];
-        else return (ok_a[q] && t.k0 + kc[q] < ke) ? voff_a[q] + t.k0 * 2 : kOob;
-    };
-    auto off_b = [&](const TileLoad& t, int q) {
-        if constexpr (IS_DW) return voff_b[q];
-        else return (ok_b[q] && t.k0 + kc[q] < ke) ? voff_b[q] + t.k0 * 2 : kOob;
-    };
-    // register copies: q < 4 operand A, q >= 4 operand B
-    auto load_one = [&](const TileLoad& t, int q) {
-        if (q < 4) return __builtin_amdgcn_raw_buffer_load_b128(make_desc(t.ba, t.bytes_a), off_a(t, q), 0, 0);
-        return __builtin_amdgcn_raw_buffer_load_b128(make_desc(t.bb, t.bytes_b), off_b(t, q - 4), 0, 0);
-    };
-    auto write_one = [&](int stage, int q, const u32x4_t& v) {
-        char* base = reinterpret_cast<char*>(&lds[stage][q / 4][0]);
-        *reinterpret_cast<u32x4_t*>(base + (wave * 4 + q % 4) * 1024 + l * 16) = v;
-    };
-
-    // ---- fragment geometry ----
-    // dH: fragment row = wave base + block*32 + l%32, chunk kk*2 + l/32 (two swizzled offsets).
-    // dW: 16-lane group g = l/16, s = l%16 supplies k row (g/2)*8 + s/4 (+4 for the upper half) and
-    // columns base + (g%2)*16 + (s%4)*4; block i changes the swizzled chunk, so one offset per block.
-    int fa[4], fb[4];
-    if constexpr (IS_DW) {
-        const int s = l % 16, g = l / 16;
-        const int krow = (g >> 1) * 8 + (s >> 2);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int lo = ((i ^ (s >> 2)) * 4) + (g & 1) * 2 + ((s >> 1) & 1);
-            fa[i] = krow * 512 + ((wm * 16 + lo) << 4) + (s & 1) * 8;
-            fb[i] = krow * 512 + ((wn * 16 + lo) << 4) + (s & 1) * 8;
-        }
-    } else {
-        const int r = l % 32, sw = (r >> 2) & 3;
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            const int c = (kk * 2 + l / 32) ^ sw;
-            fa[kk] = (wm * 128 + r) * 64 + (c << 4);
-            fb[kk] = (wn * 128 + r) * 64 + (c << 4);
-        }
-        fa[2] = fa[3] = fb[2] = fb[3] = 0;
-    }
-
-    f32x16_t acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-    auto read_frags = [&](int stage, int kk, bf16x8_t (&a)[4], bf16x8_t (&b)[4]) {
-        const char* As = reinterpret_cast<const char*>(&lds[stage][0][0]);
-        const char* Bs = reinterpret_cast<const char*>(&lds[stage][1][0]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if constexpr (IS_DW) {
-                a[i] = ld_frag_tr(As + fa[i] + kk * 16 * 512);
-                b[i] = ld_frag_tr(Bs + fb[i] + kk * 16 * 512);
-            } else {
-                a[i] = ld_frag_b128(As + fa[kk] + i * 32 * 64);
-                b[i] = ld_frag_b128(Bs + fb[kk] + i * 32 * 64);
-            }
-        }
-    };
-    auto mfma_rows = [&](const bf16x8_t (&a)[4], const bf16x8_t (&b)[4], int i0, int i1) {
-#pragma unroll
-        for (int i = i0; i < i1; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    };
-    // Instruction order inside each half of an iteration: the first 8 MFMAs each followed by their
-    // share of the next k step's fragment reads (dW reads two 8-byte halves per fragment); in the
-    // first half the last 8 MFMAs each followed by one copy step for later tiles.
-    constexpr int kReadsPerMfma = IS_DW ? 2 : 1;
-    auto interleave_reads = [&]() {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x100, kReadsPerMfma, 0);  // DS read
-        }
-    };
-    // Pipeline: tile kt in LDS stage kt % LS is multiplied while tile kt+1 (already in LDS) waits;
-    // tile kt+2 is written from one register set and tile kt+4 loaded into it (tile kt+3 is in
-    // flight in the other set). A stage is refilled only after the barrier that follows every
-    // wave's last reads of it (each wave drains its LDS reads before that barrier).
-    u32x4_t r0[8], r1[8];
-    bf16x8_t a0[4], b0[4], a1[4], b1[4];
-    auto iteration = [&](int kt, u32x4_t (&rg)[8]) {
-        read_frags(kt % LS, 1, a1, b1);
-        mfma_rows(a0, b0, 0, 2);
-        interleave_reads();
-        __builtin_amdgcn_sched_barrier(0);
-        const int ws = (kt + 2) % LS;
-        const TileLoad t = tile_load(kt + 4);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int i = 2 + q / 4, j = q % 4;
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            write_one(ws, q, rg[q]);
-            rg[q] = load_one(t, q);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-        __builtin_amdgcn_sched_barrier(0);
-        read_frags((kt + 1) % LS, 0, a0, b0);
-        mfma_rows(a1, b1, 0, 4);
-        interleave_reads();
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    {
-        const TileLoad t0 = tile_load(0), t1 = tile_load(1), t2 = tile_load(2), t3 = tile_load(3);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) r0[q] = load_one(t0, q);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) r1[q] = load_one(t1, q);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) write_one(0, q, r0[q]);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) r0[q] = load_one(t2, q);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) write_one(1, q, r1[q]);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) r1[q] = load_one(t3, q);
-    }
-    __syncthreads();
-    read_frags(0, 0, a0, b0);
-    for (int kt = 0; kt < nk2; kt += 2) {
-        iteration(kt, r0);
-        iteration(kt + 1, r1);
-    }
-    __syncthreads();
-    const float alpha = *alpha_p;
-    if (part == nullptr) {
-        rv_s[threadIdx.x] = rv_reg;
-        __syncthreads();
-        for_each_acc256(acc, [&](int r, int c, float v) {
-            const int m = m0 + r, n = n0 + c;
-            if (m < M && n < Nn) {
-                const float x = fmaf(alpha, v, rv_s[r] * cvv[(c >> 5) & 3]);
-                if constexpr (IS_DW) {
-                    float* p = reinterpret_cast<float*>(out) + (int64_t)m * ldo + n;
-                    *p = beta != 0.f ? x + beta * *p : x;
-                } else {
-                    stf<TO>(out, (int64_t)m * ldo + n, x);
-                }
-            }
-        });
-    } else {
-        float* pz = part + (int64_t)blockIdx.z * M * Nn;
-        for_each_acc256(acc, [&](int r, int c, float v) {
-            const int m = m0 + r, n = n0 + c;
-            if (m < M && n < Nn) pz[(int64_t)m * Nn + n] = alpha * v;
-        });
-    }
-}
-
-// The same product with k tiles of 64 in two LDS stages (one barrier per 64 k instead of per 32): the
-// workgroup copies 32 kilobytes per operand per tile, 1 KB per wave and copy step. A k-contiguous operand (dH's two) has LDS rows
-// of 64 k (128 B) with chunk c of row r at swz(r, c) and 16-byte
-// fragment reads; a k-outer operand (dW's two) has LDS rows of 512 B per k as in lds256_kernel and
-// transposing fragment reads. (dW with A given as H^T, k-contiguous, from a transpose of H measured no
+// C = A B for one 256 x 256 output tile over k in [kb, ke), k tiles of 64 in two LDS stages (one barrier
+// per 64 k): the workgroup copies 32 kilobytes per operand per tile, 1 KB per wave and copy step, with
+// buffer loads into registers and ds_write_b128 (copies straight from memory into LDS with buffer_load
+// ... lds share the same ~64 B/clk LDS fill bandwidth and measured slower). A k-contiguous operand (dH's
+// two) has LDS rows of 64 k (128 B) with chunk c of row r at swz(r, c) and 16-byte fragment reads; a
+// k-outer operand (dW's two) has LDS rows of 256 values per k (512 B), chunk c of row k at
+// c ^ ((k & 3) << 2), and fragments read with the transposing ds_read_b64_tr_b16 (a 16-lane group reads a
+// 4 x 16 block and each lane receives 4 consecutive k of one column); every 16-lane read phase touches
+// 16 distinct 16-byte bank groups, so there are no bank conflicts. (dW with A given as H^T, k-contiguous, from a transpose of H measured no
 // faster: the transposing reads of one operand are not what bounds it.) Tile kt+1 is written from registers at the start of
 // iteration kt and tile kt+2 loaded behind it; the barrier sits before the last MFMA step of the tile.
 // Measured on the three language-model shapes, eight waves (two per SIMD) beat four by 5-9 % on every
@@ -871,6 +681,8 @@ struct WideArgs {
     float beta;
     float* part;
     const uint16_t* bias;   // forward: bf16 bias [Nn] or null
+    const float* zc;        // logits input (ZR): c_i per row of R, and the labels
+    const int32_t* labels;
 };
 
 // Products of the 64-deep kernel: C = A B with
@@ -883,7 +695,9 @@ constexpr int kWideDH = 0, kWideDW = 1, kWideFWD = 2;
 // are the workgroup's LDS (two stages of both operands, and the rank-1 row vector of the tile).
 // NW waves share the 256 x 256 tile: four (one per SIMD) each own 128 x 128, or eight (two per SIMD,
 // so that one wave's copies and LDS reads overlap the other's MFMAs) each own 128 x 64.
-template <int MODE, typename TO, int NW>
+// ZR: the operand that is R (dH's A, dW's B) holds the logits Z, and each copy is turned into R in
+// registers before its LDS write (z_chunk_to_r).
+template <int MODE, typename TO, int NW, bool ZR = false>
 __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t (&lds)[2][2][WSE], float (&rv_s)[LB]) {
     static_assert(NW == 4 || NW == 8, "four or eight waves");
     constexpr int KT = WKT;
@@ -952,6 +766,27 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         geo(KA, lda, M - m0, q, &voff_a[q], &kc_a[q], &ok_a[q]);
         geo(KB, ldb, Nn - n0, q, &voff_b[q], &kc_b[q], &ok_b[q]);
     }
+    // logits input: per copy slot of the R operand, c of its row and the label (dH: rows fixed per
+    // slot, labels as offsets from the chunk's k at write time; dW: rows change with the k tile, so both
+    // are loaded with each copy, the label as an offset from the chunk's first column)
+    constexpr bool ZA = ZR && MODE == kWideDH, ZB = ZR && MODE == kWideDW;
+    float zrc[CPO];
+    int zry[CPO], zcol[CPO];
+#pragma unroll
+    for (int q = 0; q < CPO; ++q) {
+        zrc[q] = INFINITY;
+        zry[q] = -1;
+        zcol[q] = 0;
+        const int chunk = (wave * CPO + q) * 64 + l;
+        if constexpr (ZA) {
+            const int i = m0 + chunk / 8;
+            if (i < M) {
+                zrc[q] = args.zc[i];
+                zry[q] = args.labels[i];
+            }
+        }
+        if constexpr (ZB) zcol[q] = n0 + (((chunk % 32) ^ (((chunk / 32) & 3) << 2)) << 3);
+    }
     // k-contiguous operands: one descriptor per workgroup over the tile's rows (exact extent)
     const int bytes_ta = KA ? (int)(((int64_t)(min(LB, M - m0) - 1) * lda + K) * 2) : 0;
     const int bytes_tb = KB ? (int)(((int64_t)(min(LB, Nn - n0) - 1) * ldb + K) * 2) : 0;
@@ -990,12 +825,30 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
             return __builtin_amdgcn_raw_buffer_load_b128(make_desc(tl.ba, tl.bytes_a), vo, 0, 0);
         }
         const int r = q - CPO;
+        if constexpr (ZB) {   // the row of this copy: its c and its label's offset from the chunk's columns
+            const int k = tl.k0 + kc_b[r];
+            const bool kin = k < ke;
+            const int kcl = kin ? k : K - 1;
+            zrc[r] = kin ? args.zc[kcl] : INFINITY;
+            zry[r] = kin ? args.labels[kcl] - zcol[r] : -1;
+        }
         const int vo = !KB ? voff_b[r] : ((ok_b[r] && tl.k0 + kc_b[r] < ke) ? voff_b[r] + tl.k0 * 2 : kOob);
         return __builtin_amdgcn_raw_buffer_load_b128(make_desc(tl.bb, tl.bytes_b), vo, 0, 0);
     };
-    auto write_one = [&](int stage, int q, const u32x4_t& v) {
+    // k0w: the first k of the tile whose copy v holds
+    auto write_one = [&](int stage, int q, const u32x4_t& v, int k0w) {
         char* base = reinterpret_cast<char*>(&lds[stage][q / CPO][0]);
-        *reinterpret_cast<u32x4_t*>(base + (wave * CPO + q % CPO) * 1024 + l * 16) = v;
+        u32x4_t x = v;
+        if constexpr (ZA) {
+            if (q < CPO) {
+                const int j0 = k0w + kc_a[q];
+                x = z_chunk_to_r(v, zrc[q], zry[q] - j0, ok_a[q] && j0 < ke);
+            }
+        }
+        if constexpr (ZB) {
+            if (q >= CPO) x = z_chunk_to_r(v, zrc[q - CPO], zry[q - CPO], true);
+        }
+        *reinterpret_cast<u32x4_t*>(base + (wave * CPO + q % CPO) * 1024 + l * 16) = x;
     };
 
     // fragments for MFMA step s (k = 16 s .. +15) of `cnt` 32-wide blocks from tile row/column `base`:
@@ -1050,7 +903,7 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
                 __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[m / NJ], b[m % NJ], acc[m / NJ][m % NJ], 0, 0, 0);
             if (q0 >= 0 && m < CPS) {
                 __builtin_amdgcn_sched_barrier(0);
-                write_one(ws, q0 + m, rg[q0 + m]);
+                write_one(ws, q0 + m, rg[q0 + m], tl.k0 - KT);
                 rg[q0 + m] = load_one(tl, q0 + m);
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -1075,7 +928,7 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
 #pragma unroll
         for (int q = 0; q < 2 * CPO; ++q) rg[q] = load_one(t0, q);
 #pragma unroll
-        for (int q = 0; q < 2 * CPO; ++q) write_one(0, q, rg[q]);
+        for (int q = 0; q < 2 * CPO; ++q) write_one(0, q, rg[q], t0.k0);
 #pragma unroll
         for (int q = 0; q < 2 * CPO; ++q) rg[q] = load_one(t1, q);
     }
@@ -1146,11 +999,11 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
     }
 }
 
-template <bool IS_DW, typename TO, int NW>
+template <bool IS_DW, typename TO, int NW, bool ZR = false>
 __global__ __launch_bounds__(NW * 64, 1) void lds256w_kernel(WideArgs a) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    wide_tile<IS_DW ? kWideDW : kWideDH, TO, NW>(a, blockIdx.x, lds, rv_s);
+    wide_tile<IS_DW ? kWideDW : kWideDH, TO, NW, ZR>(a, blockIdx.x, lds, rv_s);
 }
 
 // The head forward Z = H W (+ b) in bf16 on the same tiles (fp32 accumulation, one rounding of Z).
@@ -1165,12 +1018,12 @@ __global__ __launch_bounds__(NW * 64, 1) void lds256w_fwd_kernel(WideArgs a) {
 // tiles, so that the shorter dW tiles fill the compute units that dH's last round leaves idle instead of
 // a second launch starting after a partly empty round. nh is a multiple of 8, so each part keeps its
 // own XCD order.
-template <typename TO, int NW>
+template <typename TO, int NW, bool ZR = false>
 __global__ __launch_bounds__(NW * 64, 1) void lds256w_pair_kernel(WideArgs h, WideArgs w, int nh) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    if ((int)blockIdx.x < nh) wide_tile<kWideDH, TO, NW>(h, blockIdx.x, lds, rv_s);
-    else wide_tile<kWideDW, float, NW>(w, (int)blockIdx.x - nh, lds, rv_s);
+    if ((int)blockIdx.x < nh) wide_tile<kWideDH, TO, NW, ZR>(h, blockIdx.x, lds, rv_s);
+    else wide_tile<kWideDW, float, NW, ZR>(w, (int)blockIdx.x - nh, lds, rv_s);
 }
 
 // Split-K reduction for the rank-1 form over the rectangle [pm0, M) x [pn0, Nn) of the output, in split
@@ -1319,6 +1172,7 @@ struct FusedArgs {
     void* dH; int64_t lddh; int dh_bf16;
     float* db;
     int tw_n, tw, th_n;   // dW tiles along V, dW tile count, dH tiles along d
+    const float* row_lse; // logits input: R is formed from Z (the R argument) and lse; null: R is stored
 };
 
 // element offset of (row, col) in a 64 x 64 bf16 LDS tile whose 16-byte chunks are swizzled by row
@@ -1372,9 +1226,26 @@ __device__ __forceinline__ void fused_tile(const FusedArgs& a, int id, uint16_t 
         u32x4_t c[4];
         int lab[2];     // dW: labels of the two H rows (rows past N: ignore_index)
         float4 q[2];    // dH: q_hat over the chunk's 8 k
+        float zl[2];    // dW with logits input: lse of the two R rows
+        int kt;
     };
+    const bool zin = a.row_lse != nullptr;
+    // dH with logits input: c and label of this thread's two R rows (fixed over k)
+    float zc_h[2] = {INFINITY, INFINITY};
+    int zy_h[2] = {-1, -1};
+    if (!is_dw && zin) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int i = m0 + r0 + 32 * e;
+            if (i < a.N) {
+                zc_h[e] = z_row_c(a.row_lse, a.labels, i, a.V, a.ig);
+                zy_h[e] = a.labels[i];
+            }
+        }
+    }
     auto load_set = [&](Set& st, int kt) {
         const int k0 = kt * FK;
+        st.kt = kt;
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
             st.c[e] = __builtin_amdgcn_raw_buffer_load_b128(da, off_a(k0, e), 0, 0);
@@ -1385,6 +1256,7 @@ __device__ __forceinline__ void fused_tile(const FusedArgs& a, int id, uint16_t 
             for (int e = 0; e < 2; ++e) {
                 const int k = k0 + r0 + 32 * e;
                 st.lab[e] = a.labels[k < a.N ? k : a.N - 1];
+                if (zin) st.zl[e] = a.row_lse[k < a.N ? k : a.N - 1];
                 if (k >= a.N) st.lab[e] = a.ig;
             }
         } else {
@@ -1403,8 +1275,20 @@ __device__ __forceinline__ void fused_tile(const FusedArgs& a, int id, uint16_t 
         for (int e = 0; e < 2; ++e) {
             const int r = r0 + 32 * e;
             const int o = r * FB + ((lc ^ (r & 7)) << 3);
-            *reinterpret_cast<u32x4_t*>(&sa[buf][o]) = st.c[e];
-            *reinterpret_cast<u32x4_t*>(&sb[buf][o]) = st.c[2 + e];
+            u32x4_t ca = st.c[e], cb = st.c[2 + e];
+            if (zin) {
+                if constexpr (is_dw) {   // R is operand B: row k0 + r, columns n0 + 8 lc
+                    bool bad = false;
+                    const bool valid = label_valid(st.lab[e], a.V, a.ig, &bad);
+                    const int n = n0 + lc * 8;
+                    cb = z_chunk_to_r(cb, valid ? st.zl[e] * kLog2e : INFINITY, st.lab[e] - n, n < a.V);
+                } else {                 // R is operand A: row m0 + r, k chunk kt FK + 8 lc
+                    const int k = st.kt * FK + lc * 8;
+                    ca = z_chunk_to_r(ca, zc_h[e], zy_h[e] - k, k < a.V);
+                }
+            }
+            *reinterpret_cast<u32x4_t*>(&sa[buf][o]) = ca;
+            *reinterpret_cast<u32x4_t*>(&sb[buf][o]) = cb;
         }
         if constexpr (is_dw) {
 #pragma unroll
@@ -1534,11 +1418,11 @@ __global__ __launch_bounds__(256, 2) void vjp_fused_small_kernel(FusedArgs a) {
 constexpr int kCUs = 256;        // MI355X compute units
 constexpr int kMaxSplits = 8;
 
-enum GemmKind { kSimt = 0, kMfma128 = 1, kRank1 = 3 };
+// kRank1: the 256-tile rank-1 form on the 64-deep kernel (lds256w_kernel)
+enum GemmKind { kSimt = 0, kMfma128 = 1, kRank1 = 4 };
 struct GemmPlan {
     int kind, splits;
-    int wide = 0;   // rank-1 kind: k tiles of 64 in two stages (lds256w_kernel)
-    // wide rank-1 kind: outer tiles [0, outer_dp) run with the whole k range, the rest with `splits`
+    // rank-1 kind: outer tiles [0, outer_dp) run with the whole k range, the rest with `splits`
     int outer_dp = 0;
 };
 struct Plan {
@@ -1582,12 +1466,11 @@ GemmPlan plan_wide(int64_t M, int64_t N, int64_t K, bool inner_is_m) {
     constexpr int64_t kXcd = 8, kCuPerXcd = kCUs / 8;
     const int64_t MT = cdiv(M, LB), NT = cdiv(N, LB);
     const int64_t inner = inner_is_m ? MT : NT, outer = inner_is_m ? NT : MT;
-    const int64_t nk = cdiv(K, 2 * LK);
+    const int64_t nk = cdiv(K, WKT);
     auto rounds = [&](int64_t pairs) { return cdiv(cdiv(pairs, kXcd) * inner, kCuPerXcd); };
     const int64_t per_round = kXcd * std::max<int64_t>(1, kCuPerXcd / inner);   // outer tiles per whole round
     const int64_t full = (outer / per_round) * per_round;
     GemmPlan best{kRank1, 1};
-    best.wide = 1;
     best.outer_dp = (int)outer;
     double best_t = (double)rounds(outer) * nk * kTileStep;
     for (int64_t dp : {(int64_t)0, full}) {
@@ -1615,7 +1498,7 @@ GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K, bool
     // large products: 256-tile rank-1 kernel; small ones (a few dozen 256 tiles or a short k) are
     // latency bound and run faster on the 128-tile kernel, which needs no rank-1 pre-pass
     const int64_t t256 = cdiv(M, LB) * cdiv(N, LB);
-    if (t256 >= 24 && K >= 8 * LK) return plan_wide(M, N, K, inner_is_m);
+    if (t256 >= 24 && K >= 4 * WKT) return plan_wide(M, N, K, inner_is_m);
     // 128 tiles: split k so that every workgroup loads its whole k range at once, when that takes
     // at most kMaxSplits splits
     const int64_t t128 = cdiv(M, MB) * cdiv(N, MB);
@@ -1626,8 +1509,7 @@ GemmPlan plan_gemm(bool mfma, bool big_ok, int64_t M, int64_t N, int64_t K, bool
 
 // Plan override for A/B measurement (environment BOM_VJP_PLAN = "kind_w,splits_w,kind_h,splits_h",
 // read once; 0 keeps the automatic choice (small products: the fused launch); kinds 1 = 128-tile
-// MFMA (and no fused launch), 3 = 256-tile rank-1 kernel with 32-deep k tiles in four stages,
-// 4 = the same with 64-deep k tiles in two stages).
+// MFMA (and no fused launch), 4 = 256-tile rank-1 kernel; splits > 0 force that k split on every tile).
 struct PlanOverride {
     int kw = 0, sw = 0, kh = 0, sh = 0;
 };
@@ -1663,19 +1545,14 @@ const WaveCfg& wave_cfg() {
 
 void apply_override(GemmPlan& g, int kind, int splits, int64_t M, int64_t N, int64_t K) {
     if (g.kind == kSimt) return;
-    if (kind == kMfma128) g.kind = kMfma128;
-    if (kind == kRank1) {
-        g.kind = kRank1;
-        g.wide = 0;
+    if (kind == kMfma128) {
+        g.kind = kMfma128;
+        g.outer_dp = 0;
     }
-    if (kind == 4) {
-        g.kind = kRank1;
-        g.wide = 1;
-    }
-    if (kind == kRank1 || kind == kMfma128) g.outer_dp = 0;
+    if (kind == kRank1) g.kind = kRank1;
 
     if (splits > 0) {
-        const int ktile = g.kind == kRank1 ? LK * (1 + g.wide) : MK;
+        const int ktile = g.kind == kRank1 ? WKT : MK;
         // every split keeps at least one k tile
         g.splits = (int)(splits < cdiv(K, ktile) ? splits : cdiv(K, ktile));
         g.outer_dp = 0;   // a forced split applies to every tile
@@ -1712,7 +1589,7 @@ void plan_pair(Plan& p, int64_t N, int64_t d, int64_t V) {
     constexpr double kStep = 1.8e-6, kBw = 5e12;
     const int64_t inner = cdiv(d, LB);
     const int64_t ow = cdiv(V, LB), oh = cdiv(N, LB);
-    const int64_t nkw = cdiv(N, 2 * LK), nkh = cdiv(V, 2 * LK);
+    const int64_t nkw = cdiv(N, WKT), nkh = cdiv(V, WKT);
     auto red = [&](int s, int64_t rect) { return s > 1 ? (2.0 * s + 2.0) * 4.0 * (double)rect / kBw / kStep : 0.0; };
     // separate launches as planned (each split launch followed by its reduction)
     auto sep = [&](const GemmPlan& g, int64_t outer, int64_t nk, int64_t rect_per_outer) {
@@ -1754,8 +1631,7 @@ Plan make_plan_uncached(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     const PlanOverride& o = plan_override();
     apply_override(p.w, o.kw, o.sw, d, V, N);
     apply_override(p.h, o.kh, o.sh, N, d, V);
-    if (o.kw == 0 && o.kh == 0 && o.sw == 0 && o.sh == 0 && p.w.kind == kRank1 && p.w.wide && p.h.kind == kRank1 &&
-        p.h.wide)
+    if (o.kw == 0 && o.kh == 0 && o.sw == 0 && o.sh == 0 && p.w.kind == kRank1 && p.h.kind == kRank1)
         plan_pair(p, N, d, V);
     return p;
 }
@@ -1776,6 +1652,27 @@ Plan make_plan(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     return p;
 }
 
+// Plan of the SIMT kernels, which run bf16 operands that the MFMA kernels cannot stage (a leading
+// dimension that is not a multiple of 8, or a base that is not 16-byte aligned): SIMT tiles with their own
+// k split over every tile.
+Plan simt_plan(int64_t N, int64_t d, int64_t V) {
+    Plan p;
+    p.w = plan_gemm(false, false, d, V, N, true);
+    p.h = plan_gemm(false, false, N, d, V, false);
+    return p;
+}
+
+// Bytes of fp32 split-K partials a plan writes: the rectangle of the tiles that split k (all of them
+// unless the wide kernel runs outer tiles [0, outer_dp) unsplit); dW and dH share the buffer.
+size_t partial_bytes(const Plan& p, int64_t N, int64_t d, int64_t V) {
+    const int64_t wcols = std::max<int64_t>(0, V - (int64_t)p.w.outer_dp * LB);
+    const int64_t hrows = std::max<int64_t>(0, N - (int64_t)p.h.outer_dp * LB);
+    const bool ww = p.w.kind == kRank1, hw = p.h.kind == kRank1;
+    const size_t pw = p.w.splits > 1 ? (size_t)p.w.splits * d * (ww ? wcols : V) * 4 : 0;
+    const size_t ph = p.h.splits > 1 ? (size_t)p.h.splits * (hw ? hrows : N) * d * 4 : 0;
+    return std::max(pw, ph);
+}
+
 VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     const Plan p = make_plan(N, d, V, dt);
     VjpWs w;
@@ -1784,16 +1681,15 @@ VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     w.vmask_off = align256(w.cqp_off + (size_t)V * 4);
     w.scal_off = align256(w.vmask_off + (size_t)N * 4);
     const bool r1 = p.w.kind == kRank1 || p.h.kind == kRank1;
-    w.hpart_off = align256(w.scal_off + 16);
+    w.zc_off = align256(w.scal_off + 16);
+    w.hpart_off = align256(w.zc_off + (size_t)N * 4);
     w.hsum_off = align256(w.hpart_off + (r1 ? (size_t)cdiv(N, kHsRows) * d * 4 : 0));
     w.u_off = align256(w.hsum_off + (r1 ? (size_t)d * 4 : 0));
     w.part_off = align256(w.u_off + (r1 ? (size_t)d * 4 : 0));
-    // split partials: the rectangle of the tiles that split k (all of them unless outer_dp > 0)
-    const int64_t wcols = std::max<int64_t>(0, V - (int64_t)p.w.outer_dp * LB);
-    const int64_t hrows = std::max<int64_t>(0, N - (int64_t)p.h.outer_dp * LB);
-    size_t pw = p.w.splits > 1 ? (size_t)p.w.splits * d * (p.w.kind == kRank1 && p.w.wide ? wcols : V) * 4 : 0;
-    size_t ph = p.h.splits > 1 ? (size_t)p.h.splits * (p.h.kind == kRank1 && p.h.wide ? hrows : N) * d * 4 : 0;
-    w.total = align256(w.part_off + (pw > ph ? pw : ph));
+    size_t need = partial_bytes(p, N, d, V);
+    // the same call may take the SIMT plan (misaligned operands)
+    if (dt == BOM_BF16) need = std::max(need, partial_bytes(simt_plan(N, d, V), N, d, V));
+    w.total = align256(w.part_off + need);
     return w;
 }
 
@@ -1804,22 +1700,26 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
     const int splits = g.splits;
     if (g.kind == kRank1) {
         // rank-1 form: out = alpha A B + rv cv^T (+ beta out)
-        const int kt = g.wide ? 2 * LK : LK;
+        const int kt = WKT;
         const int kps = (int)(cdiv(cdiv(K, splits), kt) * kt);
         const int MT = (int)cdiv(M, LB), NT = (int)cdiv(Nn, LB);
         const int inner = is_dw ? MT : NT, outer = is_dw ? NT : MT;
-        dim3 grid((unsigned)(cdiv(outer, 8) * 8 * inner), 1, splits);
         float* pz = splits > 1 ? part : nullptr;
         const uint16_t* a16 = static_cast<const uint16_t*>(A);
         const uint16_t* b16 = static_cast<const uint16_t*>(B);
-        if (g.wide) {
+        {
             // whole rounds over the full k range, then the leftover outer tiles with split k
             const int dp = std::min(g.outer_dp, outer);
             auto launch = [&](int ob, int oe, int nsplit, int kp, float* pp, const TileRange& tr) {
                 dim3 gr((unsigned)(cdiv((int64_t)(oe - ob) * nsplit, 8) * 8 * inner));
-                const WideArgs wa{a16, lda, b16, ldb, M, Nn, K, kp, tr, f.scal, rv, cv, out, ldo, beta, pp, nullptr};
+                const WideArgs wa{a16, lda, b16, ldb, M, Nn, K, kp, tr, f.scal, rv, cv, out, ldo, beta, pp, nullptr,
+                                  f.zc, f.labels};
                 const int nw = is_dw ? wave_cfg().dw : wave_cfg().dh;
-                if (is_dw && nw == 8)
+                if (f.zc != nullptr && is_dw)   // logits input: eight waves
+                    hipLaunchKernelGGL((lds256w_kernel<true, float, 8, true>), gr, dim3(512), 0, st, wa);
+                else if (f.zc != nullptr)
+                    hipLaunchKernelGGL((lds256w_kernel<false, TO, 8, true>), gr, dim3(512), 0, st, wa);
+                else if (is_dw && nw == 8)
                     hipLaunchKernelGGL((lds256w_kernel<true, float, 8>), gr, dim3(512), 0, st, wa);
                 else if (is_dw)
                     hipLaunchKernelGGL((lds256w_kernel<true, float, 4>), gr, dim3(256), 0, st, wa);
@@ -1845,18 +1745,6 @@ hipError_t run_gemm(bool is_dw, const GemmPlan& g, const void* A, int64_t lda, c
                                Nn, pm0, pn0, rv, cv, out, ldo, beta);
             return hipGetLastError();
         }
-        if (is_dw)
-            hipLaunchKernelGGL((lds256_kernel<true, float>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
-                               inner, outer, f.scal, rv, cv, reinterpret_cast<float*>(out), ldo, beta, pz);
-        else
-            hipLaunchKernelGGL((lds256_kernel<false, TO>), grid, dim3(256), 0, st, a16, lda, b16, ldb, M, Nn, K, kps,
-                               inner, outer, f.scal, rv, cv, out, ldo, beta, pz);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess || splits == 1) return e;
-        const int64_t MN = (int64_t)M * Nn;
-        hipLaunchKernelGGL(splitk_rank1_kernel<TO>, dim3((unsigned)cdiv(MN, 256)), dim3(256), 0, st, part, splits, M, Nn,
-                           0, 0, rv, cv, out, ldo, beta);
-        return hipGetLastError();
     }
     const int tb = g.kind == kMfma128 ? MB : SB;
     const int ktile = g.kind == kMfma128 ? MK : SK;
@@ -1962,15 +1850,17 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
     float* hsum = reinterpret_cast<float*>(base + L.hsum_off);
     float* u = reinterpret_cast<float*>(base + L.u_off);
     float* part = reinterpret_cast<float*>(base + L.part_off);
+    float* zc = reinterpret_cast<float*>(base + L.zc_off);
+    const bool zin = !a.is_residual;   // the R argument holds the logits Z
 
     // MFMA kernels stage 16-byte rows: leading dimensions multiples of 8 and 16-byte bases;
     // otherwise the SIMT kernels (same plan shape, SIMT tiles) run.
     auto al = [](const void* ptr, int64_t ld) { return reinterpret_cast<uintptr_t>(ptr) % 16 == 0 && ld % 8 == 0; };
     if (a.dt == BOM_BF16 && !(al(a.H, a.ldh) && al(a.W, a.ldw) && al(a.R, a.ldr))) {
-        // same split factors (the workspace holds their partials), SIMT tiles
-        p.w.kind = kSimt;
-        p.h.kind = kSimt;
+        // SIMT tiles with their own k splits over every tile (the workspace covers their partials too)
+        p = simt_plan(a.N, a.d, a.V);
     }
+    if (L.part_off + partial_bytes(p, a.N, a.d, a.V) > L.total) return hipErrorInvalidValue;   // never taken
     if (!a.dH) p.h.kind = kSimt;   // no dH: no rank-1 vector for it
 
     // small products (both on the 128-tile kernel): one fused launch, nothing staged beforehand
@@ -2007,6 +1897,7 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
         fa.tw_n = (int)cdiv(a.V, FB);
         fa.tw = (int)cdiv(a.d, FB) * fa.tw_n;
         fa.th_n = (int)cdiv(a.d, FB);
+        fa.row_lse = zin ? a.row_lse : nullptr;
         const int th = a.dH ? (int)cdiv(a.N, FB) * fa.th_n : 0;
         hipLaunchKernelGGL(vjp_fused_small_kernel, dim3((unsigned)(fa.tw + th)), dim3(256), 0, st, fa);
         return hipGetLastError();
@@ -2029,42 +1920,47 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
     if (nprep < a.d) nprep = a.d;
     hipLaunchKernelGGL(vjp_prep_kernel, dim3((nprep + 255) / 256), dim3(256), 0, st, a.q_hat, a.s, a.n_valid, a.lambda,
                        a.V, a.N, a.labels, a.ignore_index, cq, cqp, vmask, scal, static_cast<float*>(a.db),
-                       rw ? hpart : nullptr, nrb, a.d,
-                       hsum);
+                       rw ? hpart : nullptr, nrb, a.d, hsum, zin ? a.row_lse : nullptr, zc);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const Fold f{cq, vmask, scal, cqp};
+    const Fold f{cq, vmask, scal, cqp, zin ? zc : nullptr, a.labels};
 
     if (p.pair && a.dH && p.w.kind == kRank1 && p.h.kind == kRank1) {
         // one grid: dH's units (k split p.h.splits) first, then dW's tiles over the full k range
         const int inner = (int)cdiv(a.d, LB);
         const int oh = (int)cdiv(a.N, LB), ow = (int)cdiv(a.V, LB);
         const int sh = p.h.splits;
-        const int kps_h = (int)(cdiv(cdiv(a.V, sh), 2 * LK) * 2 * LK);
-        const int kps_w = (int)(cdiv(a.N, 2 * LK) * 2 * LK);
+        const int kps_h = (int)(cdiv(cdiv(a.V, sh), WKT) * WKT);
+        const int kps_w = (int)(cdiv(a.N, WKT) * WKT);
         const uint16_t* H16 = static_cast<const uint16_t*>(a.H);
         const uint16_t* R16 = static_cast<const uint16_t*>(a.R);
         const uint16_t* W16 = static_cast<const uint16_t*>(a.W);
         const TileRange trh{inner, 0, oh, sh, 0, 0, a.d, (int64_t)a.N * a.d};
         const TileRange trw{inner, 0, ow, 1, 0, 0, 0, 0};
         const WideArgs wh{R16, a.ldr, W16, a.ldw, a.N, a.d, a.V, kps_h, trh, f.scal, vmask, u, a.dH, a.lddh, 0.f,
-                          sh > 1 ? part : nullptr, nullptr};
+                          sh > 1 ? part : nullptr, nullptr, f.zc, a.labels};
         const WideArgs ww{H16, a.ldh, R16, a.ldr, a.d, a.V, a.N, kps_w, trw, f.scal, hsum, cq, a.dW, a.lddw,
-                          a.dW_beta, nullptr, nullptr};
+                          a.dW_beta, nullptr, nullptr, f.zc, a.labels};
         const int nh = (int)(cdiv((int64_t)oh * sh, 8) * 8 * inner);
         const int nw = (int)(cdiv(ow, 8) * 8 * inner);
-        if (a.dh_dt == BOM_BF16)
-            if (wave_cfg().pair == 8)
-                hipLaunchKernelGGL((lds256w_pair_kernel<uint16_t, 8>), dim3((unsigned)(nh + nw)), dim3(512), 0, st, wh, ww,
-                                   nh);
+        const dim3 grid((unsigned)(nh + nw));
+        const bool w8 = wave_cfg().pair == 8;
+        if (zin) {   // logits input: eight waves
+            if (a.dh_dt == BOM_BF16)
+                hipLaunchKernelGGL((lds256w_pair_kernel<uint16_t, 8, true>), grid, dim3(512), 0, st, wh, ww, nh);
             else
-                hipLaunchKernelGGL((lds256w_pair_kernel<uint16_t, 4>), dim3((unsigned)(nh + nw)), dim3(256), 0, st, wh, ww,
-                                   nh);
-        else
-            if (wave_cfg().pair == 8)
-                hipLaunchKernelGGL((lds256w_pair_kernel<float, 8>), dim3((unsigned)(nh + nw)), dim3(512), 0, st, wh, ww, nh);
+                hipLaunchKernelGGL((lds256w_pair_kernel<float, 8, true>), grid, dim3(512), 0, st, wh, ww, nh);
+        } else if (a.dh_dt == BOM_BF16) {
+            if (w8)
+                hipLaunchKernelGGL((lds256w_pair_kernel<uint16_t, 8>), grid, dim3(512), 0, st, wh, ww, nh);
             else
-                hipLaunchKernelGGL((lds256w_pair_kernel<float, 4>), dim3((unsigned)(nh + nw)), dim3(256), 0, st, wh, ww, nh);
+                hipLaunchKernelGGL((lds256w_pair_kernel<uint16_t, 4>), grid, dim3(256), 0, st, wh, ww, nh);
+        } else {
+            if (w8)
+                hipLaunchKernelGGL((lds256w_pair_kernel<float, 8>), grid, dim3(512), 0, st, wh, ww, nh);
+            else
+                hipLaunchKernelGGL((lds256w_pair_kernel<float, 4>), grid, dim3(256), 0, st, wh, ww, nh);
+        }
         if ((e = hipGetLastError()) != hipSuccess || sh == 1) return e;
         const int64_t MN = (int64_t)a.N * a.d;
         if (a.dh_dt == BOM_BF16)

@@ -26,7 +26,9 @@ hipError_t launch_ema(float* q, const float* s, int64_t V, float beta1, float in
 struct HeadVjpArgs {
     const void* H; int64_t ldh;
     const void* W; int64_t ldw;
-    const void* R; int64_t ldr;
+    const void* R; int64_t ldr;       // residual rows R, or the logits Z when is_residual == 0
+    int is_residual;
+    const float* row_lse;             // [N], read when is_residual == 0
     bom_dtype dt;
     int N, d, V;
     const int32_t* labels; int32_t ignore_index;

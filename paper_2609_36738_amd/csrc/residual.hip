@@ -502,11 +502,13 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
 // columns [q W, min(V, (q + 1) W)), and together stream Z once. Each part parks its slice in LDS
 // like residual_rows_lds_kernel, reduces its (max, sum of exp(z - max), first argmax) and publishes
 // them as three 64-bit words (validity marker in the high half, value in the low half; the area is
-// zeroed before the launch) with relaxed device-scope atomic stores; thread 0 then polls the other
-// parts' words with relaxed device-scope atomic loads and combines all S records in part order, so
-// every part derives the same lse. A poll is bounded: after spin_limit polls (or at once when
-// spin_limit < 0) thread 0 computes the missing part's record from Z itself and stops waiting for
-// that part, so the kernel finishes whatever the scheduling. The part holding a row's label (part 0
+// zeroed before the launch) with relaxed device-scope atomic stores; lane q of wave 0 then polls part
+// q's words with relaxed device-scope atomic loads, and every thread combines all S records in part
+// order, so every part derives the same lse. A poll is bounded: after spin_limit polls (or at once when
+// spin_limit < 0) the whole workgroup reduces the missing part's slice from Z itself with the same code
+// and operation order that part runs (so the record has the same bits as the one it would have
+// published) and stops waiting for that part, so the kernel finishes whatever the scheduling and its
+// results do not depend on it; the flags word then carries BOM_FLAG_RESIDUAL_RECOMPUTED. The part holding a row's label (part 0
 // for ignored rows) writes that row's outputs and loss term. Workgroup (g, q) writes columns of
 // partial row g; the S parts of group g together fill it. Its logit loads and residual stores carry the
 // non-temporal hint (128 K vocabulary: 1.80 -> 1.73 ms; the row-parked kernel of narrower rows ran 5 %
@@ -524,7 +526,11 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
     __shared__ float sh_l[2][NW];
     __shared__ int sh_am;
     __shared__ float sh_zt[2];
-    __shared__ float sh_row[3];   // combined max, sum and (as bits) argmax of the current row
+    __shared__ float sh_rec_m[kSplitMaxParts], sh_rec_l[kSplitMaxParts];   // the row's per-part records
+    __shared__ int sh_rec_a[kSplitMaxParts];
+    __shared__ int sh_miss;   // parts whose record did not arrive (bit q)
+    __shared__ float sh_fm[NW], sh_fl[NW];   // reduction of a partner's slice
+    __shared__ int sh_fam;
     const int tid = threadIdx.x;
     const int part = blockIdx.x % S, g = blockIdx.x / S, G = gridDim.x / S;
     const int c0 = part * W;
@@ -538,6 +544,7 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
     double ce = 0.0;
     bool bad = false;
     bool dead = false;   // wave 0, lane q: part q is no longer waited for
+    bool recomputed = false;   // some partner record was recomputed from Z (reported in the flags word)
     auto unpack = [](const uint4& u, float* x) {
         x[0] = bf16_lo(u.x); x[1] = bf16_hi(u.x); x[2] = bf16_lo(u.y); x[3] = bf16_hi(u.y);
         x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z); x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
@@ -571,49 +578,106 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
             for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(d1, c);
         }
     }
-    if (tid == 0) sh_am = INT_MAX;
+    if (tid == 0) {
+        sh_am = INT_MAX;
+        sh_fam = INT_MAX;
+    }
     constexpr unsigned long long kValid = 1ull << 32;
     auto xword = [&](int i, int q, int f) { return ws.xch + ((int64_t)i * kSplitMaxParts + q) * 3 + f; };
-    // wave 0, lane q: part q's record of row i, from its words or, failing that, from Z
+    // wave 0, lane q: part q's record of row i from its words; false when the poll bound runs out (from
+    // then on part q is not waited for) or when spin_limit < 0
     auto fetch = [&](int i, int q, float* mq, float* lq, int* aq) {
-        if (!dead) {
-            unsigned long long v[3];
-            bool ok = true;
-            for (int f = 0; f < 3 && ok; ++f) {
-                ok = false;
-                for (int it = 0; spin_limit >= 0 && it <= spin_limit; ++it) {
-                    v[f] = __hip_atomic_load(xword(i, q, f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if ((v[f] >> 32) == 1) {
-                        ok = true;
-                        break;
-                    }
-                    __builtin_amdgcn_s_sleep(2);
+        if (dead) return false;
+        unsigned long long v[3];
+        bool ok = true;
+        for (int f = 0; f < 3 && ok; ++f) {
+            ok = false;
+            for (int it = 0; spin_limit >= 0 && it <= spin_limit; ++it) {
+                v[f] = __hip_atomic_load(xword(i, q, f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if ((v[f] >> 32) == 1) {
+                    ok = true;
+                    break;
                 }
+                __builtin_amdgcn_s_sleep(2);
             }
-            if (ok) {
-                *mq = __uint_as_float((uint32_t)v[0]);
-                *lq = __uint_as_float((uint32_t)v[1]);
-                *aq = (int)(uint32_t)v[2];
-                return;
-            }
+        }
+        if (!ok) {
             dead = true;
+            return false;
         }
-        const int q0 = q * W, q1 = min(V, q0 + W);
-        const uint16_t* zr = Z + (int64_t)i * ldz;
+        *mq = __uint_as_float((uint32_t)v[0]);
+        *lq = __uint_as_float((uint32_t)v[1]);
+        *aq = (int)(uint32_t)v[2];
+        return true;
+    };
+    // The reduction of one part's slice, shared by a part's own pass and by the recomputation of a
+    // partner's record when that record does not arrive: the same operations in the same order give the
+    // partner's bits exactly (contraction off, explicit fma only), so every part derives the same lse
+    // whichever way it obtained a record. chunk_at(c) is this thread's chunk c, with columns past the
+    // slice's end read as -inf.
+    auto thread_stats = [&](auto&& chunk_at, float* m_out, float* l_out, int* cmax_out) {
+#pragma clang fp contract(off)
         float m = -INFINITY, l = 0.f;
-        int a = q0;
-        for (int col = q0; col < q1; ++col) {
-            const float x = bf16_to_f32(zr[col]);
-            if (x > m) {
-                l = (m == -INFINITY) ? 0.f : l * exp2_fast((m - x) * kLog2e);
-                m = x;
-                a = col;
-            }
-            l += exp2_fast((x - m) * kLog2e);
+        int cmax = 0;
+        uint4 u_next = chunk_at(0);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const uint4 u = u_next;
+            if (c + 1 < NCH) u_next = chunk_at(c + 1);
+            float x[VEC];
+            unpack(u, x);
+            auto mx = [](float a, float b2) { return __builtin_elementwise_maximum(a, b2); };
+            const float cm = mx(mx(mx(x[0], x[1]), mx(x[2], x[3])), mx(mx(x[4], x[5]), mx(x[6], x[7])));
+            const float mn = mx(m, cm);
+            const float mn2 = mn * kLog2e;
+            float e[VEC];
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) e[k] = exp2_fast(fmaf(x[k], kLog2e, -mn2));
+            const float cl = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+            l = (c == 0 ? cl : fmaf(l, exp2_fast((m - mn) * kLog2e), cl));
+            if (c > 0 && cm > m) cmax = c;
+            m = mn;
         }
-        *mq = m;
-        *lq = l;
-        *aq = a;
+        *m_out = m;
+        *l_out = l;
+        *cmax_out = cmax;
+    };
+    // wave reduction of (m, l) into shm[wave], shl[wave] (the caller then passes a barrier)
+    auto wave_stats = [&](float m, float l, float* shm, float* shl) {
+#pragma clang fp contract(off)
+        float mw = m;
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o, kWave));
+        float lw = l * exp2_fast((m - mw) * kLog2e);
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) lw += __shfl_xor(lw, o, kWave);
+        if ((tid & (kWave - 1)) == 0) {
+            shm[tid / kWave] = mw;
+            shl[tid / kWave] = lw;
+        }
+    };
+    // the workgroup's (max, sum) from the per-wave values (uniform)
+    auto group_stats = [&](const float* shm, const float* shl, float* mp, float* lp) {
+#pragma clang fp contract(off)
+        const int lane = tid & (kWave - 1);
+        const float mg = lane < NW ? shm[lane] : -INFINITY;
+        float mm = mg;
+#pragma unroll
+        for (int o = NW / 2; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o, kWave));
+        float lg = lane < NW ? shl[lane] * exp2_fast((mg - mm) * kLog2e) : 0.f;
+#pragma unroll
+        for (int o = NW / 2; o > 0; o >>= 1) lg += __shfl_xor(lg, o, kWave);
+        *mp = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(mm)));
+        *lp = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lg)));
+    };
+    // first column of chunk cmax holding the maximum mp (the lowest one over the workgroup, by atomicMin)
+    auto first_max = [&](const uint4& w, int cmax, float mp, int* sh) {
+        float x[VEC];
+        unpack(w, x);
+        int k0 = VEC - 1;
+#pragma unroll
+        for (int k = VEC - 2; k >= 0; --k) k0 = (x[k] == mp) ? k : k0;
+        atomicMin(sh, (cmax * THREADS + tid) * VEC + k0);
     };
     auto finish_row = [&](int i, int b, float lse, bool valid, int am) {
         if (row_argmax) row_argmax[i] = am;
@@ -632,64 +696,17 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
         const int i = row_of(j);
         const int b = j & 1;
         // pass 1 (LDS): online (max, sum) of this part's slice, as in residual_rows_lds_kernel
-        float m = -INFINITY, l = 0.f;
-        int cmax = 0;
-        uint4 u_next = slots[tid];
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const uint4 u = u_next;
-            if (c + 1 < NCH) u_next = slots[(c + 1) * THREADS + tid];
-            float x[VEC];
-            unpack(u, x);
-            auto mx = [](float a, float b2) { return __builtin_elementwise_maximum(a, b2); };
-            const float cm = mx(mx(mx(x[0], x[1]), mx(x[2], x[3])), mx(mx(x[4], x[5]), mx(x[6], x[7])));
-            const float mn = mx(m, cm);
-            const float mn2 = mn * kLog2e;
-            float e[VEC];
-#pragma unroll
-            for (int k = 0; k < VEC; ++k) e[k] = exp2_fast(fmaf(x[k], kLog2e, -mn2));
-            const float cl = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
-            l = (c == 0 ? cl : fmaf(l, exp2_fast((m - mn) * kLog2e), cl));
-            if (c > 0 && cm > m) cmax = c;
-            m = mn;
-        }
-        const float m_thread = m;
-        float mw = m;
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o, kWave));
-        float lw = l * exp2_fast((m - mw) * kLog2e);
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) lw += __shfl_xor(lw, o, kWave);
-        if ((tid & (kWave - 1)) == 0) {
-            sh_m[b][tid / kWave] = mw;
-            sh_l[b][tid / kWave] = lw;
-        }
+        float m_thread, l;
+        int cmax;
+        thread_stats([&](int c) { return slots[c * THREADS + tid]; }, &m_thread, &l, &cmax);
+        wave_stats(m_thread, l, sh_m[b], sh_l[b]);
         __syncthreads();
         if (tid == 0 && j > 0 && prev_own) finish_row(row_of(j - 1), b ^ 1, prev_lse, prev_valid, prev_am);
         float mp, lp;
-        {
-            const int lane = tid & (kWave - 1);
-            const float mg = lane < NW ? sh_m[b][lane] : -INFINITY;
-            float mm = mg;
-#pragma unroll
-            for (int o = NW / 2; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o, kWave));
-            float lg = lane < NW ? sh_l[b][lane] * exp2_fast((mg - mm) * kLog2e) : 0.f;
-#pragma unroll
-            for (int o = NW / 2; o > 0; o >>= 1) lg += __shfl_xor(lg, o, kWave);
-            mp = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(mm)));
-            lp = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lg)));
-        }
-        if (m_thread == mp) {
-            float x[VEC];
-            unpack(slots[cmax * THREADS + tid], x);
-            int k0 = VEC - 1;
-#pragma unroll
-            for (int k = VEC - 2; k >= 0; --k) k0 = (x[k] == mp) ? k : k0;
-            atomicMin(&sh_am, (cmax * THREADS + tid) * VEC + k0);
-        }
+        group_stats(sh_m[b], sh_l[b], &mp, &lp);
+        if (m_thread == mp) first_max(slots[cmax * THREADS + tid], cmax, mp, &sh_am);
         __syncthreads();
-        // wave 0: lane 0 publishes this part's record; lane q < S fetches part q's (all in
-        // parallel); lane 0 combines them in part order
+        // wave 0: lane 0 publishes this part's record; lane q < S fetches part q's (all in parallel)
         if (tid < kWave) {
             const int ap = c0 + sh_am;
             if (tid == 0) {
@@ -703,13 +720,56 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
             }
             float mq = mp, lq = lp;
             int aq = ap;
-            if (tid < S && tid != part) fetch(i, tid, &mq, &lq, &aq);
-            // every part runs the same operations on the same values
-            float M = -INFINITY, L = 0.f;
-            int A = 0;
+            bool have = true;
+            if (tid < S && tid != part) have = fetch(i, tid, &mq, &lq, &aq);
+            if (tid < S) {
+                sh_rec_m[tid] = mq;
+                sh_rec_l[tid] = lq;
+                sh_rec_a[tid] = aq;
+            }
+            const unsigned long long miss = __ballot(tid < S && !have);
+            if (tid == 0) sh_miss = (int)(miss & 0xFFu);
+        }
+        __syncthreads();
+        // records that did not arrive: the whole workgroup reduces that part's slice from Z
+        if (sh_miss != 0) recomputed = true;
+        for (int miss = sh_miss; miss != 0; miss &= miss - 1) {
+            const int q = __builtin_ctz(miss);
+            const int q0 = q * W, nq = min(W, V - q0);
+            const auto dq = make_desc(Z + (int64_t)i * ldz + q0, nq * 2);
+            auto chunk_q = [&](int c) {
+                uint4 w = load_chunk(dq, c);
+                if ((c * THREADS + wave_last) * VEC >= nq) {   // the same padding as park() gives its slots
+                    const bool ok = ((c * THREADS + tid) * VEC) < nq;
+                    const uint32_t mk = lane_mask(ok), fb = 0xFF80FF80u & ~mk;
+                    w = make_uint4((w.x & mk) | fb, (w.y & mk) | fb, (w.z & mk) | fb, (w.w & mk) | fb);
+                }
+                return w;
+            };
+            float mt, lt, mq, lq;
+            int cq;
+            thread_stats(chunk_q, &mt, &lt, &cq);
+            wave_stats(mt, lt, sh_fm, sh_fl);
+            __syncthreads();
+            group_stats(sh_fm, sh_fl, &mq, &lq);
+            if (mt == mq) first_max(chunk_q(cq), cq, mq, &sh_fam);
+            __syncthreads();
+            if (tid == 0) {
+                sh_rec_m[q] = mq;
+                sh_rec_l[q] = lq;
+                sh_rec_a[q] = q0 + sh_fam;
+                sh_fam = INT_MAX;
+            }
+            __syncthreads();
+        }
+        // every thread combines the S records in part order (the same operations in every part)
+        float M = -INFINITY, L = 0.f;
+        int A = 0;
+        {
+#pragma clang fp contract(off)
             for (int q = 0; q < S; ++q) {
-                const float m2 = __shfl(mq, q, kWave), l2 = __shfl(lq, q, kWave);
-                const int a2 = __shfl(aq, q, kWave);
+                const float m2 = sh_rec_m[q], l2 = sh_rec_l[q];
+                const int a2 = sh_rec_a[q];
                 if (q == 0) {
                     M = m2;
                     L = l2;
@@ -722,15 +782,7 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
                     L = fmaf(l2, exp2_fast((m2 - M) * kLog2e), L);
                 }
             }
-            if (tid == 0) {
-                sh_row[0] = M;
-                sh_row[1] = L;
-                sh_row[2] = __int_as_float(A);
-            }
         }
-        __syncthreads();
-        const float M = sh_row[0], L = sh_row[1];
-        const int A = __float_as_int(sh_row[2]);
         const float lse = M + logf(L);
         const int y = labels[i];
         bool rbad = false;
@@ -795,7 +847,7 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
     if (tid == 0) {
         ws.wg_count[blockIdx.x] = cnt;
         ws.wg_loss[blockIdx.x] = ce;
-        ws.wg_flags[blockIdx.x] = bad ? BOM_FLAG_LABEL_RANGE : 0;
+        ws.wg_flags[blockIdx.x] = (bad ? BOM_FLAG_LABEL_RANGE : 0) | (recomputed ? BOM_FLAG_RESIDUAL_RECOMPUTED : 0);
     }
 }
 

@@ -54,16 +54,30 @@ __device__ __forceinline__ void adam_style(float& th, float& v, float up, float 
 }
 
 // ---- dense ----------------------------------------------------------------------------------
-// One 16-byte group per thread, non-temporal loads and stores (each byte is touched once).
+// One launch over [0, P): elements [0, head) and the tail past head + 4 nvec one per thread (threads
+// nvec, nvec + 1, ... of the grid), the body [head, head + 4 nvec) one 16-byte group per thread, with
+// non-temporal loads and stores (each byte is touched once). head makes theta + head, v + head,
+// u + head (and h + head) 16-byte aligned: the arrays share their offset inside a 16-byte group.
 template <bool SPLIT>
 __global__ __launch_bounds__(kUpdThreads) void update_dense_vec4_kernel(float* __restrict__ theta, float* __restrict__ v,
                                                                         const float* __restrict__ u,
-                                                                        const float* __restrict__ h, int64_t nvec,
-                                                                        SegTable segs, UpdateScalars sc) {
+                                                                        const float* __restrict__ h, int64_t head,
+                                                                        int64_t nvec, int64_t P, SegTable segs,
+                                                                        UpdateScalars sc) {
     const int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x;
-    if (q >= nvec) return;
     sc = clipped(sc);
-    const int64_t e = q * 4;
+    if (q >= nvec) {
+        const int64_t r = q - nvec;
+        const int64_t tail0 = head + 4 * nvec;
+        const int64_t e = r < head ? r : tail0 + (r - head);
+        if (e >= P) return;
+        float t = theta[e], vv = v[e];
+        adam_style(t, vv, numerator<SPLIT>(u[e], SPLIT ? h[e] : 0.f, sc), decay_of(e, segs), sc);
+        theta[e] = t;
+        v[e] = vv;
+        return;
+    }
+    const int64_t e = head + q * 4;
     f32x4 t4 = ld_stream(theta + e);
     f32x4 v4 = ld_stream(v + e);
     const f32x4 u4 = ld_stream(u + e);
@@ -101,16 +115,28 @@ __global__ __launch_bounds__(kUpdThreads) void update_dense_scalar_kernel(float*
 // (16 bytes of each array) per thread.
 __device__ __forceinline__ float bf16_at(const u32x4_t& x, int c) { return c & 1 ? bf16_hi(x[c / 2]) : bf16_lo(x[c / 2]); }
 
+// One launch over [0, P) like the fp32 kernel: scalar head and tail, 16-byte groups of 8 in between.
 template <bool SPLIT>
 __global__ __launch_bounds__(kUpdThreads) void update_dense_bf16x8_kernel(uint16_t* __restrict__ theta,
                                                                           uint16_t* __restrict__ v,
                                                                           const uint16_t* __restrict__ u,
-                                                                          const uint16_t* __restrict__ h, int64_t nvec,
-                                                                          SegTable segs, UpdateScalars sc) {
+                                                                          const uint16_t* __restrict__ h, int64_t head,
+                                                                          int64_t nvec, int64_t P, SegTable segs,
+                                                                          UpdateScalars sc) {
     const int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x;
-    if (q >= nvec) return;
     sc = clipped(sc);
-    const int64_t e = q * 8;
+    if (q >= nvec) {
+        const int64_t r = q - nvec;
+        const int64_t tail0 = head + 8 * nvec;
+        const int64_t e = r < head ? r : tail0 + (r - head);
+        if (e >= P) return;
+        float t = bf16_to_f32(theta[e]), vv = bf16_to_f32(v[e]);
+        adam_style(t, vv, numerator<SPLIT>(bf16_to_f32(u[e]), SPLIT ? bf16_to_f32(h[e]) : 0.f, sc), decay_of(e, segs), sc);
+        theta[e] = f32_to_bf16(t);
+        v[e] = f32_to_bf16(vv);
+        return;
+    }
+    const int64_t e = head + q * 8;
     const u32x4_t t8 = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(theta + e));
     const u32x4_t v8 = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(v + e));
     const u32x4_t u8 = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(u + e));
@@ -872,36 +898,47 @@ size_t update_workspace_bytes(int64_t P, const bom_update_cfg* cfg) {
 namespace {
 bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
 
-// The dense kernels over P elements (the clipping factor, if any, already in sc.clip).
+// Elements before the first 16-byte boundary of arrays that share their offset inside a 16-byte group
+// (esz-byte elements, esz-aligned pointers), or -1 when the offsets differ (or a pointer is not esz-aligned).
+int64_t common_head(std::initializer_list<const void*> ptrs, int esz) {
+    int64_t off = -1;
+    for (const void* p : ptrs) {
+        if (p == nullptr) continue;
+        const int64_t o = (int64_t)(reinterpret_cast<uintptr_t>(p) % 16);
+        if (o % esz != 0 || (off >= 0 && o != off)) return -1;
+        off = o;
+    }
+    return off <= 0 ? 0 : (16 - off) / esz;
+}
+
+// The dense kernels over P elements (the clipping factor, if any, already in sc.clip): one launch, with a
+// scalar head up to the arrays' common 16-byte boundary and a scalar tail; arrays with different offsets
+// inside a 16-byte group take the scalar kernel.
 hipError_t dense_range(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
                        const UpdateScalars& sc, hipStream_t st) {
-    const bool aligned = aligned16(theta) && aligned16(v) && aligned16(u) && (h == nullptr || aligned16(h));
-    int64_t done = 0;
-    if (aligned && P >= 4) {
-        const int64_t nvec = P / 4;
-        const int64_t grid = (nvec + kUpdThreads - 1) / kUpdThreads;
+    int64_t head = common_head({theta, v, u, h}, 4);
+    if (head >= 0) {
+        head = std::min(head, P);
+        const int64_t nvec = (P - head) / 4;
+        const int64_t extra = P - 4 * nvec;   // head + tail elements, one thread each
+        const int64_t grid = (nvec + extra + kUpdThreads - 1) / kUpdThreads;
         if (h)
             hipLaunchKernelGGL(update_dense_vec4_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v, u,
-                               h, nvec, segs, sc);
+                               h, head, nvec, P, segs, sc);
         else
             hipLaunchKernelGGL(update_dense_vec4_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
-                               u, h, nvec, segs, sc);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        done = nvec * 4;
-    }
-    if (done < P) {
-        int64_t grid = (P - done + kUpdThreads - 1) / kUpdThreads;
-        if (grid > 8192) grid = 8192;
-        if (h)
-            hipLaunchKernelGGL(update_dense_scalar_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
-                               u, h, done, P, segs, sc);
-        else
-            hipLaunchKernelGGL(update_dense_scalar_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta,
-                               v, u, h, done, P, segs, sc);
+                               u, h, head, nvec, P, segs, sc);
         return hipGetLastError();
     }
-    return hipSuccess;
+    int64_t grid = (P + kUpdThreads - 1) / kUpdThreads;
+    if (grid > 8192) grid = 8192;
+    if (h)
+        hipLaunchKernelGGL(update_dense_scalar_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v, u,
+                           h, (int64_t)0, P, segs, sc);
+    else
+        hipLaunchKernelGGL(update_dense_scalar_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v, u,
+                           h, (int64_t)0, P, segs, sc);
+    return hipGetLastError();
 }
 
 // Global-norm clipping pass over the whole numerator: sets sc.clip (no-op without clipping).
@@ -1033,32 +1070,29 @@ hipError_t launch_update_dense_bf16(uint16_t* theta, uint16_t* v, const uint16_t
         if ((e = hipGetLastError()) != hipSuccess) return e;
         sc.clip = clip;
     }
-    int64_t done = 0;
-    if (aligned && P >= 8) {
-        const int64_t nvec = P / 8;
-        const int64_t grid = (nvec + kUpdThreads - 1) / kUpdThreads;
+    int64_t head = common_head({theta, v, u, h}, 2);
+    if (head >= 0) {
+        head = std::min(head, P);
+        const int64_t nvec = (P - head) / 8;
+        const int64_t extra = P - 8 * nvec;   // head + tail elements, one thread each
+        const int64_t grid = (nvec + extra + kUpdThreads - 1) / kUpdThreads;
         if (h)
             hipLaunchKernelGGL(update_dense_bf16x8_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
-                               u, h, nvec, segs, sc);
+                               u, h, head, nvec, P, segs, sc);
         else
             hipLaunchKernelGGL(update_dense_bf16x8_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
-                               u, h, nvec, segs, sc);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        done = nvec * 8;
-    }
-    if (done < P) {
-        int64_t grid = (P - done + kUpdThreads - 1) / kUpdThreads;
-        if (grid > 8192) grid = 8192;
-        if (h)
-            hipLaunchKernelGGL(update_dense_bf16_scalar_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st,
-                               theta, v, u, h, done, P, segs, sc);
-        else
-            hipLaunchKernelGGL(update_dense_bf16_scalar_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st,
-                               theta, v, u, h, done, P, segs, sc);
+                               u, h, head, nvec, P, segs, sc);
         return hipGetLastError();
     }
-    return hipSuccess;
+    int64_t grid = (P + kUpdThreads - 1) / kUpdThreads;
+    if (grid > 8192) grid = 8192;
+    if (h)
+        hipLaunchKernelGGL(update_dense_bf16_scalar_kernel<true>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
+                           u, h, (int64_t)0, P, segs, sc);
+    else
+        hipLaunchKernelGGL(update_dense_bf16_scalar_kernel<false>, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, v,
+                           u, h, (int64_t)0, P, segs, sc);
+    return hipGetLastError();
 }
 
 hipError_t launch_update_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P,

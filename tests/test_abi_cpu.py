@@ -77,17 +77,20 @@ def test_ema_rejects(lib, args, code):
 
 
 def _vjp(lib, **kw):
-    a = dict(H=FAKE, ldh=64, W=FAKE, ldw=100, R=FAKE, ldr=100, dt=bom.BOM_BF16, N=32, d=64, V=100, labels=FAKE, ig=-100,
-             qh=FAKE, s=FAKE, nv=FAKE, lam=0.5, dW=FAKE, dwdt=bom.BOM_F32, lddw=100, beta=0.0, db=None, dH=None,
-             dhdt=bom.BOM_BF16, lddh=64, ws=ctypes.c_void_p(0x100000), wsb=1 << 30)
+    a = dict(H=FAKE, ldh=64, W=FAKE, ldw=100, R=FAKE, isr=1, ldr=100, dt=bom.BOM_BF16, N=32, d=64, V=100, labels=FAKE,
+             ig=-100, lse=None, qh=FAKE, s=FAKE, nv=FAKE, lam=0.5, dW=FAKE, dwdt=bom.BOM_F32, lddw=100, beta=0.0, db=None,
+             dH=None, dhdt=bom.BOM_BF16, lddh=64, ws=ctypes.c_void_p(0x100000), wsb=1 << 30)
     a.update(kw)
-    return lib.bom_head_vjp(a["H"], a["ldh"], a["W"], a["ldw"], a["R"], a["ldr"], a["dt"], a["N"], a["d"], a["V"],
-                            a["labels"], a["ig"], a["qh"], a["s"], a["nv"], a["lam"], a["dW"], a["dwdt"], a["lddw"],
-                            a["beta"], a["db"], a["dH"], a["dhdt"], a["lddh"], a["ws"], a["wsb"], None)
+    return lib.bom_head_vjp(a["H"], a["ldh"], a["W"], a["ldw"], a["R"], a["isr"], a["ldr"], a["dt"], a["N"], a["d"],
+                            a["V"], a["labels"], a["ig"], a["lse"], a["qh"], a["s"], a["nv"], a["lam"], a["dW"],
+                            a["dwdt"], a["lddw"], a["beta"], a["db"], a["dH"], a["dhdt"], a["lddh"], a["ws"], a["wsb"],
+                            None)
 
 
 @pytest.mark.parametrize("kw,code", [
     (dict(H=None), 1), (dict(dW=None), 1), (dict(nv=None), 1), (dict(db=FAKE, s=None), 1),
+    (dict(isr=0), 1),                                # the logits input needs row_lse
+    (dict(isr=2), 2), (dict(isr=-1), 2),
     (dict(N=0), 2), (dict(V=1), 2), (dict(ldh=63), 2), (dict(lddw=99), 2), (dict(dH=FAKE, lddh=10), 2),
     (dict(dt=5), 3), (dict(dH=FAKE, dhdt=9), 3), (dict(dwdt=4), 3),
     (dict(dwdt=bom.BOM_BF16, wsb=0), 5),           # bf16 dW needs its fp32 staging in the workspace

@@ -1,10 +1,13 @@
-"""The 64-deep GEMM tiles on four waves per workgroup (one per SIMD, each 128 x 128).
+"""Head-VJP kernel routes selected by environment variables (read once per process), each run in a
+child process and checked against the oracle like the default-path parity cases.
 
-The library runs the 256 x 256 tiles of dH, dW, the paired launch and the forward on eight waves by
-default; four waves remain selectable (environment BOM_VJP_WAVES = "dH,dW,fwd,pair", read once per
-process). This test runs the library in a child process with every product on four waves and checks the
-results against the oracle like the default-path parity cases: whole rounds with leftover split-k tiles
-for dW and for dH, ragged tiles in m, n and k, the paired launch of both products, and the forward.
+* BOM_VJP_WAVES = "4,4,4,4": the 256 x 256 tiles of dH, dW, the paired launch and the forward on four
+  waves per workgroup (one per SIMD, each 128 x 128) instead of eight: whole rounds with leftover split-k
+  tiles for dW and for dH, ragged tiles in m, n and k, the paired launch of both products, the forward.
+* BOM_VJP_PLAN = "4,3,4,2": the 256-tile rank-1 kernel with k split three ways (dW) and two ways (dH) on
+  every tile, followed by the split-k reduction with the rank-1 term.
+* BOM_VJP_PLAN = "1,0,1,0": the 128-tile kernels that fold the history into G while staging R (no
+  fused small-product launch), with their own k splits.
 """
 import os
 import subprocess
@@ -39,7 +42,7 @@ sys.path.insert(0, {tests!r})
 from paper_2609_36738_amd import bom
 from test_gpu_parity import B1, LAM, _vjp_inputs
 N, d, V, out_path = {N}, {d}, {V}, {out!r}
-print(f"[child] four waves N={{N}} d={{d}} V={{V}}", flush=True)
+print(f"[child] N={{N}} d={{d}} V={{V}}", flush=True)
 Hh, Hd, Wh, Wd, Zh, Zd, y, q_prev, t = _vjp_inputs(N, d, V, "bf16", 0.05)
 yd = torch.from_numpy(y).to("cuda:0")
 res = bom.bom_residual(Zd, yd)
@@ -55,14 +58,23 @@ print("[child] done", flush=True)
 """
 
 
-@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_four_wave_tiles(case):
+VARIANTS = [("BOM_VJP_WAVES", "4,4,4,4", c) for c in CASES] + [
+    ("BOM_VJP_PLAN", "4,3,4,2", CASES[0]),
+    ("BOM_VJP_PLAN", "4,3,4,2", CASES[2]),
+    ("BOM_VJP_PLAN", "1,0,1,0", CASES[2]),
+    ("BOM_VJP_PLAN", "1,0,1,0", ("short_128", 640, 256, 3000, None, None)),
+]
+
+
+@pytest.mark.parametrize("var", VARIANTS, ids=[f"{v[0]}={v[1]}-{v[2][0]}" for v in VARIANTS])
+def test_env_variant(var):
+    env_name, env_value, case = var
     name, N, d, V, cols, rows = case
-    log(f"[four waves] {name}: child process with BOM_VJP_WAVES=4,4,4,4")
+    log(f"[env variant] {name}: child process with {env_name}={env_value}")
     with tempfile.TemporaryDirectory() as td:
         out = os.path.join(td, "out.npz")
         code = CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"), N=N, d=d, V=V, out=out)
-        env = dict(os.environ, BOM_VJP_WAVES="4,4,4,4")
+        env = dict(os.environ, **{env_name: env_value})
         r = subprocess.run([sys.executable, "-u", "-c", code], env=env, cwd=ROOT, timeout=240,
                            capture_output=True, text=True)
         log(r.stdout[-2000:])

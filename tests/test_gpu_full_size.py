@@ -2,8 +2,9 @@
 
 Residual: every row's statistics and the batch-mean residual s are checked in full (the oracle runs
 on row chunks in fp64 and the chunk means are combined by their valid-row counts); residual rows on
-a sample. Head VJP: sampled dW columns and dH rows (the oracle takes only those slices of Z), plus
-the dW row-sum invariant over the whole matrix. Update: sampled chunks (dense) or blocks (factored)
+a sample. Head VJP: 256 sampled dW columns (among them one in each leftover tile band and the ragged
+last column) and 256 dH rows (every 256-row tile); the oracle takes only those slices of Z, plus the
+dW row-sum invariant over the whole matrix. Update: sampled chunks (dense) or blocks (factored)
 whose inputs come from the seeded generator; the rest of the flat buffer holds other seeded values
 and is checked by a property (|step| <= lr at t = 1).
 """
@@ -110,8 +111,14 @@ def test_head_vjp_full(lm):
     torch.cuda.synchronize()
     _, qho = oracle.ema(q_prev, o["s"], f32(w.beta1), t)
     assert rel_fro(to_f64(qh), qho) <= 1e-5
-    cols = np.unique(np.r_[np.linspace(0, V - 1, 48).astype(int), [V - 1]])
-    rows = np.unique(np.r_[np.linspace(0, N - 1, 12 if V > 100000 else 32).astype(int), [N - 1]])
+    # 256 dW columns: spread over V, one in each of the last 96 tiles of 256 columns (the tiles a
+    # partly filled last round of the wide kernel runs with split k), and the ragged last column;
+    # 256 dH rows: spread over N (every 256-row tile) and the last row
+    tiles_v = -(-V // 256)
+    tail = [min(V - 1, t * 256 + (37 * t) % 256) for t in range(max(0, tiles_v - 96), tiles_v)]
+    cols = np.unique(np.r_[np.linspace(0, V - 1, 256 - len(tail)).astype(int), tail, [V - 1]])
+    rows = np.unique(np.r_[np.linspace(0, N - 1, 255).astype(int), [N - 1]])
+    assert cols.size >= 250 and rows.size >= 250
     Zh = lm["Zh"]
     dWo = oracle.dW_cols_sub(Hh, Zh[:, cols], cols, V, y, o["row_lse"], qho, o["n_valid"], f32(w.lam))
     dHo = oracle.dH_rows_sub(Wh, Zh[rows], rows, y, o["row_lse"], qho, o["n_valid"], f32(w.lam))

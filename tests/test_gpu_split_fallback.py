@@ -1,10 +1,12 @@
 """Split-row residual with the partner exchange switched off from the host.
 
 When rows are too wide for one workgroup, several workgroups share each row and exchange their
-per-part (max, sum, argmax) records; every wait is bounded and, past the bound, a workgroup computes
-the missing record from Z itself. A poll limit below zero (environment BOM_RESIDUAL_SPIN, read once
-per process) takes that path for every part of every row, so this test runs the library in a child
-process with it set and checks the results against the oracle like any other parity case.
+per-part (max, sum, argmax) records; every wait is bounded and, past the bound, a workgroup reduces
+the missing part's slice from Z itself with the operations that part runs, in the same order. A poll
+limit below zero (environment BOM_RESIDUAL_SPIN, read once per process) takes that path for every part
+of every row, so this test runs the library in a child process with it set, checks the results against
+the oracle like any other parity case, and checks that every output is bitwise equal to the normal
+path's (run in this process); the flags word differs only by BOM_FLAG_RESIDUAL_RECOMPUTED.
 """
 import os
 import subprocess
@@ -18,6 +20,7 @@ import torch
 import oracle
 import synth
 from gpu_util import gen_labels, gen_matrix, log, needs_gpu
+from paper_2609_36738_amd import bom
 from test_gpu_parity import _compare_residual
 
 pytestmark = [pytest.mark.gpu, needs_gpu]
@@ -61,6 +64,19 @@ def test_split_rows_without_exchange(case):
         got = np.load(out)
         # npz arrays as torch tensors, like the binding's outputs, for the shared comparison
         res = {k: torch.from_numpy(np.asarray(got[k])) for k in got.files}
-    Zh, _ = gen_matrix(N, V, synth.STREAM_Z, 1.28, "bf16")
+    Zh, Zd = gen_matrix(N, V, synth.STREAM_Z, 1.28, "bf16")
     y = gen_labels(N, V, "zipf", 0.05, 2)
-    _compare_residual(name, Zh, y, res, oracle.residual(Zh, y), "bf16")
+    orc = oracle.residual(Zh, y)
+    flags_fb = int(res["flags"][0])
+    assert flags_fb & bom.BOM_FLAG_RESIDUAL_RECOMPUTED, "the fallback path must report the recomputation"
+    res["flags"] = res["flags"] & ~bom.BOM_FLAG_RESIDUAL_RECOMPUTED
+    _compare_residual(name, Zh, y, res, orc, "bf16")
+    # the normal path (exchange on) in this process: the same bits everywhere
+    log(f"[residual] {name}: normal path, bitwise comparison")
+    ref = bom.bom_residual(Zd, torch.from_numpy(y).to("cuda:0"))
+    torch.cuda.synchronize()
+    assert int(ref["flags"][0]) == flags_fb & ~bom.BOM_FLAG_RESIDUAL_RECOMPUTED
+    for k in ("s", "row_lse", "row_argmax", "row_target", "loss", "n_valid"):
+        a, b = ref[k].cpu().numpy(), res[k].numpy()
+        assert a.dtype == b.dtype and np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
+    assert np.array_equal(ref["R"].float().cpu().numpy().view(np.uint32), res["R"].numpy().view(np.uint32)), "R"

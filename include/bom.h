@@ -111,6 +111,28 @@ bom_status bom_residual(const void* Z, bom_dtype z_dt, int64_t N, int64_t V, int
                         void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------------
+ * bom_residual_noalloc -- for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): bom_residual with the library's own fixed
+ * scratch array in place of the workspace. Same arguments, outputs and errors as bom_residual, without
+ * workspace and ws_bytes; it allocates nothing (no hipMalloc, no allocating library routine).
+ *
+ * The scratch is a device array of BOM_RESIDUAL_SCRATCH_BYTES that every device the library runs on holds
+ * until the process ends; its address on the current device (the stream must belong to the device that
+ * is current) is looked up on the first call on that device. A shape whose workspace would exceed it
+ * (bom_residual_workspace_bytes(N, V, z_dt) > BOM_RESIDUAL_SCRATCH_BYTES; e.g. V above about 60,000
+ * bf16 columns) returns BOM_ERR_WORKSPACE before anything is enqueued. Every call on one device shares
+ * that device's array and leaves its last contents there (each call rewrites what it reads, and clears
+ * what must start at zero with a kernel, not a memset), so calls that may overlap on one device (other
+ * streams, other threads) race: serialise them, or use bom_residual with separate workspaces.
+ * ---------------------------------------------------------------------------------------- */
+#define BOM_RESIDUAL_SCRATCH_BYTES ((size_t)64 << 20)
+bom_status bom_residual_noalloc(const void* Z, bom_dtype z_dt, int64_t N, int64_t V, int64_t ldz,
+                                const int32_t* labels, int32_t ignore_index,
+                                float* s, float* row_lse, int32_t* row_argmax, float* row_target,
+                                void* R, bom_dtype r_dt, int64_t ldr,
+                                float* loss, int32_t* n_valid, int32_t* flags, void* stream);
+
+/* ------------------------------------------------------------------------------------------
  * bom_ema -- Sec. 3.2, Eq. (2) and Algorithm 1: q_t = beta1 q_{t-1} + (1 - beta1) s_t,
  * q_hat_t = q_t / (1 - beta1^t), with q_0 = 0 and t >= 1.
  *

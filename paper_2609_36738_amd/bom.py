@@ -81,6 +81,9 @@ def load(build_if_missing: bool = True):
         lib.bom_residual.restype = ctypes.c_int
         lib.bom_residual.argtypes = [vp, ctypes.c_int, i64, i64, i64, vp, i32, vp, vp, vp, vp, vp, ctypes.c_int, i64, vp,
                                      vp, vp, vp, sz, vp]
+        lib.bom_residual_noalloc.restype = ctypes.c_int
+        lib.bom_residual_noalloc.argtypes = [vp, ctypes.c_int, i64, i64, i64, vp, i32, vp, vp, vp, vp, vp, ctypes.c_int,
+                                             i64, vp, vp, vp, vp]
         lib.bom_ema.restype = ctypes.c_int
         lib.bom_ema.argtypes = [vp, vp, i64, f32, i64, vp, vp]
         lib.bom_head_vjp_workspace_bytes.restype = sz
@@ -173,6 +176,27 @@ def bom_residual(Z, labels, *, ignore_index=-100, s=None, row_lse=None, row_argm
                             _stream(stream)))
     return dict(s=s, row_lse=row_lse, row_argmax=row_argmax, row_target=row_target, R=R, loss=loss, n_valid=n_valid,
                 flags=flags, workspace=workspace)
+
+
+RESIDUAL_SCRATCH_BYTES = 64 << 20   # BOM_RESIDUAL_SCRATCH_BYTES
+
+
+def bom_residual_noalloc(Z, labels, *, ignore_index=-100, s, row_lse, row_argmax=None, row_target=None, R=None,
+                         loss, n_valid, flags, stream=None) -> dict:
+    """bom_residual on the library's fixed scratch array (no workspace; the call allocates nothing, so every
+    output tensor is passed in). Calls that overlap on one device race on the shared scratch."""
+    lib = load()
+    N, V = Z.shape
+    dt = _dtype_code(Z)
+    ldz = _rowmajor(Z, "Z")
+    if labels.dtype != torch.int32:
+        raise TypeError("labels must be int32")
+    ldr = _rowmajor(R, "R") if R is not None else V
+    _check(lib.bom_residual_noalloc(_ptr(Z), dt, N, V, ldz, _ptr(labels), ignore_index, _ptr(s), _ptr(row_lse),
+                                    _ptr(row_argmax), _ptr(row_target), _ptr(R), dt, ldr, _ptr(loss), _ptr(n_valid),
+                                    _ptr(flags), _stream(stream)))
+    return dict(s=s, row_lse=row_lse, row_argmax=row_argmax, row_target=row_target, R=R, loss=loss, n_valid=n_valid,
+                flags=flags)
 
 
 def bom_ema(q, s, beta1: float, t: int, q_hat=None, stream=None):

@@ -75,10 +75,14 @@ size_t bom_residual_workspace_bytes(int64_t N, int64_t V, bom_dtype z_dt) {
     return bom::residual_workspace_bytes(N, V, z_dt);
 }
 
-bom_status bom_residual(const void* Z, bom_dtype z_dt, int64_t N, int64_t V, int64_t ldz, const int32_t* labels,
-                        int32_t ignore_index, float* s, float* row_lse, int32_t* row_argmax, float* row_target, void* R,
-                        bom_dtype r_dt, int64_t ldr, float* loss, int32_t* n_valid, int32_t* flags, void* workspace,
-                        size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+// Argument checks of bom_residual (also run by the allocation-free variant before it touches the device).
+bom_status bom_residual_validate(const void* Z, bom_dtype z_dt, int64_t N, int64_t V, int64_t ldz,
+                                 const int32_t* labels, const float* s, const float* row_lse, const void* R,
+                                 bom_dtype r_dt, int64_t ldr, const float* loss, const int32_t* n_valid,
+                                 const int32_t* flags, const void* workspace, size_t ws_bytes) {
     if (!Z || !labels || !s || !row_lse || !loss || !n_valid || !flags)
         return fail(BOM_ERR_NULL, "bom_residual: Z, labels, s, row_lse, loss, n_valid and flags are required");
     if (N < 1 || V < 2 || N >= kMaxDim || V >= kMaxDim)
@@ -97,10 +101,49 @@ bom_status bom_residual(const void* Z, bom_dtype z_dt, int64_t N, int64_t V, int
     const size_t esz = z_dt == BOM_BF16 ? 2 : 4;
     if (R && overlap(R, (size_t)((N - 1) * ldr + V) * esz, Z, (size_t)((N - 1) * ldz + V) * esz))
         return fail(BOM_ERR_ALIAS, "bom_residual: R must not overlap Z");
+    return BOM_OK;
+}
+}  // namespace
+
+extern "C" {
+
+bom_status bom_residual(const void* Z, bom_dtype z_dt, int64_t N, int64_t V, int64_t ldz, const int32_t* labels,
+                        int32_t ignore_index, float* s, float* row_lse, int32_t* row_argmax, float* row_target, void* R,
+                        bom_dtype r_dt, int64_t ldr, float* loss, int32_t* n_valid, int32_t* flags, void* workspace,
+                        size_t ws_bytes, void* stream) {
+    const bom_status st = bom_residual_validate(Z, z_dt, N, V, ldz, labels, s, row_lse, R, r_dt, ldr, loss, n_valid,
+                                                flags, workspace, ws_bytes);
+    if (st != BOM_OK) return st;
     hipError_t e = bom::launch_residual(Z, z_dt, (int)N, (int)V, ldz, labels, ignore_index, s, row_lse, row_argmax,
                                         row_target, R, ldr, loss, n_valid, flags, workspace,
                                         static_cast<hipStream_t>(stream));
     return hip_status(e, "bom_residual");
+}
+
+bom_status bom_residual_noalloc(const void* Z, bom_dtype z_dt, int64_t N, int64_t V, int64_t ldz,
+                                const int32_t* labels, int32_t ignore_index, float* s, float* row_lse,
+                                int32_t* row_argmax, float* row_target, void* R, bom_dtype r_dt, int64_t ldr,
+                                float* loss, int32_t* n_valid, int32_t* flags, void* stream) {
+    if (N >= 1 && V >= 2 && N < kMaxDim && V < kMaxDim && is_dtype(z_dt)) {
+        const size_t need = bom::residual_workspace_bytes(N, V, z_dt);
+        if (need > bom::kResidualScratchBytes)
+            return fail(BOM_ERR_WORKSPACE,
+                        "bom_residual_noalloc: this shape needs %zu bytes of scratch; the library's fixed scratch "
+                        "holds %zu (use bom_residual with a workspace)",
+                        need, bom::kResidualScratchBytes);
+    }
+    // the arguments are validated by bom_residual before anything touches the device: look the scratch
+    // up only for a call that passes them
+    const size_t big = bom::kResidualScratchBytes;
+    void* probe = reinterpret_cast<void*>((uintptr_t)256);   // aligned stand-in, never dereferenced
+    bom_status st = bom_residual_validate(Z, z_dt, N, V, ldz, labels, s, row_lse, R, r_dt, ldr, loss, n_valid, flags,
+                                          probe, big);
+    if (st != BOM_OK) return st;
+    void* ws = nullptr;
+    const hipError_t e = bom::residual_scratch(&ws);
+    if (e != hipSuccess) return hip_status(e, "bom_residual_noalloc (scratch lookup)");
+    return bom_residual(Z, z_dt, N, V, ldz, labels, ignore_index, s, row_lse, row_argmax, row_target, R, r_dt, ldr,
+                        loss, n_valid, flags, ws, big, stream);
 }
 
 bom_status bom_ema(float* q, const float* s, int64_t V, float beta1, int64_t t, float* q_hat, void* stream) {

@@ -18,6 +18,11 @@ hipError_t launch_residual(const void* Z, bom_dtype dt, int N, int V, int64_t ld
                            void* R, int64_t ldr, float* loss, int32_t* n_valid, int32_t* flags, void* ws,
                            hipStream_t stream);
 
+// Allocation-free residual: the device address of this device's fixed scratch array (looked up once per
+// device, with that device current) of kResidualScratchBytes, which takes the workspace's place.
+constexpr size_t kResidualScratchBytes = (size_t)BOM_RESIDUAL_SCRATCH_BYTES;
+hipError_t residual_scratch(void** ptr);
+
 // ---- EMA -----------------------------------------------------------------------------------
 hipError_t launch_ema(float* q, const float* s, int64_t V, float beta1, float inv_bc1, float* q_hat,
                       hipStream_t stream);

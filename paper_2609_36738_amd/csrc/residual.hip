@@ -13,6 +13,7 @@
 #include <climits>
 #include <cmath>
 #include <cstdlib>
+#include <mutex>
 #include <type_traits>
 
 #include "common.hpp"
@@ -1358,6 +1359,36 @@ hipError_t launch_residual(const void* Z, bom_dtype dt, int N, int V, int64_t ld
                                            ldr, loss, n_valid, flags, ws, stream)
                   : run_residual<float, 1>(z, N, V, ldz, labels, ignore_index, s, row_lse, row_argmax, row_target, r,
                                            ldr, loss, n_valid, flags, ws, stream);
+}
+
+// ---- allocation-free variant ----------------------------------------------------------------------
+// A fixed device array that stands in for the caller's workspace (for callers that cannot allocate).
+// Each device holds its own copy for the life of the process; host code never passes the array's name
+// to a kernel (in host code it is a stand-in, not a device address): it looks up the device address once
+// per device and passes that. Calls that overlap on one device share the array and race.
+static __device__ __align__(256) unsigned char scratch[kResidualScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t residual_scratch(void** ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr || reinterpret_cast<uintptr_t>(p) % 256 != 0) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 }  // namespace bom

@@ -203,3 +203,14 @@ def test_head_forward_rejects(lib):
     assert lib.bom_head_forward(FAKE, 8, FAKE, 4, None, 5, 4, 8, 4, FAKE2, 4, None) == 3
     assert lib.bom_head_forward(FAKE, 7, FAKE, 4, None, bom.BOM_F32, 4, 8, 4, FAKE2, 4, None) == 2
     assert lib.bom_head_forward(None, 8, FAKE, 4, None, bom.BOM_F32, 4, 8, 4, FAKE2, 4, None) == 1
+
+
+def test_residual_noalloc_refuses_beyond_scratch(lib):
+    # the size check runs before the scratch is looked up or anything is enqueued (no GPU needed)
+    N, V = 512, 70000
+    assert lib.bom_residual_workspace_bytes(N, V, bom.BOM_BF16) > bom.RESIDUAL_SCRATCH_BYTES
+    st = lib.bom_residual_noalloc(FAKE, bom.BOM_BF16, N, V, V, FAKE, -100, FAKE, FAKE, None, None, None, bom.BOM_BF16,
+                                  V, FAKE, FAKE, FAKE, None)
+    assert st == 5 and b"scratch" in lib.bom_last_error()
+    assert lib.bom_residual_noalloc(None, bom.BOM_BF16, 8, 100, 100, FAKE, -100, FAKE, FAKE, None, None, None,
+                                    bom.BOM_BF16, 100, FAKE, FAKE, FAKE, None) == 1

@@ -61,6 +61,10 @@ def _load():
                                             f64, f64, f64, f64, i64]
         lib.orc_update_blocks.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp, vp, ctypes.c_int, f64, f64, f64, f64, f64,
                                           i64]
+        lib.orc_update_adamw.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp, ctypes.c_int, f64, f64, f64, f64, f64, f64,
+                                         i64]
+        lib.orc_update_adamw_factored.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp, vp, vp, ctypes.c_int, f64,
+                                                  f64, f64, f64, f64, f64, i64]
         lib.orc_head_forward.argtypes = [vp, i64, i64, vp, i64, vp, vp]
         lib.orc_clip_factor.argtypes = [vp, vp, i64, f64, f64, f64]
         lib.orc_round_bf16.argtypes = [vp, i64, vp]
@@ -192,6 +196,27 @@ def update_dense(theta, v, u, *, lr, beta2, eps, t, segments=None, weight_decay=
                              float(weight_decay), float(lr), float(beta2), float(eps), float(lam), float(u_scale),
                              int(t))
     return theta, v
+
+
+def update_adamw(theta, m, v, g, *, lr, beta1, beta2, eps, t, segments=None, weight_decay=0.0, u_scale=1.0):
+    """AdamW step (the comparison arm of the cost model): returns (theta_new, m_new, v_new) in fp64."""
+    theta, m, v, g = _f64(theta).copy(), _f64(m).copy(), _f64(v).copy(), _f64(g)
+    off, ln, wd, ns = _segs(segments)
+    _load().orc_update_adamw(_p(theta), _p(m), _p(v), _p(g), theta.size, _p(off), _p(ln), _p(wd), ns,
+                             float(weight_decay), float(lr), float(beta1), float(beta2), float(eps), float(u_scale),
+                             int(t))
+    return theta, m, v
+
+
+def update_adamw_factored(theta, m, Rr, Cc, g, *, lr, beta1, beta2, eps, t, block_rows, block_cols, segments=None,
+                          weight_decay=0.0, u_scale=1.0):
+    """AdamW with the factored second moment: returns (theta_new, m_new, Rr_new, Cc_new) in fp64."""
+    theta, m, Rr, Cc, g = _f64(theta).copy(), _f64(m).copy(), _f64(Rr).copy(), _f64(Cc).copy(), _f64(g)
+    off, ln, wd, ns = _segs(segments)
+    _load().orc_update_adamw_factored(_p(theta), _p(m), _p(Rr), _p(Cc), _p(g), theta.size, int(block_rows),
+                                      int(block_cols), _p(off), _p(ln), _p(wd), ns, float(weight_decay), float(lr),
+                                      float(beta1), float(beta2), float(eps), float(u_scale), int(t))
+    return theta, m, Rr, Cc
 
 
 TELEMETRY_FIELDS = ("cos", "drift", "cancellation", "m_norm", "h_norm")

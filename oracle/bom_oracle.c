@@ -348,6 +348,79 @@ void orc_update_factored(double* theta, double* Rr, double* Cc, const double* u,
 }
 
 /*
+ * AdamW, the comparison optimizer whose dense first moment BOM deletes (Sec. 1: an EMA m_t of the
+ * gradients beside every tensor; Sec. 3.5: its update map a / (sqrt(v_hat) + eps) applied to the
+ * bias-corrected first moment m_hat = m / (1 - beta1^t)). It is here as the other arm of the cost model of
+ * appendix "First-order cost accounting" (Delta t = alpha N_out - beta P: deleting m removes its
+ * maintenance over the P elements). With g the gradient (times u_scale):
+ *   m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g^2;
+ *   theta = (1 - lr * omega) theta - lr * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps).
+ */
+void orc_update_adamw(double* theta, double* m, double* v, const double* g, int64_t P, const int64_t* seg_off,
+                      const int64_t* seg_len, const double* seg_wd, int nsegs, double wd_default, double lr,
+                      double beta1, double beta2, double eps, double u_scale, int64_t t) {
+    double bc1 = 1.0 - pow(beta1, (double)t);
+    double bc2 = 1.0 - pow(beta2, (double)t);
+#pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < P; ++e) {
+        double ge = u_scale * g[e];
+        double om = orc_decay_of(e, seg_off, seg_len, seg_wd, nsegs, wd_default);
+        m[e] = beta1 * m[e] + (1.0 - beta1) * ge;
+        v[e] = beta2 * v[e] + (1.0 - beta2) * ge * ge;
+        double mhat = m[e] / bc1;
+        double vhat = v[e] / bc2;
+        theta[e] = (1.0 - lr * om) * theta[e] - lr * mhat / (sqrt(vhat) + eps);
+    }
+}
+
+/*
+ * AdamW with the factored second moment of orc_update_factored (the same reading, here of g^2): the dense
+ * first moment m as in orc_update_adamw, v_hat_ij = Rr_i Cc_j / (sum_{k in block} Rr_k) / (1 - beta2^t).
+ */
+void orc_update_adamw_factored(double* theta, double* m, double* Rr, double* Cc, const double* g, int64_t P,
+                               int64_t block_rows, int64_t block_cols, const int64_t* seg_off, const int64_t* seg_len,
+                               const double* seg_wd, int nsegs, double wd_default, double lr, double beta1,
+                               double beta2, double eps, double u_scale, int64_t t) {
+    double bc1 = 1.0 - pow(beta1, (double)t);
+    double bc2 = 1.0 - pow(beta2, (double)t);
+    int64_t nrows = (P + block_cols - 1) / block_cols;
+    int64_t nblocks = (nrows + block_rows - 1) / block_rows;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < nblocks; ++b) {
+        int64_t r0 = b * block_rows;
+        int64_t r1 = r0 + block_rows < nrows ? r0 + block_rows : nrows;
+        double* kappa = (double*)calloc((size_t)block_cols, sizeof(double));
+        double* Cb = Cc + b * block_cols;
+        for (int64_t i = r0; i < r1; ++i) {
+            double rho = 0.0;
+            for (int64_t j = 0; j < block_cols; ++j) {
+                int64_t e = i * block_cols + j;
+                if (e >= P) break;
+                double ge = u_scale * g[e];
+                rho += ge * ge;
+                kappa[j] += ge * ge;
+            }
+            Rr[i] = beta2 * Rr[i] + (1.0 - beta2) * rho;
+        }
+        for (int64_t j = 0; j < block_cols; ++j) Cb[j] = beta2 * Cb[j] + (1.0 - beta2) * kappa[j];
+        double rsum = 0.0;
+        for (int64_t i = r0; i < r1; ++i) rsum += Rr[i];
+        for (int64_t i = r0; i < r1; ++i) {
+            for (int64_t j = 0; j < block_cols; ++j) {
+                int64_t e = i * block_cols + j;
+                if (e >= P) break;
+                double ge = u_scale * g[e];
+                double om = orc_decay_of(e, seg_off, seg_len, seg_wd, nsegs, wd_default);
+                m[e] = beta1 * m[e] + (1.0 - beta1) * ge;
+                double vhat = rsum > 0.0 ? Rr[i] * Cb[j] / rsum / bc2 : 0.0;
+                theta[e] = (1.0 - lr * om) * theta[e] - lr * (m[e] / bc1) / (sqrt(vhat) + eps);
+            }
+        }
+        free(kappa);
+    }
+}
+
+/*
  * Block-shared second moment: Adam-mini's update map driven by the BOM numerator. Sec. 3.5 deletes the
  * base optimizer's first moment and feeds the numerator u' to its map Phi(a, v); for Adam-mini that map
  * is a / (sqrt(v_hat) + eps) with one second-moment value per block of parameters, the block average of

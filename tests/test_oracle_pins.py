@@ -445,6 +445,86 @@ def test_factored_zero_block_keeps_decay_only():
     np.testing.assert_allclose(thf, (1 - 1e-3) * th, rtol=1e-15)
 
 
+# AdamW, the comparison arm of the cost model (appendix "First-order cost accounting"): the dense first
+# moment m that BOM deletes, with the same second moment and step map (Sec. 3.5).
+def test_adamw_first_step_closed_form():
+    # t = 1 from m = v = 0: m_hat = g and v_hat = g^2, so theta_1 = (1 - lr wd) theta - lr g / (|g| + eps)
+    r = _rng(40)
+    P = 900
+    th, g = r.standard_normal(P), r.standard_normal(P) * 1e-3
+    g[:4] = 0.0
+    segs = [(0, 500, 0.01), (500, 100, 0.0)]
+    t1, m1, v1 = oracle.update_adamw(th, np.zeros(P), np.zeros(P), g, lr=1e-2, beta1=0.9, beta2=B2, eps=EPS, t=1,
+                                     segments=segs, weight_decay=0.1)
+    wd = np.r_[np.full(500, 0.01), np.zeros(100), np.full(300, 0.1)]
+    np.testing.assert_allclose(t1, (1 - 1e-2 * wd) * th - 1e-2 * g / (np.abs(g) + EPS), rtol=1e-12, atol=1e-16)
+    np.testing.assert_allclose(m1, 0.1 * g, rtol=1e-15)
+    np.testing.assert_allclose(v1, (1 - B2) * g * g, rtol=1e-15)
+
+
+def test_adamw_moments_explicit_sums():
+    # m_t = sum_tau (1 - b1) b1^(t - tau) g_tau, v_t likewise with g^2; the step uses their bias corrections
+    r = _rng(41)
+    P, T, b1 = 48, 6, 0.9
+    G = r.standard_normal((T, P))
+    th, m, v = r.standard_normal(P), np.zeros(P), np.zeros(P)
+    for t in range(1, T + 1):
+        th_prev = th
+        th, m, v = oracle.update_adamw(th, m, v, G[t - 1], lr=1e-3, beta1=b1, beta2=B2, eps=EPS, t=t)
+        em = sum((1 - b1) * b1 ** (t - k) * G[k - 1] for k in range(1, t + 1))
+        ev = sum((1 - B2) * B2 ** (t - k) * G[k - 1] ** 2 for k in range(1, t + 1))
+        np.testing.assert_allclose(m, em, rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(v, ev, rtol=1e-12)
+        step = (em / (1 - b1 ** t)) / (np.sqrt(ev / (1 - B2 ** t)) + EPS)
+        np.testing.assert_allclose(th, th_prev - 1e-3 * step, rtol=1e-12, atol=1e-15)
+
+
+def test_adamw_without_first_moment_is_the_bom_update_of_g():
+    # beta1 = 0: m_hat = g, so AdamW takes the same step as the BOM update with numerator g (Sec. 3.5's map)
+    r = _rng(42)
+    P = 300
+    th, g, v0 = r.standard_normal(P), r.standard_normal(P) * 1e-3, np.abs(r.standard_normal(P)) * 1e-6
+    segs = [(0, 200, 0.01)]
+    ta, _, va = oracle.update_adamw(th, r.standard_normal(P), v0, g, lr=1e-2, beta1=0.0, beta2=B2, eps=EPS, t=3,
+                                    segments=segs, weight_decay=0.1, u_scale=0.5)
+    tb, vb = oracle.update_dense(th, v0, g, lr=1e-2, beta2=B2, eps=EPS, t=3, segments=segs, weight_decay=0.1,
+                                 u_scale=0.5)
+    np.testing.assert_allclose(ta, tb, rtol=1e-15)
+    np.testing.assert_allclose(va, vb, rtol=1e-15)
+
+
+def test_adamw_factored_reductions():
+    r = _rng(43)
+    br, bc = 4, 8
+    P = 11 * 8 + 5
+    th, g = r.standard_normal(P), r.standard_normal(P) * 1e-3
+    Rr0, Cc0 = np.abs(r.standard_normal(12)) * 1e-6, np.abs(r.standard_normal(3 * bc)) * 1e-6
+    # beta1 = 0: the factored BOM update of g
+    ta, _, Ra, Ca = oracle.update_adamw_factored(th, r.standard_normal(P), Rr0, Cc0, g, lr=1e-2, beta1=0.0, beta2=B2,
+                                                 eps=EPS, t=2, block_rows=br, block_cols=bc, weight_decay=0.1)
+    tb, Rb, Cb = oracle.update_factored(th, Rr0, Cc0, g, lr=1e-2, beta2=B2, eps=EPS, t=2, block_rows=br, block_cols=bc,
+                                        weight_decay=0.1)
+    np.testing.assert_allclose(ta, tb, rtol=1e-15)
+    np.testing.assert_allclose(Ra, Rb, rtol=1e-15)
+    np.testing.assert_allclose(Ca, Cb, rtol=1e-15)
+    # g^2 exactly rank one on every block: the factored v_hat is the dense one (Adafactor identity), so the
+    # whole AdamW trajectory, first moment included, equals the dense AdamW one
+    rows = 20
+    P2 = rows * 8
+    a, bb = np.exp(r.standard_normal(rows)), np.exp(r.standard_normal(8))
+    sign = np.where(r.random((rows, 8)) < 0.5, -1.0, 1.0)
+    th2 = r.standard_normal(P2)
+    thd, thf, md, mf, v = th2.copy(), th2.copy(), np.zeros(P2), np.zeros(P2), np.zeros(P2)
+    Rr, Cc = np.zeros(rows), np.zeros(3 * 8)
+    for t in range(1, 5):
+        gg = (sign * np.sqrt(np.outer(a, bb)) * (1.0 + 0.5 * t)).ravel()
+        thd, md, v = oracle.update_adamw(thd, md, v, gg, lr=1e-2, beta1=0.9, beta2=B2, eps=EPS, t=t, weight_decay=0.1)
+        thf, mf, Rr, Cc = oracle.update_adamw_factored(thf, mf, Rr, Cc, gg, lr=1e-2, beta1=0.9, beta2=B2, eps=EPS,
+                                                       t=t, block_rows=8, block_cols=8, weight_decay=0.1)
+        np.testing.assert_allclose(thf, thd, rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(mf, md, rtol=1e-15)
+
+
 # Block-shared second moment: Adam-mini's map with the BOM numerator (Sec. 3.5, the substitution into a
 # base optimizer's update map; Adam-mini shares one second-moment value per block).
 def test_blocks_of_one_are_the_dense_update():

@@ -147,6 +147,53 @@ class Problem:
         torch.cuda.synchronize()
         log(f"[bench] inputs for {w.name} ready in {time.time() - t0:.1f}s")
 
+    def init_adamw(self):
+        """State of the comparison arm: AdamW's first moment m and its own second moment (dense, or the same
+        factored layout as BOM's), on the same parameter and gradient buffers."""
+        w = self.w
+        dev = self.theta.device
+        self.m = torch.zeros(w.P, dtype=torch.float32, device=dev)
+        if w.factored:
+            nrows = -(-w.P // w.block_cols)
+            nblocks = -(-nrows // w.block_rows)
+            self.va = torch.zeros(nrows, dtype=torch.float32, device=dev)
+            self.va_col = torch.zeros(nblocks * w.block_cols, dtype=torch.float32, device=dev)
+        else:
+            self.va = torch.zeros(w.P, dtype=torch.float32, device=dev)
+            self.va_col = None
+        self.ws_adamw = None
+        torch.cuda.synchronize()
+
+    def step_adamw(self, t: int, ev=None):
+        """One step of the AdamW arm: the same residual (the cross-entropy backward needs R), the head
+        products at lambda = 0 (the plain gradient, no history term) and AdamW's update with its first
+        moment. Stage events: residual, (no EMA), head VJP, update."""
+        w = self.w
+        d, V = w.d, w.V
+        if ev is not None:
+            ev[0].record()
+        self.res = bom.bom_residual(self.Z, self.labels, R=self.R, workspace=self.ws_res,
+                                    **({} if self.res is None else {k: self.res[k] for k in (
+                                        "s", "row_lse", "row_argmax", "row_target", "loss", "n_valid", "flags")}))
+        self.ws_res = self.res["workspace"]
+        if ev is not None:
+            ev[1].record()
+            ev[2].record()
+        W = self.W if self.W is not None else self.theta[: d * V].view(d, V)
+        dW = self.u[: d * V].view(d, V)
+        db = self.u[d * V: d * V + V] if w.has_bias else None
+        g = bom.bom_head_vjp(self.H, W, self.R, self.labels, self.q_hat, self.res["n_valid"], s=self.res["s"],
+                             lam=0.0, dW=dW, db=db, dH=self.dH, workspace=self.ws_vjp)
+        self.ws_vjp = g["workspace"]
+        if ev is not None:
+            ev[3].record()
+        cfg = bom.make_update_cfg(lr=w.lr, beta2=w.beta2, eps=w.eps, t=t, factored=w.factored,
+                                  block_rows=w.block_rows, block_cols=w.block_cols)
+        self.ws_adamw = bom.bom_adamw_update(self.theta, self.m, self.va, self.u, cfg, beta1=w.beta1,
+                                             v_col=self.va_col, segments=self.segments, workspace=self.ws_adamw)
+        if ev is not None:
+            ev[4].record()
+
     def step(self, t: int, ev=None):
         w = self.w
         d, V = w.d, w.V
@@ -182,6 +229,70 @@ class Problem:
                                      workspace=self.ws_upd)
         if ev is not None:
             ev[4].record()
+
+
+def time_adamw_arm(prob, args, bom_ms):
+    """The AdamW arm on the same inputs (W warmup and K timed steps, like the BOM arm): step time, stage
+    times, its update against the HBM roofline (28 bytes per parameter dense: read theta, m, v, g; write
+    theta, m, v; factored second moment: 24 bytes, g read twice), and Delta t = t_BOM - t_AdamW."""
+    w = prob.w
+    prob.init_adamw()
+    for k in range(args.warmup):
+        prob.step_adamw(k + 1)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for k in range(args.steps):
+        prob.step_adamw(args.warmup + k + 1, evs[k])
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    st = {name: float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
+          for i, name in ((0, "residual"), (2, "head_vjp"), (3, "update"))}
+    nbytes = (24 if w.factored else 28) * w.P + (8 * -(-w.P // w.block_cols) if w.factored else 0)
+    rate = nbytes / (st["update"] / 1e3) / 1e9
+    del prob.m, prob.va, prob.va_col
+    torch.cuda.empty_cache()
+    log(f"[bench] {w.name}: AdamW arm {ms:.4f} ms/step (BOM {bom_ms:.4f})")
+    return {"ms_per_step": round(ms, 5), "stages_ms": {k: round(v, 5) for k, v in st.items()},
+            "bom_stages_ms": None,   # filled by run_workload
+            "update": {"rate": round(rate, 2), "unit": "GB/s", "frac": round(rate / HBM_PEAK_GBS, 4),
+                       "algorithmic_bytes": nbytes,
+                       "per_unit": "24 bytes per parameter (factored v: read g twice, read+write theta and m)"
+                       if w.factored else "28 bytes per parameter (read theta, m, v, g; write theta, m, v)"},
+            "delta_ms": round(bom_ms - ms, 5), "ratio": round(bom_ms / ms, 5),
+            "N_out": w.N * w.V, "P": w.P}
+
+
+def cost_model_fit(rows):
+    """Delta t = t_BOM - t_AdamW = alpha N_out - beta P (appendix 'First-order cost accounting'), alpha and beta
+    in ms per 1e9 elements, r* = alpha / beta. 'joint': the paper's rule, least squares without intercept of
+    the step-time differences on (N_out, -P). 'by_stage': each term on its own stages (the residual is the
+    same call in both arms): the output side, EMA + head VJP (BOM) - head VJP (AdamW, lambda = 0), regressed
+    on N_out; the parameter side, update (AdamW) - update (BOM), regressed on P. Across these workloads N_out
+    and P grow together, so the joint fit is poorly conditioned and the staged one separates the terms."""
+    A = np.array([[r["N_out"] / 1e9, -r["P"] / 1e9] for r in rows])
+    y = np.array([r["delta_ms"] for r in rows])
+    (alpha, beta), *_ = np.linalg.lstsq(A, y, rcond=None)
+    pred = A @ np.array([alpha, beta])
+    n_out = np.array([r["N_out"] / 1e9 for r in rows])
+    p_par = np.array([r["P"] / 1e9 for r in rows])
+    d_out = np.array([r["bom_stages_ms"]["bom_ema"] + r["bom_stages_ms"]["bom_head_vjp"] - r["stages_ms"]["head_vjp"]
+                      for r in rows])
+    d_par = np.array([r["stages_ms"]["update"] - r["bom_stages_ms"]["bom_update"] for r in rows])
+    a_s = float(n_out @ d_out / (n_out @ n_out))
+    b_s = float(p_par @ d_par / (p_par @ p_par))
+    return {"joint": {"alpha_ms_per_1e9_nout": round(float(alpha), 4), "beta_ms_per_1e9_params": round(float(beta), 4),
+                      "r_star": round(float(alpha / beta), 4) if beta != 0 else None},
+            "by_stage": {"alpha_ms_per_1e9_nout": round(a_s, 4), "beta_ms_per_1e9_params": round(b_s, 4),
+                         "r_star": round(a_s / b_s, 4) if b_s != 0 else None},
+            "points": [{"workload": r["workload"], "N_out": r["N_out"], "P": r["P"], "delta_ms": r["delta_ms"],
+                        "joint_fit_ms": round(float(p_), 4), "output_side_ms": round(float(do), 5),
+                        "parameter_side_ms": round(float(dp), 5)}
+                       for r, p_, do, dp in zip(rows, pred, d_out, d_par)],
+            "paper_h800_context": {"alpha_ms_per_1e9_nout": 43.2758, "beta_ms_per_1e9_params": 15.4769,
+                                   "r_star": 2.80}}
 
 
 def time_forward(prob, steps):
@@ -489,6 +600,9 @@ def run_workload(w, args, cpu_budget, dev):
         "stages": per_stage,
         "roofline": roofline,
     }
+    if args.adamw:
+        out["adamw"] = time_adamw_arm(prob, args, ms_per_step)
+        out["adamw"]["bom_stages_ms"] = {s: round(stage_ms[s], 5) for s in stages}
     if args.forward:
         out["forward"] = time_forward(prob, args.steps)
     if args.telemetry:
@@ -528,6 +642,8 @@ def main():
     ap.add_argument("--adam-mini", action="store_true",
                     help="block-shared second moment (Adam-mini's update map with the BOM numerator) over a "
                          "transformer-shaped partition of the flat buffer, instead of the dense or factored one")
+    ap.add_argument("--no-adamw", dest="adamw", action="store_false",
+                    help="skip the AdamW comparison arm (and the cost-model fit) after each workload's BOM steps")
     ap.add_argument("--z-route", action="store_true",
                     help="the head products take the logits Z and row_lse and form R themselves; the residual "
                          "writes no R")
@@ -591,6 +707,14 @@ def main():
         out["per_config"] = {}
         for w in others:
             out["per_config"][w.name] = run_workload(w, args, args.cpu_budget_other, dev)
+    if args.adamw:
+        # the paper's ladder is the language-model pretraining rungs: fit over the bf16-logit workloads (the
+        # tiny fp32 classifier is launch-bound, its Delta t a few microseconds of launch jitter)
+        rows = [dict(r["adamw"], workload=r["config"]["workload"])
+                for r in [out] + list(out.get("per_config", {}).values())
+                if "adamw" in r and BY_NAME[r["config"]["workload"]].dtype == "bf16"]
+        if len(rows) >= 2:
+            out["cost_model"] = cost_model_fit(rows)
     print(json.dumps(out), flush=True)
 
 

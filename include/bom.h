@@ -278,6 +278,29 @@ bom_status bom_update(void* theta, void* v, float* v_col, const void* u, const v
                       void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------------
+ * bom_adamw_update -- the comparison optimizer, not part of BOM's step: AdamW's update with its dense
+ * first moment (Sec. 1: the EMA m of the gradients that BOM deletes; Sec. 3.5: the update map
+ * a / (sqrt(v_hat) + eps) applied to m_hat = m / (1 - beta1^t)). It is the other arm of the first-order
+ * cost model of appendix "First-order cost accounting" (Delta t = alpha N_out - beta P), timed beside
+ * bom_update on the same buffers. With g' = u_scale * g:
+ *   m = beta1 m + (1 - beta1) g';  v = beta2 v + (1 - beta2) g'^2 (dense), or the factored Rr, Cc of
+ *   bom_update's BOM_V_FACTORED layout over g'^2;
+ *   theta = (1 - lr * omega) theta - lr * (m / (1 - beta1^t)) / (sqrt(v_hat) + eps).
+ * 28 bytes per parameter dense (read theta, m, v, g; write theta, m, v).
+ *
+ *   theta, m, g device fp32 [P] (theta, m in place).   v dense: device fp32 [P]; factored: Rr as in
+ *   bom_update, with v_col = Cc.   segs, nsegs, weight_decay as in bom_update.   beta1 in [0, 1).
+ *   cfg: lr, beta2, eps, u_scale, t, v_layout (BOM_V_DENSE, or BOM_V_FACTORED with block_cols 1024, 2048 or
+ *   4096), block_rows, block_cols; clip_norm must be 0 and state_dt BOM_F32; lambda is not used.
+ *   workspace: at least bom_update_workspace_bytes(P, cfg) bytes (0 for the dense layout).
+ * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_HYPER, BOM_ERR_ALIAS, BOM_ERR_WORKSPACE, BOM_ERR_UNSUPPORTED,
+ *         BOM_ERR_HIP.
+ * ---------------------------------------------------------------------------------------- */
+bom_status bom_adamw_update(float* theta, float* m, float* v, float* v_col, const float* g, int64_t P,
+                            const bom_segment* segs, int32_t nsegs, float weight_decay, float beta1,
+                            const bom_update_cfg* cfg, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------------
  * bom_head_telemetry -- diagnostic beside the four steps (for telemetry steps only): the
  * historical-projection drift of the linear head, Sec. 3.3 Eq. (8) and appendix "Measuring historical
  * projection drift". For z_i = W^T h_i + b the batch-mean Jacobian maps a task-space x to

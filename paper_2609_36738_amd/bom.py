@@ -96,6 +96,9 @@ def load(build_if_missing: bool = True):
         lib.bom_update.restype = ctypes.c_int
         lib.bom_update.argtypes = [vp, vp, vp, vp, vp, i64, ctypes.POINTER(bom_segment), i32, f32,
                                    ctypes.POINTER(bom_update_cfg), vp, sz, vp]
+        lib.bom_adamw_update.restype = ctypes.c_int
+        lib.bom_adamw_update.argtypes = [vp, vp, vp, vp, vp, i64, ctypes.POINTER(bom_segment), i32, f32, f32,
+                                         ctypes.POINTER(bom_update_cfg), vp, sz, vp]
         lib.bom_head_telemetry_workspace_bytes.restype = sz
         lib.bom_head_telemetry_workspace_bytes.argtypes = [i64, i64, i64]
         lib.bom_head_telemetry.restype = ctypes.c_int
@@ -305,6 +308,23 @@ def bom_update(theta, v, u, cfg: bom_update_cfg, *, v_col=None, h=None, segments
     _check(lib.bom_update(_ptr(theta), _ptr(v), _ptr(v_col), _ptr(u), _ptr(h), P, segs, len(segments),
                           float(weight_decay), ctypes.byref(cfg), _ptr(workspace),
                           0 if workspace is None else workspace.numel(), _stream(stream)))
+    return workspace
+
+
+def bom_adamw_update(theta, m, v, g, cfg: bom_update_cfg, *, beta1=0.9, v_col=None, segments=(), weight_decay=0.0,
+                     workspace=None, stream=None):
+    """AdamW (the comparison optimizer) in place: theta, m and v (or the factored Rr = v, Cc = v_col)."""
+    lib = load()
+    P = theta.numel()
+    for name, x in (("theta", theta), ("m", m), ("g", g)) + ((("v", v),) if v_col is None else ()):
+        if x.dtype != torch.float32 or not x.is_contiguous() or x.numel() != P:
+            raise ValueError(f"{name} must be a contiguous float32 tensor of {P} elements")
+    segs = (bom_segment * max(1, len(segments)))(*[bom_segment(int(o), int(n), float(w)) for o, n, w in segments])
+    nb = lib.bom_update_workspace_bytes(P, ctypes.byref(cfg))
+    workspace = _workspace(nb, theta.device, workspace)
+    _check(lib.bom_adamw_update(_ptr(theta), _ptr(m), _ptr(v), _ptr(v_col), _ptr(g), P, segs, len(segments),
+                                float(weight_decay), float(beta1), ctypes.byref(cfg), _ptr(workspace),
+                                0 if workspace is None else workspace.numel(), _stream(stream)))
     return workspace
 
 

@@ -328,6 +328,77 @@ bom_status bom_update(void* theta_p, void* v_p, float* v_col, const void* u_p, c
                       "bom_update");
 }
 
+bom_status bom_adamw_update(float* theta, float* m, float* v, float* v_col, const float* g, int64_t P,
+                            const bom_segment* segs, int32_t nsegs, float weight_decay, float beta1,
+                            const bom_update_cfg* cfg, void* workspace, size_t ws_bytes, void* stream) {
+    if (!theta || !m || !v || !g || !cfg) return fail(BOM_ERR_NULL, "bom_adamw_update: theta, m, v, g and cfg are required");
+    if (P < 1) return fail(BOM_ERR_SHAPE, "bom_adamw_update: need P >= 1");
+    if (nsegs < 0 || nsegs > BOM_MAX_SEGMENTS || (nsegs > 0 && !segs))
+        return fail(BOM_ERR_SHAPE, "bom_adamw_update: need 0 <= nsegs <= %d and segs when nsegs > 0", BOM_MAX_SEGMENTS);
+    const bom_update_cfg& c = *cfg;
+    if (!(beta1 >= 0.f && beta1 < 1.f) || !(c.beta2 >= 0.f && c.beta2 < 1.f) || c.t < 1 || !(c.eps > 0.f) ||
+        !finite(c.eps) || !finite(c.lr) || !finite(c.u_scale) || !finite(weight_decay))
+        return fail(BOM_ERR_HYPER, "bom_adamw_update: need beta1, beta2 in [0,1), t >= 1, eps > 0, finite lr, u_scale "
+                                   "and weight decay");
+    if (c.clip_norm != 0.f || c.state_dt != BOM_F32 || (c.v_layout != BOM_V_DENSE && c.v_layout != BOM_V_FACTORED))
+        return fail(BOM_ERR_UNSUPPORTED, "bom_adamw_update: fp32 state, the dense or factored layout, no clipping");
+    bom::SegTable st{};
+    st.n = nsegs;
+    st.wd_default = weight_decay;
+    for (int k = 0; k < nsegs; ++k) {
+        const bom_segment& sg = segs[k];
+        if (sg.offset < 0 || sg.length < 0 || sg.offset + sg.length > P)
+            return fail(BOM_ERR_SHAPE, "bom_adamw_update: segment %d is outside [0, P)", k);
+        if (!finite(sg.weight_decay)) return fail(BOM_ERR_HYPER, "bom_adamw_update: segment %d decay is not finite", k);
+        st.begin[k] = sg.offset;
+        st.end[k] = sg.offset + sg.length;
+        st.wd[k] = sg.weight_decay;
+    }
+    bom::UpdateScalars sc{};
+    sc.lr = c.lr;
+    sc.beta2 = c.beta2;
+    sc.one_minus_beta2 = (float)(1.0 - (double)c.beta2);
+    sc.eps = c.eps;
+    sc.lambda = 0.f;
+    sc.u_scale = c.u_scale;
+    sc.inv_bc2 = (float)(1.0 / (1.0 - std::pow((double)c.beta2, (double)c.t)));
+    sc.clip_norm = 0.f;
+    sc.clip = nullptr;
+    sc.clip_stats = nullptr;
+    sc.beta1 = beta1;
+    sc.one_minus_beta1 = (float)(1.0 - (double)beta1);
+    sc.inv_bc1 = (float)(1.0 / (1.0 - std::pow((double)beta1, (double)c.t)));
+    const size_t pb = (size_t)P * 4;
+    if (overlap(theta, pb, g, pb) || overlap(m, pb, theta, pb) || overlap(m, pb, g, pb))
+        return fail(BOM_ERR_ALIAS, "bom_adamw_update: theta, m and g must be distinct");
+    hipStream_t strm = static_cast<hipStream_t>(stream);
+    if (c.v_layout == BOM_V_DENSE) {
+        if (v_col) return fail(BOM_ERR_SHAPE, "bom_adamw_update: v_col must be NULL for the dense layout");
+        if (overlap(v, pb, theta, pb) || overlap(v, pb, m, pb) || overlap(v, pb, g, pb))
+            return fail(BOM_ERR_ALIAS, "bom_adamw_update: v must not overlap theta, m or g");
+        return hip_status(bom::launch_adamw_dense(theta, m, v, g, P, st, sc, strm), "bom_adamw_update");
+    }
+    if (!v_col) return fail(BOM_ERR_NULL, "bom_adamw_update: the factored layout needs v_col");
+    if (c.block_rows < 1 || (c.block_cols != 1024 && c.block_cols != 2048 && c.block_cols != 4096))
+        return fail(BOM_ERR_UNSUPPORTED, "bom_adamw_update: factored layout needs block_cols of 1024, 2048 or 4096");
+    auto al = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
+    if (P % 4 != 0 || !al(theta) || !al(m) || !al(g) || !al(v_col))
+        return fail(BOM_ERR_UNSUPPORTED, "bom_adamw_update: factored layout needs P % 4 == 0 and 16-byte aligned arrays");
+    const size_t need = bom::update_workspace_bytes(P, cfg);
+    if (!workspace || ws_bytes < need)
+        return fail(BOM_ERR_WORKSPACE, "bom_adamw_update: workspace needs %zu bytes, got %zu", need, ws_bytes);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+        return fail(BOM_ERR_WORKSPACE, "bom_adamw_update: workspace must be 256-byte aligned");
+    const int64_t nrows = (P + c.block_cols - 1) / c.block_cols;
+    const int64_t nblocks = (nrows + c.block_rows - 1) / c.block_rows;
+    if (overlap(v, (size_t)nrows * 4, v_col, (size_t)nblocks * c.block_cols * 4) || overlap(v, (size_t)nrows * 4, theta, pb) ||
+        overlap(v_col, (size_t)nblocks * c.block_cols * 4, theta, pb))
+        return fail(BOM_ERR_ALIAS, "bom_adamw_update: Rr, Cc and theta must be distinct");
+    return hip_status(bom::launch_adamw_factored(theta, m, v, v_col, g, P, c.block_rows, c.block_cols, st, sc, workspace,
+                                                 strm),
+                      "bom_adamw_update");
+}
+
 size_t bom_head_telemetry_workspace_bytes(int64_t N, int64_t d, int64_t V) {
     if (N < 1 || d < 1 || V < 1 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim) return 0;
     return bom::head_telemetry_workspace_bytes(N, d);

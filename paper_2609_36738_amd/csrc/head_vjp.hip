@@ -735,13 +735,14 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int wm = wave / (NW / 2), wn = wave % (NW / 2);
 
-    const float rv_reg =
-        (RANK1 && part == nullptr && (int)threadIdx.x < LB && m0 + (int)threadIdx.x < M) ? rv[m0 + threadIdx.x] : 0.f;
+    // rank-1 term of the epilogue (none when rv is null: lambda = 0 has no history term)
+    const bool r1 = RANK1 && part == nullptr && rv != nullptr;
+    const float rv_reg = (r1 && (int)threadIdx.x < LB && m0 + (int)threadIdx.x < M) ? rv[m0 + threadIdx.x] : 0.f;
     float cvv[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         const int n = n0 + wn * WCOLS + j * 32 + l % 32;
-        cvv[j] = (RANK1 && part == nullptr && n < Nn) ? cv[n] : 0.f;
+        cvv[j] = (r1 && n < Nn) ? cv[n] : 0.f;
     }
 
     // copy step q (< CPO) of this wave fills kilobyte wave*CPO + q of an operand's stage
@@ -1040,7 +1041,7 @@ __global__ __launch_bounds__(256) void splitk_rank1_kernel(const float* __restri
     const int64_t m = pm0 + idx / Nr, n = pn0 + idx % Nr;
     float a = 0.f;
     for (int z = 0; z < splits; ++z) a += part[(int64_t)z * MN + idx];
-    a = fmaf(rv[m], cv[n], a);
+    if (rv != nullptr) a = fmaf(rv[m], cv[n], a);
     if (beta != 0.f) a += beta * ldf<TO>(out, m * ldo + n);
     stf<TO>(out, m * ldo + n, a);
 }
@@ -1903,9 +1904,11 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
         return hipGetLastError();
     }
 
-    // rank-1 vectors first: u for dH, row-block partial sums of H over I for dW
+    // rank-1 vectors first: u for dH, row-block partial sums of H over I for dW (lambda = 0: no history
+    // term, so neither is needed and the epilogues add nothing)
     hipError_t e;
-    const bool rw = p.w.kind == kRank1, rh = p.h.kind == kRank1;
+    const bool hist = a.lambda != 0.f;
+    const bool rw = p.w.kind == kRank1 && hist, rh = p.h.kind == kRank1 && hist;
     const int nrb = (int)cdiv(a.N, kHsRows);
     if (rw || rh) {
         const int nu = rh ? (int)cdiv(a.d, 4) : 0;
@@ -1937,9 +1940,9 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
         const uint16_t* W16 = static_cast<const uint16_t*>(a.W);
         const TileRange trh{inner, 0, oh, sh, 0, 0, a.d, (int64_t)a.N * a.d};
         const TileRange trw{inner, 0, ow, 1, 0, 0, 0, 0};
-        const WideArgs wh{R16, a.ldr, W16, a.ldw, a.N, a.d, a.V, kps_h, trh, f.scal, vmask, u, a.dH, a.lddh, 0.f,
+        const WideArgs wh{R16, a.ldr, W16, a.ldw, a.N, a.d, a.V, kps_h, trh, f.scal, hist ? vmask : nullptr, u, a.dH, a.lddh, 0.f,
                           sh > 1 ? part : nullptr, nullptr, f.zc, a.labels};
-        const WideArgs ww{H16, a.ldh, R16, a.ldr, a.d, a.V, a.N, kps_w, trw, f.scal, hsum, cq, a.dW, a.lddw,
+        const WideArgs ww{H16, a.ldh, R16, a.ldr, a.d, a.V, a.N, kps_w, trw, f.scal, hist ? hsum : nullptr, cq, a.dW, a.lddw,
                           a.dW_beta, nullptr, nullptr, f.zc, a.labels};
         const int nh = (int)(cdiv((int64_t)oh * sh, 8) * 8 * inner);
         const int nw = (int)(cdiv(ow, 8) * 8 * inner);
@@ -1965,25 +1968,25 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
         const int64_t MN = (int64_t)a.N * a.d;
         if (a.dh_dt == BOM_BF16)
             hipLaunchKernelGGL(splitk_rank1_kernel<uint16_t>, dim3((unsigned)cdiv(MN, 256)), dim3(256), 0, st, part, sh,
-                               a.N, a.d, 0, 0, vmask, u, static_cast<uint16_t*>(a.dH), a.lddh, 0.f);
+                               a.N, a.d, 0, 0, hist ? vmask : nullptr, u, static_cast<uint16_t*>(a.dH), a.lddh, 0.f);
         else
             hipLaunchKernelGGL(splitk_rank1_kernel<float>, dim3((unsigned)cdiv(MN, 256)), dim3(256), 0, st, part, sh, a.N,
-                               a.d, 0, 0, vmask, u, static_cast<float*>(a.dH), a.lddh, 0.f);
+                               a.d, 0, 0, hist ? vmask : nullptr, u, static_cast<float*>(a.dH), a.lddh, 0.f);
         return hipGetLastError();
     }
 
     // dW = H^T G
     e = run_gemm<float>(true, p.w, a.H, a.ldh, a.R, a.ldr, a.dt, a.d, a.V, a.N, f, static_cast<float*>(a.dW), a.lddw,
-                        a.dW_beta, part, hsum, cq,
+                        a.dW_beta, part, hist ? hsum : nullptr, cq,
                         st);
     if (e != hipSuccess) return e;
     // dH = G W^T (shares the split-K buffer: same stream, so it runs after the dW reduction)
     if (a.dH) {
         if (a.dh_dt == BOM_BF16)
             return run_gemm<uint16_t>(false, p.h, a.R, a.ldr, a.W, a.ldw, a.dt, a.N, a.d, a.V, f,
-                                      static_cast<uint16_t*>(a.dH), a.lddh, 0.f, part, vmask, u, st);
+                                      static_cast<uint16_t*>(a.dH), a.lddh, 0.f, part, hist ? vmask : nullptr, u, st);
         return run_gemm<float>(false, p.h, a.R, a.ldr, a.W, a.ldw, a.dt, a.N, a.d, a.V, f, static_cast<float*>(a.dH),
-                               a.lddh, 0.f, part, vmask, u, st);
+                               a.lddh, 0.f, part, hist ? vmask : nullptr, u, st);
     }
     return hipSuccess;
 }

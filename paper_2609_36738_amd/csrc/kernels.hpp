@@ -78,6 +78,7 @@ struct UpdateScalars {
     float clip_norm;      // > 0: global-norm clipping of the numerator
     const float* clip;    // device word with the clipping factor (written on the device), or null
     float* clip_stats;    // optional device [2]: the numerator's norm before clipping and the factor
+    float beta1, one_minus_beta1, inv_bc1;   // AdamW's first moment (the comparison update)
 };
 size_t update_workspace_bytes(int64_t P, const bom_update_cfg* cfg);
 hipError_t launch_update_dense(float* theta, float* v, const float* u, const float* h, int64_t P, const SegTable& segs,
@@ -98,5 +99,12 @@ hipError_t launch_update_blocks(float* theta, float* v, const float* u, const fl
 hipError_t launch_update_factored(float* theta, float* Rr, float* Cc, const float* u, const float* h, int64_t P,
                                   int64_t block_rows, int64_t block_cols, const SegTable& segs,
                                   const UpdateScalars& sc, void* ws, hipStream_t stream);
+// AdamW (the comparison optimizer of the cost model): dense, or with the factored second moment for
+// block_cols of 1024, 2048 or 4096.
+hipError_t launch_adamw_dense(float* theta, float* m, float* v, const float* g, int64_t P, const SegTable& segs,
+                              const UpdateScalars& sc, hipStream_t stream);
+hipError_t launch_adamw_factored(float* theta, float* m, float* Rr, float* Cc, const float* g, int64_t P,
+                                 int64_t block_rows, int64_t block_cols, const SegTable& segs, const UpdateScalars& sc,
+                                 void* ws, hipStream_t stream);
 
 }  // namespace bom

@@ -109,6 +109,65 @@ __global__ __launch_bounds__(kUpdThreads) void update_dense_scalar_kernel(float*
     }
 }
 
+// ---- AdamW (the comparison arm of the cost model) ---------------------------------------------------
+// The dense first moment BOM deletes: m = b1 m + (1 - b1) g, v = b2 v + (1 - b2) g^2,
+// theta = (1 - lr w) theta - lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps); 28 bytes per parameter.
+__device__ __forceinline__ void adamw_step(float& th, float& m, float& v, float g, float wd, const UpdateScalars& sc) {
+    m = sc.beta1 * m + sc.one_minus_beta1 * g;
+    v = sc.beta2 * v + sc.one_minus_beta2 * (g * g);
+    const float vhat = v * sc.inv_bc2;
+    th = (1.0f - sc.lr * wd) * th - sc.lr * ((m * sc.inv_bc1) / (sqrtf(vhat) + sc.eps));
+}
+
+// One launch over [0, P) laid out like update_dense_vec4_kernel: scalar head and tail, 16-byte groups.
+__global__ __launch_bounds__(kUpdThreads) void adamw_dense_vec4_kernel(float* __restrict__ theta, float* __restrict__ m,
+                                                                       float* __restrict__ v, const float* __restrict__ g,
+                                                                       int64_t head, int64_t nvec, int64_t P,
+                                                                       SegTable segs, UpdateScalars sc) {
+    const int64_t q = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x;
+    if (q >= nvec) {
+        const int64_t r = q - nvec;
+        const int64_t e = r < head ? r : head + 4 * nvec + (r - head);
+        if (e >= P) return;
+        float t = theta[e], mm = m[e], vv = v[e];
+        adamw_step(t, mm, vv, sc.u_scale * g[e], decay_of(e, segs), sc);
+        theta[e] = t;
+        m[e] = mm;
+        v[e] = vv;
+        return;
+    }
+    const int64_t e = head + q * 4;
+    f32x4 t4 = ld_stream(theta + e);
+    f32x4 m4 = ld_stream(m + e);
+    f32x4 v4 = ld_stream(v + e);
+    const f32x4 g4 = ld_stream(g + e);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        float th = t4[c], mm = m4[c], vv = v4[c];
+        adamw_step(th, mm, vv, sc.u_scale * g4[c], decay_of(e + c, segs), sc);
+        t4[c] = th;
+        m4[c] = mm;
+        v4[c] = vv;
+    }
+    st_stream(theta + e, t4);
+    st_stream(m + e, m4);
+    st_stream(v + e, v4);
+}
+
+__global__ __launch_bounds__(kUpdThreads) void adamw_dense_scalar_kernel(float* __restrict__ theta, float* __restrict__ m,
+                                                                         float* __restrict__ v,
+                                                                         const float* __restrict__ g, int64_t P,
+                                                                         SegTable segs, UpdateScalars sc) {
+    const int64_t stride = (int64_t)gridDim.x * kUpdThreads;
+    for (int64_t e = (int64_t)blockIdx.x * kUpdThreads + threadIdx.x; e < P; e += stride) {
+        float t = theta[e], mm = m[e], vv = v[e];
+        adamw_step(t, mm, vv, sc.u_scale * g[e], decay_of(e, segs), sc);
+        theta[e] = t;
+        m[e] = mm;
+        v[e] = vv;
+    }
+}
+
 // ---- dense, bf16 storage ------------------------------------------------------------------------
 // theta, v, u (and h) stored as bf16 (10 bytes per parameter, 12 with h); the step is computed in fp32
 // from the widened values and theta and v are rounded to nearest-even bf16 when stored. Eight elements
@@ -367,6 +426,53 @@ __global__ __launch_bounds__(kUpdThreads) void factored_update_rows_kernel(float
 // columns (k*64 + l)*4 .. +3 for k < NV, so each row's loads are all in flight together and the row
 // statistic is one wave reduction. Elements at or past P (only in the last row) count as zero. The
 // statistics read u with non-temporal loads (8B parameters: 5.73 -> 5.22 ms against cached loads).
+// AdamW with the factored second moment (block_cols = NV * 256): the update of factored_update_rows_kernel
+// with the numerator m_hat, m = b1 m + (1 - b1) g read and written in the same pass.
+template <int NV>
+__global__ __launch_bounds__(kUpdThreads) void factored_adamw_rows_kernel(float* __restrict__ theta, float* __restrict__ m,
+                                                                          const float* __restrict__ g, int64_t P,
+                                                                          int64_t block_rows,
+                                                                          const float* __restrict__ Rr,
+                                                                          const float* __restrict__ Cc,
+                                                                          const float* __restrict__ rsum, SegTable segs,
+                                                                          UpdateScalars sc) {
+    constexpr int BC = NV * 256;
+    constexpr int KV = NV / 4;
+    const int64_t i = blockIdx.x;
+    const int64_t b = i / block_rows;
+    const float rs = rsum[b];
+    const float a = rs > 0.f ? Rr[i] / rs * sc.inv_bc2 : 0.f;
+    const float* cb = Cc + b * BC;
+    const int t = threadIdx.x;
+    f32x4 t4[KV], g4[KV], m4[KV], c4[KV];
+#pragma unroll
+    for (int k = 0; k < KV; ++k) {
+        const int j = (k * kUpdThreads + t) * 4;
+        const int64_t e = i * BC + j;
+        const int64_t ec = e < P ? e : P - 4;
+        t4[k] = ld_stream(theta + ec);
+        g4[k] = ld_stream(g + ec);
+        m4[k] = ld_stream(m + ec);
+        c4[k] = *reinterpret_cast<const f32x4*>(cb + j);
+    }
+#pragma unroll
+    for (int k = 0; k < KV; ++k) {
+        const int j = (k * kUpdThreads + t) * 4;
+        const int64_t e = i * BC + j;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float mm = sc.beta1 * m4[k][c] + sc.one_minus_beta1 * (sc.u_scale * g4[k][c]);
+            const float vhat = a * c4[k][c];
+            m4[k][c] = mm;
+            t4[k][c] = (1.0f - sc.lr * decay_of(e + c, segs)) * t4[k][c] - sc.lr * ((mm * sc.inv_bc1) / (sqrtf(vhat) + sc.eps));
+        }
+        if (e < P) {
+            st_stream(theta + e, t4[k]);
+            st_stream(m + e, m4[k]);
+        }
+    }
+}
+
 template <bool SPLIT, int NV>
 __global__ __launch_bounds__(kUpdThreads) void factored_stats_rows_kernel(const float* __restrict__ u,
                                                                           const float* __restrict__ h, int64_t P,
@@ -1100,6 +1206,55 @@ hipError_t launch_update_factored(float* theta, float* Rr, float* Cc, const floa
                                   const UpdateScalars& sc, void* ws, hipStream_t st) {
     if (h) return dispatch_factored<true>(theta, Rr, Cc, u, h, P, block_rows, (int)block_cols, segs, sc, ws, st);
     return dispatch_factored<false>(theta, Rr, Cc, u, h, P, block_rows, (int)block_cols, segs, sc, ws, st);
+}
+
+hipError_t launch_adamw_dense(float* theta, float* m, float* v, const float* g, int64_t P, const SegTable& segs,
+                              const UpdateScalars& sc, hipStream_t st) {
+    int64_t head = common_head({theta, m, v, g}, 4);
+    if (head >= 0) {
+        head = std::min(head, P);
+        const int64_t nvec = (P - head) / 4;
+        const int64_t grid = (nvec + (P - 4 * nvec) + kUpdThreads - 1) / kUpdThreads;
+        hipLaunchKernelGGL(adamw_dense_vec4_kernel, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, m, v, g, head,
+                           nvec, P, segs, sc);
+        return hipGetLastError();
+    }
+    const int64_t grid = std::min<int64_t>((P + kUpdThreads - 1) / kUpdThreads, 8192);
+    hipLaunchKernelGGL(adamw_dense_scalar_kernel, dim3((unsigned)grid), dim3(kUpdThreads), 0, st, theta, m, v, g, P, segs,
+                       sc);
+    return hipGetLastError();
+}
+
+namespace {
+template <int NV>
+hipError_t run_adamw_factored_rows(float* theta, float* m, float* Rr, float* Cc, const float* g, int64_t P, int64_t br,
+                                   const SegTable& segs, const UpdateScalars& sc, void* ws, hipStream_t st) {
+    constexpr int BC = NV * 256;
+    const FacLayout L = fac_layout(P, br, BC, false);
+    float* kpart = reinterpret_cast<float*>(static_cast<char*>(ws) + L.kpart_off);
+    float* rsum = reinterpret_cast<float*>(static_cast<char*>(ws) + L.rsum_off);
+    // the second moment's statistics are those of the factored BOM update with numerator g
+    hipLaunchKernelGGL((factored_stats_rows_kernel<false, NV>), dim3((unsigned)L.ngroups), dim3(kUpdThreads), 0, st, g,
+                       nullptr, P, L.nrows, br, (int)L.groups_per_block, Rr, kpart, nullptr, sc);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int nchunks = (BC + 1023) / 1024;
+    hipLaunchKernelGGL(factored_finish_cols_kernel, dim3((unsigned)(L.nblocks * nchunks)), dim3(kUpdThreads), 0, st,
+                       kpart, (int)L.groups_per_block, L.nrows, br, BC, nchunks, Rr, Cc, rsum, nullptr, sc);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((factored_adamw_rows_kernel<NV>), dim3((unsigned)L.nrows), dim3(kUpdThreads), 0, st, theta, m, g,
+                       P, br, Rr, Cc, rsum, segs, sc);
+    return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_adamw_factored(float* theta, float* m, float* Rr, float* Cc, const float* g, int64_t P,
+                                 int64_t block_rows, int64_t block_cols, const SegTable& segs, const UpdateScalars& sc,
+                                 void* ws, hipStream_t st) {
+    if (block_cols == 4096) return run_adamw_factored_rows<16>(theta, m, Rr, Cc, g, P, block_rows, segs, sc, ws, st);
+    if (block_cols == 2048) return run_adamw_factored_rows<8>(theta, m, Rr, Cc, g, P, block_rows, segs, sc, ws, st);
+    if (block_cols == 1024) return run_adamw_factored_rows<4>(theta, m, Rr, Cc, g, P, block_rows, segs, sc, ws, st);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace bom

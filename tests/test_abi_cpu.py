@@ -214,3 +214,24 @@ def test_residual_noalloc_refuses_beyond_scratch(lib):
     assert st == 5 and b"scratch" in lib.bom_last_error()
     assert lib.bom_residual_noalloc(None, bom.BOM_BF16, 8, 100, 100, FAKE, -100, FAKE, FAKE, None, None, None,
                                     bom.BOM_BF16, 100, FAKE, FAKE, FAKE, None) == 1
+
+
+def _adamw(lib, P=1000, beta1=0.9, v_col=None, ws=None, wsb=0, m=ctypes.c_void_p(0x500000), **cfgkw):
+    c = dict(lr=1e-3, beta2=0.999, eps=1e-8, t=1)
+    c.update(cfgkw)
+    cfg = bom.make_update_cfg(**c)
+    arr = (bom.bom_segment * 1)()
+    return lib.bom_adamw_update(ctypes.c_void_p(0x100000), m, ctypes.c_void_p(0x200000), v_col,
+                                ctypes.c_void_p(0x300000), P, arr, 0, 0.0, beta1, ctypes.byref(cfg), ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(m=None), 1), (dict(P=0), 2), (dict(beta1=1.0), 4), (dict(beta1=-0.5), 4), (dict(t=0), 4),
+    (dict(clip_norm=1.0), 8), (dict(state_dtype=__import__("torch").bfloat16), 8),
+    (dict(v_col=FAKE), 2), (dict(m=ctypes.c_void_p(0x100100)), 6),
+    (dict(factored=True), 1), (dict(factored=True, v_col=ctypes.c_void_p(0x400000), block_cols=512), 8),
+    (dict(factored=True, v_col=ctypes.c_void_p(0x400000), block_cols=1024, P=1002), 8),
+    (dict(factored=True, v_col=ctypes.c_void_p(0x400000), block_cols=1024, P=4096), 5),
+])
+def test_adamw_update_rejects(lib, kw, code):
+    assert _adamw(lib, **kw) == code

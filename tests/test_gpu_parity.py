@@ -258,11 +258,14 @@ ROUND_CASES = [
 # ldr = V + 4 (a leading dimension the MFMA tiles cannot stage): the same shapes on the SIMT kernels, whose
 # own k splits must fit the workspace sized for the shape (regression: they once kept the wide plan's
 # split count and wrote partials for every tile past the workspace).
-@pytest.mark.parametrize("layout", ["dense", "ldr_plus4"])
+# lam0: lambda = 0 (no history term: no rank-1 pre-pass, no rank-1 term in the epilogues or the split-k
+# reduction), the plain cross-entropy backward of the AdamW arm.
+@pytest.mark.parametrize("layout", ["dense", "ldr_plus4", "dense_lam0"])
 @pytest.mark.parametrize("case", ROUND_CASES, ids=[c[0] for c in ROUND_CASES])
 def test_head_vjp_whole_rounds_and_leftovers(case, layout):
     name, N, d, V, cols, rows = case
-    log(f"[head_vjp] {name} N={N} d={d} V={V} R layout {layout}")
+    lam = 0.0 if layout.endswith("lam0") else LAM
+    log(f"[head_vjp] {name} N={N} d={d} V={V} R layout {layout} lambda {lam}")
     Hh, Hd, Wh, Wd, Zh, Zd, y, q_prev, t = _vjp_inputs(N, d, V, "bf16", 0.05)
     yd = torch.from_numpy(y).to(dev())
     R = None
@@ -271,13 +274,13 @@ def test_head_vjp_whole_rounds_and_leftovers(case, layout):
     res = bom.bom_residual(Zd, yd, R=R)
     q = torch.from_numpy(q_prev.copy()).to(dev())
     qh = bom.bom_ema(q, res["s"], B1, t)
-    g = bom.bom_head_vjp(Hd, Wd, res["R"], yd, qh, res["n_valid"], s=res["s"], lam=LAM, want_db=True,
+    g = bom.bom_head_vjp(Hd, Wd, res["R"], yd, qh, res["n_valid"], s=res["s"], lam=lam, want_db=True,
                          dh_dtype=torch.float32)
     torch.cuda.synchronize()
     o = oracle.residual(Zh, y, want_R=False)
     _, qho = oracle.ema(q_prev, o["s"], f32(B1), t)
-    dW = oracle.dW_cols(Hh, Zh, y, o["row_lse"], qho, o["n_valid"], LAM, cols=cols)
-    dH = oracle.dH_rows(Wh, Zh, y, o["row_lse"], qho, o["n_valid"], LAM, rows=rows)
+    dW = oracle.dW_cols(Hh, Zh, y, o["row_lse"], qho, o["n_valid"], lam, cols=cols)
+    dH = oracle.dH_rows(Wh, Zh, y, o["row_lse"], qho, o["n_valid"], lam, rows=rows)
     gdw = to_f64(g["dW"])
     e_dw = rel_fro(gdw[:, cols], dW)
     e_dh = rel_fro(to_f64(g["dH"])[rows], dH)
@@ -858,3 +861,55 @@ def test_head_vjp_from_logits(case):
     # rows outside I contribute nothing: their dH rows are the rank-1 term's zero rows
     bad = np.flatnonzero((y < 0) | (y >= V))
     assert (zh[bad] == 0).all()
+
+
+# ------------------------------------------------------------------------------------------------ AdamW arm
+# The comparison optimizer of the cost model: AdamW with its dense first moment, dense or factored second
+# moment, three steps teacher-forced (each step starts from the GPU's own state).
+@pytest.mark.parametrize("offset", [0, 1], ids=["aligned", "misaligned"])
+def test_adamw_dense_parity(offset):
+    log(f"[adamw dense] offset={offset}")
+    P, lr, b1 = 1_000_003, 1e-3, 0.9
+    segs = [(0, 500_000, 0.01), (500_000, 3, 0.0)]
+    th = synth.normal_f32(P, synth.STREAM_THETA, 0.02)
+    buf = lambda x: torch.from_numpy(np.r_[np.zeros(offset, np.float32), x.astype(np.float32)]).to(dev())[offset:]
+    theta, m, v = buf(th), buf(np.zeros(P)), buf(np.zeros(P))
+    for t in range(1, 4):
+        g = synth.normal_f32(P, synth.STREAM_U + t, 1e-3)
+        th_in, m_in, v_in = to_f64(theta), to_f64(m), to_f64(v)
+        cfg = bom.make_update_cfg(lr=lr, beta2=B2, eps=EPS, t=t, u_scale=0.5)
+        bom.bom_adamw_update(theta, m, v, buf(g), cfg, beta1=b1, segments=segs, weight_decay=0.1)
+        torch.cuda.synchronize()
+        tho, mo, vo = oracle.update_adamw(th_in, m_in, v_in, g, lr=f32(lr), beta1=f32(b1), beta2=f32(B2),
+                                          eps=f32(EPS), t=t, segments=[(a, b_, f32(c)) for a, b_, c in segs],
+                                          weight_decay=f32(0.1), u_scale=0.5)
+        _check_theta(to_f64(theta), tho, lr, f"adamw theta t={t}")
+        # m = b1 m + (1 - b1) g cancels: the bound is relative to the magnitude of its terms
+        scale_m = b1 * np.abs(m_in) + (1 - b1) * 0.5 * np.abs(g.astype(np.float64))
+        assert (np.abs(to_f64(m) - mo) <= 1e-5 * scale_m + 1e-30).all(), f"m t={t}"
+        assert (np.abs(to_f64(v) - vo) <= 1e-5 * vo + 1e-30).all(), f"v t={t}"
+
+
+@pytest.mark.parametrize("bc", [1024, 4096])
+def test_adamw_factored_parity(bc):
+    log(f"[adamw factored] block_cols={bc}")
+    br, lr, b1 = 64, 1e-3, 0.9
+    P = 3 * br * bc + 7 * bc + 1000   # three whole blocks, a short last block, a short last row
+    nrows = -(-P // bc)
+    nblocks = -(-nrows // br)
+    theta = torch.from_numpy(synth.normal_f32(P, synth.STREAM_THETA, 0.02)).to(dev())
+    m = torch.zeros(P, device=dev())
+    Rr, Cc = torch.zeros(nrows, device=dev()), torch.zeros(nblocks * bc, device=dev())
+    for t in range(1, 4):
+        g = synth.normal_f32(P, synth.STREAM_U + t, 1e-3)
+        th_in, m_in, R_in, C_in = to_f64(theta), to_f64(m), to_f64(Rr), to_f64(Cc)
+        cfg = bom.make_update_cfg(lr=lr, beta2=B2, eps=EPS, t=t, factored=True, block_rows=br, block_cols=bc)
+        bom.bom_adamw_update(theta, m, Rr, torch.from_numpy(g).to(dev()), cfg, beta1=b1, v_col=Cc, weight_decay=0.1)
+        torch.cuda.synchronize()
+        tho, mo, Ro, Co = oracle.update_adamw_factored(th_in, m_in, R_in, C_in, g, lr=f32(lr), beta1=f32(b1),
+                                                       beta2=f32(B2), eps=f32(EPS), t=t, block_rows=br,
+                                                       block_cols=bc, weight_decay=f32(0.1))
+        _check_theta(to_f64(theta), tho, lr, f"adamw factored theta t={t}")
+        assert rel_fro(to_f64(Rr), Ro) <= 1e-5 and rel_fro(to_f64(Cc), Co) <= 1e-5
+        scale_m = b1 * np.abs(m_in) + (1 - b1) * np.abs(g.astype(np.float64))
+        assert (np.abs(to_f64(m) - mo) <= 1e-5 * scale_m + 1e-30).all(), f"m t={t}"

@@ -319,6 +319,50 @@ def time_forward(prob, steps):
             "algorithmic_flop": 2 * w.N * w.d * w.V}
 
 
+def time_forward_residual(prob, steps):
+    """The head forward followed by the residual, as two calls (bom_head_forward, bom_residual) and as the
+    fused call (bom_head_forward_residual: row statistics from the forward's epilogue, then one pass over Z
+    for R and s), each timed over `steps` calls into scratch Z and R; inputs H, W, labels of the workload."""
+    w = prob.w
+    W = prob.W if prob.W is not None else prob.theta[: w.d * w.V].view(w.d, w.V)
+    b = None if not w.has_bias else prob.theta[w.d * w.V: w.d * w.V + w.V]
+    Z = torch.empty_like(prob.Z)
+    R = torch.empty_like(prob.Z)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    res, ws = None, None
+
+    def separate():
+        nonlocal res, ws
+        bom.bom_head_forward(prob.H, W, b, Z=Z)
+        res = bom.bom_residual(Z, prob.labels, R=R, workspace=ws,
+                               **({} if res is None else {k: res[k] for k in (
+                                   "s", "row_lse", "row_argmax", "row_target", "loss", "n_valid", "flags")}))
+        ws = res["workspace"]
+
+    out, wsf = None, None
+
+    def fused():
+        nonlocal out, wsf
+        out = bom.bom_head_forward_residual(prob.H, W, prob.labels, b=b, Z=Z, R=R, out=out, workspace=wsf)
+        wsf = out["workspace"]
+
+    times = {}
+    for name, fn in (("separate", separate), ("fused", fused)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        times[name] = e0.elapsed_time(e1) / steps
+    del Z, R, ws, wsf, res, out
+    torch.cuda.empty_cache()
+    return {"separate_ms": round(times["separate"], 5), "fused_ms": round(times["fused"], 5),
+            "saved_ms": round(times["separate"] - times["fused"], 5)}
+
+
 def time_telemetry(prob, steps):
     """Mean time of the drift telemetry call over `steps` calls (M_W, M_b updated each call), and its
     HBM rate against the algorithmic bytes: read R and H, read and write M_W (and M_b)."""
@@ -605,6 +649,8 @@ def run_workload(w, args, cpu_budget, dev):
         out["adamw"]["bom_stages_ms"] = {s: round(stage_ms[s], 5) for s in stages}
     if args.forward:
         out["forward"] = time_forward(prob, args.steps)
+    if args.fused_forward:
+        out["forward_residual"] = time_forward_residual(prob, args.steps)
     if args.telemetry:
         out["telemetry"] = time_telemetry(prob, args.steps)
     del prob
@@ -633,6 +679,9 @@ def main():
     ap.add_argument("--forward", action="store_true",
                     help="also time the head forward Z = H W that produces the logits (common work, outside the "
                          "step) against the MFMA roofline")
+    ap.add_argument("--fused-forward", action="store_true",
+                    help="also time the head forward plus the residual as two calls and as the fused call with the "
+                         "row statistics from the forward's epilogue (common work plus the residual, outside the step)")
     ap.add_argument("--telemetry", action="store_true",
                     help="also time the head drift telemetry call (a diagnostic for telemetry steps, outside the "
                          "step) on the last step's residual, history and features")

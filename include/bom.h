@@ -339,6 +339,31 @@ bom_status bom_head_telemetry(const void* H, int64_t ldh, bom_dtype h_dt, const 
 bom_status bom_head_forward(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
                             int64_t N, int64_t d, int64_t V, void* Z, int64_t ldz, void* stream);
 
+/* ------------------------------------------------------------------------------------------
+ * bom_head_forward_residual -- the head forward and bom_residual in one call (appendix "First-order cost
+ * accounting": the output-side work over N_out = N V coordinates is where BOM's bookkeeping sits).
+ * Computes Z = H W (+ b) as bom_head_forward does and then every output of bom_residual on that Z.
+ * For bf16 on the matrix cores (d and V multiples of 8, 16-byte aligned H, W, Z and R with leading
+ * dimensions that are multiples of 8) the forward's epilogue also reduces each 256-column tile of every
+ * row of the rounded logits (maximum, first column reaching it, sum of exp(z - max)) and records the
+ * target logit, so the residual only merges those records per row and re-reads Z once for R and the
+ * column sums: no row is split across workgroups and no row statistics pass is made over Z. Other shapes
+ * and fp32 run the forward, then bom_residual.
+ *
+ *   H, ldh, W, ldw, b, dt, N, d, V, Z, ldz: as bom_head_forward (Z is written).
+ *   labels, ignore_index, s, row_lse, row_argmax (nullable), row_target (required here), R (nullable), ldr,
+ *   loss, n_valid, flags: as bom_residual (r_dt = dt).
+ *   workspace: at least bom_head_forward_residual_workspace_bytes(N, V, dt) bytes, 256-byte aligned.
+ * Errors: BOM_ERR_NULL, BOM_ERR_SHAPE, BOM_ERR_DTYPE, BOM_ERR_WORKSPACE, BOM_ERR_ALIAS, BOM_ERR_HIP.
+ * ---------------------------------------------------------------------------------------- */
+size_t bom_head_forward_residual_workspace_bytes(int64_t N, int64_t V, bom_dtype dt);
+bom_status bom_head_forward_residual(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b,
+                                     bom_dtype dt, int64_t N, int64_t d, int64_t V, void* Z, int64_t ldz,
+                                     const int32_t* labels, int32_t ignore_index,
+                                     float* s, float* row_lse, int32_t* row_argmax, float* row_target,
+                                     void* R, int64_t ldr, float* loss, int32_t* n_valid, int32_t* flags,
+                                     void* workspace, size_t ws_bytes, void* stream);
+
 /* Environment variables, each read once per process on first use (for measurement and tests; results do
  * not depend on them beyond rounding order):
  *   BOM_VJP_WAVES = "dH,dW,fwd,pair"  waves per workgroup (4 or 8) of the 256-tile products; default 8,8,8,8.

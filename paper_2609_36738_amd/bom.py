@@ -104,6 +104,11 @@ def load(build_if_missing: bool = True):
         lib.bom_head_telemetry.restype = ctypes.c_int
         lib.bom_head_telemetry.argtypes = [vp, i64, ctypes.c_int, vp, i64, ctypes.c_int, i64, i64, i64, vp, i32, vp, vp,
                                            vp, vp, i64, vp, f32, i64, vp, vp, sz, vp]
+        lib.bom_head_forward_residual_workspace_bytes.restype = sz
+        lib.bom_head_forward_residual_workspace_bytes.argtypes = [i64, i64, ctypes.c_int]
+        lib.bom_head_forward_residual.restype = ctypes.c_int
+        lib.bom_head_forward_residual.argtypes = [vp, i64, vp, i64, vp, ctypes.c_int, i64, i64, i64, vp, i64, vp, i32,
+                                                  vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, sz, vp]
         lib.bom_head_forward.restype = ctypes.c_int
         lib.bom_head_forward.argtypes = [vp, i64, vp, i64, vp, ctypes.c_int, i64, i64, i64, vp, i64, vp]
         _lib = lib
@@ -359,3 +364,33 @@ def bom_head_forward(H, W, b=None, Z=None, stream=None):
     _check(lib.bom_head_forward(_ptr(H), _rowmajor(H, "H"), _ptr(W), _rowmajor(W, "W"), _ptr(b), _dtype_code(H), N, d,
                                 V, _ptr(Z), _rowmajor(Z, "Z"), _stream(stream)))
     return Z
+
+
+def bom_head_forward_residual(H, W, labels, *, b=None, Z=None, ignore_index=-100, R=None, write_R=True, out=None,
+                              workspace=None, stream=None) -> dict:
+    """Z = H W (+ b) and the residual outputs of bom_residual on it, in one call (the forward's epilogue
+    reduces each row's tiles on the matrix-core path). out: a dict of preallocated outputs to reuse."""
+    lib = load()
+    N, d = H.shape
+    V = W.shape[1]
+    dev = H.device
+    dt = _dtype_code(H)
+    o = dict(out or {})
+    Z = Z if Z is not None else o.get("Z", torch.empty((N, V), dtype=H.dtype, device=dev))
+    if R is None and write_R:
+        R = o.get("R", torch.empty((N, V), dtype=H.dtype, device=dev))
+    res = dict(Z=Z, R=R)
+    for k, shape, dtype in (("s", (V,), torch.float32), ("row_lse", (N,), torch.float32),
+                            ("row_argmax", (N,), torch.int32), ("row_target", (N,), torch.float32),
+                            ("loss", (1,), torch.float32), ("n_valid", (1,), torch.int32), ("flags", (1,), torch.int32)):
+        res[k] = o.get(k, torch.empty(shape, dtype=dtype, device=dev))
+    nb = lib.bom_head_forward_residual_workspace_bytes(N, V, dt)
+    workspace = _workspace(nb, dev, workspace)
+    _check(lib.bom_head_forward_residual(_ptr(H), _rowmajor(H, "H"), _ptr(W), _rowmajor(W, "W"), _ptr(b), dt, N, d, V,
+                                         _ptr(Z), _rowmajor(Z, "Z"), _ptr(labels), ignore_index, _ptr(res["s"]),
+                                         _ptr(res["row_lse"]), _ptr(res["row_argmax"]), _ptr(res["row_target"]), _ptr(R),
+                                         _rowmajor(R, "R") if R is not None else V, _ptr(res["loss"]),
+                                         _ptr(res["n_valid"]), _ptr(res["flags"]), _ptr(workspace),
+                                         0 if workspace is None else workspace.numel(), _stream(stream)))
+    res["workspace"] = workspace
+    return res

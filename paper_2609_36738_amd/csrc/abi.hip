@@ -399,6 +399,55 @@ bom_status bom_adamw_update(float* theta, float* m, float* v, float* v_col, cons
                       "bom_adamw_update");
 }
 
+size_t bom_head_forward_residual_workspace_bytes(int64_t N, int64_t V, bom_dtype dt) {
+    if (N < 1 || V < 2 || N >= kMaxDim || V >= kMaxDim || !is_dtype(dt)) return 0;
+    const size_t a = bom::residual_from_stats_workspace_bytes(N, V), b = bom::residual_workspace_bytes(N, V, dt);
+    return a > b ? a : b;
+}
+
+bom_status bom_head_forward_residual(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
+                                     int64_t N, int64_t d, int64_t V, void* Z, int64_t ldz, const int32_t* labels,
+                                     int32_t ignore_index, float* s, float* row_lse, int32_t* row_argmax,
+                                     float* row_target, void* R, int64_t ldr, float* loss, int32_t* n_valid,
+                                     int32_t* flags, void* workspace, size_t ws_bytes, void* stream) {
+    if (!H || !W || !Z || !labels || !s || !row_lse || !row_target || !loss || !n_valid || !flags)
+        return fail(BOM_ERR_NULL, "bom_head_forward_residual: H, W, Z, labels, s, row_lse, row_target, loss, n_valid "
+                                  "and flags are required");
+    if (N < 1 || d < 1 || V < 2 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim)
+        return fail(BOM_ERR_SHAPE, "bom_head_forward_residual: need N >= 1, d >= 1, V >= 2, all < 2^31");
+    if (ldh < d || ldw < V || ldz < V || (R && ldr < V))
+        return fail(BOM_ERR_SHAPE, "bom_head_forward_residual: a leading dimension is smaller than its row length");
+    if (!is_dtype(dt)) return fail(BOM_ERR_DTYPE, "bom_head_forward_residual: dt must be BOM_F32 or BOM_BF16");
+    const size_t need = bom_head_forward_residual_workspace_bytes(N, V, dt);
+    if (!workspace || ws_bytes < need)
+        return fail(BOM_ERR_WORKSPACE, "bom_head_forward_residual: workspace needs %zu bytes, got %zu", need, ws_bytes);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+        return fail(BOM_ERR_WORKSPACE, "bom_head_forward_residual: workspace must be 256-byte aligned");
+    const size_t esz = dt == BOM_BF16 ? 2 : 4;
+    const size_t zb = (size_t)((N - 1) * ldz + V) * esz;
+    if ((R && overlap(R, (size_t)((N - 1) * ldr + V) * esz, Z, zb)) || overlap(Z, zb, H, (size_t)((N - 1) * ldh + d) * esz) ||
+        overlap(Z, zb, W, (size_t)((d - 1) * ldw + V) * esz))
+        return fail(BOM_ERR_ALIAS, "bom_head_forward_residual: Z must not overlap H, W or R");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool r_ok = R == nullptr || (reinterpret_cast<uintptr_t>(R) % 16 == 0 && ldr % 8 == 0);
+    if (dt == BOM_BF16 && r_ok && bom::head_forward_stats_supported(H, ldh, W, ldw, Z, ldz, (int)N, (int)d, (int)V)) {
+        hipError_t e = bom::launch_head_forward_stats(H, ldh, W, ldw, b, (int)N, (int)d, (int)V, Z, ldz, labels,
+                                                      ignore_index, static_cast<float*>(workspace), row_target, st);
+        if (e != hipSuccess) return hip_status(e, "bom_head_forward_residual (forward)");
+        return hip_status(bom::launch_residual_from_stats(static_cast<const uint16_t*>(Z), ldz, (int)N, (int)V, labels,
+                                                          ignore_index, s, row_lse, row_argmax, row_target,
+                                                          static_cast<uint16_t*>(R), ldr, loss, n_valid, flags,
+                                                          workspace, st),
+                          "bom_head_forward_residual (residual)");
+    }
+    // other shapes and fp32: the forward, then the residual on its logits
+    hipError_t e = bom::launch_head_forward(H, ldh, W, ldw, b, dt, (int)N, (int)d, (int)V, Z, ldz, st);
+    if (e != hipSuccess) return hip_status(e, "bom_head_forward_residual (forward)");
+    return hip_status(bom::launch_residual(Z, dt, (int)N, (int)V, ldz, labels, ignore_index, s, row_lse, row_argmax,
+                                           row_target, R, ldr, loss, n_valid, flags, workspace, st),
+                      "bom_head_forward_residual (residual)");
+}
+
 size_t bom_head_telemetry_workspace_bytes(int64_t N, int64_t d, int64_t V) {
     if (N < 1 || d < 1 || V < 1 || N >= kMaxDim || d >= kMaxDim || V >= kMaxDim) return 0;
     return bom::head_telemetry_workspace_bytes(N, d);

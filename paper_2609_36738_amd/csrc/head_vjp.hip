@@ -683,6 +683,13 @@ struct WideArgs {
     const uint16_t* bias;   // forward: bf16 bias [Nn] or null
     const float* zc;        // logits input (ZR): c_i per row of R, and the labels
     const int32_t* labels;
+    // forward with row statistics: per (row, 256-column tile) records (max, sum of exp(z - max), first
+    // argmax) of the rounded logits at stats + (row * stats_ld + tile) * 3, and the target logit of each
+    // row whose label is valid (written by the tile that holds the label)
+    float* stats;
+    int64_t stats_ld;
+    int32_t ignore_index;
+    float* row_target;
 };
 
 // Products of the 64-deep kernel: C = A B with
@@ -969,10 +976,86 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
     };
     if constexpr (MODE == kWideFWD) {
         const uint16_t* __restrict__ bias = args.bias;
-        for_each_acc([&](int r, int c, int, float v) {
-            const int m = m0 + r, n = n0 + c;
-            if (m < M && n < Nn) stf<TO>(out, (int64_t)m * ldo + n, bias ? v + bf16_to_f32(bias[n]) : v);
-        });
+        if (args.stats == nullptr) {
+            for_each_acc([&](int r, int c, int, float v) {
+                const int m = m0 + r, n = n0 + c;
+                if (m < M && n < Nn) stf<TO>(out, (int64_t)m * ldo + n, bias ? v + bf16_to_f32(bias[n]) : v);
+            });
+            return;
+        }
+        if constexpr (std::is_same<TO, uint16_t>::value) {
+            // row statistics: the rounded tile goes to LDS (the operand stages are free after the k loop:
+            // 256 rows of 512 bytes), then two threads per row store it with 16-byte writes and reduce
+            // their 128 columns (maximum, first column reaching it, sum of exp(z - max)); the pair's
+            // records are merged and the row's record for this tile is written
+            // 16-byte chunk c8 of row r sits at chunk c8 ^ (r % 32): the two threads of each row read
+            // 32 different chunk positions across a wave, so the reads are free of bank conflicts
+            uint16_t* zt = &lds[0][0][0];
+            auto zpos = [](int r, int c) { return r * LB + ((((c >> 3) ^ (r & 31))) << 3) + (c & 7); };
+            for_each_acc([&](int r, int c, int, float v) {
+                const float x = bias && n0 + c < Nn ? v + bf16_to_f32(bias[n0 + c]) : v;
+                zt[zpos(r, c)] = f32_to_bf16(x);
+            });
+            __syncthreads();
+            const int t = threadIdx.x;
+            for (int rr = t / 2; rr < LB; rr += NW * 32) {
+                const int h = t % 2;
+                const int m = m0 + rr;
+                const int ncol = min(128, Nn - n0 - h * 128);   // columns of this half inside the matrix
+                // pass 1: store the chunks, maximum and its first column (columns past the matrix: -inf)
+                float mx = -INFINITY;
+                int am = 0;
+                uint4 wk[16];
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const int c = h * 128 + q * 8;
+                    wk[q] = *reinterpret_cast<const uint4*>(zt + zpos(rr, c));
+                    if (m < M && q * 8 < ncol)
+                        *reinterpret_cast<uint4*>(static_cast<uint16_t*>(args.out) + (int64_t)m * ldo + n0 + c) = wk[q];
+                    const uint32_t ww[4] = {wk[q].x, wk[q].y, wk[q].z, wk[q].w};
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const float x = q * 8 + k < ncol ? ((k & 1) ? bf16_hi(ww[k / 2]) : bf16_lo(ww[k / 2])) : -INFINITY;
+                        am = x > mx ? c + k : am;
+                        mx = fmaxf(mx, x);
+                    }
+                }
+                am += n0;
+                // pass 2: sum of exp(z - max) (padding contributes 0)
+                const float mx2 = mx * kLog2e;
+                float sum = 0.f;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const uint32_t ww[4] = {wk[q].x, wk[q].y, wk[q].z, wk[q].w};
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const float x = q * 8 + k < ncol ? ((k & 1) ? bf16_hi(ww[k / 2]) : bf16_lo(ww[k / 2])) : -INFINITY;
+                        sum += exp2_fast(fmaf(x, kLog2e, -mx2));
+                    }
+                }
+                // merge with the other half of the row (lane t ^ 1); the lower columns win ties
+                const float mo = __shfl_xor(mx, 1, kWave), so = __shfl_xor(sum, 1, kWave);
+                const int ao = __shfl_xor(am, 1, kWave);
+                if (h == 0 && m < M) {
+                    float M2 = mx, S2 = sum;
+                    int A2 = am;
+                    if (mo > mx) {
+                        S2 = (mx == -INFINITY ? 0.f : sum * exp2_fast((mx - mo) * kLog2e)) + so;
+                        M2 = mo;
+                        A2 = ao;
+                    } else if (mo != -INFINITY) {
+                        S2 = sum + so * exp2_fast((mo - mx) * kLog2e);
+                    }
+                    float* rec = args.stats + ((int64_t)m * args.stats_ld + tn) * 3;
+                    rec[0] = M2;
+                    rec[1] = S2;
+                    rec[2] = __int_as_float(A2);
+                    const int y = args.labels[m];
+                    if (y != args.ignore_index && y >= n0 && y < n0 + LB && y < Nn)
+                        args.row_target[m] = bf16_to_f32(zt[zpos(rr, y - n0)]);
+                }
+            }
+        }
         return;
     }
     const float alpha = *alpha_p;
@@ -2066,6 +2149,31 @@ hipError_t launch_head_forward(const void* H, int64_t ldh, const void* W, int64_
     dim3 grid((V + SB - 1) / SB, (N + SB - 1) / SB);
     hipLaunchKernelGGL(head_forward_simt_kernel<uint16_t>, grid, dim3(256), 0, st, H16, ldh, W16, ldw, b16, N, d, V,
                        static_cast<uint16_t*>(Z), ldz);
+    return hipGetLastError();
+}
+
+bool head_forward_stats_supported(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* Z, int64_t ldz,
+                                  int N, int d, int V) {
+    auto al = [](const void* ptr, int64_t ld) { return reinterpret_cast<uintptr_t>(ptr) % 16 == 0 && ld % 8 == 0; };
+    return d % 8 == 0 && V % 8 == 0 && al(H, ldh) && al(W, ldw) && al(Z, ldz) &&
+           ((int64_t)(N - 1) * ldh + d) * 2 < (1LL << 31) && ((int64_t)(d - 1) * ldw + V) * 2 < (1LL << 31);
+}
+
+hipError_t launch_head_forward_stats(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, int N, int d,
+                                     int V, void* Z, int64_t ldz, const int32_t* labels, int32_t ignore_index,
+                                     float* stats, float* row_target, hipStream_t st) {
+    if (!head_forward_stats_supported(H, ldh, W, ldw, Z, ldz, N, d, V)) return hipErrorInvalidValue;
+    const int MT = (int)cdiv(N, LB), NT = (int)cdiv(V, LB);
+    const TileRange tr{MT, 0, NT, 1, 0, 0, 0, 0};
+    WideArgs wa{static_cast<const uint16_t*>(H), ldh, static_cast<const uint16_t*>(W), ldw, N, V, d,
+                (int)(cdiv(d, WKT) * WKT), tr, nullptr, nullptr, nullptr, Z, ldz, 0.f, nullptr,
+                static_cast<const uint16_t*>(b)};
+    wa.stats = stats;
+    wa.stats_ld = NT;
+    wa.labels = labels;
+    wa.ignore_index = ignore_index;
+    wa.row_target = row_target;
+    hipLaunchKernelGGL((lds256w_fwd_kernel<uint16_t, 8>), dim3((unsigned)(cdiv(NT, 8) * 8 * MT)), dim3(512), 0, st, wa);
     return hipGetLastError();
 }
 

@@ -65,6 +65,22 @@ hipError_t launch_head_telemetry(const TeleArgs& a, hipStream_t stream);
 hipError_t launch_head_forward(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, bom_dtype dt,
                                int N, int d, int V, void* Z, int64_t ldz, hipStream_t stream);
 
+// ---- head forward with row statistics, then the residual from them --------------------------------
+// The forward on the 256-tile MFMA kernel also writes, per row and 256-column tile, (max, sum of
+// exp(z - max), first argmax) of the rounded logits ([N][ceil(V/256)][3] floats) and the target logit of
+// each row whose label is valid. Unsupported shapes (see head_forward_stats_supported) return
+// hipErrorInvalidValue.
+bool head_forward_stats_supported(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* Z, int64_t ldz,
+                                  int N, int d, int V);
+hipError_t launch_head_forward_stats(const void* H, int64_t ldh, const void* W, int64_t ldw, const void* b, int N, int d,
+                                     int V, void* Z, int64_t ldz, const int32_t* labels, int32_t ignore_index,
+                                     float* stats, float* row_target, hipStream_t stream);
+size_t residual_from_stats_workspace_bytes(int64_t N, int64_t V);
+hipError_t launch_residual_from_stats(const uint16_t* Z, int64_t ldz, int N, int V, const int32_t* labels,
+                                      int32_t ignore_index, float* s, float* row_lse, int32_t* row_argmax,
+                                      float* row_target, uint16_t* R, int64_t ldr, float* loss, int32_t* n_valid,
+                                      int32_t* flags, void* ws, hipStream_t stream);
+
 // ---- update ----------------------------------------------------------------------------------
 struct SegTable {
     int n;

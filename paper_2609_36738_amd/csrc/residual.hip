@@ -1328,6 +1328,104 @@ hipError_t run_residual(const T* Z, int N, int V, int64_t ldz, const int32_t* la
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------------------------
+// Residual from the forward's row statistics: the head forward's epilogue already reduced each 256-column
+// tile of every row (max, sum of exp(z - max), first argmax), so one wave per row merges the row's tile
+// records in a fixed order (lane t takes tiles t, t + 64, ...; then a butterfly with the same tie rule as
+// residual_stats_kernel: the lower column wins equal maxima) into lse and argmax, and forms the row's
+// count and loss term with the target logit the forward wrote. The column-slab kernel then re-reads Z
+// once for R and the column sums: no row is shared between workgroups, so nothing is exchanged.
+__global__ __launch_bounds__(kStatsRowsPerWG * kWave) void residual_combine_kernel(
+    const float* __restrict__ stats, int nT, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
+    float* __restrict__ row_lse, int32_t* __restrict__ row_argmax, float* __restrict__ row_target, Partials ws) {
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int i = blockIdx.x * kStatsRowsPerWG + wave;
+    float m = -INFINITY, l = 0.f;
+    int idx = INT_MAX;
+    if (i < N) {
+        const float* rec = stats + (int64_t)i * nT * 3;
+        for (int t = lane; t < nT; t += kWave) {
+            const float mt = rec[t * 3], lt = rec[t * 3 + 1];
+            const int at = __float_as_int(rec[t * 3 + 2]);
+            if (mt > m) {
+                l = (m == -INFINITY ? 0.f : l * exp2_fast((m - mt) * kLog2e)) + lt;
+                m = mt;
+                idx = at;
+            } else {
+                l += lt * exp2_fast((mt - m) * kLog2e);
+                if (mt == m) idx = min(idx, at);
+            }
+        }
+    }
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const float mo = __shfl_xor(m, o, kWave);
+        const float lo = __shfl_xor(l, o, kWave);
+        const int io = __shfl_xor(idx, o, kWave);
+        const float mn = fmaxf(m, mo);
+        const float a = (m == -INFINITY) ? 0.f : l * exp2_fast((m - mn) * kLog2e);
+        const float b = (mo == -INFINITY) ? 0.f : lo * exp2_fast((mo - mn) * kLog2e);
+        l = a + b;
+        idx = (m > mo) ? idx : (mo > m ? io : min(idx, io));
+        m = mn;
+    }
+    __shared__ int sh_cnt[kStatsRowsPerWG];
+    __shared__ int sh_bad[kStatsRowsPerWG];
+    __shared__ double sh_ce[kStatsRowsPerWG];
+    if (lane == 0) {
+        int c = 0, bd = 0;
+        double e = 0.0;
+        if (i < N) {
+            const float lse = m + logf(l);
+            bool rbad = false;
+            const bool valid = label_valid(labels[i], V, ignore_index, &rbad);
+            const float zt = valid ? row_target[i] : 0.f;   // the forward wrote the valid rows' targets
+            row_lse[i] = lse;
+            if (row_argmax) row_argmax[i] = idx;
+            row_target[i] = zt;
+            c = valid ? 1 : 0;
+            bd = rbad ? 1 : 0;
+            e = valid ? (double)lse - (double)zt : 0.0;
+        }
+        sh_cnt[wave] = c;
+        sh_bad[wave] = bd;
+        sh_ce[wave] = e;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int c = 0, bd = 0;
+        double e = 0.0;
+        for (int w = 0; w < kStatsRowsPerWG; ++w) {
+            c += sh_cnt[w];
+            bd |= sh_bad[w];
+            e += sh_ce[w];
+        }
+        ws.wg_count[blockIdx.x] = c;
+        ws.wg_loss[blockIdx.x] = e;
+        ws.wg_flags[blockIdx.x] = bd ? BOM_FLAG_LABEL_RANGE : 0;
+    }
+}
+
+struct StatsLayout {
+    size_t stats_off, part_off, count_off, flags_off, loss_off, total;
+    int nT, rb, nparts, nwg;
+};
+
+StatsLayout stats_layout(int64_t N, int64_t V) {
+    StatsLayout L;
+    L.nT = (int)((V + 255) / 256);
+    L.rb = cols_row_block(N, V, 8);
+    L.nparts = (int)((N + L.rb - 1) / L.rb);
+    L.nwg = (int)((N + kStatsRowsPerWG - 1) / kStatsRowsPerWG);
+    L.stats_off = 0;
+    L.part_off = align256((size_t)N * L.nT * 3 * sizeof(float));
+    L.count_off = align256(L.part_off + (size_t)L.nparts * V * sizeof(float));
+    L.flags_off = align256(L.count_off + (size_t)L.nwg * sizeof(int));
+    L.loss_off = align256(L.flags_off + (size_t)L.nwg * sizeof(int));
+    L.total = align256(L.loss_off + (size_t)L.nwg * sizeof(double));
+    return L;
+}
+
 }  // namespace
 
 size_t residual_workspace_bytes(int64_t N, int64_t V, bom_dtype) { return ws_layout(N, V).total; }
@@ -1389,6 +1487,32 @@ hipError_t residual_scratch(void** ptr) {
     }
     *ptr = g_scratch_ptr[dev];
     return hipSuccess;
+}
+
+size_t residual_from_stats_workspace_bytes(int64_t N, int64_t V) { return stats_layout(N, V).total; }
+
+// The row-statistics records live at the start of the workspace (written by launch_head_forward_stats).
+hipError_t launch_residual_from_stats(const uint16_t* Z, int64_t ldz, int N, int V, const int32_t* labels,
+                                      int32_t ignore_index, float* s, float* row_lse, int32_t* row_argmax,
+                                      float* row_target, uint16_t* R, int64_t ldr, float* loss, int32_t* n_valid,
+                                      int32_t* flags, void* wsp, hipStream_t st) {
+    const StatsLayout L = stats_layout(N, V);
+    char* base = static_cast<char*>(wsp);
+    Partials ws{reinterpret_cast<float*>(base + L.part_off), reinterpret_cast<int*>(base + L.count_off),
+                reinterpret_cast<int*>(base + L.flags_off), reinterpret_cast<double*>(base + L.loss_off), nullptr};
+    hipLaunchKernelGGL(residual_combine_kernel, dim3((unsigned)L.nwg), dim3(kStatsRowsPerWG * kWave), 0, st,
+                       reinterpret_cast<const float*>(base + L.stats_off), L.nT, N, V, labels, ignore_index, row_lse,
+                       row_argmax, row_target, ws);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int slab = kColsThreads * kColsCPT * 8;
+    dim3 grid((unsigned)(((V + slab - 1) / slab) * L.nparts));
+    hipLaunchKernelGGL((residual_cols_kernel<uint16_t, 8>), grid, dim3(kColsThreads), 0, st, Z, ldz, N, V, labels,
+                       ignore_index, row_lse, R, ldr, L.rb, ws.part);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(residual_finish_kernel, dim3((V + kWave - 1) / kWave), dim3(kFinThreads), 0, st, L.nparts, V, L.nwg,
+                       ws, s, loss, n_valid, flags);
+    return hipGetLastError();
 }
 
 }  // namespace bom

@@ -913,3 +913,63 @@ def test_adamw_factored_parity(bc):
         assert rel_fro(to_f64(Rr), Ro) <= 1e-5 and rel_fro(to_f64(Cc), Co) <= 1e-5
         scale_m = b1 * np.abs(m_in) + (1 - b1) * np.abs(g.astype(np.float64))
         assert (np.abs(to_f64(m) - mo) <= 1e-5 * scale_m + 1e-30).all(), f"m t={t}"
+
+
+# ------------------------------------------------------------------------------------------------ forward + residual
+# bom_head_forward_residual: Z = H W (+ b), then the residual of that Z, with the row statistics reduced in
+# the forward's epilogue (per 256-column tile) on the matrix-core path. Z must equal bom_head_forward's
+# bitwise; every residual output is checked against the oracle on the GPU's own Z, and the integer outputs
+# against bom_residual on it.
+FWD_RES_CASES = [
+    # name, N, d, V, dtype, bias, ignore_frac, out-of-range labels
+    ("bf16_ragged_tiles", 300, 136, 1000, "bf16", True, 0.05, 2),
+    ("bf16_lm_32k", 512, 768, 32000, "bf16", False, 0.05, 2),
+    ("bf16_v128k", 64, 256, 128256, "bf16", False, 0.0, 0),
+    ("bf16_unaligned_v", 200, 64, 333, "bf16", False, 0.05, 2),
+    ("f32_tiny", 256, 128, 10, "f32", True, 0.0, 0),
+]
+
+
+@pytest.mark.parametrize("case", FWD_RES_CASES, ids=[c[0] for c in FWD_RES_CASES])
+def test_head_forward_residual_parity(case):
+    name, N, d, V, dtype, with_bias, ign, noor = case
+    log(f"[forward+residual] {name} N={N} d={d} V={V} {dtype} bias={with_bias}")
+    Hh, Hd = gen_matrix(N, d, synth.STREAM_H, 1.0, dtype)
+    Wh, Wd = gen_matrix(d, V, synth.STREAM_W, 0.02, dtype)
+    bd = None
+    if with_bias:
+        _, bd = gen_matrix(1, V, synth.STREAM_THETA, 0.5, dtype)
+        bd = bd.reshape(V)
+    y = gen_labels(N, V, "zipf" if V > 1000 else "uniform", ign, noor)
+    yd = torch.from_numpy(y).to(dev())
+    out = bom.bom_head_forward_residual(Hd, Wd, yd, b=bd)
+    Zref = bom.bom_head_forward(Hd, Wd, bd)
+    torch.cuda.synchronize()
+    Zg = out["Z"]
+    zb = lambda t: t.view(torch.int16).cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy().view(np.int32)
+    assert np.array_equal(zb(Zg), zb(Zref)), f"{name}: Z differs from bom_head_forward"
+    Zh = to_f64(Zg)
+    o = oracle.residual(Zh, y)
+    _compare_residual(name, Zh, y, out, o, dtype)
+    ref = bom.bom_residual(Zg, yd)
+    torch.cuda.synchronize()
+    for k in ("row_argmax", "n_valid", "flags"):
+        assert torch.equal(out[k], ref[k]), k
+    assert torch.equal(out["row_target"], ref["row_target"])
+
+
+def test_head_forward_residual_argmax_ties_across_tiles():
+    # H = 0: every row of Z is the bias; its maximum sits at columns 700 and 5 (tiles 2 and 0) and twice in
+    # tile 1: the first column (5) must win, as the oracle's lowest-index rule says
+    N, d, V = 64, 64, 1024
+    Hd = torch.zeros((N, d), dtype=torch.bfloat16, device=dev())
+    Wd = torch.zeros((d, V), dtype=torch.bfloat16, device=dev())
+    b = torch.full((V,), -1.0, dtype=torch.float32)
+    b[[700, 5, 300, 301]] = 2.0
+    bd = b.to(torch.bfloat16).to(dev())
+    y = gen_labels(N, V, "uniform")
+    out = bom.bom_head_forward_residual(Hd, Wd, torch.from_numpy(y).to(dev()), b=bd)
+    torch.cuda.synchronize()
+    assert (out["row_argmax"].cpu().numpy() == 5).all()
+    Zh = to_f64(out["Z"])
+    _compare_residual("ties", Zh, y, out, oracle.residual(Zh, y), "bf16")

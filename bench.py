@@ -231,6 +231,30 @@ class Problem:
             ev[4].record()
 
 
+def time_graph(prob, args, t):
+    """One step captured in a HIP graph (the library's launches on torch's capture stream) and replayed
+    `steps` times: the step without the host's launch overhead (a replay repeats the captured step counter,
+    whose bias corrections are kernel arguments, so this times the same work, not the same trajectory)."""
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        prob.step(t + 1)
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    del g
+    log(f"[bench] {prob.w.name}: graph replay {ms:.4f} ms/step")
+    return {"ms_per_step": round(ms, 5), "us_per_step": round(ms * 1e3, 2),
+            "value": round(int(prob.res["n_valid"].item()) / (ms / 1e3), 1), "unit": "tokens/s"}
+
+
 def time_adamw_arm(prob, args, bom_ms):
     """The AdamW arm on the same inputs (W warmup and K timed steps, like the BOM arm): step time, stage
     times, its update against the HBM roofline (28 bytes per parameter dense: read theta, m, v, g; write
@@ -644,6 +668,8 @@ def run_workload(w, args, cpu_budget, dev):
         "stages": per_stage,
         "roofline": roofline,
     }
+    if args.graph:
+        out["graph"] = time_graph(prob, args, t)
     if args.adamw:
         out["adamw"] = time_adamw_arm(prob, args, ms_per_step)
         out["adamw"]["bom_stages_ms"] = {s: round(stage_ms[s], 5) for s in stages}
@@ -691,6 +717,8 @@ def main():
     ap.add_argument("--adam-mini", action="store_true",
                     help="block-shared second moment (Adam-mini's update map with the BOM numerator) over a "
                          "transformer-shaped partition of the flat buffer, instead of the dense or factored one")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time one step captured in a HIP graph and replayed (no host launch overhead)")
     ap.add_argument("--no-adamw", dest="adamw", action="store_false",
                     help="skip the AdamW comparison arm (and the cost-model fit) after each workload's BOM steps")
     ap.add_argument("--z-route", action="store_true",

@@ -232,6 +232,95 @@ __global__ __launch_bounds__(256) void simt_dH_kernel(const T* __restrict__ R, i
         }
 }
 
+// ---- fp32 small heads in one launch -------------------------------------------------------------------
+// Both products of a small fp32 head (the tiny classifier) in one grid, each workgroup one 64 x 64 SIMT tile
+// of dW (blocks [0, tw)) or of dH (the rest) over the whole k range in chunks of 64, with G folded in as its operand is
+// staged: G_ij = [i in I] (alpha R_ij + cq_j), alpha = (1 - lambda) / N_t, cq_j = lambda q_hat_j / N_t,
+// formed here from the device words (no prep kernel); R may come from the logits (row_lse given). Block 0
+// also writes db = (1 - lambda) s + lambda q_hat.
+struct SmallF32Args {
+    const float* H; int64_t ldh;
+    const float* W; int64_t ldw;
+    const float* R; int64_t ldr;
+    const float* row_lse;   // logits input: R formed from Z and lse; null: R is stored
+    const int32_t* labels; int32_t ig;
+    const float* q_hat; const float* s; const int32_t* n_valid; float lambda;
+    int N, d, V;
+    float* dW; int64_t lddw; float beta;
+    float* db;
+    void* dH; int64_t lddh; int dh_bf16;
+    int tw_n, tw, th_n;
+};
+
+__global__ __launch_bounds__(256) void vjp_small_f32_kernel(SmallF32Args a) {
+    constexpr int FK = 64;   // k chunk: every load of a chunk (16 per operand per thread) is in flight at once
+    __shared__ float As[FK][SB + 4];
+    __shared__ float Bs[FK][SB + 4];
+    const bool is_dw = (int)blockIdx.x < a.tw;
+    const int id = is_dw ? blockIdx.x : blockIdx.x - a.tw;
+    const int tn_count = is_dw ? a.tw_n : a.th_n;
+    const int m0 = (id / tn_count) * SB, n0 = (id % tn_count) * SB;
+    const int M = is_dw ? a.d : a.N, Nn = is_dw ? a.V : a.d, K = is_dw ? a.N : a.V;
+    const int t = threadIdx.x, tx = t % 16, ty = t / 16;
+    const int nt = *a.n_valid;
+    const float alpha = nt > 0 ? (float)((1.0 - (double)a.lambda) / (double)nt) : 0.f;
+    const double cs = nt > 0 ? (double)a.lambda / (double)nt : 0.0;
+    // G element (row i, column j) of the output gradient
+    auto g_of = [&](int i, int j) {
+        bool bad = false;
+        const int y = a.labels[i];
+        if (!label_valid(y, a.V, a.ig, &bad)) return 0.f;
+        float r = a.R[(int64_t)i * a.ldr + j];
+        if (a.row_lse != nullptr) r = r_from_z(r, a.row_lse[i] * kLog2e, j == y);
+        return fmaf(alpha, r, (float)(cs * (double)a.q_hat[j]));
+    };
+    float acc[4][4] = {};
+    for (int k0 = 0; k0 < K; k0 += FK) {
+#pragma unroll
+        for (int e = 0; e < FK * SB / 256; ++e) {
+            const int idx = e * 256 + t;
+            if (is_dw) {   // A(m, k) = H[k][m], B(k, n) = G[k][n]
+                const int kk = idx / SB, cc = idx % SB, k = k0 + kk;
+                As[kk][cc] = (k < K && m0 + cc < M) ? a.H[(int64_t)k * a.ldh + m0 + cc] : 0.f;
+                Bs[kk][cc] = (k < K && n0 + cc < Nn) ? g_of(k, n0 + cc) : 0.f;
+            } else {       // A(i, k) = G[i][k], B(k, n) = W[n][k]
+                const int rr = idx / FK, kk = idx % FK, k = k0 + kk;
+                As[kk][rr] = (k < K && m0 + rr < M) ? g_of(m0 + rr, k) : 0.f;
+                Bs[kk][rr] = (k < K && n0 + rr < Nn) ? a.W[(int64_t)(n0 + rr) * a.ldw + k] : 0.f;
+            }
+        }
+        __syncthreads();
+#pragma unroll 16
+        for (int kk = 0; kk < FK; ++kk) {
+            float x[4], w[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) x[i] = As[kk][ty * 4 + i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) w[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(x[i], w[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+    for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) {
+            const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+            if (m >= M || n >= Nn) continue;
+            if (is_dw) {
+                float* p = a.dW + (int64_t)m * a.lddw + n;
+                *p = a.beta != 0.f ? acc[i][j] + a.beta * *p : acc[i][j];
+            } else if (a.dh_bf16) {
+                stf<uint16_t>(static_cast<uint16_t*>(a.dH), (int64_t)m * a.lddh + n, acc[i][j]);
+            } else {
+                stf<float>(static_cast<float*>(a.dH), (int64_t)m * a.lddh + n, acc[i][j]);
+            }
+        }
+    if (blockIdx.x == 0 && a.db != nullptr)
+        for (int j = t; j < a.V; j += 256) a.db[j] = nt > 0 ? (1.0f - a.lambda) * a.s[j] + a.lambda * a.q_hat[j] : 0.f;
+}
+
 // ---- MFMA bf16 path -----------------------------------------------------------------------------
 constexpr int MB = 128;          // output tile (both dims)
 constexpr int MK = 64;           // k tile
@@ -1946,6 +2035,20 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
     }
     if (L.part_off + partial_bytes(p, a.N, a.d, a.V) > L.total) return hipErrorInvalidValue;   // never taken
     if (!a.dH) p.h.kind = kSimt;   // no dH: no rank-1 vector for it
+
+    // small fp32 heads (at most 64 tiles of 64 x 64 in both products, k ranges up to 8192): one launch
+    if (a.dt == BOM_F32) {
+        const int64_t tw = cdiv(a.d, SB) * cdiv(a.V, SB), th = a.dH ? cdiv(a.N, SB) * cdiv(a.d, SB) : 0;
+        if (tw + th <= 64 && a.N <= 8192 && a.V <= 8192) {
+            SmallF32Args sa{static_cast<const float*>(a.H), a.ldh, static_cast<const float*>(a.W), a.ldw,
+                            static_cast<const float*>(a.R), a.ldr, zin ? a.row_lse : nullptr, a.labels, a.ignore_index,
+                            a.q_hat, a.s, a.n_valid, a.lambda, a.N, a.d, a.V, static_cast<float*>(a.dW), a.lddw,
+                            a.dW_beta, static_cast<float*>(a.db), a.dH, a.lddh, a.dh_dt == BOM_BF16 ? 1 : 0,
+                            (int)cdiv(a.V, SB), (int)tw, (int)cdiv(a.d, SB)};
+            hipLaunchKernelGGL(vjp_small_f32_kernel, dim3((unsigned)(tw + th)), dim3(256), 0, st, sa);
+            return hipGetLastError();
+        }
+    }
 
     // small products (both on the 128-tile kernel): one fused launch, nothing staged beforehand
     const PlanOverride& ov = plan_override();

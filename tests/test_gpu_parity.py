@@ -164,7 +164,8 @@ def test_ema_parity():
 VJP_CASES = [
     # name, N, d, V, dtype, ignore_frac
     ("f32_tiny", 256, 128, 10, "f32", 0.0),
-    ("f32_ragged", 130, 200, 520, "f32", 0.05),
+    ("f32_ragged", 130, 200, 520, "f32", 0.05),        # one launch (small fp32 heads)
+    ("f32_simt_route", 600, 300, 700, "f32", 0.05),    # more than 64 tiles: the SIMT kernels with k splits
     ("bf16_ragged", 300, 136, 1000, "bf16", 0.05),
     ("bf16_unaligned_simt", 200, 64, 333, "bf16", 0.05),
     ("bf16_vision_head", 1024, 768, 1000, "bf16", 0.0),

@@ -794,7 +794,8 @@ constexpr int kWideDH = 0, kWideDW = 1, kWideFWD = 2;
 // ZR: the operand that is R (dH's A, dW's B) holds the logits Z, and each copy is turned into R in
 // registers before its LDS write (z_chunk_to_r).
 template <int MODE, typename TO, int NW, bool ZR = false>
-__device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t (&lds)[2][2][WSE], float (&rv_s)[LB]) {
+__device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t (&lds)[2][2][WSE], float (&rv_s)[LB],
+                                          float2* zs = nullptr) {
     static_assert(NW == 4 || NW == 8, "four or eight waves");
     constexpr int KT = WKT;
     constexpr int WCOLS = NW == 4 ? 128 : 64;   // columns of a wave's part of the tile
@@ -863,9 +864,10 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         geo(KA, lda, M - m0, q, &voff_a[q], &kc_a[q], &ok_a[q]);
         geo(KB, ldb, Nn - n0, q, &voff_b[q], &kc_b[q], &ok_b[q]);
     }
-    // logits input: per copy slot of the R operand, c of its row and the label (dH: rows fixed per
-    // slot, labels as offsets from the chunk's k at write time; dW: rows change with the k tile, so both
-    // are loaded with each copy, the label as an offset from the chunk's first column)
+    // logits input: c of each row of the R operand and its label. dH: the tile's 256 rows are fixed, so
+    // (c, label) sit in LDS (zs) and each copy looks its row up at write time, the label as an offset
+    // from the chunk's k; dW: rows change with the k tile, so both are loaded into registers with each
+    // copy, the label as an offset from the chunk's first column
     constexpr bool ZA = ZR && MODE == kWideDH, ZB = ZR && MODE == kWideDW;
     float zrc[CPO];
     int zry[CPO], zcol[CPO];
@@ -875,13 +877,6 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         zry[q] = -1;
         zcol[q] = 0;
         const int chunk = (wave * CPO + q) * 64 + l;
-        if constexpr (ZA) {
-            const int i = m0 + chunk / 8;
-            if (i < M) {
-                zrc[q] = args.zc[i];
-                zry[q] = args.labels[i];
-            }
-        }
         if constexpr (ZB) zcol[q] = n0 + (((chunk % 32) ^ (((chunk / 32) & 3) << 2)) << 3);
     }
     // k-contiguous operands: one descriptor per workgroup over the tile's rows (exact extent)
@@ -939,7 +934,8 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
         if constexpr (ZA) {
             if (q < CPO) {
                 const int j0 = k0w + kc_a[q];
-                x = z_chunk_to_r(v, zrc[q], zry[q] - j0, ok_a[q] && j0 < ke);
+                const float2 zz = zs[((wave * CPO + q) * 64 + l) / 8];   // the copy's row: c and label
+                x = z_chunk_to_r(v, zz.x, __float_as_int(zz.y) - j0, ok_a[q] && j0 < ke);
             }
         }
         if constexpr (ZB) {
@@ -1020,6 +1016,13 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
     };
     u32x4_t rg[2 * CPO];
     bf16x8_t a0[4], b0[NJ], a1[4], b1[NJ];
+    if constexpr (ZA) {   // logits rows of the tile: c and label, held in LDS (registers are taken in full)
+        for (int t = threadIdx.x; t < LB; t += NW * kWave) {
+            const int i = m0 + t;
+            zs[t] = i < M ? make_float2(args.zc[i], __int_as_float(args.labels[i])) : make_float2(INFINITY, __int_as_float(-1));
+        }
+        __syncthreads();
+    }
     {
         const TileLoad t0 = tile_load(0), t1 = tile_load(1);
 #pragma unroll
@@ -1176,7 +1179,8 @@ template <bool IS_DW, typename TO, int NW, bool ZR = false>
 __global__ __launch_bounds__(NW * 64, 1) void lds256w_kernel(WideArgs a) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    wide_tile<IS_DW ? kWideDW : kWideDH, TO, NW, ZR>(a, blockIdx.x, lds, rv_s);
+    __shared__ float2 zs[ZR && !IS_DW ? LB : 1];
+    wide_tile<IS_DW ? kWideDW : kWideDH, TO, NW, ZR>(a, blockIdx.x, lds, rv_s, zs);
 }
 
 // The head forward Z = H W (+ b) in bf16 on the same tiles (fp32 accumulation, one rounding of Z).
@@ -1195,7 +1199,8 @@ template <typename TO, int NW, bool ZR = false>
 __global__ __launch_bounds__(NW * 64, 1) void lds256w_pair_kernel(WideArgs h, WideArgs w, int nh) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    if ((int)blockIdx.x < nh) wide_tile<kWideDH, TO, NW, ZR>(h, blockIdx.x, lds, rv_s);
+    __shared__ float2 zs[ZR ? LB : 1];
+    if ((int)blockIdx.x < nh) wide_tile<kWideDH, TO, NW, ZR>(h, blockIdx.x, lds, rv_s, zs);
     else wide_tile<kWideDW, float, NW, ZR>(w, (int)blockIdx.x - nh, lds, rv_s);
 }
 

@@ -36,6 +36,9 @@ RESIDUAL_CASES = [
     ("bf16_v70000_split2", 40, 70000, "bf16", "zipf", 0.05, 2, 1.28),
     ("bf16_v100008_split3", 24, 100008, "bf16", "zipf", 0.05, 2, 1.28),
     ("bf16_v128256_split4", 20, 128256, "bf16", "zipf", 0.05, 2, 1.28),
+    # 64 row groups of 4 parts: three or four rows per group (the next row is prefetched during a row)
+    ("bf16_v128256_split4_multirow", 200, 128256, "bf16", "zipf", 0.05, 3, 1.28),
+    ("bf16_v200000_split5", 12, 200000, "bf16", "zipf", 0.05, 1, 1.28),
     ("bf16_v330000_twopass", 8, 330000, "bf16", "zipf", 0.0, 1, 1.28),
     ("f32_v70003_twopass_scalar", 40, 70003, "f32", "zipf", 0.05, 2, 1.28),
     ("bf16_v4_n1", 1, 8, "bf16", "uniform", 0.0, 0, 1.0),

@@ -26,7 +26,9 @@ from test_gpu_parity import _compare_residual
 pytestmark = [pytest.mark.gpu, needs_gpu]
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-CASES = [("split3_v100008", 24, 100008), ("split4_v128256", 20, 128256)]
+# the multirow cases give each row group several rows (a workgroup prefetches the next row during one)
+CASES = [("split2_v70000_multirow", 300, 70000), ("split3_v100008", 24, 100008),
+         ("split4_v128256_multirow", 200, 128256)]
 
 CHILD = r"""
 import sys

@@ -793,7 +793,7 @@ constexpr int kWideDH = 0, kWideDW = 1, kWideFWD = 2;
 // so that one wave's copies and LDS reads overlap the other's MFMAs) each own 128 x 64.
 // ZR: the operand that is R (dH's A, dW's B) holds the logits Z, and each copy is turned into R in
 // registers before its LDS write (z_chunk_to_r).
-template <int MODE, typename TO, int NW, bool ZR = false>
+template <int MODE, typename TO, int NW, bool ZR = false, bool FS = false>
 __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t (&lds)[2][2][WSE], float (&rv_s)[LB],
                                           float2* zs = nullptr) {
     static_assert(NW == 4 || NW == 8, "four or eight waves");
@@ -1068,14 +1068,13 @@ __device__ __forceinline__ void wide_tile(const WideArgs& args, int id, uint16_t
     };
     if constexpr (MODE == kWideFWD) {
         const uint16_t* __restrict__ bias = args.bias;
-        if (args.stats == nullptr) {
+        if constexpr (!FS) {
             for_each_acc([&](int r, int c, int, float v) {
                 const int m = m0 + r, n = n0 + c;
                 if (m < M && n < Nn) stf<TO>(out, (int64_t)m * ldo + n, bias ? v + bf16_to_f32(bias[n]) : v);
             });
             return;
-        }
-        if constexpr (std::is_same<TO, uint16_t>::value) {
+        } else if constexpr (std::is_same<TO, uint16_t>::value) {
             // row statistics: the rounded tile goes to LDS (the operand stages are free after the k loop:
             // 256 rows of 512 bytes), then two threads per row store it with 16-byte writes and reduce
             // their 128 columns (maximum, first column reaching it, sum of exp(z - max)); the pair's
@@ -1183,12 +1182,14 @@ __global__ __launch_bounds__(NW * 64, 1) void lds256w_kernel(WideArgs a) {
     wide_tile<IS_DW ? kWideDW : kWideDH, TO, NW, ZR>(a, blockIdx.x, lds, rv_s, zs);
 }
 
-// The head forward Z = H W (+ b) in bf16 on the same tiles (fp32 accumulation, one rounding of Z).
-template <typename TO, int NW>
+// The head forward Z = H W (+ b) in bf16 on the same tiles (fp32 accumulation, one rounding of Z); FS:
+// with the per-tile row statistics in the epilogue (a kernel of its own: the statistics epilogue's
+// registers would otherwise constrain the plain forward's k loop).
+template <typename TO, int NW, bool FS = false>
 __global__ __launch_bounds__(NW * 64, 1) void lds256w_fwd_kernel(WideArgs a) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2][WSE];
     __shared__ float rv_s[LB];
-    wide_tile<kWideFWD, TO, NW>(a, blockIdx.x, lds, rv_s);
+    wide_tile<kWideFWD, TO, NW, false, FS>(a, blockIdx.x, lds, rv_s);
 }
 
 // Both products in one grid: blocks [0, nh) run dH's units (the long k ranges first), the rest dW's
@@ -2281,7 +2282,7 @@ hipError_t launch_head_forward_stats(const void* H, int64_t ldh, const void* W, 
     wa.labels = labels;
     wa.ignore_index = ignore_index;
     wa.row_target = row_target;
-    hipLaunchKernelGGL((lds256w_fwd_kernel<uint16_t, 8>), dim3((unsigned)(cdiv(NT, 8) * 8 * MT)), dim3(512), 0, st, wa);
+    hipLaunchKernelGGL((lds256w_fwd_kernel<uint16_t, 8, true>), dim3((unsigned)(cdiv(NT, 8) * 8 * MT)), dim3(512), 0, st, wa);
     return hipGetLastError();
 }
 

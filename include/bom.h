@@ -368,6 +368,8 @@ bom_status bom_head_forward_residual(const void* H, int64_t ldh, const void* W, 
  * not depend on them beyond rounding order):
  *   BOM_VJP_WAVES = "dH,dW,fwd,pair"  waves per workgroup (4 or 8) of the 256-tile products; default 8,8,8,8.
  *   BOM_VJP_PLAN  = "kw,sw,kh,sh"     force a head-VJP kernel kind and k split per product (A/B runs only).
+ *   BOM_VJP_XCD_BLOCK = 0             the plain XCD tile order of the 256-tile products instead of the
+ *                                      blocked one (4 outer x 8 inner tiles per XCD round; the same sums).
  *   BOM_RESIDUAL_SPIN = n             poll bound of the split-row residual exchange; negative: every part
  *                                      recomputes its partners' row records from Z (the fallback path).
  */

@@ -150,12 +150,13 @@ __global__ __launch_bounds__(THREADS) void residual_rows_kernel(
         const T* zr = Z + (int64_t)i * ldz;
         float x[NXF];
         uint32_t xw[NXW];
-        // Chunks 0..NCH-2 of every thread lie inside the row (NCH is the ceiling of the chunk count);
-        // only the last chunk needs a bounds check.
+        // A chunk whose columns can reach past the row's end is loaded with a bounds check (padding -inf):
+        // the last one, and the ones before it when NCH exceeds the row's chunk count (NCH comes from a
+        // fixed set of sizes). Uniform across the workgroup.
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const int col = (c * THREADS + tid) * VEC;
-            const bool last = c == NCH - 1;
+            const bool last = (c + 1) * THREADS * VEC > V;
             if constexpr (PACKED) {
                 const bool ok = !last || col < V;
                 const uint4 u = *reinterpret_cast<const uint4*>(zr + (ok ? col : V - VEC));

@@ -28,6 +28,10 @@ RESIDUAL_CASES = [
     ("tiny_f32_v10", 256, 10, "f32", "uniform", 0.0, 0, 0.23),
     ("bf16_v1000_ign", 300, 1000, "bf16", "uniform", 0.05, 4, 0.55),
     ("bf16_v1003_scalar", 77, 1003, "bf16", "zipf", 0.05, 2, 0.55),
+    # register rows with more chunks per thread than the row holds (a chunk count from the fixed set): 2050
+    # scalar columns at 512 threads need 5 chunks and run with 6, 10000 fp32 columns (float4) likewise
+    ("bf16_v2050_scalar_spare_chunk", 300, 2050, "bf16", "zipf", 0.05, 2, 0.55),
+    ("f32_v10000_spare_chunk", 64, 10000, "f32", "zipf", 0.05, 1, 0.55),
     ("f32_v4100_peaked", 129, 4100, "f32", "zipf", 0.05, 2, 11.0),
     ("bf16_v32000", 96, 32000, "bf16", "zipf", 0.05, 2, 0.55),
     ("bf16_v12000_multirow", 600, 12000, "bf16", "zipf", 0.05, 3, 0.55),
@@ -214,6 +218,37 @@ def test_head_vjp_parity(case):
     # invariant: rows of G sum to zero, so dW 1 vanishes up to the rounding of G
     gdw = to_f64(g["dW"])
     assert (np.abs(gdw.sum(1)) <= (tol if dtype == "bf16" else 1e-4) * np.abs(gdw).sum(1) + 1e-12).all()
+
+
+# d = 4096: 16 inner tiles per outer tile in both products, so their whole rounds run in the blocked XCD order
+# (4 outer x 8 inner tiles per XCD round). dW's 47 outer tiles (ragged last) all run in whole rounds: XCDs 0-6
+# own 6 of them (a group of 4, then one of 2) and XCD 7 owns 5 (4, then 1); dH runs 32 of its 41 outer tiles
+# (ragged last) in whole rounds and the rest with split k. Sampled dW columns and dH rows include the ragged
+# tiles and tiles of first and last groups.
+XCD_COLS = np.r_[0:64, 5880:5940, 11700:11760, 11940:12000]
+XCD_ROWS = np.r_[0:16, 5100:5120, 8180:8200, 10230:10248]
+
+
+def test_head_vjp_blocked_xcd_order():
+    N, d, V = 10248, 4096, 12000
+    log(f"[head_vjp blocked XCD order] N={N} d={d} V={V}")
+    Hh, Hd, Wh, Wd, Zh, Zd, y, q_prev, t = _vjp_inputs(N, d, V, "bf16", 0.05)
+    yd = torch.from_numpy(y).to(dev())
+    res = bom.bom_residual(Zd, yd)
+    q = torch.from_numpy(q_prev.copy()).to(dev())
+    qh = bom.bom_ema(q, res["s"], B1, t)
+    g = bom.bom_head_vjp(Hd, Wd, res["R"], yd, qh, res["n_valid"], s=res["s"], lam=LAM, want_db=True,
+                         dh_dtype=torch.float32)
+    torch.cuda.synchronize()
+    o = oracle.residual(Zh, y, want_R=False)
+    _, qho = oracle.ema(q_prev, o["s"], f32(B1), t)
+    dW = oracle.dW_cols(Hh, Zh, y, o["row_lse"], qho, o["n_valid"], LAM, cols=XCD_COLS)
+    dH = oracle.dH_rows(Wh, Zh, y, o["row_lse"], qho, o["n_valid"], LAM, rows=XCD_ROWS)
+    e_dw = rel_fro(to_f64(g["dW"])[:, XCD_COLS], dW)
+    e_dh = rel_fro(to_f64(g["dH"])[XCD_ROWS], dH)
+    log(f"    rel err dW={e_dw:.3e} dH={e_dh:.3e}")
+    assert e_dw <= 2e-2 and e_dh <= 2e-2
+    assert np.isfinite(to_f64(g["dW"])).all() and np.isfinite(to_f64(g["dH"])).all()
 
 
 # Padded leading dimensions (multiples of 8) with V not a multiple of 8: the padding holds large values

@@ -4,6 +4,8 @@ child process and checked against the oracle like the default-path parity cases.
 * BOM_VJP_WAVES = "4,4,4,4": the 256 x 256 tiles of dH, dW, the paired launch and the forward on four
   waves per workgroup (one per SIMD, each 128 x 128) instead of eight: whole rounds with leftover split-k
   tiles for dW and for dH, ragged tiles in m, n and k, the paired launch of both products, the forward.
+* BOM_VJP_XCD_BLOCK = "0": the plain XCD tile order (2 outer tiles x all 16 inner tiles per XCD round) at
+  d = 4096, where the default is the blocked order.
 * BOM_VJP_PLAN = "4,3,4,2": the 256-tile rank-1 kernel with k split three ways (dW) and two ways (dH) on
   every tile, followed by the split-k reduction with the rank-1 term.
 * BOM_VJP_PLAN = "1,0,1,0": the 128-tile kernels that fold the history into G while staging R (no
@@ -63,6 +65,8 @@ VARIANTS = [("BOM_VJP_WAVES", "4,4,4,4", c) for c in CASES] + [
     ("BOM_VJP_PLAN", "4,3,4,2", CASES[2]),
     ("BOM_VJP_PLAN", "1,0,1,0", CASES[2]),
     ("BOM_VJP_PLAN", "1,0,1,0", ("short_128", 640, 256, 3000, None, None)),
+    ("BOM_VJP_XCD_BLOCK", "0", ("d4096_plain_order", 10248, 4096, 12000, np.r_[0:64, 11940:12000],
+                                np.r_[0:16, 10230:10248])),
 ]
 
 

@@ -262,6 +262,10 @@ __global__ __launch_bounds__(256) void vjp_small_f32_kernel(SmallF32Args a) {
     const int m0 = (id / tn_count) * SB, n0 = (id % tn_count) * SB;
     const int M = is_dw ? a.d : a.N, Nn = is_dw ? a.V : a.d, K = is_dw ? a.N : a.V;
     const int t = threadIdx.x, tx = t % 16, ty = t / 16;
+    // a tile with at most 16 columns inside the output (the classifier's dW over 10 classes) maps its threads
+    // to 64 rows x 4 column groups, so no thread spends its products on columns past the output
+    const bool narrow = Nn - n0 <= 16;
+    const int nr = t / 4, nc = t % 4;
     const int nt = *a.n_valid;
     const float alpha = nt > 0 ? (float)((1.0 - (double)a.lambda) / (double)nt) : 0.f;
     const double cs = nt > 0 ? (double)a.lambda / (double)nt : 0.0;
@@ -327,23 +331,33 @@ __global__ __launch_bounds__(256) void vjp_small_f32_kernel(SmallF32Args a) {
         }
         if (k0 + FK < K) load_chunk(k0 + FK);
         __syncthreads();
-#pragma unroll 16
-        for (int kk = 0; kk < FK; ++kk) {
-            float x[4], w[4];
+        const int kmax = min(FK, K - k0);   // the chunk's k range (a short last chunk skips its padding)
+        if (narrow) {   // at most 16 columns: thread (row nr, column group nc) owns 1 x 4 outputs
+#pragma unroll 8
+            for (int kk = 0; kk < kmax; ++kk) {
+                const float x = As[kk][nr];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) x[i] = As[kk][ty * 4 + i];
+                for (int j = 0; j < 4; ++j) acc[0][j] = fmaf(x, Bs[kk][nc * 4 + j], acc[0][j]);
+            }
+        } else {
+#pragma unroll 8
+            for (int kk = 0; kk < kmax; ++kk) {
+                float x[4], w[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) w[j] = Bs[kk][tx * 4 + j];
+                for (int i = 0; i < 4; ++i) x[i] = As[kk][ty * 4 + i];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+                for (int j = 0; j < 4; ++j) w[j] = Bs[kk][tx * 4 + j];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(x[i], w[j], acc[i][j]);
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(x[i], w[j], acc[i][j]);
+            }
         }
         __syncthreads();
     }
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < (narrow ? 1 : 4); ++i)
         for (int j = 0; j < 4; ++j) {
-            const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+            const int m = narrow ? m0 + nr : m0 + ty * 4 + i, n = narrow ? n0 + nc * 4 + j : n0 + tx * 4 + j;
             if (m >= M || n >= Nn) continue;
             if (is_dw) {
                 float* p = a.dW + (int64_t)m * a.lddw + n;

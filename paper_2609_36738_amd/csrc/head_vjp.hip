@@ -1297,7 +1297,7 @@ __global__ __launch_bounds__(256) void splitk_rank1_kernel(const float* __restri
     stf<TO>(out, m * ldo + n, a);
 }
 
-// Rank-1 vectors. Blocks [0, nu): u_n = (lambda / N_t) sum_j W[n][j] q_hat_j, one workgroup per row of W.
+// Rank-1 vectors. Blocks [0, nu): u_n = (lambda / N_t) sum_j W[n][j] q_hat_j, one wave per row of W.
 // Blocks [nu, ...): partial column sums of H over rows in I, kHsRows rows by 512 columns per block
 // (wave w adds rows w, w + 4, ...; the four wave sums are added in wave order).
 constexpr int kHsRows = 128;
@@ -1309,26 +1309,24 @@ __global__ __launch_bounds__(256) void vjp_rank1_kernel(const uint16_t* __restri
                                                         float* __restrict__ hpart) {
     const int l = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     if ((int)blockIdx.x < nu) {
-        // one workgroup per row of W: thread t takes the 8-element chunks t, t + 256, ... of the row, the
-        // four wave sums are added in wave order
-        __shared__ float wsum[4];
-        const int n = blockIdx.x;
+        const int n = blockIdx.x * 4 + wave;
+        if (n >= d) return;
         const uint16_t* wr = W + (int64_t)n * ldw;
         float a0 = 0.f, a1 = 0.f;
-        int j = threadIdx.x * 8;
-        for (; j + 2048 < V; j += 4096) {
+        int j = l * 8;
+        for (; j + 512 < V; j += 1024) {
             const uint4 w0 = *reinterpret_cast<const uint4*>(wr + j);
-            const uint4 w1 = *reinterpret_cast<const uint4*>(wr + j + 2048);
+            const uint4 w1 = *reinterpret_cast<const uint4*>(wr + j + 512);
             const float4 q0 = *reinterpret_cast<const float4*>(q_hat + j);
             const float4 q1 = *reinterpret_cast<const float4*>(q_hat + j + 4);
-            const float4 q2 = *reinterpret_cast<const float4*>(q_hat + j + 2048);
-            const float4 q3 = *reinterpret_cast<const float4*>(q_hat + j + 2052);
+            const float4 q2 = *reinterpret_cast<const float4*>(q_hat + j + 512);
+            const float4 q3 = *reinterpret_cast<const float4*>(q_hat + j + 516);
             a0 += bf16_lo(w0.x) * q0.x + bf16_hi(w0.x) * q0.y + bf16_lo(w0.y) * q0.z + bf16_hi(w0.y) * q0.w +
                   bf16_lo(w0.z) * q1.x + bf16_hi(w0.z) * q1.y + bf16_lo(w0.w) * q1.z + bf16_hi(w0.w) * q1.w;
             a1 += bf16_lo(w1.x) * q2.x + bf16_hi(w1.x) * q2.y + bf16_lo(w1.y) * q2.z + bf16_hi(w1.y) * q2.w +
                   bf16_lo(w1.z) * q3.x + bf16_hi(w1.z) * q3.y + bf16_lo(w1.w) * q3.z + bf16_hi(w1.w) * q3.w;
         }
-        for (; j < V; j += 2048) {
+        for (; j < V; j += 512) {
             const uint4 w0 = *reinterpret_cast<const uint4*>(wr + j);
             const float4 q0 = *reinterpret_cast<const float4*>(q_hat + j);
             const float4 q1 = *reinterpret_cast<const float4*>(q_hat + j + 4);
@@ -1336,12 +1334,9 @@ __global__ __launch_bounds__(256) void vjp_rank1_kernel(const uint16_t* __restri
                   bf16_lo(w0.z) * q1.x + bf16_hi(w0.z) * q1.y + bf16_lo(w0.w) * q1.z + bf16_hi(w0.w) * q1.w;
         }
         const float sum = wave_sum(a0 + a1);
-        if (l == 0) wsum[wave] = sum;
-        __syncthreads();
-        if (threadIdx.x == 0) {
+        if (l == 0) {
             const int nt = *n_valid;
-            const float tot = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
-            u[n] = nt > 0 ? (float)((double)lambda / (double)nt) * tot : 0.f;
+            u[n] = nt > 0 ? (float)((double)lambda / (double)nt) * sum : 0.f;
         }
         return;
     }
@@ -2192,7 +2187,7 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
     const bool rw = p.w.kind == kRank1 && hist, rh = p.h.kind == kRank1 && hist;
     const int nrb = (int)cdiv(a.N, kHsRows);
     if (rw || rh) {
-        const int nu = rh ? a.d : 0;   // one workgroup per row of W
+        const int nu = rh ? (int)cdiv(a.d, 4) : 0;
         const int ns = rw ? (int)cdiv(a.d, 512) * nrb : 0;
         hipLaunchKernelGGL(vjp_rank1_kernel, dim3((unsigned)(nu + ns)), dim3(256), 0, st,
                            static_cast<const uint16_t*>(a.W), a.ldw, a.d, a.V, a.q_hat, a.n_valid, a.lambda, nu,

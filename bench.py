@@ -733,8 +733,8 @@ def main():
                          "reference for hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: the BOM hot path here is built and measured on a single MI355X "
-              "(sharding is a design note, not part of this build).", file=sys.stderr)
+        print("bench.py runs on one GPU only: the BOM hot path is implemented and measured on a single MI355X; "
+              "its sharding across GPUs is described, not implemented.", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)

@@ -13,7 +13,7 @@
  *   bom_residual  -> s, row statistics, R           (Algorithm 1: s_t)
  *   bom_ema       -> q (in place), q_hat            (Algorithm 1: q_t, q_hat_t)
  *   bom_head_vjp  -> dW, db, dH of the mixed loss   (Eq. 3 / Eq. 4, output head)
- *   bom_update    -> theta, v in place              (Sec. 3.4, Algorithm 1 last two lines)
+ *   bom_update    -> theta, v in place              (Sec. 3.4; Algorithm 1, the update)
  *
  * Conventions shared by every entry point:
  *   - Every array argument is caller-owned DEVICE memory, except the small
@@ -51,7 +51,7 @@ typedef enum {
     BOM_ERR_WORKSPACE = 5,   /* workspace missing or smaller than the query returns */
     BOM_ERR_ALIAS = 6,       /* buffers that must be distinct overlap */
     BOM_ERR_HIP = 7,         /* a HIP runtime call failed (detail in bom_last_error) */
-    BOM_ERR_UNSUPPORTED = 8  /* valid request this build does not implement */
+    BOM_ERR_UNSUPPORTED = 8  /* valid request this library does not implement */
 } bom_status;
 
 typedef enum { BOM_F32 = 0, BOM_BF16 = 1 } bom_dtype;
@@ -73,7 +73,7 @@ typedef enum { BOM_F32 = 0, BOM_BF16 = 1 } bom_dtype;
 #define BOM_MAX_SEGMENTS 16
 
 /* ------------------------------------------------------------------------------------------
- * bom_residual -- Algorithm 1, the line computing s_t; Sec. 3.2 (r = softmax(z) - onehot(y));
+ * bom_residual -- Algorithm 1 (the batch-mean residual s_t); Sec. 3.2 (r = softmax(z) - onehot(y));
  * token-level form: the appendix on language models (each valid target position is an
  * example; ignored targets are excluded from every mean).
  *
@@ -198,7 +198,7 @@ bom_status bom_head_vjp(const void* H, int64_t ldh, const void* W, int64_t ldw,
                         void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------------
- * bom_update -- Sec. 3.4 and the last two lines of Algorithm 1, over one flat fp32 buffer:
+ * bom_update -- Sec. 3.4 and Algorithm 1 (the second-moment and parameter updates), over one flat fp32 buffer:
  *   u' = u_scale * u                       (or, when h != NULL: u_scale * ((1-lambda) u + lambda h))
  *   v  = beta2 v + (1 - beta2) u'^2,  v_hat = v / (1 - beta2^t)
  *   theta = (1 - lr * omega) theta - lr * u' / (sqrt(v_hat) + eps)

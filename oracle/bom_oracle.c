@@ -58,7 +58,7 @@ static int orc_is_valid(int32_t y, int64_t V, int32_t ignore_index, int* bad) {
 }
 
 /*
- * Residual step: Algorithm 1, the line computing s_t; Sec. 3.2.
+ * Residual step: Algorithm 1 (the batch-mean residual s_t); Sec. 3.2.
  *   m_i = max_j z_ij, argmax_i = lowest j attaining it, l_i = sum_j exp(z_ij - m_i),
  *   lse_i = m_i + ln l_i; for i in I: r_ij = exp(z_ij - lse_i) - [j = y_i],
  *   CE_i = lse_i - z_{i,y_i}; s_j = (1/N_t) sum_{i in I} r_ij; loss = (1/N_t) sum_{i in I} CE_i.

@@ -56,7 +56,7 @@ const char* bom_status_string(bom_status s) {
         case BOM_ERR_WORKSPACE: return "BOM_ERR_WORKSPACE: workspace missing or too small";
         case BOM_ERR_ALIAS: return "BOM_ERR_ALIAS: buffers that must be distinct overlap";
         case BOM_ERR_HIP: return "BOM_ERR_HIP: a HIP runtime call failed";
-        case BOM_ERR_UNSUPPORTED: return "BOM_ERR_UNSUPPORTED: not implemented in this build";
+        case BOM_ERR_UNSUPPORTED: return "BOM_ERR_UNSUPPORTED: not implemented by this library";
     }
     return "unknown bom_status";
 }

@@ -1,5 +1,5 @@
 // bom_residual kernels: per-row softmax statistics, the residual rows R = softmax(Z) - onehot(y)
-// and the batch-mean residual s over the valid rows (Algorithm 1, the s_t line; Sec. 3.2; the
+// and the batch-mean residual s over the valid rows (Algorithm 1, s_t; Sec. 3.2; the
 // token-level appendix for ignored targets).
 //
 // Two paths, both deterministic (fixed reduction orders, no floating-point atomics):

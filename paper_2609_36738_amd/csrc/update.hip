@@ -1,5 +1,5 @@
 // bom_update kernels: second moment of the BOM numerator and the decoupled-decay update over one
-// flat fp32 parameter buffer (Sec. 3.4; the last two lines of Algorithm 1). There is no first
+// flat fp32 parameter buffer (Sec. 3.4; Algorithm 1, the second-moment and parameter updates). There is no first
 // moment: 20 bytes per parameter (read theta, v, u; write theta, v), 24 with a split numerator.
 //
 // Factored layout (a reading; the paper does not define one): the buffer is a row-major matrix of

@@ -496,11 +496,12 @@ def test_head_telemetry_parity(N, d, V, dtype, bias, moving):
 
 # ------------------------------------------------------------------------------------------------ forward
 # The head forward in bf16 (row a0: the logits of the large workloads): matrix-core tiles with ragged m, n
-# and k, the vision head with a bias, an LM shape checked on sampled rows, and an unaligned shape on the
+# and k, the vision head with a bias, an LM shape checked on sampled rows (16 row tiles: the blocked XCD
+# order, rows from four of them), and an unaligned shape on the
 # SIMT kernel. Z is rounded once to bf16: the bar is the bf16-input GEMM bound, and every element within two
 # bf16 steps plus the fp32 accumulation error of its row.
 @pytest.mark.parametrize("N,d,V,bias,rows", [(2056, 520, 6000, False, None), (1024, 768, 1000, True, None),
-                                            (4096, 768, 32000, False, np.r_[0:32, 4064:4096]),
+                                            (4096, 768, 32000, False, np.r_[0:32, 1000:1040, 2300:2330, 4064:4096]),
                                             (300, 100, 333, True, None)],
                          ids=["tiles_ragged", "vision_bias", "lm_sampled", "simt_unaligned"])
 def test_head_forward_bf16_parity(N, d, V, bias, rows):

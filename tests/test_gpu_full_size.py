@@ -6,7 +6,8 @@ a sample. Head VJP: 256 sampled dW columns (among them one in each leftover tile
 last column) and 256 dH rows (every 256-row tile); the oracle takes only those slices of Z, plus the
 dW row-sum invariant over the whole matrix. Update: sampled chunks (dense) or blocks (factored)
 whose inputs come from the seeded generator; the rest of the flat buffer holds other seeded values
-and is checked by a property (|step| <= lr at t = 1).
+and is checked by a property (|step| <= lr at t = 1). Forward: sampled rows against the oracle, and the fused
+forward + residual against the forward and bom_residual on the same logits.
 """
 import math
 
@@ -134,6 +135,51 @@ def test_head_vjp_full(lm):
     ra = out["dW"].double().abs().sum(1).cpu().numpy()
     assert (np.abs(rs) <= 2e-2 * ra + 1e-12).all()
     del Hd, Wd, out
+    torch.cuda.empty_cache()
+
+
+def test_head_forward_full(lm):
+    """The forward Z = H W at the full LM shapes (the blocked XCD order of its whole rounds at 32K, 1B and 8B):
+    48 rows spread over every band of row tiles against the oracle, each element within two bf16 steps plus
+    the fp32 accumulation error of its row; then the fused forward + residual on the same inputs: Z bitwise
+    equal to the plain forward, row statistics on the sampled rows against the oracle run on that Z, and s,
+    argmax, target, N_t and the flags against bom_residual on the same Z."""
+    w, y = lm["w"], lm["y"]
+    N, d, V = w.N, w.d, w.V
+    log(f"[full] {w.name}: head forward")
+    hb = synth.normal_bf16(N * d, synth.STREAM_H, 1.0)
+    wb = synth.normal_bf16(d * V, synth.STREAM_W, 0.02)
+    Hd, Wd = bf16_tensor(hb, (N, d)), bf16_tensor(wb, (d, V))
+    Hh = synth.bf16_to_f32(hb).reshape(N, d).astype(np.float64)
+    Wh = synth.bf16_to_f32(wb).reshape(d, V).astype(np.float64)
+    del hb, wb
+    Z = bom.bom_head_forward(Hd, Wd, None)
+    torch.cuda.synchronize()
+    rows = np.unique(np.r_[np.linspace(0, N - 1, 47).astype(int), [N - 1]])
+    Zg = to_f64(Z[torch.from_numpy(rows).to(dev())])
+    Zo = oracle.head_forward(Hh[rows], Wh, None)
+    e = rel_fro(Zg, Zo)
+    log(f"    forward rel err {e:.3e} on {rows.size} rows")
+    assert e <= 2e-2
+    acc = 1e-6 * (np.abs(Hh[rows]) @ np.abs(Wh))
+    assert (np.abs(Zg - Zo) <= 2 * 2.0 ** -8 * np.abs(Zo) + acc + 1e-30).all()
+    log(f"[full] {w.name}: fused forward + residual")
+    fr = bom.bom_head_forward_residual(Hd, Wd, lm["yd"])
+    torch.cuda.synchronize()
+    assert torch.equal(fr["Z"].view(torch.int16), Z.view(torch.int16)), "fused Z differs from bom_head_forward"
+    del Z
+    ref = bom.bom_residual(fr["Z"], lm["yd"])
+    torch.cuda.synchronize()
+    for k in ("row_argmax", "row_target", "n_valid", "flags"):
+        assert torch.equal(fr[k], ref[k]), k
+    es = rel_fro(to_f64(fr["s"]), to_f64(ref["s"]))
+    el = float((fr["row_lse"] - ref["row_lse"]).abs().max().item())
+    log(f"    fused vs bom_residual: s rel {es:.2e}, max |lse diff| {el:.2e}")
+    assert es <= 1e-5 and el <= 1e-5 * max(1.0, float(ref["row_lse"].abs().max().item()))
+    o = oracle.residual(to_f64(fr["Z"][torch.from_numpy(rows).to(dev())]), y[rows], want_R=False)
+    assert np.allclose(fr["row_lse"].cpu().numpy()[rows], o["row_lse"], rtol=1e-5, atol=1e-5)
+    assert np.array_equal(fr["row_argmax"].cpu().numpy()[rows], o["row_argmax"])
+    del fr, ref, Hd, Wd
     torch.cuda.empty_cache()
 
 

@@ -43,8 +43,24 @@ struct Fold {
 };
 
 struct VjpWs {
-    size_t cq_off, cqp_off, vmask_off, scal_off, zc_off, hpart_off, hsum_off, u_off, part_off, total;
+    size_t cq_off, cqp_off, vmask_off, scal_off, zc_off, hpart_off, hsum_off, u_off, upart_off, part_off, total;
 };
+
+// Rank-1 vector u = W q_hat is summed over column chunks (one wave per row of W and chunk at a time, four
+// 16-byte loads of W in flight per lane); the chunk sums are added in chunk order by the prep kernel. Rows
+// are cut into as many chunks as bring the work to about 4096 units (a short row count, as at d = 768, needs
+// several per row; d = 4096 rows need none), each a multiple of the 2048 columns a wave covers per
+// iteration, and kUWaves waves take the units in turn: 1024 or 4096 waves measured slower at the three LM
+// shapes (at d = 4096, 359 and 300 against 264 us).
+constexpr int kUWaves = 2048;
+inline int u_chunk_cols(int64_t d, int64_t V) {
+    const int64_t c = std::max<int64_t>(1, std::min<int64_t>((4096 + d - 1) / d, (V + 2047) / 2048));
+    return (int)(((V + c - 1) / c + 2047) / 2048 * 2048);
+}
+inline int u_chunks(int64_t d, int64_t V) {   // every chunk starts inside the row
+    const int64_t cw = u_chunk_cols(d, V);
+    return (int)((V + cw - 1) / cw);
+}
 
 // ---- residual rows from the logits ----------------------------------------------------------------
 // With the logits Z as input, the products take R = softmax(Z) - onehot(y) chunk by chunk as the operand
@@ -84,14 +100,28 @@ __global__ __launch_bounds__(256) void vjp_prep_kernel(const float* __restrict__
                                                        float* __restrict__ vmask, float* __restrict__ scal,
                                                        float* __restrict__ db, const float* __restrict__ hpart, int nrb,
                                                        int d, float* __restrict__ hsum, const float* __restrict__ row_lse,
-                                                       float* __restrict__ zc) {
+                                                       float* __restrict__ zc, const float* __restrict__ upart, int uch,
+                                                       float* __restrict__ u) {
     const int idx = blockIdx.x * 256 + threadIdx.x;
+    const int nt = *n_valid;
     if (hpart != nullptr && idx < d) {   // rank-1 form: hsum_m = sum of the row-block partials, in block order
         float a = 0.f;
-        for (int b = 0; b < nrb; ++b) a += hpart[(int64_t)b * d + idx];
+        int b = 0;
+        for (; b + 8 <= nrb; b += 8) {   // eight loads in flight, added in block order
+            float h[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) h[k] = hpart[(int64_t)(b + k) * d + idx];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) a += h[k];
+        }
+        for (; b < nrb; ++b) a += hpart[(int64_t)b * d + idx];
         hsum[idx] = a;
     }
-    const int nt = *n_valid;
+    if (upart != nullptr && idx < d) {   // u_n = (lambda / N_t) sum of the chunk sums, in chunk order
+        float a = 0.f;
+        for (int c = 0; c < uch; ++c) a += upart[(int64_t)c * d + idx];
+        u[idx] = nt > 0 ? (float)((double)lambda / (double)nt) * a : 0.f;
+    }
     const bool hist_only = !(lambda < 1.0f);
     if (idx < V) {
         cq[idx] = nt > 0 ? (float)((double)lambda * (double)q_hat[idx] / (double)nt) : 0.f;
@@ -1297,46 +1327,49 @@ __global__ __launch_bounds__(256) void splitk_rank1_kernel(const float* __restri
     stf<TO>(out, m * ldo + n, a);
 }
 
-// Rank-1 vectors. Blocks [0, nu): u_n = (lambda / N_t) sum_j W[n][j] q_hat_j, one wave per row of W.
-// Blocks [nu, ...): partial column sums of H over rows in I, kHsRows rows by 512 columns per block
-// (wave w adds rows w, w + 4, ...; the four wave sums are added in wave order).
+// Rank-1 vectors. Blocks [0, nu): chunk sums of W q_hat, one wave per (row n of W, chunk c of ucw columns),
+// four 16-byte loads of W (and the matching q_hat) in flight per lane: upart[c][n]. Blocks
+// [nu, ...): partial column sums of H over rows in I, kHsRows rows by 512 columns per block (wave w adds rows
+// w, w + 4, ...; the four wave sums are added in wave order).
 constexpr int kHsRows = 128;
 __global__ __launch_bounds__(256) void vjp_rank1_kernel(const uint16_t* __restrict__ W, int64_t ldw, int d, int V,
-                                                        const float* __restrict__ q_hat, const int32_t* __restrict__ n_valid,
-                                                        float lambda, int nu, const uint16_t* __restrict__ H,
-                                                        int64_t ldh, int N, const int32_t* __restrict__ labels,
-                                                        int32_t ignore_index, float* __restrict__ u,
-                                                        float* __restrict__ hpart) {
+                                                        const float* __restrict__ q_hat, int nu, int uch, int ucw,
+                                                        const uint16_t* __restrict__ H, int64_t ldh, int N,
+                                                        const int32_t* __restrict__ labels, int32_t ignore_index,
+                                                        float* __restrict__ upart, float* __restrict__ hpart) {
     const int l = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     if ((int)blockIdx.x < nu) {
-        const int n = blockIdx.x * 4 + wave;
-        if (n >= d) return;
-        const uint16_t* wr = W + (int64_t)n * ldw;
-        float a0 = 0.f, a1 = 0.f;
-        int j = l * 8;
-        for (; j + 512 < V; j += 1024) {
-            const uint4 w0 = *reinterpret_cast<const uint4*>(wr + j);
-            const uint4 w1 = *reinterpret_cast<const uint4*>(wr + j + 512);
-            const float4 q0 = *reinterpret_cast<const float4*>(q_hat + j);
-            const float4 q1 = *reinterpret_cast<const float4*>(q_hat + j + 4);
-            const float4 q2 = *reinterpret_cast<const float4*>(q_hat + j + 512);
-            const float4 q3 = *reinterpret_cast<const float4*>(q_hat + j + 516);
-            a0 += bf16_lo(w0.x) * q0.x + bf16_hi(w0.x) * q0.y + bf16_lo(w0.y) * q0.z + bf16_hi(w0.y) * q0.w +
-                  bf16_lo(w0.z) * q1.x + bf16_hi(w0.z) * q1.y + bf16_lo(w0.w) * q1.z + bf16_hi(w0.w) * q1.w;
-            a1 += bf16_lo(w1.x) * q2.x + bf16_hi(w1.x) * q2.y + bf16_lo(w1.y) * q2.z + bf16_hi(w1.y) * q2.w +
-                  bf16_lo(w1.z) * q3.x + bf16_hi(w1.z) * q3.y + bf16_lo(w1.w) * q3.z + bf16_hi(w1.w) * q3.w;
-        }
-        for (; j < V; j += 512) {
-            const uint4 w0 = *reinterpret_cast<const uint4*>(wr + j);
-            const float4 q0 = *reinterpret_cast<const float4*>(q_hat + j);
-            const float4 q1 = *reinterpret_cast<const float4*>(q_hat + j + 4);
-            a0 += bf16_lo(w0.x) * q0.x + bf16_hi(w0.x) * q0.y + bf16_lo(w0.y) * q0.z + bf16_hi(w0.y) * q0.w +
-                  bf16_lo(w0.z) * q1.x + bf16_hi(w0.z) * q1.y + bf16_lo(w0.w) * q1.z + bf16_hi(w0.w) * q1.w;
-        }
-        const float sum = wave_sum(a0 + a1);
-        if (l == 0) {
-            const int nt = *n_valid;
-            u[n] = nt > 0 ? (float)((double)lambda / (double)nt) * sum : 0.f;
+        // nu * 4 (at most kUWaves) waves take the d * uch units in turn
+        for (int unit = blockIdx.x * 4 + wave; unit < d * uch; unit += nu * 4) {
+            const int n = unit / uch, c = unit % uch;
+            const uint16_t* wr = W + (int64_t)n * ldw;
+            const int j1 = min(V, (c + 1) * ucw);   // V and the chunk bounds are multiples of 8
+            float acc[4] = {0.f, 0.f, 0.f, 0.f};
+            for (int j = c * ucw + l * 8; j < j1; j += 4 * 512) {
+                uint4 w[4];
+                float4 q[8];
+                // all loads unconditional (clamped to the chunk's last 8 columns, which exist) so that they are in
+                // flight together; the W of a clamped load is masked to zero
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int jj = min(j + k * 512, j1 - 8);
+                    w[k] = *reinterpret_cast<const uint4*>(wr + jj);
+                    q[2 * k] = *reinterpret_cast<const float4*>(q_hat + jj);
+                    q[2 * k + 1] = *reinterpret_cast<const float4*>(q_hat + jj + 4);
+                }
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t mk = lane_mask(j + k * 512 < j1);
+                    w[k] = make_uint4(w[k].x & mk, w[k].y & mk, w[k].z & mk, w[k].w & mk);
+                }
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    acc[k] += bf16_lo(w[k].x) * q[2 * k].x + bf16_hi(w[k].x) * q[2 * k].y + bf16_lo(w[k].y) * q[2 * k].z +
+                              bf16_hi(w[k].y) * q[2 * k].w + bf16_lo(w[k].z) * q[2 * k + 1].x + bf16_hi(w[k].z) * q[2 * k + 1].y +
+                              bf16_lo(w[k].w) * q[2 * k + 1].z + bf16_hi(w[k].w) * q[2 * k + 1].w;
+            }
+            const float sum = wave_sum((acc[0] + acc[1]) + (acc[2] + acc[3]));
+            if (l == 0) upart[(int64_t)c * d + n] = sum;
         }
         return;
     }
@@ -1357,8 +1390,11 @@ __global__ __launch_bounds__(256) void vjp_rank1_kernel(const uint16_t* __restri
         for (int e = 0; e < 8; ++e) {
             const int i = rbeg + wave + 4 * (e0 + e);
             const int ic = i < N ? i : N - 1;
-            bool bad = false;
-            mk[e] = (i < N && label_valid(labels[ic], V, ignore_index, &bad)) ? 1.f : 0.f;
+            // the label is loaded unconditionally (ic is clamped) and tested without short-circuit evaluation,
+            // so that no load moves under a branch and all of the group's loads are in flight together
+            const int32_t lab = labels[ic];
+            const bool ok = (i < N) & (lab != ignore_index) & (lab >= 0) & ((int64_t)lab < V);
+            mk[e] = ok ? 1.f : 0.f;
             h[e] = *reinterpret_cast<const uint4*>(H + (int64_t)ic * ldh + colc);
         }
 #pragma unroll
@@ -1949,7 +1985,8 @@ VjpWs vjp_ws(int64_t N, int64_t d, int64_t V, bom_dtype dt) {
     w.hpart_off = align256(w.zc_off + (size_t)N * 4);
     w.hsum_off = align256(w.hpart_off + (r1 ? (size_t)cdiv(N, kHsRows) * d * 4 : 0));
     w.u_off = align256(w.hsum_off + (r1 ? (size_t)d * 4 : 0));
-    w.part_off = align256(w.u_off + (r1 ? (size_t)d * 4 : 0));
+    w.upart_off = align256(w.u_off + (r1 ? (size_t)d * 4 : 0));
+    w.part_off = align256(w.upart_off + (r1 ? (size_t)u_chunks(d, V) * d * 4 : 0));
     size_t need = partial_bytes(p, N, d, V);
     // the same call may take the SIMT plan (misaligned operands)
     if (dt == BOM_BF16) need = std::max(need, partial_bytes(simt_plan(N, d, V), N, d, V));
@@ -2113,6 +2150,7 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
     float* hpart = reinterpret_cast<float*>(base + L.hpart_off);
     float* hsum = reinterpret_cast<float*>(base + L.hsum_off);
     float* u = reinterpret_cast<float*>(base + L.u_off);
+    float* upart = reinterpret_cast<float*>(base + L.upart_off);
     float* part = reinterpret_cast<float*>(base + L.part_off);
     float* zc = reinterpret_cast<float*>(base + L.zc_off);
     const bool zin = !a.is_residual;   // the R argument holds the logits Z
@@ -2187,12 +2225,13 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
     const bool hist = a.lambda != 0.f;
     const bool rw = p.w.kind == kRank1 && hist, rh = p.h.kind == kRank1 && hist;
     const int nrb = (int)cdiv(a.N, kHsRows);
+    const int uch = u_chunks(a.d, a.V), ucw = u_chunk_cols(a.d, a.V);
     if (rw || rh) {
-        const int nu = rh ? (int)cdiv(a.d, 4) : 0;
+        const int nu = rh ? (int)cdiv(std::min<int64_t>((int64_t)a.d * uch, kUWaves), 4) : 0;
         const int ns = rw ? (int)cdiv(a.d, 512) * nrb : 0;
         hipLaunchKernelGGL(vjp_rank1_kernel, dim3((unsigned)(nu + ns)), dim3(256), 0, st,
-                           static_cast<const uint16_t*>(a.W), a.ldw, a.d, a.V, a.q_hat, a.n_valid, a.lambda, nu,
-                           static_cast<const uint16_t*>(a.H), a.ldh, a.N, a.labels, a.ignore_index, u, hpart);
+                           static_cast<const uint16_t*>(a.W), a.ldw, a.d, a.V, a.q_hat, nu, uch, ucw,
+                           static_cast<const uint16_t*>(a.H), a.ldh, a.N, a.labels, a.ignore_index, upart, hpart);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -2200,7 +2239,7 @@ hipError_t launch_head_vjp_f32(const HeadVjpArgs& a, hipStream_t st) {
     if (nprep < a.d) nprep = a.d;
     hipLaunchKernelGGL(vjp_prep_kernel, dim3((nprep + 255) / 256), dim3(256), 0, st, a.q_hat, a.s, a.n_valid, a.lambda,
                        a.V, a.N, a.labels, a.ignore_index, cq, cqp, vmask, scal, static_cast<float*>(a.db),
-                       rw ? hpart : nullptr, nrb, a.d, hsum, zin ? a.row_lse : nullptr, zc);
+                       rw ? hpart : nullptr, nrb, a.d, hsum, zin ? a.row_lse : nullptr, zc, rh ? upart : nullptr, uch, u);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const Fold f{cq, vmask, scal, cqp, zin ? zc : nullptr, a.labels};

@@ -590,18 +590,17 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
     // then on part q is not waited for) or when spin_limit < 0
     auto fetch = [&](int i, int q, float* mq, float* lq, int* aq) {
         if (dead) return false;
+        // the three words are polled together (one round trip per poll when the record is there)
         unsigned long long v[3];
-        bool ok = true;
-        for (int f = 0; f < 3 && ok; ++f) {
-            ok = false;
-            for (int it = 0; spin_limit >= 0 && it <= spin_limit; ++it) {
-                v[f] = __hip_atomic_load(xword(i, q, f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if ((v[f] >> 32) == 1) {
-                    ok = true;
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(2);
+        bool ok = false;
+        for (int it = 0; spin_limit >= 0 && it <= spin_limit; ++it) {
+#pragma unroll
+            for (int f = 0; f < 3; ++f) v[f] = __hip_atomic_load(xword(i, q, f), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if ((v[0] >> 32) == 1 && (v[1] >> 32) == 1 && (v[2] >> 32) == 1) {
+                ok = true;
+                break;
             }
+            __builtin_amdgcn_s_sleep(2);
         }
         if (!ok) {
             dead = true;

@@ -99,6 +99,7 @@ constexpr int kOob = (int)0x80000000u;  // an offset past every range: the load 
 constexpr int kNonTemporal = 2;           // buffer access cache policy: nt (streamed data touched once)
 
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x4_t __attribute__((ext_vector_type(4)));   // buffer descriptor words for inline assembly
 
 // Raw buffer descriptor over [base, base + bytes): loads at offsets >= bytes return zeros and
 // stores there are dropped.

@@ -2,11 +2,13 @@
 // and the batch-mean residual s over the valid rows (Algorithm 1, s_t; Sec. 3.2; the
 // token-level appendix for ignored targets).
 //
-// Two paths, both deterministic (fixed reduction orders, no floating-point atomics):
+// Three paths, all deterministic (fixed reduction orders, no floating-point atomics):
 //  * single pass (V up to ~53k bf16 / ~26k fp32): one persistent workgroup per CU keeps a whole
-//    row in registers, reduces max / argmax / sum across the workgroup, writes R, and accumulates
-//    its rows' residuals per column in registers; Z is read from HBM exactly once.
-//  * two pass (larger V): a stats kernel (one wave per row, online max / sum / argmax) writes the
+//    row in registers or LDS, reduces max / argmax / sum across the workgroup, writes R, and
+//    accumulates its rows' residuals per column in registers; Z is read from HBM exactly once.
+//  * split rows (bf16 up to 524,288 columns): several workgroups share each row and exchange their
+//    per-part statistics; Z is still read once.
+//  * two pass (other shapes): a stats kernel (one wave per row, online max / sum / argmax) writes the
 //    row statistics, then a column-slab kernel re-reads Z, writes R and accumulates per-column
 //    partials for blocks of rows.
 // A finish step sums the per-workgroup partials in a fixed order into s, loss, N_t and flags.
@@ -28,8 +30,8 @@ constexpr int kStatsRowsPerWG = 4;    // two pass, stats: one wave per row, 4 wa
 constexpr int kColsThreads = 256;     // two pass, columns: threads per workgroup
 constexpr int kColsCPT = 8;           // two pass, columns: chunks per thread
 constexpr int kColsMaxRowBlock = 256; // two pass, columns: at most this many rows per partial-sum block
-constexpr int kSplitMaxParts = 8;     // split rows: at most this many workgroups share a row
-constexpr int kSplitMaxNch = 5;       // split rows: 1024 threads x 5 chunks x 8 = 40960 columns per part
+constexpr int kSplitMaxParts = 16;    // split rows: at most this many workgroups share a row
+constexpr int kSplitMaxNch = 4;       // split rows: 1024 threads x 4 chunks x 8 = 32768 columns per part
 
 // Rows per column-kernel workgroup: enough workgroups (about 1024) to fill the chip.
 int cols_row_block(int64_t N, int64_t V, int vec) {
@@ -46,12 +48,14 @@ struct Partials {
     int* wg_count;    // [nwg] valid rows
     int* wg_flags;    // [nwg] BOM_FLAG_LABEL_RANGE bits
     double* wg_loss;  // [nwg] sum of per-row cross-entropy
-    unsigned long long* xch;  // [N][kSplitMaxParts][3] split rows: per-part (max, sum, argmax) records
+    unsigned long long* xch;  // [N][S][3] split rows: per-part (max, sum, argmax) records
 };
 
 struct WsLayout {
     size_t part_off, count_off, flags_off, loss_off, xch_off, total;
 };
+
+bool plan_split(int V, int* S, int* W, int* nch);
 
 WsLayout ws_layout(int64_t N, int64_t V) {
     int64_t nwg1 = N < kSingleMaxWG ? N : kSingleMaxWG;
@@ -69,7 +73,9 @@ WsLayout ws_layout(int64_t N, int64_t V) {
     L.flags_off = align256(L.count_off + (size_t)nwg * sizeof(int));
     L.loss_off = align256(L.flags_off + (size_t)nwg * sizeof(int));
     L.xch_off = align256(L.loss_off + (size_t)nwg * sizeof(double));
-    L.total = align256(L.xch_off + (size_t)N * kSplitMaxParts * 3 * sizeof(unsigned long long));
+    int S = 0, W = 0, nch = 0;
+    const int64_t xparts = plan_split((int)V, &S, &W, &nch) ? S : 0;
+    L.total = align256(L.xch_off + (size_t)N * (size_t)xparts * 3 * sizeof(unsigned long long));
     return L;
 }
 
@@ -501,29 +507,35 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
 
 // ---------------------------------------------------------------------------------------------
 // Single pass, rows too wide for one workgroup (bf16): S workgroups share each row, part q owning
-// columns [q W, min(V, (q + 1) W)), and together stream Z once. Each part parks its slice in LDS
-// like residual_rows_lds_kernel, reduces its (max, sum of exp(z - max), first argmax) and publishes
-// them as three 64-bit words (validity marker in the high half, value in the low half; the area is
-// zeroed before the launch) with relaxed device-scope atomic stores; lane q of wave 0 then polls part
-// q's words with relaxed device-scope atomic loads, and every thread combines all S records in part
-// order, so every part derives the same lse. A poll is bounded: after spin_limit polls (or at once when
-// spin_limit < 0) the whole workgroup reduces the missing part's slice from Z itself with the same code
-// and operation order that part runs (so the record has the same bits as the one it would have
-// published) and stops waiting for that part, so the kernel finishes whatever the scheduling and its
-// results do not depend on it; the flags word then carries BOM_FLAG_RESIDUAL_RECOMPUTED. The part holding a row's label (part 0
-// for ignored rows) writes that row's outputs and loss term. Workgroup (g, q) writes columns of
-// partial row g; the S parts of group g together fill it. Its logit loads and residual stores carry the
-// non-temporal hint (128 K vocabulary: 1.80 -> 1.73 ms; the row-parked kernel of narrower rows ran 5 %
-// slower with it and keeps the default policy).
+// columns [q W, min(V, (q + 1) W)), and together stream Z once. A part's slice of a row goes straight
+// from memory into one of two LDS row buffers (buffer loads that write LDS: the slice holds no registers
+// on its way), the slice of the row after next is requested as soon as a row's residual is written, and
+// a single wait on the vector memory counter (which retires in issue order) tells a wave that its own
+// chunks of the next row have landed; each thread reads only the slots its own wave loaded, so no
+// barrier guards the buffers. Pass one keeps exp(z - m) of the thread's columns in registers (m: the
+// thread's maximum), so pass two scales them by exp(m - lse) instead of evaluating exp again. Each part
+// reduces its (max, sum of exp(z - max), first argmax) and publishes them as three 64-bit words
+// (validity marker in the high half, value in the low half; the area is zeroed before the launch) with
+// relaxed device-scope atomic stores; lane q of wave 0 then polls part q's words with relaxed
+// device-scope atomic loads, and every thread combines all S records in part order, so every part
+// derives the same lse. A poll is bounded: after spin_limit polls (or at once when spin_limit < 0) the
+// whole workgroup reduces the missing part's slice from Z itself with the same operations in the same
+// order that part runs (so the record has the same bits as the one it would have published) and stops
+// waiting for that part, so the kernel finishes whatever the scheduling and its results do not depend on
+// it; the flags word then carries BOM_FLAG_RESIDUAL_RECOMPUTED. The part holding a row's label (part 0
+// for ignored rows) writes that row's outputs and loss term. Workgroup (g, q) writes columns of partial
+// row g; the S parts of group g together fill it. Logit loads and residual stores carry the non-temporal
+// hint.
 template <int THREADS, int NCH>
 __global__ __launch_bounds__(THREADS) void residual_split_kernel(
     const uint16_t* __restrict__ Z, int64_t ldz, int N, int V, const int32_t* __restrict__ labels, int32_t ignore_index,
     float* __restrict__ row_lse, int32_t* __restrict__ row_argmax, float* __restrict__ row_target,
     uint16_t* __restrict__ R, int64_t ldr, int S, int W, int spin_limit, Partials ws) {
+    static_assert(NCH >= 2 && NCH <= kSplitMaxNch, "two LDS row buffers of NCH chunks per thread");
     constexpr int VEC = 8;
     constexpr int NW = THREADS / kWave;
     constexpr int VPT = NCH * VEC;
-    __shared__ uint4 slots[NCH * THREADS];
+    __shared__ uint4 slots[2][NCH * THREADS];
     __shared__ float sh_m[2][NW];
     __shared__ float sh_l[2][NW];
     __shared__ int sh_am;
@@ -552,40 +564,53 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
         x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z); x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
     };
     const int voff = tid * 16;
-    // the first chunk index of this wave's lanes whose chunks may lie past the row's end
+    // the first chunk index of this wave's lanes whose chunks may lie past the slice's end
     const int wave_last = (tid | (kWave - 1));
-    auto row_desc = [&](int i) { return make_desc(Z + (int64_t)i * ldz + c0, Vp * 2); };
-    auto load_chunk = [&](const __amdgpu_buffer_rsrc_t& d, int c) {
-        const u32x4_t w = __builtin_amdgcn_raw_buffer_load_b128(d, voff + c * THREADS * 16, 0, kNonTemporal);
-        return make_uint4(w[0], w[1], w[2], w[3]);
-    };
-    auto park = [&](int c, uint4 w) {
-        if ((c * THREADS + wave_last) * VEC >= Vp) {   // uniform per wave
-            const bool ok = ((c * THREADS + tid) * VEC) < Vp;
+    // chunk c of the thread with the columns past the end of a slice of nq columns read as -inf
+    auto pad = [&](int c, int nq, uint4 w) {
+        if ((c * THREADS + wave_last) * VEC >= nq) {   // uniform per wave
+            const bool ok = ((c * THREADS + tid) * VEC) < nq;
             const uint32_t mk = lane_mask(ok), fb = 0xFF80FF80u & ~mk;
             w = make_uint4((w.x & mk) | fb, (w.y & mk) | fb, (w.z & mk) | fb, (w.w & mk) | fb);
         }
-        slots[c * THREADS + tid] = w;
+        return w;
     };
-    uint4 nxt[NCH];
-    if (nr > 0) {
-        const auto d0 = row_desc(row_of(0));
+    // Row i's slice into LDS buffer buf: chunk c of the thread at slots[buf][c * THREADS + tid]. m0 holds the
+    // LDS address of the wave's 64 slots of the chunk (each lane's 16 bytes land at m0 + 16 lane) and is
+    // restored afterwards; one wait state separates the write of m0 from the load that reads it. Bytes past
+    // the slice's end read as zeros (the descriptor's range) and are padded as they are unpacked.
+    auto issue_row = [&](int buf, int i) {
+        const uint64_t pa = reinterpret_cast<uint64_t>(Z + (int64_t)i * ldz + c0);
+        const i32x4_t rs = {__builtin_amdgcn_readfirstlane((int)(uint32_t)pa),
+                            __builtin_amdgcn_readfirstlane((int)((uint32_t)(pa >> 32) & 0xFFFFu)),
+                            __builtin_amdgcn_readfirstlane(Vp * 2), kBufFlags};
+        const uint32_t lds0 = __builtin_amdgcn_readfirstlane(
+            (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)(&slots[buf][tid & ~(kWave - 1)]));
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(d0, c);
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) park(c, nxt[c]);
-        if (nr > 1) {
-            const auto d1 = row_desc(row_of(1));
-#pragma unroll
-            for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(d1, c);
+        for (int c = 0; c < NCH; ++c) {
+            int m0_saved;
+            asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                         "buffer_load_dwordx4 %2, %3, %4 offen nt lds\n\ts_mov_b32 m0, %0"
+                         : "=&s"(m0_saved)
+                         : "s"(lds0 + c * THREADS * 16), "v"(voff), "s"(rs), "s"(c * THREADS * 16)
+                         : "memory");
         }
-    }
+    };
+    // this wave's chunks of the row in the buffer about to be read have landed once at most `younger`
+    // vector memory operations issued after them remain
+    auto wait_landed = [](int younger) {
+        if (younger >= 2 * NCH) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * NCH) : "memory");
+        else if (younger >= NCH) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NCH) : "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    };
+    if (nr > 0) issue_row(0, row_of(0));
+    if (nr > 1) issue_row(1, row_of(1));
     if (tid == 0) {
         sh_am = INT_MAX;
         sh_fam = INT_MAX;
     }
     constexpr unsigned long long kValid = 1ull << 32;
-    auto xword = [&](int i, int q, int f) { return ws.xch + ((int64_t)i * kSplitMaxParts + q) * 3 + f; };
+    auto xword = [&](int i, int q, int f) { return ws.xch + ((int64_t)i * S + q) * 3 + f; };
     // wave 0, lane q: part q's record of row i from its words; false when the poll bound runs out (from
     // then on part q is not waited for) or when spin_limit < 0
     auto fetch = [&](int i, int q, float* mq, float* lq, int* aq) {
@@ -612,32 +637,66 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
         return true;
     };
     // The reduction of one part's slice, shared by a part's own pass and by the recomputation of a
-    // partner's record when that record does not arrive: the same operations in the same order give the
-    // partner's bits exactly (contraction off, explicit fma only), so every part derives the same lse
-    // whichever way it obtained a record. chunk_at(c) is this thread's chunk c, with columns past the
-    // slice's end read as -inf.
-    auto thread_stats = [&](auto&& chunk_at, float* m_out, float* l_out, int* cmax_out) {
+    // partner's record when that record does not arrive: the thread's maximum m over its columns (chunk
+    // maxima in chunk order; cmax = the chunk where it first appears), then l = the sum, in chunk order, of
+    // each chunk's pairwise sum of exp(z - m). Both callers run these same operations in the same order
+    // (contraction off, explicit fma only) on the same padded chunks, so a recomputed record has the
+    // partner's bits and every part derives the same lse whichever way it obtained a record.
+    auto chunk_max = [](const float* x) {
+        auto mx = [](float a, float b2) { return __builtin_elementwise_maximum(a, b2); };
+        return mx(mx(mx(x[0], x[1]), mx(x[2], x[3])), mx(mx(x[4], x[5]), mx(x[6], x[7])));
+    };
+    auto max_step = [](int c, float cm, float* m, int* cmax) {
+        if (c > 0 && cm > *m) *cmax = c;
+        *m = __builtin_elementwise_maximum(*m, cm);
+    };
+    // exp(z - m) of one chunk in place (m2 = m log2 e) and its pairwise sum
+    auto chunk_exp_sum = [](float* x, float m2) {
+#pragma clang fp contract(off)
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) x[k] = exp2_fast(fmaf(x[k], kLog2e, -m2));
+        return ((x[0] + x[1]) + (x[2] + x[3])) + ((x[4] + x[5]) + (x[6] + x[7]));
+    };
+    // this part's own slice from LDS buffer b; e receives exp(z - m) of every column the thread holds
+    auto own_stats = [&](int b, float* e, float* m_out, float* l_out, int* cmax_out) {
 #pragma clang fp contract(off)
         float m = -INFINITY, l = 0.f;
         int cmax = 0;
-        uint4 u_next = chunk_at(0);
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            const uint4 u = u_next;
-            if (c + 1 < NCH) u_next = chunk_at(c + 1);
-            float x[VEC];
-            unpack(u, x);
-            auto mx = [](float a, float b2) { return __builtin_elementwise_maximum(a, b2); };
-            const float cm = mx(mx(mx(x[0], x[1]), mx(x[2], x[3])), mx(mx(x[4], x[5]), mx(x[6], x[7])));
-            const float mn = mx(m, cm);
-            const float mn2 = mn * kLog2e;
-            float e[VEC];
+            unpack(pad(c, Vp, slots[b][c * THREADS + tid]), &e[c * VEC]);
+            max_step(c, chunk_max(&e[c * VEC]), &m, &cmax);
+        }
+        const float m2 = m * kLog2e;
 #pragma unroll
-            for (int k = 0; k < VEC; ++k) e[k] = exp2_fast(fmaf(x[k], kLog2e, -mn2));
-            const float cl = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
-            l = (c == 0 ? cl : fmaf(l, exp2_fast((m - mn) * kLog2e), cl));
-            if (c > 0 && cm > m) cmax = c;
-            m = mn;
+        for (int c = 0; c < NCH; ++c) {
+            const float cl = chunk_exp_sum(&e[c * VEC], m2);
+            l = c == 0 ? cl : l + cl;
+        }
+        *m_out = m;
+        *l_out = l;
+        *cmax_out = cmax;
+    };
+    // a partner's slice, chunk_at(c) loading this thread's padded chunk c of it (read once per sweep; the
+    // loops stay rolled, so that this rare path holds one chunk at a time and adds no register pressure to
+    // the rest of the kernel)
+    auto partner_stats = [&](auto&& chunk_at, float* m_out, float* l_out, int* cmax_out) {
+#pragma clang fp contract(off)
+        float m = -INFINITY, l = 0.f;
+        int cmax = 0;
+#pragma unroll 1
+        for (int c = 0; c < NCH; ++c) {
+            float x[VEC];
+            unpack(chunk_at(c), x);
+            max_step(c, chunk_max(x), &m, &cmax);
+        }
+        const float m2 = m * kLog2e;
+#pragma unroll 1
+        for (int c = 0; c < NCH; ++c) {
+            float x[VEC];
+            unpack(chunk_at(c), x);
+            const float cl = chunk_exp_sum(x, m2);
+            l = c == 0 ? cl : l + cl;
         }
         *m_out = m;
         *l_out = l;
@@ -696,16 +755,20 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
     for (int j = 0; j < nr; ++j) {
         const int i = row_of(j);
         const int b = j & 1;
-        // pass 1 (LDS): online (max, sum) of this part's slice, as in residual_rows_lds_kernel
+        // vector memory operations this wave issued after row j's loads: row j - 1's residual stores, then
+        // row j + 1's loads
+        wait_landed((j > 0 ? NCH : 0) + (j + 1 < nr ? NCH : 0));
+        // pass 1 (LDS): (max, sum of exp(z - max)) of this thread's columns; their exp(z - max) stay in e
+        float e[VPT];
         float m_thread, l;
         int cmax;
-        thread_stats([&](int c) { return slots[c * THREADS + tid]; }, &m_thread, &l, &cmax);
+        own_stats(b, e, &m_thread, &l, &cmax);
         wave_stats(m_thread, l, sh_m[b], sh_l[b]);
         __syncthreads();
         if (tid == 0 && j > 0 && prev_own) finish_row(row_of(j - 1), b ^ 1, prev_lse, prev_valid, prev_am);
         float mp, lp;
         group_stats(sh_m[b], sh_l[b], &mp, &lp);
-        if (m_thread == mp) first_max(slots[cmax * THREADS + tid], cmax, mp, &sh_am);
+        if (m_thread == mp) first_max(pad(cmax, Vp, slots[b][cmax * THREADS + tid]), cmax, mp, &sh_am);
         __syncthreads();
         // wave 0: lane 0 publishes this part's record; lane q < S fetches part q's (all in parallel)
         if (tid < kWave) {
@@ -729,27 +792,23 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
                 sh_rec_a[tid] = aq;
             }
             const unsigned long long miss = __ballot(tid < S && !have);
-            if (tid == 0) sh_miss = (int)(miss & 0xFFu);
+            if (tid == 0) sh_miss = (int)(miss & ((1u << kSplitMaxParts) - 1));
         }
         __syncthreads();
         // records that did not arrive: the whole workgroup reduces that part's slice from Z
-        if (sh_miss != 0) recomputed = true;
-        for (int miss = sh_miss; miss != 0; miss &= miss - 1) {
+        const int missing = sh_miss;
+        if (missing != 0) recomputed = true;
+        for (int miss = missing; miss != 0; miss &= miss - 1) {
             const int q = __builtin_ctz(miss);
             const int q0 = q * W, nq = min(W, V - q0);
             const auto dq = make_desc(Z + (int64_t)i * ldz + q0, nq * 2);
             auto chunk_q = [&](int c) {
-                uint4 w = load_chunk(dq, c);
-                if ((c * THREADS + wave_last) * VEC >= nq) {   // the same padding as park() gives its slots
-                    const bool ok = ((c * THREADS + tid) * VEC) < nq;
-                    const uint32_t mk = lane_mask(ok), fb = 0xFF80FF80u & ~mk;
-                    w = make_uint4((w.x & mk) | fb, (w.y & mk) | fb, (w.z & mk) | fb, (w.w & mk) | fb);
-                }
-                return w;
+                const u32x4_t w = __builtin_amdgcn_raw_buffer_load_b128(dq, voff + c * THREADS * 16, 0, kNonTemporal);
+                return pad(c, nq, make_uint4(w[0], w[1], w[2], w[3]));
             };
             float mt, lt, mq, lq;
             int cq;
-            thread_stats(chunk_q, &mt, &lt, &cq);
+            partner_stats(chunk_q, &mt, &lt, &cq);
             wave_stats(mt, lt, sh_fm, sh_fl);
             __syncthreads();
             group_stats(sh_fm, sh_fl, &mq, &lq);
@@ -763,6 +822,8 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
             }
             __syncthreads();
         }
+        // the recomputation reused the registers of e: rebuild it from the slots (the same values)
+        if (missing != 0) own_stats(b, e, &m_thread, &l, &cmax);
         // every thread combines the S records in part order (the same operations in every part)
         float M = -INFINITY, L = 0.f;
         int A = 0;
@@ -791,28 +852,26 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
         const bool own = valid ? (y / W == part) : (part == 0);
         if (own) bad |= rbad;
         const auto rdesc = make_desc(R ? R + (int64_t)i * ldr + c0 : nullptr, R ? Vp * 2 : 0);
-        const bool has_next = j + 1 < nr, has_next2 = j + 2 < nr;
-        const auto dn = row_desc(has_next2 ? row_of(j + 2) : i);
         const int yl = y - c0;
         const bool here = valid && yl >= 0 && yl < Vp;
         const int yv = yl / VEC;
         const int slot = (here && yv % THREADS == tid) ? (yv / THREADS) * VEC + (yl % VEC) : -1;
-        const float lse2 = lse * kLog2e;
+        // pass 2 (registers): p = exp(z - lse) = exp(z - m) exp(m - lse), one scale per thread
+        const float sc = exp2_fast(m_thread * kLog2e - lse * kLog2e);
+        if (slot >= 0) {
+            const uint32_t w = reinterpret_cast<const uint32_t*>(&slots[b][(slot / VEC) * THREADS + tid])[(slot % VEC) >> 1];
+            sh_zt[b] = (slot & 1) ? bf16_hi(w) : bf16_lo(w);
+        }
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             float p[VEC];
             if (valid) {
-                float x[VEC];
-                unpack(slots[c * THREADS + tid], x);
 #pragma unroll
-                for (int k = 0; k < VEC; ++k) p[k] = exp2_fast(fmaf(x[k], kLog2e, -lse2));
+                for (int k = 0; k < VEC; ++k) p[k] = e[c * VEC + k] * sc;
                 if (slot >= 0) {
 #pragma unroll
                     for (int k = 0; k < VEC; ++k)
-                        if (c * VEC + k == slot) {
-                            p[k] -= 1.0f;
-                            sh_zt[b] = x[k];
-                        }
+                        if (c * VEC + k == slot) p[k] -= 1.0f;
                 }
 #pragma unroll
                 for (int k = 0; k < VEC; ++k) acc[c * VEC + k] += p[k];
@@ -827,14 +886,8 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
             w[3] = pack_bf16x2(p[6], p[7]);
             __builtin_amdgcn_raw_buffer_store_b128(w, rdesc, voff + c * THREADS * 16, 0, kNonTemporal);
         }
-        if (has_next) {
-#pragma unroll
-            for (int c = 0; c < NCH; ++c) park(c, nxt[c]);
-            if (has_next2) {
-#pragma unroll
-                for (int c = 0; c < NCH; ++c) nxt[c] = load_chunk(dn, c);
-            }
-        }
+        // buffer b is free once this thread's reads of it are done (its own wave loaded every slot it reads)
+        if (j + 2 < nr) issue_row(b, row_of(j + 2));
         prev_lse = lse;
         prev_valid = valid;
         prev_own = own;
@@ -1242,14 +1295,12 @@ bool plan_single(int V, int VEC, int* threads, int* nch) {
     return false;
 }
 
-// Split-row plan for bf16 rows of 16-byte chunks that no single workgroup holds: S parts of at most four
-// chunks per thread at 1024 threads while eight parts cover the row (V up to 262,144), else of at most
-// kSplitMaxNch; part width W columns (a multiple of 8). The five-chunk instance spills registers: at
-// V = 100,008 four parts of four chunks take 866 us against 1094 us for three parts of five.
+// Split-row plan for bf16 rows of 16-byte chunks that no single workgroup holds: S parts (at most
+// kSplitMaxParts, so V up to 524,288) of at most kSplitMaxNch chunks per thread at 1024 threads; part
+// width W columns (a multiple of 8). Two LDS row buffers of four chunks fill 128 KB of the CU's LDS.
 bool plan_split(int V, int* S, int* W, int* nch) {
     const int slots = V / 8;
-    const int maxn = (slots + 1024 * 4 - 1) / (1024 * 4) > kSplitMaxParts ? kSplitMaxNch : 4;
-    int parts = (slots + 1024 * maxn - 1) / (1024 * maxn);
+    int parts = (slots + 1024 * kSplitMaxNch - 1) / (1024 * kSplitMaxNch);
     if (plan_override() == 6 && parts < 2 && slots > 512) parts = 2;
     if (parts < 2 || parts > kSplitMaxParts) return false;
     const int per = (slots + parts - 1) / parts;
@@ -1274,7 +1325,7 @@ hipError_t launch_split(const uint16_t* Z, int64_t ldz, int N, int V, const int3
                         int32_t* am, float* tg, uint16_t* R, int64_t ldr, Partials ws, int S, int W, int nch, int* nwg,
                         int* nparts, hipStream_t st) {
     const int G = N < kSingleMaxWG / S ? N : kSingleMaxWG / S;
-    const int64_t nx = (int64_t)N * kSplitMaxParts * 3;
+    const int64_t nx = (int64_t)N * S * 3;
     hipLaunchKernelGGL(zero_u64_kernel, dim3((unsigned)((nx + 255) / 256)), dim3(256), 0, st, ws.xch, nx);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -1286,7 +1337,6 @@ hipError_t launch_split(const uint16_t* Z, int64_t ldz, int N, int V, const int3
         case 2: BOM_SPLIT(2); break;
         case 3: BOM_SPLIT(3); break;
         case 4: BOM_SPLIT(4); break;
-        case 5: BOM_SPLIT(5); break;
         default: return hipErrorInvalidValue;
     }
 #undef BOM_SPLIT

@@ -37,7 +37,7 @@ RESIDUAL_CASES = [
     ("bf16_v12000_multirow", 600, 12000, "bf16", "zipf", 0.05, 3, 0.55),
     ("bf16_v50304_packed", 64, 50304, "bf16", "zipf", 0.05, 2, 0.91),
     ("bf16_v50304_multirow", 600, 50304, "bf16", "zipf", 0.05, 3, 0.91),
-    # split rows: parts of 1024 threads x 4 chunks (32,768 columns) while 8 parts cover the row, 5 chunks beyond
+    # split rows: parts of 1024 threads x 4 chunks (32,768 columns), up to 16 parts; wider rows take two passes
     ("bf16_v60000_split2", 40, 60000, "bf16", "zipf", 0.05, 2, 1.28),
     ("bf16_v70000_split3", 40, 70000, "bf16", "zipf", 0.05, 2, 1.28),
     ("bf16_v100008_split4", 24, 100008, "bf16", "zipf", 0.05, 2, 1.28),
@@ -45,8 +45,10 @@ RESIDUAL_CASES = [
     # 64 row groups of 4 parts: three or four rows per group (the next row is prefetched during a row)
     ("bf16_v128256_split4_multirow", 200, 128256, "bf16", "zipf", 0.05, 3, 1.28),
     ("bf16_v200000_split7", 12, 200000, "bf16", "zipf", 0.05, 1, 1.28),
-    ("bf16_v300000_split8_five_chunks", 8, 300000, "bf16", "zipf", 0.0, 1, 1.28),
-    ("bf16_v330000_twopass", 8, 330000, "bf16", "zipf", 0.0, 1, 1.28),
+    ("bf16_v300000_split10", 8, 300000, "bf16", "zipf", 0.0, 1, 1.28),
+    ("bf16_v330000_split11", 8, 330000, "bf16", "zipf", 0.0, 1, 1.28),
+    ("bf16_v520000_split16", 6, 520000, "bf16", "zipf", 0.0, 1, 1.28),
+    ("bf16_v530000_twopass", 4, 530000, "bf16", "zipf", 0.0, 1, 1.28),
     ("f32_v70003_twopass_scalar", 40, 70003, "f32", "zipf", 0.05, 2, 1.28),
     ("bf16_v4_n1", 1, 8, "bf16", "uniform", 0.0, 0, 1.0),
 ]

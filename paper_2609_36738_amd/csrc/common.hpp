@@ -80,6 +80,40 @@ __device__ __forceinline__ int wave_or(int v) {
     return v;
 }
 
+// ---- reductions with DPP lane permutes (VALU only: no LDS round trip per step) -------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+// Every lane of each 16-lane row ends with the row's maximum (sum): partners at xor 1 and xor 2 (quad
+// permutes 0xB1, 0x4E), then the other quad of each eight (half mirror, 0x141) and the other eight of
+// the sixteen (mirror, 0x140). Each step combines two lanes that hold the same partial in either
+// order, so all lanes of a row end with the same bits.
+__device__ __forceinline__ float row16_max(float v) {
+    v = fmaxf(v, dpp_f32<0xB1>(v));
+    v = fmaxf(v, dpp_f32<0x4E>(v));
+    v = fmaxf(v, dpp_f32<0x141>(v));
+    return fmaxf(v, dpp_f32<0x140>(v));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+    v += dpp_f32<0xB1>(v);
+    v += dpp_f32<0x4E>(v);
+    v += dpp_f32<0x141>(v);
+    return v + dpp_f32<0x140>(v);
+}
+__device__ __forceinline__ float lane_f32(float v, int lane) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+// wave-uniform maximum and sum: the four row results combined as ((r0, r1), (r2, r3))
+__device__ __forceinline__ float wave_max_dpp(float v) {
+    v = row16_max(v);
+    return fmaxf(fmaxf(lane_f32(v, 0), lane_f32(v, 16)), fmaxf(lane_f32(v, 32), lane_f32(v, 48)));
+}
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+    v = row16_sum(v);
+    return (lane_f32(v, 0) + lane_f32(v, 16)) + (lane_f32(v, 32) + lane_f32(v, 48));
+}
+
 // exp and log with the hardware base-2 units: exp(x) = 2^(x log2 e).
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;

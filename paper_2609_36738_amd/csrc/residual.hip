@@ -702,33 +702,28 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
         *l_out = l;
         *cmax_out = cmax;
     };
-    // wave reduction of (m, l) into shm[wave], shl[wave] (the caller then passes a barrier)
+    // wave reduction of (m, l) into shm[wave], shl[wave] (the caller then passes a barrier); DPP lane
+    // permutes, so the chain of steps makes no LDS round trips
     auto wave_stats = [&](float m, float l, float* shm, float* shl) {
 #pragma clang fp contract(off)
-        float mw = m;
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o, kWave));
-        float lw = l * exp2_fast((m - mw) * kLog2e);
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) lw += __shfl_xor(lw, o, kWave);
+        const float mw = wave_max_dpp(m);
+        const float lw = wave_sum_dpp(l * exp2_fast((m - mw) * kLog2e));
         if ((tid & (kWave - 1)) == 0) {
             shm[tid / kWave] = mw;
             shl[tid / kWave] = lw;
         }
     };
-    // the workgroup's (max, sum) from the per-wave values (uniform)
+    // the workgroup's (max, sum) from the per-wave values (uniform): lanes 0 .. NW - 1 of every wave hold
+    // them, so one 16-lane row reduces them
+    static_assert(NW <= 16, "the per-wave values fit one 16-lane row");
     auto group_stats = [&](const float* shm, const float* shl, float* mp, float* lp) {
 #pragma clang fp contract(off)
         const int lane = tid & (kWave - 1);
         const float mg = lane < NW ? shm[lane] : -INFINITY;
-        float mm = mg;
-#pragma unroll
-        for (int o = NW / 2; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o, kWave));
-        float lg = lane < NW ? shl[lane] * exp2_fast((mg - mm) * kLog2e) : 0.f;
-#pragma unroll
-        for (int o = NW / 2; o > 0; o >>= 1) lg += __shfl_xor(lg, o, kWave);
-        *mp = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(mm)));
-        *lp = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lg)));
+        const float mm = lane_f32(row16_max(mg), 0);
+        const float lg = lane < NW ? shl[lane] * exp2_fast((mg - mm) * kLog2e) : 0.f;
+        *mp = mm;
+        *lp = lane_f32(row16_sum(lg), 0);
     };
     // first column of chunk cmax holding the maximum mp (the lowest one over the workgroup, by atomicMin)
     auto first_max = [&](const uint4& w, int cmax, float mp, int* sh) {
@@ -1305,6 +1300,9 @@ bool plan_split(int V, int* S, int* W, int* nch) {
     if (parts < 2 || parts > kSplitMaxParts) return false;
     const int per = (slots + parts - 1) / parts;
     if ((parts - 1) * per >= slots) return false;   // every part holds columns
+    // every thread holds columns of every part (a thread with padding only would turn its sum into NaN);
+    // the automatic plan always gives a part more than 2048 chunks, only the override can give fewer
+    if (slots - (parts - 1) * per <= 1024) return false;
     *S = parts;
     *W = per * 8;
     *nch = (per + 1023) / 1024 < 2 ? 2 : (per + 1023) / 1024;

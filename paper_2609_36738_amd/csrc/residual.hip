@@ -81,7 +81,7 @@ WsLayout ws_layout(int64_t N, int64_t V) {
 
 template <int NW>
 __device__ __forceinline__ float block_max(float v, float* sh) {
-    v = wave_max(v);
+    v = wave_max_dpp(v);
     if ((threadIdx.x & (kWave - 1)) == 0) sh[threadIdx.x / kWave] = v;
     __syncthreads();
     float r = sh[0];
@@ -91,7 +91,7 @@ __device__ __forceinline__ float block_max(float v, float* sh) {
 }
 template <int NW>
 __device__ __forceinline__ float block_sum(float v, float* sh) {
-    v = wave_sum(v);
+    v = wave_sum_dpp(v);
     if ((threadIdx.x & (kWave - 1)) == 0) sh[threadIdx.x / kWave] = v;
     __syncthreads();
     float r = sh[0];
@@ -101,7 +101,7 @@ __device__ __forceinline__ float block_sum(float v, float* sh) {
 }
 template <int NW>
 __device__ __forceinline__ int block_min(int v, int* sh) {
-    v = wave_min(v);
+    v = wave_min_dpp(v);
     if ((threadIdx.x & (kWave - 1)) == 0) sh[threadIdx.x / kWave] = v;
     __syncthreads();
     int r = sh[0];
@@ -399,32 +399,25 @@ __global__ __launch_bounds__(THREADS) void residual_rows_lds_kernel(
             m = mn;
         }
         const float m_thread = m;
-        // wave: the maximum, then the lanes' sums rescaled to it
-        float mw = m;
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) mw = fmaxf(mw, __shfl_xor(mw, o, kWave));
-        float lw = l * exp2_fast((m - mw) * kLog2e);
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) lw += __shfl_xor(lw, o, kWave);
+        // wave: the maximum, then the lanes' sums rescaled to it (DPP lane permutes)
+        const float mw = wave_max_dpp(m);
+        const float lw = wave_sum_dpp(l * exp2_fast((m - mw) * kLog2e));
         if ((tid & (kWave - 1)) == 0) {
             sh_m[b][tid / kWave] = mw;
             sh_l[b][tid / kWave] = lw;
         }
         __syncthreads();
         if (tid == 0 && j > 0) finish_row(row_of(j - 1), b ^ 1, prev_lse, prev_valid);
-        // workgroup: the same over the NW wave pairs, lane w of every wave holding pair w; lane 0's
-        // result is broadcast
+        // workgroup: the same over the NW wave pairs, lane w of every wave holding pair w (one 16-lane
+        // row reduces them); lane 0's result is broadcast
+        static_assert(NW <= 16, "the per-wave values fit one 16-lane row");
         {
             const int lane = tid & (kWave - 1);
             const float mg = lane < NW ? sh_m[b][lane] : -INFINITY;
-            float mm = mg;
-#pragma unroll
-            for (int o = NW / 2; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o, kWave));
-            float lg = lane < NW ? sh_l[b][lane] * exp2_fast((mg - mm) * kLog2e) : 0.f;
-#pragma unroll
-            for (int o = NW / 2; o > 0; o >>= 1) lg += __shfl_xor(lg, o, kWave);
-            m = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(mm)));
-            l = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lg)));
+            const float mm = lane_f32(row16_max(mg), 0);
+            const float lg = lane < NW ? sh_l[b][lane] * exp2_fast((mg - mm) * kLog2e) : 0.f;
+            m = mm;
+            l = lane_f32(row16_sum(lg), 0);
         }
         // argmax: the first column holding the row maximum lies in the first chunk where some
         // thread holding that maximum reached it; those threads search that chunk

@@ -48,6 +48,8 @@ RESIDUAL_CASES = [
     ("bf16_v300000_split10", 8, 300000, "bf16", "zipf", 0.0, 1, 1.28),
     ("bf16_v330000_split11", 8, 330000, "bf16", "zipf", 0.0, 1, 1.28),
     ("bf16_v520000_split16", 6, 520000, "bf16", "zipf", 0.0, 1, 1.28),
+    # 16 row groups of 16 parts with two or three rows each: the next rows' slices land in the LDS buffers
+    ("bf16_v520000_split16_multirow", 40, 520000, "bf16", "zipf", 0.05, 2, 1.28),
     ("bf16_v530000_twopass", 4, 530000, "bf16", "zipf", 0.0, 1, 1.28),
     ("f32_v70003_twopass_scalar", 40, 70003, "f32", "zipf", 0.05, 2, 1.28),
     ("bf16_v4_n1", 1, 8, "bf16", "uniform", 0.0, 0, 1.0),

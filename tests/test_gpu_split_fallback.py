@@ -28,7 +28,8 @@ pytestmark = [pytest.mark.gpu, needs_gpu]
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 # the multirow cases give each row group several rows (a workgroup prefetches the next row during one)
 CASES = [("split3_v70000_multirow", 300, 70000), ("split4_v100008", 24, 100008),
-         ("split4_v128256_multirow", 200, 128256), ("split10_v300000", 8, 300000), ("split16_v520000", 6, 520000)]
+         ("split4_v128256_multirow", 200, 128256), ("split10_v300000", 8, 300000), ("split16_v520000", 6, 520000),
+         ("split16_v520000_multirow", 40, 520000)]
 
 CHILD = r"""
 import sys

@@ -570,8 +570,10 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
     };
     // Row i's slice into LDS buffer buf: chunk c of the thread at slots[buf][c * THREADS + tid]. m0 holds the
     // LDS address of the wave's 64 slots of the chunk (each lane's 16 bytes land at m0 + 16 lane) and is
-    // restored afterwards; one wait state separates the write of m0 from the load that reads it. Bytes past
-    // the slice's end read as zeros (the descriptor's range) and are padded as they are unpacked.
+    // restored afterwards; one wait state separates the write of m0 from the load that reads it. The whole
+    // byte offset goes in the VGPR operand (the scalar offset is outside the descriptor's range check), so
+    // bytes past the slice's end read as zeros and nothing past it is touched; they are padded as they are
+    // unpacked.
     auto issue_row = [&](int buf, int i) {
         const uint64_t pa = reinterpret_cast<uint64_t>(Z + (int64_t)i * ldz + c0);
         const i32x4_t rs = {__builtin_amdgcn_readfirstlane((int)(uint32_t)pa),
@@ -583,9 +585,9 @@ __global__ __launch_bounds__(THREADS) void residual_split_kernel(
         for (int c = 0; c < NCH; ++c) {
             int m0_saved;
             asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
-                         "buffer_load_dwordx4 %2, %3, %4 offen nt lds\n\ts_mov_b32 m0, %0"
+                         "buffer_load_dwordx4 %2, %3, 0 offen nt lds\n\ts_mov_b32 m0, %0"
                          : "=&s"(m0_saved)
-                         : "s"(lds0 + c * THREADS * 16), "v"(voff), "s"(rs), "s"(c * THREADS * 16)
+                         : "s"(lds0 + c * THREADS * 16), "v"(voff + c * THREADS * 16), "s"(rs)
                          : "memory");
         }
     };

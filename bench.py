@@ -527,8 +527,8 @@ def cpu_baseline(w, budget_s: float):
     """The fp64 oracle (as it stands) timed on the host on a bounded sample of the same workload,
     scaled to the whole step. Starting from a small probe, the sample of each part (residual rows,
     head-product columns and rows, update parameters) grows until that part takes about a third of
-    `budget_s` or covers the whole workload; a sample that is the whole step is repeated until half
-    the budget is used. The last sample is the one reported."""
+    `budget_s`, covers the whole workload or reaches its host-memory bound; the final sample is then
+    repeated until two thirds of the budget is used, and the mean over the repetitions is reported."""
     N, d, V, P = w.N, w.d, w.V, w.P
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     max_rows = max(16, min(N, int(4e7 // V), int(4e7 // d)))     # bounded host memory (fp64 copies)
@@ -559,7 +559,7 @@ def cpu_baseline(w, budget_s: float):
         spent += sum(raw.values())
     whole = rows == N and ncols == V and nrows_dh == N and npar == P
     reps, t_sample, acc = 1, sum(raw.values()), dict(full)
-    while whole and t_sample < 0.5 * budget_s and reps < 200:
+    while t_sample < budget_s * 2.0 / 3.0 and reps < 200:
         raw, full, npar = _oracle_sample(w, rows, ncols, nrows_dh, npar)
         t_sample += sum(raw.values())
         reps += 1

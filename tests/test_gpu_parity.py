@@ -147,17 +147,22 @@ def test_residual_all_ignored_is_empty():
     assert out["loss"].item() == 0 and (out["s"] == 0).all() and (out["R"].float() == 0).all()
 
 
-def test_residual_strided_rows():
-    log("[residual] strided Z and R views")
-    Zh, Zd = gen_matrix(64, 1040, synth.STREAM_Z, 0.5, "bf16")
-    y = gen_labels(64, 1000, "zipf")
-    Zv = Zd[:, :1000]
-    Rbuf = torch.full((64, 1024), 7.0, dtype=torch.bfloat16, device=dev())
-    out = _run_residual(Zv, torch.from_numpy(y).to(dev()), R=Rbuf[:, :1000])
-    orc = oracle.residual(Zh[:, :1000], y)
-    out["R"] = Rbuf[:, :1000]
-    _compare_residual("strided", np.ascontiguousarray(Zh[:, :1000]), y, out, orc, "bf16")
-    assert (Rbuf[:, 1000:].float() == 7.0).all()
+# Z and R as views of wider buffers (leading dimensions past V) on each single-pass route: register rows,
+# LDS-parked rows and split rows (four parts, several rows per row group); R's extra columns stay untouched.
+@pytest.mark.parametrize("N,V,ldz,ldr,std", [(64, 1000, 1040, 1024, 0.5), (96, 50304, 50368, 50320, 0.91),
+                                              (200, 128256, 128320, 128264, 1.28)],
+                         ids=["register_rows", "lds_rows", "split_rows"])
+def test_residual_strided_rows(N, V, ldz, ldr, std):
+    log(f"[residual] strided Z and R views N={N} V={V} ldz={ldz} ldr={ldr}")
+    Zh, Zd = gen_matrix(N, ldz, synth.STREAM_Z, std, "bf16")
+    y = gen_labels(N, V, "zipf")
+    Zv = Zd[:, :V]
+    Rbuf = torch.full((N, ldr), 7.0, dtype=torch.bfloat16, device=dev())
+    out = _run_residual(Zv, torch.from_numpy(y).to(dev()), R=Rbuf[:, :V])
+    orc = oracle.residual(Zh[:, :V], y)
+    out["R"] = Rbuf[:, :V]
+    _compare_residual("strided", np.ascontiguousarray(Zh[:, :V]), y, out, orc, "bf16")
+    assert (Rbuf[:, V:].float() == 7.0).all()
 
 
 # ------------------------------------------------------------------------------------------------ EMA
